@@ -1,0 +1,268 @@
+"""CPU oracle for the rotated, key-centered INT2 KV cache and its decode attention.
+
+TEST INFRASTRUCTURE ONLY. Nothing in the product path imports, calls or links
+this module: only the tests, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it. It shares no code with the HIP
+library; the only common inputs are the seeded arrays drawn by
+``paper_2608_02691_amd.workloads`` (which holds none of the method's arithmetic).
+
+It is the paper's definitions written out plainly, in fp64 numpy, except for the
+quantizer, whose fp32/fp16 rounding sequence is fixed below so that its codes,
+scales and zeros are reproducible bit for bit:
+
+* attention, eq:fp_attention / eq:head_output (Sec. 3):
+    a_s = <q, k_s>/sqrt(d),  p = softmax_s(a),  o = sum_s p_s v_s,
+  with query head j reading KV head h(j) = floor(j / G_q) under GQA;
+* the output projection, eq:residual_readout: y = concat_j(o_j) W_O^T;
+* the rotated INT2 map, eq:rotated_int2_map: D_{R,c}(z) = Q_2(z R; c, G) R^T;
+* key centering, Sec. 4.1: keys enter as D_{R_K,c_K}(k - mu), values as D_{R_V,c_V}(v);
+* the INT2 attention of eq:int2_attention / eq:int2_residual_readout evaluated on
+  those effective keys and values (the main-text, inverse-rotation form).
+
+Q_2 is "group-wise affine INT2" (Sec. 5 implementation details, Table A). The
+paper gives no arithmetic for it; the reading used here (and by the library):
+per token and per group of 32 consecutive rotated channels, over fp32 inputs,
+    mn = min x, mx = max x;  if c != 1: mn = fp32(c*mn), mx = fp32(c*mx)
+    s  = fp16_rne(fp32(fp32(mx - mn) / 3)),   z = fp16_rne(mn)
+    inv = fp32(1 / s) if s > 0 else 0
+    code = clamp(rne(fp32(fp32(x - z) * inv)), 0, 3)
+    dequant = code * s + z            (exact in fp64)
+The rotated tensor fed to Q_2 is the fp64 product rounded once to fp32.
+
+Packed cache layout (one 1536-byte record per physical block and KV head, the
+format the library writes; record address = pool + (block * H_kv + h) * 1536):
+    [   0,  512) K codes,  token-major: the 16-bit half m of token t at byte 32*t + 2*m
+    [ 512, 1024) V codes,  half-major : the 16-bit half m of token t at byte 512 + 32*m + 2*t
+    [1024, 1280) K meta,   token t, group g at byte 1024 + 16*t + 4*g: fp16 scale, then fp16 zero
+    [1280, 1408) V scales, group g, token t at byte 1280 + 32*g + 2*t (fp16)
+    [1408, 1536) V zeros,  group g, token t at byte 1408 + 32*g + 2*t (fp16)
+Inside a 16-bit half m, channel c = 16*p + m occupies bits 2p..2p+1 (little endian).
+
+Every function below is a plain definition; none is blocked, fused or reordered.
+Parity pins (tests/test_oracle_pins.py) tie it to what the paper and the
+mathematics fix; the packed layout is this library's own format and is pinned
+by hand-derived byte fixtures.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+HEAD_DIM = 128
+GROUP = 32
+N_GROUPS = HEAD_DIM // GROUP
+BLOCK = 16
+RECORD_BYTES = 1536
+OFF_KC, OFF_VC, OFF_KM, OFF_VS, OFF_VZ = 0, 512, 1024, 1280, 1408
+
+
+# --------------------------------------------------------------------------- inputs
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) to fp64 values (exact)."""
+    u = np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return u.view(np.float32).astype(np.float64)
+
+
+# --------------------------------------------------------------------------- rotation
+def mu_rot(R_k: np.ndarray, mu: np.ndarray) -> np.ndarray:
+    """Rotated key mean mu_h R_{K,h} per KV head (fp64), the constant subtracted after rotation
+    in the cache-write formulation (Sec. 6 efficiency analysis; appendix key-mean application)."""
+    return np.einsum("hi,hic->hc", mu.astype(np.float64), R_k.astype(np.float64))
+
+
+def center_rotate(k_bits: np.ndarray, mu: np.ndarray, R_k: np.ndarray) -> np.ndarray:
+    """(k - mu) R_K per token and KV head, fp64 (Sec. 4.1 reparameterization). k: [n, H, 128]."""
+    k = bf16_to_f64(k_bits) - mu.astype(np.float64)[None]
+    return np.einsum("nhi,hic->nhc", k, R_k.astype(np.float64))
+
+
+def rotate(v_bits: np.ndarray, R_v: np.ndarray) -> np.ndarray:
+    """v R_V per token and KV head, fp64. v: [n, H, 128]."""
+    return np.einsum("nhi,hic->nhc", bf16_to_f64(v_bits), R_v.astype(np.float64))
+
+
+# --------------------------------------------------------------------------- quantizer
+def quantize(x: np.ndarray, clip: float = 1.0):
+    """Group-wise affine INT2 quantization of fp32 rows (last axis 128, groups of 32).
+
+    Returns (codes uint8 [..., 128], s float16 [..., 4], z float16 [..., 4])."""
+    x = np.asarray(x, dtype=np.float32)
+    if x.shape[-1] != HEAD_DIM:
+        raise ValueError("last axis must be 128")
+    xg = x.reshape(x.shape[:-1] + (N_GROUPS, GROUP))
+    mn = xg.min(axis=-1)
+    mx = xg.max(axis=-1)
+    if clip != 1.0:
+        c = np.float32(clip)
+        mn = (c * mn).astype(np.float32)
+        mx = (c * mx).astype(np.float32)
+    s32 = (mx - mn).astype(np.float32) / np.float32(3.0)
+    s = s32.astype(np.float16)
+    z = mn.astype(np.float16)
+    if not (np.all(np.isfinite(s)) and np.all(np.isfinite(z))):
+        raise OverflowError("group range exceeds fp16 metadata")
+    sf = s.astype(np.float32)
+    inv = np.where(sf > 0, np.float32(1.0) / np.where(sf > 0, sf, np.float32(1.0)), np.float32(0.0))
+    inv = inv.astype(np.float32)
+    d = (xg - z.astype(np.float32)[..., None]).astype(np.float32)
+    t = (d * inv[..., None]).astype(np.float32)
+    codes = np.clip(np.rint(t), 0, 3).astype(np.uint8)
+    return codes.reshape(x.shape), s, z
+
+
+def dequantize(codes: np.ndarray, s: np.ndarray, z: np.ndarray) -> np.ndarray:
+    """code * s + z per group, fp64 (exact)."""
+    c = codes.astype(np.float64).reshape(codes.shape[:-1] + (N_GROUPS, GROUP))
+    out = c * s.astype(np.float64)[..., None] + z.astype(np.float64)[..., None]
+    return out.reshape(codes.shape)
+
+
+# --------------------------------------------------------------------------- packing
+def _halves_from_codes(codes: np.ndarray) -> np.ndarray:
+    """[..., 128] codes -> [..., 16] uint16 halves: channel 16p+m at bits 2p of half m."""
+    c = codes.astype(np.uint16).reshape(codes.shape[:-1] + (8, 16))  # (p, m)
+    shifts = (2 * np.arange(8, dtype=np.uint16))[:, None]
+    return np.bitwise_or.reduce(c << shifts, axis=-2).astype(np.uint16)
+
+
+def _codes_from_halves(halves: np.ndarray) -> np.ndarray:
+    """Inverse of _halves_from_codes."""
+    h = halves.astype(np.uint16)[..., None, :]                        # (1, m)
+    shifts = (2 * np.arange(8, dtype=np.uint16))[:, None]             # (p, 1)
+    c = (h >> shifts) & 3
+    return c.reshape(halves.shape[:-1] + (HEAD_DIM,)).astype(np.uint8)
+
+
+def write_records(pool: np.ndarray, slots: np.ndarray, kc, ks, kz, vc, vs, vz) -> None:
+    """Store quantized tokens into the paged pool at the byte offsets of the layout above.
+
+    pool: uint8 [num_blocks, H, 1536]; slots: [n] distinct cache slots (block * 16 + row);
+    kc/vc: uint8 [n, H, 128]; ks/kz/vs/vz: float16 [n, H, 4]."""
+    slots = np.asarray(slots, dtype=np.int64)
+    if np.unique(slots).size != slots.size:
+        raise ValueError("slots must be distinct")
+    n, H = slots.shape[0], pool.shape[1]
+    blk, t = slots // BLOCK, slots % BLOCK
+    B_ = blk[:, None, None]
+    H_ = np.arange(H)[None, :, None]
+    # K codes: 16 halves of token t at 32*t + 2*m
+    kh = _halves_from_codes(kc).astype("<u2").view(np.uint8).reshape(n, H, 32)
+    pool[B_, H_, (OFF_KC + 32 * t)[:, None, None] + np.arange(32)[None, None, :]] = kh
+    # V codes: half m of token t at 512 + 32*m + 2*t
+    vh = _halves_from_codes(vc).astype("<u2").view(np.uint8).reshape(n, H, 32)
+    vidx = (OFF_VC + 2 * t)[:, None] + (32 * np.arange(16)[:, None] + np.arange(2)[None, :]).reshape(1, 32)
+    pool[B_, H_, vidx[:, None, :]] = vh
+    # K meta: (s, z) of group g at 1024 + 16*t + 4*g
+    km = np.stack([ks, kz], axis=-1).astype("<f2").view(np.uint8).reshape(n, H, 16)
+    pool[B_, H_, (OFF_KM + 16 * t)[:, None, None] + np.arange(16)[None, None, :]] = km
+    # V scales / zeros: group g of token t at base + 32*g + 2*t
+    gidx = (32 * np.arange(N_GROUPS)[:, None] + np.arange(2)[None, :]).reshape(1, 8)
+    pool[B_, H_, ((OFF_VS + 2 * t)[:, None] + gidx)[:, None, :]] = \
+        np.ascontiguousarray(vs, dtype="<f2").view(np.uint8).reshape(n, H, 8)
+    pool[B_, H_, ((OFF_VZ + 2 * t)[:, None] + gidx)[:, None, :]] = \
+        np.ascontiguousarray(vz, dtype="<f2").view(np.uint8).reshape(n, H, 8)
+
+
+def read_tokens(pool: np.ndarray, block_row: np.ndarray, length: int, h: int):
+    """Unpack the first `length` tokens of one sequence and KV head.
+
+    Returns (kc, ks, kz, vc, vs, vz): codes uint8 [L, 128], metadata float16 [L, 4]."""
+    nblk = (length + BLOCK - 1) // BLOCK
+    recs = pool[np.asarray(block_row[:nblk], dtype=np.int64), h]          # [nb, 1536]
+    kh = recs[:, OFF_KC:OFF_VC].copy().view("<u2").reshape(nblk, BLOCK, 16)          # [nb, t, m]
+    vh = recs[:, OFF_VC:OFF_KM].copy().view("<u2").reshape(nblk, 16, BLOCK).transpose(0, 2, 1)
+    km = recs[:, OFF_KM:OFF_VS].copy().view("<f2").reshape(nblk, BLOCK, N_GROUPS, 2)
+    vs = recs[:, OFF_VS:OFF_VZ].copy().view("<f2").reshape(nblk, N_GROUPS, BLOCK).transpose(0, 2, 1)
+    vz = recs[:, OFF_VZ:RECORD_BYTES].copy().view("<f2").reshape(nblk, N_GROUPS, BLOCK).transpose(0, 2, 1)
+    flat = lambda a: a.reshape((nblk * BLOCK,) + a.shape[2:])[:length]
+    return (flat(_codes_from_halves(kh)), flat(km[..., 0]).astype(np.float16), flat(km[..., 1]).astype(np.float16),
+            flat(_codes_from_halves(vh)), flat(vs).astype(np.float16), flat(vz).astype(np.float16))
+
+
+def new_pool(num_blocks: int, num_kv_heads: int) -> np.ndarray:
+    return np.zeros((num_blocks, num_kv_heads, RECORD_BYTES), dtype=np.uint8)
+
+
+# --------------------------------------------------------------------------- cache write
+def quantize_pack_rotated(pool, k_rot, v_rot, slots, clip_k=1.0, clip_v=1.0):
+    """Quantize already rotated (and, for keys, centered) fp32 rows and store them."""
+    kc, ks, kz = quantize(k_rot, clip_k)
+    vc, vs, vz = quantize(v_rot, clip_v)
+    write_records(pool, slots, kc, ks, kz, vc, vs, vz)
+    return kc, ks, kz, vc, vs, vz
+
+
+def quantize_append(pool, k_bits, v_bits, slots, R_k, R_v, mu, clip_k=1.0, clip_v=1.0):
+    """Cache write of Sec. 4.1 / Sec. 6: (k - mu) R_K and v R_V, each rounded once to fp32,
+    group-quantized to INT2 and stored at the given slots. Returns the fp32 rotated rows too."""
+    k_rot = center_rotate(k_bits, mu, R_k).astype(np.float32)
+    v_rot = rotate(v_bits, R_v).astype(np.float32)
+    q = quantize_pack_rotated(pool, k_rot, v_rot, slots, clip_k, clip_v)
+    return k_rot, v_rot, q
+
+
+# --------------------------------------------------------------------------- attention
+def softmax_attention(q: np.ndarray, K: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """eq:fp_attention and eq:head_output for a set of query rows against one KV head.
+
+    q: [G, d], K, V: [L, d] (fp64). Returns o: [G, d]."""
+    a = (q @ K.T) / np.sqrt(q.shape[-1])
+    a = a - a.max(axis=-1, keepdims=True)
+    p = np.exp(a)
+    p /= p.sum(axis=-1, keepdims=True)
+    return p @ V
+
+
+def attention_probs(q: np.ndarray, K: np.ndarray) -> np.ndarray:
+    """softmax_s(<q, k_s>/sqrt(d)) (fp64), eq:fp_attention."""
+    a = (q @ K.T) / np.sqrt(q.shape[-1])
+    a = a - a.max(axis=-1, keepdims=True)
+    p = np.exp(a)
+    return p / p.sum(axis=-1, keepdims=True)
+
+
+def effective_kv(pool, block_row, length, h, R_k, R_v):
+    """Effective INT2 keys and values of eq:rotated_int2_map: k~ = Q2((k-mu)R_K) R_K^T and
+    v~ = Q2(v R_V) R_V^T, read back from the packed cache (fp64, [L, 128] each)."""
+    kc, ks, kz, vc, vs, vz = read_tokens(pool, block_row, length, h)
+    k_hat = dequantize(kc, ks, kz)
+    v_hat = dequantize(vc, vs, vz)
+    return k_hat @ R_k[h].astype(np.float64).T, v_hat @ R_v[h].astype(np.float64).T
+
+
+def decode(pool, q_bits, block_table, ctx_lens, R_k, R_v, W_o_bits=None, heads_out=False):
+    """INT2 decode attention of eq:int2_attention and eq:int2_residual_readout.
+
+    q_bits: bf16 [B, H_q, 128]; block_table: [B, max_blocks]; ctx_lens: [B];
+    W_o_bits: bf16 [d_model, H_q*128] or None.
+    Returns fp64 o [B, H_q, 128] when W_o_bits is None, else y [B, d_model]
+    (and o as well when heads_out is set)."""
+    q = bf16_to_f64(q_bits)
+    B, Hq, d = q.shape
+    H = R_k.shape[0]
+    gq = Hq // H
+    o = np.zeros((B, Hq, d), dtype=np.float64)
+    for b in range(B):
+        L = int(ctx_lens[b])
+        if L == 0:
+            continue
+        for h in range(H):
+            Kt, Vt = effective_kv(pool, block_table[b], L, h, R_k, R_v)
+            js = slice(h * gq, (h + 1) * gq)
+            o[b, js] = softmax_attention(q[b, js], Kt, Vt)
+    if W_o_bits is None:
+        return o
+    y = o.reshape(B, Hq * d) @ bf16_to_f64(W_o_bits).T
+    return (y, o) if heads_out else y
+
+
+def fold_wo(W_o_bits: np.ndarray, R_v: np.ndarray, num_q_heads: int) -> np.ndarray:
+    """W-bar_{O,j} = W_{O,j} R_{V,h(j)} per query head (appendix, equivalent inference
+    implementation). Returns fp64 [d_model, H_q*128]."""
+    W = bf16_to_f64(W_o_bits)
+    H = R_v.shape[0]
+    gq = num_q_heads // H
+    out = np.empty_like(W)
+    for j in range(num_q_heads):
+        cols = slice(j * HEAD_DIM, (j + 1) * HEAD_DIM)
+        out[:, cols] = W[:, cols] @ R_v[j // gq].astype(np.float64)
+    return out
