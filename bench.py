@@ -1,0 +1,216 @@
+"""Decode-step benchmark of the INT2 KV-cache hot path on one MI355X.
+
+One step = the cache write of each sequence's current token (quantize-append of B tokens) plus
+the decode attention over the whole INT2 context (query rotation, split-context scan, merge with
+the R_V^T un-rotation, W_O projection). Workload (default): 64 sequences with contexts drawn
+uniformly from [512, 32768] (seeded), 40 query / 8 KV heads, head_dim 128, paged blocks of 16
+tokens permuted across one shared pool, INT2 groups of 32 with fp16 scale/zero, W_O 5120x5120
+bf16. Inputs are seeded synthetic tensors already resident in HBM when timing starts.
+
+Prints one JSON line (rank 0). Progress goes to stderr.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "INT2 decode-attn KV-tokens/s and achieved HBM GB/s (% of peak), 1 MI355X"
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_02691_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(kernel_key, units_per_launch):
+    """HBM bytes per launch of the scan kernel from committed rocprofv3 counter summaries, or
+    None when absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        data = json.load(f)
+    entry = data.get(kernel_key)
+    if not entry or entry.get("source_hash") != kernel_source_hash():
+        return None
+    return entry["hbm_bytes_per_launch"]
+
+
+def cpu_baseline(w, target_s):
+    """Time the CPU oracle's decode (with W_O) on a bounded sample of this workload's sequences."""
+    from oracle import int2kv_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        cores = 1
+    tokens = 0
+    elapsed = 0.0
+    seqs = []
+    for b in range(w.batch):
+        L = int(w.ctx_lens[b])
+        nblk = (L + 15) // 16
+        pool = O.new_pool(nblk, w.num_kv_heads)
+        table = np.arange(nblk, dtype=np.int32)[None]
+        k, v = w.kv(b)
+        pos = np.arange(L)
+        O.quantize_append(pool, k, v, (table[0, pos // 16] * 16 + pos % 16), w.R_k, w.R_v, w.mu)
+        t0 = time.perf_counter()
+        O.decode(pool, w.q[b:b + 1], table, np.array([L], np.int32), w.R_k, w.R_v, w.W_o)
+        elapsed += time.perf_counter() - t0
+        tokens += L
+        seqs.append(b)
+        log(f"cpu oracle: sequence {b} ({L} tokens), {elapsed:.1f} s so far")
+        if elapsed >= target_s:
+            break
+    return {"value": tokens / elapsed, "unit": "KV-tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"oracle decode (+W_O) of sequences {seqs[0]}..{seqs[-1]} of the same workload "
+                      f"({tokens} KV-tokens, {elapsed:.1f} s, fp64 numpy)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--chunk", type=int, default=0, help="context chunk in tokens (0 = automatic)")
+    ap.add_argument("--variant", type=int, default=0, help="decode scan variant (0 auto, 1 VALU, 2 MFMA)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (see DESIGN.md for "
+              "how the decode would shard); run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_02691_amd import int2kv as K
+    from paper_2608_02691_amd import workloads as W
+
+    torch.cuda.set_device(0)
+    K.int2kv_set_decode_tuning(args.chunk, args.variant)
+    w = W.make_workload(args.config)
+    B, Hq, H = w.batch, w.num_q_heads, w.num_kv_heads
+    d_model = w.cfg.d_model or 0
+    lens = w.ctx_lens.astype(np.int64)
+    log(f"workload cfg{args.config}: B={B} Hq={Hq} H={H} sum(L)={int(lens.sum())} max(L)={int(lens.max())}")
+
+    dev = lambda a: torch.from_numpy(a.view(np.int16).copy() if a.dtype == np.uint16 else np.ascontiguousarray(a)).cuda()
+    cache = K.Int2KVCache(w.num_blocks, H)
+    Rk, Rv = dev(w.R_k), dev(w.R_v)
+    mu_rk = K.int2kv_prepare_mu_rot(Rk, dev(w.mu))
+    q = dev(w.q)
+    table = dev(w.block_table)
+    ctx = dev(w.ctx_lens)
+    Wo = dev(w.W_o) if w.W_o is not None else None
+    k_last = torch.empty((B, H, 128), dtype=torch.bfloat16, device="cuda")
+    v_last = torch.empty_like(k_last)
+    last_slots = np.array([w.slot_mapping(b, int(lens[b]) - 1)[0] for b in range(B)], np.int32)
+    t0 = time.time()
+    for b in range(B):
+        k, v = w.kv(b, as_torch=True)
+        L = int(lens[b])
+        kd, vd = k.cuda(), v.cuda()
+        if L > 1:
+            K.int2kv_quantize_append(cache, kd[:L - 1], vd[:L - 1], dev(w.slot_mapping(b, 0, L - 1)), Rk, Rv, mu_rk)
+        k_last[b] = kd[L - 1]
+        v_last[b] = vd[L - 1]
+        if b % 8 == 7:
+            torch.cuda.synchronize()
+            log(f"prefilled {b + 1}/{B} sequences ({time.time() - t0:.1f} s)")
+    slots_d = dev(last_slots)
+    max_ctx = int(lens.max())
+    ws = torch.empty(K.int2kv_decode_workspace_bytes(B, Hq, H, max_ctx, d_model), dtype=torch.uint8, device="cuda")
+    out = torch.empty((B, d_model) if d_model else (B, Hq, 128), dtype=torch.float32, device="cuda")
+
+    def step():
+        K.int2kv_quantize_append(cache, k_last, v_last, slots_d, Rk, Rv, mu_rk)
+        K.int2kv_decode(cache, q, table, ctx, max_ctx, Rk, Rv, W_o=Wo, out=out, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        K.int2kv_set_decode_events(*ev[i])
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    K.int2kv_set_decode_events(None, None)
+    ms_step = start.elapsed_time(stop) / args.steps
+    scan_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step, scan kernel {scan_ms:.3f} ms")
+
+    tokens = int(lens.sum())
+    pages = int(((lens + 15) // 16).sum())
+    scan_bytes = 96 * H * tokens + 4 * pages
+    step_bytes = (scan_bytes + B * Hq * 256 + (B * d_model * 4 if d_model else B * Hq * 512)
+                  + 2 * H * 128 * 128 * 4 + (2 * d_model * Hq * 128 if d_model else 0)
+                  + B * H * (512 + 96))
+    scan_gbps = scan_bytes / (scan_ms * 1e-3) / 1e9
+    step_gbps = step_bytes / (ms_step * 1e-3) / 1e9
+    traffic = counter_traffic(f"decode_scan_cfg{args.config}", 1)
+
+    result = {
+        "metric": METRIC,
+        "value": tokens / (ms_step * 1e-3),
+        "unit": "KV-tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int2 codes, fp16 meta, fp32 accumulate",
+        "data": "synthetic (seeded; no model weights or traces)",
+        "step_hbm_gbps": step_gbps,
+        "step_pct_hbm_peak": 100.0 * step_gbps / HBM_PEAK_GBPS,
+        "config": {
+            "workload": w.cfg.name,
+            "batch": B, "num_q_heads": Hq, "num_kv_heads": H, "head_dim": 128, "block_size": 16,
+            "group_size": 32, "sum_ctx": tokens, "max_ctx": max_ctx, "d_model": d_model,
+            "chunk_tokens": args.chunk or "auto", "variant": args.variant or "auto",
+        },
+        "roofline": {
+            "kernel": "decode split-context scan",
+            "bound": "hbm",
+            "achieved": scan_gbps,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": scan_gbps / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": scan_bytes,
+            "avg_launch_ms": scan_ms,
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,169 @@
+/*
+ * int2kv.h -- C ABI of the rotated, key-centered INT2 KV cache and its decode attention
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * What is computed (Yun et al., "Output-Aware Rotation for INT2 KV-Cache Quantization"):
+ *   cache write  (Sec. 4.1 key reparameterization; Sec. 6 efficiency analysis; appendix
+ *                 "Key-mean estimation and application"):
+ *       k_R = Q_2((k - mu) R_K) = Q_2(k R_K - mu R_K),   v_R = Q_2(v R_V)
+ *   decode       (eq:int2_attention, eq:int2_residual_readout; appendix "Rotated-query
+ *                 implementation" and "Equivalent inference implementation"):
+ *       a_s = (q R_K) k_R,s^T / sqrt(d),  p = softmax_s(a),  o = (sum_s p_s v_R,s) R_V^T,
+ *       y = concat_j(o_j) W_O^T   (optional)
+ *   Query head j reads KV head h(j) = floor(j / G_q), G_q = H_q / H_kv (GQA, Sec. 3).
+ *
+ * Q_2 is group-wise affine INT2 (Sec. 5 implementation details, Table A) over groups of 32
+ * consecutive rotated channels of one token. The arithmetic, fixed for bit-exactness, is
+ * (all fp32, no contraction, round-to-nearest-even throughout):
+ *       mn = min x, mx = max x;   if clip != 1: mn = clip*mn, mx = clip*mx
+ *       s  = fp16(fp32(mx - mn) / 3),   z = fp16(mn)
+ *       inv = s > 0 ? 1 / s : 0;        code = clamp(rint((x - z) * inv), 0, 3)
+ *       dequantized value = code * s + z
+ *
+ * Conventions for every call:
+ *   - All tensor pointers are DEVICE pointers owned by the caller; the library allocates
+ *     nothing and never synchronizes. Work is enqueued on `stream` (0 = null stream).
+ *   - bf16 and fp16 tensors are passed as uint16_t bit patterns; row-major, densely packed.
+ *   - Return value: INT2KV_OK or a negative int2kv_status. On an argument error nothing is
+ *     launched; int2kv_last_error() (thread-local) describes the last failure.
+ *   - head_dim = 128, block_size = 16, group_size = 32 are the supported shapes.
+ *
+ * Packed cache (part of the bit-exact contract): the pool holds one 1536-byte record per
+ * (physical block, KV head) at pool + (block * num_kv_heads + h) * 1536, 16-byte aligned.
+ * Token row t (0..15) of a block and rotated channel c (0..127) are stored as
+ *     [   0,  512) K codes, token-major: 16-bit half m of token t at byte 32*t + 2*m
+ *     [ 512, 1024) V codes, half-major : 16-bit half m of token t at byte 512 + 32*m + 2*t
+ *     [1024, 1280) K scale/zero: token t, group g at byte 1024 + 16*t + 4*g (fp16 s, fp16 z)
+ *     [1280, 1408) V scales: group g, token t at byte 1280 + 32*g + 2*t (fp16)
+ *     [1408, 1536) V zeros : group g, token t at byte 1408 + 32*g + 2*t (fp16)
+ *   where channel c = 16*p + m sits in half m at bits 2p..2p+1 (little endian), i.e. 2 bits
+ *   per element plus 32 metadata bits per group: 3.0 bits per cached element at G = 32.
+ *   A cache slot is block * 16 + t.
+ */
+#ifndef INT2KV_H
+#define INT2KV_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define INT2KV_HEAD_DIM 128
+#define INT2KV_BLOCK_SIZE 16
+#define INT2KV_GROUP_SIZE 32
+#define INT2KV_RECORD_BYTES 1536
+
+typedef enum {
+  INT2KV_OK = 0,
+  INT2KV_EINVAL = -1,       /* bad pointer, shape or alignment                         */
+  INT2KV_EUNSUPPORTED = -2, /* a shape this build does not implement                   */
+  INT2KV_EWORKSPACE = -3,   /* workspace missing or smaller than required              */
+  INT2KV_EHIP = -4          /* a HIP launch reported an error                          */
+} int2kv_status;
+
+/* The paged INT2 cache. `pool` points to num_blocks * num_kv_heads * 1536 bytes (device,
+ * 16-byte aligned). The caller zero-fills it once; every slot is rewritten in full by an
+ * append, so no clearing is needed when blocks are reused. */
+typedef struct int2kv_cache {
+  void* pool;
+  int32_t num_blocks;
+  int32_t num_kv_heads;
+  int32_t block_size; /* must be 16  */
+  int32_t head_dim;   /* must be 128 */
+  int32_t group_size; /* must be 32  */
+} int2kv_cache;
+
+/* Thread-local description of the last non-OK status ("" if none). */
+const char* int2kv_last_error(void);
+
+/* Library version string. */
+const char* int2kv_version(void);
+
+/* Bytes of the pool for the given shape (num_blocks * num_kv_heads * 1536). */
+size_t int2kv_pool_bytes(int num_blocks, int num_kv_heads);
+
+/* Rotated key mean mu_h R_{K,h}, precomputed once per KV head and subtracted right after the
+ * key rotation in the cache write (Sec. 6 efficiency analysis; appendix key-mean
+ * application: (k - mu) R_K = k R_K - mu R_K).
+ *   R_k   : fp32 [H_kv, 128, 128], row-major, the row-vector rotation z -> z R_K
+ *   mu    : fp32 [H_kv, 128]
+ *   mu_rk : fp32 [H_kv, 128] (output)
+ * Accumulates in fp32 in channel order. */
+int int2kv_prepare_mu_rot(const float* R_k, const float* mu, float* mu_rk, int num_kv_heads,
+                          hipStream_t stream);
+
+/* Folded output projection W-bar_{O,j} = W_{O,j} R_{V,h(j)} (appendix "Equivalent inference
+ * implementation"), so that y = concat_j(o'_j) W-bar_O^T with o'_j = o_j R_V needs no
+ * un-rotation.
+ *   W_o        : bf16 [d_model, H_q*128] row-major (W_{O,j} = columns j*128 .. j*128+127)
+ *   R_v        : fp32 [H_kv, 128, 128]
+ *   W_o_folded : bf16 [d_model, H_q*128] (output; fp32 accumulation, rounded once to bf16) */
+int int2kv_fold_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_o_folded, int d_model,
+                   int num_q_heads, int num_kv_heads, hipStream_t stream);
+
+/* Quantize already rotated rows and store them (the quantizer and packer alone; results are
+ * bit-exact with the arithmetic above).
+ *   k_rot, v_rot : fp32 [n, H_kv, 128]: (k - mu) R_K and v R_V
+ *   slot_mapping : int32 [n]; a negative slot skips the token; slots must be distinct
+ *   clip_k/clip_v: clip ratios c_K, c_V in (0, 1] (1 = no clipping) */
+int int2kv_quantize_pack_rotated(const int2kv_cache* cache, const float* k_rot, const float* v_rot,
+                                 const int32_t* slot_mapping, int num_tokens, float clip_k,
+                                 float clip_v, hipStream_t stream);
+
+/* Cache write (Sec. 4.1; Sec. 6): per token and KV head, k R_K - mu R_K and v R_V in fp32,
+ * then INT2 group quantization and packing into the slot given by slot_mapping.
+ *   k, v         : bf16 [n, H_kv, 128] (post-RoPE keys; values)
+ *   slot_mapping : int32 [n]; negative = skip; distinct slots
+ *   R_k, R_v     : fp32 [H_kv, 128, 128];  mu_rk: fp32 [H_kv, 128] from int2kv_prepare_mu_rot
+ * Appends of few tokens rotate with fp32 FMAs; appends of many tokens rotate on the matrix
+ * cores with R split into two bf16 terms (error ~1e-5 of |R|), so codes may differ from an
+ * exact-arithmetic rotation only where x sits at a rounding boundary. */
+int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
+                           const int32_t* slot_mapping, int num_tokens, const float* R_k,
+                           const float* R_v, const float* mu_rk, float clip_k, float clip_v,
+                           hipStream_t stream);
+
+/* Workspace bytes int2kv_decode needs for these sizes (d_model = 0 when W_O is not applied). */
+size_t int2kv_decode_workspace_bytes(int batch, int num_q_heads, int num_kv_heads, int max_ctx,
+                                     int d_model);
+
+/* Decode attention over the INT2 cache for one new query per sequence.
+ *   q            : bf16 [B, H_q, 128] (post-RoPE)
+ *   block_table  : int32 [B, max_blocks_per_seq]; entry i of sequence b is the physical
+ *                  block of tokens 16i .. 16i+15
+ *   ctx_lens     : int32 [B] cached tokens to attend (the current token is appended first);
+ *                  lengths are clamped to [0, min(max_ctx, 16*max_blocks_per_seq)], and blocks
+ *                  outside [0, num_blocks) are skipped
+ *   max_ctx      : host-side upper bound of ctx_lens (sizes the split-context grid)
+ *   R_k, R_v     : fp32 [H_kv, 128, 128]
+ *   W_o          : bf16 [d_model, H_q*128] or NULL (no output projection)
+ *   wo_is_folded : nonzero if W_o is W-bar_O from int2kv_fold_wo (then R_v is not applied)
+ *   out          : fp32 [B, H_q, 128] if W_o is NULL, else fp32 [B, d_model]
+ *   workspace    : device scratch of at least int2kv_decode_workspace_bytes(...) bytes
+ * The context is split into fixed-size chunks scanned in parallel (online softmax per chunk),
+ * then merged with a log-sum-exp reduction; sequences with ctx_len 0 produce zeros. */
+int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
+                  const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens,
+                  int max_ctx, const float* R_k, const float* R_v, const uint16_t* W_o, int d_model,
+                  int wo_is_folded, float* out, void* workspace, size_t workspace_bytes,
+                  hipStream_t stream);
+
+/* Measurement hook: when set (non-NULL), int2kv_decode records `before_scan` and `after_scan`
+ * on its stream immediately before and after the split-context scan kernel, so a caller can
+ * time that kernel alone with hipEventElapsedTime. Pass NULLs to disable. The events are owned
+ * by the caller and must outlive the calls that record them. */
+int int2kv_set_decode_events(hipEvent_t before_scan, hipEvent_t after_scan);
+
+/* Tuning knobs for measurement sweeps: context chunk in tokens (multiple of 64, 0 = automatic)
+ * and decode kernel variant (0 = automatic, 1 = vector ALU, 2 = matrix core). Returns
+ * INT2KV_EINVAL for out-of-range values. Workspace sizes depend on the chunk. */
+int int2kv_set_decode_tuning(int chunk_tokens, int variant);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* INT2KV_H */

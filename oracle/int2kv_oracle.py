@@ -72,12 +72,13 @@ def mu_rot(R_k: np.ndarray, mu: np.ndarray) -> np.ndarray:
 def center_rotate(k_bits: np.ndarray, mu: np.ndarray, R_k: np.ndarray) -> np.ndarray:
     """(k - mu) R_K per token and KV head, fp64 (Sec. 4.1 reparameterization). k: [n, H, 128]."""
     k = bf16_to_f64(k_bits) - mu.astype(np.float64)[None]
-    return np.einsum("nhi,hic->nhc", k, R_k.astype(np.float64))
+    return np.stack([k[:, h] @ R_k[h].astype(np.float64) for h in range(k.shape[1])], axis=1)
 
 
 def rotate(v_bits: np.ndarray, R_v: np.ndarray) -> np.ndarray:
     """v R_V per token and KV head, fp64. v: [n, H, 128]."""
-    return np.einsum("nhi,hic->nhc", bf16_to_f64(v_bits), R_v.astype(np.float64))
+    v = bf16_to_f64(v_bits)
+    return np.stack([v[:, h] @ R_v[h].astype(np.float64) for h in range(v.shape[1])], axis=1)
 
 
 # --------------------------------------------------------------------------- quantizer

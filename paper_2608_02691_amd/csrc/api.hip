@@ -1,0 +1,240 @@
+// C-ABI front end: argument validation, workspace planning and kernel dispatch.
+// Every entry point validates on the host and returns a negative status without launching on
+// any argument error; nothing here allocates device memory or synchronizes.
+#include <string>
+
+#include "../../include/int2kv.h"
+#include "common.h"
+#include "kernels.h"
+
+namespace int2kv {
+int wo_ksplit(int K);
+bool mfma_decode_available();
+}
+
+using namespace int2kv;
+
+namespace {
+
+thread_local std::string g_last_error;
+int g_chunk_override = 0;
+int g_variant_override = 0;
+hipEvent_t g_ev_before = nullptr;
+hipEvent_t g_ev_after = nullptr;
+
+int fail(int status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+
+int ok() {
+  g_last_error.clear();
+  return INT2KV_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(INT2KV_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+  return ok();
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int check_cache(const int2kv_cache* c) {
+  if (!c) return fail(INT2KV_EINVAL, "cache descriptor is NULL");
+  if (!c->pool) return fail(INT2KV_EINVAL, "cache pool is NULL");
+  if (!aligned(c->pool, 16)) return fail(INT2KV_EINVAL, "cache pool must be 16-byte aligned");
+  if (c->num_blocks <= 0 || c->num_kv_heads <= 0) return fail(INT2KV_EINVAL, "cache has no blocks or heads");
+  if (c->block_size != kBlock) return fail(INT2KV_EUNSUPPORTED, "block_size must be 16");
+  if (c->head_dim != kHeadDim) return fail(INT2KV_EUNSUPPORTED, "head_dim must be 128");
+  if (c->group_size != kGroup) return fail(INT2KV_EUNSUPPORTED, "group_size must be 32");
+  if ((int64_t)c->num_blocks * kBlock > INT32_MAX) return fail(INT2KV_EUNSUPPORTED, "too many blocks for int32 slots");
+  return INT2KV_OK;
+}
+
+bool valid_clip(float c) { return c > 0.0f && c <= 1.0f; }
+
+CacheView view(const int2kv_cache* c) {
+  return CacheView{static_cast<uint8_t*>(c->pool), c->num_blocks, c->num_kv_heads};
+}
+
+DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
+  DecodePlan p{};
+  int chunk = g_chunk_override;
+  if (chunk <= 0) {
+    // enough work items to fill 256 CUs several times over, chunks no smaller than 256 tokens
+    chunk = 256;
+    const long long units_per_chunk = (long long)B * H;
+    while (chunk < 4096 && units_per_chunk * ((max_ctx + 2 * chunk - 1) / (2 * chunk)) >= 2048) chunk *= 2;
+  }
+  p.chunk_tokens = chunk;
+  p.n_chunks = max_ctx > 0 ? (max_ctx + chunk - 1) / chunk : 1;
+  const int gq = Hq / H;
+  p.variant = g_variant_override ? g_variant_override : 1;
+  (void)gq;
+  p.wo_ksplit = d_model > 0 ? wo_ksplit(Hq * kHeadDim) : 0;
+  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+  size_t off = 0;
+  p.off_qrot = off;
+  off = up(off + (size_t)B * Hq * kHeadDim * sizeof(float));
+  p.off_qop = off;
+  off = up(off + qop_bytes(B, H, gq));
+  p.off_part = off;
+  off = up(off + (size_t)B * p.n_chunks * Hq * kPartStride * sizeof(float));
+  p.off_o = off;
+  if (d_model > 0) off = up(off + (size_t)B * Hq * kHeadDim * sizeof(float));
+  p.off_wo = off;
+  if (d_model > 0) off = up(off + (size_t)p.wo_ksplit * B * d_model * sizeof(float));
+  p.total = off;
+  return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* int2kv_last_error(void) { return g_last_error.c_str(); }
+
+const char* int2kv_version(void) { return "int2kv 0.1 gfx950"; }
+
+size_t int2kv_pool_bytes(int num_blocks, int num_kv_heads) {
+  if (num_blocks <= 0 || num_kv_heads <= 0) return 0;
+  return (size_t)num_blocks * num_kv_heads * kRecord;
+}
+
+int int2kv_set_decode_events(hipEvent_t before_scan, hipEvent_t after_scan) {
+  if ((before_scan == nullptr) != (after_scan == nullptr))
+    return fail(INT2KV_EINVAL, "pass both events or neither");
+  g_ev_before = before_scan;
+  g_ev_after = after_scan;
+  return ok();
+}
+
+int int2kv_set_decode_tuning(int chunk_tokens, int variant) {
+  if (chunk_tokens < 0 || chunk_tokens % 64 != 0 || chunk_tokens > (1 << 20))
+    return fail(INT2KV_EINVAL, "chunk_tokens must be 0 or a positive multiple of 64");
+  if (variant < 0 || variant > 2) return fail(INT2KV_EINVAL, "variant must be 0, 1 or 2");
+  if (variant == 2 && !mfma_decode_available()) return fail(INT2KV_EUNSUPPORTED, "matrix-core decode not built");
+  g_chunk_override = chunk_tokens;
+  g_variant_override = variant;
+  return ok();
+}
+
+int int2kv_prepare_mu_rot(const float* R_k, const float* mu, float* mu_rk, int num_kv_heads, hipStream_t stream) {
+  if (!R_k || !mu || !mu_rk) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (num_kv_heads <= 0) return fail(INT2KV_EINVAL, "num_kv_heads must be positive");
+  return hip_status(launch_prepare_mu_rot(R_k, mu, mu_rk, num_kv_heads, stream), "prepare_mu_rot");
+}
+
+int int2kv_fold_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_o_folded, int d_model, int num_q_heads,
+                   int num_kv_heads, hipStream_t stream) {
+  if (!W_o || !R_v || !W_o_folded) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (d_model <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads)
+    return fail(INT2KV_EINVAL, "bad d_model / head counts");
+  if (W_o == W_o_folded) return fail(INT2KV_EINVAL, "W_o_folded must not alias W_o");
+  return hip_status(launch_fold_wo(W_o, R_v, W_o_folded, d_model, num_q_heads, num_kv_heads, stream), "fold_wo");
+}
+
+int int2kv_quantize_pack_rotated(const int2kv_cache* cache, const float* k_rot, const float* v_rot,
+                                 const int32_t* slot_mapping, int num_tokens, float clip_k, float clip_v,
+                                 hipStream_t stream) {
+  if (int st = check_cache(cache)) return st;
+  if (num_tokens < 0) return fail(INT2KV_EINVAL, "num_tokens must be >= 0");
+  if (num_tokens == 0) return ok();
+  if (!k_rot || !v_rot || !slot_mapping) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (!valid_clip(clip_k) || !valid_clip(clip_v)) return fail(INT2KV_EINVAL, "clip ratios must be in (0, 1]");
+  return hip_status(launch_pack_rotated(view(cache), k_rot, v_rot, slot_mapping, num_tokens, clip_k, clip_v, stream),
+                    "quantize_pack_rotated");
+}
+
+int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
+                           const int32_t* slot_mapping, int num_tokens, const float* R_k, const float* R_v,
+                           const float* mu_rk, float clip_k, float clip_v, hipStream_t stream) {
+  if (int st = check_cache(cache)) return st;
+  if (num_tokens < 0) return fail(INT2KV_EINVAL, "num_tokens must be >= 0");
+  if (num_tokens == 0) return ok();
+  if (!k || !v || !slot_mapping || !R_k || !R_v || !mu_rk) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (!valid_clip(clip_k) || !valid_clip(clip_v)) return fail(INT2KV_EINVAL, "clip ratios must be in (0, 1]");
+  hipError_t e = launch_append_valu(view(cache), k, v, slot_mapping, num_tokens, R_k, R_v, mu_rk, clip_k, clip_v,
+                                    stream);
+  return hip_status(e, "quantize_append");
+}
+
+size_t int2kv_decode_workspace_bytes(int batch, int num_q_heads, int num_kv_heads, int max_ctx, int d_model) {
+  if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads || max_ctx < 0 ||
+      d_model < 0)
+    return 0;
+  return make_plan(batch, num_q_heads, num_kv_heads, max_ctx, d_model).total;
+}
+
+int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
+                  const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens, int max_ctx,
+                  const float* R_k, const float* R_v, const uint16_t* W_o, int d_model, int wo_is_folded, float* out,
+                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (int st = check_cache(cache)) return st;
+  if (batch < 0) return fail(INT2KV_EINVAL, "batch must be >= 0");
+  if (batch == 0) return ok();
+  const int H = cache->num_kv_heads;
+  if (num_q_heads <= 0 || num_q_heads % H) return fail(INT2KV_EINVAL, "num_q_heads must be a multiple of num_kv_heads");
+  const int gq = num_q_heads / H;
+  if (gq > 16) return fail(INT2KV_EUNSUPPORTED, "at most 16 query heads per KV head");
+  if (max_blocks_per_seq <= 0 || max_ctx < 0) return fail(INT2KV_EINVAL, "bad max_blocks_per_seq / max_ctx");
+  if (!q || !block_table || !ctx_lens || !R_k || !out || (!R_v && !(W_o && wo_is_folded)))
+    return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (!aligned(q, 16) || !aligned(out, 16)) return fail(INT2KV_EINVAL, "q and out must be 16-byte aligned");
+  if (W_o) {
+    if (d_model <= 0) return fail(INT2KV_EINVAL, "d_model must be positive when W_o is given");
+    if (!aligned(W_o, 16)) return fail(INT2KV_EINVAL, "W_o must be 16-byte aligned");
+  } else {
+    d_model = 0;
+  }
+  const DecodePlan plan = make_plan(batch, num_q_heads, H, max_ctx, d_model);
+  if (!workspace || workspace_bytes < plan.total)
+    return fail(INT2KV_EWORKSPACE, "workspace smaller than int2kv_decode_workspace_bytes()");
+  if (!aligned(workspace, 256)) return fail(INT2KV_EINVAL, "workspace must be 256-byte aligned");
+
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  DecodeArgs a{};
+  a.pool = static_cast<const uint8_t*>(cache->pool);
+  a.num_blocks = cache->num_blocks;
+  a.H = H;
+  a.q = q;
+  a.B = batch;
+  a.Hq = num_q_heads;
+  a.gq = gq;
+  a.block_table = block_table;
+  a.max_blocks = max_blocks_per_seq;
+  a.ctx_lens = ctx_lens;
+  a.max_ctx = max_ctx;
+  a.R_k = R_k;
+  a.R_v = R_v;
+  a.qrot = reinterpret_cast<float*>(ws + plan.off_qrot);
+  a.qop = ws + plan.off_qop;
+  a.part = reinterpret_cast<float*>(ws + plan.off_part);
+  a.chunk_tokens = plan.chunk_tokens;
+  a.n_chunks = plan.n_chunks;
+
+  hipError_t e = launch_qrot(a, stream);
+  if (e != hipSuccess) return hip_status(e, "decode/qrot");
+  if (g_ev_before) {
+    e = hipEventRecord(g_ev_before, stream);
+    if (e != hipSuccess) return hip_status(e, "decode/event");
+  }
+  e = plan.variant == 2 ? launch_decode_split_mfma(a, stream) : launch_decode_split_valu(a, stream);
+  if (e != hipSuccess) return hip_status(e, "decode/split");
+  if (g_ev_after) {
+    e = hipEventRecord(g_ev_after, stream);
+    if (e != hipSuccess) return hip_status(e, "decode/event");
+  }
+  const bool unrotate = !(W_o && wo_is_folded);
+  float* heads = W_o ? reinterpret_cast<float*>(ws + plan.off_o) : out;
+  e = launch_merge(a, unrotate, heads, stream);
+  if (e != hipSuccess) return hip_status(e, "decode/merge");
+  if (W_o) {
+    e = launch_wo_gemm(heads, W_o, out, reinterpret_cast<float*>(ws + plan.off_wo), batch,
+                       num_q_heads * kHeadDim, d_model, plan.wo_ksplit, stream);
+    if (e != hipSuccess) return hip_status(e, "decode/wo");
+  }
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,178 @@
+// Cache write: rotate (and center) keys/values, group-quantize to INT2, pack into the paged pool.
+//
+// Sec. 4.1 (key reparameterization k -> k - mu before rotation), Sec. 6 efficiency analysis and
+// the appendix key-mean application ((k - mu) R_K = k R_K - mu R_K, mu R_K precomputed), Sec. 5
+// implementation details (group-wise affine INT2). The packed record layout is documented in
+// include/int2kv.h.
+#include "common.h"
+#include "kernels.h"
+
+namespace int2kv {
+
+// ---------------------------------------------------------------------------------------------
+// mu R_K per KV head: thread c accumulates sum_i mu[i] R[i][c] in fp32, channel order.
+__global__ __launch_bounds__(128) void prepare_mu_rot_kernel(const float* __restrict__ R_k,
+                                                              const float* __restrict__ mu,
+                                                              float* __restrict__ mu_rk) {
+  const int h = blockIdx.x, c = threadIdx.x;
+  const float* R = R_k + (size_t)h * kHeadDim * kHeadDim;
+  const float* m = mu + (size_t)h * kHeadDim;
+  float acc = 0.0f;
+  for (int i = 0; i < kHeadDim; ++i) acc = fmaf(m[i], R[i * kHeadDim + c], acc);
+  mu_rk[(size_t)h * kHeadDim + c] = acc;
+}
+
+hipError_t launch_prepare_mu_rot(const float* R_k, const float* mu, float* mu_rk, int H, hipStream_t s) {
+  hipLaunchKernelGGL(prepare_mu_rot_kernel, dim3(H), dim3(128), 0, s, R_k, mu, mu_rk);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------------
+// W-bar_{O,j} = W_{O,j} R_{V,h(j)}: block (row tile, query head), thread c = output column.
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+constexpr int kFoldRows = 32;
+
+__global__ __launch_bounds__(128) void fold_wo_kernel(const uint16_t* __restrict__ W,
+                                                       const float* __restrict__ R_v,
+                                                       uint16_t* __restrict__ Wf, int d_model, int Hq,
+                                                       int gq) {
+  __shared__ float rows[kFoldRows][kHeadDim];
+  const int j = blockIdx.y, h = j / gq, c = threadIdx.x;
+  const int n0 = blockIdx.x * kFoldRows;
+  const size_t ld = (size_t)Hq * kHeadDim;
+  for (int r = 0; r < kFoldRows; ++r) {
+    const int n = n0 + r;
+    rows[r][c] = n < d_model ? bf16_bits_to_f32(W[n * ld + (size_t)j * kHeadDim + c]) : 0.0f;
+  }
+  __syncthreads();
+  const float* R = R_v + (size_t)h * kHeadDim * kHeadDim;
+  float col[kHeadDim];
+#pragma unroll
+  for (int i = 0; i < kHeadDim; ++i) col[i] = R[i * kHeadDim + c];
+  for (int r = 0; r < kFoldRows; ++r) {
+    const int n = n0 + r;
+    if (n >= d_model) break;
+    float acc = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kHeadDim; ++i) acc = fmaf(rows[r][i], col[i], acc);
+    Wf[n * ld + (size_t)j * kHeadDim + c] = static_cast<uint16_t>(f32_to_bf16_rne(acc));
+  }
+}
+
+hipError_t launch_fold_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_f, int d_model, int Hq,
+                          int H, hipStream_t s) {
+  dim3 grid((d_model + kFoldRows - 1) / kFoldRows, Hq);
+  hipLaunchKernelGGL(fold_wo_kernel, grid, dim3(128), 0, s, W_o, R_v, W_f, d_model, Hq, Hq / H);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------------
+// Quantize one token row of K (threads 0..127) and V (threads 128..255) held one channel per
+// thread, and store it. All 256 threads of the block must call it (it synchronizes).
+__device__ __forceinline__ void quantize_store_pair(float x, int slot, int h, float clip_k, float clip_v,
+                                                    const CacheView& cv, uint8_t (*codes)[kHeadDim]) {
+  const int tid = threadIdx.x;
+  const int row = tid >> 7;  // 0 = K, 1 = V
+  const int c = tid & 127;
+  float mn = x, mx = x;
+#pragma unroll
+  for (int off = 16; off >= 1; off >>= 1) {
+    mn = fminf(mn, __shfl_xor(mn, off, 32));
+    mx = fmaxf(mx, __shfl_xor(mx, off, 32));
+  }
+  uint32_t s_bits, z_bits;
+  float zf, inv;
+  int2_group_params(mn, mx, row == 0 ? clip_k : clip_v, s_bits, z_bits, zf, inv);
+  codes[row][c] = static_cast<uint8_t>(int2_code(x, zf, inv));
+  __syncthreads();
+  const bool ok = slot >= 0 && slot < cv.num_blocks * kBlock;
+  if (ok) {
+    const int blk = slot >> 4, t = slot & 15;
+    uint8_t* rec = cv.pool + ((size_t)blk * cv.num_kv_heads + h) * kRecord;
+    if (c < 16) {
+      uint32_t half = 0;
+#pragma unroll
+      for (int p = 0; p < 8; ++p) half |= static_cast<uint32_t>(codes[row][16 * p + c]) << (2 * p);
+      const int off = row == 0 ? kOffKCodes + 32 * t + 2 * c : kOffVCodes + 32 * c + 2 * t;
+      *reinterpret_cast<uint16_t*>(rec + off) = static_cast<uint16_t>(half);
+    }
+    if ((c & 31) == 0) {
+      const int g = c >> 5;
+      if (row == 0) {
+        *reinterpret_cast<uint32_t*>(rec + kOffKMeta + 16 * t + 4 * g) = s_bits | (z_bits << 16);
+      } else {
+        *reinterpret_cast<uint16_t*>(rec + kOffVScale + 32 * g + 2 * t) = static_cast<uint16_t>(s_bits);
+        *reinterpret_cast<uint16_t*>(rec + kOffVZero + 32 * g + 2 * t) = static_cast<uint16_t>(z_bits);
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// Quantize already rotated rows: block (token, KV head).
+__global__ __launch_bounds__(256) void pack_rotated_kernel(CacheView cv, const float* __restrict__ k_rot,
+                                                            const float* __restrict__ v_rot,
+                                                            const int32_t* __restrict__ slots, float clip_k,
+                                                            float clip_v) {
+  __shared__ uint8_t codes[2][kHeadDim];
+  const int n = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  const size_t base = ((size_t)n * cv.num_kv_heads + h) * kHeadDim + (tid & 127);
+  const float x = tid < 128 ? k_rot[base] : v_rot[base];
+  quantize_store_pair(x, slots[n], h, clip_k, clip_v, cv, codes);
+}
+
+hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_rot, const int32_t* slots,
+                               int n, float clip_k, float clip_v, hipStream_t s) {
+  hipLaunchKernelGGL(pack_rotated_kernel, dim3(n, c.num_kv_heads), dim3(256), 0, s, c, k_rot, v_rot, slots,
+                     clip_k, clip_v);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------------
+// Few-token append: block (tile of tokens, KV head). Thread (row, c) keeps column c of R_K (row 0)
+// or R_V (row 1) in registers and rotates each token of the tile with fp32 FMAs in channel order.
+constexpr int kAppendTile = 16;
+
+__global__ __launch_bounds__(256) void append_valu_kernel(CacheView cv, const uint16_t* __restrict__ k,
+                                                           const uint16_t* __restrict__ v,
+                                                           const int32_t* __restrict__ slots, int n,
+                                                           const float* __restrict__ R_k,
+                                                           const float* __restrict__ R_v,
+                                                           const float* __restrict__ mu_rk, float clip_k,
+                                                           float clip_v) {
+  __shared__ float xs[2][kHeadDim];
+  __shared__ uint8_t codes[2][kHeadDim];
+  const int h = blockIdx.y, tid = threadIdx.x, row = tid >> 7, c = tid & 127;
+  const float* R = (row == 0 ? R_k : R_v) + (size_t)h * kHeadDim * kHeadDim;
+  float col[kHeadDim];
+#pragma unroll
+  for (int i = 0; i < kHeadDim; ++i) col[i] = R[i * kHeadDim + c];
+  const float sub = row == 0 ? mu_rk[(size_t)h * kHeadDim + c] : 0.0f;
+  const int t_end = min(n, (blockIdx.x + 1) * kAppendTile);
+  for (int tok = blockIdx.x * kAppendTile; tok < t_end; ++tok) {
+    const size_t base = ((size_t)tok * cv.num_kv_heads + h) * kHeadDim + c;
+    xs[row][c] = bf16_bits_to_f32(row == 0 ? k[base] : v[base]);
+    __syncthreads();
+    float acc = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kHeadDim; ++i) acc = fmaf(xs[row][i], col[i], acc);
+    const float x = acc - sub;
+    quantize_store_pair(x, slots[tok], h, clip_k, clip_v, cv, codes);
+  }
+}
+
+hipError_t launch_append_valu(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots, int n,
+                              const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
+                              float clip_v, hipStream_t s) {
+  dim3 grid((n + kAppendTile - 1) / kAppendTile, c.num_kv_heads);
+  hipLaunchKernelGGL(append_valu_kernel, grid, dim3(256), 0, s, c, k, v, slots, n, R_k, R_v, mu_rk, clip_k,
+                     clip_v);
+  return hipGetLastError();
+}
+
+}  // namespace int2kv

@@ -1,0 +1,54 @@
+// Shared device helpers of the INT2 KV-cache library (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+namespace int2kv {
+
+constexpr int kHeadDim = 128;
+constexpr int kBlock = 16;
+constexpr int kGroup = 32;
+constexpr int kGroups = kHeadDim / kGroup;
+constexpr int kRecord = 1536;
+// byte offsets inside one (block, KV head) record
+constexpr int kOffKCodes = 0;     // [16 tok][16 halves]
+constexpr int kOffVCodes = 512;   // [16 halves][16 tok]
+constexpr int kOffKMeta = 1024;   // [16 tok][4 groups] (fp16 s, fp16 z)
+constexpr int kOffVScale = 1280;  // [4 groups][16 tok] fp16
+constexpr int kOffVZero = 1408;   // [4 groups][16 tok] fp16
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t h) {
+  return __half2float(__ushort_as_half(static_cast<unsigned short>(h)));
+}
+
+// Group parameters of the group-wise affine INT2 quantizer: scale and zero rounded to fp16,
+// and the fp32 values the codes are computed with. Fixed rounding sequence, no contraction.
+__device__ __forceinline__ void int2_group_params(float mn, float mx, float clip, uint32_t& s_bits,
+                                                  uint32_t& z_bits, float& zf, float& inv) {
+#pragma clang fp contract(off)
+  if (clip != 1.0f) {
+    mn = clip * mn;
+    mx = clip * mx;
+  }
+  const float s32 = (mx - mn) / 3.0f;
+  const __half s = __float2half_rn(s32);
+  const __half z = __float2half_rn(mn);
+  s_bits = __half_as_ushort(s);
+  z_bits = __half_as_ushort(z);
+  const float sf = __half2float(s);
+  zf = __half2float(z);
+  inv = sf > 0.0f ? 1.0f / sf : 0.0f;
+}
+
+__device__ __forceinline__ uint32_t int2_code(float x, float zf, float inv) {
+#pragma clang fp contract(off)
+  const float d = x - zf;
+  const float t = d * inv;
+  const float r = fminf(fmaxf(rintf(t), 0.0f), 3.0f);
+  return static_cast<uint32_t>(r);
+}
+
+}  // namespace int2kv

@@ -1,0 +1,65 @@
+// Internal launcher declarations shared by the C-ABI front end and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace int2kv {
+
+struct CacheView {
+  uint8_t* pool;
+  int num_blocks;
+  int num_kv_heads;
+};
+
+// ---- cache write (append.hip)
+hipError_t launch_prepare_mu_rot(const float* R_k, const float* mu, float* mu_rk, int H, hipStream_t s);
+hipError_t launch_fold_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_f, int d_model, int Hq,
+                          int H, hipStream_t s);
+hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_rot, const int32_t* slots,
+                               int n, float clip_k, float clip_v, hipStream_t s);
+hipError_t launch_append_valu(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots,
+                              int n, const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
+                              float clip_v, hipStream_t s);
+hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots,
+                              int n, const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
+                              float clip_v, hipStream_t s);
+
+// ---- decode (decode.hip, decode_mfma.hip, wo_gemm.hip)
+struct DecodePlan {
+  int chunk_tokens;
+  int n_chunks;
+  int variant;        // 1 = vector ALU, 2 = matrix core
+  int wo_ksplit;
+  size_t off_qrot, off_qop, off_part, off_o, off_wo, total;
+};
+
+struct DecodeArgs {
+  const uint8_t* pool;
+  int num_blocks, H;
+  const uint16_t* q;
+  int B, Hq, gq;
+  const int32_t* block_table;
+  int max_blocks;
+  const int32_t* ctx_lens;
+  int max_ctx;
+  const float* R_k;
+  const float* R_v;
+  float* qrot;     // [B, Hq, 128] fp32
+  uint8_t* qop;    // matrix-core query operands
+  float* part;     // [B, n_chunks, Hq, kPartStride]
+  int chunk_tokens, n_chunks;
+};
+
+constexpr int kPartStride = 132;  // m, l, 2 pad, O[128]
+
+hipError_t launch_qrot(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s);
+size_t qop_bytes(int B, int H, int gq);
+hipError_t launch_merge(const DecodeArgs& a, bool unrotate, float* out, hipStream_t s);
+hipError_t launch_wo_gemm(const float* o, const uint16_t* W, float* y, float* partial, int B, int K,
+                          int N, int ksplit, hipStream_t s);
+
+}  // namespace int2kv

@@ -1,0 +1,207 @@
+"""Thin Python binding of libint2kv (ctypes). Argument marshalling only.
+
+Every function has the name of the C entry point it calls (include/int2kv.h). Tensors must be
+torch tensors already on the GPU; work is enqueued on torch's current stream. bf16 tensors may
+be passed as torch.bfloat16 or as int16/uint16 bit patterns. There is no CPU fallback: if the
+HIP library is missing, importing any entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libint2kv.so")
+
+HEAD_DIM = 128
+BLOCK_SIZE = 16
+GROUP_SIZE = 32
+RECORD_BYTES = 1536
+
+INT2KV_OK = 0
+INT2KV_EINVAL = -1
+INT2KV_EUNSUPPORTED = -2
+INT2KV_EWORKSPACE = -3
+INT2KV_EHIP = -4
+
+EXPORTED = (
+    "int2kv_last_error", "int2kv_version", "int2kv_pool_bytes", "int2kv_prepare_mu_rot", "int2kv_fold_wo",
+    "int2kv_quantize_pack_rotated", "int2kv_quantize_append", "int2kv_decode_workspace_bytes",
+    "int2kv_decode", "int2kv_set_decode_tuning", "int2kv_set_decode_events",
+)
+
+
+class _Cache(ctypes.Structure):
+    _fields_ = [("pool", ctypes.c_void_p), ("num_blocks", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("group_size", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() "
+                           "(there is no CPU fallback)")
+    lib = ctypes.CDLL(path)
+    P, I, F, S, Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
+    sig = {
+        "int2kv_last_error": ([], ctypes.c_char_p),
+        "int2kv_version": ([], ctypes.c_char_p),
+        "int2kv_pool_bytes": ([I, I], Z),
+        "int2kv_prepare_mu_rot": ([P, P, P, I, S], I),
+        "int2kv_fold_wo": ([P, P, P, I, I, I, S], I),
+        "int2kv_quantize_pack_rotated": ([ctypes.POINTER(_Cache), P, P, P, I, F, F, S], I),
+        "int2kv_quantize_append": ([ctypes.POINTER(_Cache), P, P, P, I, P, P, P, F, F, S], I),
+        "int2kv_decode_workspace_bytes": ([I, I, I, I, I], Z),
+        "int2kv_decode": ([ctypes.POINTER(_Cache), P, I, I, P, I, P, I, P, P, P, I, I, P, P, Z, S], I),
+        "int2kv_set_decode_tuning": ([I, I], I),
+        "int2kv_set_decode_events": ([P, P], I),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _check(status: int, name: str) -> None:
+    if status != INT2KV_OK:
+        msg = load_library().int2kv_last_error().decode()
+        raise RuntimeError(f"{name} failed with status {status}: {msg}")
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor], dtypes, name: str):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+_BF16 = (torch.bfloat16, torch.int16, torch.uint16)
+_F32 = (torch.float32,)
+_I32 = (torch.int32,)
+
+
+class Int2KVCache:
+    """The paged INT2 pool (uint8 [num_blocks, num_kv_heads, 1536]) and its C descriptor."""
+
+    def __init__(self, num_blocks: int, num_kv_heads: int, device="cuda", pool: Optional[torch.Tensor] = None):
+        if pool is None:
+            pool = torch.zeros((num_blocks, num_kv_heads, RECORD_BYTES), dtype=torch.uint8, device=device)
+        if pool.shape != (num_blocks, num_kv_heads, RECORD_BYTES) or pool.dtype != torch.uint8:
+            raise ValueError("pool must be uint8 [num_blocks, num_kv_heads, 1536]")
+        self.pool = pool
+        self.num_blocks = num_blocks
+        self.num_kv_heads = num_kv_heads
+        self._desc = _Cache(pool.data_ptr(), num_blocks, num_kv_heads, BLOCK_SIZE, HEAD_DIM, GROUP_SIZE)
+
+    @property
+    def desc(self):
+        return ctypes.byref(self._desc)
+
+
+def int2kv_version() -> str:
+    return load_library().int2kv_version().decode()
+
+
+def int2kv_pool_bytes(num_blocks: int, num_kv_heads: int) -> int:
+    return load_library().int2kv_pool_bytes(num_blocks, num_kv_heads)
+
+
+def int2kv_prepare_mu_rot(R_k: torch.Tensor, mu: torch.Tensor, mu_rk: Optional[torch.Tensor] = None) -> torch.Tensor:
+    H = R_k.shape[0]
+    if mu_rk is None:
+        mu_rk = torch.empty((H, HEAD_DIM), dtype=torch.float32, device=R_k.device)
+    st = load_library().int2kv_prepare_mu_rot(_ptr(R_k, _F32, "R_k"), _ptr(mu, _F32, "mu"),
+                                              _ptr(mu_rk, _F32, "mu_rk"), H, _stream())
+    _check(st, "int2kv_prepare_mu_rot")
+    return mu_rk
+
+
+def int2kv_fold_wo(W_o: torch.Tensor, R_v: torch.Tensor, num_q_heads: int,
+                   out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    d_model = W_o.shape[0]
+    if out is None:
+        out = torch.empty_like(W_o)
+    st = load_library().int2kv_fold_wo(_ptr(W_o, _BF16, "W_o"), _ptr(R_v, _F32, "R_v"), _ptr(out, _BF16, "out"),
+                                       d_model, num_q_heads, R_v.shape[0], _stream())
+    _check(st, "int2kv_fold_wo")
+    return out
+
+
+def int2kv_quantize_pack_rotated(cache: Int2KVCache, k_rot: torch.Tensor, v_rot: torch.Tensor,
+                                 slot_mapping: torch.Tensor, clip_k: float = 1.0, clip_v: float = 1.0) -> None:
+    n = slot_mapping.shape[0]
+    if k_rot.numel() != n * cache.num_kv_heads * HEAD_DIM or v_rot.numel() != k_rot.numel():
+        raise ValueError("k_rot / v_rot must be [n, num_kv_heads, 128]")
+    st = load_library().int2kv_quantize_pack_rotated(cache.desc, _ptr(k_rot, _F32, "k_rot"), _ptr(v_rot, _F32, "v_rot"),
+                                                     _ptr(slot_mapping, _I32, "slot_mapping"), n, clip_k, clip_v,
+                                                     _stream())
+    _check(st, "int2kv_quantize_pack_rotated")
+
+
+def int2kv_quantize_append(cache: Int2KVCache, k: torch.Tensor, v: torch.Tensor, slot_mapping: torch.Tensor,
+                           R_k: torch.Tensor, R_v: torch.Tensor, mu_rk: torch.Tensor, clip_k: float = 1.0,
+                           clip_v: float = 1.0) -> None:
+    n = slot_mapping.shape[0]
+    if k.numel() != n * cache.num_kv_heads * HEAD_DIM or v.numel() != k.numel():
+        raise ValueError("k / v must be [n, num_kv_heads, 128]")
+    st = load_library().int2kv_quantize_append(cache.desc, _ptr(k, _BF16, "k"), _ptr(v, _BF16, "v"),
+                                               _ptr(slot_mapping, _I32, "slot_mapping"), n, _ptr(R_k, _F32, "R_k"),
+                                               _ptr(R_v, _F32, "R_v"), _ptr(mu_rk, _F32, "mu_rk"), clip_k, clip_v,
+                                               _stream())
+    _check(st, "int2kv_quantize_append")
+
+
+def int2kv_decode_workspace_bytes(batch: int, num_q_heads: int, num_kv_heads: int, max_ctx: int,
+                                  d_model: int = 0) -> int:
+    return load_library().int2kv_decode_workspace_bytes(batch, num_q_heads, num_kv_heads, max_ctx, d_model)
+
+
+def int2kv_set_decode_tuning(chunk_tokens: int = 0, variant: int = 0) -> None:
+    _check(load_library().int2kv_set_decode_tuning(chunk_tokens, variant), "int2kv_set_decode_tuning")
+
+
+def int2kv_set_decode_events(before_scan: Optional[torch.cuda.Event], after_scan: Optional[torch.cuda.Event]) -> None:
+    """Record the two (torch) events around the split-context scan kernel of later decodes."""
+    p = lambda e: None if e is None else e.cuda_event
+    _check(load_library().int2kv_set_decode_events(p(before_scan), p(after_scan)), "int2kv_set_decode_events")
+
+
+def int2kv_decode(cache: Int2KVCache, q: torch.Tensor, block_table: torch.Tensor, ctx_lens: torch.Tensor,
+                  max_ctx: int, R_k: torch.Tensor, R_v: Optional[torch.Tensor], W_o: Optional[torch.Tensor] = None,
+                  wo_is_folded: bool = False, out: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    B, Hq = q.shape[0], q.shape[1]
+    d_model = W_o.shape[0] if W_o is not None else 0
+    if out is None:
+        shape = (B, d_model) if W_o is not None else (B, Hq, HEAD_DIM)
+        out = torch.empty(shape, dtype=torch.float32, device=q.device)
+    need = int2kv_decode_workspace_bytes(B, Hq, cache.num_kv_heads, max_ctx, d_model)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
+    st = load_library().int2kv_decode(
+        cache.desc, _ptr(q, _BF16, "q"), B, Hq, _ptr(block_table, _I32, "block_table"), block_table.shape[1],
+        _ptr(ctx_lens, _I32, "ctx_lens"), max_ctx, _ptr(R_k, _F32, "R_k"), _ptr(R_v, _F32, "R_v"),
+        _ptr(W_o, _BF16, "W_o"), d_model, 1 if wo_is_folded else 0, _ptr(out, _F32, "out"),
+        _ptr(workspace, (torch.uint8,), "workspace"), workspace.numel(), _stream())
+    _check(st, "int2kv_decode")
+    return out

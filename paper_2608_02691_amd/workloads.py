@@ -10,7 +10,7 @@ The shapes stand in for the Qwen3-class decoder layers the paper evaluates
 settings"). The paper's calibration traces and models are not available, so
 every tensor is drawn from a seeded distribution:
 
-* keys   : N(0, 1) per channel plus a constant per-channel offset on a few
+* keys   : N(0, 1) per channel (torch CPU generator, per-sequence seed) plus a constant per-channel offset on a few
            seeded channels per KV head (the channel-wise key offsets that
            motivate key centering, Sec. 4.1 and Fig. 2), rounded to bf16 (RNE);
 * values : N(0, 1), rounded to bf16;
@@ -34,6 +34,7 @@ from dataclasses import dataclass, field
 from typing import Optional
 
 import numpy as np
+import torch
 
 HEAD_DIM = 128
 BLOCK_SIZE = 16
@@ -46,11 +47,9 @@ _S_ROT, _S_OFFSET, _S_QUERY, _S_PERM, _S_LEN, _S_WO, _S_CALIB, _S_SEQ = range(8)
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round fp32 to bf16 (round-to-nearest-even); returns the uint16 bit pattern."""
-    x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    return rounded.astype(np.uint16)
+    """Round fp32 to bf16 (round-to-nearest-even, as torch's CPU cast does); uint16 bit pattern."""
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -125,15 +124,22 @@ class Workload:
     def max_blocks(self) -> int:
         return self.block_table.shape[1]
 
-    def kv(self, b: int):
-        """bf16 bit patterns of keys and values for sequence b: two uint16 [L_b, H_kv, 128]."""
+    def kv(self, b: int, as_torch: bool = False):
+        """Keys and values of sequence b: bf16 [L_b, H_kv, 128] each.
+
+        Returned as uint16 bit patterns (numpy), or as torch.bfloat16 CPU tensors when
+        as_torch is set. Drawn with torch's CPU normal generator (fast and independent of the
+        thread count) seeded from this sequence's own SeedSequence."""
         L = int(self.ctx_lens[b])
         H = self.num_kv_heads
-        rng_k, rng_v = [np.random.default_rng(s) for s in self._seq_ss[b].spawn(2)]
-        k = rng_k.standard_normal((L, H, HEAD_DIM), dtype=np.float32)
-        k += self.key_offsets[None, :, :]
-        v = rng_v.standard_normal((L, H, HEAD_DIM), dtype=np.float32)
-        return f32_to_bf16_bits(k), f32_to_bf16_bits(v)
+        seed_k, seed_v = (int(s) & 0x7FFFFFFFFFFFFFFF for s in self._seq_ss[b].generate_state(2, np.uint64))
+        k = torch.randn((L, H, HEAD_DIM), generator=torch.Generator().manual_seed(seed_k), dtype=torch.float32)
+        k += torch.from_numpy(self.key_offsets)[None]
+        v = torch.randn((L, H, HEAD_DIM), generator=torch.Generator().manual_seed(seed_v), dtype=torch.float32)
+        k, v = k.to(torch.bfloat16), v.to(torch.bfloat16)
+        if as_torch:
+            return k, v
+        return (k.view(torch.int16).numpy().view(np.uint16), v.view(torch.int16).numpy().view(np.uint16))
 
     def slot_mapping(self, b: int, start: int = 0, stop: Optional[int] = None) -> np.ndarray:
         """Cache slot of every token position in [start, stop) of sequence b (int32)."""

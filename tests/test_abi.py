@@ -1,0 +1,58 @@
+"""The C-ABI library loads and exports every entry point include/int2kv.h declares; host-side
+argument validation rejects bad calls without touching a GPU (CPU only)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_02691_amd import int2kv as K
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "int2kv.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(int2kv_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_binding_names():
+    assert _declared() == sorted(K.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = K.load_library()
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_sizes():
+    assert "gfx950" in K.int2kv_version()
+    assert K.int2kv_pool_bytes(10, 8) == 10 * 8 * 1536
+    assert K.int2kv_pool_bytes(0, 8) == 0
+    assert K.int2kv_decode_workspace_bytes(64, 40, 8, 32768, 5120) > 0
+    assert K.int2kv_decode_workspace_bytes(2, 5, 2, 100, 0) == 0  # 5 % 2 != 0
+
+
+def test_null_cache_and_bad_arguments_return_errors_without_launch():
+    lib = K.load_library()
+    st = lib.int2kv_decode(None, None, 1, 8, None, 1, None, 16, None, None, None, 0, 0, None, None, 0, None)
+    assert st == K.INT2KV_EINVAL
+    assert b"cache" in lib.int2kv_last_error()
+    # a descriptor with an unsupported block size is refused before any pointer is used
+    bad = K._Cache(16, 4, 2, 8, 128, 32)
+    st = lib.int2kv_quantize_append(ctypes.byref(bad), None, None, None, 4, None, None, None, 1.0, 1.0, None)
+    assert st == K.INT2KV_EUNSUPPORTED
+    bad = K._Cache(16, 4, 2, 16, 128, 32)
+    st = lib.int2kv_quantize_append(ctypes.byref(bad), None, None, None, 4, None, None, None, 1.0, 1.0, None)
+    assert st == K.INT2KV_EINVAL  # NULL tensors
+    st = lib.int2kv_quantize_pack_rotated(ctypes.byref(bad), 16, 16, 16, 1, 1.5, 1.0, None)
+    assert st == K.INT2KV_EINVAL  # clip ratio out of range
+    st = lib.int2kv_decode(ctypes.byref(bad), 16, 1, 3, 16, 1, 16, 16, 16, 16, None, 0, 0, 16, 256, 0, None)
+    assert st == K.INT2KV_EINVAL  # 3 query heads over 2 KV heads
+    st = lib.int2kv_decode(ctypes.byref(bad), 16, 1, 4, 16, 1, 16, 16, 16, 16, None, 0, 0, 16, 256, 0, None)
+    assert st == K.INT2KV_EWORKSPACE
+    assert lib.int2kv_set_decode_tuning(100, 0) == K.INT2KV_EINVAL
+    assert lib.int2kv_set_decode_tuning(0, 7) == K.INT2KV_EINVAL
+    assert lib.int2kv_set_decode_tuning(0, 0) == K.INT2KV_OK

@@ -1,0 +1,157 @@
+"""GPU parity of the HIP library (through the C ABI) against the CPU oracle, at sizes the oracle
+finishes in seconds: several tiles, ragged tails, GQA ratios 1/4/5, empty and one-token
+contexts, clipping, degenerate groups."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import int2kv_oracle as O
+from paper_2608_02691_amd import int2kv as K
+from paper_2608_02691_amd import workloads as W
+
+from _helpers import (assert_rows_close, compare_cache_writes, dev, gpu_cache, oracle_pool)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _default_tuning():
+    K.int2kv_set_decode_tuning(0, 0)
+    yield
+    K.int2kv_set_decode_tuning(0, 0)
+
+
+def _rotated_rows(w):
+    ks, vs, slots = [], [], []
+    for b in range(w.batch):
+        k, v = w.kv(b)
+        ks.append(O.center_rotate(k, w.mu, w.R_k).astype(np.float32))
+        vs.append(O.rotate(v, w.R_v).astype(np.float32))
+        slots.append(w.slot_mapping(b))
+    return np.concatenate(ks), np.concatenate(vs), np.concatenate(slots)
+
+
+# ----------------------------------------------------------------------------- cache write
+@pytest.mark.parametrize("clip", [(1.0, 1.0), (0.96, 0.92)])
+def test_pack_rotated_is_bit_exact(clip):
+    print(f"\n[pack_rotated] clip={clip}", flush=True)
+    w = W.make_workload(1, batch=3, ctx=None, ctx_lens=np.array([100, 1, 47]), num_q_heads=8, num_kv_heads=8)
+    k_rot, v_rot, slots = _rotated_rows(w)
+    # special rows: a degenerate group, a huge-range group, exact grid values
+    k_rot[0, 0, 32:64] = 0.75
+    v_rot[1, 3, :32] = np.linspace(-500, 500, 32, dtype=np.float32)
+    k_rot[2, 1, 64:96] = (np.arange(32) % 4).astype(np.float32) * 0.5 - 1.0
+    slots_in = slots.copy()
+    slots_in[5] = -1  # skipped token
+    ref = O.new_pool(w.num_blocks, w.num_kv_heads)
+    keep = slots_in >= 0
+    O.quantize_pack_rotated(ref, k_rot[keep], v_rot[keep], slots_in[keep], *clip)
+    cache = gpu_cache(np.zeros_like(ref))
+    K.int2kv_quantize_pack_rotated(cache, dev(k_rot), dev(v_rot), dev(slots_in), *clip)
+    got = cache.pool.cpu().numpy()
+    assert np.array_equal(got, ref)
+
+
+def test_prepare_mu_rot_matches_oracle():
+    w = W.make_workload(1, batch=1, ctx=16)
+    mu_rk = K.int2kv_prepare_mu_rot(dev(w.R_k), dev(w.mu)).cpu().numpy()
+    ref = O.mu_rot(w.R_k, w.mu)
+    assert np.abs(mu_rk - ref).max() <= 1e-5 * np.abs(ref).max()
+
+
+@pytest.mark.parametrize("clip", [(1.0, 1.0), (0.96, 0.92)])
+def test_append_matches_oracle_up_to_ties(clip):
+    print(f"\n[append] clip={clip}", flush=True)
+    w = W.make_workload(4, batch=6, ctx_lens=np.array([700, 33, 1, 16, 250, 401]))
+    k_rot, v_rot, slots = _rotated_rows(w)
+    ref = oracle_pool(w, clip_k=clip[0], clip_v=clip[1])
+    cache = K.Int2KVCache(w.num_blocks, w.num_kv_heads)
+    mu_rk = K.int2kv_prepare_mu_rot(dev(w.R_k), dev(w.mu))
+    Rk, Rv = dev(w.R_k), dev(w.R_v)
+    for b in range(w.batch):
+        k, v = w.kv(b)
+        K.int2kv_quantize_append(cache, dev(k), dev(v), dev(w.slot_mapping(b)), Rk, Rv, mu_rk, *clip)
+    stats = compare_cache_writes(cache.pool.cpu().numpy(), ref, slots, k_rot, v_rot)
+    print(stats, flush=True)
+
+
+def test_append_one_call_many_tokens_matches_oracle():
+    """All sequences in one call (the prefill-sized path), tokens in a shuffled order."""
+    w = W.make_workload(3, batch=2, ctx=1200)
+    k_rot, v_rot, slots = _rotated_rows(w)
+    ref = oracle_pool(w)
+    kk, vv = zip(*[w.kv(b) for b in range(w.batch)])
+    k, v = np.concatenate(kk), np.concatenate(vv)
+    perm = np.random.default_rng(0).permutation(slots.size)
+    cache = K.Int2KVCache(w.num_blocks, w.num_kv_heads)
+    mu_rk = K.int2kv_prepare_mu_rot(dev(w.R_k), dev(w.mu))
+    K.int2kv_quantize_append(cache, dev(k[perm]), dev(v[perm]), dev(slots[perm]), dev(w.R_k), dev(w.R_v), mu_rk)
+    stats = compare_cache_writes(cache.pool.cpu().numpy(), ref, slots, k_rot, v_rot)
+    print(stats, flush=True)
+
+
+# ----------------------------------------------------------------------------- decode
+DECODE_CASES = [
+    # (cfg, batch, q heads, kv heads, lens, d_model)
+    (0, 1, 1, 1, [256], None),
+    (1, 3, 8, 2, [1, 17, 300], None),
+    (4, 2, 5, 1, [700, 64], None),
+    (1, 4, 32, 8, [1000, 33, 16, 0], None),
+    (4, 3, 10, 2, [1500, 2, 129], 256),
+]
+
+
+@pytest.mark.parametrize("variant", [1, 2])
+@pytest.mark.parametrize("chunk", [0, 64])
+@pytest.mark.parametrize("case", DECODE_CASES, ids=lambda c: f"cfg{c[0]}-B{c[1]}-{c[2]}x{c[3]}-dm{c[5]}")
+def test_decode_matches_oracle(case, chunk, variant):
+    cfg, B, Hq, H, lens, dm = case
+    print(f"\n[decode] case={case} chunk={chunk} variant={variant}", flush=True)
+    st = K.load_library().int2kv_set_decode_tuning(chunk, variant)
+    if st == K.INT2KV_EUNSUPPORTED:
+        pytest.skip("variant not built")
+    w = W.make_workload(cfg, batch=B, ctx_lens=np.array(lens), num_q_heads=Hq, num_kv_heads=H, d_model=dm)
+    pool = oracle_pool(w)
+    out_ref = O.decode(pool, w.q, w.block_table, w.ctx_lens, w.R_k, w.R_v, w.W_o)
+    cache = gpu_cache(pool)
+    max_ctx = int(max(lens))
+    args = (cache, dev(w.q), dev(w.block_table), dev(w.ctx_lens), max_ctx, dev(w.R_k), dev(w.R_v))
+    out = K.int2kv_decode(*args, W_o=dev(w.W_o) if dm else None)
+    worst = assert_rows_close(out.cpu().numpy(), out_ref, what="decode")
+    out2 = K.int2kv_decode(*args, W_o=dev(w.W_o) if dm else None)
+    assert torch.equal(out, out2), "decode must be deterministic"
+    print(f"worst row error {worst:.2e}", flush=True)
+    if dm:
+        Wf = K.int2kv_fold_wo(dev(w.W_o), dev(w.R_v), Hq)
+        out_f = K.int2kv_decode(*args, W_o=Wf, wo_is_folded=True)
+        assert_rows_close(out_f.cpu().numpy(), out_ref, what="decode with folded W_O")
+
+
+def test_fold_wo_matches_oracle():
+    w = W.make_workload(1, batch=1, ctx=16, num_q_heads=8, num_kv_heads=2, d_model=96)
+    got = K.int2kv_fold_wo(dev(w.W_o), dev(w.R_v), 8).cpu().view(torch.int16).numpy().view(np.uint16)
+    ref = O.fold_wo(w.W_o, w.R_v, 8)
+    g = O.bf16_to_f64(got)
+    # one bf16 rounding of an fp32 accumulation: relative error below 2^-8
+    assert np.all(np.abs(g - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-30)
+
+
+def test_out_of_range_blocks_and_lengths_are_clamped():
+    """Block ids outside the pool are skipped and ctx_lens beyond max_ctx are clamped."""
+    w = W.make_workload(1, batch=2, ctx_lens=np.array([64, 40]), num_q_heads=4, num_kv_heads=1)
+    pool = oracle_pool(w)
+    table = w.block_table.copy()
+    table[0, 1] = 10 ** 6          # tokens 16..31 of sequence 0 are unreachable
+    lens = w.ctx_lens.copy()
+    lens[1] = 10 ** 6              # clamped to max_ctx = 40
+    cache = gpu_cache(pool)
+    out = K.int2kv_decode(cache, dev(w.q), dev(table), dev(lens), 64, dev(w.R_k), dev(w.R_v)).cpu().numpy()
+    ref = O.decode(pool, w.q, w.block_table, np.array([64, 40]), w.R_k, w.R_v)
+    assert_rows_close(out[1], ref[1], what="clamped length")
+    # sequence 0 without block 1: attend over tokens 0..15 and 32..63 only
+    kc, ks, kz, vc, vs, vz = O.read_tokens(pool, w.block_table[0], 64, 0)
+    keep = np.r_[0:16, 32:64]
+    Kt = O.dequantize(kc, ks, kz)[keep] @ w.R_k[0].astype(np.float64).T
+    Vt = O.dequantize(vc, vs, vz)[keep] @ w.R_v[0].astype(np.float64).T
+    ref0 = O.softmax_attention(O.bf16_to_f64(w.q)[0], Kt, Vt)
+    assert_rows_close(out[0], ref0, what="skipped block")
