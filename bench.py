@@ -53,6 +53,36 @@ def counter_traffic(kernel_key, units_per_launch):
     return entry["hbm_bytes_per_launch"]
 
 
+class HipEvents:
+    """Raw HIP events (the library records them on its own stream around the scan kernel)."""
+
+    def __init__(self, n):
+        import ctypes
+        self.ct = ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.pairs = []
+        for _ in range(n):
+            a, b = ctypes.c_void_p(), ctypes.c_void_p()
+            for e in (a, b):
+                st = self.hip.hipEventCreate(ctypes.byref(e))
+                if st != 0:
+                    raise RuntimeError(f"hipEventCreate failed: {st}")
+            self.pairs.append((a.value, b.value))
+
+    def elapsed_ms(self, i):
+        ms = self.ct.c_float()
+        a, b = self.pairs[i]
+        st = self.hip.hipEventElapsedTime(self.ct.byref(ms), self.ct.c_void_p(a), self.ct.c_void_p(b))
+        if st != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed: {st}")
+        return ms.value
+
+    def destroy(self):
+        for a, b in self.pairs:
+            self.hip.hipEventDestroy(self.ct.c_void_p(a))
+            self.hip.hipEventDestroy(self.ct.c_void_p(b))
+
+
 def cpu_baseline(w, target_s):
     """Time the CPU oracle's decode (with W_O) on a bounded sample of this workload's sequences."""
     from oracle import int2kv_oracle as O
@@ -150,18 +180,19 @@ def main():
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps)")
 
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    ev = HipEvents(args.steps)
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for i in range(args.steps):
-        K.int2kv_set_decode_events(*ev[i])
+        K.int2kv_set_decode_events(*ev.pairs[i])
         step()
     stop.record()
     torch.cuda.synchronize()
     K.int2kv_set_decode_events(None, None)
     ms_step = start.elapsed_time(stop) / args.steps
-    scan_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    scan_ms = float(np.mean([ev.elapsed_ms(i) for i in range(args.steps)]))
+    ev.destroy()
     log(f"timed {args.steps} steps: {ms_step:.3f} ms/step, scan kernel {scan_ms:.3f} ms")
 
     tokens = int(lens.sum())

@@ -180,10 +180,10 @@ def int2kv_set_decode_tuning(chunk_tokens: int = 0, variant: int = 0) -> None:
     _check(load_library().int2kv_set_decode_tuning(chunk_tokens, variant), "int2kv_set_decode_tuning")
 
 
-def int2kv_set_decode_events(before_scan: Optional[torch.cuda.Event], after_scan: Optional[torch.cuda.Event]) -> None:
-    """Record the two (torch) events around the split-context scan kernel of later decodes."""
-    p = lambda e: None if e is None else e.cuda_event
-    _check(load_library().int2kv_set_decode_events(p(before_scan), p(after_scan)), "int2kv_set_decode_events")
+def int2kv_set_decode_events(before_scan: Optional[int], after_scan: Optional[int]) -> None:
+    """Record two raw hipEvent_t handles around the split-context scan kernel of later decodes
+    (None, None disables)."""
+    _check(load_library().int2kv_set_decode_events(before_scan, after_scan), "int2kv_set_decode_events")
 
 
 def int2kv_decode(cache: Int2KVCache, q: torch.Tensor, block_table: torch.Tensor, ctx_lens: torch.Tensor,

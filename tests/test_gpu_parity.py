@@ -132,8 +132,9 @@ def test_fold_wo_matches_oracle():
     got = K.int2kv_fold_wo(dev(w.W_o), dev(w.R_v), 8).cpu().view(torch.int16).numpy().view(np.uint16)
     ref = O.fold_wo(w.W_o, w.R_v, 8)
     g = O.bf16_to_f64(got)
-    # one bf16 rounding of an fp32 accumulation: relative error below 2^-8
-    assert np.all(np.abs(g - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-30)
+    # one bf16 rounding (half an ulp: 2^-8 relative) of an fp32 accumulation of 128 products
+    # (absolute error ~1e-6 of the row scale, which matters only for entries near zero)
+    assert np.all(np.abs(g - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-6 * np.abs(ref).max())
 
 
 def test_out_of_range_blocks_and_lengths_are_clamped():
@@ -143,11 +144,13 @@ def test_out_of_range_blocks_and_lengths_are_clamped():
     table = w.block_table.copy()
     table[0, 1] = 10 ** 6          # tokens 16..31 of sequence 0 are unreachable
     lens = w.ctx_lens.copy()
-    lens[1] = 10 ** 6              # clamped to max_ctx = 40
+    lens[1] = 10 ** 6              # clamped to max_ctx = 64 (= 16 * max_blocks)
     cache = gpu_cache(pool)
     out = K.int2kv_decode(cache, dev(w.q), dev(table), dev(lens), 64, dev(w.R_k), dev(w.R_v)).cpu().numpy()
-    ref = O.decode(pool, w.q, w.block_table, np.array([64, 40]), w.R_k, w.R_v)
-    assert_rows_close(out[1], ref[1], what="clamped length")
+    # sequence 1 then reads 64 tokens through its (zero-padded) table row: never-written slots
+    # decode to zero keys and values, and padding entry 0 points at a real block
+    ref = O.decode(pool, w.q[1:], w.block_table[1:], np.array([64]), w.R_k, w.R_v)
+    assert_rows_close(out[1], ref[0], what="clamped length")
     # sequence 0 without block 1: attend over tokens 0..15 and 32..63 only
     kc, ks, kz, vc, vs, vz = O.read_tokens(pool, w.block_table[0], 64, 0)
     keep = np.r_[0:16, 32:64]
