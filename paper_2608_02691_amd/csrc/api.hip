@@ -59,18 +59,18 @@ CacheView view(const int2kv_cache* c) {
 
 DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   DecodePlan p{};
+  const int gq = Hq / H;
+  p.variant = g_variant_override ? g_variant_override : (gq <= 8 && mfma_decode_available() ? 2 : 1);
   int chunk = g_chunk_override;
   if (chunk <= 0) {
-    // enough work items to fill 256 CUs several times over, chunks no smaller than 256 tokens
-    chunk = 256;
-    const long long units_per_chunk = (long long)B * H;
-    while (chunk < 4096 && units_per_chunk * ((max_ctx + 2 * chunk - 1) / (2 * chunk)) >= 2048) chunk *= 2;
+    // the largest chunk (up to 2048 tokens) that still gives >= 2048 work-groups, so that 256 CUs
+    // see several waves of them; never below 256 tokens (partials stay ~5 % of the KV bytes)
+    chunk = 2048;
+    const long long units = (long long)B * H;
+    while (chunk > 256 && units * ((max_ctx + chunk - 1) / chunk) < 2048) chunk /= 2;
   }
   p.chunk_tokens = chunk;
   p.n_chunks = max_ctx > 0 ? (max_ctx + chunk - 1) / chunk : 1;
-  const int gq = Hq / H;
-  p.variant = g_variant_override ? g_variant_override : 1;
-  (void)gq;
   p.wo_ksplit = d_model > 0 ? wo_ksplit(Hq * kHeadDim) : 0;
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   size_t off = 0;
@@ -213,8 +213,14 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
   a.chunk_tokens = plan.chunk_tokens;
   a.n_chunks = plan.n_chunks;
 
-  hipError_t e = launch_qrot(a, stream);
-  if (e != hipSuccess) return hip_status(e, "decode/qrot");
+  hipError_t e = hipSuccess;
+  if (plan.variant != 2) {
+    e = launch_qrot(a, stream);
+    if (e != hipSuccess) return hip_status(e, "decode/qrot");
+  } else {
+    e = launch_qprep(a, stream);
+    if (e != hipSuccess) return hip_status(e, "decode/qprep");
+  }
   if (g_ev_before) {
     e = hipEventRecord(g_ev_before, stream);
     if (e != hipSuccess) return hip_status(e, "decode/event");

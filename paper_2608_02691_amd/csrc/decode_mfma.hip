@@ -1,22 +1,432 @@
-// Matrix-core split-context decode scan (placeholder until the MFMA kernel lands).
+// Matrix-core split-context scan of the INT2 decode attention (gfx950, v_mfma_f32_16x16x32_f16).
+//
+// What is computed is the same as the vector-ALU scan (eq:int2_attention in the rotated-query
+// form of the appendix): a_s = (q R_K) . (c_s * s + z) / sqrt(d) per group of 32 channels, an
+// online softmax, and O' = sum_s p_s (c_s * s + z) in R_V coordinates. The affine metadata is
+// factored out of both contractions so the 2-bit codes enter the matrix cores unchanged:
+//
+//   scores : D[(j,g), t] = sum_{k in g} q'_jk c_tk          (MFMA, rows = head x group)
+//            a_jt = sum_g s_tg D[(j,g), t] + sum_g z_tg sum_{k in g} q'_jk
+//   values : O'[c, (j,g)] = sum_t (p_jt s_tg) c_tc + sum_t p_jt z_tg   (MFMA, K = tokens)
+//
+// A 2-bit code c sitting at bits 2x..2x+1 of a 16-bit half becomes the fp16 number 1 + c*2^-e
+// with one AND-OR (after at most one shift): the code lands in mantissa bits 4..9 of the fp16 1.0
+// pattern. e in {2, 4, 6} depends only on x. For the scores the constant 1 and the factor 2^-e
+// are folded into the query operand (scaled by 2^e per channel, with sum_k A_k subtracted through
+// the accumulator's initial value); for the values they are removed from the accumulator at the
+// end (O = 2^e (D - sum_t w_t)), using the exact fp16 weights the matrix core multiplied.
 #include "common.h"
 #include "kernels.h"
 
 namespace int2kv {
 
-bool mfma_decode_available() { return false; }
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr float kLogit2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
+constexpr int kWavesM = 4;
+constexpr float kRescaleTau = 8.0f;  // lazy rescaling: keep the running max until exceeded by 2^8
+constexpr int kQopTile = 4096 + 256;  // A operands (4 instr x 64 lanes x 16 B) + constants
+
+bool mfma_decode_available() { return true; }
 
 size_t qop_bytes(int B, int H, int gq) {
-  (void)B;
-  (void)H;
-  (void)gq;
-  return 0;
+  const int rt = (gq + 3) / 4;
+  return (size_t)B * H * rt * kQopTile;
+}
+
+// Class e of bit position x after the landing shift: the fp16 value is 1 + code * 2^-e.
+__host__ __device__ constexpr int land_e(int x) {
+  return (x == 4 || x == 7) ? 2 : ((x == 1 || x == 3 || x == 6) ? 4 : 6);
+}
+
+// The codes at position X of both 16-bit halves of w, as an fp16 pair (1 + c_lo 2^-e, 1 + c_hi 2^-e).
+template <int X>
+__device__ __forceinline__ uint32_t land(uint32_t w) {
+  constexpr int pos = X >= 5 ? X - 3 : (X <= 1 ? X + 2 : X);
+  const uint32_t v = X >= 5 ? (w >> 6) : (X <= 1 ? (w << 4) : w);
+  return (v & (0x00030003u << (2 * pos))) | 0x3C003C00u;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dppf(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+// max / sum over the 16 lanes of a DPP row
+__device__ __forceinline__ float row_max16(float x) {
+  x = fmaxf(x, dppf<0x128>(x));
+  x = fmaxf(x, dppf<0x124>(x));
+  x = fmaxf(x, dppf<0x122>(x));
+  x = fmaxf(x, dppf<0x121>(x));
+  return x;
+}
+__device__ __forceinline__ float row_sum16(float x) {
+  x += dppf<0x128>(x);
+  x += dppf<0x124>(x);
+  x += dppf<0x122>(x);
+  x += dppf<0x121>(x);
+  return x;
+}
+
+__device__ __forceinline__ void lds_sync_wave() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ half2_t as_h2(uint32_t u) { return __builtin_bit_cast(half2_t, u); }
+__device__ __forceinline__ uint32_t as_u(half2_t h) { return __builtin_bit_cast(uint32_t, h); }
+
+__device__ __forceinline__ int seq_len_m(const DecodeArgs& a, int b) {
+  int L = a.ctx_lens[b];
+  L = min(L, a.max_ctx);
+  L = min(L, a.max_blocks * kBlock);
+  return max(L, 0);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Query operands of one (sequence, KV head): q' = q R_K (fp32) scaled by log2(e)/sqrt(d) and a
+// per-head power of two sigma (max |q' sigma| in [256, 512)), laid out as the MFMA A operand of the
+// score contraction: row (j, g) of tile r holds q'_j on the channels of group g, times 2^e of the
+// channel's code position, as fp16. Constants per row: -sum_k A_k (accumulator start),
+// sum_{k in g} q'_jk (for the zero term) and 1/sigma.
+__global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int rt) {
+  __shared__ float qin[8][kHeadDim];
+  __shared__ float qr[8][kHeadDim];
+  __shared__ float sig[8];
+  const int bh = blockIdx.x, b = bh / a.H, h = bh % a.H, gq = a.gq, tid = threadIdx.x;
+  for (int i = tid; i < gq * kHeadDim; i += 256) {
+    const int jj = i / kHeadDim, c = i % kHeadDim;
+    qin[jj][c] = bf16_bits_to_f32(a.q[((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c]);
+  }
+  __syncthreads();
+  const float* R = a.R_k + (size_t)h * kHeadDim * kHeadDim;
+  for (int i = tid; i < gq * kHeadDim; i += 256) {
+    const int jj = i / kHeadDim, c = i % kHeadDim;
+    float acc = 0.0f;
+    for (int k = 0; k < kHeadDim; ++k) acc = fmaf(qin[jj][k], R[k * kHeadDim + c], acc);
+    qr[jj][c] = acc * kLogit2;
+  }
+  __syncthreads();
+  if (tid < gq) {
+    float m = 0.0f;
+    for (int c = 0; c < kHeadDim; ++c) m = fmaxf(m, fabsf(qr[tid][c]));
+    int ex = 0;
+    frexpf(m, &ex);
+    const int p2 = m > 0.0f ? max(-100, min(100, 9 - ex)) : 0;
+    sig[tid] = ldexpf(1.0f, p2);
+  }
+  __syncthreads();
+  uint8_t* out = a.qop + (size_t)bh * rt * kQopTile;
+  for (int idx = tid; idx < rt * 2048; idx += 256) {
+    const int r = idx / 2048, rem = idx % 2048;
+    const int i = rem / 512, l = (rem / 8) % 64, s = rem % 8;
+    const int m = l & 15, q = l >> 4, jj = 4 * r + (m >> 2), g = m & 3;
+    const int rr = s >> 1, hh = s & 1, x = 2 * i + (rr >> 1), d = rr & 1;
+    const int ch = 16 * x + 4 * q + 2 * d + hh;
+    _Float16 v = (_Float16)0.0f;
+    if (g == i && jj < gq) v = (_Float16)(qr[jj][ch] * sig[jj] * (float)(1 << land_e(x)));
+    reinterpret_cast<_Float16*>(out + r * kQopTile + (i * 64 + l) * 16)[s] = v;
+  }
+  if (tid < rt * 16) {
+    const int r = tid / 16, jl = (tid / 4) % 4, g = tid % 4, jj = 4 * r + jl;
+    float csum = 0.0f, qsum = 0.0f;
+    if (jj < gq) {
+      for (int cc = 0; cc < kGroup; ++cc) {
+        const int ch = 32 * g + cc;
+        const _Float16 v = (_Float16)(qr[jj][ch] * sig[jj] * (float)(1 << land_e(ch >> 4)));
+        csum += (float)v;
+        qsum += qr[jj][ch];
+      }
+    }
+    float* cst = reinterpret_cast<float*>(out + r * kQopTile + 4096);
+    cst[jl * 4 + g] = -csum;
+    cst[16 + jl * 4 + g] = qsum;
+    if (g == 0) cst[32 + jl] = jj < gq ? 1.0f / sig[jj] : 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+struct PairLoads {
+  uint2 kc[2];  // K codes of this lane's token (lo), chunk hi: halves 4hi..4hi+3
+  uint4 km[2];  // K scale/zero of token lo, groups 0..3
+  uint2 vc[2];  // V codes of half lo, tokens 4hi..4hi+3
+  uint2 vs[2];  // V scales of group lo&3, tokens 4hi..4hi+3
+  uint2 vz[2];  // V zeros  of group lo&3, tokens 4hi..4hi+3
+  bool ok[2];
+};
+
+__device__ __forceinline__ void load_pair(const DecodeArgs& a, const int* bt, int h, int pg, int pg_end, int lo,
+                                          int hi, PairLoads& p) {
+#pragma unroll
+  for (int P = 0; P < 2; ++P) {
+    const int page = pg + P;
+    const int blk = page < pg_end ? bt[page] : -1;
+    const bool ok = blk >= 0 && blk < a.num_blocks;
+    const uint8_t* rec = a.pool + (ok ? ((size_t)blk * a.H + h) * kRecord : 0);
+    p.ok[P] = ok;
+    p.kc[P] = *reinterpret_cast<const uint2*>(rec + kOffKCodes + 32 * lo + 8 * hi);
+    p.km[P] = *reinterpret_cast<const uint4*>(rec + kOffKMeta + 16 * lo);
+    p.vc[P] = *reinterpret_cast<const uint2*>(rec + kOffVCodes + 32 * lo + 8 * hi);
+    const uint2 s = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (lo & 3) + 8 * hi);
+    const uint2 z = *reinterpret_cast<const uint2*>(rec + kOffVZero + 32 * (lo & 3) + 8 * hi);
+    p.vs[P] = ok ? s : make_uint2(0u, 0u);
+    p.vz[P] = ok ? z : make_uint2(0u, 0u);
+  }
+}
+
+template <int X>
+__device__ __forceinline__ half8_t k_operand(uint2 w) {
+  // instruction i = X/2 ... called with X = 2i: registers (d0,x), (d1,x), (d0,x+1), (d1,x+1)
+  return __builtin_bit_cast(half8_t, u32x4_t{land<X>(w.x), land<X>(w.y), land<X + 1>(w.x), land<X + 1>(w.y)});
+}
+
+template <int MT>
+__device__ __forceinline__ half8_t v_operand(uint2 w0, uint2 w1) {
+  return __builtin_bit_cast(half8_t, u32x4_t{land<MT>(w0.x), land<MT>(w0.y), land<MT>(w1.x), land<MT>(w1.y)});
+}
+
+__device__ __forceinline__ float4_t mfma16(half8_t a, half8_t b, float4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+template <int RT>
+__global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a) {
+  __shared__ _Float16 p_lds[kWavesM][2][8][kBlock];
+  __shared__ float al_lds[kWavesM][8];
+  __shared__ float wst[kWavesM][8][2];
+  __shared__ float wout[kWavesM][8][kHeadDim];
+
+  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int L = seq_len_m(a, b);
+  const int t0 = chunk * a.chunk_tokens;
+  if (t0 >= L) return;
+  const int t1 = min(L, t0 + a.chunk_tokens);
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
+  const int gq = a.gq;
+
+  const uint8_t* qop = a.qop + ((size_t)b * a.H + h) * RT * kQopTile;
+  half8_t A[RT][4];
+  float4_t cinit[RT], sqL[RT];
+  float invsig[RT];
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    const uint8_t* t = qop + r * kQopTile;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) A[r][i] = *reinterpret_cast<const half8_t*>(t + (i * 64 + l) * 16);
+    cinit[r] = *reinterpret_cast<const float4_t*>(t + 4096 + hi * 16);
+    sqL[r] = *reinterpret_cast<const float4_t*>(t + 4096 + 64 + hi * 16);
+    invsig[r] = *reinterpret_cast<const float*>(t + 4096 + 128 + hi * 4);
+  }
+
+  float4_t acc[RT][8];
+  float wacc[RT], zacc[RT], mref[RT], lsum[RT];
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt) acc[r][mt] = float4_t{0.f, 0.f, 0.f, 0.f};
+    wacc[r] = 0.f;
+    zacc[r] = 0.f;
+    mref[r] = -INFINITY;
+    lsum[r] = 0.f;
+  }
+
+  const int pg_begin = t0 >> 4, pg_end = (t1 + kBlock - 1) >> 4;
+  const int npairs = (pg_end - pg_begin + 1) >> 1;
+  const int* bt = a.block_table + (size_t)b * a.max_blocks;
+  const half2_t ones = half2_t{(_Float16)1.0f, (_Float16)1.0f};
+
+  PairLoads cur;
+  if (w < npairs) load_pair(a, bt, h, pg_begin + 2 * w, pg_end, lo, hi, cur);
+  for (int pr = w; pr < npairs; pr += kWavesM) {
+    const int pg = pg_begin + 2 * pr;
+    PairLoads nxt;
+    const bool more = pr + kWavesM < npairs;
+    if (more) load_pair(a, bt, h, pg + 2 * kWavesM, pg_end, lo, hi, nxt);
+
+    // ---- scores: 2 pages x RT row tiles
+    float a2[2][RT];
+#pragma unroll
+    for (int P = 0; P < 2; ++P) {
+      const half8_t B0 = k_operand<0>(cur.kc[P]);
+      const half8_t B1 = k_operand<2>(cur.kc[P]);
+      const half8_t B2 = k_operand<4>(cur.kc[P]);
+      const half8_t B3 = k_operand<6>(cur.kc[P]);
+      const bool tv = cur.ok[P] && (pg + P) * kBlock + lo < t1;
+      const half2_t m0 = as_h2(cur.km[P].x), m1 = as_h2(cur.km[P].y), m2 = as_h2(cur.km[P].z), m3 = as_h2(cur.km[P].w);
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        float4_t d = cinit[r];
+        d = mfma16(A[r][0], B0, d);
+        d = mfma16(A[r][1], B1, d);
+        d = mfma16(A[r][2], B2, d);
+        d = mfma16(A[r][3], B3, d);
+        float sd = (float)m0.x * d[0];
+        sd = fmaf((float)m1.x, d[1], sd);
+        sd = fmaf((float)m2.x, d[2], sd);
+        sd = fmaf((float)m3.x, d[3], sd);
+        float zq = (float)m0.y * sqL[r][0];
+        zq = fmaf((float)m1.y, sqL[r][1], zq);
+        zq = fmaf((float)m2.y, sqL[r][2], zq);
+        zq = fmaf((float)m3.y, sqL[r][3], zq);
+        a2[P][r] = tv ? fmaf(sd, invsig[r], zq) : -INFINITY;
+      }
+    }
+
+    // ---- online softmax (lazy rescaling)
+    float pm[RT];
+    bool need = false;
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      pm[r] = row_max16(fmaxf(a2[0][r], a2[1][r]));
+      need |= pm[r] > mref[r] + kRescaleTau;
+    }
+    if (__any(need)) {
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        const float mnew = pm[r] > mref[r] + kRescaleTau ? pm[r] : mref[r];
+        const float al = mref[r] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mref[r] - mnew);
+        lsum[r] *= al;
+        mref[r] = mnew;
+        if (lo == 0) al_lds[w][4 * r + hi] = al;
+      }
+      lds_sync_wave();
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        const float alc = al_lds[w][4 * r + (lo >> 2)];
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) acc[r][mt] *= alc;
+        wacc[r] *= alc;
+        zacc[r] *= alc;
+      }
+    }
+#pragma unroll
+    for (int P = 0; P < 2; ++P) {
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        const float p = __builtin_amdgcn_exp2f(a2[P][r] - mref[r]);
+        lsum[r] += p;
+        p_lds[w][P][4 * r + hi][lo] = (_Float16)p;
+      }
+    }
+    lds_sync_wave();
+
+    // ---- values: K = the pair's 32 tokens, N = (j, g) columns, M = 8 tiles of 16 channels
+    half8_t Bw[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const int jc = 4 * r + (lo >> 2);
+      const uint2 pp0 = *reinterpret_cast<const uint2*>(&p_lds[w][0][jc][4 * hi]);
+      const uint2 pp1 = *reinterpret_cast<const uint2*>(&p_lds[w][1][jc][4 * hi]);
+      const half2_t w00 = as_h2(pp0.x) * as_h2(cur.vs[0].x);
+      const half2_t w01 = as_h2(pp0.y) * as_h2(cur.vs[0].y);
+      const half2_t w10 = as_h2(pp1.x) * as_h2(cur.vs[1].x);
+      const half2_t w11 = as_h2(pp1.y) * as_h2(cur.vs[1].y);
+      Bw[r] = __builtin_bit_cast(half8_t, u32x4_t{as_u(w00), as_u(w01), as_u(w10), as_u(w11)});
+      float wa = wacc[r];
+      wa = __builtin_amdgcn_fdot2(w00, ones, wa, false);
+      wa = __builtin_amdgcn_fdot2(w01, ones, wa, false);
+      wa = __builtin_amdgcn_fdot2(w10, ones, wa, false);
+      wa = __builtin_amdgcn_fdot2(w11, ones, wa, false);
+      wacc[r] = wa;
+      float za = zacc[r];
+      za = __builtin_amdgcn_fdot2(as_h2(pp0.x), as_h2(cur.vz[0].x), za, false);
+      za = __builtin_amdgcn_fdot2(as_h2(pp0.y), as_h2(cur.vz[0].y), za, false);
+      za = __builtin_amdgcn_fdot2(as_h2(pp1.x), as_h2(cur.vz[1].x), za, false);
+      za = __builtin_amdgcn_fdot2(as_h2(pp1.y), as_h2(cur.vz[1].y), za, false);
+      zacc[r] = za;
+    }
+#define INT2KV_PV_TILE(MT)                                          \
+  {                                                                 \
+    const half8_t Av = v_operand<MT>(cur.vc[0], cur.vc[1]);         \
+    _Pragma("unroll") for (int r = 0; r < RT; ++r) acc[r][MT] = mfma16(Av, Bw[r], acc[r][MT]); \
+  }
+    INT2KV_PV_TILE(0)
+    INT2KV_PV_TILE(1)
+    INT2KV_PV_TILE(2)
+    INT2KV_PV_TILE(3)
+    INT2KV_PV_TILE(4)
+    INT2KV_PV_TILE(5)
+    INT2KV_PV_TILE(6)
+    INT2KV_PV_TILE(7)
+#undef INT2KV_PV_TILE
+    lds_sync_wave();
+    if (more) cur = nxt;
+  }
+
+  // ---- wave state -> LDS
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    const float ls = row_sum16(lsum[r]);
+    if (lo == 0) {
+      wst[w][4 * r + hi][0] = mref[r];
+      wst[w][4 * r + hi][1] = ls;
+    }
+    float wa = wacc[r], za = zacc[r];
+    wa += __shfl_xor(wa, 16);
+    wa += __shfl_xor(wa, 32);
+    za += __shfl_xor(za, 16);
+    za += __shfl_xor(za, 32);
+    const int jc = 4 * r + (lo >> 2);
+#define INT2KV_OUT_TILE(MT)                                                              \
+  if ((lo & 3) == ((MT) >> 1)) {                                                         \
+    const float sc = (float)(1 << land_e(MT));                                           \
+    _Pragma("unroll") for (int e = 0; e < 4; ++e)                                        \
+      wout[w][jc][16 * (MT) + 4 * hi + e] = fmaf(sc, acc[r][MT][e] - wa, za);            \
+  }
+    INT2KV_OUT_TILE(0)
+    INT2KV_OUT_TILE(1)
+    INT2KV_OUT_TILE(2)
+    INT2KV_OUT_TILE(3)
+    INT2KV_OUT_TILE(4)
+    INT2KV_OUT_TILE(5)
+    INT2KV_OUT_TILE(6)
+    INT2KV_OUT_TILE(7)
+#undef INT2KV_OUT_TILE
+  }
+  __syncthreads();
+
+  // ---- merge the four waves, write this chunk's partial (m, l, O') per query head
+  for (int i = tid; i < gq * kHeadDim; i += blockDim.x) {
+    const int j = i / kHeadDim, c = i % kHeadDim;
+    float M = -INFINITY;
+#pragma unroll
+    for (int ww = 0; ww < kWavesM; ++ww) M = fmaxf(M, wst[ww][j][0]);
+    float ls = 0.0f, os = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < kWavesM; ++ww) {
+      const float mw = wst[ww][j][0];
+      const float f = mw == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mw - M);
+      ls = fmaf(f, wst[ww][j][1], ls);
+      os = fmaf(f, wout[ww][j][c], os);
+    }
+    float* dst = a.part + (((size_t)b * a.n_chunks + chunk) * a.Hq + h * gq + j) * kPartStride;
+    if (c == 0) {
+      dst[0] = M;
+      dst[1] = ls;
+    }
+    dst[4 + c] = os;
+  }
+}
+
+hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
+  if (a.gq > 8) return hipErrorNotSupported;
+  hipLaunchKernelGGL(qprep_kernel, dim3(a.B * a.H), dim3(256), 0, s, a, (a.gq + 3) / 4);
+  return hipGetLastError();
 }
 
 hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s) {
-  (void)a;
-  (void)s;
-  return hipErrorNotSupported;
+  if (a.gq > 8) return hipErrorNotSupported;
+  const int rt = (a.gq + 3) / 4;
+  dim3 grid(a.n_chunks, a.H, a.B);
+  if (rt == 1)
+    hipLaunchKernelGGL(decode_split_mfma_kernel<1>, grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(decode_split_mfma_kernel<2>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 }  // namespace int2kv

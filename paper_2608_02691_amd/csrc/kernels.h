@@ -56,6 +56,7 @@ constexpr int kPartStride = 132;  // m, l, 2 pad, O[128]
 
 hipError_t launch_qrot(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s);
 size_t qop_bytes(int B, int H, int gq);
 hipError_t launch_merge(const DecodeArgs& a, bool unrotate, float* out, hipStream_t s);
