@@ -69,6 +69,7 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
     const long long units = (long long)B * H;
     while (chunk > 256 && units * ((max_ctx + chunk - 1) / chunk) < 2048) chunk /= 2;
   }
+  if (p.variant == 2 && chunk > 4096) chunk = 4096;  // the matrix-core scan stages <= 256 pages
   p.chunk_tokens = chunk;
   p.n_chunks = max_ctx > 0 ? (max_ctx + chunk - 1) / chunk : 1;
   p.wo_ksplit = d_model > 0 ? wo_ksplit(Hq * kHeadDim) : 0;

@@ -47,7 +47,11 @@ template <int X>
 __device__ __forceinline__ uint32_t land(uint32_t w) {
   constexpr int pos = X >= 5 ? X - 3 : (X <= 1 ? X + 2 : X);
   const uint32_t v = X >= 5 ? (w >> 6) : (X <= 1 ? (w << 4) : w);
-  return (v & (0x00030003u << (2 * pos))) | 0x3C003C00u;
+  // one v_and_or_b32; gfx9 VOP3 encodings take no literal, so the mask rides in an SGPR and the
+  // fp16 1.0 pattern in a VGPR
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(v), "s"(0x00030003u << (2 * pos)), "v"(0x3C003C00u));
+  return r;
 }
 
 template <int CTRL>
@@ -156,23 +160,25 @@ struct PairLoads {
   uint2 vc[2];  // V codes of half lo, tokens 4hi..4hi+3
   uint2 vs[2];  // V scales of group lo&3, tokens 4hi..4hi+3
   uint2 vz[2];  // V zeros  of group lo&3, tokens 4hi..4hi+3
-  bool ok[2];
+  int ok[2];    // wave-uniform: page holds cached tokens
 };
 
-__device__ __forceinline__ void load_pair(const DecodeArgs& a, const int* bt, int h, int pg, int pg_end, int lo,
-                                          int hi, PairLoads& p) {
+// Loads of one page pair. Block ids come from the work-group's LDS copy of its block-table slice
+// (-1 = no page); missing pages read block 0 (always resident) and are masked by `ok`.
+__device__ __forceinline__ void load_pair(const DecodeArgs& a, const int* bt_lds, int npages, int h, int pair,
+                                          int lane_k, int lane_km, int lane_v, int lane_vm, PairLoads& p) {
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
-    const int page = pg + P;
-    const int blk = page < pg_end ? bt[page] : -1;
-    const bool ok = blk >= 0 && blk < a.num_blocks;
+    const int i = 2 * pair + P;
+    const int blk = __builtin_amdgcn_readfirstlane(i < npages ? bt_lds[i] : -1);
+    const bool ok = blk >= 0;
     const uint8_t* rec = a.pool + (ok ? ((size_t)blk * a.H + h) * kRecord : 0);
     p.ok[P] = ok;
-    p.kc[P] = *reinterpret_cast<const uint2*>(rec + kOffKCodes + 32 * lo + 8 * hi);
-    p.km[P] = *reinterpret_cast<const uint4*>(rec + kOffKMeta + 16 * lo);
-    p.vc[P] = *reinterpret_cast<const uint2*>(rec + kOffVCodes + 32 * lo + 8 * hi);
-    const uint2 s = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (lo & 3) + 8 * hi);
-    const uint2 z = *reinterpret_cast<const uint2*>(rec + kOffVZero + 32 * (lo & 3) + 8 * hi);
+    p.kc[P] = *reinterpret_cast<const uint2*>(rec + lane_k);
+    p.km[P] = *reinterpret_cast<const uint4*>(rec + lane_km);
+    p.vc[P] = *reinterpret_cast<const uint2*>(rec + lane_v);
+    const uint2 s = *reinterpret_cast<const uint2*>(rec + kOffVScale + lane_vm);
+    const uint2 z = *reinterpret_cast<const uint2*>(rec + kOffVZero + lane_vm);
     p.vs[P] = ok ? s : make_uint2(0u, 0u);
     p.vz[P] = ok ? z : make_uint2(0u, 0u);
   }
@@ -194,7 +200,131 @@ __device__ __forceinline__ float4_t mfma16(half8_t a, half8_t b, float4_t c) {
 }
 
 template <int RT>
+struct ScanState {
+  half8_t A[RT][4];
+  float4_t cinit[RT], sqL[RT];
+  float invsig[RT];
+  float4_t acc[RT][8];
+  float wacc[RT], zacc[RT], mref[RT], lsum[RT];
+};
+
+// One page pair (32 tokens) of one wave: scores on the matrix cores, lazy online softmax, and the
+// value accumulation on the matrix cores.
+template <int RT>
+__device__ __forceinline__ void scan_pair(ScanState<RT>& st, const PairLoads& cur, int pg, int t1, int lo, int hi,
+                                          _Float16 (*p_w)[8][kBlock], float* al_w) {
+  const half2_t ones = half2_t{(_Float16)1.0f, (_Float16)1.0f};
+  // ---- scores: 2 pages x RT row tiles
+  float a2[2][RT];
+  bool need = false;
+#pragma unroll
+  for (int P = 0; P < 2; ++P) {
+    const half8_t B0 = k_operand<0>(cur.kc[P]);
+    const half8_t B1 = k_operand<2>(cur.kc[P]);
+    const half8_t B2 = k_operand<4>(cur.kc[P]);
+    const half8_t B3 = k_operand<6>(cur.kc[P]);
+    const bool tv = cur.ok[P] && (pg + P) * kBlock + lo < t1;
+    const half2_t m0 = as_h2(cur.km[P].x), m1 = as_h2(cur.km[P].y), m2 = as_h2(cur.km[P].z), m3 = as_h2(cur.km[P].w);
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      float4_t d = st.cinit[r];
+      d = mfma16(st.A[r][0], B0, d);
+      d = mfma16(st.A[r][1], B1, d);
+      d = mfma16(st.A[r][2], B2, d);
+      d = mfma16(st.A[r][3], B3, d);
+      float sd = (float)m0.x * d[0];
+      sd = fmaf((float)m1.x, d[1], sd);
+      sd = fmaf((float)m2.x, d[2], sd);
+      sd = fmaf((float)m3.x, d[3], sd);
+      float zq = (float)m0.y * st.sqL[r][0];
+      zq = fmaf((float)m1.y, st.sqL[r][1], zq);
+      zq = fmaf((float)m2.y, st.sqL[r][2], zq);
+      zq = fmaf((float)m3.y, st.sqL[r][3], zq);
+      const float v = tv ? fmaf(sd, st.invsig[r], zq) : -INFINITY;
+      a2[P][r] = v;
+      need |= v > st.mref[r] + kRescaleTau;
+    }
+  }
+
+  // ---- lazy online softmax: the reference max only moves when a score exceeds it by 2^tau,
+  // which a wave-wide vote detects without a row reduction
+  if (__any(need)) {
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const float pm = row_max16(fmaxf(a2[0][r], a2[1][r]));
+      const float mnew = pm > st.mref[r] + kRescaleTau ? pm : st.mref[r];
+      const float al = st.mref[r] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(st.mref[r] - mnew);
+      st.lsum[r] *= al;
+      st.mref[r] = mnew;
+      if (lo == 0) al_w[4 * r + hi] = al;
+    }
+    lds_sync_wave();
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const float alc = al_w[4 * r + (lo >> 2)];
+#pragma unroll
+      for (int mt = 0; mt < 8; ++mt) st.acc[r][mt] *= alc;
+      st.wacc[r] *= alc;
+      st.zacc[r] *= alc;
+    }
+  }
+#pragma unroll
+  for (int P = 0; P < 2; ++P) {
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const float p = __builtin_amdgcn_exp2f(a2[P][r] - st.mref[r]);
+      st.lsum[r] += p;
+      p_w[P][4 * r + hi][lo] = (_Float16)p;
+    }
+  }
+  lds_sync_wave();
+
+  // ---- values: K = the pair's 32 tokens, N = (j, g) columns, M = 8 tiles of 16 channels
+  half8_t Bw[RT];
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    const int jc = 4 * r + (lo >> 2);
+    const uint2 pp0 = *reinterpret_cast<const uint2*>(&p_w[0][jc][4 * hi]);
+    const uint2 pp1 = *reinterpret_cast<const uint2*>(&p_w[1][jc][4 * hi]);
+    const half2_t w00 = as_h2(pp0.x) * as_h2(cur.vs[0].x);
+    const half2_t w01 = as_h2(pp0.y) * as_h2(cur.vs[0].y);
+    const half2_t w10 = as_h2(pp1.x) * as_h2(cur.vs[1].x);
+    const half2_t w11 = as_h2(pp1.y) * as_h2(cur.vs[1].y);
+    Bw[r] = __builtin_bit_cast(half8_t, u32x4_t{as_u(w00), as_u(w01), as_u(w10), as_u(w11)});
+    float wa = st.wacc[r];
+    wa = __builtin_amdgcn_fdot2(w00, ones, wa, false);
+    wa = __builtin_amdgcn_fdot2(w01, ones, wa, false);
+    wa = __builtin_amdgcn_fdot2(w10, ones, wa, false);
+    wa = __builtin_amdgcn_fdot2(w11, ones, wa, false);
+    st.wacc[r] = wa;
+    float za = st.zacc[r];
+    za = __builtin_amdgcn_fdot2(as_h2(pp0.x), as_h2(cur.vz[0].x), za, false);
+    za = __builtin_amdgcn_fdot2(as_h2(pp0.y), as_h2(cur.vz[0].y), za, false);
+    za = __builtin_amdgcn_fdot2(as_h2(pp1.x), as_h2(cur.vz[1].x), za, false);
+    za = __builtin_amdgcn_fdot2(as_h2(pp1.y), as_h2(cur.vz[1].y), za, false);
+    st.zacc[r] = za;
+  }
+#define INT2KV_PV_TILE(MT)                                                                   \
+  {                                                                                          \
+    const half8_t Av = v_operand<MT>(cur.vc[0], cur.vc[1]);                                  \
+    _Pragma("unroll") for (int r = 0; r < RT; ++r) st.acc[r][MT] = mfma16(Av, Bw[r], st.acc[r][MT]); \
+  }
+  INT2KV_PV_TILE(0)
+  INT2KV_PV_TILE(1)
+  INT2KV_PV_TILE(2)
+  INT2KV_PV_TILE(3)
+  INT2KV_PV_TILE(4)
+  INT2KV_PV_TILE(5)
+  INT2KV_PV_TILE(6)
+  INT2KV_PV_TILE(7)
+#undef INT2KV_PV_TILE
+}
+
+constexpr int kMaxChunkPages = 256;
+
+template <int RT>
 __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a) {
+  __shared__ int bt_lds[kMaxChunkPages];
   __shared__ _Float16 p_lds[kWavesM][2][8][kBlock];
   __shared__ float al_lds[kWavesM][8];
   __shared__ float wst[kWavesM][8][2];
@@ -208,164 +338,64 @@ __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a)
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
   const int gq = a.gq;
 
+  // block-table slice of this chunk -> LDS (ids outside the pool become -1)
+  const int pg_begin = t0 >> 4, pg_end = (t1 + kBlock - 1) >> 4;
+  const int npages = pg_end - pg_begin;
+  const int npairs = (npages + 1) >> 1;
+  const int* bt = a.block_table + (size_t)b * a.max_blocks + pg_begin;
+  for (int i = tid; i < npages; i += blockDim.x) {
+    const int blk = bt[i];
+    bt_lds[i] = (blk >= 0 && blk < a.num_blocks) ? blk : -1;
+  }
+
+  ScanState<RT> st;
   const uint8_t* qop = a.qop + ((size_t)b * a.H + h) * RT * kQopTile;
-  half8_t A[RT][4];
-  float4_t cinit[RT], sqL[RT];
-  float invsig[RT];
 #pragma unroll
   for (int r = 0; r < RT; ++r) {
     const uint8_t* t = qop + r * kQopTile;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) A[r][i] = *reinterpret_cast<const half8_t*>(t + (i * 64 + l) * 16);
-    cinit[r] = *reinterpret_cast<const float4_t*>(t + 4096 + hi * 16);
-    sqL[r] = *reinterpret_cast<const float4_t*>(t + 4096 + 64 + hi * 16);
-    invsig[r] = *reinterpret_cast<const float*>(t + 4096 + 128 + hi * 4);
+    for (int i = 0; i < 4; ++i) st.A[r][i] = *reinterpret_cast<const half8_t*>(t + (i * 64 + l) * 16);
+    st.cinit[r] = *reinterpret_cast<const float4_t*>(t + 4096 + hi * 16);
+    st.sqL[r] = *reinterpret_cast<const float4_t*>(t + 4096 + 64 + hi * 16);
+    st.invsig[r] = *reinterpret_cast<const float*>(t + 4096 + 128 + hi * 4);
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt) st.acc[r][mt] = float4_t{0.f, 0.f, 0.f, 0.f};
+    st.wacc[r] = 0.f;
+    st.zacc[r] = 0.f;
+    st.mref[r] = -INFINITY;
+    st.lsum[r] = 0.f;
   }
+  __syncthreads();
 
-  float4_t acc[RT][8];
-  float wacc[RT], zacc[RT], mref[RT], lsum[RT];
-#pragma unroll
-  for (int r = 0; r < RT; ++r) {
-#pragma unroll
-    for (int mt = 0; mt < 8; ++mt) acc[r][mt] = float4_t{0.f, 0.f, 0.f, 0.f};
-    wacc[r] = 0.f;
-    zacc[r] = 0.f;
-    mref[r] = -INFINITY;
-    lsum[r] = 0.f;
-  }
+  // per-lane byte offsets inside a page record
+  const int lane_k = kOffKCodes + 32 * lo + 8 * hi;
+  const int lane_km = kOffKMeta + 16 * lo;
+  const int lane_v = kOffVCodes + 32 * lo + 8 * hi;
+  const int lane_vm = 32 * (lo & 3) + 8 * hi;
 
-  const int pg_begin = t0 >> 4, pg_end = (t1 + kBlock - 1) >> 4;
-  const int npairs = (pg_end - pg_begin + 1) >> 1;
-  const int* bt = a.block_table + (size_t)b * a.max_blocks;
-  const half2_t ones = half2_t{(_Float16)1.0f, (_Float16)1.0f};
-
-  PairLoads cur;
-  if (w < npairs) load_pair(a, bt, h, pg_begin + 2 * w, pg_end, lo, hi, cur);
-  for (int pr = w; pr < npairs; pr += kWavesM) {
-    const int pg = pg_begin + 2 * pr;
-    PairLoads nxt;
-    const bool more = pr + kWavesM < npairs;
-    if (more) load_pair(a, bt, h, pg + 2 * kWavesM, pg_end, lo, hi, nxt);
-
-    // ---- scores: 2 pages x RT row tiles
-    float a2[2][RT];
-#pragma unroll
-    for (int P = 0; P < 2; ++P) {
-      const half8_t B0 = k_operand<0>(cur.kc[P]);
-      const half8_t B1 = k_operand<2>(cur.kc[P]);
-      const half8_t B2 = k_operand<4>(cur.kc[P]);
-      const half8_t B3 = k_operand<6>(cur.kc[P]);
-      const bool tv = cur.ok[P] && (pg + P) * kBlock + lo < t1;
-      const half2_t m0 = as_h2(cur.km[P].x), m1 = as_h2(cur.km[P].y), m2 = as_h2(cur.km[P].z), m3 = as_h2(cur.km[P].w);
-#pragma unroll
-      for (int r = 0; r < RT; ++r) {
-        float4_t d = cinit[r];
-        d = mfma16(A[r][0], B0, d);
-        d = mfma16(A[r][1], B1, d);
-        d = mfma16(A[r][2], B2, d);
-        d = mfma16(A[r][3], B3, d);
-        float sd = (float)m0.x * d[0];
-        sd = fmaf((float)m1.x, d[1], sd);
-        sd = fmaf((float)m2.x, d[2], sd);
-        sd = fmaf((float)m3.x, d[3], sd);
-        float zq = (float)m0.y * sqL[r][0];
-        zq = fmaf((float)m1.y, sqL[r][1], zq);
-        zq = fmaf((float)m2.y, sqL[r][2], zq);
-        zq = fmaf((float)m3.y, sqL[r][3], zq);
-        a2[P][r] = tv ? fmaf(sd, invsig[r], zq) : -INFINITY;
-      }
-    }
-
-    // ---- online softmax (lazy rescaling)
-    float pm[RT];
-    bool need = false;
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-      pm[r] = row_max16(fmaxf(a2[0][r], a2[1][r]));
-      need |= pm[r] > mref[r] + kRescaleTau;
-    }
-    if (__any(need)) {
-#pragma unroll
-      for (int r = 0; r < RT; ++r) {
-        const float mnew = pm[r] > mref[r] + kRescaleTau ? pm[r] : mref[r];
-        const float al = mref[r] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mref[r] - mnew);
-        lsum[r] *= al;
-        mref[r] = mnew;
-        if (lo == 0) al_lds[w][4 * r + hi] = al;
-      }
-      lds_sync_wave();
-#pragma unroll
-      for (int r = 0; r < RT; ++r) {
-        const float alc = al_lds[w][4 * r + (lo >> 2)];
-#pragma unroll
-        for (int mt = 0; mt < 8; ++mt) acc[r][mt] *= alc;
-        wacc[r] *= alc;
-        zacc[r] *= alc;
-      }
-    }
-#pragma unroll
-    for (int P = 0; P < 2; ++P) {
-#pragma unroll
-      for (int r = 0; r < RT; ++r) {
-        const float p = __builtin_amdgcn_exp2f(a2[P][r] - mref[r]);
-        lsum[r] += p;
-        p_lds[w][P][4 * r + hi][lo] = (_Float16)p;
-      }
-    }
-    lds_sync_wave();
-
-    // ---- values: K = the pair's 32 tokens, N = (j, g) columns, M = 8 tiles of 16 channels
-    half8_t Bw[RT];
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-      const int jc = 4 * r + (lo >> 2);
-      const uint2 pp0 = *reinterpret_cast<const uint2*>(&p_lds[w][0][jc][4 * hi]);
-      const uint2 pp1 = *reinterpret_cast<const uint2*>(&p_lds[w][1][jc][4 * hi]);
-      const half2_t w00 = as_h2(pp0.x) * as_h2(cur.vs[0].x);
-      const half2_t w01 = as_h2(pp0.y) * as_h2(cur.vs[0].y);
-      const half2_t w10 = as_h2(pp1.x) * as_h2(cur.vs[1].x);
-      const half2_t w11 = as_h2(pp1.y) * as_h2(cur.vs[1].y);
-      Bw[r] = __builtin_bit_cast(half8_t, u32x4_t{as_u(w00), as_u(w01), as_u(w10), as_u(w11)});
-      float wa = wacc[r];
-      wa = __builtin_amdgcn_fdot2(w00, ones, wa, false);
-      wa = __builtin_amdgcn_fdot2(w01, ones, wa, false);
-      wa = __builtin_amdgcn_fdot2(w10, ones, wa, false);
-      wa = __builtin_amdgcn_fdot2(w11, ones, wa, false);
-      wacc[r] = wa;
-      float za = zacc[r];
-      za = __builtin_amdgcn_fdot2(as_h2(pp0.x), as_h2(cur.vz[0].x), za, false);
-      za = __builtin_amdgcn_fdot2(as_h2(pp0.y), as_h2(cur.vz[0].y), za, false);
-      za = __builtin_amdgcn_fdot2(as_h2(pp1.x), as_h2(cur.vz[1].x), za, false);
-      za = __builtin_amdgcn_fdot2(as_h2(pp1.y), as_h2(cur.vz[1].y), za, false);
-      zacc[r] = za;
-    }
-#define INT2KV_PV_TILE(MT)                                          \
-  {                                                                 \
-    const half8_t Av = v_operand<MT>(cur.vc[0], cur.vc[1]);         \
-    _Pragma("unroll") for (int r = 0; r < RT; ++r) acc[r][MT] = mfma16(Av, Bw[r], acc[r][MT]); \
-  }
-    INT2KV_PV_TILE(0)
-    INT2KV_PV_TILE(1)
-    INT2KV_PV_TILE(2)
-    INT2KV_PV_TILE(3)
-    INT2KV_PV_TILE(4)
-    INT2KV_PV_TILE(5)
-    INT2KV_PV_TILE(6)
-    INT2KV_PV_TILE(7)
-#undef INT2KV_PV_TILE
-    lds_sync_wave();
-    if (more) cur = nxt;
+  // pairs w, w+4, ... with the next pair's loads in flight (ping-pong buffers)
+  PairLoads bufA, bufB;
+  int pr = w;
+  load_pair(a, bt_lds, npages, h, pr, lane_k, lane_km, lane_v, lane_vm, bufA);
+  while (pr < npairs) {
+    load_pair(a, bt_lds, npages, h, pr + kWavesM, lane_k, lane_km, lane_v, lane_vm, bufB);
+    scan_pair<RT>(st, bufA, pg_begin + 2 * pr, t1, lo, hi, p_lds[w], al_lds[w]);
+    pr += kWavesM;
+    if (pr >= npairs) break;
+    load_pair(a, bt_lds, npages, h, pr + kWavesM, lane_k, lane_km, lane_v, lane_vm, bufA);
+    scan_pair<RT>(st, bufB, pg_begin + 2 * pr, t1, lo, hi, p_lds[w], al_lds[w]);
+    pr += kWavesM;
   }
 
   // ---- wave state -> LDS
 #pragma unroll
   for (int r = 0; r < RT; ++r) {
-    const float ls = row_sum16(lsum[r]);
+    const float ls = row_sum16(st.lsum[r]);
     if (lo == 0) {
-      wst[w][4 * r + hi][0] = mref[r];
+      wst[w][4 * r + hi][0] = st.mref[r];
       wst[w][4 * r + hi][1] = ls;
     }
-    float wa = wacc[r], za = zacc[r];
+    float wa = st.wacc[r], za = st.zacc[r];
     wa += __shfl_xor(wa, 16);
     wa += __shfl_xor(wa, 32);
     za += __shfl_xor(za, 16);
@@ -375,7 +405,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a)
   if ((lo & 3) == ((MT) >> 1)) {                                                         \
     const float sc = (float)(1 << land_e(MT));                                           \
     _Pragma("unroll") for (int e = 0; e < 4; ++e)                                        \
-      wout[w][jc][16 * (MT) + 4 * hi + e] = fmaf(sc, acc[r][MT][e] - wa, za);            \
+      wout[w][jc][16 * (MT) + 4 * hi + e] = fmaf(sc, st.acc[r][MT][e] - wa, za);         \
   }
     INT2KV_OUT_TILE(0)
     INT2KV_OUT_TILE(1)
