@@ -125,6 +125,8 @@ def main():
     ap.add_argument("--variant", type=int, default=0, help="decode scan variant (0 auto, 1 VALU, 2 MFMA)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (see DESIGN.md for "
@@ -136,6 +138,15 @@ def main():
     from paper_2608_02691_amd import workloads as W
 
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        n = 1 << 30
+        src_t = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst_t = torch.empty_like(src_t)
+        for _ in range(3):
+            dst_t.copy_(src_t)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": n, "bytes_written": n, "launches": 3}), flush=True)
+        return
     K.int2kv_set_decode_tuning(args.chunk, args.variant)
     w = W.make_workload(args.config)
     B, Hq, H = w.batch, w.num_q_heads, w.num_kv_heads

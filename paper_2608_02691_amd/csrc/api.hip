@@ -63,11 +63,11 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   p.variant = g_variant_override ? g_variant_override : (gq <= 8 && mfma_decode_available() ? 2 : 1);
   int chunk = g_chunk_override;
   if (chunk <= 0) {
-    // the largest chunk (up to 2048 tokens) that still gives >= 2048 work-groups, so that 256 CUs
-    // see several waves of them; never below 256 tokens (partials stay ~5 % of the KV bytes)
-    chunk = 2048;
+    // the largest chunk (up to 4096 tokens) that still gives >= 1024 work-groups, so that 256 CUs
+    // see several rounds of them; never below 512 tokens (per-group set-up and partials amortized)
+    chunk = 4096;
     const long long units = (long long)B * H;
-    while (chunk > 256 && units * ((max_ctx + chunk - 1) / chunk) < 2048) chunk /= 2;
+    while (chunk > 512 && units * ((max_ctx + chunk - 1) / chunk) < 1024) chunk /= 2;
   }
   if (p.variant == 2 && chunk > 4096) chunk = 4096;  // the matrix-core scan stages <= 256 pages
   p.chunk_tokens = chunk;

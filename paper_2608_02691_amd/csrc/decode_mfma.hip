@@ -163,22 +163,53 @@ struct PairLoads {
   int ok[2];    // wave-uniform: page holds cached tokens
 };
 
-// Loads of one page pair. Block ids come from the work-group's LDS copy of its block-table slice
-// (-1 = no page); missing pages read block 0 (always resident) and are masked by `ok`.
-__device__ __forceinline__ void load_pair(const DecodeArgs& a, const int* bt_lds, int npages, int h, int pair,
-                                          int lane_k, int lane_km, int lane_v, int lane_vm, PairLoads& p) {
+// Page records are staged in LDS by the wave that consumes them, with LDS-DMA loads
+// (global_load_lds: lane i's bytes land at M0 + 16 i, or 4 i), so that several page pairs are in
+// flight per wave without holding registers. Each record is fetched whole: 1024 B of codes with one
+// dwordx4 load and 512 B of metadata with two dword loads. Issued through inline asm because the
+// compiler would otherwise wait for every outstanding DMA before any LDS read; the waits are
+// explicit instead (vmcnt counts this wave's DMA loads in issue order).
+__device__ __forceinline__ void dma16(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_addr), "v"(voff), "s"(base)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds_addr), "v"(voff), "s"(base)
+               : "memory", "m0");
+}
+
+// Block id of page index i of the chunk (-1 = none), wave-uniform.
+__device__ __forceinline__ int page_block(const int* bt_lds, int npages, int i) {
+  return __builtin_amdgcn_readfirstlane(i < npages ? bt_lds[i] : -1);
+}
+
+// Issue the 6 DMA loads of one page pair into a staging slot (2 x 1536 B at lds_slot).
+__device__ __forceinline__ void stage_pair(const DecodeArgs& a, const int* bt_lds, int npages, int h, int pair,
+                                           uint32_t lds_slot, int l) {
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
-    const int i = 2 * pair + P;
-    const int blk = __builtin_amdgcn_readfirstlane(i < npages ? bt_lds[i] : -1);
-    const bool ok = blk >= 0;
-    const uint8_t* rec = a.pool + (ok ? ((size_t)blk * a.H + h) * kRecord : 0);
+    const int blk = page_block(bt_lds, npages, 2 * pair + P);
+    const uint8_t* rec = a.pool + (blk >= 0 ? ((size_t)blk * a.H + h) * kRecord : 0);
+    const uint32_t dst = lds_slot + P * kRecord;
+    dma16(rec, 16 * l, dst);
+    dma4(rec + kOffKMeta, 4 * l, dst + kOffKMeta);
+    dma4(rec + kOffVScale, 4 * l, dst + kOffVScale);
+  }
+}
+
+// Operands of one page pair read back from its staging slot.
+__device__ __forceinline__ void read_pair(const uint8_t* slot, const int* bt_lds, int npages, int pair, int lo, int hi,
+                                          PairLoads& p) {
+#pragma unroll
+  for (int P = 0; P < 2; ++P) {
+    const uint8_t* rec = slot + P * kRecord;
+    const bool ok = page_block(bt_lds, npages, 2 * pair + P) >= 0;
     p.ok[P] = ok;
-    p.kc[P] = *reinterpret_cast<const uint2*>(rec + lane_k);
-    p.km[P] = *reinterpret_cast<const uint4*>(rec + lane_km);
-    p.vc[P] = *reinterpret_cast<const uint2*>(rec + lane_v);
-    const uint2 s = *reinterpret_cast<const uint2*>(rec + kOffVScale + lane_vm);
-    const uint2 z = *reinterpret_cast<const uint2*>(rec + kOffVZero + lane_vm);
+    p.kc[P] = *reinterpret_cast<const uint2*>(rec + kOffKCodes + 32 * lo + 8 * hi);
+    p.km[P] = *reinterpret_cast<const uint4*>(rec + kOffKMeta + 16 * lo);
+    p.vc[P] = *reinterpret_cast<const uint2*>(rec + kOffVCodes + 32 * lo + 8 * hi);
+    const uint2 s = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (lo & 3) + 8 * hi);
+    const uint2 z = *reinterpret_cast<const uint2*>(rec + kOffVZero + 32 * (lo & 3) + 8 * hi);
     p.vs[P] = ok ? s : make_uint2(0u, 0u);
     p.vz[P] = ok ? z : make_uint2(0u, 0u);
   }
@@ -321,9 +352,11 @@ __device__ __forceinline__ void scan_pair(ScanState<RT>& st, const PairLoads& cu
 }
 
 constexpr int kMaxChunkPages = 256;
+constexpr int kStages = 4;  // page pairs staged (in flight) per wave
 
 template <int RT>
 __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t stage[kWavesM][kStages][2][kRecord];
   __shared__ int bt_lds[kMaxChunkPages];
   __shared__ _Float16 p_lds[kWavesM][2][8][kBlock];
   __shared__ float al_lds[kWavesM][8];
@@ -365,26 +398,38 @@ __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a)
     st.mref[r] = -INFINITY;
     st.lsum[r] = 0.f;
   }
+  // Consume the operand loads here: the compiler counts only its own loads in vmcnt, so a wait
+  // for them placed inside the loop would also drain the staged DMA loads every iteration.
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) asm volatile("" ::"v"(st.A[r][i]));
+    asm volatile("" ::"v"(st.cinit[r]), "v"(st.sqL[r]), "v"(st.invsig[r]));
+  }
   __syncthreads();
 
-  // per-lane byte offsets inside a page record
-  const int lane_k = kOffKCodes + 32 * lo + 8 * hi;
-  const int lane_km = kOffKMeta + 16 * lo;
-  const int lane_v = kOffVCodes + 32 * lo + 8 * hi;
-  const int lane_vm = 32 * (lo & 3) + 8 * hi;
-
-  // pairs w, w+4, ... with the next pair's loads in flight (ping-pong buffers)
-  PairLoads bufA, bufB;
-  int pr = w;
-  load_pair(a, bt_lds, npages, h, pr, lane_k, lane_km, lane_v, lane_vm, bufA);
-  while (pr < npairs) {
-    load_pair(a, bt_lds, npages, h, pr + kWavesM, lane_k, lane_km, lane_v, lane_vm, bufB);
-    scan_pair<RT>(st, bufA, pg_begin + 2 * pr, t1, lo, hi, p_lds[w], al_lds[w]);
-    pr += kWavesM;
+  // pairs w, w+4, ... of the chunk, kStages of them in flight per wave
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const uint32_t stage_base = (uint32_t)(uintptr_t)&stage[wu][0][0][0];
+#pragma unroll
+  for (int k = 0; k < kStages; ++k) {
+    const int pr = wu + kWavesM * k;
+    if (pr < npairs) stage_pair(a, bt_lds, npages, h, pr, stage_base + k * 2 * kRecord, l);
+  }
+  for (int k = 0;; ++k) {
+    const int pr = wu + kWavesM * k;
     if (pr >= npairs) break;
-    load_pair(a, bt_lds, npages, h, pr + kWavesM, lane_k, lane_km, lane_v, lane_vm, bufA);
-    scan_pair<RT>(st, bufB, pg_begin + 2 * pr, t1, lo, hi, p_lds[w], al_lds[w]);
-    pr += kWavesM;
+    const int slot = k % kStages;
+    if (pr + kWavesM * (kStages - 1) < npairs)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6 * (kStages - 1)) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    PairLoads cur;
+    read_pair(&stage[wu][slot][0][0], bt_lds, npages, pr, lo, hi, cur);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    const int nxt = pr + kWavesM * kStages;
+    if (nxt < npairs) stage_pair(a, bt_lds, npages, h, nxt, stage_base + slot * 2 * kRecord, l);
+    scan_pair<RT>(st, cur, pg_begin + 2 * pr, t1, lo, hi, p_lds[w], al_lds[w]);
   }
 
   // ---- wave state -> LDS
