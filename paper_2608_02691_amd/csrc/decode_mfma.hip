@@ -178,17 +178,12 @@ __device__ __forceinline__ void dma4(const uint8_t* base, uint32_t voff, uint32_
                : "memory", "m0");
 }
 
-// Block id of page index i of the chunk (-1 = none), wave-uniform.
-__device__ __forceinline__ int page_block(const int* bt_lds, int npages, int i) {
-  return __builtin_amdgcn_readfirstlane(i < npages ? bt_lds[i] : -1);
-}
-
-// Issue the 6 DMA loads of one page pair into a staging slot (2 x 1536 B at lds_slot).
-__device__ __forceinline__ void stage_pair(const DecodeArgs& a, const int* bt_lds, int npages, int h, int pair,
-                                           uint32_t lds_slot, int l) {
+// Issue the 6 DMA loads of one page pair into a staging slot (2 x 1536 B at lds_slot). blk0/blk1
+// are wave-uniform block ids (-1: no page; block 0 is read instead and the pair is masked later).
+__device__ __forceinline__ void stage_pair(const DecodeArgs& a, int h, int blk0, int blk1, uint32_t lds_slot, int l) {
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
-    const int blk = page_block(bt_lds, npages, 2 * pair + P);
+    const int blk = P == 0 ? blk0 : blk1;
     const uint8_t* rec = a.pool + (blk >= 0 ? ((size_t)blk * a.H + h) * kRecord : 0);
     const uint32_t dst = lds_slot + P * kRecord;
     dma16(rec, 16 * l, dst);
@@ -198,12 +193,11 @@ __device__ __forceinline__ void stage_pair(const DecodeArgs& a, const int* bt_ld
 }
 
 // Operands of one page pair read back from its staging slot.
-__device__ __forceinline__ void read_pair(const uint8_t* slot, const int* bt_lds, int npages, int pair, int lo, int hi,
-                                          PairLoads& p) {
+__device__ __forceinline__ void read_pair(const uint8_t* slot, bool ok0, bool ok1, int lo, int hi, PairLoads& p) {
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
     const uint8_t* rec = slot + P * kRecord;
-    const bool ok = page_block(bt_lds, npages, 2 * pair + P) >= 0;
+    const bool ok = P == 0 ? ok0 : ok1;
     p.ok[P] = ok;
     p.kc[P] = *reinterpret_cast<const uint2*>(rec + kOffKCodes + 32 * lo + 8 * hi);
     p.km[P] = *reinterpret_cast<const uint4*>(rec + kOffKMeta + 16 * lo);
@@ -239,46 +233,59 @@ struct ScanState {
   float wacc[RT], zacc[RT], mref[RT], lsum[RT];
 };
 
-// One page pair (32 tokens) of one wave: scores on the matrix cores, lazy online softmax, and the
-// value accumulation on the matrix cores.
+// Scores of one page pair (2 pages x RT row tiles), base-2 logits, -inf where masked. The four
+// accumulation chains are issued interleaved so each hides the others' latency.
 template <int RT>
-__device__ __forceinline__ void scan_pair(ScanState<RT>& st, const PairLoads& cur, int pg, int t1, int lo, int hi,
-                                          _Float16 (*p_w)[8][kBlock], float* al_w) {
-  const half2_t ones = half2_t{(_Float16)1.0f, (_Float16)1.0f};
-  // ---- scores: 2 pages x RT row tiles
-  float a2[2][RT];
-  bool need = false;
+__device__ __forceinline__ void qk_pair(const ScanState<RT>& st, const PairLoads& cur, int pg, int t1, int lo,
+                                        float (&a2)[2][RT]) {
+  half8_t B[2][4];
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
-    const half8_t B0 = k_operand<0>(cur.kc[P]);
-    const half8_t B1 = k_operand<2>(cur.kc[P]);
-    const half8_t B2 = k_operand<4>(cur.kc[P]);
-    const half8_t B3 = k_operand<6>(cur.kc[P]);
+    B[P][0] = k_operand<0>(cur.kc[P]);
+    B[P][1] = k_operand<2>(cur.kc[P]);
+    B[P][2] = k_operand<4>(cur.kc[P]);
+    B[P][3] = k_operand<6>(cur.kc[P]);
+  }
+  float4_t d[2][RT];
+#pragma unroll
+  for (int P = 0; P < 2; ++P)
+#pragma unroll
+    for (int r = 0; r < RT; ++r) d[P][r] = st.cinit[r];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int P = 0; P < 2; ++P)
+#pragma unroll
+      for (int r = 0; r < RT; ++r) d[P][r] = mfma16(st.A[r][i], B[P][i], d[P][r]);
+#pragma unroll
+  for (int P = 0; P < 2; ++P) {
     const bool tv = cur.ok[P] && (pg + P) * kBlock + lo < t1;
     const half2_t m0 = as_h2(cur.km[P].x), m1 = as_h2(cur.km[P].y), m2 = as_h2(cur.km[P].z), m3 = as_h2(cur.km[P].w);
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
-      float4_t d = st.cinit[r];
-      d = mfma16(st.A[r][0], B0, d);
-      d = mfma16(st.A[r][1], B1, d);
-      d = mfma16(st.A[r][2], B2, d);
-      d = mfma16(st.A[r][3], B3, d);
-      float sd = (float)m0.x * d[0];
-      sd = fmaf((float)m1.x, d[1], sd);
-      sd = fmaf((float)m2.x, d[2], sd);
-      sd = fmaf((float)m3.x, d[3], sd);
+      float sd = (float)m0.x * d[P][r][0];
+      sd = fmaf((float)m1.x, d[P][r][1], sd);
+      sd = fmaf((float)m2.x, d[P][r][2], sd);
+      sd = fmaf((float)m3.x, d[P][r][3], sd);
       float zq = (float)m0.y * st.sqL[r][0];
       zq = fmaf((float)m1.y, st.sqL[r][1], zq);
       zq = fmaf((float)m2.y, st.sqL[r][2], zq);
       zq = fmaf((float)m3.y, st.sqL[r][3], zq);
-      const float v = tv ? fmaf(sd, st.invsig[r], zq) : -INFINITY;
-      a2[P][r] = v;
-      need |= v > st.mref[r] + kRescaleTau;
+      a2[P][r] = tv ? fmaf(sd, st.invsig[r], zq) : -INFINITY;
     }
   }
+}
 
-  // ---- lazy online softmax: the reference max only moves when a score exceeds it by 2^tau,
-  // which a wave-wide vote detects without a row reduction
+// Lazy online softmax of one pair: the reference max only moves when a score exceeds it by 2^tau
+// (detected by a wave-wide vote, no row reduction in the common case). Writes p (fp16) to LDS.
+template <int RT>
+__device__ __forceinline__ void softmax_pair(ScanState<RT>& st, const float (&a2)[2][RT], int lo, int hi,
+                                             _Float16 (*p_w)[8][kBlock], float* al_w) {
+  bool need = false;
+#pragma unroll
+  for (int P = 0; P < 2; ++P)
+#pragma unroll
+    for (int r = 0; r < RT; ++r) need |= a2[P][r] > st.mref[r] + kRescaleTau;
   if (__any(need)) {
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
@@ -308,9 +315,14 @@ __device__ __forceinline__ void scan_pair(ScanState<RT>& st, const PairLoads& cu
       p_w[P][4 * r + hi][lo] = (_Float16)p;
     }
   }
-  lds_sync_wave();
+}
 
-  // ---- values: K = the pair's 32 tokens, N = (j, g) columns, M = 8 tiles of 16 channels
+// Value accumulation of one pair: K = the pair's 32 tokens, N = (j, g) columns, M = 8 tiles of 16
+// channels; p comes back from LDS in the layout of the B operand.
+template <int RT>
+__device__ __forceinline__ void pv_pair(ScanState<RT>& st, const PairLoads& cur, int lo, int hi,
+                                        const _Float16 (*p_w)[8][kBlock]) {
+  const half2_t ones = half2_t{(_Float16)1.0f, (_Float16)1.0f};
   half8_t Bw[RT];
 #pragma unroll
   for (int r = 0; r < RT; ++r) {
@@ -357,8 +369,7 @@ constexpr int kStages = 4;  // page pairs staged (in flight) per wave
 template <int RT>
 __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t stage[kWavesM][kStages][2][kRecord];
-  __shared__ int bt_lds[kMaxChunkPages];
-  __shared__ _Float16 p_lds[kWavesM][2][8][kBlock];
+  __shared__ _Float16 p_lds[kWavesM][2][2][8][kBlock];
   __shared__ float al_lds[kWavesM][8];
   __shared__ float wst[kWavesM][8][2];
   __shared__ float wout[kWavesM][8][kHeadDim];
@@ -370,15 +381,19 @@ __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a)
   const int t1 = min(L, t0 + a.chunk_tokens);
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
   const int gq = a.gq;
+  (void)kMaxChunkPages;
 
-  // block-table slice of this chunk -> LDS (ids outside the pool become -1)
+  // pages of this chunk; wave w takes pairs w, w+4, ... (at most 32 pairs = 64 pages, one per lane)
   const int pg_begin = t0 >> 4, pg_end = (t1 + kBlock - 1) >> 4;
   const int npages = pg_end - pg_begin;
   const int npairs = (npages + 1) >> 1;
-  const int* bt = a.block_table + (size_t)b * a.max_blocks + pg_begin;
-  for (int i = tid; i < npages; i += blockDim.x) {
-    const int blk = bt[i];
-    bt_lds[i] = (blk >= 0 && blk < a.num_blocks) ? blk : -1;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const int nmine = wu < npairs ? (npairs - wu + kWavesM - 1) / kWavesM : 0;  // pairs of this wave
+  int wblk;  // lane i: block id of this wave's page i (pair i/2, page i%2), -1 if none
+  {
+    const int page = 2 * (wu + kWavesM * (l >> 1)) + (l & 1);
+    const int blk = page < npages ? a.block_table[(size_t)b * a.max_blocks + pg_begin + page] : -1;
+    wblk = (blk >= 0 && blk < a.num_blocks) ? blk : -1;
   }
 
   ScanState<RT> st;
@@ -408,28 +423,51 @@ __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a)
   }
   __syncthreads();
 
-  // pairs w, w+4, ... of the chunk, kStages of them in flight per wave
-  const int wu = __builtin_amdgcn_readfirstlane(w);
+  // Software pipeline over this wave's pairs k = 0..nmine-1 (chunk pair wu + 4k), kStages of them
+  // staged in LDS ahead: iteration k reads pair k+1's operands and refills its slot, then runs
+  // the scores of pair k+1 and the value accumulation of pair k (independent matrix-core work),
+  // then the softmax of pair k+1.
   const uint32_t stage_base = (uint32_t)(uintptr_t)&stage[wu][0][0][0];
+  auto blk_of = [&](int k, int P) { return __builtin_amdgcn_readlane(wblk, 2 * k + P); };
+  auto pg_of = [&](int k) { return pg_begin + 2 * (wu + kWavesM * k); };
 #pragma unroll
-  for (int k = 0; k < kStages; ++k) {
-    const int pr = wu + kWavesM * k;
-    if (pr < npairs) stage_pair(a, bt_lds, npages, h, pr, stage_base + k * 2 * kRecord, l);
-  }
-  for (int k = 0;; ++k) {
-    const int pr = wu + kWavesM * k;
-    if (pr >= npairs) break;
-    const int slot = k % kStages;
-    if (pr + kWavesM * (kStages - 1) < npairs)
+  for (int k = 0; k < kStages; ++k)
+    if (k < nmine) stage_pair(a, h, blk_of(k, 0), blk_of(k, 1), stage_base + k * 2 * kRecord, l);
+  PairLoads cur;
+  if (nmine > 0) {
+    if (kStages - 1 < nmine)
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6 * (kStages - 1)) : "memory");
     else
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    PairLoads cur;
-    read_pair(&stage[wu][slot][0][0], bt_lds, npages, pr, lo, hi, cur);
+    read_pair(&stage[wu][0][0][0], blk_of(0, 0) >= 0, blk_of(0, 1) >= 0, lo, hi, cur);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    const int nxt = pr + kWavesM * kStages;
-    if (nxt < npairs) stage_pair(a, bt_lds, npages, h, nxt, stage_base + slot * 2 * kRecord, l);
-    scan_pair<RT>(st, cur, pg_begin + 2 * pr, t1, lo, hi, p_lds[w], al_lds[w]);
+    if (kStages < nmine) stage_pair(a, h, blk_of(kStages, 0), blk_of(kStages, 1), stage_base, l);
+    float a2[2][RT];
+    qk_pair<RT>(st, cur, pg_of(0), t1, lo, a2);
+    softmax_pair<RT>(st, a2, lo, hi, p_lds[w][0], al_lds[w]);
+  }
+  for (int k = 0; k < nmine; ++k) {
+    const bool more = k + 1 < nmine;
+    PairLoads nxt;
+    if (more) {
+      const int slot = (k + 1) % kStages;
+      if (k + 1 + kStages - 1 < nmine)
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6 * (kStages - 1)) : "memory");
+      else
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      read_pair(&stage[wu][slot][0][0], blk_of(k + 1, 0) >= 0, blk_of(k + 1, 1) >= 0, lo, hi, nxt);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      const int refill = k + 1 + kStages;
+      if (refill < nmine) stage_pair(a, h, blk_of(refill, 0), blk_of(refill, 1), stage_base + slot * 2 * kRecord, l);
+    }
+    float a2[2][RT];
+    if (more) qk_pair<RT>(st, nxt, pg_of(k + 1), t1, lo, a2);
+    lds_sync_wave();
+    pv_pair<RT>(st, cur, lo, hi, p_lds[w][k & 1]);
+    if (more) {
+      softmax_pair<RT>(st, a2, lo, hi, p_lds[w][(k + 1) & 1], al_lds[w]);
+      cur = nxt;
+    }
   }
 
   // ---- wave state -> LDS
