@@ -57,6 +57,20 @@ CacheView view(const int2kv_cache* c) {
   return CacheView{static_cast<uint8_t*>(c->pool), c->num_blocks, c->num_kv_heads};
 }
 
+// Compute units of the current device (queried once per device; 256 when no device answers).
+int num_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    hipDeviceProp_t prop;
+    cached[dev] = hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0
+                      ? prop.multiProcessorCount
+                      : 256;
+  }
+  return cached[dev];
+}
+
 DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   DecodePlan p{};
   const int gq = Hq / H;
@@ -72,6 +86,9 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   if (p.variant == 2 && chunk > 4096) chunk = 4096;  // the matrix-core scan stages <= 256 pages
   p.chunk_tokens = chunk;
   p.n_chunks = max_ctx > 0 ? (max_ctx + chunk - 1) / chunk : 1;
+  // matrix-core scan: persistent work-groups of min(H, 8) waves, enough to fill every CU
+  const int nw = H < 8 ? H : 8;
+  p.grid_g = num_cus() * (8 / nw);
   p.wo_ksplit = d_model > 0 ? wo_ksplit(Hq * kHeadDim) : 0;
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   size_t off = 0;
@@ -79,8 +96,11 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   off = up(off + (size_t)B * Hq * kHeadDim * sizeof(float));
   p.off_qop = off;
   off = up(off + qop_bytes(B, H, gq));
+  p.off_prefix = off;
+  off = up(off + (size_t)(B + 1) * sizeof(int32_t));
   p.off_part = off;
-  off = up(off + (size_t)B * p.n_chunks * Hq * kPartStride * sizeof(float));
+  const size_t part_rows = p.variant == 2 ? (size_t)(p.grid_g + B) : (size_t)B * p.n_chunks;
+  off = up(off + part_rows * Hq * kPartStride * sizeof(float));
   p.off_o = off;
   if (d_model > 0) off = up(off + (size_t)B * Hq * kHeadDim * sizeof(float));
   p.off_wo = off;
@@ -213,6 +233,8 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
   a.part = reinterpret_cast<float*>(ws + plan.off_part);
   a.chunk_tokens = plan.chunk_tokens;
   a.n_chunks = plan.n_chunks;
+  a.prefix = reinterpret_cast<int32_t*>(ws + plan.off_prefix);
+  a.grid_g = plan.grid_g;
 
   hipError_t e = hipSuccess;
   if (plan.variant != 2) {
@@ -234,7 +256,7 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
   }
   const bool unrotate = !(W_o && wo_is_folded);
   float* heads = W_o ? reinterpret_cast<float*>(ws + plan.off_o) : out;
-  e = launch_merge(a, unrotate, heads, stream);
+  e = plan.variant == 2 ? launch_merge_flat(a, unrotate, heads, stream) : launch_merge(a, unrotate, heads, stream);
   if (e != hipSuccess) return hip_status(e, "decode/merge");
   if (W_o) {
     e = launch_wo_gemm(heads, W_o, out, reinterpret_cast<float*>(ws + plan.off_wo), batch,

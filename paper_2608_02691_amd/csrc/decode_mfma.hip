@@ -28,6 +28,9 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 constexpr float kLogit2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
 constexpr int kWavesM = 4;
 constexpr float kRescaleTau = 8.0f;  // lazy rescaling: keep the running max until exceeded by 2^8
+// Starting reference max: finite, so a segment whose tokens are all masked (-inf scores) still gives
+// p = exp2(-inf - m0) = 0 rather than NaN; any real score exceeds it by more than 2^tau.
+constexpr float kMaxInit = -1.0e30f;
 constexpr int kQopTile = 4096 + 256;  // A operands (4 instr x 64 lanes x 16 B) + constants
 
 bool mfma_decode_available() { return true; }
@@ -291,7 +294,7 @@ __device__ __forceinline__ void softmax_pair(ScanState<RT>& st, const float (&a2
     for (int r = 0; r < RT; ++r) {
       const float pm = row_max16(fmaxf(a2[0][r], a2[1][r]));
       const float mnew = pm > st.mref[r] + kRescaleTau ? pm : st.mref[r];
-      const float al = st.mref[r] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(st.mref[r] - mnew);
+      const float al = __builtin_amdgcn_exp2f(st.mref[r] - mnew);
       st.lsum[r] *= al;
       st.mref[r] = mnew;
       if (lo == 0) al_w[4 * r + hi] = al;
@@ -363,44 +366,63 @@ __device__ __forceinline__ void pv_pair(ScanState<RT>& st, const PairLoads& cur,
 #undef INT2KV_PV_TILE
 }
 
-constexpr int kMaxChunkPages = 256;
-constexpr int kStages = 4;  // page pairs staged (in flight) per wave
+constexpr int kStages = 3;       // page pairs staged (in flight) per wave
+constexpr int kWavesPerWG = 8;   // one wave per KV head of a head group
 
-template <int RT>
-__global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t stage[kWavesM][kStages][2][kRecord];
-  __shared__ _Float16 p_lds[kWavesM][2][2][8][kBlock];
-  __shared__ float al_lds[kWavesM][8];
-  __shared__ float wst[kWavesM][8][2];
-  __shared__ float wout[kWavesM][8][kHeadDim];
+typedef __attribute__((address_space(4))) const int32_t* cint_ptr;  // read through the scalar cache
 
-  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int L = seq_len_m(a, b);
-  const int t0 = chunk * a.chunk_tokens;
-  if (t0 >= L) return;
-  const int t1 = min(L, t0 + a.chunk_tokens);
-  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
-  const int gq = a.gq;
-  (void)kMaxChunkPages;
-
-  // pages of this chunk; wave w takes pairs w, w+4, ... (at most 32 pairs = 64 pages, one per lane)
-  const int pg_begin = t0 >> 4, pg_end = (t1 + kBlock - 1) >> 4;
-  const int npages = pg_end - pg_begin;
-  const int npairs = (npages + 1) >> 1;
-  const int wu = __builtin_amdgcn_readfirstlane(w);
-  const int nmine = wu < npairs ? (npairs - wu + kWavesM - 1) / kWavesM : 0;  // pairs of this wave
-  int wblk;  // lane i: block id of this wave's page i (pair i/2, page i%2), -1 if none
-  {
-    const int page = 2 * (wu + kWavesM * (l >> 1)) + (l & 1);
-    const int blk = page < npages ? a.block_table[(size_t)b * a.max_blocks + pg_begin + page] : -1;
-    wblk = (blk >= 0 && blk < a.num_blocks) ? blk : -1;
+// Pages of every sequence and their exclusive prefix sums (prefix[B] = total pages). One block.
+__global__ __launch_bounds__(1024) void page_prefix_kernel(DecodeArgs a) {
+  __shared__ int sums[1024];
+  const int tid = threadIdx.x;
+  const int per = (a.B + 1023) / 1024;
+  const int b0 = min(a.B, tid * per), b1 = min(a.B, b0 + per);
+  int s = 0;
+  for (int b = b0; b < b1; ++b) s += (seq_len_m(a, b) + kBlock - 1) >> 4;
+  sums[tid] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int v = tid >= off ? sums[tid - off] : 0;
+    __syncthreads();
+    sums[tid] += v;
+    __syncthreads();
   }
+  int run = tid > 0 ? sums[tid - 1] : 0;
+  for (int b = b0; b < b1; ++b) {
+    a.prefix[b] = run;
+    run += (seq_len_m(a, b) + kBlock - 1) >> 4;
+  }
+  if (tid == 1023) a.prefix[a.B] = sums[1023];
+}
 
-  ScanState<RT> st;
+// First page of work-group g's range when P pages are split evenly over G groups.
+__host__ __device__ __forceinline__ int range_lo(int g, int P, int G) { return (int)(((long long)g * P) / G); }
+
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// One wave: KV head h of sequence b, pages [p0, p1) of that sequence, with its partial (m, l, O')
+// per query head written to partial slot `slot`.
+template <int RT>
+__device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, int p0, int p1, int slot, int l,
+                                             uint8_t* stage_w, _Float16 (*p_w)[2][8][kBlock], float* al_w) {
+  const int lo = l & 15, hi = l >> 4;
+  const int L = seq_len_m(a, b);
+  const int npairs = (p1 - p0 + 1) >> 1;
+  const uint32_t stage_base = (uint32_t)(uintptr_t)stage_w;
+
+  // ---- query operands of (b, h): DMA into the staging area, then into registers
   const uint8_t* qop = a.qop + ((size_t)b * a.H + h) * RT * kQopTile;
 #pragma unroll
   for (int r = 0; r < RT; ++r) {
-    const uint8_t* t = qop + r * kQopTile;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(qop + r * kQopTile + i * 1024, 16 * l, stage_base + r * kQopTile + i * 1024);
+    dma4(qop + r * kQopTile + 4096, 4 * l, stage_base + r * kQopTile + 4096);
+  }
+  wait_vm_all();
+  ScanState<RT> st;
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    const uint8_t* t = stage_w + r * kQopTile;
 #pragma unroll
     for (int i = 0; i < 4; ++i) st.A[r][i] = *reinterpret_cast<const half8_t*>(t + (i * 64 + l) * 16);
     st.cinit[r] = *reinterpret_cast<const float4_t*>(t + 4096 + hi * 16);
@@ -410,73 +432,69 @@ __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a)
     for (int mt = 0; mt < 8; ++mt) st.acc[r][mt] = float4_t{0.f, 0.f, 0.f, 0.f};
     st.wacc[r] = 0.f;
     st.zacc[r] = 0.f;
-    st.mref[r] = -INFINITY;
+    st.mref[r] = kMaxInit;
     st.lsum[r] = 0.f;
   }
-  // Consume the operand loads here: the compiler counts only its own loads in vmcnt, so a wait
-  // for them placed inside the loop would also drain the staged DMA loads every iteration.
-#pragma unroll
-  for (int r = 0; r < RT; ++r) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) asm volatile("" ::"v"(st.A[r][i]));
-    asm volatile("" ::"v"(st.cinit[r]), "v"(st.sqL[r]), "v"(st.invsig[r]));
-  }
-  __syncthreads();
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 
-  // Software pipeline over this wave's pairs k = 0..nmine-1 (chunk pair wu + 4k), kStages of them
-  // staged in LDS ahead: iteration k reads pair k+1's operands and refills its slot, then runs
-  // the scores of pair k+1 and the value accumulation of pair k (independent matrix-core work),
-  // then the softmax of pair k+1.
-  const uint32_t stage_base = (uint32_t)(uintptr_t)&stage[wu][0][0][0];
-  auto blk_of = [&](int k, int P) { return __builtin_amdgcn_readlane(wblk, 2 * k + P); };
-  auto pg_of = [&](int k) { return pg_begin + 2 * (wu + kWavesM * k); };
+  // ---- pipeline over the segment's page pairs (pages p0 + 2k, p0 + 2k + 1)
+  const cint_ptr bt = (cint_ptr)(uintptr_t)(a.block_table + (size_t)b * a.max_blocks);
+  auto blk_of = [&](int k, int P) -> int {
+    const int page = p0 + 2 * k + P;
+    if (page >= p1) return -1;
+    const int blk = bt[page];
+    return (blk >= 0 && blk < a.num_blocks) ? blk : -1;
+  };
 #pragma unroll
   for (int k = 0; k < kStages; ++k)
-    if (k < nmine) stage_pair(a, h, blk_of(k, 0), blk_of(k, 1), stage_base + k * 2 * kRecord, l);
+    if (k < npairs) stage_pair(a, h, blk_of(k, 0), blk_of(k, 1), stage_base + k * 2 * kRecord, l);
   PairLoads cur;
-  if (nmine > 0) {
-    if (kStages - 1 < nmine)
+  {
+    if (kStages - 1 < npairs)
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6 * (kStages - 1)) : "memory");
     else
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    read_pair(&stage[wu][0][0][0], blk_of(0, 0) >= 0, blk_of(0, 1) >= 0, lo, hi, cur);
+      wait_vm_all();
+    read_pair(stage_w, blk_of(0, 0) >= 0, blk_of(0, 1) >= 0, lo, hi, cur);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    if (kStages < nmine) stage_pair(a, h, blk_of(kStages, 0), blk_of(kStages, 1), stage_base, l);
+    if (kStages < npairs) stage_pair(a, h, blk_of(kStages, 0), blk_of(kStages, 1), stage_base, l);
     float a2[2][RT];
-    qk_pair<RT>(st, cur, pg_of(0), t1, lo, a2);
-    softmax_pair<RT>(st, a2, lo, hi, p_lds[w][0], al_lds[w]);
+    qk_pair<RT>(st, cur, p0, L, lo, a2);
+    softmax_pair<RT>(st, a2, lo, hi, p_w[0], al_w);
   }
-  for (int k = 0; k < nmine; ++k) {
-    const bool more = k + 1 < nmine;
+  for (int k = 0; k < npairs; ++k) {
+    const bool more = k + 1 < npairs;
     PairLoads nxt;
     if (more) {
-      const int slot = (k + 1) % kStages;
-      if (k + 1 + kStages - 1 < nmine)
+      const int sl = (k + 1) % kStages;
+      if (k + 1 + kStages - 1 < npairs)
         asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6 * (kStages - 1)) : "memory");
       else
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      read_pair(&stage[wu][slot][0][0], blk_of(k + 1, 0) >= 0, blk_of(k + 1, 1) >= 0, lo, hi, nxt);
+        wait_vm_all();
+      read_pair(stage_w + sl * 2 * kRecord, blk_of(k + 1, 0) >= 0, blk_of(k + 1, 1) >= 0, lo, hi, nxt);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       const int refill = k + 1 + kStages;
-      if (refill < nmine) stage_pair(a, h, blk_of(refill, 0), blk_of(refill, 1), stage_base + slot * 2 * kRecord, l);
+      if (refill < npairs) stage_pair(a, h, blk_of(refill, 0), blk_of(refill, 1), stage_base + sl * 2 * kRecord, l);
     }
     float a2[2][RT];
-    if (more) qk_pair<RT>(st, nxt, pg_of(k + 1), t1, lo, a2);
+    if (more) qk_pair<RT>(st, nxt, p0 + 2 * (k + 1), L, lo, a2);
     lds_sync_wave();
-    pv_pair<RT>(st, cur, lo, hi, p_lds[w][k & 1]);
+    pv_pair<RT>(st, cur, lo, hi, p_w[k & 1]);
     if (more) {
-      softmax_pair<RT>(st, a2, lo, hi, p_lds[w][(k + 1) & 1], al_lds[w]);
+      softmax_pair<RT>(st, a2, lo, hi, p_w[(k + 1) & 1], al_w);
       cur = nxt;
     }
   }
 
-  // ---- wave state -> LDS
+  // ---- partial (m, l, O') of every query head of this KV head
+  const int gq = a.gq;
+  float* part = a.part + ((size_t)slot * a.Hq + h * gq) * kPartStride;
 #pragma unroll
   for (int r = 0; r < RT; ++r) {
     const float ls = row_sum16(st.lsum[r]);
-    if (lo == 0) {
-      wst[w][4 * r + hi][0] = st.mref[r];
-      wst[w][4 * r + hi][1] = ls;
+    if (lo == 0 && 4 * r + hi < gq) {
+      float* dst = part + (size_t)(4 * r + hi) * kPartStride;
+      dst[0] = st.mref[r];
+      dst[1] = ls;
     }
     float wa = st.wacc[r], za = st.zacc[r];
     wa += __shfl_xor(wa, 16);
@@ -484,11 +502,16 @@ __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a)
     za += __shfl_xor(za, 16);
     za += __shfl_xor(za, 32);
     const int jc = 4 * r + (lo >> 2);
-#define INT2KV_OUT_TILE(MT)                                                              \
-  if ((lo & 3) == ((MT) >> 1)) {                                                         \
-    const float sc = (float)(1 << land_e(MT));                                           \
-    _Pragma("unroll") for (int e = 0; e < 4; ++e)                                        \
-      wout[w][jc][16 * (MT) + 4 * hi + e] = fmaf(sc, st.acc[r][MT][e] - wa, za);         \
+    float* dst = part + (size_t)jc * kPartStride + 4;
+#define INT2KV_OUT_TILE(MT)                                                                         \
+  if ((lo & 3) == ((MT) >> 1) && jc < gq) {                                                         \
+    const float sc = (float)(1 << land_e(MT));                                                      \
+    float4 o;                                                                                       \
+    o.x = fmaf(sc, st.acc[r][MT][0] - wa, za);                                                      \
+    o.y = fmaf(sc, st.acc[r][MT][1] - wa, za);                                                      \
+    o.z = fmaf(sc, st.acc[r][MT][2] - wa, za);                                                      \
+    o.w = fmaf(sc, st.acc[r][MT][3] - wa, za);                                                      \
+    *reinterpret_cast<float4*>(dst + 16 * (MT) + 4 * hi) = o;                                      \
   }
     INT2KV_OUT_TILE(0)
     INT2KV_OUT_TILE(1)
@@ -500,33 +523,106 @@ __global__ __launch_bounds__(256, 2) void decode_split_mfma_kernel(DecodeArgs a)
     INT2KV_OUT_TILE(7)
 #undef INT2KV_OUT_TILE
   }
-  __syncthreads();
+  wait_vm_all();
+}
 
-  // ---- merge the four waves, write this chunk's partial (m, l, O') per query head
-  for (int i = tid; i < gq * kHeadDim; i += blockDim.x) {
-    const int j = i / kHeadDim, c = i % kHeadDim;
+// Persistent, head-grouped scan: work-group g covers pages [lo(g), lo(g+1)) of the concatenation
+// of all sequences (even split, so every group streams the same number of page records); wave w
+// handles KV head 8*blockIdx.y + w of those pages, so the eight waves read the adjacent records
+// of one block together. A range crossing sequence boundaries is scanned segment by segment; the
+// partial of (group g, sequence b) goes to slot g + b, which is unique because the (g, b) pairs
+// that meet form a monotone staircase.
+template <int RT>
+__global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t stage[kWavesPerWG][kStages][2][kRecord];
+  __shared__ _Float16 p_lds[kWavesPerWG][2][2][8][kBlock];
+  __shared__ float al_lds[kWavesPerWG][8];
+  static_assert(2 * kRecord * kStages >= 2 * kQopTile, "query operands are staged through the page slots");
+
+  const int g = blockIdx.x, G = gridDim.x;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
+  const int h = blockIdx.y * kWavesPerWG + w;
+  if (h >= a.H) return;
+  const cint_ptr prefix = (cint_ptr)(uintptr_t)(a.prefix);
+  const int P = prefix[a.B];
+  const int s = range_lo(g, P, G), e = range_lo(g + 1, P, G);
+  if (s >= e) return;
+  int b = 0, bh = a.B;  // prefix[b] <= s < prefix[bh]
+  while (bh - b > 1) {
+    const int mid = (b + bh) >> 1;
+    if (prefix[mid] <= s) b = mid;
+    else bh = mid;
+  }
+  for (int pos = s; pos < e; ++b) {
+    const int Sb = prefix[b], Sb1 = prefix[b + 1];
+    if (Sb1 <= pos) continue;
+    const int seg_end = min(e, Sb1);
+    scan_segment<RT>(a, b, h, pos - Sb, seg_end - Sb, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w]);
+    pos = seg_end;
+  }
+}
+
+// Merge the partials of each (sequence, query head) over the work-groups whose ranges met the
+// sequence, then undo the value rotation (o = o' R_V^T, unless W_O arrives pre-folded).
+// Block (sequence, KV head), thread c = channel.
+__global__ __launch_bounds__(128) void merge_flat_kernel(DecodeArgs a, int G, int unrotate, float* __restrict__ out) {
+  __shared__ float os[kHeadDim];
+  const int b = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+  const int P = a.prefix[a.B];
+  const int Sb = a.prefix[b], Sb1 = a.prefix[b + 1];
+  int ga = 0, gb = -1;
+  if (Sb1 > Sb && P > 0) {
+    // groups whose ranges contain the first and the last page of the sequence
+    ga = (int)(((long long)Sb * G) / P);
+    while (ga > 0 && range_lo(ga, P, G) > Sb) --ga;
+    while (range_lo(ga + 1, P, G) <= Sb) ++ga;
+    gb = (int)(((long long)(Sb1 - 1) * G) / P);
+    while (gb > 0 && range_lo(gb, P, G) > Sb1 - 1) --gb;
+    while (range_lo(gb + 1, P, G) <= Sb1 - 1) ++gb;
+  }
+  const float* Rv = a.R_v + (size_t)h * kHeadDim * kHeadDim;
+  for (int jj = 0; jj < a.gq; ++jj) {
+    const int j = h * a.gq + jj;
     float M = -INFINITY;
-#pragma unroll
-    for (int ww = 0; ww < kWavesM; ++ww) M = fmaxf(M, wst[ww][j][0]);
-    float ls = 0.0f, os = 0.0f;
-#pragma unroll
-    for (int ww = 0; ww < kWavesM; ++ww) {
-      const float mw = wst[ww][j][0];
-      const float f = mw == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mw - M);
-      ls = fmaf(f, wst[ww][j][1], ls);
-      os = fmaf(f, wout[ww][j][c], os);
+    for (int gg = ga; gg <= gb; ++gg) {
+      if (range_lo(gg, P, G) >= range_lo(gg + 1, P, G)) continue;  // empty range wrote nothing
+      M = fmaxf(M, a.part[((size_t)(gg + b) * a.Hq + j) * kPartStride]);
     }
-    float* dst = a.part + (((size_t)b * a.n_chunks + chunk) * a.Hq + h * gq + j) * kPartStride;
-    if (c == 0) {
-      dst[0] = M;
-      dst[1] = ls;
+    float lsum = 0.0f, osum = 0.0f;
+    for (int gg = ga; gg <= gb; ++gg) {
+      if (range_lo(gg, P, G) >= range_lo(gg + 1, P, G)) continue;
+      const float* pp = a.part + ((size_t)(gg + b) * a.Hq + j) * kPartStride;
+      const float f = pp[0] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(pp[0] - M);
+      lsum = fmaf(f, pp[1], lsum);
+      osum = fmaf(f, pp[4 + c], osum);
     }
-    dst[4 + c] = os;
+    const float val = lsum > 0.0f ? osum / lsum : 0.0f;
+    float res = val;
+    if (unrotate) {
+      os[c] = val;
+      __syncthreads();
+      const float4* row = reinterpret_cast<const float4*>(Rv + (size_t)c * kHeadDim);
+      float acc = 0.0f;
+#pragma unroll 8
+      for (int i = 0; i < kHeadDim / 4; ++i) {
+        const float4 rr = row[i];
+        acc = fmaf(os[4 * i], rr.x, acc);
+        acc = fmaf(os[4 * i + 1], rr.y, acc);
+        acc = fmaf(os[4 * i + 2], rr.z, acc);
+        acc = fmaf(os[4 * i + 3], rr.w, acc);
+      }
+      res = acc;
+      __syncthreads();
+    }
+    out[((size_t)b * a.Hq + j) * kHeadDim + c] = res;
   }
 }
 
 hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
   if (a.gq > 8) return hipErrorNotSupported;
+  hipLaunchKernelGGL(page_prefix_kernel, dim3(1), dim3(1024), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(qprep_kernel, dim3(a.B * a.H), dim3(256), 0, s, a, (a.gq + 3) / 4);
   return hipGetLastError();
 }
@@ -534,11 +630,17 @@ hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
 hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s) {
   if (a.gq > 8) return hipErrorNotSupported;
   const int rt = (a.gq + 3) / 4;
-  dim3 grid(a.n_chunks, a.H, a.B);
+  dim3 grid(a.grid_g, (a.H + kWavesPerWG - 1) / kWavesPerWG);
+  const int threads = 64 * min(a.H, kWavesPerWG);
   if (rt == 1)
-    hipLaunchKernelGGL(decode_split_mfma_kernel<1>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(decode_scan_flat_kernel<1>, grid, dim3(threads), 0, s, a);
   else
-    hipLaunchKernelGGL(decode_split_mfma_kernel<2>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(decode_scan_flat_kernel<2>, grid, dim3(threads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(merge_flat_kernel, dim3(a.B, a.H), dim3(128), 0, s, a, a.grid_g, unrotate ? 1 : 0, out);
   return hipGetLastError();
 }
 

@@ -32,7 +32,8 @@ struct DecodePlan {
   int n_chunks;
   int variant;        // 1 = vector ALU, 2 = matrix core
   int wo_ksplit;
-  size_t off_qrot, off_qop, off_part, off_o, off_wo, total;
+  int grid_g;         // work-groups of the matrix-core scan
+  size_t off_qrot, off_qop, off_prefix, off_part, off_o, off_wo, total;
 };
 
 struct DecodeArgs {
@@ -48,8 +49,10 @@ struct DecodeArgs {
   const float* R_v;
   float* qrot;     // [B, Hq, 128] fp32
   uint8_t* qop;    // matrix-core query operands
-  float* part;     // [B, n_chunks, Hq, kPartStride]
+  float* part;     // vector-ALU scan: [B, n_chunks, Hq, kPartStride]; matrix-core scan: [G + B, Hq, kPartStride]
   int chunk_tokens, n_chunks;
+  int32_t* prefix; // [B + 1] page prefix sums (matrix-core scan)
+  int grid_g;      // work-groups of the matrix-core scan
 };
 
 constexpr int kPartStride = 132;  // m, l, 2 pad, O[128]
@@ -60,6 +63,7 @@ hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s);
 size_t qop_bytes(int B, int H, int gq);
 hipError_t launch_merge(const DecodeArgs& a, bool unrotate, float* out, hipStream_t s);
+hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, hipStream_t s);
 hipError_t launch_wo_gemm(const float* o, const uint16_t* W, float* y, float* partial, int B, int K,
                           int N, int ksplit, hipStream_t s);
 
