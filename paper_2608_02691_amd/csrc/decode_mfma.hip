@@ -233,7 +233,9 @@ struct ScanState {
   float4_t cinit[RT], sqL[RT];
   float invsig[RT];
   float4_t acc[RT][8];
-  float wacc[RT], zacc[RT], mref[RT], lsum[RT];
+  float4_t wsum[RT];  // sum_t w_t per (j, g) column (every row)
+  float4_t zl[RT];    // rows 0..3: sum_t p_t z_tg (row = group); rows 4..7: sum_t p_t
+  float mref[RT];
 };
 
 // Scores of one page pair (2 pages x RT row tiles), base-2 logits, -inf where masked. The four
@@ -274,7 +276,7 @@ __device__ __forceinline__ void qk_pair(const ScanState<RT>& st, const PairLoads
       zq = fmaf((float)m1.y, st.sqL[r][1], zq);
       zq = fmaf((float)m2.y, st.sqL[r][2], zq);
       zq = fmaf((float)m3.y, st.sqL[r][3], zq);
-      a2[P][r] = tv ? fmaf(sd, st.invsig[r], zq) : -INFINITY;
+      a2[P][r] = fmaf(sd, st.invsig[r], zq) + (tv ? 0.0f : -INFINITY);
     }
   }
 }
@@ -295,7 +297,6 @@ __device__ __forceinline__ void softmax_pair(ScanState<RT>& st, const float (&a2
       const float pm = row_max16(fmaxf(a2[0][r], a2[1][r]));
       const float mnew = pm > st.mref[r] + kRescaleTau ? pm : st.mref[r];
       const float al = __builtin_amdgcn_exp2f(st.mref[r] - mnew);
-      st.lsum[r] *= al;
       st.mref[r] = mnew;
       if (lo == 0) al_w[4 * r + hi] = al;
     }
@@ -305,8 +306,8 @@ __device__ __forceinline__ void softmax_pair(ScanState<RT>& st, const float (&a2
       const float alc = al_w[4 * r + (lo >> 2)];
 #pragma unroll
       for (int mt = 0; mt < 8; ++mt) st.acc[r][mt] *= alc;
-      st.wacc[r] *= alc;
-      st.zacc[r] *= alc;
+      st.wsum[r] *= alc;
+      st.zl[r] *= alc;
     }
   }
 #pragma unroll
@@ -314,7 +315,6 @@ __device__ __forceinline__ void softmax_pair(ScanState<RT>& st, const float (&a2
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
       const float p = __builtin_amdgcn_exp2f(a2[P][r] - st.mref[r]);
-      st.lsum[r] += p;
       p_w[P][4 * r + hi][lo] = (_Float16)p;
     }
   }
@@ -325,30 +325,29 @@ __device__ __forceinline__ void softmax_pair(ScanState<RT>& st, const float (&a2
 template <int RT>
 __device__ __forceinline__ void pv_pair(ScanState<RT>& st, const PairLoads& cur, int lo, int hi,
                                         const _Float16 (*p_w)[8][kBlock]) {
-  const half2_t ones = half2_t{(_Float16)1.0f, (_Float16)1.0f};
+  // A operand of the (Z, l) contraction: rows 0..3 hold z of group `row` (the V zeros this lane
+  // already has, group lo & 3 = row), rows 4..7 hold 1.0, rows 8..15 zero
+  const half2_t zmul = lo < 4 ? half2_t{(_Float16)1.0f, (_Float16)1.0f} : half2_t{(_Float16)0.0f, (_Float16)0.0f};
+  const half2_t zadd = (lo >= 4 && lo < 8) ? half2_t{(_Float16)1.0f, (_Float16)1.0f}
+                                           : half2_t{(_Float16)0.0f, (_Float16)0.0f};
+  const half8_t Azl = __builtin_bit_cast(
+      half8_t, u32x4_t{as_u(as_h2(cur.vz[0].x) * zmul + zadd), as_u(as_h2(cur.vz[0].y) * zmul + zadd),
+                       as_u(as_h2(cur.vz[1].x) * zmul + zadd), as_u(as_h2(cur.vz[1].y) * zmul + zadd)});
+  const half8_t Aones = __builtin_bit_cast(half8_t, u32x4_t{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u});
   half8_t Bw[RT];
 #pragma unroll
   for (int r = 0; r < RT; ++r) {
     const int jc = 4 * r + (lo >> 2);
     const uint2 pp0 = *reinterpret_cast<const uint2*>(&p_w[0][jc][4 * hi]);
     const uint2 pp1 = *reinterpret_cast<const uint2*>(&p_w[1][jc][4 * hi]);
+    const half8_t Bp = __builtin_bit_cast(half8_t, u32x4_t{pp0.x, pp0.y, pp1.x, pp1.y});
     const half2_t w00 = as_h2(pp0.x) * as_h2(cur.vs[0].x);
     const half2_t w01 = as_h2(pp0.y) * as_h2(cur.vs[0].y);
     const half2_t w10 = as_h2(pp1.x) * as_h2(cur.vs[1].x);
     const half2_t w11 = as_h2(pp1.y) * as_h2(cur.vs[1].y);
     Bw[r] = __builtin_bit_cast(half8_t, u32x4_t{as_u(w00), as_u(w01), as_u(w10), as_u(w11)});
-    float wa = st.wacc[r];
-    wa = __builtin_amdgcn_fdot2(w00, ones, wa, false);
-    wa = __builtin_amdgcn_fdot2(w01, ones, wa, false);
-    wa = __builtin_amdgcn_fdot2(w10, ones, wa, false);
-    wa = __builtin_amdgcn_fdot2(w11, ones, wa, false);
-    st.wacc[r] = wa;
-    float za = st.zacc[r];
-    za = __builtin_amdgcn_fdot2(as_h2(pp0.x), as_h2(cur.vz[0].x), za, false);
-    za = __builtin_amdgcn_fdot2(as_h2(pp0.y), as_h2(cur.vz[0].y), za, false);
-    za = __builtin_amdgcn_fdot2(as_h2(pp1.x), as_h2(cur.vz[1].x), za, false);
-    za = __builtin_amdgcn_fdot2(as_h2(pp1.y), as_h2(cur.vz[1].y), za, false);
-    st.zacc[r] = za;
+    st.wsum[r] = mfma16(Aones, Bw[r], st.wsum[r]);
+    st.zl[r] = mfma16(Azl, Bp, st.zl[r]);
   }
 #define INT2KV_PV_TILE(MT)                                                                   \
   {                                                                                          \
@@ -430,10 +429,9 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
     st.invsig[r] = *reinterpret_cast<const float*>(t + 4096 + 128 + hi * 4);
 #pragma unroll
     for (int mt = 0; mt < 8; ++mt) st.acc[r][mt] = float4_t{0.f, 0.f, 0.f, 0.f};
-    st.wacc[r] = 0.f;
-    st.zacc[r] = 0.f;
+    st.wsum[r] = float4_t{0.f, 0.f, 0.f, 0.f};
+    st.zl[r] = float4_t{0.f, 0.f, 0.f, 0.f};
     st.mref[r] = kMaxInit;
-    st.lsum[r] = 0.f;
   }
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 
@@ -490,17 +488,18 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   float* part = a.part + ((size_t)slot * a.Hq + h * gq) * kPartStride;
 #pragma unroll
   for (int r = 0; r < RT; ++r) {
-    const float ls = row_sum16(st.lsum[r]);
+    // column (j, g) = lo of tile r: W from any row; Z[j][g] from lane (lo, hi = 0), register g;
+    // l[j] from lane (4 (j - 4r), hi = 1), register 0
+    const float wa = st.wsum[r][0];
+    const int g = lo & 3;
+    const float zown = g == 0 ? st.zl[r][0] : g == 1 ? st.zl[r][1] : g == 2 ? st.zl[r][2] : st.zl[r][3];
+    const float za = __shfl(zown, lo);
+    const float ls = __shfl(st.zl[r][0], 16 + 4 * hi);  // l of row j = 4r + hi
     if (lo == 0 && 4 * r + hi < gq) {
       float* dst = part + (size_t)(4 * r + hi) * kPartStride;
       dst[0] = st.mref[r];
       dst[1] = ls;
     }
-    float wa = st.wacc[r], za = st.zacc[r];
-    wa += __shfl_xor(wa, 16);
-    wa += __shfl_xor(wa, 32);
-    za += __shfl_xor(za, 16);
-    za += __shfl_xor(za, 32);
     const int jc = 4 * r + (lo >> 2);
     float* dst = part + (size_t)jc * kPartStride + 4;
 #define INT2KV_OUT_TILE(MT)                                                                         \
