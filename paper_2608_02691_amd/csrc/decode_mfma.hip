@@ -181,18 +181,35 @@ __device__ __forceinline__ void dma4(const uint8_t* base, uint32_t voff, uint32_
                : "memory", "m0");
 }
 
-// Issue the 6 DMA loads of one page pair into a staging slot (2 x 1536 B at lds_slot). blk0/blk1
-// are wave-uniform block ids (-1: no page; block 0 is read instead and the pair is masked later).
-__device__ __forceinline__ void stage_pair(const DecodeArgs& a, int h, int blk0, int blk1, uint32_t lds_slot, int l) {
+// DMA of one 1536-byte page record into LDS at lds_addr: the 1024 bytes of codes with one dwordx4
+// load, the two 256-byte metadata blocks with dword loads. The instruction offset moves both the
+// global and the LDS address, so one M0 value serves the whole record.
+__device__ __forceinline__ void dma_page(const uint8_t* rec, uint32_t lds_addr, int l) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %3\n\t"
+      "global_load_lds_dword %2, %3 offset:1024\n\t"
+      "global_load_lds_dword %2, %3 offset:1280" ::"s"(lds_addr),
+      "v"(16 * l), "v"(4 * l), "s"(rec)
+      : "memory", "m0");
+}
+
+// Stage page pair k of a segment (pages p0 + 2k, p0 + 2k + 1 of sequence row `bt`) into slot
+// `slot`; returns the two validity bits (page inside the segment and block id inside the pool).
+__device__ __forceinline__ uint32_t stage_pair(const DecodeArgs& a, const int32_t __attribute__((address_space(4)))* bt,
+                                               int h, int p0, int p1, int k, uint32_t slot_addr, int l) {
+  uint32_t okbits = 0;
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
-    const int blk = P == 0 ? blk0 : blk1;
-    const uint8_t* rec = a.pool + (blk >= 0 ? ((size_t)blk * a.H + h) * kRecord : 0);
-    const uint32_t dst = lds_slot + P * kRecord;
-    dma16(rec, 16 * l, dst);
-    dma4(rec + kOffKMeta, 4 * l, dst + kOffKMeta);
-    dma4(rec + kOffVScale, 4 * l, dst + kOffVScale);
+    const int page = p0 + 2 * k + P;
+    const int blk = page < p1 ? bt[page] : -1;
+    const bool ok = (uint32_t)blk < (uint32_t)a.num_blocks;
+    const uint8_t* rec = a.pool + (ok ? ((size_t)(blk * a.H + h)) * kRecord : 0);
+    dma_page(rec, slot_addr + P * kRecord, l);
+    okbits |= (ok ? 1u : 0u) << P;
   }
+  return okbits;
 }
 
 // Operands of one page pair read back from its staging slot.
@@ -436,42 +453,42 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 
   // ---- pipeline over the segment's page pairs (pages p0 + 2k, p0 + 2k + 1)
-  const cint_ptr bt = (cint_ptr)(uintptr_t)(a.block_table + (size_t)b * a.max_blocks);
-  auto blk_of = [&](int k, int P) -> int {
-    const int page = p0 + 2 * k + P;
-    if (page >= p1) return -1;
-    const int blk = bt[page];
-    return (blk >= 0 && blk < a.num_blocks) ? blk : -1;
-  };
+  const int32_t __attribute__((address_space(4)))* bt =
+      (const int32_t __attribute__((address_space(4)))*)(uintptr_t)(a.block_table + (size_t)b * a.max_blocks);
+  uint32_t okmask = 0;  // bits 2*slot, 2*slot+1: validity of the two pages staged in slot
 #pragma unroll
   for (int k = 0; k < kStages; ++k)
-    if (k < npairs) stage_pair(a, h, blk_of(k, 0), blk_of(k, 1), stage_base + k * 2 * kRecord, l);
+    if (k < npairs) okmask |= stage_pair(a, bt, h, p0, p1, k, stage_base + k * 2 * kRecord, l) << (2 * k);
   PairLoads cur;
   {
     if (kStages - 1 < npairs)
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6 * (kStages - 1)) : "memory");
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * 2 * (kStages - 1)) : "memory");
     else
       wait_vm_all();
-    read_pair(stage_w, blk_of(0, 0) >= 0, blk_of(0, 1) >= 0, lo, hi, cur);
+    read_pair(stage_w, okmask & 1u, (okmask >> 1) & 1u, lo, hi, cur);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    if (kStages < npairs) stage_pair(a, h, blk_of(kStages, 0), blk_of(kStages, 1), stage_base, l);
+    if (kStages < npairs)
+      okmask = (okmask & ~3u) | stage_pair(a, bt, h, p0, p1, kStages, stage_base, l);
     float a2[2][RT];
     qk_pair<RT>(st, cur, p0, L, lo, a2);
     softmax_pair<RT>(st, a2, lo, hi, p_w[0], al_w);
   }
+  int sl = 0;  // slot of pair k
   for (int k = 0; k < npairs; ++k) {
     const bool more = k + 1 < npairs;
+    sl = sl + 1 == kStages ? 0 : sl + 1;  // slot of pair k + 1
     PairLoads nxt;
     if (more) {
-      const int sl = (k + 1) % kStages;
       if (k + 1 + kStages - 1 < npairs)
-        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6 * (kStages - 1)) : "memory");
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * 2 * (kStages - 1)) : "memory");
       else
         wait_vm_all();
-      read_pair(stage_w + sl * 2 * kRecord, blk_of(k + 1, 0) >= 0, blk_of(k + 1, 1) >= 0, lo, hi, nxt);
+      read_pair(stage_w + sl * 2 * kRecord, (okmask >> (2 * sl)) & 1u, (okmask >> (2 * sl + 1)) & 1u, lo, hi, nxt);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       const int refill = k + 1 + kStages;
-      if (refill < npairs) stage_pair(a, h, blk_of(refill, 0), blk_of(refill, 1), stage_base + sl * 2 * kRecord, l);
+      if (refill < npairs)
+        okmask = (okmask & ~(3u << (2 * sl))) |
+                 (stage_pair(a, bt, h, p0, p1, refill, stage_base + sl * 2 * kRecord, l) << (2 * sl));
     }
     float a2[2][RT];
     if (more) qk_pair<RT>(st, nxt, p0 + 2 * (k + 1), L, lo, a2);
