@@ -98,6 +98,8 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   off = up(off + qop_bytes(B, H, gq));
   p.off_prefix = off;
   off = up(off + (size_t)(B + 1) * sizeof(int32_t));
+  p.off_wginfo = off;
+  off = up(off + (size_t)p.grid_g * 4 * sizeof(int32_t));
   p.off_part = off;
   const size_t part_rows = p.variant == 2 ? (size_t)(p.grid_g + B) : (size_t)B * p.n_chunks;
   off = up(off + part_rows * Hq * kPartStride * sizeof(float));
@@ -234,6 +236,7 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
   a.chunk_tokens = plan.chunk_tokens;
   a.n_chunks = plan.n_chunks;
   a.prefix = reinterpret_cast<int32_t*>(ws + plan.off_prefix);
+  a.wg_info = reinterpret_cast<int32_t*>(ws + plan.off_wginfo);
   a.grid_g = plan.grid_g;
 
   hipError_t e = hipSuccess;

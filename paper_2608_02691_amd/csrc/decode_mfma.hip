@@ -195,24 +195,45 @@ __device__ __forceinline__ void dma_page(const uint8_t* rec, uint32_t lds_addr, 
       : "memory", "m0");
 }
 
-// Stage page pair k of a segment (pages p0 + 2k, p0 + 2k + 1 of sequence row `bt`) into slot
-// `slot`; returns the two validity bits (page inside the segment and block id inside the pool).
-__device__ __forceinline__ uint32_t stage_pair(const DecodeArgs& a, const int32_t __attribute__((address_space(4)))* bt,
-                                               int h, int p0, int p1, int k, uint32_t slot_addr, int l) {
-  uint32_t okbits = 0;
-#pragma unroll
-  for (int P = 0; P < 2; ++P) {
-    const int page = p0 + 2 * k + P;
-    const int blk = page < p1 ? bt[page] : -1;
-    const bool ok = (uint32_t)blk < (uint32_t)a.num_blocks;
-    const uint8_t* rec = a.pool + (ok ? ((size_t)(blk * a.H + h)) * kRecord : 0);
-    dma_page(rec, slot_addr + P * kRecord, l);
-    okbits |= (ok ? 1u : 0u) << P;
-  }
-  return okbits;
+typedef const int32_t __attribute__((address_space(4)))* bt_ptr;
+
+struct BlockIds {
+  int b0, b1;
+};
+
+// Block ids of pages page0 and page0 + 1 of a sequence row `bt` (indexes clamped to the last page
+// p1 - 1 of the segment, so the reads stay inside the row).
+__device__ __forceinline__ BlockIds load_ids(bt_ptr bt, int page0, int p1) {
+  const int last = p1 - 1;
+  return {bt[page0 < last ? page0 : last], bt[page0 + 1 < last ? page0 + 1 : last]};
+}
+
+// Stage the page pair (page0, page0 + 1) with block ids `id` into the slot at slot_addr; returns
+// the two validity bits (page inside the segment and block id inside the pool). Invalid pages
+// stage the pool's first record instead (read, then ignored). base_h = pool + h * 1536,
+// stride = H * 1536.
+__device__ __forceinline__ uint32_t stage_pair(const uint8_t* pool, const uint8_t* base_h, uint32_t stride,
+                                               uint32_t nblk, BlockIds id, int page0, int p1,
+                                               uint32_t slot_addr, int l) {
+  const bool ok0 = page0 < p1 && (uint32_t)id.b0 < nblk;
+  const bool ok1 = page0 + 1 < p1 && (uint32_t)id.b1 < nblk;
+  dma_page(ok0 ? base_h + (size_t)(uint32_t)id.b0 * stride : pool, slot_addr, l);
+  dma_page(ok1 ? base_h + (size_t)(uint32_t)id.b1 * stride : pool, slot_addr + kRecord, l);
+  return (ok0 ? 1u : 0u) | (ok1 ? 2u : 0u);
 }
 
 // Operands of one page pair read back from its staging slot.
+// An empty asm that uses every register read_pair filled: the compiler places its wait for those
+// LDS reads here, ahead of the scalar block-id loads that follow (a later wait would have to
+// wait for those loads too, since scalar loads return out of order).
+__device__ __forceinline__ void pin_pair(PairLoads& p) {
+#pragma unroll
+  for (int P = 0; P < 2; ++P) {
+    asm volatile("" : "+v"(p.kc[P].x), "+v"(p.kc[P].y), "+v"(p.vc[P].x), "+v"(p.vc[P].y));
+    asm volatile("" : "+v"(p.km[P].x), "+v"(p.km[P].y), "+v"(p.km[P].z), "+v"(p.km[P].w));
+    asm volatile("" : "+v"(p.vs[P].x), "+v"(p.vs[P].y), "+v"(p.vz[P].x), "+v"(p.vz[P].y));
+  }
+}
 __device__ __forceinline__ void read_pair(const uint8_t* slot, bool ok0, bool ok1, int lo, int hi, PairLoads& p) {
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
@@ -222,10 +243,17 @@ __device__ __forceinline__ void read_pair(const uint8_t* slot, bool ok0, bool ok
     p.kc[P] = *reinterpret_cast<const uint2*>(rec + kOffKCodes + 32 * lo + 8 * hi);
     p.km[P] = *reinterpret_cast<const uint4*>(rec + kOffKMeta + 16 * lo);
     p.vc[P] = *reinterpret_cast<const uint2*>(rec + kOffVCodes + 32 * lo + 8 * hi);
-    const uint2 s = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (lo & 3) + 8 * hi);
-    const uint2 z = *reinterpret_cast<const uint2*>(rec + kOffVZero + 32 * (lo & 3) + 8 * hi);
-    p.vs[P] = ok ? s : make_uint2(0u, 0u);
-    p.vz[P] = ok ? z : make_uint2(0u, 0u);
+    p.vs[P] = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (lo & 3) + 8 * hi);
+    p.vz[P] = *reinterpret_cast<const uint2*>(rec + kOffVZero + 32 * (lo & 3) + 8 * hi);
+  }
+}
+// Zero the value scales and zeros of a page that holds no cached tokens (its staged record is a
+// stand-in), after pin_pair so that the selects do not pull the LDS wait forward.
+__device__ __forceinline__ void mask_pair(PairLoads& p) {
+#pragma unroll
+  for (int P = 0; P < 2; ++P) {
+    p.vs[P] = p.ok[P] ? p.vs[P] : make_uint2(0u, 0u);
+    p.vz[P] = p.ok[P] ? p.vz[P] : make_uint2(0u, 0u);
   }
 }
 
@@ -387,7 +415,14 @@ constexpr int kWavesPerWG = 8;   // one wave per KV head of a head group
 
 typedef __attribute__((address_space(4))) const int32_t* cint_ptr;  // read through the scalar cache
 
-// Pages of every sequence and their exclusive prefix sums (prefix[B] = total pages). One block.
+// First page of work-group g's range when P pages are split evenly over G groups.
+__host__ __device__ __forceinline__ int range_lo(int g, int P, int G) { return (int)(((long long)g * P) / G); }
+
+// Pages of every sequence and their exclusive prefix sums (prefix[B] = total pages), and for each
+// scan work-group g the sequence b holding the first page of its range with that sequence's page
+// range: wg_info[g] = {b, prefix[b], prefix[b + 1], 0}. Group g starts inside sequence b exactly
+// when prefix[b] <= lo(g) < prefix[b + 1], i.e. for g in [ceil(prefix[b] G / P), ...) while lo(g)
+// stays below prefix[b + 1], so every group is written once (by the thread owning b). One block.
 __global__ __launch_bounds__(1024) void page_prefix_kernel(DecodeArgs a) {
   __shared__ int sums[1024];
   const int tid = threadIdx.x;
@@ -403,16 +438,19 @@ __global__ __launch_bounds__(1024) void page_prefix_kernel(DecodeArgs a) {
     sums[tid] += v;
     __syncthreads();
   }
+  const int P = sums[1023], G = a.grid_g;
   int run = tid > 0 ? sums[tid - 1] : 0;
   for (int b = b0; b < b1; ++b) {
+    const int n = (seq_len_m(a, b) + kBlock - 1) >> 4;
     a.prefix[b] = run;
-    run += (seq_len_m(a, b) + kBlock - 1) >> 4;
+    if (n > 0) {
+      for (int g = (int)(((long long)run * G + P - 1) / P); g < G && range_lo(g, P, G) < run + n; ++g)
+        *reinterpret_cast<int4*>(a.wg_info + 4 * g) = make_int4(b, run, run + n, 0);
+    }
+    run += n;
   }
-  if (tid == 1023) a.prefix[a.B] = sums[1023];
+  if (tid == 1023) a.prefix[a.B] = P;
 }
-
-// First page of work-group g's range when P pages are split evenly over G groups.
-__host__ __device__ __forceinline__ int range_lo(int g, int P, int G) { return (int)(((long long)g * P) / G); }
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
@@ -426,19 +464,13 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   const int npairs = (p1 - p0 + 1) >> 1;
   const uint32_t stage_base = (uint32_t)(uintptr_t)stage_w;
 
-  // ---- query operands of (b, h): DMA into the staging area, then into registers
+  // ---- query operands of (b, h): plain loads, issued ahead of the first page DMAs so that both
+  // latencies overlap (the first use waits for every load in flight, which the prologue does anyway)
   const uint8_t* qop = a.qop + ((size_t)b * a.H + h) * RT * kQopTile;
-#pragma unroll
-  for (int r = 0; r < RT; ++r) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(qop + r * kQopTile + i * 1024, 16 * l, stage_base + r * kQopTile + i * 1024);
-    dma4(qop + r * kQopTile + 4096, 4 * l, stage_base + r * kQopTile + 4096);
-  }
-  wait_vm_all();
   ScanState<RT> st;
 #pragma unroll
   for (int r = 0; r < RT; ++r) {
-    const uint8_t* t = stage_w + r * kQopTile;
+    const uint8_t* t = qop + r * kQopTile;
 #pragma unroll
     for (int i = 0; i < 4; ++i) st.A[r][i] = *reinterpret_cast<const half8_t*>(t + (i * 64 + l) * 16);
     st.cinit[r] = *reinterpret_cast<const float4_t*>(t + 4096 + hi * 16);
@@ -450,54 +482,87 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
     st.zl[r] = float4_t{0.f, 0.f, 0.f, 0.f};
     st.mref[r] = kMaxInit;
   }
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 
   // ---- pipeline over the segment's page pairs (pages p0 + 2k, p0 + 2k + 1)
-  const int32_t __attribute__((address_space(4)))* bt =
-      (const int32_t __attribute__((address_space(4)))*)(uintptr_t)(a.block_table + (size_t)b * a.max_blocks);
+  const bt_ptr bt = (bt_ptr)(uintptr_t)(a.block_table + (size_t)b * a.max_blocks);
+  const uint8_t* base_h = a.pool + (size_t)h * kRecord;
+  const uint32_t stride = (uint32_t)a.H * kRecord;
+  const uint32_t nblk = (uint32_t)a.num_blocks;
   uint32_t okmask = 0;  // bits 2*slot, 2*slot+1: validity of the two pages staged in slot
+  BlockIds ids[kStages];
+#pragma unroll
+  for (int k = 0; k < kStages; ++k) ids[k] = load_ids(bt, p0 + 2 * k, p1);
 #pragma unroll
   for (int k = 0; k < kStages; ++k)
-    if (k < npairs) okmask |= stage_pair(a, bt, h, p0, p1, k, stage_base + k * 2 * kRecord, l) << (2 * k);
-  PairLoads cur;
+    if (k < npairs)
+      okmask |= stage_pair(a.pool, base_h, stride, nblk, ids[k], p0 + 2 * k, p1, stage_base + k * 2 * kRecord, l)
+                << (2 * k);
+  // block ids of the next pair to stage, read one step ahead of their use so that the scalar
+  // loads overlap the step's arithmetic
+  BlockIds nid = load_ids(bt, p0 + 2 * kStages, p1);
+  PairLoads X, Y;
   {
     if (kStages - 1 < npairs)
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * 2 * (kStages - 1)) : "memory");
     else
       wait_vm_all();
-    read_pair(stage_w, okmask & 1u, (okmask >> 1) & 1u, lo, hi, cur);
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    if (kStages < npairs)
-      okmask = (okmask & ~3u) | stage_pair(a, bt, h, p0, p1, kStages, stage_base, l);
+    read_pair(stage_w, okmask & 1u, (okmask >> 1) & 1u, lo, hi, X);
+    pin_pair(X);
+    mask_pair(X);
+    if (kStages < npairs) {
+      asm volatile("" : "+s"(nid.b0), "+s"(nid.b1));
+      const BlockIds next = load_ids(bt, p0 + 2 * (kStages + 1), p1);
+      okmask = (okmask & ~3u) | stage_pair(a.pool, base_h, stride, nblk, nid, p0 + 2 * kStages, p1, stage_base, l);
+      nid = next;
+    }
     float a2[2][RT];
-    qk_pair<RT>(st, cur, p0, L, lo, a2);
+    qk_pair<RT>(st, X, p0, L, lo, a2);
     softmax_pair<RT>(st, a2, lo, hi, p_w[0], al_w);
   }
+  // One step: read pair k+1 (staged kStages pairs ago), refill its slot with pair k+1+kStages,
+  // scores of pair k+1 beside the value accumulation of pair k, then the softmax of pair k+1.
+  // STEADY: every condition holds (k + 1 + kStages < npairs).
   int sl = 0;  // slot of pair k
-  for (int k = 0; k < npairs; ++k) {
-    const bool more = k + 1 < npairs;
+  auto step = [&](auto steady_tag, const PairLoads& cur, PairLoads& nxt, int k) {
+    constexpr bool STEADY = decltype(steady_tag)::value;
     sl = sl + 1 == kStages ? 0 : sl + 1;  // slot of pair k + 1
-    PairLoads nxt;
+    const bool more = STEADY || k + 1 < npairs;
     if (more) {
-      if (k + 1 + kStages - 1 < npairs)
+      if (STEADY || k + kStages < npairs)
         asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * 2 * (kStages - 1)) : "memory");
       else
         wait_vm_all();
       read_pair(stage_w + sl * 2 * kRecord, (okmask >> (2 * sl)) & 1u, (okmask >> (2 * sl + 1)) & 1u, lo, hi, nxt);
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      const int refill = k + 1 + kStages;
-      if (refill < npairs)
+      pin_pair(nxt);
+      mask_pair(nxt);
+      if (STEADY || k + 1 + kStages < npairs) {
+        const int page0 = p0 + 2 * (k + 1 + kStages);
+        // The ids read one step ago are pinned (their wait placed) before the next loads issue:
+        // scalar loads return out of order, so a wait placed after those would wait for them
+        // too. The new loads sit between the empty asm and the DMA (both memory barriers), so
+        // they issue before the DMA and have the step to return.
+        asm volatile("" : "+s"(nid.b0), "+s"(nid.b1));
+        const BlockIds next = load_ids(bt, page0 + 2, p1);
         okmask = (okmask & ~(3u << (2 * sl))) |
-                 (stage_pair(a, bt, h, p0, p1, refill, stage_base + sl * 2 * kRecord, l) << (2 * sl));
+                 (stage_pair(a.pool, base_h, stride, nblk, nid, page0, p1, stage_base + sl * 2 * kRecord, l)
+                  << (2 * sl));
+        nid = next;
+      }
     }
     float a2[2][RT];
     if (more) qk_pair<RT>(st, nxt, p0 + 2 * (k + 1), L, lo, a2);
     lds_sync_wave();
     pv_pair<RT>(st, cur, lo, hi, p_w[k & 1]);
-    if (more) {
-      softmax_pair<RT>(st, a2, lo, hi, p_w[(k + 1) & 1], al_w);
-      cur = nxt;
-    }
+    if (more) softmax_pair<RT>(st, a2, lo, hi, p_w[(k + 1) & 1], al_w);
+  };
+  int k = 0;
+  for (; k + 2 + kStages < npairs; k += 2) {
+    step(std::true_type{}, X, Y, k);
+    step(std::true_type{}, Y, X, k + 1);
+  }
+  for (; k < npairs; ++k) {
+    step(std::false_type{}, X, Y, k);
+    X = Y;
   }
 
   // ---- partial (m, l, O') of every query head of this KV head
@@ -553,7 +618,6 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   __shared__ __attribute__((aligned(16))) uint8_t stage[kWavesPerWG][kStages][2][kRecord];
   __shared__ _Float16 p_lds[kWavesPerWG][2][2][8][kBlock];
   __shared__ float al_lds[kWavesPerWG][8];
-  static_assert(2 * kRecord * kStages >= 2 * kQopTile, "query operands are staged through the page slots");
 
   const int g = blockIdx.x, G = gridDim.x;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
@@ -563,18 +627,18 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   const int P = prefix[a.B];
   const int s = range_lo(g, P, G), e = range_lo(g + 1, P, G);
   if (s >= e) return;
-  int b = 0, bh = a.B;  // prefix[b] <= s < prefix[bh]
-  while (bh - b > 1) {
-    const int mid = (b + bh) >> 1;
-    if (prefix[mid] <= s) b = mid;
-    else bh = mid;
-  }
-  for (int pos = s; pos < e; ++b) {
-    const int Sb = prefix[b], Sb1 = prefix[b + 1];
-    if (Sb1 <= pos) continue;
+  const cint_ptr info = (cint_ptr)(uintptr_t)(a.wg_info + 4 * g);
+  int b = info[0], Sb = info[1], Sb1 = info[2];  // prefix[b] <= s < prefix[b + 1]
+  for (int pos = s;;) {
     const int seg_end = min(e, Sb1);
+    const int Sb2 = seg_end < e ? prefix[b + 2] : 0;  // next sequence's end, fetched ahead
     scan_segment<RT>(a, b, h, pos - Sb, seg_end - Sb, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w]);
     pos = seg_end;
+    if (pos >= e) break;
+    ++b;
+    Sb = Sb1;
+    Sb1 = Sb2;
+    while (Sb1 <= pos) Sb1 = prefix[++b + 1];  // skip empty sequences
   }
 }
 
