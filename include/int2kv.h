@@ -113,14 +113,15 @@ int int2kv_quantize_pack_rotated(const int2kv_cache* cache, const float* k_rot, 
                                  const int32_t* slot_mapping, int num_tokens, float clip_k,
                                  float clip_v, hipStream_t stream);
 
-/* Cache write (Sec. 4.1; Sec. 6): per token and KV head, k R_K - mu R_K and v R_V in fp32,
- * then INT2 group quantization and packing into the slot given by slot_mapping.
- *   k, v         : bf16 [n, H_kv, 128] (post-RoPE keys; values)
+/* Cache write (Sec. 4.1; Sec. 6): per token and KV head, k R_K - mu R_K and v R_V with fp32
+ * accumulation, then INT2 group quantization and packing into the slot given by slot_mapping.
+ *   k, v         : bf16 [n, H_kv, 128] (post-RoPE keys; values), 16-byte aligned
  *   slot_mapping : int32 [n]; negative = skip; distinct slots
- *   R_k, R_v     : fp32 [H_kv, 128, 128];  mu_rk: fp32 [H_kv, 128] from int2kv_prepare_mu_rot
- * Appends of few tokens rotate with fp32 FMAs; appends of many tokens rotate on the matrix
- * cores with R split into two bf16 terms (error ~1e-5 of |R|), so codes may differ from an
- * exact-arithmetic rotation only where x sits at a rounding boundary. */
+ *   R_k, R_v     : fp32 [H_kv, 128, 128], 16-byte aligned;  mu_rk: fp32 [H_kv, 128] from
+ *                  int2kv_prepare_mu_rot
+ * The rotation runs on the matrix cores with R split into two bf16 terms (R_hi + R_lo, error
+ * below 2^-17 |R|), so codes may differ from an exact-arithmetic rotation only where x sits at
+ * a rounding boundary of the quantizer. */
 int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
                            const int32_t* slot_mapping, int num_tokens, const float* R_k,
                            const float* R_v, const float* mu_rk, float clip_k, float clip_v,
@@ -131,15 +132,17 @@ size_t int2kv_decode_workspace_bytes(int batch, int num_q_heads, int num_kv_head
                                      int d_model);
 
 /* Decode attention over the INT2 cache for one new query per sequence.
- *   q            : bf16 [B, H_q, 128] (post-RoPE)
+ *   q            : bf16 [B, H_q, 128] (post-RoPE), 16-byte aligned
  *   block_table  : int32 [B, max_blocks_per_seq]; entry i of sequence b is the physical
  *                  block of tokens 16i .. 16i+15
  *   ctx_lens     : int32 [B] cached tokens to attend (the current token is appended first);
  *                  lengths are clamped to [0, min(max_ctx, 16*max_blocks_per_seq)], and blocks
  *                  outside [0, num_blocks) are skipped
  *   max_ctx      : host-side upper bound of ctx_lens (sizes the split-context grid)
- *   R_k, R_v     : fp32 [H_kv, 128, 128]
- *   W_o          : bf16 [d_model, H_q*128] or NULL (no output projection)
+ *   R_k, R_v     : fp32 [H_kv, 128, 128], 16-byte aligned (R_v may be NULL with a folded W_o)
+ *   W_o          : bf16 [d_model, H_q*128], 16-byte aligned, or NULL (no output projection);
+ *                  applied on the matrix cores with o split into two bf16 terms (fp32-like
+ *                  precision), split over K in fixed slices summed in a fixed order
  *   wo_is_folded : nonzero if W_o is W-bar_O from int2kv_fold_wo (then R_v is not applied)
  *   out          : fp32 [B, H_q, 128] if W_o is NULL, else fp32 [B, d_model]
  *   workspace    : device scratch of at least int2kv_decode_workspace_bytes(...) bytes

@@ -8,7 +8,6 @@
 #include "kernels.h"
 
 namespace int2kv {
-int wo_ksplit(int K);
 bool mfma_decode_available();
 }
 
@@ -177,7 +176,9 @@ int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const u
   if (num_tokens == 0) return ok();
   if (!k || !v || !slot_mapping || !R_k || !R_v || !mu_rk) return fail(INT2KV_EINVAL, "NULL pointer argument");
   if (!valid_clip(clip_k) || !valid_clip(clip_v)) return fail(INT2KV_EINVAL, "clip ratios must be in (0, 1]");
-  hipError_t e = launch_append_valu(view(cache), k, v, slot_mapping, num_tokens, R_k, R_v, mu_rk, clip_k, clip_v,
+  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(R_k, 16) || !aligned(R_v, 16))
+    return fail(INT2KV_EINVAL, "k, v, R_k and R_v must be 16-byte aligned");
+  hipError_t e = launch_append_mfma(view(cache), k, v, slot_mapping, num_tokens, R_k, R_v, mu_rk, clip_k, clip_v,
                                     stream);
   return hip_status(e, "quantize_append");
 }
@@ -203,7 +204,8 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
   if (max_blocks_per_seq <= 0 || max_ctx < 0) return fail(INT2KV_EINVAL, "bad max_blocks_per_seq / max_ctx");
   if (!q || !block_table || !ctx_lens || !R_k || !out || (!R_v && !(W_o && wo_is_folded)))
     return fail(INT2KV_EINVAL, "NULL pointer argument");
-  if (!aligned(q, 16) || !aligned(out, 16)) return fail(INT2KV_EINVAL, "q and out must be 16-byte aligned");
+  if (!aligned(q, 16) || !aligned(out, 16) || !aligned(R_k, 16) || (R_v && !aligned(R_v, 16)))
+    return fail(INT2KV_EINVAL, "q, out, R_k and R_v must be 16-byte aligned");
   if (W_o) {
     if (d_model <= 0) return fail(INT2KV_EINVAL, "d_model must be positive when W_o is given");
     if (!aligned(W_o, 16)) return fail(INT2KV_EINVAL, "W_o must be 16-byte aligned");
@@ -258,11 +260,12 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
     if (e != hipSuccess) return hip_status(e, "decode/event");
   }
   const bool unrotate = !(W_o && wo_is_folded);
-  float* heads = W_o ? reinterpret_cast<float*>(ws + plan.off_o) : out;
-  e = plan.variant == 2 ? launch_merge_flat(a, unrotate, heads, stream) : launch_merge(a, unrotate, heads, stream);
+  // with W_O the merge writes each head output as two bf16 terms (hi, lo) for the projection
+  uint16_t* ob = W_o ? reinterpret_cast<uint16_t*>(ws + plan.off_o) : nullptr;
+  e = plan.variant == 2 ? launch_merge_flat(a, unrotate, out, ob, stream) : launch_merge(a, unrotate, out, ob, stream);
   if (e != hipSuccess) return hip_status(e, "decode/merge");
   if (W_o) {
-    e = launch_wo_gemm(heads, W_o, out, reinterpret_cast<float*>(ws + plan.off_wo), batch,
+    e = launch_wo_gemm(ob, W_o, out, reinterpret_cast<float*>(ws + plan.off_wo), batch,
                        num_q_heads * kHeadDim, d_model, plan.wo_ksplit, stream);
     if (e != hipSuccess) return hip_status(e, "decode/wo");
   }

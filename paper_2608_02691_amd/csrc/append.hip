@@ -29,12 +29,6 @@ hipError_t launch_prepare_mu_rot(const float* R_k, const float* mu, float* mu_rk
 
 // ---------------------------------------------------------------------------------------------
 // W-bar_{O,j} = W_{O,j} R_{V,h(j)}: block (row tile, query head), thread c = output column.
-__device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
-  uint32_t u = __float_as_uint(x);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
-}
-
 constexpr int kFoldRows = 32;
 
 __global__ __launch_bounds__(128) void fold_wo_kernel(const uint16_t* __restrict__ W,
@@ -134,43 +128,128 @@ hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_r
 }
 
 // ---------------------------------------------------------------------------------------------
-// Few-token append: block (tile of tokens, KV head). Thread (row, c) keeps column c of R_K (row 0)
-// or R_V (row 1) in registers and rotates each token of the tile with fp32 FMAs in channel order.
-constexpr int kAppendTile = 16;
+// Append on the matrix cores: x R (x bf16 [n, H, 128], R fp32 [128, 128]) as bf16 MFMA with R split
+// into two bf16 terms (R = R_hi + R_lo + O(2^-18 |R|)), fp32 accumulation; then - mu R_K for keys,
+// the group quantizer and the packed stores. Work-group (KV head h, K or V, a stride of 16-token
+// tiles); R^T of the work-group's (h, K|V) is converted once into LDS as the B operand.
+// Tile layout: D[token][channel] of n-tile p (channels 16p .. 16p + 15) sits in lane
+// (channel % 16) + 16 (token / 4), register token % 4, so lane m holds channels m + 16p, p = 0..7,
+// of four tokens: exactly the eight 2-bit codes of half m of the packed layout, and the 32
+// channels of group g are n-tiles 2g, 2g + 1 across the 16 lanes of one DPP row.
+typedef __bf16 ap_bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float ap_f4_t __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(256) void append_valu_kernel(CacheView cv, const uint16_t* __restrict__ k,
+constexpr int kApWaves = 4;
+constexpr int kApRow = 136;  // bf16 per LDS row of R^T (128 + 8 pad: conflict-free 16-byte reads)
+
+__global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v,
                                                            const int32_t* __restrict__ slots, int n,
                                                            const float* __restrict__ R_k,
                                                            const float* __restrict__ R_v,
                                                            const float* __restrict__ mu_rk, float clip_k,
                                                            float clip_v) {
-  __shared__ float xs[2][kHeadDim];
-  __shared__ uint8_t codes[2][kHeadDim];
-  const int h = blockIdx.y, tid = threadIdx.x, row = tid >> 7, c = tid & 127;
-  const float* R = (row == 0 ? R_k : R_v) + (size_t)h * kHeadDim * kHeadDim;
-  float col[kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t rt[2][kHeadDim][kApRow];  // [hi, lo][c][i] = R[i][c]
+  const int h = blockIdx.y, kv = blockIdx.z, H = cv.num_kv_heads, tid = threadIdx.x;
+  const float* R = (kv == 0 ? R_k : R_v) + (size_t)h * kHeadDim * kHeadDim;
+  {
+    // R with 16 independent 16-byte loads per thread (one round trip), then transposed into LDS
+    const float4* R4 = reinterpret_cast<const float4*>(R);
+    float4 rv[16];
 #pragma unroll
-  for (int i = 0; i < kHeadDim; ++i) col[i] = R[i * kHeadDim + c];
-  const float sub = row == 0 ? mu_rk[(size_t)h * kHeadDim + c] : 0.0f;
-  const int t_end = min(n, (blockIdx.x + 1) * kAppendTile);
-  for (int tok = blockIdx.x * kAppendTile; tok < t_end; ++tok) {
-    const size_t base = ((size_t)tok * cv.num_kv_heads + h) * kHeadDim + c;
-    xs[row][c] = bf16_bits_to_f32(row == 0 ? k[base] : v[base]);
-    __syncthreads();
-    float acc = 0.0f;
+    for (int u = 0; u < 16; ++u) rv[u] = R4[tid + 256 * u];
 #pragma unroll
-    for (int i = 0; i < kHeadDim; ++i) acc = fmaf(xs[row][i], col[i], acc);
-    const float x = acc - sub;
-    quantize_store_pair(x, slots[tok], h, clip_k, clip_v, cv, codes);
+    for (int u = 0; u < 16; ++u) {
+      const int e = 4 * (tid + 256 * u), i = e >> 7, c = e & 127;
+      const float r4[4] = {rv[u].x, rv[u].y, rv[u].z, rv[u].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t rh = f32_to_bf16_rne(r4[q]);
+        rt[0][c + q][i] = (uint16_t)rh;
+        rt[1][c + q][i] = (uint16_t)f32_to_bf16_rne(r4[q] - __uint_as_float(rh << 16));
+      }
+    }
+  }
+  __syncthreads();
+  const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
+  float sub[8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p) sub[p] = kv == 0 ? mu_rk[(size_t)h * kHeadDim + 16 * p + lo] : 0.0f;
+  const uint16_t* X = kv == 0 ? k : v;
+  const float clip = kv == 0 ? clip_k : clip_v;
+  const int nslots = cv.num_blocks * kBlock;
+  for (int tile = blockIdx.x * kApWaves + w; tile * 16 < n; tile += gridDim.x * kApWaves) {
+    const int tok0 = tile * 16;
+    const uint16_t* xrow = X + ((size_t)min(tok0 + lo, n - 1) * H + h) * kHeadDim + 8 * hi;
+    ap_bf16x8_t A[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) A[ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
+    ap_f4_t acc[8];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) acc[p] = ap_f4_t{0.f, 0.f, 0.f, 0.f};
+    // the B fragments are the same for every tile: an opaque offset keeps the compiler from
+    // hoisting all 64 of them into registers (which would cap occupancy at one wave per SIMD)
+    int boff = (lo * kApRow + 8 * hi) * 2;
+    asm volatile("" : "+v"(boff));
+    const uint8_t* rb = reinterpret_cast<const uint8_t*>(&rt[0][0][0]) + boff;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        const ap_bf16x8_t bh = *reinterpret_cast<const ap_bf16x8_t*>(rb + ((16 * p) * kApRow + 32 * ks) * 2);
+        const ap_bf16x8_t bl =
+            *reinterpret_cast<const ap_bf16x8_t*>(rb + ((kHeadDim + 16 * p) * kApRow + 32 * ks) * 2);
+        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[ks], bh, acc[p], 0, 0, 0);
+        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[ks], bl, acc[p], 0, 0, 0);
+      }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int tok = tok0 + 4 * hi + r;
+      float x[8];
+#pragma unroll
+      for (int p = 0; p < 8; ++p) x[p] = acc[p][r] - sub[p];
+      uint32_t half = 0, meta[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float mn = row_min16(fminf(x[2 * g], x[2 * g + 1]));
+        const float mx = row_max16(fmaxf(x[2 * g], x[2 * g + 1]));
+        uint32_t s_bits, z_bits;
+        float zf, inv;
+        int2_group_params(mn, mx, clip, s_bits, z_bits, zf, inv);
+        half |= int2_code(x[2 * g], zf, inv) << (4 * g);
+        half |= int2_code(x[2 * g + 1], zf, inv) << (4 * g + 2);
+        meta[g] = s_bits | (z_bits << 16);
+      }
+      const int slot = tok < n ? slots[tok] : -1;
+      if (slot >= 0 && slot < nslots) {
+        const int blk = slot >> 4, t = slot & 15;
+        uint8_t* rec = cv.pool + ((size_t)blk * H + h) * kRecord;
+        const uint32_t my = lo == 0 ? meta[0] : lo == 1 ? meta[1] : lo == 2 ? meta[2] : meta[3];
+        if (kv == 0) {
+          *reinterpret_cast<uint16_t*>(rec + kOffKCodes + 32 * t + 2 * lo) = (uint16_t)half;
+          if (lo < 4) *reinterpret_cast<uint32_t*>(rec + kOffKMeta + 16 * t + 4 * lo) = my;
+        } else {
+          *reinterpret_cast<uint16_t*>(rec + kOffVCodes + 32 * lo + 2 * t) = (uint16_t)half;
+          if (lo < 4) {
+            *reinterpret_cast<uint16_t*>(rec + kOffVScale + 32 * lo + 2 * t) = (uint16_t)(my & 0xFFFFu);
+            *reinterpret_cast<uint16_t*>(rec + kOffVZero + 32 * lo + 2 * t) = (uint16_t)(my >> 16);
+          }
+        }
+      }
+    }
   }
 }
 
-hipError_t launch_append_valu(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots, int n,
+hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots, int n,
                               const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
                               float clip_v, hipStream_t s) {
-  dim3 grid((n + kAppendTile - 1) / kAppendTile, c.num_kv_heads);
-  hipLaunchKernelGGL(append_valu_kernel, grid, dim3(256), 0, s, c, k, v, slots, n, R_k, R_v, mu_rk, clip_k,
+  if (n <= 0) return hipSuccess;
+  // enough work-groups to fill the chip at two per CU, each converting R once for many tiles
+  const int tiles = (n + 15) / 16;
+  const int per_head = max(1, 512 / (2 * c.num_kv_heads));
+  const int nx = min((tiles + kApWaves - 1) / kApWaves, per_head);
+  dim3 grid(nx, c.num_kv_heads, 2);
+  hipLaunchKernelGGL(append_mfma_kernel, grid, dim3(256), 0, s, c, k, v, slots, n, R_k, R_v, mu_rk, clip_k,
                      clip_v);
   return hipGetLastError();
 }

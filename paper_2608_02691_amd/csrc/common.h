@@ -20,6 +20,22 @@ constexpr int kOffVScale = 1280;  // [4 groups][16 tok] fp16
 constexpr int kOffVZero = 1408;   // [4 groups][16 tok] fp16
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+// round to nearest even on the upper 16 bits (finite inputs)
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+// One head-output value, either as fp32 (out) or as two bf16 terms for the output projection:
+// hi = bf16(v) at ob[idx], lo = bf16(v - hi) at ob[total + idx].
+__device__ __forceinline__ void store_head_out(float v, float* out, uint16_t* ob, size_t idx, size_t total) {
+  if (ob) {
+    const uint32_t h = f32_to_bf16_rne(v);
+    ob[idx] = (uint16_t)h;
+    ob[total + idx] = (uint16_t)f32_to_bf16_rne(v - __uint_as_float(h << 16));
+  } else {
+    out[idx] = v;
+  }
+}
 __device__ __forceinline__ float f16_bits_to_f32(uint32_t h) {
   return __half2float(__ushort_as_half(static_cast<unsigned short>(h)));
 }
@@ -49,6 +65,35 @@ __device__ __forceinline__ uint32_t int2_code(float x, float zf, float inv) {
   const float t = d * inv;
   const float r = fminf(fmaxf(rintf(t), 0.0f), 3.0f);
   return static_cast<uint32_t>(r);
+}
+
+// DPP lane move inside rows of 16 lanes (CTRL = row_ror:n is 0x120 + n)
+template <int CTRL>
+__device__ __forceinline__ float dppf(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+// max / min / sum over the 16 lanes of a DPP row (every lane gets the result)
+__device__ __forceinline__ float row_max16(float x) {
+  x = fmaxf(x, dppf<0x128>(x));
+  x = fmaxf(x, dppf<0x124>(x));
+  x = fmaxf(x, dppf<0x122>(x));
+  x = fmaxf(x, dppf<0x121>(x));
+  return x;
+}
+__device__ __forceinline__ float row_min16(float x) {
+  x = fminf(x, dppf<0x128>(x));
+  x = fminf(x, dppf<0x124>(x));
+  x = fminf(x, dppf<0x122>(x));
+  x = fminf(x, dppf<0x121>(x));
+  return x;
+}
+__device__ __forceinline__ float row_sum16(float x) {
+  x += dppf<0x128>(x);
+  x += dppf<0x124>(x);
+  x += dppf<0x122>(x);
+  x += dppf<0x121>(x);
+  return x;
 }
 
 }  // namespace int2kv

@@ -57,27 +57,6 @@ __device__ __forceinline__ uint32_t land(uint32_t w) {
   return r;
 }
 
-template <int CTRL>
-__device__ __forceinline__ float dppf(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
-}
-
-// max / sum over the 16 lanes of a DPP row
-__device__ __forceinline__ float row_max16(float x) {
-  x = fmaxf(x, dppf<0x128>(x));
-  x = fmaxf(x, dppf<0x124>(x));
-  x = fmaxf(x, dppf<0x122>(x));
-  x = fmaxf(x, dppf<0x121>(x));
-  return x;
-}
-__device__ __forceinline__ float row_sum16(float x) {
-  x += dppf<0x128>(x);
-  x += dppf<0x124>(x);
-  x += dppf<0x122>(x);
-  x += dppf<0x121>(x);
-  return x;
-}
-
 __device__ __forceinline__ void lds_sync_wave() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -99,32 +78,53 @@ __device__ __forceinline__ int seq_len_m(const DecodeArgs& a, int b) {
 // per-head power of two sigma (max |q' sigma| in [256, 512)), laid out as the MFMA A operand of the
 // score contraction: row (j, g) of tile r holds q'_j on the channels of group g, times 2^e of the
 // channel's code position, as fp16. Constants per row: -sum_k A_k (accumulator start),
-// sum_{k in g} q'_jk (for the zero term) and 1/sigma.
-__global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int rt) {
+// sum_{k in g} q'_jk (for the zero term) and 1/sigma. Thread (half, c): channel c of the query
+// heads jj = half, half + 2, ...
+__device__ void qprep_block(const DecodeArgs& a, int bh, int rt) {
+  __shared__ __attribute__((aligned(16))) float Rs[kHeadDim * kHeadDim];  // R_K of head h
   __shared__ float qin[8][kHeadDim];
   __shared__ float qr[8][kHeadDim];
+  __shared__ int smax[8];
   __shared__ float sig[8];
-  const int bh = blockIdx.x, b = bh / a.H, h = bh % a.H, gq = a.gq, tid = threadIdx.x;
+  const int b = bh / a.H, h = bh % a.H, gq = a.gq, tid = threadIdx.x;
+  const int c = tid & 127, half = tid >> 7;
+  if (tid < 8) smax[tid] = 0;
+  {
+    // all of R_K[h] with 16 independent 16-byte loads per thread (one round trip)
+    const float4* Rg = reinterpret_cast<const float4*>(a.R_k + (size_t)h * kHeadDim * kHeadDim);
+    float4 rv[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) rv[u] = Rg[tid + 256 * u];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) reinterpret_cast<float4*>(Rs)[tid + 256 * u] = rv[u];
+  }
   for (int i = tid; i < gq * kHeadDim; i += 256) {
-    const int jj = i / kHeadDim, c = i % kHeadDim;
-    qin[jj][c] = bf16_bits_to_f32(a.q[((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c]);
+    const int jj = i / kHeadDim, cc = i % kHeadDim;
+    qin[jj][cc] = bf16_bits_to_f32(a.q[((size_t)b * a.Hq + h * gq + jj) * kHeadDim + cc]);
   }
   __syncthreads();
-  const float* R = a.R_k + (size_t)h * kHeadDim * kHeadDim;
-  for (int i = tid; i < gq * kHeadDim; i += 256) {
-    const int jj = i / kHeadDim, c = i % kHeadDim;
-    float acc = 0.0f;
-    for (int k = 0; k < kHeadDim; ++k) acc = fmaf(qin[jj][k], R[k * kHeadDim + c], acc);
-    qr[jj][c] = acc * kLogit2;
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // query heads half, half + 2, half + 4, half + 6
+#pragma unroll 8
+  for (int k = 0; k < kHeadDim; ++k) {
+    const float r = Rs[k * kHeadDim + c];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc[u] = fmaf(qin[half + 2 * u][k], r, acc[u]);
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int jj = half + 2 * u;
+    if (jj < gq) {
+      const float v = acc[u] * kLogit2;
+      qr[jj][c] = v;
+      atomicMax(&smax[jj], __float_as_int(fabsf(v)));  // non-negative floats order like their bits
+    }
   }
   __syncthreads();
-  if (tid < gq) {
-    float m = 0.0f;
-    for (int c = 0; c < kHeadDim; ++c) m = fmaxf(m, fabsf(qr[tid][c]));
+  if (tid < 8) {
+    const float m = __int_as_float(smax[tid]);
     int ex = 0;
     frexpf(m, &ex);
-    const int p2 = m > 0.0f ? max(-100, min(100, 9 - ex)) : 0;
-    sig[tid] = ldexpf(1.0f, p2);
+    sig[tid] = tid < gq && m > 0.0f ? ldexpf(1.0f, max(-100, min(100, 9 - ex))) : 1.0f;
   }
   __syncthreads();
   uint8_t* out = a.qop + (size_t)bh * rt * kQopTile;
@@ -138,21 +138,26 @@ __global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int rt) {
     if (g == i && jj < gq) v = (_Float16)(qr[jj][ch] * sig[jj] * (float)(1 << land_e(x)));
     reinterpret_cast<_Float16*>(out + r * kQopTile + (i * 64 + l) * 16)[s] = v;
   }
-  if (tid < rt * 16) {
-    const int r = tid / 16, jl = (tid / 4) % 4, g = tid % 4, jj = 4 * r + jl;
+  // per row (jj, g): sums over the 32 channels of group g, one element per lane of a 32-lane group
+  for (int e = tid; e < rt * 512; e += 256) {
+    const int jj = e / 128, g = (e / 32) % 4, cc = e % 32, ch = 32 * g + cc;
     float csum = 0.0f, qsum = 0.0f;
     if (jj < gq) {
-      for (int cc = 0; cc < kGroup; ++cc) {
-        const int ch = 32 * g + cc;
-        const _Float16 v = (_Float16)(qr[jj][ch] * sig[jj] * (float)(1 << land_e(ch >> 4)));
-        csum += (float)v;
-        qsum += qr[jj][ch];
-      }
+      csum = (float)(_Float16)(qr[jj][ch] * sig[jj] * (float)(1 << land_e(ch >> 4)));
+      qsum = qr[jj][ch];
     }
-    float* cst = reinterpret_cast<float*>(out + r * kQopTile + 4096);
-    cst[jl * 4 + g] = -csum;
-    cst[16 + jl * 4 + g] = qsum;
-    if (g == 0) cst[32 + jl] = jj < gq ? 1.0f / sig[jj] : 0.0f;
+#pragma unroll
+    for (int off = 16; off >= 1; off >>= 1) {
+      csum += __shfl_xor(csum, off, 32);
+      qsum += __shfl_xor(qsum, off, 32);
+    }
+    if (cc == 0) {
+      const int r = jj / 4, jl = jj % 4;
+      float* cst = reinterpret_cast<float*>(out + r * kQopTile + 4096);
+      cst[jl * 4 + g] = -csum;
+      cst[16 + jl * 4 + g] = qsum;
+      if (g == 0) cst[32 + jl] = jj < gq ? 1.0f / sig[jj] : 0.0f;
+    }
   }
 }
 
@@ -422,23 +427,24 @@ __host__ __device__ __forceinline__ int range_lo(int g, int P, int G) { return (
 // scan work-group g the sequence b holding the first page of its range with that sequence's page
 // range: wg_info[g] = {b, prefix[b], prefix[b + 1], 0}. Group g starts inside sequence b exactly
 // when prefix[b] <= lo(g) < prefix[b + 1], i.e. for g in [ceil(prefix[b] G / P), ...) while lo(g)
-// stays below prefix[b + 1], so every group is written once (by the thread owning b). One block.
-__global__ __launch_bounds__(1024) void page_prefix_kernel(DecodeArgs a) {
-  __shared__ int sums[1024];
+// stays below prefix[b + 1], so every group is written once (by the thread owning b). One block
+// of 256 threads.
+__device__ void page_prefix_block(const DecodeArgs& a) {
+  __shared__ int sums[256];
   const int tid = threadIdx.x;
-  const int per = (a.B + 1023) / 1024;
+  const int per = (a.B + 255) / 256;
   const int b0 = min(a.B, tid * per), b1 = min(a.B, b0 + per);
   int s = 0;
   for (int b = b0; b < b1; ++b) s += (seq_len_m(a, b) + kBlock - 1) >> 4;
   sums[tid] = s;
   __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
+  for (int off = 1; off < 256; off <<= 1) {
     const int v = tid >= off ? sums[tid - off] : 0;
     __syncthreads();
     sums[tid] += v;
     __syncthreads();
   }
-  const int P = sums[1023], G = a.grid_g;
+  const int P = sums[255], G = a.grid_g;
   int run = tid > 0 ? sums[tid - 1] : 0;
   for (int b = b0; b < b1; ++b) {
     const int n = (seq_len_m(a, b) + kBlock - 1) >> 4;
@@ -449,7 +455,15 @@ __global__ __launch_bounds__(1024) void page_prefix_kernel(DecodeArgs a) {
     }
     run += n;
   }
-  if (tid == 1023) a.prefix[a.B] = P;
+  if (tid == 255) a.prefix[a.B] = P;
+}
+
+// Blocks 0 .. B*H-1: query operands of (b, h); the last block: page prefix sums.
+__global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int rt) {
+  if (blockIdx.x == gridDim.x - 1)
+    page_prefix_block(a);
+  else
+    qprep_block(a, blockIdx.x, rt);
 }
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -644,10 +658,12 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
 
 // Merge the partials of each (sequence, query head) over the work-groups whose ranges met the
 // sequence, then undo the value rotation (o = o' R_V^T, unless W_O arrives pre-folded).
-// Block (sequence, KV head), thread c = channel.
-__global__ __launch_bounds__(128) void merge_flat_kernel(DecodeArgs a, int G, int unrotate, float* __restrict__ out) {
-  __shared__ float os[kHeadDim];
-  const int b = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+// Block (sequence, KV head), thread c = channel; the G_q query heads of the block share one pass
+// over R_V (row c of R_V per thread).
+__global__ __launch_bounds__(128) void merge_flat_kernel(DecodeArgs a, int G, int unrotate, float* __restrict__ out,
+                                                         uint16_t* __restrict__ ob) {
+  __shared__ float os[8][kHeadDim];
+  const int b = blockIdx.x, h = blockIdx.y, c = threadIdx.x, gq = a.gq;
   const int P = a.prefix[a.B];
   const int Sb = a.prefix[b], Sb1 = a.prefix[b + 1];
   int ga = 0, gb = -1;
@@ -660,50 +676,75 @@ __global__ __launch_bounds__(128) void merge_flat_kernel(DecodeArgs a, int G, in
     while (gb > 0 && range_lo(gb, P, G) > Sb1 - 1) --gb;
     while (range_lo(gb + 1, P, G) <= Sb1 - 1) ++gb;
   }
-  const float* Rv = a.R_v + (size_t)h * kHeadDim * kHeadDim;
-  for (int jj = 0; jj < a.gq; ++jj) {
-    const int j = h * a.gq + jj;
-    float M = -INFINITY;
-    for (int gg = ga; gg <= gb; ++gg) {
-      if (range_lo(gg, P, G) >= range_lo(gg + 1, P, G)) continue;  // empty range wrote nothing
-      M = fmaxf(M, a.part[((size_t)(gg + b) * a.Hq + j) * kPartStride]);
-    }
-    float lsum = 0.0f, osum = 0.0f;
-    for (int gg = ga; gg <= gb; ++gg) {
-      if (range_lo(gg, P, G) >= range_lo(gg + 1, P, G)) continue;
-      const float* pp = a.part + ((size_t)(gg + b) * a.Hq + j) * kPartStride;
-      const float f = pp[0] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(pp[0] - M);
-      lsum = fmaf(f, pp[1], lsum);
-      osum = fmaf(f, pp[4 + c], osum);
-    }
-    const float val = lsum > 0.0f ? osum / lsum : 0.0f;
-    float res = val;
-    if (unrotate) {
-      os[c] = val;
-      __syncthreads();
-      const float4* row = reinterpret_cast<const float4*>(Rv + (size_t)c * kHeadDim);
-      float acc = 0.0f;
-#pragma unroll 8
-      for (int i = 0; i < kHeadDim / 4; ++i) {
-        const float4 rr = row[i];
-        acc = fmaf(os[4 * i], rr.x, acc);
-        acc = fmaf(os[4 * i + 1], rr.y, acc);
-        acc = fmaf(os[4 * i + 2], rr.z, acc);
-        acc = fmaf(os[4 * i + 3], rr.w, acc);
-      }
-      res = acc;
-      __syncthreads();
-    }
-    out[((size_t)b * a.Hq + j) * kHeadDim + c] = res;
+  // one pass over the groups with a running max, all query heads of the block together (their
+  // loads are independent, so each group costs one round trip)
+  float M[8], lsum[8], osum[8], val[8];
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) {
+    M[jj] = -INFINITY;
+    lsum[jj] = 0.0f;
+    osum[jj] = 0.0f;
   }
+  for (int gg = ga; gg <= gb; ++gg) {
+    if (range_lo(gg, P, G) >= range_lo(gg + 1, P, G)) continue;  // empty range wrote nothing
+    const float* base = a.part + ((size_t)(gg + b) * a.Hq + h * gq) * kPartStride;
+    float mv[8], lv[8], ov[8];
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {  // every load first, then the arithmetic (no load behind a test)
+      const float* pp = base + min(jj, gq - 1) * kPartStride;
+      mv[jj] = pp[0];
+      lv[jj] = pp[1];
+      ov[jj] = pp[4 + c];
+    }
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      // a partial with no cached token has m = -inf (or the scan's finite floor) and l = 0
+      const bool valid = mv[jj] != -INFINITY;
+      const float Mn = valid ? fmaxf(M[jj], mv[jj]) : M[jj];
+      const float fa = valid ? __builtin_amdgcn_exp2f(M[jj] - Mn) : 1.0f;
+      const float fb = valid ? __builtin_amdgcn_exp2f(mv[jj] - Mn) : 0.0f;
+      lsum[jj] = fmaf(lsum[jj], fa, fb * lv[jj]);
+      osum[jj] = fmaf(osum[jj], fa, fb * ov[jj]);
+      M[jj] = Mn;
+    }
+  }
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) val[jj] = lsum[jj] > 0.0f ? osum[jj] / lsum[jj] : 0.0f;
+  if (unrotate) {
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj)
+      if (jj < gq) os[jj][c] = val[jj];
+    __syncthreads();
+    const float4* row = reinterpret_cast<const float4*>(a.R_v + ((size_t)h * kHeadDim + c) * kHeadDim);
+    float acc[8];
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) acc[jj] = 0.0f;
+#pragma unroll 4
+    for (int i = 0; i < kHeadDim / 4; ++i) {
+      const float4 rr = row[i];
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        if (jj < gq) {
+          acc[jj] = fmaf(os[jj][4 * i], rr.x, acc[jj]);
+          acc[jj] = fmaf(os[jj][4 * i + 1], rr.y, acc[jj]);
+          acc[jj] = fmaf(os[jj][4 * i + 2], rr.z, acc[jj]);
+          acc[jj] = fmaf(os[jj][4 * i + 3], rr.w, acc[jj]);
+        }
+      }
+    }
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) val[jj] = acc[jj];
+  }
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj)
+    if (jj < gq)
+      store_head_out(val[jj], out, ob, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c,
+                     (size_t)a.B * a.Hq * kHeadDim);
 }
 
 hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
   if (a.gq > 8) return hipErrorNotSupported;
-  hipLaunchKernelGGL(page_prefix_kernel, dim3(1), dim3(1024), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(qprep_kernel, dim3(a.B * a.H), dim3(256), 0, s, a, (a.gq + 3) / 4);
+  hipLaunchKernelGGL(qprep_kernel, dim3(a.B * a.H + 1), dim3(256), 0, s, a, (a.gq + 3) / 4);
   return hipGetLastError();
 }
 
@@ -719,8 +760,9 @@ hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, hipStream_t s) {
-  hipLaunchKernelGGL(merge_flat_kernel, dim3(a.B, a.H), dim3(128), 0, s, a, a.grid_g, unrotate ? 1 : 0, out);
+hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, hipStream_t s) {
+  if (a.gq > 8) return hipErrorNotSupported;
+  hipLaunchKernelGGL(merge_flat_kernel, dim3(a.B, a.H), dim3(128), 0, s, a, a.grid_g, unrotate ? 1 : 0, out, ob);
   return hipGetLastError();
 }
 

@@ -19,9 +19,6 @@ hipError_t launch_fold_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_f, 
                           int H, hipStream_t s);
 hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_rot, const int32_t* slots,
                                int n, float clip_k, float clip_v, hipStream_t s);
-hipError_t launch_append_valu(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots,
-                              int n, const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
-                              float clip_v, hipStream_t s);
 hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots,
                               int n, const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
                               float clip_v, hipStream_t s);
@@ -63,9 +60,12 @@ hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s);
 size_t qop_bytes(int B, int H, int gq);
-hipError_t launch_merge(const DecodeArgs& a, bool unrotate, float* out, hipStream_t s);
-hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, hipStream_t s);
-hipError_t launch_wo_gemm(const float* o, const uint16_t* W, float* y, float* partial, int B, int K,
+// merges write fp32 head outputs to `out`, or (ob != NULL) the two bf16 terms of each value for
+// the output projection: ob[0 .. B*Hq*128) = hi, ob[B*Hq*128 ..) = lo
+hipError_t launch_merge(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, hipStream_t s);
+hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, hipStream_t s);
+int wo_ksplit(int K);  // K slices of the output projection (partial products in the workspace)
+hipError_t launch_wo_gemm(const uint16_t* ob, const uint16_t* W, float* y, float* partial, int B, int K,
                           int N, int ksplit, hipStream_t s);
 
 }  // namespace int2kv

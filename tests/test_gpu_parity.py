@@ -98,12 +98,14 @@ DECODE_CASES = [
     (4, 2, 5, 1, [700, 64], None),
     (1, 4, 32, 8, [1000, 33, 16, 0], None),
     (4, 3, 10, 2, [1500, 2, 129], 256),
+    # two batch blocks and four K slices of the output projection (K = 40 * 128)
+    (4, 66, 40, 8, [17 + 5 * i for i in range(66)], 1024),
 ]
 
 
 @pytest.mark.parametrize("variant", [1, 2])
 @pytest.mark.parametrize("chunk", [0, 64])
-@pytest.mark.parametrize("case", DECODE_CASES, ids=lambda c: f"cfg{c[0]}-B{c[1]}-{c[2]}x{c[3]}-dm{c[5]}")
+@pytest.mark.parametrize("case", DECODE_CASES, ids=lambda c: f"cfg{c[0]}-B{c[1]}-{c[2]}x{c[3]}-dm{c[5]}-L{max(c[4])}")
 def test_decode_matches_oracle(case, chunk, variant):
     cfg, B, Hq, H, lens, dm = case
     print(f"\n[decode] case={case} chunk={chunk} variant={variant}", flush=True)
