@@ -118,8 +118,8 @@ def cpu_baseline(w, target_s):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--chunk", type=int, default=0, help="context chunk in tokens (0 = automatic)")
     ap.add_argument("--variant", type=int, default=0, help="decode scan variant (0 auto, 1 VALU, 2 MFMA)")
