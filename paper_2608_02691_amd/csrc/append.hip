@@ -152,38 +152,69 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
   __shared__ __attribute__((aligned(16))) uint16_t rt[2][kHeadDim][kApRow];  // [hi, lo][c][i] = R[i][c]
   const int h = blockIdx.y, kv = blockIdx.z, H = cv.num_kv_heads, tid = threadIdx.x;
   const float* R = (kv == 0 ? R_k : R_v) + (size_t)h * kHeadDim * kHeadDim;
+  const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
+  const uint16_t* X = kv == 0 ? k : v;
+  // the first tile's operands and slots are fetched before R, so their latency overlaps R's
+  const int tile0 = blockIdx.x * kApWaves + w;
+  ap_bf16x8_t A0[4];
+  int slot0[4];
+  if (tile0 * 16 < n) {
+    const uint16_t* xrow = X + ((size_t)min(tile0 * 16 + lo, n - 1) * H + h) * kHeadDim + 8 * hi;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) A0[ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int tok = tile0 * 16 + 4 * hi + r;
+      slot0[r] = tok < n ? slots[tok] : -1;
+    }
+  }
   {
-    // R with 16 independent 16-byte loads per thread (one round trip), then transposed into LDS
-    const float4* R4 = reinterpret_cast<const float4*>(R);
-    float4 rv[16];
+    // R^T as bf16 hi/lo: thread (c, i0) reads R[i0 .. i0 + 7][c] (coalesced over c), converts
+    // the eight values and writes them as one 16-byte row piece per term (conflict-free)
+    const int c = tid & 127, ib = tid >> 7;
+#pragma unroll 2
+    for (int u = 0; u < 8; ++u) {
+      const int i0 = 8 * (ib + 2 * u);
+      float r8[8];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) rv[u] = R4[tid + 256 * u];
-#pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const int e = 4 * (tid + 256 * u), i = e >> 7, c = e & 127;
-      const float r4[4] = {rv[u].x, rv[u].y, rv[u].z, rv[u].w};
+      for (int q = 0; q < 8; ++q) r8[q] = R[(i0 + q) * kHeadDim + c];
+      uint32_t hw[4], lw[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const uint32_t rh = f32_to_bf16_rne(r4[q]);
-        rt[0][c + q][i] = (uint16_t)rh;
-        rt[1][c + q][i] = (uint16_t)f32_to_bf16_rne(r4[q] - __uint_as_float(rh << 16));
+        const uint32_t h0 = f32_to_bf16_rne(r8[2 * q]), h1 = f32_to_bf16_rne(r8[2 * q + 1]);
+        hw[q] = h0 | (h1 << 16);
+        lw[q] = f32_to_bf16_rne(r8[2 * q] - __uint_as_float(h0 << 16)) |
+                (f32_to_bf16_rne(r8[2 * q + 1] - __uint_as_float(h1 << 16)) << 16);
       }
+      *reinterpret_cast<uint4*>(&rt[0][c][i0]) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+      *reinterpret_cast<uint4*>(&rt[1][c][i0]) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
     }
   }
   __syncthreads();
-  const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
   float sub[8];
 #pragma unroll
   for (int p = 0; p < 8; ++p) sub[p] = kv == 0 ? mu_rk[(size_t)h * kHeadDim + 16 * p + lo] : 0.0f;
-  const uint16_t* X = kv == 0 ? k : v;
   const float clip = kv == 0 ? clip_k : clip_v;
   const int nslots = cv.num_blocks * kBlock;
-  for (int tile = blockIdx.x * kApWaves + w; tile * 16 < n; tile += gridDim.x * kApWaves) {
+  for (int tile = tile0; tile * 16 < n; tile += gridDim.x * kApWaves) {
     const int tok0 = tile * 16;
-    const uint16_t* xrow = X + ((size_t)min(tok0 + lo, n - 1) * H + h) * kHeadDim + 8 * hi;
     ap_bf16x8_t A[4];
+    int slot[4];
+    if (tile == tile0) {
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) A[ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
+      for (int ks = 0; ks < 4; ++ks) A[ks] = A0[ks];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) slot[r] = slot0[r];
+    } else {
+      const uint16_t* xrow = X + ((size_t)min(tok0 + lo, n - 1) * H + h) * kHeadDim + 8 * hi;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) A[ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int tok = tok0 + 4 * hi + r;
+        slot[r] = tok < n ? slots[tok] : -1;
+      }
+    }
     ap_f4_t acc[8];
 #pragma unroll
     for (int p = 0; p < 8; ++p) acc[p] = ap_f4_t{0.f, 0.f, 0.f, 0.f};
@@ -204,7 +235,6 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
       }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int tok = tok0 + 4 * hi + r;
       float x[8];
 #pragma unroll
       for (int p = 0; p < 8; ++p) x[p] = acc[p][r] - sub[p];
@@ -220,9 +250,9 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
         half |= int2_code(x[2 * g + 1], zf, inv) << (4 * g + 2);
         meta[g] = s_bits | (z_bits << 16);
       }
-      const int slot = tok < n ? slots[tok] : -1;
-      if (slot >= 0 && slot < nslots) {
-        const int blk = slot >> 4, t = slot & 15;
+      const int sl = slot[r];
+      if (sl >= 0 && sl < nslots) {
+        const int blk = sl >> 4, t = sl & 15;
         uint8_t* rec = cv.pool + ((size_t)blk * H + h) * kRecord;
         const uint32_t my = lo == 0 ? meta[0] : lo == 1 ? meta[1] : lo == 2 ? meta[2] : meta[3];
         if (kv == 0) {

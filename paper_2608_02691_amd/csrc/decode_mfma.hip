@@ -78,85 +78,137 @@ __device__ __forceinline__ int seq_len_m(const DecodeArgs& a, int b) {
 // per-head power of two sigma (max |q' sigma| in [256, 512)), laid out as the MFMA A operand of the
 // score contraction: row (j, g) of tile r holds q'_j on the channels of group g, times 2^e of the
 // channel's code position, as fp16. Constants per row: -sum_k A_k (accumulator start),
-// sum_{k in g} q'_jk (for the zero term) and 1/sigma. Thread (half, c): channel c of the query
-// heads jj = half, half + 2, ...
-__device__ void qprep_block(const DecodeArgs& a, int bh, int rt) {
-  __shared__ __attribute__((aligned(16))) float Rs[kHeadDim * kHeadDim];  // R_K of head h
-  __shared__ float qin[8][kHeadDim];
-  __shared__ float qr[8][kHeadDim];
-  __shared__ int smax[8];
-  __shared__ float sig[8];
-  const int b = bh / a.H, h = bh % a.H, gq = a.gq, tid = threadIdx.x;
-  const int c = tid & 127, half = tid >> 7;
-  if (tid < 8) smax[tid] = 0;
+// sum_{k in g} q'_jk (for the zero term) and 1/sigma.
+// One block serves KV head h of kQpSeqs sequences: R_K[h] goes once into LDS as the B operand of a
+// bf16 matrix-core product (split into two bf16 terms, as in the cache write: error below
+// 2^-17 |R|); the query rows are exact in bf16. Rows s * 8 + jj = query head jj of sequence
+// b0 + s (16-row tiles, wave w owns tile w).
+constexpr int kQpSeqs = 8;
+constexpr int kQpRow = 136;  // bf16 per LDS row of R^T (128 + 8 pad: conflict-free 16-byte reads)
+typedef __bf16 qp_bf16x8_t __attribute__((ext_vector_type(8)));
+
+__device__ void qprep_block(const DecodeArgs& a, int blk, int rt) {
+  __shared__ __attribute__((aligned(16))) uint16_t Rt[2][kHeadDim][kQpRow];     // [hi, lo][c][k] = R[k][c]
+  __shared__ __attribute__((aligned(16))) float qb[8 * kQpSeqs][kHeadDim + 4];  // q' rows
+  __shared__ int smax[8 * kQpSeqs];
+  __shared__ float sig[8 * kQpSeqs];
+  const int H = a.H, gq = a.gq, tid = threadIdx.x;
+  const int h = blk % H, b0 = kQpSeqs * (blk / H), nseq = min(kQpSeqs, a.B - b0);
+  const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
+  if (tid < 8 * kQpSeqs) smax[tid] = 0;
+  // A operand (query rows 16 w + lo, 8 consecutive channels per lane), fetched before R so the
+  // two latencies overlap; absent rows are zero
+  qp_bf16x8_t A[4];
   {
-    // all of R_K[h] with 16 independent 16-byte loads per thread (one round trip)
-    const float4* Rg = reinterpret_cast<const float4*>(a.R_k + (size_t)h * kHeadDim * kHeadDim);
-    float4 rv[16];
+    const int row = 16 * w + lo, sq = row >> 3, jj = row & 7;
+    const bool ok = sq < nseq && jj < gq;
+    const uint16_t* qr = a.q + ((size_t)(b0 + (ok ? sq : 0)) * a.Hq + h * gq + (ok ? jj : 0)) * kHeadDim + 8 * hi;
 #pragma unroll
-    for (int u = 0; u < 16; ++u) rv[u] = Rg[tid + 256 * u];
-#pragma unroll
-    for (int u = 0; u < 16; ++u) reinterpret_cast<float4*>(Rs)[tid + 256 * u] = rv[u];
+    for (int ks = 0; ks < 4; ++ks) {
+      const uint4 v = *reinterpret_cast<const uint4*>(qr + 32 * ks);
+      A[ks] = __builtin_bit_cast(qp_bf16x8_t, ok ? v : make_uint4(0u, 0u, 0u, 0u));
+    }
   }
-  for (int i = tid; i < gq * kHeadDim; i += 256) {
-    const int jj = i / kHeadDim, cc = i % kHeadDim;
-    qin[jj][cc] = bf16_bits_to_f32(a.q[((size_t)b * a.Hq + h * gq + jj) * kHeadDim + cc]);
-  }
-  __syncthreads();
-  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // query heads half, half + 2, half + 4, half + 6
-#pragma unroll 8
-  for (int k = 0; k < kHeadDim; ++k) {
-    const float r = Rs[k * kHeadDim + c];
+  {
+    // R^T as bf16 hi/lo: thread (c, k0) reads R[k0 .. k0 + 7][c] (coalesced over c) and writes one
+    // 16-byte row piece per term
+    const float* R = a.R_k + (size_t)h * kHeadDim * kHeadDim;
+    const int c = tid & 127, kb = tid >> 7;
+#pragma unroll 2
+    for (int u = 0; u < 8; ++u) {
+      const int k0 = 8 * (kb + 2 * u);
+      float r8[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) acc[u] = fmaf(qin[half + 2 * u][k], r, acc[u]);
-  }
+      for (int q = 0; q < 8; ++q) r8[q] = R[(k0 + q) * kHeadDim + c];
+      uint32_t hw[4], lw[4];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int jj = half + 2 * u;
-    if (jj < gq) {
-      const float v = acc[u] * kLogit2;
-      qr[jj][c] = v;
-      atomicMax(&smax[jj], __float_as_int(fabsf(v)));  // non-negative floats order like their bits
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t h0 = f32_to_bf16_rne(r8[2 * q]), h1 = f32_to_bf16_rne(r8[2 * q + 1]);
+        hw[q] = h0 | (h1 << 16);
+        lw[q] = f32_to_bf16_rne(r8[2 * q] - __uint_as_float(h0 << 16)) |
+                (f32_to_bf16_rne(r8[2 * q + 1] - __uint_as_float(h1 << 16)) << 16);
+      }
+      *reinterpret_cast<uint4*>(&Rt[0][c][k0]) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+      *reinterpret_cast<uint4*>(&Rt[1][c][k0]) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
     }
   }
   __syncthreads();
-  if (tid < 8) {
+  // D[row][c] of n-tile p sits in lane (c % 16) + 16 (row / 4), register row % 4
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    float4_t d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const qp_bf16x8_t bh = *reinterpret_cast<const qp_bf16x8_t*>(&Rt[0][16 * p + lo][32 * ks + 8 * hi]);
+      const qp_bf16x8_t bl = *reinterpret_cast<const qp_bf16x8_t*>(&Rt[1][16 * p + lo][32 * ks + 8 * hi]);
+      d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[ks], bh, d, 0, 0, 0);
+      d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[ks], bl, d, 0, 0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) qb[16 * w + 4 * hi + r][16 * p + lo] = d[r] * kLogit2;
+  }
+  __syncthreads();
+  {
+    // per-row max |q'|: thread -> (row, 32-channel quarter), then a 4-way LDS max
+    const int row = tid >> 2, qt = tid & 3;
+    float m = 0.0f;
+#pragma unroll 8
+    for (int c = 0; c < 32; ++c) m = fmaxf(m, fabsf(qb[row][32 * qt + c]));
+    atomicMax(&smax[row], __float_as_int(m));  // non-negative floats order like their bits
+  }
+  __syncthreads();
+  if (tid < 8 * kQpSeqs) {
     const float m = __int_as_float(smax[tid]);
     int ex = 0;
     frexpf(m, &ex);
-    sig[tid] = tid < gq && m > 0.0f ? ldexpf(1.0f, max(-100, min(100, 9 - ex))) : 1.0f;
+    sig[tid] = m > 0.0f ? ldexpf(1.0f, max(-100, min(100, 9 - ex))) : 1.0f;
   }
   __syncthreads();
-  uint8_t* out = a.qop + (size_t)bh * rt * kQopTile;
-  for (int idx = tid; idx < rt * 2048; idx += 256) {
-    const int r = idx / 2048, rem = idx % 2048;
-    const int i = rem / 512, l = (rem / 8) % 64, s = rem % 8;
-    const int m = l & 15, q = l >> 4, jj = 4 * r + (m >> 2), g = m & 3;
-    const int rr = s >> 1, hh = s & 1, x = 2 * i + (rr >> 1), d = rr & 1;
-    const int ch = 16 * x + 4 * q + 2 * d + hh;
-    _Float16 v = (_Float16)0.0f;
-    if (g == i && jj < gq) v = (_Float16)(qr[jj][ch] * sig[jj] * (float)(1 << land_e(x)));
-    reinterpret_cast<_Float16*>(out + r * kQopTile + (i * 64 + l) * 16)[s] = v;
-  }
-  // per row (jj, g): sums over the 32 channels of group g, one element per lane of a 32-lane group
-  for (int e = tid; e < rt * 512; e += 256) {
-    const int jj = e / 128, g = (e / 32) % 4, cc = e % 32, ch = 32 * g + cc;
-    float csum = 0.0f, qsum = 0.0f;
-    if (jj < gq) {
-      csum = (float)(_Float16)(qr[jj][ch] * sig[jj] * (float)(1 << land_e(ch >> 4)));
-      qsum = qr[jj][ch];
-    }
+  // A operand chunks: (sequence, tile r, k block i, lane l) -> 8 fp16 values. Row (jj, g) of lane
+  // l = m + 16 q (jj = 4 r + m / 4, g = m % 4) is nonzero only in block i = g, where its eight
+  // values are channels 32 i + 4 q + 0..3 (code position x = 2 i) and 32 i + 16 + 4 q + 0..3
+  // (x = 2 i + 1), scaled by sigma and 2^e(x).
+  for (int cidx = tid; cidx < nseq * rt * 256; cidx += 256) {
+    const int sq = cidx / (rt * 256), r = (cidx / 256) % rt, i = (cidx / 64) % 4, l = cidx % 64;
+    const int m = l & 15, q = l >> 4, jj = 4 * r + (m >> 2), g = m & 3, row = 8 * sq + jj;
+    uint32_t packed[4] = {0u, 0u, 0u, 0u};
+    if (g == i && jj < gq) {
+      const float4 lo4 = *reinterpret_cast<const float4*>(&qb[row][32 * i + 4 * q]);
+      const float4 hi4 = *reinterpret_cast<const float4*>(&qb[row][32 * i + 16 + 4 * q]);
+      const float s0 = sig[row] * (float)(1 << land_e(2 * i)), s1 = sig[row] * (float)(1 << land_e(2 * i + 1));
+      const float v[8] = {lo4.x * s0, lo4.y * s0, lo4.z * s0, lo4.w * s0, hi4.x * s1, hi4.y * s1, hi4.z * s1, hi4.w * s1};
 #pragma unroll
-    for (int off = 16; off >= 1; off >>= 1) {
-      csum += __shfl_xor(csum, off, 32);
-      qsum += __shfl_xor(qsum, off, 32);
+      for (int u = 0; u < 4; ++u) {
+        const _Float16 h0 = (_Float16)v[2 * u], h1 = (_Float16)v[2 * u + 1];
+        packed[u] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+      }
     }
-    if (cc == 0) {
+    uint8_t* out = a.qop + ((size_t)(b0 + sq) * H + h) * rt * kQopTile;
+    *reinterpret_cast<uint4*>(out + r * kQopTile + (i * 64 + l) * 16) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+  }
+  // per row (jj, g) of a tile: -sum of its 32 fp16 A values, sum of q' over group g, 1/sigma;
+  // thread -> (row, g), a sequential sum over the group's channels
+  {
+    const int row = tid >> 2, g = tid & 3, sq = row >> 3, jj = row & 7;
+    if (sq < nseq && jj < 4 * rt) {
+      float csum = 0.0f, qsum = 0.0f;
+      if (jj < gq) {
+        const float s0 = sig[row] * (float)(1 << land_e(2 * g)), s1 = sig[row] * (float)(1 << land_e(2 * g + 1));
+#pragma unroll
+        for (int c4 = 0; c4 < 8; ++c4) {
+          const float4 v = *reinterpret_cast<const float4*>(&qb[row][32 * g + 4 * c4]);
+          const float sc = c4 < 4 ? s0 : s1;  // channels 32 g + 0..15 sit at code position 2 g
+          csum += (float)(_Float16)(v.x * sc) + (float)(_Float16)(v.y * sc) + (float)(_Float16)(v.z * sc) +
+                  (float)(_Float16)(v.w * sc);
+          qsum += v.x + v.y + v.z + v.w;
+        }
+      }
       const int r = jj / 4, jl = jj % 4;
+      uint8_t* out = a.qop + ((size_t)(b0 + sq) * H + h) * rt * kQopTile;
       float* cst = reinterpret_cast<float*>(out + r * kQopTile + 4096);
       cst[jl * 4 + g] = -csum;
       cst[16 + jl * 4 + g] = qsum;
-      if (g == 0) cst[32 + jl] = jj < gq ? 1.0f / sig[jj] : 0.0f;
+      if (g == 0) cst[32 + jl] = jj < gq ? 1.0f / sig[row] : 0.0f;
     }
   }
 }
@@ -458,12 +510,13 @@ __device__ void page_prefix_block(const DecodeArgs& a) {
   if (tid == 255) a.prefix[a.B] = P;
 }
 
-// Blocks 0 .. B*H-1: query operands of (b, h); the last block: page prefix sums.
+// Block 0: page prefix sums (first, so it never waits for a free slot); blocks 1 ..: query
+// operands of KV head h for kQpSeqs sequences.
 __global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int rt) {
-  if (blockIdx.x == gridDim.x - 1)
+  if (blockIdx.x == 0)
     page_prefix_block(a);
   else
-    qprep_block(a, blockIdx.x, rt);
+    qprep_block(a, blockIdx.x - 1, rt);
 }
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -744,7 +797,8 @@ __global__ __launch_bounds__(128) void merge_flat_kernel(DecodeArgs a, int G, in
 
 hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
   if (a.gq > 8) return hipErrorNotSupported;
-  hipLaunchKernelGGL(qprep_kernel, dim3(a.B * a.H + 1), dim3(256), 0, s, a, (a.gq + 3) / 4);
+  hipLaunchKernelGGL(qprep_kernel, dim3(1 + a.H * ((a.B + kQpSeqs - 1) / kQpSeqs)), dim3(256), 0, s, a,
+                     (a.gq + 3) / 4);
   return hipGetLastError();
 }
 
