@@ -279,7 +279,9 @@ __device__ __forceinline__ uint32_t stage_pair(const uint8_t* pool, const uint8_
   return (ok0 ? 1u : 0u) | (ok1 ? 2u : 0u);
 }
 
-// Operands of one page pair read back from its staging slot.
+// Operands of one page pair read back from its staging slot. A page that holds no cached tokens
+// (past the segment, or a block id outside the pool) stages a stand-in record; its scores are
+// masked to -inf, so p = 0 multiplies its (finite) codes and metadata and it adds nothing.
 // An empty asm that uses every register read_pair filled: the compiler places its wait for those
 // LDS reads here, ahead of the scalar block-id loads that follow (a later wait would have to
 // wait for those loads too, since scalar loads return out of order).
@@ -304,16 +306,6 @@ __device__ __forceinline__ void read_pair(const uint8_t* slot, bool ok0, bool ok
     p.vz[P] = *reinterpret_cast<const uint2*>(rec + kOffVZero + 32 * (lo & 3) + 8 * hi);
   }
 }
-// Zero the value scales and zeros of a page that holds no cached tokens (its staged record is a
-// stand-in), after pin_pair so that the selects do not pull the LDS wait forward.
-__device__ __forceinline__ void mask_pair(PairLoads& p) {
-#pragma unroll
-  for (int P = 0; P < 2; ++P) {
-    p.vs[P] = p.ok[P] ? p.vs[P] : make_uint2(0u, 0u);
-    p.vz[P] = p.ok[P] ? p.vz[P] : make_uint2(0u, 0u);
-  }
-}
-
 template <int X>
 __device__ __forceinline__ half8_t k_operand(uint2 w) {
   // instruction i = X/2 ... called with X = 2i: registers (d0,x), (d1,x), (d0,x+1), (d1,x+1)
@@ -575,7 +567,6 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
       wait_vm_all();
     read_pair(stage_w, okmask & 1u, (okmask >> 1) & 1u, lo, hi, X);
     pin_pair(X);
-    mask_pair(X);
     if (kStages < npairs) {
       asm volatile("" : "+s"(nid.b0), "+s"(nid.b1));
       const BlockIds next = load_ids(bt, p0 + 2 * (kStages + 1), p1);
@@ -601,7 +592,6 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
         wait_vm_all();
       read_pair(stage_w + sl * 2 * kRecord, (okmask >> (2 * sl)) & 1u, (okmask >> (2 * sl + 1)) & 1u, lo, hi, nxt);
       pin_pair(nxt);
-      mask_pair(nxt);
       if (STEADY || k + 1 + kStages < npairs) {
         const int page0 = p0 + 2 * (k + 1 + kStages);
         // The ids read one step ago are pinned (their wait placed) before the next loads issue:
