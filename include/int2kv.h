@@ -119,9 +119,9 @@ int int2kv_quantize_pack_rotated(const int2kv_cache* cache, const float* k_rot, 
  *   slot_mapping : int32 [n]; negative = skip; distinct slots
  *   R_k, R_v     : fp32 [H_kv, 128, 128], 16-byte aligned;  mu_rk: fp32 [H_kv, 128] from
  *                  int2kv_prepare_mu_rot
- * The rotation runs on the matrix cores with R split into two bf16 terms (R_hi + R_lo, error
- * below 2^-17 |R|), so codes may differ from an exact-arithmetic rotation only where x sits at
- * a rounding boundary of the quantizer. */
+ * The rotation runs on the matrix cores with R split into three bf16 terms (exact products, fp32
+ * accumulation starting from -mu R_K), so codes may differ from an exact-arithmetic rotation only
+ * where x sits at a rounding boundary of the quantizer. */
 int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
                            const int32_t* slot_mapping, int num_tokens, const float* R_k,
                            const float* R_v, const float* mu_rk, float clip_k, float clip_v,
@@ -161,8 +161,9 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
 int int2kv_set_decode_events(hipEvent_t before_scan, hipEvent_t after_scan);
 
 /* Tuning knobs for measurement sweeps: context chunk in tokens (multiple of 64, 0 = automatic)
- * and decode kernel variant (0 = automatic, 1 = vector ALU, 2 = matrix core). Returns
- * INT2KV_EINVAL for out-of-range values. Workspace sizes depend on the chunk. */
+ * and decode kernel variant (0 = automatic, 1 = vector ALU, 2 = matrix core; the matrix-core scan
+ * serves at most 8 query heads per KV head, wider groups always use the vector-ALU scan). Returns
+ * INT2KV_EINVAL for out-of-range values. Workspace sizes depend on both. */
 int int2kv_set_decode_tuning(int chunk_tokens, int variant);
 
 #ifdef __cplusplus

@@ -73,7 +73,10 @@ int num_cus() {
 DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   DecodePlan p{};
   const int gq = Hq / H;
-  p.variant = g_variant_override ? g_variant_override : (gq <= 8 && mfma_decode_available() ? 2 : 1);
+  // the matrix-core scan serves up to 8 query heads per KV head; wider groups use the vector-ALU scan
+  // (also when the tuning knob asks for the matrix-core one)
+  const bool mfma_ok = gq <= 8 && mfma_decode_available();
+  p.variant = g_variant_override == 1 || !mfma_ok ? 1 : 2;
   int chunk = g_chunk_override;
   if (chunk <= 0) {
     // the largest chunk (up to 4096 tokens) that still gives >= 1024 work-groups, so that 256 CUs

@@ -129,8 +129,9 @@ hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_r
 
 // ---------------------------------------------------------------------------------------------
 // Append on the matrix cores: x R (x bf16 [n, H, 128], R fp32 [128, 128]) as bf16 MFMA with R split
-// into two bf16 terms (R = R_hi + R_lo + O(2^-18 |R|)), fp32 accumulation; then - mu R_K for keys,
-// the group quantizer and the packed stores. Work-group (KV head h, K or V, a stride of 16-token
+// into three bf16 terms (R = R_1 + R_2 + R_3 + O(2^-27 |R|): every product is exact and the sum is
+// an fp32 accumulation, like an fp32 GEMM), starting from - mu R_K for keys; then the group
+// quantizer and the packed stores. Work-group (KV head h, K or V, a stride of 16-token
 // tiles); R^T of the work-group's (h, K|V) is converted once into LDS as the B operand.
 // Tile layout: D[token][channel] of n-tile p (channels 16p .. 16p + 15) sits in lane
 // (channel % 16) + 16 (token / 4), register token % 4, so lane m holds channels m + 16p, p = 0..7,
@@ -149,7 +150,7 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
                                                            const float* __restrict__ R_v,
                                                            const float* __restrict__ mu_rk, float clip_k,
                                                            float clip_v) {
-  __shared__ __attribute__((aligned(16))) uint16_t rt[2][kHeadDim][kApRow];  // [hi, lo][c][i] = R[i][c]
+  __shared__ __attribute__((aligned(16))) uint16_t rt[3][kHeadDim][kApRow];  // [term][c][i] = R[i][c]
   const int h = blockIdx.y, kv = blockIdx.z, H = cv.num_kv_heads, tid = threadIdx.x;
   const float* R = (kv == 0 ? R_k : R_v) + (size_t)h * kHeadDim * kHeadDim;
   const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
@@ -169,25 +170,28 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
     }
   }
   {
-    // R^T as bf16 hi/lo: thread (c, i0) reads R[i0 .. i0 + 7][c] (coalesced over c), converts
-    // the eight values and writes them as one 16-byte row piece per term (conflict-free)
+    // R^T as three bf16 terms: thread (c, i0) reads R[i0 .. i0 + 7][c] (coalesced over c), splits
+    // the eight values (each remainder is exact in fp32) and writes one 16-byte row piece per term
+    // (conflict-free)
     const int c = tid & 127, ib = tid >> 7;
 #pragma unroll 2
     for (int u = 0; u < 8; ++u) {
       const int i0 = 8 * (ib + 2 * u);
-      float r8[8];
+      uint32_t t16[3][8];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) r8[q] = R[(i0 + q) * kHeadDim + c];
-      uint32_t hw[4], lw[4];
+      for (int q = 0; q < 8; ++q) {
+        float r = R[(i0 + q) * kHeadDim + c];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t h0 = f32_to_bf16_rne(r8[2 * q]), h1 = f32_to_bf16_rne(r8[2 * q + 1]);
-        hw[q] = h0 | (h1 << 16);
-        lw[q] = f32_to_bf16_rne(r8[2 * q] - __uint_as_float(h0 << 16)) |
-                (f32_to_bf16_rne(r8[2 * q + 1] - __uint_as_float(h1 << 16)) << 16);
+        for (int term = 0; term < 3; ++term) {
+          t16[term][q] = f32_to_bf16_rne(r);
+          r -= __uint_as_float(t16[term][q] << 16);
+        }
       }
-      *reinterpret_cast<uint4*>(&rt[0][c][i0]) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-      *reinterpret_cast<uint4*>(&rt[1][c][i0]) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+#pragma unroll
+      for (int term = 0; term < 3; ++term)
+        *reinterpret_cast<uint4*>(&rt[term][c][i0]) =
+            make_uint4(t16[term][0] | (t16[term][1] << 16), t16[term][2] | (t16[term][3] << 16),
+                       t16[term][4] | (t16[term][5] << 16), t16[term][6] | (t16[term][7] << 16));
     }
   }
   __syncthreads();
@@ -215,29 +219,30 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
         slot[r] = tok < n ? slots[tok] : -1;
       }
     }
-    ap_f4_t acc[8];
+    ap_f4_t acc[8];  // start at - mu R_K (keys) or 0 (values)
 #pragma unroll
-    for (int p = 0; p < 8; ++p) acc[p] = ap_f4_t{0.f, 0.f, 0.f, 0.f};
+    for (int p = 0; p < 8; ++p) acc[p] = ap_f4_t{-sub[p], -sub[p], -sub[p], -sub[p]};
     // the B fragments are the same for every tile: an opaque offset keeps the compiler from
     // hoisting all 64 of them into registers (which would cap occupancy at one wave per SIMD)
     int boff = (lo * kApRow + 8 * hi) * 2;
     asm volatile("" : "+v"(boff));
     const uint8_t* rb = reinterpret_cast<const uint8_t*>(&rt[0][0][0]) + boff;
+    // smallest term first
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
+    for (int term = 2; term >= 0; --term)
 #pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        const ap_bf16x8_t bh = *reinterpret_cast<const ap_bf16x8_t*>(rb + ((16 * p) * kApRow + 32 * ks) * 2);
-        const ap_bf16x8_t bl =
-            *reinterpret_cast<const ap_bf16x8_t*>(rb + ((kHeadDim + 16 * p) * kApRow + 32 * ks) * 2);
-        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[ks], bh, acc[p], 0, 0, 0);
-        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[ks], bl, acc[p], 0, 0, 0);
-      }
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int p = 0; p < 8; ++p) {
+          const ap_bf16x8_t b =
+              *reinterpret_cast<const ap_bf16x8_t*>(rb + ((term * kHeadDim + 16 * p) * kApRow + 32 * ks) * 2);
+          acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[ks], b, acc[p], 0, 0, 0);
+        }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       float x[8];
 #pragma unroll
-      for (int p = 0; p < 8; ++p) x[p] = acc[p][r] - sub[p];
+      for (int p = 0; p < 8; ++p) x[p] = acc[p][r];
       uint32_t half = 0, meta[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
