@@ -140,10 +140,73 @@ hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_r
 typedef __bf16 ap_bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float ap_f4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kApWaves = 4;
+constexpr int kApWaves = 8;
 constexpr int kApRow = 136;  // bf16 per LDS row of R^T (128 + 8 pad: conflict-free 16-byte reads)
 
-__global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const uint16_t* __restrict__ k,
+// Min and max over the 16 lanes of each DPP row for four (min, max) pairs at once, with DPP-operand
+// min/max instructions: the eight chains are interleaved so every DPP operand was written at least
+// seven instructions earlier, and the leading s_nop covers values written just before the asm.
+// Inputs and results are finite.
+__device__ __forceinline__ void row_minmax16_x4(float (&mn)[4], float (&mx)[4]) {
+#define INT2KV_MM_STEP(CTRL)                                                       \
+  "v_min_f32_dpp %0, %0, %0 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
+  "v_max_f32_dpp %4, %4, %4 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
+  "v_min_f32_dpp %1, %1, %1 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
+  "v_max_f32_dpp %5, %5, %5 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
+  "v_min_f32_dpp %2, %2, %2 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
+  "v_max_f32_dpp %6, %6, %6 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
+  "v_min_f32_dpp %3, %3, %3 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
+  "v_max_f32_dpp %7, %7, %7 " CTRL " row_mask:0xf bank_mask:0xf\n\t"
+  asm volatile("s_nop 1\n\t" INT2KV_MM_STEP("row_ror:8") INT2KV_MM_STEP("row_ror:4") INT2KV_MM_STEP("row_ror:2")
+                   INT2KV_MM_STEP("row_ror:1")
+               : "+v"(mn[0]), "+v"(mn[1]), "+v"(mn[2]), "+v"(mn[3]), "+v"(mx[0]), "+v"(mx[1]), "+v"(mx[2]),
+                 "+v"(mx[3]));
+#undef INT2KV_MM_STEP
+}
+
+// x / 3 correctly rounded, as a product with RN(1/3) and one FMA correction: checked against the
+// correctly rounded quotient for every fp32 significand (so for every x whose intermediate values
+// stay normal: x == 0 or x >= 2^-100; the caller routes other x to a division).
+__device__ __forceinline__ float div3_rn(float x) {
+#pragma clang fp contract(off)
+  const float c = 0x1.555556p-2f;  // RN(1/3)
+  const float q0 = x * c;
+  const float r = __builtin_fmaf(-q0, 3.0f, x);
+  return __builtin_fmaf(r, c, q0);
+}
+
+// The quantizer's group parameters (bit-identical to int2_group_params): s = fp16((mx - mn) / 3)
+// with the division above, and 1/s from a table of the correctly rounded reciprocals of the 1024
+// normal fp16 significands (exact after the power-of-two scaling); zero, fp16-subnormal and
+// infinite scales and tiny ranges take the division.
+__device__ __forceinline__ void int2_group_params_fast(float mn, float mx, float clip, const float* recip_tab,
+                                                       uint32_t& s_bits, uint32_t& z_bits, float& zf, float& inv) {
+#pragma clang fp contract(off)
+  if (clip != 1.0f) {
+    mn = clip * mn;
+    mx = clip * mx;
+  }
+  const float range = mx - mn;
+  float s32;
+  if (range != 0.0f && range < 0x1p-100f)
+    s32 = range / 3.0f;
+  else
+    s32 = div3_rn(range);
+  const __half s = __float2half_rn(s32);
+  const __half z = __float2half_rn(mn);
+  s_bits = __half_as_ushort(s);
+  z_bits = __half_as_ushort(z);
+  zf = __half2float(z);
+  const uint32_t e16 = (s_bits >> 10) & 31u;
+  if (e16 == 0u || e16 == 31u) {  // zero, fp16-subnormal or infinite scale
+    const float sf = __half2float(s);
+    inv = sf > 0.0f ? 1.0f / sf : 0.0f;
+  } else {
+    inv = __builtin_ldexpf(recip_tab[s_bits & 1023u], 15 - (int)e16);
+  }
+}
+
+__global__ __launch_bounds__(512) void append_mfma_kernel(CacheView cv, const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v,
                                                            const int32_t* __restrict__ slots, int n,
                                                            const float* __restrict__ R_k,
@@ -151,6 +214,7 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
                                                            const float* __restrict__ mu_rk, float clip_k,
                                                            float clip_v) {
   __shared__ __attribute__((aligned(16))) uint16_t rt[3][kHeadDim][kApRow];  // [term][c][i] = R[i][c]
+  __shared__ float recip_tab[1024];  // RN(1 / (1 + m / 1024))
   const int h = blockIdx.y, kv = blockIdx.z, H = cv.num_kv_heads, tid = threadIdx.x;
   const float* R = (kv == 0 ? R_k : R_v) + (size_t)h * kHeadDim * kHeadDim;
   const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
@@ -175,8 +239,8 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
     // (conflict-free)
     const int c = tid & 127, ib = tid >> 7;
 #pragma unroll 2
-    for (int u = 0; u < 8; ++u) {
-      const int i0 = 8 * (ib + 2 * u);
+    for (int u = 0; u < 4; ++u) {
+      const int i0 = 8 * (ib + 4 * u);
       uint32_t t16[3][8];
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
@@ -194,29 +258,34 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
                        t16[term][4] | (t16[term][5] << 16), t16[term][6] | (t16[term][7] << 16));
     }
   }
+  for (int m = tid; m < 1024; m += 64 * kApWaves) recip_tab[m] = 1.0f / (1.0f + (float)m * 0x1p-10f);
   __syncthreads();
   float sub[8];
 #pragma unroll
   for (int p = 0; p < 8; ++p) sub[p] = kv == 0 ? mu_rk[(size_t)h * kHeadDim + 16 * p + lo] : 0.0f;
   const float clip = kv == 0 ? clip_k : clip_v;
   const int nslots = cv.num_blocks * kBlock;
-  for (int tile = tile0; tile * 16 < n; tile += gridDim.x * kApWaves) {
-    const int tok0 = tile * 16;
-    ap_bf16x8_t A[4];
-    int slot[4];
-    if (tile == tile0) {
+  // software pipeline over the wave's tiles: the next tile's operands and slots are fetched while
+  // this one is computed (indexes clamped, so the fetch past the last tile stays in bounds)
+  const int tstride = gridDim.x * kApWaves;
+  ap_bf16x8_t A[4];
+  int slot[4];
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) A[ks] = A0[ks];
+  for (int ks = 0; ks < 4; ++ks) A[ks] = A0[ks];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) slot[r] = slot0[r];
-    } else {
-      const uint16_t* xrow = X + ((size_t)min(tok0 + lo, n - 1) * H + h) * kHeadDim + 8 * hi;
+  for (int r = 0; r < 4; ++r) slot[r] = slot0[r];
+  for (int tile = tile0; tile * 16 < n; tile += tstride) {
+    ap_bf16x8_t An[4];
+    int slotn[4];
+    {
+      const int nt0 = (tile + tstride) * 16;
+      const uint16_t* xrow = X + ((size_t)min(nt0 + lo, n - 1) * H + h) * kHeadDim + 8 * hi;
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) A[ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
+      for (int ks = 0; ks < 4; ++ks) An[ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int tok = tok0 + 4 * hi + r;
-        slot[r] = tok < n ? slots[tok] : -1;
+        const int tok = nt0 + 4 * hi + r;
+        slotn[r] = tok < n ? slots[tok] : -1;
       }
     }
     ap_f4_t acc[8];  // start at - mu R_K (keys) or 0 (values)
@@ -238,33 +307,40 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
               *reinterpret_cast<const ap_bf16x8_t*>(rb + ((term * kHeadDim + 16 * p) * kApRow + 32 * ks) * 2);
           acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[ks], b, acc[p], 0, 0, 0);
         }
+    // group quantizer: per group g, the four rows' lane-local min/max of channels 16 (2g) + lo and
+    // 16 (2g + 1) + lo, then the 16-lane row reductions, parameters and codes
+    uint32_t half[4] = {0u, 0u, 0u, 0u}, meta[4][4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float x[8];
+    for (int g = 0; g < 4; ++g) {
+      float mn[4], mx[4];
 #pragma unroll
-      for (int p = 0; p < 8; ++p) x[p] = acc[p][r];
-      uint32_t half = 0, meta[4];
+      for (int r = 0; r < 4; ++r) {
+        mn[r] = fminf(acc[2 * g][r], acc[2 * g + 1][r]);
+        mx[r] = fmaxf(acc[2 * g][r], acc[2 * g + 1][r]);
+      }
+      row_minmax16_x4(mn, mx);
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const float mn = row_min16(fminf(x[2 * g], x[2 * g + 1]));
-        const float mx = row_max16(fmaxf(x[2 * g], x[2 * g + 1]));
+      for (int r = 0; r < 4; ++r) {
         uint32_t s_bits, z_bits;
         float zf, inv;
-        int2_group_params(mn, mx, clip, s_bits, z_bits, zf, inv);
-        half |= int2_code(x[2 * g], zf, inv) << (4 * g);
-        half |= int2_code(x[2 * g + 1], zf, inv) << (4 * g + 2);
-        meta[g] = s_bits | (z_bits << 16);
+        int2_group_params_fast(mn[r], mx[r], clip, recip_tab, s_bits, z_bits, zf, inv);
+        half[r] |= int2_code(acc[2 * g][r], zf, inv) << (4 * g);
+        half[r] |= int2_code(acc[2 * g + 1][r], zf, inv) << (4 * g + 2);
+        meta[r][g] = s_bits | (z_bits << 16);
       }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
       const int sl = slot[r];
       if (sl >= 0 && sl < nslots) {
         const int blk = sl >> 4, t = sl & 15;
         uint8_t* rec = cv.pool + ((size_t)blk * H + h) * kRecord;
-        const uint32_t my = lo == 0 ? meta[0] : lo == 1 ? meta[1] : lo == 2 ? meta[2] : meta[3];
+        const uint32_t my = lo == 0 ? meta[r][0] : lo == 1 ? meta[r][1] : lo == 2 ? meta[r][2] : meta[r][3];
         if (kv == 0) {
-          *reinterpret_cast<uint16_t*>(rec + kOffKCodes + 32 * t + 2 * lo) = (uint16_t)half;
+          *reinterpret_cast<uint16_t*>(rec + kOffKCodes + 32 * t + 2 * lo) = (uint16_t)half[r];
           if (lo < 4) *reinterpret_cast<uint32_t*>(rec + kOffKMeta + 16 * t + 4 * lo) = my;
         } else {
-          *reinterpret_cast<uint16_t*>(rec + kOffVCodes + 32 * lo + 2 * t) = (uint16_t)half;
+          *reinterpret_cast<uint16_t*>(rec + kOffVCodes + 32 * lo + 2 * t) = (uint16_t)half[r];
           if (lo < 4) {
             *reinterpret_cast<uint16_t*>(rec + kOffVScale + 32 * lo + 2 * t) = (uint16_t)(my & 0xFFFFu);
             *reinterpret_cast<uint16_t*>(rec + kOffVZero + 32 * lo + 2 * t) = (uint16_t)(my >> 16);
@@ -272,6 +348,10 @@ __global__ __launch_bounds__(256) void append_mfma_kernel(CacheView cv, const ui
         }
       }
     }
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) A[ks] = An[ks];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) slot[r] = slotn[r];
   }
 }
 
@@ -279,13 +359,13 @@ hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v,
                               const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
                               float clip_v, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  // enough work-groups to fill the chip at two per CU, each converting R once for many tiles
+  // one work-group per CU (its R^T terms fill most of the LDS), each converting R once for many tiles
   const int tiles = (n + 15) / 16;
-  const int per_head = max(1, 512 / (2 * c.num_kv_heads));
+  const int per_head = max(1, 256 / (2 * c.num_kv_heads));
   const int nx = min((tiles + kApWaves - 1) / kApWaves, per_head);
   dim3 grid(nx, c.num_kv_heads, 2);
-  hipLaunchKernelGGL(append_mfma_kernel, grid, dim3(256), 0, s, c, k, v, slots, n, R_k, R_v, mu_rk, clip_k,
-                     clip_v);
+  hipLaunchKernelGGL(append_mfma_kernel, grid, dim3(64 * kApWaves), 0, s, c, k, v, slots, n, R_k, R_v, mu_rk,
+                     clip_k, clip_v);
   return hipGetLastError();
 }
 
