@@ -118,7 +118,7 @@ int int2kv_quantize_pack_rotated(const int2kv_cache* cache, const float* k_rot, 
  *   k, v         : bf16 [n, H_kv, 128] (post-RoPE keys; values), 16-byte aligned
  *   slot_mapping : int32 [n]; negative = skip; distinct slots
  *   R_k, R_v     : fp32 [H_kv, 128, 128], 16-byte aligned;  mu_rk: fp32 [H_kv, 128] from
- *                  int2kv_prepare_mu_rot
+ *                  int2kv_prepare_mu_rot, 16-byte aligned
  * The rotation runs on the matrix cores with R split into three bf16 terms (exact products, fp32
  * accumulation starting from -mu R_K), so codes may differ from an exact-arithmetic rotation only
  * where x sits at a rounding boundary of the quantizer. */

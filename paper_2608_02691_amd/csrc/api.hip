@@ -179,8 +179,8 @@ int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const u
   if (num_tokens == 0) return ok();
   if (!k || !v || !slot_mapping || !R_k || !R_v || !mu_rk) return fail(INT2KV_EINVAL, "NULL pointer argument");
   if (!valid_clip(clip_k) || !valid_clip(clip_v)) return fail(INT2KV_EINVAL, "clip ratios must be in (0, 1]");
-  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(R_k, 16) || !aligned(R_v, 16))
-    return fail(INT2KV_EINVAL, "k, v, R_k and R_v must be 16-byte aligned");
+  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(R_k, 16) || !aligned(R_v, 16) || !aligned(mu_rk, 16))
+    return fail(INT2KV_EINVAL, "k, v, R_k, R_v and mu_rk must be 16-byte aligned");
   hipError_t e = launch_append_mfma(view(cache), k, v, slot_mapping, num_tokens, R_k, R_v, mu_rk, clip_k, clip_v,
                                     stream);
   return hip_status(e, "quantize_append");

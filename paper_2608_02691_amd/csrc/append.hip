@@ -133,36 +133,17 @@ hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_r
 // an fp32 accumulation, like an fp32 GEMM), starting from - mu R_K for keys; then the group
 // quantizer and the packed stores. Work-group (KV head h, K or V, a stride of 16-token
 // tiles); R^T of the work-group's (h, K|V) is converted once into LDS as the B operand.
-// Tile layout: D[token][channel] of n-tile p (channels 16p .. 16p + 15) sits in lane
-// (channel % 16) + 16 (token / 4), register token % 4, so lane m holds channels m + 16p, p = 0..7,
-// of four tokens: exactly the eight 2-bit codes of half m of the packed layout, and the 32
-// channels of group g are n-tiles 2g, 2g + 1 across the 16 lanes of one DPP row.
+// Tile layout: the product is formed transposed, D^T = R^T x^T, with R^T fragments as the A operand
+// and token rows as the B operand. D^T[channel][token] of m-tile p (channels 16p .. 16p + 15) sits
+// in lane token + 16 ((channel % 16) / 4), register channel % 4: lane (token, hi) holds channels
+// 16 p + 4 hi + j, so register j of tiles p = 0..7 gives the eight 2-bit codes of half 4 hi + j of
+// the packed layout, and the 32 channels of group g (tiles 2g, 2g + 1) sit in the four lanes of
+// one token, eight in each. The group parameters are then computed once per (token, group).
 typedef __bf16 ap_bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float ap_f4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kApWaves = 8;
 constexpr int kApRow = 136;  // bf16 per LDS row of R^T (128 + 8 pad: conflict-free 16-byte reads)
-
-// Min and max over the 16 lanes of each DPP row for four (min, max) pairs at once, with DPP-operand
-// min/max instructions: the eight chains are interleaved so every DPP operand was written at least
-// seven instructions earlier, and the leading s_nop covers values written just before the asm.
-// Inputs and results are finite.
-__device__ __forceinline__ void row_minmax16_x4(float (&mn)[4], float (&mx)[4]) {
-#define INT2KV_MM_STEP(CTRL)                                                       \
-  "v_min_f32_dpp %0, %0, %0 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
-  "v_max_f32_dpp %4, %4, %4 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
-  "v_min_f32_dpp %1, %1, %1 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
-  "v_max_f32_dpp %5, %5, %5 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
-  "v_min_f32_dpp %2, %2, %2 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
-  "v_max_f32_dpp %6, %6, %6 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
-  "v_min_f32_dpp %3, %3, %3 " CTRL " row_mask:0xf bank_mask:0xf\n\t"              \
-  "v_max_f32_dpp %7, %7, %7 " CTRL " row_mask:0xf bank_mask:0xf\n\t"
-  asm volatile("s_nop 1\n\t" INT2KV_MM_STEP("row_ror:8") INT2KV_MM_STEP("row_ror:4") INT2KV_MM_STEP("row_ror:2")
-                   INT2KV_MM_STEP("row_ror:1")
-               : "+v"(mn[0]), "+v"(mn[1]), "+v"(mn[2]), "+v"(mn[3]), "+v"(mx[0]), "+v"(mx[1]), "+v"(mx[2]),
-                 "+v"(mx[3]));
-#undef INT2KV_MM_STEP
-}
 
 // x / 3 correctly rounded, as a product with RN(1/3) and one FMA correction: checked against the
 // correctly rounded quotient for every fp32 significand (so for every x whose intermediate values
@@ -221,17 +202,14 @@ __global__ __launch_bounds__(512) void append_mfma_kernel(CacheView cv, const ui
   const uint16_t* X = kv == 0 ? k : v;
   // the first tile's operands and slots are fetched before R, so their latency overlaps R's
   const int tile0 = blockIdx.x * kApWaves + w;
-  ap_bf16x8_t A0[4];
-  int slot0[4];
+  ap_bf16x8_t X0[4];
+  int slot0 = -1;
   if (tile0 * 16 < n) {
-    const uint16_t* xrow = X + ((size_t)min(tile0 * 16 + lo, n - 1) * H + h) * kHeadDim + 8 * hi;
+    const int tok = tile0 * 16 + lo;
+    const uint16_t* xrow = X + ((size_t)min(tok, n - 1) * H + h) * kHeadDim + 8 * hi;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) A0[ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int tok = tile0 * 16 + 4 * hi + r;
-      slot0[r] = tok < n ? slots[tok] : -1;
-    }
+    for (int ks = 0; ks < 4; ++ks) X0[ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
+    slot0 = tok < n ? slots[tok] : -1;
   }
   {
     // R^T as three bf16 terms: thread (c, i0) reads R[i0 .. i0 + 7][c] (coalesced over c), splits
@@ -260,39 +238,37 @@ __global__ __launch_bounds__(512) void append_mfma_kernel(CacheView cv, const ui
   }
   for (int m = tid; m < 1024; m += 64 * kApWaves) recip_tab[m] = 1.0f / (1.0f + (float)m * 0x1p-10f);
   __syncthreads();
-  float sub[8];
+  // lane (token lo, hi) holds channels 16 p + 4 hi + j of its token in register j of tile p
+  ap_f4_t sub[8];
 #pragma unroll
-  for (int p = 0; p < 8; ++p) sub[p] = kv == 0 ? mu_rk[(size_t)h * kHeadDim + 16 * p + lo] : 0.0f;
+  for (int p = 0; p < 8; ++p)
+    sub[p] = kv == 0 ? -*reinterpret_cast<const ap_f4_t*>(mu_rk + (size_t)h * kHeadDim + 16 * p + 4 * hi)
+                     : ap_f4_t{0.f, 0.f, 0.f, 0.f};
   const float clip = kv == 0 ? clip_k : clip_v;
   const int nslots = cv.num_blocks * kBlock;
-  // software pipeline over the wave's tiles: the next tile's operands and slots are fetched while
+  // software pipeline over the wave's tiles: the next tile's operands and slot are fetched while
   // this one is computed (indexes clamped, so the fetch past the last tile stays in bounds)
   const int tstride = gridDim.x * kApWaves;
-  ap_bf16x8_t A[4];
-  int slot[4];
+  ap_bf16x8_t X8[4];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) A[ks] = A0[ks];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) slot[r] = slot0[r];
+  for (int ks = 0; ks < 4; ++ks) X8[ks] = X0[ks];
+  int slot = slot0;
+  const bool h1 = (hi & 2) != 0, h0 = (hi & 1) != 0;
   for (int tile = tile0; tile * 16 < n; tile += tstride) {
-    ap_bf16x8_t An[4];
-    int slotn[4];
+    ap_bf16x8_t Xn[4];
+    int slotn;
     {
-      const int nt0 = (tile + tstride) * 16;
-      const uint16_t* xrow = X + ((size_t)min(nt0 + lo, n - 1) * H + h) * kHeadDim + 8 * hi;
+      const int tok = (tile + tstride) * 16 + lo;
+      const uint16_t* xrow = X + ((size_t)min(tok, n - 1) * H + h) * kHeadDim + 8 * hi;
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) An[ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int tok = nt0 + 4 * hi + r;
-        slotn[r] = tok < n ? slots[tok] : -1;
-      }
+      for (int ks = 0; ks < 4; ++ks) Xn[ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
+      slotn = tok < n ? slots[tok] : -1;
     }
     ap_f4_t acc[8];  // start at - mu R_K (keys) or 0 (values)
 #pragma unroll
-    for (int p = 0; p < 8; ++p) acc[p] = ap_f4_t{-sub[p], -sub[p], -sub[p], -sub[p]};
-    // the B fragments are the same for every tile: an opaque offset keeps the compiler from
-    // hoisting all 64 of them into registers (which would cap occupancy at one wave per SIMD)
+    for (int p = 0; p < 8; ++p) acc[p] = sub[p];
+    // the R^T fragments are the same for every tile: an opaque offset keeps the compiler from
+    // hoisting all 96 of them into registers (which would cap occupancy at one wave per SIMD)
     int boff = (lo * kApRow + 8 * hi) * 2;
     asm volatile("" : "+v"(boff));
     const uint8_t* rb = reinterpret_cast<const uint8_t*>(&rt[0][0][0]) + boff;
@@ -303,55 +279,80 @@ __global__ __launch_bounds__(512) void append_mfma_kernel(CacheView cv, const ui
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
         for (int p = 0; p < 8; ++p) {
-          const ap_bf16x8_t b =
+          const ap_bf16x8_t a =
               *reinterpret_cast<const ap_bf16x8_t*>(rb + ((term * kHeadDim + 16 * p) * kApRow + 32 * ks) * 2);
-          acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[ks], b, acc[p], 0, 0, 0);
+          acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, X8[ks], acc[p], 0, 0, 0);
         }
-    // group quantizer: per group g, the four rows' lane-local min/max of channels 16 (2g) + lo and
-    // 16 (2g + 1) + lo, then the 16-lane row reductions, parameters and codes
-    uint32_t half[4] = {0u, 0u, 0u, 0u}, meta[4][4];
+    // group g = tiles 2g, 2g + 1: lane-local min/max of its eight values, then a reduce-scatter
+    // over the four lanes of the token (xor 32, then xor 16) leaves group hi's extremes in lane hi
+    float pmn[4], pmx[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      float mn[4], mx[4];
+      float a = __builtin_fminf(acc[2 * g][0], acc[2 * g][1]), b = __builtin_fmaxf(acc[2 * g][0], acc[2 * g][1]);
+      a = __builtin_fminf(a, __builtin_fminf(acc[2 * g][2], acc[2 * g][3]));
+      b = __builtin_fmaxf(b, __builtin_fmaxf(acc[2 * g][2], acc[2 * g][3]));
+      a = __builtin_fminf(a, __builtin_fminf(acc[2 * g + 1][0], acc[2 * g + 1][1]));
+      b = __builtin_fmaxf(b, __builtin_fmaxf(acc[2 * g + 1][0], acc[2 * g + 1][1]));
+      pmn[g] = __builtin_fminf(a, __builtin_fminf(acc[2 * g + 1][2], acc[2 * g + 1][3]));
+      pmx[g] = __builtin_fmaxf(b, __builtin_fmaxf(acc[2 * g + 1][2], acc[2 * g + 1][3]));
+    }
+    float mn, mx;
+    {
+      // keep groups 2 h1, 2 h1 + 1, send the other two to the lane 32 away
+      const float sn0 = h1 ? pmn[0] : pmn[2], sn1 = h1 ? pmn[1] : pmn[3];
+      const float sx0 = h1 ? pmx[0] : pmx[2], sx1 = h1 ? pmx[1] : pmx[3];
+      float kn0 = h1 ? pmn[2] : pmn[0], kn1 = h1 ? pmn[3] : pmn[1];
+      float kx0 = h1 ? pmx[2] : pmx[0], kx1 = h1 ? pmx[3] : pmx[1];
+      kn0 = __builtin_fminf(kn0, __shfl_xor(sn0, 32));
+      kn1 = __builtin_fminf(kn1, __shfl_xor(sn1, 32));
+      kx0 = __builtin_fmaxf(kx0, __shfl_xor(sx0, 32));
+      kx1 = __builtin_fmaxf(kx1, __shfl_xor(sx1, 32));
+      // keep group 2 h1 + h0, send the other to the lane 16 away
+      mn = __builtin_fminf(h0 ? kn1 : kn0, __shfl_xor(h0 ? kn0 : kn1, 16));
+      mx = __builtin_fmaxf(h0 ? kx1 : kx0, __shfl_xor(h0 ? kx0 : kx1, 16));
+    }
+    uint32_t s_bits, z_bits;
+    float zf, inv;
+    int2_group_params_fast(mn, mx, clip, recip_tab, s_bits, z_bits, zf, inv);
+    // every lane of the token gathers the four groups' zero and reciprocal scale
+    float zg[4], ig[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        mn[r] = fminf(acc[2 * g][r], acc[2 * g + 1][r]);
-        mx[r] = fmaxf(acc[2 * g][r], acc[2 * g + 1][r]);
+    for (int g = 0; g < 4; ++g) {
+      zg[g] = __shfl(zf, lo + 16 * g);
+      ig[g] = __shfl(inv, lo + 16 * g);
+    }
+    // codes: half 4 hi + j of the token collects tiles p = 0..7 of register j at bits 2p, summed as
+    // exact small integers in fp32
+    float hf[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < 8; ++p)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma clang fp contract(off)
+        const float t = (acc[p][j] - zg[p >> 1]) * ig[p >> 1];
+        const float c = __builtin_rintf(__builtin_amdgcn_fmed3f(t, 0.0f, 3.0f));
+        hf[j] = __builtin_fmaf(c, (float)(1 << (2 * p)), hf[j]);
       }
-      row_minmax16_x4(mn, mx);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        uint32_t s_bits, z_bits;
-        float zf, inv;
-        int2_group_params_fast(mn[r], mx[r], clip, recip_tab, s_bits, z_bits, zf, inv);
-        half[r] |= int2_code(acc[2 * g][r], zf, inv) << (4 * g);
-        half[r] |= int2_code(acc[2 * g + 1][r], zf, inv) << (4 * g + 2);
-        meta[r][g] = s_bits | (z_bits << 16);
+    if (slot >= 0 && slot < nslots) {
+      const int blk = slot >> 4, t = slot & 15;
+      uint8_t* rec = cv.pool + ((size_t)blk * H + h) * kRecord;
+      const uint32_t q0 = (uint32_t)hf[0], q1 = (uint32_t)hf[1], q2 = (uint32_t)hf[2], q3 = (uint32_t)hf[3];
+      if (kv == 0) {
+        *reinterpret_cast<uint2*>(rec + kOffKCodes + 32 * t + 8 * hi) = make_uint2(q0 | (q1 << 16), q2 | (q3 << 16));
+        *reinterpret_cast<uint32_t*>(rec + kOffKMeta + 16 * t + 4 * hi) = s_bits | (z_bits << 16);
+      } else {
+        uint8_t* vc = rec + kOffVCodes + 32 * 4 * hi + 2 * t;
+        *reinterpret_cast<uint16_t*>(vc) = (uint16_t)q0;
+        *reinterpret_cast<uint16_t*>(vc + 32) = (uint16_t)q1;
+        *reinterpret_cast<uint16_t*>(vc + 64) = (uint16_t)q2;
+        *reinterpret_cast<uint16_t*>(vc + 96) = (uint16_t)q3;
+        *reinterpret_cast<uint16_t*>(rec + kOffVScale + 32 * hi + 2 * t) = (uint16_t)s_bits;
+        *reinterpret_cast<uint16_t*>(rec + kOffVZero + 32 * hi + 2 * t) = (uint16_t)z_bits;
       }
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int sl = slot[r];
-      if (sl >= 0 && sl < nslots) {
-        const int blk = sl >> 4, t = sl & 15;
-        uint8_t* rec = cv.pool + ((size_t)blk * H + h) * kRecord;
-        const uint32_t my = lo == 0 ? meta[r][0] : lo == 1 ? meta[r][1] : lo == 2 ? meta[r][2] : meta[r][3];
-        if (kv == 0) {
-          *reinterpret_cast<uint16_t*>(rec + kOffKCodes + 32 * t + 2 * lo) = (uint16_t)half[r];
-          if (lo < 4) *reinterpret_cast<uint32_t*>(rec + kOffKMeta + 16 * t + 4 * lo) = my;
-        } else {
-          *reinterpret_cast<uint16_t*>(rec + kOffVCodes + 32 * lo + 2 * t) = (uint16_t)half[r];
-          if (lo < 4) {
-            *reinterpret_cast<uint16_t*>(rec + kOffVScale + 32 * lo + 2 * t) = (uint16_t)(my & 0xFFFFu);
-            *reinterpret_cast<uint16_t*>(rec + kOffVZero + 32 * lo + 2 * t) = (uint16_t)(my >> 16);
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) A[ks] = An[ks];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) slot[r] = slotn[r];
+    for (int ks = 0; ks < 4; ++ks) X8[ks] = Xn[ks];
+    slot = slotn;
   }
 }
 
