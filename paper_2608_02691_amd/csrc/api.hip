@@ -56,8 +56,10 @@ CacheView view(const int2kv_cache* c) {
   return CacheView{static_cast<uint8_t*>(c->pool), c->num_blocks, c->num_kv_heads};
 }
 
+}  // namespace
+
 // Compute units of the current device (queried once per device; 256 when no device answers).
-int num_cus() {
+int int2kv::num_cus() {
   static int cached[64] = {0};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
@@ -69,6 +71,8 @@ int num_cus() {
   }
   return cached[dev];
 }
+
+namespace {
 
 DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   DecodePlan p{};
@@ -91,7 +95,7 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   // matrix-core scan: persistent work-groups of min(H, 8) waves, enough to fill every CU
   const int nw = H < 8 ? H : 8;
   p.grid_g = num_cus() * (8 / nw);
-  p.wo_ksplit = d_model > 0 ? wo_ksplit(Hq * kHeadDim) : 0;
+  p.wo_ksplit = d_model > 0 ? wo_ksplit(Hq * kHeadDim, d_model, B) : 0;
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   size_t off = 0;
   p.off_qrot = off;

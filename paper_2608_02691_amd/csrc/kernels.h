@@ -64,7 +64,9 @@ size_t qop_bytes(int B, int H, int gq);
 // the output projection: ob[0 .. B*Hq*128) = hi, ob[B*Hq*128 ..) = lo
 hipError_t launch_merge(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, hipStream_t s);
 hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, hipStream_t s);
-int wo_ksplit(int K);  // K slices of the output projection (partial products in the workspace)
+int num_cus();                        // compute units of the current device
+int wo_slice(int K, int N, int B);    // K per work-group of the output projection
+int wo_ksplit(int K, int N, int B);   // K slices of the output projection (partial products in the workspace)
 hipError_t launch_wo_gemm(const uint16_t* ob, const uint16_t* W, float* y, float* partial, int B, int K,
                           int N, int ksplit, hipStream_t s);
 

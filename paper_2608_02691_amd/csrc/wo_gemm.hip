@@ -6,7 +6,7 @@
 // multiplied against the bf16 weights, which keeps the product at fp32-like precision
 // (|o - hi - lo| <= 2^-16 |o|). Work-group (128 rows of W, one K slice, 64 batch rows), four waves
 // of 32 rows. Every 32-wide k step of the weights and of o is staged in LDS with LDS-DMA loads
-// (global_load_lds: lane i's 16 bytes land at M0 + 16 i), kStages - 1 steps ahead, with no
+// (global_load_lds: lane i's 16 bytes land at M0 + 16 i), kWoStages - 1 steps ahead, with no
 // registers held for data in flight; each lane fetches exactly the 16 bytes it later reads as its
 // MFMA operand, so the LDS reads are conflict-free. The o tile is shared by the four waves: each
 // wave waits for its own DMA, then one barrier makes the whole step visible. Slices write partial
@@ -22,8 +22,7 @@ typedef float wo_f4_t __attribute__((ext_vector_type(4)));
 constexpr int kWoTileN = 128;   // rows of W (output columns) per work-group
 constexpr int kWoBatch = 64;    // batch rows per work-group (four 16-column B tiles)
 constexpr int kWoKStep = 32;
-constexpr int kWoSlice = 640;   // k per work-group (20 steps)
-constexpr int kWoStages = 4;    // LDS stages; kWoStages - 1 steps in flight
+constexpr int kWoStages = 8;    // LDS stages; kWoStages - 1 steps in flight (112 KiB per work-group)
 constexpr int kWoStageBytes = 16384;  // W: 4 waves x 2 tiles x 1 KiB; o: 2 terms x 4 tiles x 1 KiB
 constexpr int kWoDmaPerStep = 4;      // DMA instructions per wave and step (2 of W, 2 of o)
 
@@ -33,13 +32,14 @@ __device__ __forceinline__ void wo_dma(const void* base, uint32_t voff, uint32_t
 }
 
 __global__ __launch_bounds__(256) void wo_mfma_kernel(const uint16_t* __restrict__ ob, const uint16_t* __restrict__ W,
-                                                      float* __restrict__ partial, int B, int K, int N) {
+                                                      float* __restrict__ partial, int B, int K, int N,
+                                                      int slice) {
   __shared__ __attribute__((aligned(16))) uint8_t stage[kWoStages][kWoStageBytes];
   const int n0 = blockIdx.x * kWoTileN, ks = blockIdx.y, b0 = blockIdx.z * kWoBatch;
   const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), l = tid & 63;
   const int lo = l & 15, hi = l >> 4;
-  const int k_begin = ks * kWoSlice;
-  const int nsteps = (min(K, k_begin + kWoSlice) - k_begin) / kWoKStep;
+  const int k_begin = ks * slice;
+  const int nsteps = (min(K, k_begin + slice) - k_begin) / kWoKStep;
   const int last = nsteps - 1;
 
   // Per-lane byte offsets (the step's k offset rides in the scalar base):
@@ -129,11 +129,11 @@ __global__ __launch_bounds__(256) void wo_reduce_kernel(const float* __restrict_
 hipError_t launch_wo_gemm(const uint16_t* ob, const uint16_t* W, float* y, float* partial, int B, int K, int N,
                           int ksplit, hipStream_t s) {
   // 32-bit per-lane DMA offsets: the weights and both o terms must span less than 4 GiB
-  if (K % kWoKStep != 0 || B <= 0 || N <= 0 || ksplit != wo_ksplit(K) || (size_t)N * K * 2 >= (1ull << 32) ||
+  if (K % kWoKStep != 0 || B <= 0 || N <= 0 || ksplit != wo_ksplit(K, N, B) || (size_t)N * K * 2 >= (1ull << 32) ||
       (size_t)2 * B * K * 2 >= (1ull << 32))
     return hipErrorInvalidValue;
   dim3 grid((N + kWoTileN - 1) / kWoTileN, ksplit, (B + kWoBatch - 1) / kWoBatch);
-  hipLaunchKernelGGL(wo_mfma_kernel, grid, dim3(256), 0, s, ob, W, partial, B, K, N);
+  hipLaunchKernelGGL(wo_mfma_kernel, grid, dim3(256), 0, s, ob, W, partial, B, K, N, wo_slice(K, N, B));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t total = (size_t)B * N;
@@ -142,6 +142,17 @@ hipError_t launch_wo_gemm(const uint16_t* ob, const uint16_t* W, float* y, float
   return hipGetLastError();
 }
 
-int wo_ksplit(int K) { return (K + kWoSlice - 1) / kWoSlice; }
+// K per work-group: the K range is split so that the grid holds about one work-group per CU (a
+// work-group's stages fill most of the LDS), in whole 32-wide steps.
+int wo_slice(int K, int N, int B) {
+  const int tiles = ((N + kWoTileN - 1) / kWoTileN) * ((B + kWoBatch - 1) / kWoBatch);
+  const int want = max(1, num_cus() / max(1, tiles));
+  const int steps = (K + kWoKStep - 1) / kWoKStep;
+  return kWoKStep * ((steps + want - 1) / want);
+}
+int wo_ksplit(int K, int N, int B) {
+  const int sl = wo_slice(K, N, B);
+  return (K + sl - 1) / sl;
+}
 
 }  // namespace int2kv
