@@ -103,23 +103,28 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, int rt) {
     const int row = 16 * w + lo, sq = row >> 3, jj = row & 7;
     const bool ok = sq < nseq && jj < gq;
     const uint16_t* qr = a.q + ((size_t)(b0 + (ok ? sq : 0)) * a.Hq + h * gq + (ok ? jj : 0)) * kHeadDim + 8 * hi;
+    const uint32_t keep = ok ? ~0u : 0u;  // a mask, not a select: the loads stay unconditional
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const uint4 v = *reinterpret_cast<const uint4*>(qr + 32 * ks);
-      A[ks] = __builtin_bit_cast(qp_bf16x8_t, ok ? v : make_uint4(0u, 0u, 0u, 0u));
+      A[ks] = __builtin_bit_cast(qp_bf16x8_t, make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep));
     }
   }
   {
     // R^T as bf16 hi/lo: thread (c, k0) reads R[k0 .. k0 + 7][c] (coalesced over c) and writes one
     // 16-byte row piece per term
+    // (all 64 loads of a thread are issued before the first conversion: one round trip)
     const float* R = a.R_k + (size_t)h * kHeadDim * kHeadDim;
     const int c = tid & 127, kb = tid >> 7;
-#pragma unroll 2
+    float rall[8][8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) rall[u][q] = R[(8 * (kb + 2 * u) + q) * kHeadDim + c];
+#pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int k0 = 8 * (kb + 2 * u);
-      float r8[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) r8[q] = R[(k0 + q) * kHeadDim + c];
+      const float* r8 = rall[u];
       uint32_t hw[4], lw[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
