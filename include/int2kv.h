@@ -154,10 +154,11 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
                   int wo_is_folded, float* out, void* workspace, size_t workspace_bytes,
                   hipStream_t stream);
 
-/* Measurement hook: when set (non-NULL), int2kv_decode records `before_scan` and `after_scan`
- * on its stream immediately before and after the split-context scan kernel, so a caller can
- * time that kernel alone with hipEventElapsedTime. Pass NULLs to disable. The events are owned
- * by the caller and must outlive the calls that record them. */
+/* Measurement hook: when set (non-NULL), int2kv_decode attaches `before_scan` and `after_scan`
+ * to the dispatch of the split-context scan kernel (hipExtLaunchKernel), so they mark that
+ * kernel's own start and end and a caller can time it alone with hipEventElapsedTime, without
+ * extra packets between the kernels. Pass NULLs to disable. The events are owned by the caller
+ * and must outlive the calls that record them. */
 int int2kv_set_decode_events(hipEvent_t before_scan, hipEvent_t after_scan);
 
 /* Tuning knobs for measurement sweeps: context chunk in tokens (multiple of 64, 0 = automatic)

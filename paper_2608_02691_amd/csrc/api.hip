@@ -256,16 +256,10 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
     e = launch_qprep(a, stream);
     if (e != hipSuccess) return hip_status(e, "decode/qprep");
   }
-  if (g_ev_before) {
-    e = hipEventRecord(g_ev_before, stream);
-    if (e != hipSuccess) return hip_status(e, "decode/event");
-  }
-  e = plan.variant == 2 ? launch_decode_split_mfma(a, stream) : launch_decode_split_valu(a, stream);
+  // the measurement events (if set) ride on the scan's own dispatch: they mark its start and end
+  e = plan.variant == 2 ? launch_decode_split_mfma(a, stream, g_ev_before, g_ev_after)
+                        : launch_decode_split_valu(a, stream, g_ev_before, g_ev_after);
   if (e != hipSuccess) return hip_status(e, "decode/split");
-  if (g_ev_after) {
-    e = hipEventRecord(g_ev_after, stream);
-    if (e != hipSuccess) return hip_status(e, "decode/event");
-  }
   const bool unrotate = !(W_o && wo_is_folded);
   // with W_O the merge writes each head output as two bf16 terms (hi, lo) for the projection
   uint16_t* ob = W_o ? reinterpret_cast<uint16_t*>(ws + plan.off_o) : nullptr;

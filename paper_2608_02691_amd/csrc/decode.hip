@@ -216,18 +216,18 @@ __global__ __launch_bounds__(256) void decode_split_valu_kernel(DecodeArgs a) {
   }
 }
 
-hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s) {
+hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   dim3 grid(a.n_chunks, a.H, a.B);
   if (a.gq <= 1)
-    hipLaunchKernelGGL(decode_split_valu_kernel<1>, grid, dim3(256), 0, s, a);
+    hipExtLaunchKernelGGL(decode_split_valu_kernel<1>, grid, dim3(256), 0, s, ev0, ev1, 0, a);
   else if (a.gq <= 2)
-    hipLaunchKernelGGL(decode_split_valu_kernel<2>, grid, dim3(256), 0, s, a);
+    hipExtLaunchKernelGGL(decode_split_valu_kernel<2>, grid, dim3(256), 0, s, ev0, ev1, 0, a);
   else if (a.gq <= 4)
-    hipLaunchKernelGGL(decode_split_valu_kernel<4>, grid, dim3(256), 0, s, a);
+    hipExtLaunchKernelGGL(decode_split_valu_kernel<4>, grid, dim3(256), 0, s, ev0, ev1, 0, a);
   else if (a.gq <= 8)
-    hipLaunchKernelGGL(decode_split_valu_kernel<8>, grid, dim3(256), 0, s, a);
+    hipExtLaunchKernelGGL(decode_split_valu_kernel<8>, grid, dim3(256), 0, s, ev0, ev1, 0, a);
   else
-    hipLaunchKernelGGL(decode_split_valu_kernel<16>, grid, dim3(256), 0, s, a);
+    hipExtLaunchKernelGGL(decode_split_valu_kernel<16>, grid, dim3(256), 0, s, ev0, ev1, 0, a);
   return hipGetLastError();
 }
 

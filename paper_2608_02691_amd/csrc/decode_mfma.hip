@@ -797,15 +797,15 @@ hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s) {
+hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   if (a.gq > 8) return hipErrorNotSupported;
   const int rt = (a.gq + 3) / 4;
   dim3 grid(a.grid_g, (a.H + kWavesPerWG - 1) / kWavesPerWG);
   const int threads = 64 * min(a.H, kWavesPerWG);
   if (rt == 1)
-    hipLaunchKernelGGL(decode_scan_flat_kernel<1>, grid, dim3(threads), 0, s, a);
+    hipExtLaunchKernelGGL(decode_scan_flat_kernel<1>, grid, dim3(threads), 0, s, ev0, ev1, 0, a);
   else
-    hipLaunchKernelGGL(decode_scan_flat_kernel<2>, grid, dim3(threads), 0, s, a);
+    hipExtLaunchKernelGGL(decode_scan_flat_kernel<2>, grid, dim3(threads), 0, s, ev0, ev1, 0, a);
   return hipGetLastError();
 }
 

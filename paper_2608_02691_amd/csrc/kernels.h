@@ -1,6 +1,7 @@
 // Internal launcher declarations shared by the C-ABI front end and the kernel files.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -56,9 +57,10 @@ struct DecodeArgs {
 constexpr int kPartStride = 132;  // m, l, 2 pad, O[128]
 
 hipError_t launch_qrot(const DecodeArgs& a, hipStream_t s);
-hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s);
+// ev0 / ev1 (may be null): events that track the scan kernel's own start and end
+hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s);
-hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 size_t qop_bytes(int B, int H, int gq);
 // merges write fp32 head outputs to `out`, or (ob != NULL) the two bf16 terms of each value for
 // the output projection: ob[0 .. B*Hq*128) = hi, ob[B*Hq*128 ..) = lo
