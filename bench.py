@@ -110,7 +110,14 @@ def cpu_baseline(w, target_s):
         log(f"cpu oracle: sequence {b} ({L} tokens), {elapsed:.1f} s so far")
         if elapsed >= target_s:
             break
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": tokens / elapsed, "unit": "KV-tokens/s", "cores": int(cores), "kind": "oracle",
+            "host_cpus": os.cpu_count(), "cpu_model": model,
             "sample": f"oracle decode (+W_O) of sequences {seqs[0]}..{seqs[-1]} of the same workload "
                       f"({tokens} KV-tokens, {elapsed:.1f} s, fp64 numpy)"}
 
@@ -128,6 +135,13 @@ def main():
     ap.add_argument("--event-every", type=int, default=10,
                     help="time the scan kernel with HIP events on every n-th timed step (events attached to a "
                          "dispatch add ~11 us of queue gaps to that step)")
+    ap.add_argument("--ctx", type=int, default=0,
+                    help="uniform context length override (e.g. --config 1 --ctx 32768: the 402.7 MB uniform "
+                         "32K variant of the 16-sequence shape)")
+    ap.add_argument("--flush-mall", action="store_true",
+                    help="read a 1 GiB scratch buffer before every timed step (evicts L2 and the Infinity "
+                         "Cache, for workloads that would otherwise fit in it, and leaves no dirty lines behind); "
+                         "steps are then timed one by one")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -153,7 +167,7 @@ def main():
         print(json.dumps({"copy_calibration_bytes_read": n, "bytes_written": n, "launches": 3}), flush=True)
         return
     K.int2kv_set_decode_tuning(args.chunk, args.variant)
-    w = W.make_workload(args.config)
+    w = W.make_workload(args.config, ctx=args.ctx or None)
     B, Hq, H = w.batch, w.num_q_heads, w.num_kv_heads
     d_model = w.cfg.d_model or 0
     lens = w.ctx_lens.astype(np.int64)
@@ -199,26 +213,62 @@ def main():
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps)")
 
-    every = max(1, args.event_every)
-    sampled = list(range(0, args.steps, every))
-    ev = HipEvents(len(sampled))
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if args.flush_mall:
+        # every step timed alone (torch events around it), the scan with events on its dispatch; the
+        # 1 GiB read before each step is outside both (a read, so no dirty lines are left to write back)
+        scratch = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        sampled = list(range(args.steps))
+        ev = HipEvents(args.steps)
+        t_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in sampled]
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            sink = scratch.sum()
+            K.int2kv_set_decode_events(*ev.pairs[i])
+            t_ev[i][0].record()
+            step()
+            t_ev[i][1].record()
+        torch.cuda.synchronize()
+        K.int2kv_set_decode_events(None, None)
+        ms_step = float(np.mean([a.elapsed_time(b) for a, b in t_ev]))
+        scan_ms = float(np.mean([ev.elapsed_ms(j) for j in range(args.steps)]))
+        ev.destroy()
+        del scratch, sink
+        log(f"timed {args.steps} steps one by one after a 1 GiB read each: {ms_step:.3f} ms/step "
+            f"(includes the events' own queue gaps), scan kernel {scan_ms:.3f} ms")
+    else:
+        every = max(1, args.event_every)
+        sampled = list(range(0, args.steps, every))
+        ev = HipEvents(len(sampled))
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        for i in range(args.steps):
+            if i % every == 0:
+                K.int2kv_set_decode_events(*ev.pairs[i // every])
+            elif i % every == 1:
+                K.int2kv_set_decode_events(None, None)
+            step()
+        stop.record()
+        torch.cuda.synchronize()
+        K.int2kv_set_decode_events(None, None)
+        ms_step = start.elapsed_time(stop) / args.steps
+        scan_ms = float(np.mean([ev.elapsed_ms(j) for j in range(len(sampled))]))
+        ev.destroy()
+        log(f"timed {args.steps} steps: {ms_step:.3f} ms/step, scan kernel {scan_ms:.3f} ms "
+            f"(events on {len(sampled)} of the steps)")
+
+    # context: a plain 1 GiB device-to-device copy on the same GPU (read + write bytes over time)
+    cp_src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    cp_dst = torch.empty_like(cp_src)
+    cp_dst.copy_(cp_src)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(3):
+        cp_dst.copy_(cp_src)
+    c1.record()
     torch.cuda.synchronize()
-    start.record()
-    for i in range(args.steps):
-        if i % every == 0:
-            K.int2kv_set_decode_events(*ev.pairs[i // every])
-        elif i % every == 1:
-            K.int2kv_set_decode_events(None, None)
-        step()
-    stop.record()
-    torch.cuda.synchronize()
-    K.int2kv_set_decode_events(None, None)
-    ms_step = start.elapsed_time(stop) / args.steps
-    scan_ms = float(np.mean([ev.elapsed_ms(j) for j in range(len(sampled))]))
-    ev.destroy()
-    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step, scan kernel {scan_ms:.3f} ms "
-        f"(events on {len(sampled)} of the steps)")
+    copy_gbps = 3 * 2 * (1 << 30) / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del cp_src, cp_dst
 
     tokens = int(lens.sum())
     pages = int(((lens + 15) // 16).sum())
@@ -243,11 +293,12 @@ def main():
         "vs_baseline": None,
         "dtype": "int2 codes, fp16 meta, fp32 accumulate",
         "data": "synthetic (seeded; no model weights or traces)",
+        "kv_token_heads_per_s": tokens * H / (ms_step * 1e-3),
         "step_hbm_gbps": step_gbps,
         "step_pct_hbm_peak": 100.0 * step_gbps / HBM_PEAK_GBPS,
         "config": {
-            "workload": w.cfg.name,
-            "batch": B, "num_q_heads": Hq, "num_kv_heads": H, "head_dim": 128, "block_size": 16,
+            "workload": w.cfg.name if not args.ctx else f"{w.cfg.name}; context set to a uniform {args.ctx}",
+            "config_id": args.config, "batch": B, "num_q_heads": Hq, "num_kv_heads": H, "head_dim": 128, "block_size": 16,
             "group_size": 32, "sum_ctx": tokens, "max_ctx": max_ctx, "d_model": d_model,
             "chunk_tokens": args.chunk or "auto", "variant": args.variant or "auto",
             "w_o": ("folded W_O R_V (prepared once)" if folded else "W_O after R_V^T") if Wo is not None else None,
@@ -263,7 +314,9 @@ def main():
             "algorithmic_bytes_per_launch": scan_bytes,
             "avg_launch_ms": scan_ms,
             "timed_launches": len(sampled),
+            "caches": "flushed (1 GiB read) before every step" if args.flush_mall else "warm, steps back to back",
         },
+        "context": {"hbm_copy_gbps": copy_gbps, "copy": "1 GiB device-to-device copy, read + write bytes"},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
