@@ -31,13 +31,13 @@ constexpr float kRescaleTau = 8.0f;  // lazy rescaling: keep the running max unt
 // Starting reference max: finite, so a segment whose tokens are all masked (-inf scores) still gives
 // p = exp2(-inf - m0) = 0 rather than NaN; any real score exceeds it by more than 2^tau.
 constexpr float kMaxInit = -1.0e30f;
-constexpr int kQopTile = 4096 + 256;  // A operands (4 instr x 64 lanes x 16 B) + constants
+constexpr int kQopTile = 4096 + 512;  // A operands (4 blocks x 64 lanes x 16 B) + constants
 
 bool mfma_decode_available() { return true; }
 
 size_t qop_bytes(int B, int H, int gq) {
-  const int rt = (gq + 3) / 4;
-  return (size_t)B * H * rt * kQopTile;
+  (void)gq;
+  return (size_t)B * H * kQopTile;
 }
 
 // Class e of bit position x after the landing shift: the fp16 value is 1 + code * 2^-e.
@@ -76,9 +76,9 @@ __device__ __forceinline__ int seq_len_m(const DecodeArgs& a, int b) {
 // ---------------------------------------------------------------------------------------------
 // Query operands of one (sequence, KV head): q' = q R_K (fp32) scaled by log2(e)/sqrt(d) and a
 // per-head power of two sigma (max |q' sigma| in [256, 512)), laid out as the MFMA A operand of the
-// score contraction: row (j, g) of tile r holds q'_j on the channels of group g, times 2^e of the
-// channel's code position, as fp16. Constants per row: -sum_k A_k (accumulator start),
-// sum_{k in g} q'_jk (for the zero term) and 1/sigma.
+// score contraction: a row holds q'_j on the channels of one group, times 2^e of the channel's
+// code position, as fp16 (row layouts: see the scan below). Constants: -sum_k A_k per row
+// (accumulator start), sum_{k in g} q'_jk (for the zero term) and 1/sigma.
 // One block serves KV head h of kQpSeqs sequences: R_K[h] goes once into LDS as the B operand of a
 // bf16 matrix-core product (split into two bf16 terms, as in the cache write: error below
 // 2^-17 |R|); the query rows are exact in bf16. Rows s * 8 + jj = query head jj of sequence
@@ -87,7 +87,7 @@ constexpr int kQpSeqs = 8;
 constexpr int kQpRow = 136;  // bf16 per LDS row of R^T (128 + 8 pad: conflict-free 16-byte reads)
 typedef __bf16 qp_bf16x8_t __attribute__((ext_vector_type(8)));
 
-__device__ void qprep_block(const DecodeArgs& a, int blk, int rt) {
+__device__ void qprep_block(const DecodeArgs& a, int blk, bool wide) {
   __shared__ __attribute__((aligned(16))) uint16_t Rt[2][kHeadDim][kQpRow];     // [hi, lo][c][k] = R[k][c]
   __shared__ __attribute__((aligned(16))) float qb[8 * kQpSeqs][kHeadDim + 4];  // q' rows
   __shared__ int smax[8 * kQpSeqs];
@@ -169,15 +169,19 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, int rt) {
     sig[tid] = m > 0.0f ? ldexpf(1.0f, max(-100, min(100, 9 - ex))) : 1.0f;
   }
   __syncthreads();
-  // A operand chunks: (sequence, tile r, k block i, lane l) -> 8 fp16 values. Row (jj, g) of lane
-  // l = m + 16 q (jj = 4 r + m / 4, g = m % 4) is nonzero only in block i = g, where its eight
-  // values are channels 32 i + 4 q + 0..3 (code position x = 2 i) and 32 i + 16 + 4 q + 0..3
-  // (x = 2 i + 1), scaled by sigma and 2^e(x).
-  for (int cidx = tid; cidx < nseq * rt * 256; cidx += 256) {
-    const int sq = cidx / (rt * 256), r = (cidx / 256) % rt, i = (cidx / 64) % 4, l = cidx % 64;
-    const int m = l & 15, q = l >> 4, jj = 4 * r + (m >> 2), g = m & 3, row = 8 * sq + jj;
+  // A operand chunks: (sequence, k block i, lane l) -> 8 fp16 values. Lane l = m + 16 q holds row
+  // m, which belongs to query head jj and is nonzero only in the blocks of its group slot: narrow
+  // rows (j, g) = 4 j + g in block g; wide rows (j, gg) = 2 j + gg in the blocks i with i % 2 = gg.
+  // Its eight values are channels 32 i + 4 q + 0..3 (code position x = 2 i) and
+  // 32 i + 16 + 4 q + 0..3 (x = 2 i + 1), scaled by sigma and 2^e(x).
+  for (int cidx = tid; cidx < nseq * 256; cidx += 256) {
+    const int sq = cidx >> 8, i = (cidx >> 6) & 3, l = cidx & 63;
+    const int m = l & 15, q = l >> 4;
+    const int jj = wide ? m >> 1 : m >> 2;
+    const bool on = wide ? (m & 1) == (i & 1) : (m & 3) == i;
+    const int row = 8 * sq + jj;
     uint32_t packed[4] = {0u, 0u, 0u, 0u};
-    if (g == i && jj < gq) {
+    if (on && jj < gq) {
       const float4 lo4 = *reinterpret_cast<const float4*>(&qb[row][32 * i + 4 * q]);
       const float4 hi4 = *reinterpret_cast<const float4*>(&qb[row][32 * i + 16 + 4 * q]);
       const float s0 = sig[row] * (float)(1 << land_e(2 * i)), s1 = sig[row] * (float)(1 << land_e(2 * i + 1));
@@ -188,14 +192,17 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, int rt) {
         packed[u] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
       }
     }
-    uint8_t* out = a.qop + ((size_t)(b0 + sq) * H + h) * rt * kQopTile;
-    *reinterpret_cast<uint4*>(out + r * kQopTile + (i * 64 + l) * 16) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+    uint8_t* out = a.qop + ((size_t)(b0 + sq) * H + h) * kQopTile;
+    *reinterpret_cast<uint4*>(out + (i * 64 + l) * 16) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
   }
-  // per row (jj, g) of a tile: -sum of its 32 fp16 A values, sum of q' over group g, 1/sigma;
-  // thread -> (row, g), a sequential sum over the group's channels
+  // Per (query head jj, group g): -sum of the row's 32 fp16 A values in block g (the accumulator
+  // start of that row's tile), sum of q' over group g, and 1/sigma; thread -> (row, g), a
+  // sequential sum over the group's channels. Narrow layout after the 4096 bytes of A operands:
+  // start[4 jj + g], qsum[16 + 4 jj + g], 1/sigma[32 + jj]; wide: start of D01 [2 jj + g] (g < 2)
+  // and of D23 [16 + 2 jj + g - 2] (g >= 2), qsum[32 + 4 jj + g], 1/sigma[64 + jj] (floats).
   {
     const int row = tid >> 2, g = tid & 3, sq = row >> 3, jj = row & 7;
-    if (sq < nseq && jj < 4 * rt) {
+    if (sq < nseq && jj < (wide ? 8 : 4)) {
       float csum = 0.0f, qsum = 0.0f;
       if (jj < gq) {
         const float s0 = sig[row] * (float)(1 << land_e(2 * g)), s1 = sig[row] * (float)(1 << land_e(2 * g + 1));
@@ -208,23 +215,40 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, int rt) {
           qsum += v.x + v.y + v.z + v.w;
         }
       }
-      const int r = jj / 4, jl = jj % 4;
-      uint8_t* out = a.qop + ((size_t)(b0 + sq) * H + h) * rt * kQopTile;
-      float* cst = reinterpret_cast<float*>(out + r * kQopTile + 4096);
-      cst[jl * 4 + g] = -csum;
-      cst[16 + jl * 4 + g] = qsum;
-      if (g == 0) cst[32 + jl] = jj < gq ? 1.0f / sig[row] : 0.0f;
+      const float isg = jj < gq ? 1.0f / sig[row] : 0.0f;
+      float* cst = reinterpret_cast<float*>(a.qop + ((size_t)(b0 + sq) * H + h) * kQopTile + 4096);
+      if (wide) {
+        cst[16 * (g >> 1) + 2 * jj + (g & 1)] = -csum;
+        cst[32 + 4 * jj + g] = qsum;
+        if (g == 0) cst[64 + jj] = isg;
+      } else {
+        cst[4 * jj + g] = -csum;
+        cst[16 + 4 * jj + g] = qsum;
+        if (g == 0) cst[32 + jj] = isg;
+      }
     }
   }
 }
 
 // ---------------------------------------------------------------------------------------------
+// Row layouts. The matrix cores contract over 32 channels, one quant group, while a group's scale
+// multiplies only that group's partial dot product, so a score row serves one group: it is
+// nonzero only in that group's k block.
+//  * narrow (up to 4 query heads per KV head): row (j, g) = 4 j + g; the four k blocks accumulate
+//    into one 16-row tile D[(j, g), t];
+//  * wide (5 to 8 query heads): row (j, gg) = 2 j + gg, nonzero in the blocks g with g % 2 = gg;
+//    blocks 0, 1 accumulate into tile D01 and blocks 2, 3 into D23, so eight query heads take
+//    four MFMAs per page where two narrow tiles would take eight.
+// The value contraction mirrors this: its columns are (j, g) (narrow) or (j, gg) (wide) and hold
+// the weights p_jt s_tg of the column's group; channel tile mt (group mt / 2) uses the columns of
+// its group.
+template <bool WIDE>
 struct PairLoads {
   uint2 kc[2];  // K codes of this lane's token (lo), chunk hi: halves 4hi..4hi+3
   uint4 km[2];  // K scale/zero of token lo, groups 0..3
   uint2 vc[2];  // V codes of half lo, tokens 4hi..4hi+3
-  uint2 vs[2];  // V scales of group lo&3, tokens 4hi..4hi+3
-  uint2 vz[2];  // V zeros  of group lo&3, tokens 4hi..4hi+3
+  uint2 vs[2][WIDE ? 2 : 1];  // V scales, tokens 4hi..4hi+3: group lo&3 (narrow); lo&1, 2+(lo&1) (wide)
+  uint2 vz[2];  // V zeros of group lo&3, tokens 4hi..4hi+3
   int ok[2];    // wave-uniform: page holds cached tokens
 };
 
@@ -290,15 +314,19 @@ __device__ __forceinline__ uint32_t stage_pair(const uint8_t* pool, const uint8_
 // An empty asm that uses every register read_pair filled: the compiler places its wait for those
 // LDS reads here, ahead of the scalar block-id loads that follow (a later wait would have to
 // wait for those loads too, since scalar loads return out of order).
-__device__ __forceinline__ void pin_pair(PairLoads& p) {
+template <bool WIDE>
+__device__ __forceinline__ void pin_pair(PairLoads<WIDE>& p) {
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
     asm volatile("" : "+v"(p.kc[P].x), "+v"(p.kc[P].y), "+v"(p.vc[P].x), "+v"(p.vc[P].y));
     asm volatile("" : "+v"(p.km[P].x), "+v"(p.km[P].y), "+v"(p.km[P].z), "+v"(p.km[P].w));
-    asm volatile("" : "+v"(p.vs[P].x), "+v"(p.vs[P].y), "+v"(p.vz[P].x), "+v"(p.vz[P].y));
+    asm volatile("" : "+v"(p.vs[P][0].x), "+v"(p.vs[P][0].y), "+v"(p.vz[P].x), "+v"(p.vz[P].y));
+    if constexpr (WIDE) asm volatile("" : "+v"(p.vs[P][1].x), "+v"(p.vs[P][1].y));
   }
 }
-__device__ __forceinline__ void read_pair(const uint8_t* slot, bool ok0, bool ok1, int lo, int hi, PairLoads& p) {
+template <bool WIDE>
+__device__ __forceinline__ void read_pair(const uint8_t* slot, bool ok0, bool ok1, int lo, int hi,
+                                          PairLoads<WIDE>& p) {
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
     const uint8_t* rec = slot + P * kRecord;
@@ -307,7 +335,12 @@ __device__ __forceinline__ void read_pair(const uint8_t* slot, bool ok0, bool ok
     p.kc[P] = *reinterpret_cast<const uint2*>(rec + kOffKCodes + 32 * lo + 8 * hi);
     p.km[P] = *reinterpret_cast<const uint4*>(rec + kOffKMeta + 16 * lo);
     p.vc[P] = *reinterpret_cast<const uint2*>(rec + kOffVCodes + 32 * lo + 8 * hi);
-    p.vs[P] = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (lo & 3) + 8 * hi);
+    if constexpr (WIDE) {
+      p.vs[P][0] = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (lo & 1) + 8 * hi);
+      p.vs[P][1] = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (2 + (lo & 1)) + 8 * hi);
+    } else {
+      p.vs[P][0] = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (lo & 3) + 8 * hi);
+    }
     p.vz[P] = *reinterpret_cast<const uint2*>(rec + kOffVZero + 32 * (lo & 3) + 8 * hi);
   }
 }
@@ -326,22 +359,29 @@ __device__ __forceinline__ float4_t mfma16(half8_t a, half8_t b, float4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
-template <int RT>
+// Per-wave scan state. Lane (lo, hi) serves, in the score tiles, token lo and the query heads
+// jq(hi, u): narrow j = hi (u = 0); wide j = 2 hi + u (u = 0, 1).
+template <bool WIDE>
 struct ScanState {
-  half8_t A[RT][4];
-  float4_t cinit[RT], sqL[RT];
-  float invsig[RT];
-  float4_t acc[RT][8];
-  float4_t wsum[RT];  // sum_t w_t per (j, g) column (every row)
-  float4_t zl[RT];    // rows 0..3: sum_t p_t z_tg (row = group); rows 4..7: sum_t p_t
-  float mref[RT];
+  static constexpr int NJ = WIDE ? 2 : 1;   // query heads per lane in the score tiles
+  static constexpr int NT = WIDE ? 2 : 1;   // score tiles (narrow D; wide D01, D23)
+  half8_t A[4];                 // query operand of k block i
+  float4_t cinit[NT];           // accumulator start of the score tiles (rows 4hi..4hi+3)
+  float sq[NJ][4];              // sum_{k in g} q'_jk
+  float invsig[NJ];
+  float4_t acc[8];              // O' tiles: channels 16 mt + 4hi + r, column lo
+  float4_t wsum[NT];            // sum_t w_t of each column (every row); wide: groups gg, 2 + gg
+  float4_t zl;                  // rows 0..3: sum_t p_t z_tg (row = group); rows 4..7: sum_t p_t
+  float mref[NJ];
 };
 
-// Scores of one page pair (2 pages x RT row tiles), base-2 logits, -inf where masked. The four
-// accumulation chains are issued interleaved so each hides the others' latency.
-template <int RT>
-__device__ __forceinline__ void qk_pair(const ScanState<RT>& st, const PairLoads& cur, int pg, int t1, int lo,
-                                        float (&a2)[2][RT]) {
+// Scores of one page pair, base-2 logits, -inf where masked: a2[P][u] for token lo of page P and
+// query head jq(hi, u). The accumulation chains of both pages are issued interleaved so that each
+// hides the others' latency.
+template <bool WIDE>
+__device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoads<WIDE>& cur, int pg, int t1,
+                                        int lo, float (&a2)[2][ScanState<WIDE>::NJ]) {
+  constexpr int NT = ScanState<WIDE>::NT, NJ = ScanState<WIDE>::NJ;
   half8_t B[2][4];
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
@@ -350,80 +390,95 @@ __device__ __forceinline__ void qk_pair(const ScanState<RT>& st, const PairLoads
     B[P][2] = k_operand<4>(cur.kc[P]);
     B[P][3] = k_operand<6>(cur.kc[P]);
   }
-  float4_t d[2][RT];
+  float4_t d[2][NT];
 #pragma unroll
   for (int P = 0; P < 2; ++P)
 #pragma unroll
-    for (int r = 0; r < RT; ++r) d[P][r] = st.cinit[r];
+    for (int t = 0; t < NT; ++t) d[P][t] = st.cinit[t];
+  if constexpr (WIDE) {
+    // blocks 0, 2 then 1, 3: four independent chains (page x tile) of two
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int P = 0; P < 2; ++P)
+      for (int P = 0; P < 2; ++P)
 #pragma unroll
-      for (int r = 0; r < RT; ++r) d[P][r] = mfma16(st.A[r][i], B[P][i], d[P][r]);
+        for (int t = 0; t < 2; ++t) d[P][t] = mfma16(st.A[2 * t + i], B[P][2 * t + i], d[P][t]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int P = 0; P < 2; ++P) d[P][0] = mfma16(st.A[i], B[P][i], d[P][0]);
+  }
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
     const bool tv = cur.ok[P] && (pg + P) * kBlock + lo < t1;
-    const half2_t m0 = as_h2(cur.km[P].x), m1 = as_h2(cur.km[P].y), m2 = as_h2(cur.km[P].z), m3 = as_h2(cur.km[P].w);
+    const half2_t m[4] = {as_h2(cur.km[P].x), as_h2(cur.km[P].y), as_h2(cur.km[P].z), as_h2(cur.km[P].w)};
 #pragma unroll
-    for (int r = 0; r < RT; ++r) {
-      float sd = (float)m0.x * d[P][r][0];
-      sd = fmaf((float)m1.x, d[P][r][1], sd);
-      sd = fmaf((float)m2.x, d[P][r][2], sd);
-      sd = fmaf((float)m3.x, d[P][r][3], sd);
-      float zq = (float)m0.y * st.sqL[r][0];
-      zq = fmaf((float)m1.y, st.sqL[r][1], zq);
-      zq = fmaf((float)m2.y, st.sqL[r][2], zq);
-      zq = fmaf((float)m3.y, st.sqL[r][3], zq);
-      a2[P][r] = fmaf(sd, st.invsig[r], zq) + (tv ? 0.0f : -INFINITY);
+    for (int u = 0; u < NJ; ++u) {
+      // D of group g for query head jq(hi, u): narrow register g of D; wide register 2u + g % 2
+      // of tile g / 2
+      float Dg[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) Dg[g] = WIDE ? d[P][g >> 1][2 * u + (g & 1)] : d[P][0][g];
+      float sd = (float)m[0].x * Dg[0];
+      sd = fmaf((float)m[1].x, Dg[1], sd);
+      sd = fmaf((float)m[2].x, Dg[2], sd);
+      sd = fmaf((float)m[3].x, Dg[3], sd);
+      float zq = (float)m[0].y * st.sq[u][0];
+      zq = fmaf((float)m[1].y, st.sq[u][1], zq);
+      zq = fmaf((float)m[2].y, st.sq[u][2], zq);
+      zq = fmaf((float)m[3].y, st.sq[u][3], zq);
+      a2[P][u] = fmaf(sd, st.invsig[u], zq) + (tv ? 0.0f : -INFINITY);
     }
   }
 }
 
 // Lazy online softmax of one pair: the reference max only moves when a score exceeds it by 2^tau
-// (detected by a wave-wide vote, no row reduction in the common case). Writes p (fp16) to LDS.
-template <int RT>
-__device__ __forceinline__ void softmax_pair(ScanState<RT>& st, const float (&a2)[2][RT], int lo, int hi,
-                                             _Float16 (*p_w)[8][kBlock], float* al_w) {
+// (detected by a wave-wide vote, no row reduction in the common case). Writes p (fp16) to LDS as
+// p_w[page][query head][token].
+template <bool WIDE>
+__device__ __forceinline__ void softmax_pair(ScanState<WIDE>& st, const float (&a2)[2][ScanState<WIDE>::NJ], int lo,
+                                             int hi, _Float16 (*p_w)[8][kBlock], float* al_w) {
+  constexpr int NJ = ScanState<WIDE>::NJ, NT = ScanState<WIDE>::NT;
   bool need = false;
 #pragma unroll
   for (int P = 0; P < 2; ++P)
 #pragma unroll
-    for (int r = 0; r < RT; ++r) need |= a2[P][r] > st.mref[r] + kRescaleTau;
+    for (int u = 0; u < NJ; ++u) need |= a2[P][u] > st.mref[u] + kRescaleTau;
   if (__any(need)) {
 #pragma unroll
-    for (int r = 0; r < RT; ++r) {
-      const float pm = row_max16(fmaxf(a2[0][r], a2[1][r]));
-      const float mnew = pm > st.mref[r] + kRescaleTau ? pm : st.mref[r];
-      const float al = __builtin_amdgcn_exp2f(st.mref[r] - mnew);
-      st.mref[r] = mnew;
-      if (lo == 0) al_w[4 * r + hi] = al;
+    for (int u = 0; u < NJ; ++u) {
+      const float pm = row_max16(fmaxf(a2[0][u], a2[1][u]));
+      const float mnew = pm > st.mref[u] + kRescaleTau ? pm : st.mref[u];
+      const float al = __builtin_amdgcn_exp2f(st.mref[u] - mnew);
+      st.mref[u] = mnew;
+      if (lo == 0) al_w[NJ * hi + u] = al;
     }
     lds_sync_wave();
+    // every accumulator column (j, .) belongs to query head j = lo / 4 (narrow), lo / 2 (wide)
+    const float alc = al_w[WIDE ? lo >> 1 : lo >> 2];
 #pragma unroll
-    for (int r = 0; r < RT; ++r) {
-      const float alc = al_w[4 * r + (lo >> 2)];
+    for (int mt = 0; mt < 8; ++mt) st.acc[mt] *= alc;
 #pragma unroll
-      for (int mt = 0; mt < 8; ++mt) st.acc[r][mt] *= alc;
-      st.wsum[r] *= alc;
-      st.zl[r] *= alc;
-    }
+    for (int t = 0; t < NT; ++t) st.wsum[t] *= alc;
+    st.zl *= alc;
   }
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
 #pragma unroll
-    for (int r = 0; r < RT; ++r) {
-      const float p = __builtin_amdgcn_exp2f(a2[P][r] - st.mref[r]);
-      p_w[P][4 * r + hi][lo] = (_Float16)p;
+    for (int u = 0; u < NJ; ++u) {
+      const float p = __builtin_amdgcn_exp2f(a2[P][u] - st.mref[u]);
+      p_w[P][NJ * hi + u][lo] = (_Float16)p;
     }
   }
 }
 
-// Value accumulation of one pair: K = the pair's 32 tokens, N = (j, g) columns, M = 8 tiles of 16
+// Value accumulation of one pair: K = the pair's 32 tokens, N = the 16 columns, M = 8 tiles of 16
 // channels; p comes back from LDS in the layout of the B operand.
-template <int RT>
-__device__ __forceinline__ void pv_pair(ScanState<RT>& st, const PairLoads& cur, int lo, int hi,
+template <bool WIDE>
+__device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WIDE>& cur, int lo, int hi,
                                         const _Float16 (*p_w)[8][kBlock]) {
+  constexpr int NT = ScanState<WIDE>::NT;
   // A operand of the (Z, l) contraction: rows 0..3 hold z of group `row` (the V zeros this lane
   // already has, group lo & 3 = row), rows 4..7 hold 1.0, rows 8..15 zero
   const half2_t zmul = lo < 4 ? half2_t{(_Float16)1.0f, (_Float16)1.0f} : half2_t{(_Float16)0.0f, (_Float16)0.0f};
@@ -433,29 +488,27 @@ __device__ __forceinline__ void pv_pair(ScanState<RT>& st, const PairLoads& cur,
       half8_t, u32x4_t{as_u(as_h2(cur.vz[0].x) * zmul + zadd), as_u(as_h2(cur.vz[0].y) * zmul + zadd),
                        as_u(as_h2(cur.vz[1].x) * zmul + zadd), as_u(as_h2(cur.vz[1].y) * zmul + zadd)});
   const half8_t Aones = __builtin_bit_cast(half8_t, u32x4_t{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u});
-  half8_t Bw[RT];
+  // column lo: query head jc, probabilities of tokens 4hi..4hi+3 of both pages
+  const int jc = WIDE ? lo >> 1 : lo >> 2;
+  const uint2 pp0 = *reinterpret_cast<const uint2*>(&p_w[0][jc][4 * hi]);
+  const uint2 pp1 = *reinterpret_cast<const uint2*>(&p_w[1][jc][4 * hi]);
+  const half8_t Bp = __builtin_bit_cast(half8_t, u32x4_t{pp0.x, pp0.y, pp1.x, pp1.y});
+  half8_t Bw[NT];
 #pragma unroll
-  for (int r = 0; r < RT; ++r) {
-    const int jc = 4 * r + (lo >> 2);
-    const uint2 pp0 = *reinterpret_cast<const uint2*>(&p_w[0][jc][4 * hi]);
-    const uint2 pp1 = *reinterpret_cast<const uint2*>(&p_w[1][jc][4 * hi]);
-    const half8_t Bp = __builtin_bit_cast(half8_t, u32x4_t{pp0.x, pp0.y, pp1.x, pp1.y});
-    const half2_t w00 = as_h2(pp0.x) * as_h2(cur.vs[0].x);
-    const half2_t w01 = as_h2(pp0.y) * as_h2(cur.vs[0].y);
-    const half2_t w10 = as_h2(pp1.x) * as_h2(cur.vs[1].x);
-    const half2_t w11 = as_h2(pp1.y) * as_h2(cur.vs[1].y);
-    Bw[r] = __builtin_bit_cast(half8_t, u32x4_t{as_u(w00), as_u(w01), as_u(w10), as_u(w11)});
-    st.wsum[r] = mfma16(Aones, Bw[r], st.wsum[r]);
-    st.zl[r] = mfma16(Azl, Bp, st.zl[r]);
+  for (int t = 0; t < NT; ++t) {
+    const half2_t w00 = as_h2(pp0.x) * as_h2(cur.vs[0][t].x);
+    const half2_t w01 = as_h2(pp0.y) * as_h2(cur.vs[0][t].y);
+    const half2_t w10 = as_h2(pp1.x) * as_h2(cur.vs[1][t].x);
+    const half2_t w11 = as_h2(pp1.y) * as_h2(cur.vs[1][t].y);
+    Bw[t] = __builtin_bit_cast(half8_t, u32x4_t{as_u(w00), as_u(w01), as_u(w10), as_u(w11)});
+    st.wsum[t] = mfma16(Aones, Bw[t], st.wsum[t]);
   }
-#define INT2KV_PV_TILE(MT)                                                                   \
-  {                                                                                          \
-    const half8_t Av = v_operand<MT>(cur.vc[0], cur.vc[1]);                                  \
-    _Pragma("unroll") for (int r = 0; r < RT; ++r) st.acc[r][MT] = mfma16(Av, Bw[r], st.acc[r][MT]); \
-  }
+  st.zl = mfma16(Azl, Bp, st.zl);
   // the value MFMAs issue at raised wave priority, so the other wave of the SIMD fills the vector
   // ALU beside them (measured: -2 % scan time at 5 query heads per KV head)
   __builtin_amdgcn_s_setprio(1);
+#define INT2KV_PV_TILE(MT)                                                                        \
+  st.acc[MT] = mfma16(v_operand<MT>(cur.vc[0], cur.vc[1]), Bw[WIDE ? (MT) >> 2 : 0], st.acc[MT]);
   INT2KV_PV_TILE(0)
   INT2KV_PV_TILE(1)
   INT2KV_PV_TILE(2)
@@ -464,8 +517,8 @@ __device__ __forceinline__ void pv_pair(ScanState<RT>& st, const PairLoads& cur,
   INT2KV_PV_TILE(5)
   INT2KV_PV_TILE(6)
   INT2KV_PV_TILE(7)
-  __builtin_amdgcn_s_setprio(0);
 #undef INT2KV_PV_TILE
+  __builtin_amdgcn_s_setprio(0);
 }
 
 constexpr int kStages = 3;       // page pairs staged (in flight) per wave
@@ -513,20 +566,21 @@ __device__ void page_prefix_block(const DecodeArgs& a) {
 
 // Block 0: page prefix sums (first, so it never waits for a free slot); blocks 1 ..: query
 // operands of KV head h for kQpSeqs sequences.
-__global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int rt) {
+__global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int wide) {
   if (blockIdx.x == 0)
     page_prefix_block(a);
   else
-    qprep_block(a, blockIdx.x - 1, rt);
+    qprep_block(a, blockIdx.x - 1, wide != 0);
 }
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // One wave: KV head h of sequence b, pages [p0, p1) of that sequence, with its partial (m, l, O')
 // per query head written to partial slot `slot`.
-template <int RT>
+template <bool WIDE>
 __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, int p0, int p1, int slot, int l,
                                              uint8_t* stage_w, _Float16 (*p_w)[2][8][kBlock], float* al_w) {
+  constexpr int NJ = ScanState<WIDE>::NJ, NT = ScanState<WIDE>::NT;
   const int lo = l & 15, hi = l >> 4;
   const int L = seq_len_m(a, b);
   const int npairs = (p1 - p0 + 1) >> 1;
@@ -534,22 +588,35 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
 
   // ---- query operands of (b, h): plain loads, issued ahead of the first page DMAs so that both
   // latencies overlap (the first use waits for every load in flight, which the prologue does anyway)
-  const uint8_t* qop = a.qop + ((size_t)b * a.H + h) * RT * kQopTile;
-  ScanState<RT> st;
+  const uint8_t* qop = a.qop + ((size_t)b * a.H + h) * kQopTile;
+  const float* cst = reinterpret_cast<const float*>(qop + 4096);
+  ScanState<WIDE> st;
 #pragma unroll
-  for (int r = 0; r < RT; ++r) {
-    const uint8_t* t = qop + r * kQopTile;
+  for (int i = 0; i < 4; ++i) st.A[i] = *reinterpret_cast<const half8_t*>(qop + (i * 64 + l) * 16);
+  if constexpr (WIDE) {
+    st.cinit[0] = *reinterpret_cast<const float4_t*>(cst + 4 * hi);       // D01 rows 4hi..4hi+3
+    st.cinit[1] = *reinterpret_cast<const float4_t*>(cst + 16 + 4 * hi);  // D23 rows 4hi..4hi+3
 #pragma unroll
-    for (int i = 0; i < 4; ++i) st.A[r][i] = *reinterpret_cast<const half8_t*>(t + (i * 64 + l) * 16);
-    st.cinit[r] = *reinterpret_cast<const float4_t*>(t + 4096 + hi * 16);
-    st.sqL[r] = *reinterpret_cast<const float4_t*>(t + 4096 + 64 + hi * 16);
-    st.invsig[r] = *reinterpret_cast<const float*>(t + 4096 + 128 + hi * 4);
+    for (int u = 0; u < 2; ++u) {
+      const float4_t v = *reinterpret_cast<const float4_t*>(cst + 32 + 8 * hi + 4 * u);
 #pragma unroll
-    for (int mt = 0; mt < 8; ++mt) st.acc[r][mt] = float4_t{0.f, 0.f, 0.f, 0.f};
-    st.wsum[r] = float4_t{0.f, 0.f, 0.f, 0.f};
-    st.zl[r] = float4_t{0.f, 0.f, 0.f, 0.f};
-    st.mref[r] = kMaxInit;
+      for (int g = 0; g < 4; ++g) st.sq[u][g] = v[g];
+      st.invsig[u] = cst[64 + 2 * hi + u];
+    }
+  } else {
+    st.cinit[0] = *reinterpret_cast<const float4_t*>(cst + 4 * hi);
+    const float4_t v = *reinterpret_cast<const float4_t*>(cst + 16 + 4 * hi);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) st.sq[0][g] = v[g];
+    st.invsig[0] = cst[32 + hi];
   }
+#pragma unroll
+  for (int mt = 0; mt < 8; ++mt) st.acc[mt] = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < NT; ++t) st.wsum[t] = float4_t{0.f, 0.f, 0.f, 0.f};
+  st.zl = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < NJ; ++u) st.mref[u] = kMaxInit;
 
   // ---- pipeline over the segment's page pairs (pages p0 + 2k, p0 + 2k + 1)
   const bt_ptr bt = (bt_ptr)(uintptr_t)(a.block_table + (size_t)b * a.max_blocks);
@@ -568,7 +635,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   // block ids of the next pair to stage, read one step ahead of their use so that the scalar
   // loads overlap the step's arithmetic
   BlockIds nid = load_ids(bt, p0 + 2 * kStages, p1);
-  PairLoads X, Y;
+  PairLoads<WIDE> X, Y;
   {
     if (kStages - 1 < npairs)
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * 2 * (kStages - 1)) : "memory");
@@ -582,15 +649,15 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
       okmask = (okmask & ~3u) | stage_pair(a.pool, base_h, stride, nblk, nid, p0 + 2 * kStages, p1, stage_base, l);
       nid = next;
     }
-    float a2[2][RT];
-    qk_pair<RT>(st, X, p0, L, lo, a2);
-    softmax_pair<RT>(st, a2, lo, hi, p_w[0], al_w);
+    float a2[2][NJ];
+    qk_pair<WIDE>(st, X, p0, L, lo, a2);
+    softmax_pair<WIDE>(st, a2, lo, hi, p_w[0], al_w);
   }
   // One step: read pair k+1 (staged kStages pairs ago), refill its slot with pair k+1+kStages,
   // scores of pair k+1 beside the value accumulation of pair k, then the softmax of pair k+1.
   // STEADY: every condition holds (k + 1 + kStages < npairs).
   int sl = 0;  // slot of pair k
-  auto step = [&](auto steady_tag, const PairLoads& cur, PairLoads& nxt, int k) {
+  auto step = [&](auto steady_tag, const PairLoads<WIDE>& cur, PairLoads<WIDE>& nxt, int k) {
     constexpr bool STEADY = decltype(steady_tag)::value;
     sl = sl + 1 == kStages ? 0 : sl + 1;  // slot of pair k + 1
     const bool more = STEADY || k + 1 < npairs;
@@ -615,11 +682,11 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
         nid = next;
       }
     }
-    float a2[2][RT];
-    if (more) qk_pair<RT>(st, nxt, p0 + 2 * (k + 1), L, lo, a2);
+    float a2[2][NJ];
+    if (more) qk_pair<WIDE>(st, nxt, p0 + 2 * (k + 1), L, lo, a2);
     lds_sync_wave();
-    pv_pair<RT>(st, cur, lo, hi, p_w[k & 1]);
-    if (more) softmax_pair<RT>(st, a2, lo, hi, p_w[(k + 1) & 1], al_w);
+    pv_pair<WIDE>(st, cur, lo, hi, p_w[k & 1]);
+    if (more) softmax_pair<WIDE>(st, a2, lo, hi, p_w[(k + 1) & 1], al_w);
   };
   int k = 0;
   for (; k + 2 + kStages < npairs; k += 2) {
@@ -634,42 +701,55 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   // ---- partial (m, l, O') of every query head of this KV head
   const int gq = a.gq;
   float* part = a.part + ((size_t)slot * a.Hq + h * gq) * kPartStride;
+  // m and l of query heads jq(hi, u): l_j sits in rows 4..7 of the (Z, l) tile, column of j, so in
+  // lane (first column of j, hi = 1)
 #pragma unroll
-  for (int r = 0; r < RT; ++r) {
-    // column (j, g) = lo of tile r: W from any row; Z[j][g] from lane (lo, hi = 0), register g;
-    // l[j] from lane (4 (j - 4r), hi = 1), register 0
-    const float wa = st.wsum[r][0];
-    const int g = lo & 3;
-    const float zown = g == 0 ? st.zl[r][0] : g == 1 ? st.zl[r][1] : g == 2 ? st.zl[r][2] : st.zl[r][3];
-    const float za = __shfl(zown, lo);
-    const float ls = __shfl(st.zl[r][0], 16 + 4 * hi);  // l of row j = 4r + hi
-    if (lo == 0 && 4 * r + hi < gq) {
-      float* dst = part + (size_t)(4 * r + hi) * kPartStride;
-      dst[0] = st.mref[r];
+  for (int u = 0; u < NJ; ++u) {
+    const int j = NJ * hi + u;
+    const float ls = __shfl(st.zl[0], 16 + (WIDE ? 2 * j : 4 * j));
+    if (lo == 0 && j < gq) {
+      float* dst = part + (size_t)j * kPartStride;
+      dst[0] = st.mref[u];
       dst[1] = ls;
     }
-    const int jc = 4 * r + (lo >> 2);
-    float* dst = part + (size_t)jc * kPartStride + 4;
+  }
+  // O' of column lo = (jc, g) (narrow) or (jc, gg) (wide): W from any row of the column's weight
+  // sum; Z[jc][g] from lane (lo, hi = 0), register g
+  const int jc = WIDE ? lo >> 1 : lo >> 2;
+  float zc[2], wc[2];
+  if constexpr (WIDE) {
+    const bool odd = lo & 1;
+    zc[0] = __shfl(odd ? st.zl[1] : st.zl[0], lo);  // group lo & 1
+    zc[1] = __shfl(odd ? st.zl[3] : st.zl[2], lo);  // group 2 + (lo & 1)
+    wc[0] = st.wsum[0][0];
+    wc[1] = st.wsum[NT - 1][0];
+  } else {
+    const int g = lo & 3;
+    const float zown = g == 0 ? st.zl[0] : g == 1 ? st.zl[1] : g == 2 ? st.zl[2] : st.zl[3];
+    zc[0] = zc[1] = __shfl(zown, lo);
+    wc[0] = wc[1] = st.wsum[0][0];
+  }
+  float* dst = part + (size_t)jc * kPartStride + 4;
 #define INT2KV_OUT_TILE(MT)                                                                         \
-  if ((lo & 3) == ((MT) >> 1) && jc < gq) {                                                         \
+  if ((WIDE ? (lo & 1) == (((MT) >> 1) & 1) : (lo & 3) == ((MT) >> 1)) && jc < gq) {                \
     const float sc = (float)(1 << land_e(MT));                                                      \
+    const float wa = wc[(MT) >> 2], za = zc[(MT) >> 2];                                             \
     float4 o;                                                                                       \
-    o.x = fmaf(sc, st.acc[r][MT][0] - wa, za);                                                      \
-    o.y = fmaf(sc, st.acc[r][MT][1] - wa, za);                                                      \
-    o.z = fmaf(sc, st.acc[r][MT][2] - wa, za);                                                      \
-    o.w = fmaf(sc, st.acc[r][MT][3] - wa, za);                                                      \
+    o.x = fmaf(sc, st.acc[MT][0] - wa, za);                                                         \
+    o.y = fmaf(sc, st.acc[MT][1] - wa, za);                                                         \
+    o.z = fmaf(sc, st.acc[MT][2] - wa, za);                                                         \
+    o.w = fmaf(sc, st.acc[MT][3] - wa, za);                                                         \
     *reinterpret_cast<float4*>(dst + 16 * (MT) + 4 * hi) = o;                                      \
   }
-    INT2KV_OUT_TILE(0)
-    INT2KV_OUT_TILE(1)
-    INT2KV_OUT_TILE(2)
-    INT2KV_OUT_TILE(3)
-    INT2KV_OUT_TILE(4)
-    INT2KV_OUT_TILE(5)
-    INT2KV_OUT_TILE(6)
-    INT2KV_OUT_TILE(7)
+  INT2KV_OUT_TILE(0)
+  INT2KV_OUT_TILE(1)
+  INT2KV_OUT_TILE(2)
+  INT2KV_OUT_TILE(3)
+  INT2KV_OUT_TILE(4)
+  INT2KV_OUT_TILE(5)
+  INT2KV_OUT_TILE(6)
+  INT2KV_OUT_TILE(7)
 #undef INT2KV_OUT_TILE
-  }
   wait_vm_all();
 }
 
@@ -679,7 +759,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
 // of one block together. A range crossing sequence boundaries is scanned segment by segment; the
 // partial of (group g, sequence b) goes to slot g + b, which is unique because the (g, b) pairs
 // that meet form a monotone staircase.
-template <int RT>
+template <bool WIDE>
 __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t stage[kWavesPerWG][kStages][2][kRecord];
   __shared__ _Float16 p_lds[kWavesPerWG][2][2][8][kBlock];
@@ -698,7 +778,7 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   for (int pos = s;;) {
     const int seg_end = min(e, Sb1);
     const int Sb2 = seg_end < e ? prefix[b + 2] : 0;  // next sequence's end, fetched ahead
-    scan_segment<RT>(a, b, h, pos - Sb, seg_end - Sb, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w]);
+    scan_segment<WIDE>(a, b, h, pos - Sb, seg_end - Sb, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w]);
     pos = seg_end;
     if (pos >= e) break;
     ++b;
@@ -797,19 +877,18 @@ __global__ __launch_bounds__(128) void merge_flat_kernel(DecodeArgs a, int G, in
 hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
   if (a.gq > 8) return hipErrorNotSupported;
   hipLaunchKernelGGL(qprep_kernel, dim3(1 + a.H * ((a.B + kQpSeqs - 1) / kQpSeqs)), dim3(256), 0, s, a,
-                     (a.gq + 3) / 4);
+                     a.gq > 4 ? 1 : 0);
   return hipGetLastError();
 }
 
 hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   if (a.gq > 8) return hipErrorNotSupported;
-  const int rt = (a.gq + 3) / 4;
   dim3 grid(a.grid_g, (a.H + kWavesPerWG - 1) / kWavesPerWG);
   const int threads = 64 * min(a.H, kWavesPerWG);
-  if (rt == 1)
-    hipExtLaunchKernelGGL(decode_scan_flat_kernel<1>, grid, dim3(threads), 0, s, ev0, ev1, 0, a);
+  if (a.gq > 4)
+    hipExtLaunchKernelGGL(decode_scan_flat_kernel<true>, grid, dim3(threads), 0, s, ev0, ev1, 0, a);
   else
-    hipExtLaunchKernelGGL(decode_scan_flat_kernel<2>, grid, dim3(threads), 0, s, ev0, ev1, 0, a);
+    hipExtLaunchKernelGGL(decode_scan_flat_kernel<false>, grid, dim3(threads), 0, s, ev0, ev1, 0, a);
   return hipGetLastError();
 }
 
