@@ -106,6 +106,10 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   off = up(off + (size_t)(B + 1) * sizeof(int32_t));
   p.off_wginfo = off;
   off = up(off + (size_t)p.grid_g * 4 * sizeof(int32_t));
+  // page list: one 16-byte entry per page of every sequence (lengths are clamped to max_ctx), plus
+  // padding the scan may read (never use) one pair past the last page
+  p.off_pages = off;
+  off = up(off + ((size_t)B * (((size_t)max_ctx + kBlock - 1) / kBlock) + 8) * 16);
   p.off_part = off;
   const size_t part_rows = p.variant == 2 ? (size_t)(p.grid_g + B) : (size_t)B * p.n_chunks;
   off = up(off + part_rows * Hq * kPartStride * sizeof(float));
@@ -246,6 +250,7 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
   a.n_chunks = plan.n_chunks;
   a.prefix = reinterpret_cast<int32_t*>(ws + plan.off_prefix);
   a.wg_info = reinterpret_cast<int32_t*>(ws + plan.off_wginfo);
+  a.pages = reinterpret_cast<uint32_t*>(ws + plan.off_pages);
   a.grid_g = plan.grid_g;
 
   hipError_t e = hipSuccess;

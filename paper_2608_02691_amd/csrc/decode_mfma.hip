@@ -45,16 +45,29 @@ __host__ __device__ constexpr int land_e(int x) {
   return (x == 4 || x == 7) ? 2 : ((x == 1 || x == 3 || x == 6) ? 4 : 6);
 }
 
-// The codes at position X of both 16-bit halves of w, as an fp16 pair (1 + c_lo 2^-e, 1 + c_hi 2^-e).
+// Landing constants held in registers: the masks of code positions 2, 3, 4 (SGPRs) and the fp16
+// 1.0 pattern (VGPR). They pass through empty asm statements (no instruction) so the compiler cannot
+// fold them into literals; with all three operands in registers a landing selects one v_and_or_b32
+// instead of a v_and_b32 / v_or_b32 pair with literals.
+struct LandK {
+  uint32_t m[3];  // 0x00030003 << 2 pos, pos = 2, 3, 4
+  uint32_t one;   // 0x3C003C00
+};
+__device__ __forceinline__ LandK land_constants() {
+  LandK k{{0x00300030u, 0x00C000C0u, 0x03000300u}, 0x3C003C00u};
+  asm volatile("" : "+s"(k.m[0]), "+s"(k.m[1]), "+s"(k.m[2]), "+v"(k.one));
+  return k;
+}
+
+// The codes at position X of both 16-bit halves of w, as an fp16 pair (1 + c_lo 2^-e, 1 + c_hi 2^-e):
+// one AND-OR after at most one shift. Plain C, not inline asm: the compiler sees the VGPR write and
+// keeps the matrix-core operand hazards around it (an asm landing placed right after an MFMA that
+// still has to read the same registers corrupts that MFMA's inputs).
 template <int X>
-__device__ __forceinline__ uint32_t land(uint32_t w) {
+__device__ __forceinline__ uint32_t land(uint32_t w, const LandK& k) {
   constexpr int pos = X >= 5 ? X - 3 : (X <= 1 ? X + 2 : X);
   const uint32_t v = X >= 5 ? (w >> 6) : (X <= 1 ? (w << 4) : w);
-  // one v_and_or_b32; gfx9 VOP3 encodings take no literal, so the mask rides in an SGPR and the
-  // fp16 1.0 pattern in a VGPR
-  uint32_t r;
-  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(v), "s"(0x00030003u << (2 * pos)), "v"(0x3C003C00u));
-  return r;
+  return (v & k.m[pos - 2]) | k.one;
 }
 
 __device__ __forceinline__ void lds_sync_wave() {
@@ -96,6 +109,34 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, bool wide) {
   const int h = blk % H, b0 = kQpSeqs * (blk / H), nseq = min(kQpSeqs, a.B - b0);
   const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
   if (tid < 8 * kQpSeqs) smax[tid] = 0;
+  // Page list entries of this block's sequences, for the pages i with i % H == h: the block first
+  // sums the pages of the sequences before b0 (the same prefix the page-prefix block computes).
+  {
+    __shared__ int red[256];
+    int s = 0;
+    for (int bb = tid; bb < b0; bb += 256) s += (seq_len_m(a, bb) + kBlock - 1) >> 4;
+    red[tid] = s;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+      if (tid < off) red[tid] += red[tid + off];
+      __syncthreads();
+    }
+    size_t base = (size_t)red[0];
+    const uint64_t pool = (uint64_t)(uintptr_t)a.pool;
+    const uint64_t stride = (uint64_t)H * kRecord;
+    for (int sq = 0; sq < nseq; ++sq) {
+      const int b = b0 + sq, L = seq_len_m(a, b), np = (L + kBlock - 1) >> 4;
+      const int32_t* row = a.block_table + (size_t)b * a.max_blocks;
+      for (int i = h + H * tid; i < np; i += H * 256) {
+        const int id = row[i];
+        const bool ok = (uint32_t)id < (uint32_t)a.num_blocks;
+        const uint64_t rec = pool + (ok ? (uint64_t)(uint32_t)id * stride : 0ull);
+        *reinterpret_cast<uint4*>(a.pages + 4 * (base + i)) =
+            make_uint4((uint32_t)rec, (uint32_t)(rec >> 32), ok ? (uint32_t)min(kBlock, L - kBlock * i) : 0u, 0u);
+      }
+      base += np;
+    }
+  }
   // A operand (query rows 16 w + lo, 8 consecutive channels per lane), fetched before R so the
   // two latencies overlap; absent rows are zero
   qp_bf16x8_t A[4];
@@ -249,7 +290,7 @@ struct PairLoads {
   uint2 vc[2];  // V codes of half lo, tokens 4hi..4hi+3
   uint2 vs[2][WIDE ? 2 : 1];  // V scales, tokens 4hi..4hi+3: group lo&3 (narrow); lo&1, 2+(lo&1) (wide)
   uint2 vz[2];  // V zeros of group lo&3, tokens 4hi..4hi+3
-  int ok[2];    // wave-uniform: page holds cached tokens
+  float mk[2];  // 0 if this lane's token of the page is cached, else -inf
 };
 
 // Page records are staged in LDS by the wave that consumes them, with LDS-DMA loads
@@ -267,50 +308,39 @@ __device__ __forceinline__ void dma4(const uint8_t* base, uint32_t voff, uint32_
                : "memory", "m0");
 }
 
+// Page list: one 16-byte entry per page of the concatenated sequences, written by the query-prep
+// kernel: {address of the page's record of KV head 0 (low, high word), cached tokens in the page,
+// 0}. A page whose block id lies outside the pool holds 0 tokens and points at block 0.
+struct PageEnt {
+  uint32_t lo, hi, nv, pad;
+};
+typedef const __attribute__((address_space(4))) PageEnt* ent_ptr;
+
+__device__ __forceinline__ PageEnt load_ent(ent_ptr p, int i) {
+  return PageEnt{p[i].lo, p[i].hi, p[i].nv, 0u};
+}
+
 // DMA of one 1536-byte page record into LDS at lds_addr: the 1024 bytes of codes with one dwordx4
-// load, the two 256-byte metadata blocks with dword loads. The instruction offset moves both the
-// global and the LDS address, so one M0 value serves the whole record.
-__device__ __forceinline__ void dma_page(const uint8_t* rec, uint32_t lds_addr, int l) {
+// load, the two 256-byte metadata blocks with dword loads. (rec_lo, rec_hi) is the record of KV
+// head 0; the lane offsets voff16 = 16 l + 1536 h and voff4 = 4 l + 1536 h select head h. The
+// instruction offset moves both the global and the LDS address, so one M0 value serves the whole
+// record.
+__device__ __forceinline__ void dma_page(uint32_t rec_lo, uint32_t rec_hi, uint32_t lds_addr, uint32_t voff16,
+                                         uint32_t voff4) {
+  const uint8_t* rec = reinterpret_cast<const uint8_t*>(((uint64_t)rec_hi << 32) | rec_lo);
   asm volatile(
       "s_mov_b32 m0, %0\n\t"
       "s_nop 0\n\t"
       "global_load_lds_dwordx4 %1, %3\n\t"
       "global_load_lds_dword %2, %3 offset:1024\n\t"
       "global_load_lds_dword %2, %3 offset:1280" ::"s"(lds_addr),
-      "v"(16 * l), "v"(4 * l), "s"(rec)
+      "v"(voff16), "v"(voff4), "s"(rec)
       : "memory", "m0");
 }
 
-typedef const int32_t __attribute__((address_space(4)))* bt_ptr;
-
-struct BlockIds {
-  int b0, b1;
-};
-
-// Block ids of pages page0 and page0 + 1 of a sequence row `bt` (indexes clamped to the last page
-// p1 - 1 of the segment, so the reads stay inside the row).
-__device__ __forceinline__ BlockIds load_ids(bt_ptr bt, int page0, int p1) {
-  const int last = p1 - 1;
-  return {bt[page0 < last ? page0 : last], bt[page0 + 1 < last ? page0 + 1 : last]};
-}
-
-// Stage the page pair (page0, page0 + 1) with block ids `id` into the slot at slot_addr; returns
-// the two validity bits (page inside the segment and block id inside the pool). Invalid pages
-// stage the pool's first record instead (read, then ignored). base_h = pool + h * 1536,
-// stride = H * 1536.
-__device__ __forceinline__ uint32_t stage_pair(const uint8_t* pool, const uint8_t* base_h, uint32_t stride,
-                                               uint32_t nblk, BlockIds id, int page0, int p1,
-                                               uint32_t slot_addr, int l) {
-  const bool ok0 = page0 < p1 && (uint32_t)id.b0 < nblk;
-  const bool ok1 = page0 + 1 < p1 && (uint32_t)id.b1 < nblk;
-  dma_page(ok0 ? base_h + (size_t)(uint32_t)id.b0 * stride : pool, slot_addr, l);
-  dma_page(ok1 ? base_h + (size_t)(uint32_t)id.b1 * stride : pool, slot_addr + kRecord, l);
-  return (ok0 ? 1u : 0u) | (ok1 ? 2u : 0u);
-}
-
-// Operands of one page pair read back from its staging slot. A page that holds no cached tokens
-// (past the segment, or a block id outside the pool) stages a stand-in record; its scores are
-// masked to -inf, so p = 0 multiplies its (finite) codes and metadata and it adds nothing.
+// Operands of one page pair read back from its staging slot. Tokens a page does not hold (past the
+// sequence's end, or the whole page for a block id outside the pool or a stand-in past the segment)
+// get scores of -inf, so p = 0 multiplies their (finite) codes and metadata and they add nothing.
 // An empty asm that uses every register read_pair filled: the compiler places its wait for those
 // LDS reads here, ahead of the scalar block-id loads that follow (a later wait would have to
 // wait for those loads too, since scalar loads return out of order).
@@ -325,13 +355,12 @@ __device__ __forceinline__ void pin_pair(PairLoads<WIDE>& p) {
   }
 }
 template <bool WIDE>
-__device__ __forceinline__ void read_pair(const uint8_t* slot, bool ok0, bool ok1, int lo, int hi,
+__device__ __forceinline__ void read_pair(const uint8_t* slot, uint32_t nv0, uint32_t nv1, int lo, int hi,
                                           PairLoads<WIDE>& p) {
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
     const uint8_t* rec = slot + P * kRecord;
-    const bool ok = P == 0 ? ok0 : ok1;
-    p.ok[P] = ok;
+    p.mk[P] = (uint32_t)lo < (P == 0 ? nv0 : nv1) ? 0.0f : -INFINITY;
     p.kc[P] = *reinterpret_cast<const uint2*>(rec + kOffKCodes + 32 * lo + 8 * hi);
     p.km[P] = *reinterpret_cast<const uint4*>(rec + kOffKMeta + 16 * lo);
     p.vc[P] = *reinterpret_cast<const uint2*>(rec + kOffVCodes + 32 * lo + 8 * hi);
@@ -345,14 +374,16 @@ __device__ __forceinline__ void read_pair(const uint8_t* slot, bool ok0, bool ok
   }
 }
 template <int X>
-__device__ __forceinline__ half8_t k_operand(uint2 w) {
+__device__ __forceinline__ half8_t k_operand(uint2 w, const LandK& k) {
   // instruction i = X/2 ... called with X = 2i: registers (d0,x), (d1,x), (d0,x+1), (d1,x+1)
-  return __builtin_bit_cast(half8_t, u32x4_t{land<X>(w.x), land<X>(w.y), land<X + 1>(w.x), land<X + 1>(w.y)});
+  return __builtin_bit_cast(half8_t,
+                            u32x4_t{land<X>(w.x, k), land<X>(w.y, k), land<X + 1>(w.x, k), land<X + 1>(w.y, k)});
 }
 
 template <int MT>
-__device__ __forceinline__ half8_t v_operand(uint2 w0, uint2 w1) {
-  return __builtin_bit_cast(half8_t, u32x4_t{land<MT>(w0.x), land<MT>(w0.y), land<MT>(w1.x), land<MT>(w1.y)});
+__device__ __forceinline__ half8_t v_operand(uint2 w0, uint2 w1, const LandK& k) {
+  return __builtin_bit_cast(half8_t,
+                            u32x4_t{land<MT>(w0.x, k), land<MT>(w0.y, k), land<MT>(w1.x, k), land<MT>(w1.y, k)});
 }
 
 __device__ __forceinline__ float4_t mfma16(half8_t a, half8_t b, float4_t c) {
@@ -373,22 +404,23 @@ struct ScanState {
   float4_t wsum[NT];            // sum_t w_t of each column (every row); wide: groups gg, 2 + gg
   float4_t zl;                  // rows 0..3: sum_t p_t z_tg (row = group); rows 4..7: sum_t p_t
   float mref[NJ];
+  LandK lk;                     // landing constants
 };
 
 // Scores of one page pair, base-2 logits, -inf where masked: a2[P][u] for token lo of page P and
 // query head jq(hi, u). The accumulation chains of both pages are issued interleaved so that each
 // hides the others' latency.
 template <bool WIDE>
-__device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoads<WIDE>& cur, int pg, int t1,
-                                        int lo, float (&a2)[2][ScanState<WIDE>::NJ]) {
+__device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoads<WIDE>& cur,
+                                        float (&a2)[2][ScanState<WIDE>::NJ]) {
   constexpr int NT = ScanState<WIDE>::NT, NJ = ScanState<WIDE>::NJ;
   half8_t B[2][4];
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
-    B[P][0] = k_operand<0>(cur.kc[P]);
-    B[P][1] = k_operand<2>(cur.kc[P]);
-    B[P][2] = k_operand<4>(cur.kc[P]);
-    B[P][3] = k_operand<6>(cur.kc[P]);
+    B[P][0] = k_operand<0>(cur.kc[P], st.lk);
+    B[P][1] = k_operand<2>(cur.kc[P], st.lk);
+    B[P][2] = k_operand<4>(cur.kc[P], st.lk);
+    B[P][3] = k_operand<6>(cur.kc[P], st.lk);
   }
   float4_t d[2][NT];
 #pragma unroll
@@ -411,7 +443,6 @@ __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoa
   }
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
-    const bool tv = cur.ok[P] && (pg + P) * kBlock + lo < t1;
     const half2_t m[4] = {as_h2(cur.km[P].x), as_h2(cur.km[P].y), as_h2(cur.km[P].z), as_h2(cur.km[P].w)};
 #pragma unroll
     for (int u = 0; u < NJ; ++u) {
@@ -428,7 +459,7 @@ __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoa
       zq = fmaf((float)m[1].y, st.sq[u][1], zq);
       zq = fmaf((float)m[2].y, st.sq[u][2], zq);
       zq = fmaf((float)m[3].y, st.sq[u][3], zq);
-      a2[P][u] = fmaf(sd, st.invsig[u], zq) + (tv ? 0.0f : -INFINITY);
+      a2[P][u] = fmaf(sd, st.invsig[u], zq) + cur.mk[P];
     }
   }
 }
@@ -508,7 +539,7 @@ __device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WID
   // ALU beside them (measured: -2 % scan time at 5 query heads per KV head)
   __builtin_amdgcn_s_setprio(1);
 #define INT2KV_PV_TILE(MT)                                                                        \
-  st.acc[MT] = mfma16(v_operand<MT>(cur.vc[0], cur.vc[1]), Bw[WIDE ? (MT) >> 2 : 0], st.acc[MT]);
+  st.acc[MT] = mfma16(v_operand<MT>(cur.vc[0], cur.vc[1], st.lk), Bw[WIDE ? (MT) >> 2 : 0], st.acc[MT]);
   INT2KV_PV_TILE(0)
   INT2KV_PV_TILE(1)
   INT2KV_PV_TILE(2)
@@ -575,15 +606,16 @@ __global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int wide) {
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// One wave: KV head h of sequence b, pages [p0, p1) of that sequence, with its partial (m, l, O')
-// per query head written to partial slot `slot`.
+// One wave: KV head h of sequence b, global pages [gs, ge) (all of sequence b), with its partial
+// (m, l, O') per query head written to partial slot `slot`.
 template <bool WIDE>
-__device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, int p0, int p1, int slot, int l,
+__device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, int gs, int ge, int slot, int l,
                                              uint8_t* stage_w, _Float16 (*p_w)[2][8][kBlock], float* al_w) {
   constexpr int NJ = ScanState<WIDE>::NJ, NT = ScanState<WIDE>::NT;
   const int lo = l & 15, hi = l >> 4;
-  const int L = seq_len_m(a, b);
-  const int npairs = (p1 - p0 + 1) >> 1;
+  const int n = ge - gs;             // pages
+  const int npairs = (n + 1) >> 1;   // the last pair may hold one page
+  const int nfull = n >> 1;          // pairs of two pages
   const uint32_t stage_base = (uint32_t)(uintptr_t)stage_w;
 
   // ---- query operands of (b, h): plain loads, issued ahead of the first page DMAs so that both
@@ -617,85 +649,137 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   st.zl = float4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int u = 0; u < NJ; ++u) st.mref[u] = kMaxInit;
+  st.lk = land_constants();
 
-  // ---- pipeline over the segment's page pairs (pages p0 + 2k, p0 + 2k + 1)
-  const bt_ptr bt = (bt_ptr)(uintptr_t)(a.block_table + (size_t)b * a.max_blocks);
-  const uint8_t* base_h = a.pool + (size_t)h * kRecord;
-  const uint32_t stride = (uint32_t)a.H * kRecord;
-  const uint32_t nblk = (uint32_t)a.num_blocks;
-  uint32_t okmask = 0;  // bits 2*slot, 2*slot+1: validity of the two pages staged in slot
-  BlockIds ids[kStages];
-#pragma unroll
-  for (int k = 0; k < kStages; ++k) ids[k] = load_ids(bt, p0 + 2 * k, p1);
-#pragma unroll
-  for (int k = 0; k < kStages; ++k)
-    if (k < npairs)
-      okmask |= stage_pair(a.pool, base_h, stride, nblk, ids[k], p0 + 2 * k, p1, stage_base + k * 2 * kRecord, l)
-                << (2 * k);
-  // block ids of the next pair to stage, read one step ahead of their use so that the scalar
-  // loads overlap the step's arithmetic
-  BlockIds nid = load_ids(bt, p0 + 2 * kStages, p1);
+  // ---- pipeline over the segment's page pairs (global pages gs + 2k, gs + 2k + 1; the second page
+  // of a last pair of one page is a stand-in: block 0, no tokens). Pair k sits in slot k % kStages.
+  const ent_ptr ent = (ent_ptr)(uintptr_t)(a.pages) + gs;
+  const uint32_t voff16 = 16 * l + h * kRecord, voff4 = 4 * l + h * kRecord;
+  const uint32_t pool_lo = (uint32_t)(uintptr_t)a.pool, pool_hi = (uint32_t)((uintptr_t)a.pool >> 32);
+  uint32_t nv[kStages][2];  // cached tokens of the two pages staged in each slot
+  // entries of pair k with the bounds check of the last pair (paths outside the steady loop): both
+  // loads are unconditional (the second index clamped into the segment), and a second page past
+  // the segment becomes the stand-in afterwards, by scalar selects
+  auto entries = [&](int k, PageEnt& e0, PageEnt& e1) {
+    const bool two = 2 * k + 1 < n;
+    e0 = load_ent(ent, 2 * k);
+    e1 = load_ent(ent, two ? 2 * k + 1 : 2 * k);
+    e1.lo = two ? e1.lo : pool_lo;
+    e1.hi = two ? e1.hi : pool_hi;
+    e1.nv = two ? e1.nv : 0u;
+  };
+  auto stage = [&](auto slot_tag, const PageEnt& e0, const PageEnt& e1) {
+    constexpr int SL = decltype(slot_tag)::value;
+    const uint32_t sa = stage_base + SL * 2 * kRecord;
+    dma_page(e0.lo, e0.hi, sa, voff16, voff4);
+    dma_page(e1.lo, e1.hi, sa + kRecord, voff16, voff4);
+    nv[SL][0] = e0.nv;
+    nv[SL][1] = e1.nv;
+  };
+  auto pin_ent = [](PageEnt& e0, PageEnt& e1) {
+    asm volatile("" : "+s"(e0.lo), "+s"(e0.hi), "+s"(e0.nv), "+s"(e1.lo), "+s"(e1.hi), "+s"(e1.nv));
+  };
+  {
+    PageEnt e0, e1;
+    entries(0, e0, e1);
+    stage(std::integral_constant<int, 0>{}, e0, e1);
+    if (1 < npairs) {
+      entries(1, e0, e1);
+      stage(std::integral_constant<int, 1>{}, e0, e1);
+    }
+    if (2 < npairs) {
+      entries(2, e0, e1);
+      stage(std::integral_constant<int, 2>{}, e0, e1);
+    }
+  }
+  static_assert(kStages == 3, "the prologue stages three pairs");
+  // entries of the next pair the steady loop stages, read one step ahead of their use so that the
+  // scalar loads overlap the step's arithmetic (only full pairs inside the segment are read)
+  PageEnt n0{0u, 0u, 0u, 0u}, n1 = n0;
+  if (kStages + 1 < nfull) {
+    n0 = load_ent(ent, 2 * (kStages + 1));
+    n1 = load_ent(ent, 2 * (kStages + 1) + 1);
+  }
   PairLoads<WIDE> X, Y;
   {
     if (kStages - 1 < npairs)
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * 2 * (kStages - 1)) : "memory");
     else
       wait_vm_all();
-    read_pair(stage_w, okmask & 1u, (okmask >> 1) & 1u, lo, hi, X);
+    read_pair(stage_w, nv[0][0], nv[0][1], lo, hi, X);
     pin_pair(X);
     if (kStages < npairs) {
-      asm volatile("" : "+s"(nid.b0), "+s"(nid.b1));
-      const BlockIds next = load_ids(bt, p0 + 2 * (kStages + 1), p1);
-      okmask = (okmask & ~3u) | stage_pair(a.pool, base_h, stride, nblk, nid, p0 + 2 * kStages, p1, stage_base, l);
-      nid = next;
+      PageEnt e0, e1;
+      entries(kStages, e0, e1);
+      stage(std::integral_constant<int, 0>{}, e0, e1);
     }
     float a2[2][NJ];
-    qk_pair<WIDE>(st, X, p0, L, lo, a2);
+    qk_pair<WIDE>(st, X, a2);
     softmax_pair<WIDE>(st, a2, lo, hi, p_w[0], al_w);
   }
-  // One step: read pair k+1 (staged kStages pairs ago), refill its slot with pair k+1+kStages,
-  // scores of pair k+1 beside the value accumulation of pair k, then the softmax of pair k+1.
-  // STEADY: every condition holds (k + 1 + kStages < npairs).
-  int sl = 0;  // slot of pair k
-  auto step = [&](auto steady_tag, const PairLoads<WIDE>& cur, PairLoads<WIDE>& nxt, int k) {
+  // Step J of an unrolled group that starts at pair k (k % kStages = 0): read pair kk + 1 =
+  // k + J + 1 (staged kStages pairs ago, slot SL), refill its slot with pair kk + 1 + kStages,
+  // scores of pair kk + 1 beside the value accumulation of pair kk, then the softmax of pair
+  // kk + 1. STEADY: pair kk + 1 + kStages is a full pair inside the segment.
+  auto step = [&](auto j_tag, auto steady_tag, const PairLoads<WIDE>& cur, PairLoads<WIDE>& nxt, int k) {
+    constexpr int J = decltype(j_tag)::value;
     constexpr bool STEADY = decltype(steady_tag)::value;
-    sl = sl + 1 == kStages ? 0 : sl + 1;  // slot of pair k + 1
-    const bool more = STEADY || k + 1 < npairs;
+    constexpr int SL = (J + 1) % kStages;
+    const int kk = k + J;
+    const bool more = STEADY || kk + 1 < npairs;
     if (more) {
-      if (STEADY || k + kStages < npairs)
+      if (STEADY || kk + kStages < npairs)
         asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * 2 * (kStages - 1)) : "memory");
       else
         wait_vm_all();
-      read_pair(stage_w + sl * 2 * kRecord, (okmask >> (2 * sl)) & 1u, (okmask >> (2 * sl + 1)) & 1u, lo, hi, nxt);
+      read_pair(stage_w + SL * 2 * kRecord, nv[SL][0], nv[SL][1], lo, hi, nxt);
       pin_pair(nxt);
-      if (STEADY || k + 1 + kStages < npairs) {
-        const int page0 = p0 + 2 * (k + 1 + kStages);
-        // The ids read one step ago are pinned (their wait placed) before the next loads issue:
-        // scalar loads return out of order, so a wait placed after those would wait for them
-        // too. The new loads sit between the empty asm and the DMA (both memory barriers), so
-        // they issue before the DMA and have the step to return.
-        asm volatile("" : "+s"(nid.b0), "+s"(nid.b1));
-        const BlockIds next = load_ids(bt, page0 + 2, p1);
-        okmask = (okmask & ~(3u << (2 * sl))) |
-                 (stage_pair(a.pool, base_h, stride, nblk, nid, page0, p1, stage_base + sl * 2 * kRecord, l)
-                  << (2 * sl));
-        nid = next;
+      if (STEADY) {
+        // The entries read one step ago are pinned (their wait placed) before the next loads issue:
+        // scalar loads return out of order, so a wait placed after those would wait for them too.
+        // The new loads sit between the empty asm and the DMA (both memory barriers), so they
+        // issue before the DMA and have the step to return.
+        pin_ent(n0, n1);
+        const PageEnt m0 = load_ent(ent, 2 * (kk + 2 + kStages)), m1 = load_ent(ent, 2 * (kk + 2 + kStages) + 1);
+        stage(std::integral_constant<int, SL>{}, n0, n1);
+        n0 = m0;
+        n1 = m1;
+      } else if (kk + 1 + kStages < npairs) {
+        PageEnt e0, e1;
+        entries(kk + 1 + kStages, e0, e1);
+        stage(std::integral_constant<int, SL>{}, e0, e1);
       }
     }
     float a2[2][NJ];
-    if (more) qk_pair<WIDE>(st, nxt, p0 + 2 * (k + 1), L, lo, a2);
+    if (more) qk_pair<WIDE>(st, nxt, a2);
     lds_sync_wave();
-    pv_pair<WIDE>(st, cur, lo, hi, p_w[k & 1]);
-    if (more) softmax_pair<WIDE>(st, a2, lo, hi, p_w[(k + 1) & 1], al_w);
+    pv_pair<WIDE>(st, cur, lo, hi, p_w[kk & 1]);
+    if (more) softmax_pair<WIDE>(st, a2, lo, hi, p_w[(kk + 1) & 1], al_w);
   };
+  using T = std::true_type;
+  using F = std::false_type;
   int k = 0;
-  for (; k + 2 + kStages < npairs; k += 2) {
-    step(std::true_type{}, X, Y, k);
-    step(std::true_type{}, Y, X, k + 1);
+  // steady groups of six steps (kStages = 3 slots, two register sets X / Y)
+  for (; k + 6 + kStages < nfull; k += 6) {
+    step(std::integral_constant<int, 0>{}, T{}, X, Y, k);
+    step(std::integral_constant<int, 1>{}, T{}, Y, X, k);
+    step(std::integral_constant<int, 2>{}, T{}, X, Y, k);
+    step(std::integral_constant<int, 3>{}, T{}, Y, X, k);
+    step(std::integral_constant<int, 4>{}, T{}, X, Y, k);
+    step(std::integral_constant<int, 5>{}, T{}, Y, X, k);
   }
-  for (; k < npairs; ++k) {
-    step(std::false_type{}, X, Y, k);
-    X = Y;
+  for (; k < npairs; k += 6) {
+    step(std::integral_constant<int, 0>{}, F{}, X, Y, k);
+    if (k + 1 >= npairs) break;
+    step(std::integral_constant<int, 1>{}, F{}, Y, X, k);
+    if (k + 2 >= npairs) break;
+    step(std::integral_constant<int, 2>{}, F{}, X, Y, k);
+    if (k + 3 >= npairs) break;
+    step(std::integral_constant<int, 3>{}, F{}, Y, X, k);
+    if (k + 4 >= npairs) break;
+    step(std::integral_constant<int, 4>{}, F{}, X, Y, k);
+    if (k + 5 >= npairs) break;
+    step(std::integral_constant<int, 5>{}, F{}, Y, X, k);
   }
 
   // ---- partial (m, l, O') of every query head of this KV head
@@ -778,7 +862,7 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   for (int pos = s;;) {
     const int seg_end = min(e, Sb1);
     const int Sb2 = seg_end < e ? prefix[b + 2] : 0;  // next sequence's end, fetched ahead
-    scan_segment<WIDE>(a, b, h, pos - Sb, seg_end - Sb, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w]);
+    scan_segment<WIDE>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w]);
     pos = seg_end;
     if (pos >= e) break;
     ++b;
