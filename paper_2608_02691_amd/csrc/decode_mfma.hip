@@ -109,34 +109,6 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, bool wide) {
   const int h = blk % H, b0 = kQpSeqs * (blk / H), nseq = min(kQpSeqs, a.B - b0);
   const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
   if (tid < 8 * kQpSeqs) smax[tid] = 0;
-  // Page list entries of this block's sequences, for the pages i with i % H == h: the block first
-  // sums the pages of the sequences before b0 (the same prefix the page-prefix block computes).
-  {
-    __shared__ int red[256];
-    int s = 0;
-    for (int bb = tid; bb < b0; bb += 256) s += (seq_len_m(a, bb) + kBlock - 1) >> 4;
-    red[tid] = s;
-    __syncthreads();
-    for (int off = 128; off > 0; off >>= 1) {
-      if (tid < off) red[tid] += red[tid + off];
-      __syncthreads();
-    }
-    size_t base = (size_t)red[0];
-    const uint64_t pool = (uint64_t)(uintptr_t)a.pool;
-    const uint64_t stride = (uint64_t)H * kRecord;
-    for (int sq = 0; sq < nseq; ++sq) {
-      const int b = b0 + sq, L = seq_len_m(a, b), np = (L + kBlock - 1) >> 4;
-      const int32_t* row = a.block_table + (size_t)b * a.max_blocks;
-      for (int i = h + H * tid; i < np; i += H * 256) {
-        const int id = row[i];
-        const bool ok = (uint32_t)id < (uint32_t)a.num_blocks;
-        const uint64_t rec = pool + (ok ? (uint64_t)(uint32_t)id * stride : 0ull);
-        *reinterpret_cast<uint4*>(a.pages + 4 * (base + i)) =
-            make_uint4((uint32_t)rec, (uint32_t)(rec >> 32), ok ? (uint32_t)min(kBlock, L - kBlock * i) : 0u, 0u);
-      }
-      base += np;
-    }
-  }
   // A operand (query rows 16 w + lo, 8 consecutive channels per lane), fetched before R so the
   // two latencies overlap; absent rows are zero
   qp_bf16x8_t A[4];
@@ -552,7 +524,20 @@ __device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WID
   __builtin_amdgcn_s_setprio(0);
 }
 
-constexpr int kStages = 3;       // page pairs staged (in flight) per wave
+#ifndef INT2KV_SCAN_STAGES
+#define INT2KV_SCAN_STAGES 3
+#endif
+constexpr int kStages = INT2KV_SCAN_STAGES;  // page pairs staged (in flight) per wave
+constexpr int kUnroll = kStages % 2 ? 2 * kStages : kStages;  // steps per unrolled group: slots and X / Y repeat
+
+// f(integral_constant<0>), ..., f(integral_constant<N - 1>) in order
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (N > 0) {
+    static_for<N - 1>(f);
+    f(std::integral_constant<int, N - 1>{});
+  }
+}
 constexpr int kWavesPerWG = 8;   // one wave per KV head of a head group
 
 typedef __attribute__((address_space(4))) const int32_t* cint_ptr;  // read through the scalar cache
@@ -595,13 +580,58 @@ __device__ void page_prefix_block(const DecodeArgs& a) {
   if (tid == 255) a.prefix[a.B] = P;
 }
 
-// Block 0: page prefix sums (first, so it never waits for a free slot); blocks 1 ..: query
-// operands of KV head h for kQpSeqs sequences.
-__global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int wide) {
-  if (blockIdx.x == 0)
+// Page list entries of pages [p0, p0 + kPlPages) of sequence b (four per thread, every block-table
+// load issued before the first store). The list position of page 0 of b, the pages of the
+// sequences before b, is summed by the block itself (the same prefix the page-prefix block
+// computes). Entry: address of the record of KV head 0, cached tokens of the page (0, with the
+// address of block 0, for a block id outside the pool).
+constexpr int kPlPages = 1024;
+
+__device__ void page_list_block(const DecodeArgs& a, int b, int p0) {
+  __shared__ int red[256];
+  const int tid = threadIdx.x;
+  const int L = seq_len_m(a, b), np = (L + kBlock - 1) >> 4;
+  if (p0 >= np) return;  // uniform over the block
+  int s = 0;
+  for (int bb = tid; bb < b; bb += 256) s += (seq_len_m(a, bb) + kBlock - 1) >> 4;
+  red[tid] = s;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if (tid < off) red[tid] += red[tid + off];
+    __syncthreads();
+  }
+  const size_t base = (size_t)red[0] + p0;
+  const int32_t* row = a.block_table + (size_t)b * a.max_blocks + p0;
+  const int n = min(kPlPages, np - p0);
+  int id[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) id[u] = 4 * tid + u < n ? row[4 * tid + u] : 0;
+  const uint64_t pool = (uint64_t)(uintptr_t)a.pool;
+  const uint64_t stride = (uint64_t)a.H * kRecord;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = 4 * tid + u;
+    if (i < n) {
+      const bool ok = (uint32_t)id[u] < (uint32_t)a.num_blocks;
+      const uint64_t rec = pool + (ok ? (uint64_t)(uint32_t)id[u] * stride : 0ull);
+      const int t = kBlock * (p0 + i);
+      *reinterpret_cast<uint4*>(a.pages + 4 * (base + i)) =
+          make_uint4((uint32_t)rec, (uint32_t)(rec >> 32), ok ? (uint32_t)min(kBlock, L - t) : 0u, 0u);
+    }
+  }
+}
+
+// Block 0: page prefix sums (first, so it never waits for a free slot); blocks 1 .. nq: query
+// operands of KV head h for kQpSeqs sequences; the rest: the page list, kPlPages pages of one
+// sequence per block (nseg blocks per sequence).
+__global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int wide, int nq, int nseg) {
+  const int blk = blockIdx.x;
+  if (blk == 0)
     page_prefix_block(a);
+  else if (blk <= nq)
+    qprep_block(a, blk - 1, wide != 0);
   else
-    qprep_block(a, blockIdx.x - 1, wide != 0);
+    page_list_block(a, (blk - 1 - nq) / nseg, ((blk - 1 - nq) % nseg) * kPlPages);
 }
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -679,20 +709,14 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   auto pin_ent = [](PageEnt& e0, PageEnt& e1) {
     asm volatile("" : "+s"(e0.lo), "+s"(e0.hi), "+s"(e0.nv), "+s"(e1.lo), "+s"(e1.hi), "+s"(e1.nv));
   };
-  {
-    PageEnt e0, e1;
-    entries(0, e0, e1);
-    stage(std::integral_constant<int, 0>{}, e0, e1);
-    if (1 < npairs) {
-      entries(1, e0, e1);
-      stage(std::integral_constant<int, 1>{}, e0, e1);
+  static_for<kStages>([&](auto I) {
+    constexpr int k = decltype(I)::value;
+    if (k == 0 || k < npairs) {
+      PageEnt e0, e1;
+      entries(k, e0, e1);
+      stage(I, e0, e1);
     }
-    if (2 < npairs) {
-      entries(2, e0, e1);
-      stage(std::integral_constant<int, 2>{}, e0, e1);
-    }
-  }
-  static_assert(kStages == 3, "the prologue stages three pairs");
+  });
   // entries of the next pair the steady loop stages, read one step ahead of their use so that the
   // scalar loads overlap the step's arithmetic (only full pairs inside the segment are read)
   PageEnt n0{0u, 0u, 0u, 0u}, n1 = n0;
@@ -717,7 +741,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
     qk_pair<WIDE>(st, X, a2);
     softmax_pair<WIDE>(st, a2, lo, hi, p_w[0], al_w);
   }
-  // Step J of an unrolled group that starts at pair k (k % kStages = 0): read pair kk + 1 =
+  // Step J of an unrolled group that starts at pair k (k % kUnroll = 0): read pair kk + 1 =
   // k + J + 1 (staged kStages pairs ago, slot SL), refill its slot with pair kk + 1 + kStages,
   // scores of pair kk + 1 beside the value accumulation of pair kk, then the softmax of pair
   // kk + 1. STEADY: pair kk + 1 + kStages is a full pair inside the segment.
@@ -759,27 +783,29 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   using T = std::true_type;
   using F = std::false_type;
   int k = 0;
-  // steady groups of six steps (kStages = 3 slots, two register sets X / Y)
-  for (; k + 6 + kStages < nfull; k += 6) {
-    step(std::integral_constant<int, 0>{}, T{}, X, Y, k);
-    step(std::integral_constant<int, 1>{}, T{}, Y, X, k);
-    step(std::integral_constant<int, 2>{}, T{}, X, Y, k);
-    step(std::integral_constant<int, 3>{}, T{}, Y, X, k);
-    step(std::integral_constant<int, 4>{}, T{}, X, Y, k);
-    step(std::integral_constant<int, 5>{}, T{}, Y, X, k);
+  // steady groups of kUnroll steps (the slot and the X / Y register set repeat with that period)
+  for (; k + kUnroll + kStages < nfull; k += kUnroll) {
+    static_for<kUnroll>([&](auto J) {
+      if constexpr (decltype(J)::value % 2 == 0)
+        step(J, T{}, X, Y, k);
+      else
+        step(J, T{}, Y, X, k);
+    });
   }
-  for (; k < npairs; k += 6) {
-    step(std::integral_constant<int, 0>{}, F{}, X, Y, k);
-    if (k + 1 >= npairs) break;
-    step(std::integral_constant<int, 1>{}, F{}, Y, X, k);
-    if (k + 2 >= npairs) break;
-    step(std::integral_constant<int, 2>{}, F{}, X, Y, k);
-    if (k + 3 >= npairs) break;
-    step(std::integral_constant<int, 3>{}, F{}, Y, X, k);
-    if (k + 4 >= npairs) break;
-    step(std::integral_constant<int, 4>{}, F{}, X, Y, k);
-    if (k + 5 >= npairs) break;
-    step(std::integral_constant<int, 5>{}, F{}, Y, X, k);
+  for (; k < npairs; k += kUnroll) {
+    bool go = true;
+    static_for<kUnroll>([&](auto J) {
+      constexpr int j = decltype(J)::value;
+      if (go && (j == 0 || k + j < npairs)) {
+        if constexpr (j % 2 == 0)
+          step(J, F{}, X, Y, k);
+        else
+          step(J, F{}, Y, X, k);
+      } else {
+        go = false;
+      }
+    });
+    if (!go) break;
   }
 
   // ---- partial (m, l, O') of every query head of this KV head
@@ -960,8 +986,11 @@ __global__ __launch_bounds__(128) void merge_flat_kernel(DecodeArgs a, int G, in
 
 hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
   if (a.gq > 8) return hipErrorNotSupported;
-  hipLaunchKernelGGL(qprep_kernel, dim3(1 + a.H * ((a.B + kQpSeqs - 1) / kQpSeqs)), dim3(256), 0, s, a,
-                     a.gq > 4 ? 1 : 0);
+  const int nq = a.H * ((a.B + kQpSeqs - 1) / kQpSeqs);
+  const long long maxlen = min((long long)a.max_ctx, (long long)a.max_blocks * kBlock);
+  const int maxp = (int)((maxlen + kBlock - 1) / kBlock);
+  const int nseg = max(1, (maxp + kPlPages - 1) / kPlPages);
+  hipLaunchKernelGGL(qprep_kernel, dim3(1 + nq + a.B * nseg), dim3(256), 0, s, a, a.gq > 4 ? 1 : 0, nq, nseg);
   return hipGetLastError();
 }
 
