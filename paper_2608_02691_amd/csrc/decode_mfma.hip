@@ -262,7 +262,7 @@ struct PairLoads {
   uint2 vc[2];  // V codes of half lo, tokens 4hi..4hi+3
   uint2 vs[2][WIDE ? 2 : 1];  // V scales, tokens 4hi..4hi+3: group lo&3 (narrow); lo&1, 2+(lo&1) (wide)
   uint2 vz[2];  // V zeros of group lo&3, tokens 4hi..4hi+3
-  float mk[2];  // 0 if this lane's token of the page is cached, else -inf
+  uint32_t nv[2];  // wave-uniform: cached tokens of each page (16 for a full page)
 };
 
 // Page records are staged in LDS by the wave that consumes them, with LDS-DMA loads
@@ -332,7 +332,7 @@ __device__ __forceinline__ void read_pair(const uint8_t* slot, uint32_t nv0, uin
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
     const uint8_t* rec = slot + P * kRecord;
-    p.mk[P] = (uint32_t)lo < (P == 0 ? nv0 : nv1) ? 0.0f : -INFINITY;
+    p.nv[P] = P == 0 ? nv0 : nv1;
     p.kc[P] = *reinterpret_cast<const uint2*>(rec + kOffKCodes + 32 * lo + 8 * hi);
     p.km[P] = *reinterpret_cast<const uint4*>(rec + kOffKMeta + 16 * lo);
     p.vc[P] = *reinterpret_cast<const uint2*>(rec + kOffVCodes + 32 * lo + 8 * hi);
@@ -370,7 +370,8 @@ struct ScanState {
   static constexpr int NT = WIDE ? 2 : 1;   // score tiles (narrow D; wide D01, D23)
   half8_t A[4];                 // query operand of k block i
   float4_t cinit[NT];           // accumulator start of the score tiles (rows 4hi..4hi+3)
-  float sq[NJ][4];              // sum_{k in g} q'_jk
+  half8_t Azq;                  // zero-term operand: row (j, 0) holds sum_{k in g} q'_jk, g = 0..3, as
+                                // two fp16 terms (k = 0..3 high, 4..7 low); every other entry zero
   float invsig[NJ];
   float4_t acc[8];              // O' tiles: channels 16 mt + 4hi + r, column lo
   float4_t wsum[NT];            // sum_t w_t of each column (every row); wide: groups gg, 2 + gg
@@ -383,7 +384,7 @@ struct ScanState {
 // query head jq(hi, u). The accumulation chains of both pages are issued interleaved so that each
 // hides the others' latency.
 template <bool WIDE>
-__device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoads<WIDE>& cur,
+__device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoads<WIDE>& cur, int lo,
                                         float (&a2)[2][ScanState<WIDE>::NJ]) {
   constexpr int NT = ScanState<WIDE>::NT, NJ = ScanState<WIDE>::NJ;
   half8_t B[2][4];
@@ -413,25 +414,40 @@ __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoa
 #pragma unroll
       for (int P = 0; P < 2; ++P) d[P][0] = mfma16(st.A[i], B[P][i], d[P][0]);
   }
+  // Zero term on the matrix cores: rows (j, 0) of zd = sum_g Q_jg z_tg, with z_tg exact in fp16 (the
+  // B operand: z_t0..z_t3 of token t twice, for the high and the low term of Q)
+  float4_t zd[2];
+#pragma unroll
+  for (int P = 0; P < 2; ++P) {
+    const uint32_t z01 = __builtin_amdgcn_perm(cur.km[P].y, cur.km[P].x, 0x07060302u);
+    const uint32_t z23 = __builtin_amdgcn_perm(cur.km[P].w, cur.km[P].z, 0x07060302u);
+    zd[P] = mfma16(st.Azq, __builtin_bit_cast(half8_t, u32x4_t{z01, z23, z01, z23}),
+                   float4_t{0.f, 0.f, 0.f, 0.f});
+  }
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
     const half2_t m[4] = {as_h2(cur.km[P].x), as_h2(cur.km[P].y), as_h2(cur.km[P].z), as_h2(cur.km[P].w)};
 #pragma unroll
     for (int u = 0; u < NJ; ++u) {
       // D of group g for query head jq(hi, u): narrow register g of D; wide register 2u + g % 2
-      // of tile g / 2
+      // of tile g / 2; its zero term sits in register 2u (wide) or 0 (narrow) of zd
       float Dg[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) Dg[g] = WIDE ? d[P][g >> 1][2 * u + (g & 1)] : d[P][0][g];
-      float sd = (float)m[0].x * Dg[0];
+      float sd = fmaf((float)m[0].x, Dg[0], 0.0f);
       sd = fmaf((float)m[1].x, Dg[1], sd);
       sd = fmaf((float)m[2].x, Dg[2], sd);
       sd = fmaf((float)m[3].x, Dg[3], sd);
-      float zq = (float)m[0].y * st.sq[u][0];
-      zq = fmaf((float)m[1].y, st.sq[u][1], zq);
-      zq = fmaf((float)m[2].y, st.sq[u][2], zq);
-      zq = fmaf((float)m[3].y, st.sq[u][3], zq);
-      a2[P][u] = fmaf(sd, st.invsig[u], zq) + cur.mk[P];
+      a2[P][u] = fmaf(sd, st.invsig[u], zd[P][WIDE ? 2 * u : 0]);
+    }
+  }
+  // tokens a page does not hold get -inf (a wave-uniform branch, taken only for partial pages)
+  if (cur.nv[0] < (uint32_t)kBlock || cur.nv[1] < (uint32_t)kBlock) {
+#pragma unroll
+    for (int P = 0; P < 2; ++P) {
+      const float mk = (uint32_t)lo < cur.nv[P] ? 0.0f : -INFINITY;
+#pragma unroll
+      for (int u = 0; u < NJ; ++u) a2[P][u] += mk;
     }
   }
 }
@@ -659,18 +675,24 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
     st.cinit[0] = *reinterpret_cast<const float4_t*>(cst + 4 * hi);       // D01 rows 4hi..4hi+3
     st.cinit[1] = *reinterpret_cast<const float4_t*>(cst + 16 + 4 * hi);  // D23 rows 4hi..4hi+3
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const float4_t v = *reinterpret_cast<const float4_t*>(cst + 32 + 8 * hi + 4 * u);
-#pragma unroll
-      for (int g = 0; g < 4; ++g) st.sq[u][g] = v[g];
-      st.invsig[u] = cst[64 + 2 * hi + u];
-    }
+    for (int u = 0; u < 2; ++u) st.invsig[u] = cst[64 + 2 * hi + u];
   } else {
     st.cinit[0] = *reinterpret_cast<const float4_t*>(cst + 4 * hi);
-    const float4_t v = *reinterpret_cast<const float4_t*>(cst + 16 + 4 * hi);
-#pragma unroll
-    for (int g = 0; g < 4; ++g) st.sq[0][g] = v[g];
     st.invsig[0] = cst[32 + hi];
+  }
+  {
+    // zero-term operand: lane l < 16 holds row m = l; the rows (j, 0) carry the group sums of q'_j
+    const int m = l & 15, j = WIDE ? m >> 1 : m >> 2;
+    const bool zrow = l < 16 && (WIDE ? (m & 1) == 0 : (m & 3) == 0);
+    const float4_t Q = *reinterpret_cast<const float4_t*>(cst + (WIDE ? 32 : 16) + 4 * j);
+    half8_t z;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const _Float16 qh = (_Float16)Q[g];
+      z[g] = zrow ? qh : (_Float16)0.0f;
+      z[4 + g] = zrow ? (_Float16)(Q[g] - (float)qh) : (_Float16)0.0f;
+    }
+    st.Azq = z;
   }
 #pragma unroll
   for (int mt = 0; mt < 8; ++mt) st.acc[mt] = float4_t{0.f, 0.f, 0.f, 0.f};
@@ -738,7 +760,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
       stage(std::integral_constant<int, 0>{}, e0, e1);
     }
     float a2[2][NJ];
-    qk_pair<WIDE>(st, X, a2);
+    qk_pair<WIDE>(st, X, lo, a2);
     softmax_pair<WIDE>(st, a2, lo, hi, p_w[0], al_w);
   }
   // Step J of an unrolled group that starts at pair k (k % kUnroll = 0): read pair kk + 1 =
@@ -775,7 +797,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
       }
     }
     float a2[2][NJ];
-    if (more) qk_pair<WIDE>(st, nxt, a2);
+    if (more) qk_pair<WIDE>(st, nxt, lo, a2);
     lds_sync_wave();
     pv_pair<WIDE>(st, cur, lo, hi, p_w[kk & 1]);
     if (more) softmax_pair<WIDE>(st, a2, lo, hi, p_w[(kk + 1) & 1], al_w);
@@ -875,7 +897,12 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   __shared__ _Float16 p_lds[kWavesPerWG][2][2][8][kBlock];
   __shared__ float al_lds[kWavesPerWG][8];
 
-  const int g = blockIdx.x, G = gridDim.x;
+  // Work-groups are dispatched round-robin over the 8 XCDs (each with its own L2). Range g goes to
+  // the work-group dispatched as blockIdx.x with g = (x % 8) (G / 8) + x / 8, so that each XCD scans
+  // one contiguous eighth of the pages: the few work-groups sharing a sequence then share that
+  // sequence's query operands and page-list entries through one L2.
+  const int G = gridDim.x;
+  const int g = G % 8 == 0 ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
   const int h = blockIdx.y * kWavesPerWG + w;
   if (h >= a.H) return;
