@@ -105,7 +105,9 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   p.off_prefix = off;
   off = up(off + (size_t)(B + 1) * sizeof(int32_t));
   p.off_wginfo = off;
-  off = up(off + (size_t)p.grid_g * 4 * sizeof(int32_t));
+  off = up(off + (size_t)(p.grid_g + 1) * 4 * sizeof(int32_t));
+  p.off_seqwg = off;
+  off = up(off + (size_t)B * 2 * sizeof(int32_t));
   // page list: one 16-byte entry per page of every sequence (lengths are clamped to max_ctx), plus
   // padding the scan may read (never use) one pair past the last page
   p.off_pages = off;
@@ -250,6 +252,7 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
   a.n_chunks = plan.n_chunks;
   a.prefix = reinterpret_cast<int32_t*>(ws + plan.off_prefix);
   a.wg_info = reinterpret_cast<int32_t*>(ws + plan.off_wginfo);
+  a.seq_wg = reinterpret_cast<int32_t*>(ws + plan.off_seqwg);
   a.pages = reinterpret_cast<uint32_t*>(ws + plan.off_pages);
   a.grid_g = plan.grid_g;
 

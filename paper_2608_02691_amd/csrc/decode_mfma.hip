@@ -563,7 +563,9 @@ __host__ __device__ __forceinline__ int range_lo(int g, int P, int G) { return (
 
 // Pages of every sequence and their exclusive prefix sums (prefix[B] = total pages), and for each
 // scan work-group g the sequence b holding the first page of its range with that sequence's page
-// range: wg_info[g] = {b, prefix[b], prefix[b + 1], 0}. Group g starts inside sequence b exactly
+// range: wg_info[g] = {b, prefix[b], prefix[b + 1], lo(g)}, wg_info[G].w = P, and for every sequence
+// the first and last group whose range meets it (seq_wg[b] = {ga, gb}, {0, -1} when empty), so that
+// no later wave divides. Group g starts inside sequence b exactly
 // when prefix[b] <= lo(g) < prefix[b + 1], i.e. for g in [ceil(prefix[b] G / P), ...) while lo(g)
 // stays below prefix[b + 1], so every group is written once (by the thread owning b). One block
 // of 256 threads.
@@ -587,13 +589,26 @@ __device__ void page_prefix_block(const DecodeArgs& a) {
   for (int b = b0; b < b1; ++b) {
     const int n = (seq_len_m(a, b) + kBlock - 1) >> 4;
     a.prefix[b] = run;
+    int ga = 0, gb = -1;  // groups whose ranges contain the sequence's first and last page
     if (n > 0) {
       for (int g = (int)(((long long)run * G + P - 1) / P); g < G && range_lo(g, P, G) < run + n; ++g)
-        *reinterpret_cast<int4*>(a.wg_info + 4 * g) = make_int4(b, run, run + n, 0);
+        *reinterpret_cast<int4*>(a.wg_info + 4 * g) = make_int4(b, run, run + n, range_lo(g, P, G));
+      const int last = run + n - 1;
+      ga = (int)(((long long)run * G) / P);
+      while (ga > 0 && range_lo(ga, P, G) > run) --ga;
+      while (range_lo(ga + 1, P, G) <= run) ++ga;
+      gb = (int)(((long long)last * G) / P);
+      while (gb > 0 && range_lo(gb, P, G) > last) --gb;
+      while (range_lo(gb + 1, P, G) <= last) ++gb;
     }
+    a.seq_wg[2 * b] = ga;
+    a.seq_wg[2 * b + 1] = gb;
     run += n;
   }
-  if (tid == 255) a.prefix[a.B] = P;
+  if (tid == 255) {
+    a.prefix[a.B] = P;
+    a.wg_info[4 * G + 3] = P;  // range start of the group after the last
+  }
 }
 
 // Page list entries of pages [p0, p0 + kPlPages) of sequence b (four per thread, every block-table
@@ -908,9 +923,10 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   if (h >= a.H) return;
   const cint_ptr prefix = (cint_ptr)(uintptr_t)(a.prefix);
   const int P = prefix[a.B];
-  const int s = range_lo(g, P, G), e = range_lo(g + 1, P, G);
-  if (s >= e) return;
+  if (P == 0) return;
   const cint_ptr info = (cint_ptr)(uintptr_t)(a.wg_info + 4 * g);
+  const int s = info[3], e = info[7];  // lo(g), lo(g + 1)
+  if (s >= e) return;
   int b = info[0], Sb = info[1], Sb1 = info[2];  // prefix[b] <= s < prefix[b + 1]
   for (int pos = s;;) {
     const int seg_end = min(e, Sb1);
@@ -927,35 +943,31 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
 
 // Merge the partials of each (sequence, query head) over the work-groups whose ranges met the
 // sequence, then undo the value rotation (o = o' R_V^T, unless W_O arrives pre-folded).
-// Block (sequence, KV head), thread c = channel; the G_q query heads of the block share one pass
-// over R_V (row c of R_V per thread).
-__global__ __launch_bounds__(128) void merge_flat_kernel(DecodeArgs a, int G, int unrotate, float* __restrict__ out,
-                                                         uint16_t* __restrict__ ob) {
-  __shared__ float os[8][kHeadDim];
-  const int b = blockIdx.x, h = blockIdx.y, c = threadIdx.x, gq = a.gq;
-  const int P = a.prefix[a.B];
-  const int Sb = a.prefix[b], Sb1 = a.prefix[b + 1];
-  int ga = 0, gb = -1;
-  if (Sb1 > Sb && P > 0) {
-    // groups whose ranges contain the first and the last page of the sequence
-    ga = (int)(((long long)Sb * G) / P);
-    while (ga > 0 && range_lo(ga, P, G) > Sb) --ga;
-    while (range_lo(ga + 1, P, G) <= Sb) ++ga;
-    gb = (int)(((long long)(Sb1 - 1) * G) / P);
-    while (gb > 0 && range_lo(gb, P, G) > Sb1 - 1) --gb;
-    while (range_lo(gb + 1, P, G) <= Sb1 - 1) ++gb;
-  }
-  // one pass over the groups with a running max, all query heads of the block together (their
-  // loads are independent, so each group costs one round trip)
-  float M[8], lsum[8], osum[8], val[8];
+// Block (sequence, KV head) of kMergeSlots x 128 threads: slot s merges the work-groups ga + s,
+// ga + s + kMergeSlots, ... (one round of loads for up to kMergeSlots work-groups), thread c of a
+// slot owns channel c; the slots are then combined in a fixed order through LDS (deterministic),
+// thread (c, s) finishing query head s. The un-rotation has the 128 threads of slot 0 share one
+// pass over R_V (row c of R_V per thread) for all query heads.
+constexpr int kMergeSlots = 8;
+
+__global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArgs a, int G, int unrotate,
+                                                                       float* __restrict__ out,
+                                                                       uint16_t* __restrict__ ob) {
+  __shared__ float ms[kMergeSlots][8], ls[kMergeSlots][8];
+  __shared__ float os[kMergeSlots][8][kHeadDim];
+  __shared__ float vs[8][kHeadDim];
+  const int b = blockIdx.x, h = blockIdx.y, c = threadIdx.x & 127, sl = threadIdx.x >> 7, gq = a.gq;
+  // groups whose ranges meet the sequence, from the page-prefix block
+  const int ga = a.seq_wg[2 * b], gb = a.seq_wg[2 * b + 1];
+  float M[8], lsum[8], osum[8];
 #pragma unroll
   for (int jj = 0; jj < 8; ++jj) {
     M[jj] = -INFINITY;
     lsum[jj] = 0.0f;
     osum[jj] = 0.0f;
   }
-  for (int gg = ga; gg <= gb; ++gg) {
-    if (range_lo(gg, P, G) >= range_lo(gg + 1, P, G)) continue;  // empty range wrote nothing
+  for (int gg = ga + sl; gg <= gb; gg += kMergeSlots) {
+    if (a.wg_info[4 * gg + 3] >= a.wg_info[4 * gg + 7]) continue;  // empty range wrote nothing
     const float* base = a.part + ((size_t)(gg + b) * a.Hq + h * gq) * kPartStride;
     float mv[8], lv[8], ov[8];
 #pragma unroll
@@ -977,38 +989,61 @@ __global__ __launch_bounds__(128) void merge_flat_kernel(DecodeArgs a, int G, in
       M[jj] = Mn;
     }
   }
+  if (c == 0) {
 #pragma unroll
-  for (int jj = 0; jj < 8; ++jj) val[jj] = lsum[jj] > 0.0f ? osum[jj] / lsum[jj] : 0.0f;
-  if (unrotate) {
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj)
-      if (jj < gq) os[jj][c] = val[jj];
-    __syncthreads();
-    const float4* row = reinterpret_cast<const float4*>(a.R_v + ((size_t)h * kHeadDim + c) * kHeadDim);
-    float acc[8];
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj) acc[jj] = 0.0f;
-#pragma unroll 4
-    for (int i = 0; i < kHeadDim / 4; ++i) {
-      const float4 rr = row[i];
-#pragma unroll
-      for (int jj = 0; jj < 8; ++jj) {
-        if (jj < gq) {
-          acc[jj] = fmaf(os[jj][4 * i], rr.x, acc[jj]);
-          acc[jj] = fmaf(os[jj][4 * i + 1], rr.y, acc[jj]);
-          acc[jj] = fmaf(os[jj][4 * i + 2], rr.z, acc[jj]);
-          acc[jj] = fmaf(os[jj][4 * i + 3], rr.w, acc[jj]);
-        }
-      }
+    for (int jj = 0; jj < 8; ++jj) {
+      ms[sl][jj] = M[jj];
+      ls[sl][jj] = lsum[jj];
     }
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj) val[jj] = acc[jj];
   }
 #pragma unroll
-  for (int jj = 0; jj < 8; ++jj)
-    if (jj < gq)
-      store_head_out(val[jj], out, ob, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c,
-                     (size_t)a.B * a.Hq * kHeadDim);
+  for (int jj = 0; jj < 8; ++jj) os[sl][jj][c] = osum[jj];
+  __syncthreads();
+  // thread (c, s): query head s, channel c, the slots in a fixed order
+  const int jj = sl;
+  float Mx = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < kMergeSlots; ++t) Mx = fmaxf(Mx, ms[t][jj]);
+  float L = 0.0f, O = 0.0f;
+#pragma unroll
+  for (int t = 0; t < kMergeSlots; ++t) {
+    const float mt = ms[t][jj];
+    const float f = mt == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mt - Mx);
+    L = fmaf(f, ls[t][jj], L);
+    O = fmaf(f, os[t][jj][c], O);
+  }
+  float val = L > 0.0f ? O / L : 0.0f;
+  if (unrotate) {
+    vs[jj][c] = val;
+    __syncthreads();
+    if (sl == 0) {
+      const float4* row = reinterpret_cast<const float4*>(a.R_v + ((size_t)h * kHeadDim + c) * kHeadDim);
+      float acc[8];
+#pragma unroll
+      for (int j2 = 0; j2 < 8; ++j2) acc[j2] = 0.0f;
+#pragma unroll 4
+      for (int i = 0; i < kHeadDim / 4; ++i) {
+        const float4 rr = row[i];
+#pragma unroll
+        for (int j2 = 0; j2 < 8; ++j2) {
+          if (j2 < gq) {
+            acc[j2] = fmaf(vs[j2][4 * i], rr.x, acc[j2]);
+            acc[j2] = fmaf(vs[j2][4 * i + 1], rr.y, acc[j2]);
+            acc[j2] = fmaf(vs[j2][4 * i + 2], rr.z, acc[j2]);
+            acc[j2] = fmaf(vs[j2][4 * i + 3], rr.w, acc[j2]);
+          }
+        }
+      }
+#pragma unroll
+      for (int j2 = 0; j2 < 8; ++j2)
+        if (j2 < gq)
+          store_head_out(acc[j2], out, ob, ((size_t)b * a.Hq + h * gq + j2) * kHeadDim + c,
+                         (size_t)a.B * a.Hq * kHeadDim);
+    }
+    return;
+  }
+  if (jj < gq)
+    store_head_out(val, out, ob, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c, (size_t)a.B * a.Hq * kHeadDim);
 }
 
 hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
@@ -1034,7 +1069,8 @@ hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s, hipEvent
 
 hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, hipStream_t s) {
   if (a.gq > 8) return hipErrorNotSupported;
-  hipLaunchKernelGGL(merge_flat_kernel, dim3(a.B, a.H), dim3(128), 0, s, a, a.grid_g, unrotate ? 1 : 0, out, ob);
+  hipLaunchKernelGGL(merge_flat_kernel, dim3(a.B, a.H), dim3(128 * kMergeSlots), 0, s, a, a.grid_g, unrotate ? 1 : 0,
+                     out, ob);
   return hipGetLastError();
 }
 

@@ -31,7 +31,7 @@ struct DecodePlan {
   int variant;        // 1 = vector ALU, 2 = matrix core
   int wo_ksplit;
   int grid_g;         // work-groups of the matrix-core scan
-  size_t off_qrot, off_qop, off_prefix, off_wginfo, off_pages, off_part, off_o, off_wo, total;
+  size_t off_qrot, off_qop, off_prefix, off_wginfo, off_seqwg, off_pages, off_part, off_o, off_wo, total;
 };
 
 struct DecodeArgs {
@@ -50,7 +50,8 @@ struct DecodeArgs {
   float* part;     // vector-ALU scan: [B, n_chunks, Hq, kPartStride]; matrix-core scan: [G + B, Hq, kPartStride]
   int chunk_tokens, n_chunks;
   int32_t* prefix; // [B + 1] page prefix sums (matrix-core scan)
-  int32_t* wg_info;  // [grid_g][4]: first sequence of each scan work-group and its page range
+  int32_t* wg_info;  // [grid_g + 1][4]: first sequence of each scan work-group, its page range, lo(g)
+  int32_t* seq_wg;   // [B][2]: first and last scan work-group whose range meets each sequence
   uint32_t* pages;   // page list of the matrix-core scan: [total pages + padding][4]
   int grid_g;      // work-groups of the matrix-core scan
 };
