@@ -130,8 +130,9 @@ def main():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--chunk", type=int, default=0, help="context chunk in tokens (0 = automatic)")
     ap.add_argument("--variant", type=int, default=0, help="decode scan variant (0 auto, 1 VALU, 2 MFMA)")
-    ap.add_argument("--unfolded-wo", action="store_true",
-                    help="apply R_V^T in the merge and the plain W_O (default: W_O R_V folded once at set-up)")
+    ap.add_argument("--wo", choices=("prepared", "folded", "plain"), default="prepared",
+                    help="output-projection weights: prepared fp16 tiles with R_V folded in (default), row-major "
+                         "bf16 folded with R_V, or row-major bf16 W_O with the merge un-rotating o")
     ap.add_argument("--event-every", type=int, default=10,
                     help="time the scan kernel with HIP events on every n-th timed step (events attached to a "
                          "dispatch add ~11 us of queue gaps to that step)")
@@ -181,9 +182,12 @@ def main():
     table = dev(w.block_table)
     ctx = dev(w.ctx_lens)
     Wo = dev(w.W_o) if w.W_o is not None else None
-    folded = Wo is not None and not args.unfolded_wo
-    if folded:  # weight preparation, once (the value fold W_O R_V), outside the timed steps
-        Wo = K.int2kv_fold_wo(Wo, Rv, Hq)
+    # weight preparation, once per layer (the value fold W_O R_V; tiling), outside the timed steps
+    wo_format = K.INT2KV_WO_PLAIN
+    if Wo is not None and args.wo == "prepared":
+        Wo, wo_format = K.int2kv_prepare_wo(Wo, Rv, Hq), K.INT2KV_WO_PREPARED_FOLDED
+    elif Wo is not None and args.wo == "folded":
+        Wo, wo_format = K.int2kv_fold_wo(Wo, Rv, Hq), K.INT2KV_WO_FOLDED
     k_last = torch.empty((B, H, 128), dtype=torch.bfloat16, device="cuda")
     v_last = torch.empty_like(k_last)
     last_slots = np.array([w.slot_mapping(b, int(lens[b]) - 1)[0] for b in range(B)], np.int32)
@@ -206,7 +210,8 @@ def main():
 
     def step():
         K.int2kv_quantize_append(cache, k_last, v_last, slots_d, Rk, Rv, mu_rk)
-        K.int2kv_decode(cache, q, table, ctx, max_ctx, Rk, Rv, W_o=Wo, wo_is_folded=folded, out=out, workspace=ws)
+        K.int2kv_decode(cache, q, table, ctx, max_ctx, Rk, Rv, W_o=Wo, wo_format=wo_format, d_model=d_model, out=out,
+                        workspace=ws)
 
     for _ in range(args.warmup):
         step()
@@ -301,7 +306,9 @@ def main():
             "config_id": args.config, "batch": B, "num_q_heads": Hq, "num_kv_heads": H, "head_dim": 128, "block_size": 16,
             "group_size": 32, "sum_ctx": tokens, "max_ctx": max_ctx, "d_model": d_model,
             "chunk_tokens": args.chunk or "auto", "variant": args.variant or "auto",
-            "w_o": ("folded W_O R_V (prepared once)" if folded else "W_O after R_V^T") if Wo is not None else None,
+            "w_o": {"prepared": "W_O R_V folded, fp16 tiles (prepared once)",
+                    "folded": "W_O R_V folded, bf16 row-major (prepared once)",
+                    "plain": "W_O bf16 row-major after R_V^T"}[args.wo] if Wo is not None else None,
         },
         "roofline": {
             "kernel": "decode split-context scan",

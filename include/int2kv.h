@@ -104,6 +104,29 @@ int int2kv_prepare_mu_rot(const float* R_k, const float* mu, float* mu_rk, int n
 int int2kv_fold_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_o_folded, int d_model,
                    int num_q_heads, int num_kv_heads, hipStream_t stream);
 
+/* Output-projection weights in the form the decode's projection streams best: fp16, stored as
+ * 128-row x 32-column operand tiles, each 8 KiB tile contiguous (row blocks padded with zero
+ * rows to a multiple of 128). With R_v given, the value rotation is folded in first, as in
+ * int2kv_fold_wo (W-bar_{O,j} = W_{O,j} R_{V,h(j)}, appendix "Equivalent inference
+ * implementation"), accumulated in fp32 and rounded once to fp16; without it the bf16 weights
+ * are converted exactly. Weights must lie within the fp16 range (|w| <= 65504); values below
+ * 2^-14 keep the fp16 subnormal spacing 2^-24. Done once per layer, like the fold.
+ *   W_o        : bf16 [d_model, H_q*128] row-major
+ *   R_v        : fp32 [H_kv, 128, 128], or NULL (no fold)
+ *   W_prepared : int2kv_prepared_wo_bytes(d_model, H_q) bytes, 16-byte aligned (output); must
+ *                not overlap W_o */
+size_t int2kv_prepared_wo_bytes(int d_model, int num_q_heads);
+int int2kv_prepare_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_prepared, int d_model,
+                      int num_q_heads, int num_kv_heads, hipStream_t stream);
+
+/* Weight formats of the output projection in int2kv_decode (wo_format). */
+enum {
+  INT2KV_WO_PLAIN = 0,          /* W_O, bf16 row-major; the merge un-rotates o by R_V          */
+  INT2KV_WO_FOLDED = 1,         /* W-bar_O from int2kv_fold_wo, bf16 row-major                */
+  INT2KV_WO_PREPARED = 2,       /* int2kv_prepare_wo output without R_V (merge un-rotates)    */
+  INT2KV_WO_PREPARED_FOLDED = 3 /* int2kv_prepare_wo output with R_V folded in                */
+};
+
 /* Quantize already rotated rows and store them (the quantizer and packer alone; results are
  * bit-exact with the arithmetic above).
  *   k_rot, v_rot : fp32 [n, H_kv, 128]: (k - mu) R_K and v R_V
@@ -140,10 +163,13 @@ size_t int2kv_decode_workspace_bytes(int batch, int num_q_heads, int num_kv_head
  *                  outside [0, num_blocks) are skipped
  *   max_ctx      : host-side upper bound of ctx_lens (sizes the split-context grid)
  *   R_k, R_v     : fp32 [H_kv, 128, 128], 16-byte aligned (R_v may be NULL with a folded W_o)
- *   W_o          : bf16 [d_model, H_q*128], 16-byte aligned, or NULL (no output projection);
- *                  applied on the matrix cores with o split into two bf16 terms (fp32-like
- *                  precision), split over K in fixed slices summed in a fixed order
- *   wo_is_folded : nonzero if W_o is W-bar_O from int2kv_fold_wo (then R_v is not applied)
+ *   W_o          : output-projection weights in the format wo_format names, 16-byte aligned, or
+ *                  NULL (no output projection). Row-major bf16 weights are applied on the matrix
+ *                  cores with o split into two bf16 terms (fp32-like precision); prepared fp16
+ *                  weights with o rounded once to fp16 (relative error <= 2^-11 per element). The
+ *                  K range is split in fixed slices summed in a fixed order (deterministic)
+ *   wo_format    : INT2KV_WO_PLAIN, _FOLDED, _PREPARED or _PREPARED_FOLDED (with a folded format
+ *                  R_v is not applied); ignored when W_o is NULL
  *   out          : fp32 [B, H_q, 128] if W_o is NULL, else fp32 [B, d_model]
  *   workspace    : device scratch of at least int2kv_decode_workspace_bytes(...) bytes
  * The context is split into fixed-size chunks scanned in parallel (online softmax per chunk),
@@ -151,7 +177,7 @@ size_t int2kv_decode_workspace_bytes(int batch, int num_q_heads, int num_kv_head
 int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
                   const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens,
                   int max_ctx, const float* R_k, const float* R_v, const uint16_t* W_o, int d_model,
-                  int wo_is_folded, float* out, void* workspace, size_t workspace_bytes,
+                  int wo_format, float* out, void* workspace, size_t workspace_bytes,
                   hipStream_t stream);
 
 /* Measurement hook: when set (non-NULL), int2kv_decode attaches `before_scan` and `after_scan`

@@ -118,7 +118,7 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   p.off_o = off;
   if (d_model > 0) off = up(off + (size_t)B * Hq * kHeadDim * sizeof(float));
   p.off_wo = off;
-  if (d_model > 0) off = up(off + (size_t)p.wo_ksplit * B * d_model * sizeof(float));
+  if (d_model > 0 && p.wo_ksplit > 1) off = up(off + (size_t)p.wo_ksplit * B * d_model * sizeof(float));
   p.total = off;
   return p;
 }
@@ -169,6 +169,24 @@ int int2kv_fold_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_o_folded, 
   return hip_status(launch_fold_wo(W_o, R_v, W_o_folded, d_model, num_q_heads, num_kv_heads, stream), "fold_wo");
 }
 
+size_t int2kv_prepared_wo_bytes(int d_model, int num_q_heads) {
+  if (d_model <= 0 || num_q_heads <= 0) return 0;
+  return prepared_wo_elems(d_model, num_q_heads * kHeadDim) * sizeof(uint16_t);
+}
+
+int int2kv_prepare_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_prepared, int d_model, int num_q_heads,
+                      int num_kv_heads, hipStream_t stream) {
+  if (!W_o || !W_prepared) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (d_model <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads)
+    return fail(INT2KV_EINVAL, "bad d_model / head counts");
+  if (!aligned(W_prepared, 16)) return fail(INT2KV_EINVAL, "W_prepared must be 16-byte aligned");
+  const uint8_t* src = reinterpret_cast<const uint8_t*>(W_o);
+  const uint8_t* dst = reinterpret_cast<const uint8_t*>(W_prepared);
+  if (dst < src + (size_t)d_model * num_q_heads * kHeadDim * 2 && src < dst + int2kv_prepared_wo_bytes(d_model, num_q_heads))
+    return fail(INT2KV_EINVAL, "W_prepared must not overlap W_o");
+  return hip_status(launch_prepare_wo(W_o, R_v, W_prepared, d_model, num_q_heads, num_kv_heads, stream), "prepare_wo");
+}
+
 int int2kv_quantize_pack_rotated(const int2kv_cache* cache, const float* k_rot, const float* v_rot,
                                  const int32_t* slot_mapping, int num_tokens, float clip_k, float clip_v,
                                  hipStream_t stream) {
@@ -205,7 +223,7 @@ size_t int2kv_decode_workspace_bytes(int batch, int num_q_heads, int num_kv_head
 
 int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
                   const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens, int max_ctx,
-                  const float* R_k, const float* R_v, const uint16_t* W_o, int d_model, int wo_is_folded, float* out,
+                  const float* R_k, const float* R_v, const uint16_t* W_o, int d_model, int wo_format, float* out,
                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (int st = check_cache(cache)) return st;
   if (batch < 0) return fail(INT2KV_EINVAL, "batch must be >= 0");
@@ -215,7 +233,11 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
   const int gq = num_q_heads / H;
   if (gq > 16) return fail(INT2KV_EUNSUPPORTED, "at most 16 query heads per KV head");
   if (max_blocks_per_seq <= 0 || max_ctx < 0) return fail(INT2KV_EINVAL, "bad max_blocks_per_seq / max_ctx");
-  if (!q || !block_table || !ctx_lens || !R_k || !out || (!R_v && !(W_o && wo_is_folded)))
+  if (W_o && (wo_format < INT2KV_WO_PLAIN || wo_format > INT2KV_WO_PREPARED_FOLDED))
+    return fail(INT2KV_EINVAL, "wo_format must be one of INT2KV_WO_*");
+  const bool folded = W_o && (wo_format == INT2KV_WO_FOLDED || wo_format == INT2KV_WO_PREPARED_FOLDED);
+  const bool prepared = W_o && wo_format >= INT2KV_WO_PREPARED;
+  if (!q || !block_table || !ctx_lens || !R_k || !out || (!R_v && !folded))
     return fail(INT2KV_EINVAL, "NULL pointer argument");
   if (!aligned(q, 16) || !aligned(out, 16) || !aligned(R_k, 16) || (R_v && !aligned(R_v, 16)))
     return fail(INT2KV_EINVAL, "q, out, R_k and R_v must be 16-byte aligned");
@@ -268,13 +290,16 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
   e = plan.variant == 2 ? launch_decode_split_mfma(a, stream, g_ev_before, g_ev_after)
                         : launch_decode_split_valu(a, stream, g_ev_before, g_ev_after);
   if (e != hipSuccess) return hip_status(e, "decode/split");
-  const bool unrotate = !(W_o && wo_is_folded);
-  // with W_O the merge writes each head output as two bf16 terms (hi, lo) for the projection
+  const bool unrotate = !folded;
+  // with W_O the merge writes each head output as the projection's operand: two bf16 terms (hi, lo)
+  // for row-major bf16 weights, one fp16 term for prepared weights
   uint16_t* ob = W_o ? reinterpret_cast<uint16_t*>(ws + plan.off_o) : nullptr;
-  e = plan.variant == 2 ? launch_merge_flat(a, unrotate, out, ob, stream) : launch_merge(a, unrotate, out, ob, stream);
+  const int fmt = !W_o ? kOutF32 : (prepared ? kOutF16 : kOutBf16x2);
+  e = plan.variant == 2 ? launch_merge_flat(a, unrotate, out, ob, fmt, stream)
+                        : launch_merge(a, unrotate, out, ob, fmt, stream);
   if (e != hipSuccess) return hip_status(e, "decode/merge");
   if (W_o) {
-    e = launch_wo_gemm(ob, W_o, out, reinterpret_cast<float*>(ws + plan.off_wo), batch,
+    e = launch_wo_gemm(ob, W_o, prepared, out, reinterpret_cast<float*>(ws + plan.off_wo), batch,
                        num_q_heads * kHeadDim, d_model, plan.wo_ksplit, stream);
     if (e != hipSuccess) return hip_status(e, "decode/wo");
   }

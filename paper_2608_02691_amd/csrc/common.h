@@ -27,11 +27,15 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
 }
 // One head-output value, either as fp32 (out) or as two bf16 terms for the output projection:
 // hi = bf16(v) at ob[idx], lo = bf16(v - hi) at ob[total + idx].
-__device__ __forceinline__ void store_head_out(float v, float* out, uint16_t* ob, size_t idx, size_t total) {
-  if (ob) {
+// Head output v at index idx: fp32 to out (fmt 0), two bf16 terms hi, lo = bf16(v - hi) at idx and
+// total + idx of ob (fmt 1), or one fp16 term (fmt 2).
+__device__ __forceinline__ void store_head_out(float v, float* out, uint16_t* ob, int fmt, size_t idx, size_t total) {
+  if (fmt == 1) {
     const uint32_t h = f32_to_bf16_rne(v);
     ob[idx] = (uint16_t)h;
     ob[total + idx] = (uint16_t)f32_to_bf16_rne(v - __uint_as_float(h << 16));
+  } else if (fmt == 2) {
+    ob[idx] = __half_as_ushort(__float2half_rn(v));
   } else {
     out[idx] = v;
   }

@@ -236,7 +236,7 @@ hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s, hipEvent
 // undo the value rotation: o = o' R_V^T (skipped when W_O arrives pre-folded with R_V).
 // Block (sequence, KV head), thread c = channel.
 __global__ __launch_bounds__(128) void merge_kernel(DecodeArgs a, int unrotate, float* __restrict__ out,
-                                                    uint16_t* __restrict__ ob) {
+                                                    uint16_t* __restrict__ ob, int fmt) {
   __shared__ float os[kHeadDim];
   const int b = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
   const int L = seq_len(a, b);
@@ -273,12 +273,12 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeArgs a, int unrotate, 
       res = acc;
       __syncthreads();
     }
-    store_head_out(res, out, ob, ((size_t)b * a.Hq + j) * kHeadDim + c, (size_t)a.B * a.Hq * kHeadDim);
+    store_head_out(res, out, ob, fmt, ((size_t)b * a.Hq + j) * kHeadDim + c, (size_t)a.B * a.Hq * kHeadDim);
   }
 }
 
-hipError_t launch_merge(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, hipStream_t s) {
-  hipLaunchKernelGGL(merge_kernel, dim3(a.B, a.H), dim3(128), 0, s, a, unrotate ? 1 : 0, out, ob);
+hipError_t launch_merge(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, int fmt, hipStream_t s) {
+  hipLaunchKernelGGL(merge_kernel, dim3(a.B, a.H), dim3(128), 0, s, a, unrotate ? 1 : 0, out, ob, fmt);
   return hipGetLastError();
 }
 

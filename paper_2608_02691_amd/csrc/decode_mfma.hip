@@ -952,7 +952,7 @@ constexpr int kMergeSlots = 8;
 
 __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArgs a, int G, int unrotate,
                                                                        float* __restrict__ out,
-                                                                       uint16_t* __restrict__ ob) {
+                                                                       uint16_t* __restrict__ ob, int fmt) {
   __shared__ float ms[kMergeSlots][8], ls[kMergeSlots][8];
   __shared__ float os[kMergeSlots][8][kHeadDim];
   __shared__ float vs[8][kHeadDim];
@@ -1037,13 +1037,13 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
 #pragma unroll
       for (int j2 = 0; j2 < 8; ++j2)
         if (j2 < gq)
-          store_head_out(acc[j2], out, ob, ((size_t)b * a.Hq + h * gq + j2) * kHeadDim + c,
+          store_head_out(acc[j2], out, ob, fmt, ((size_t)b * a.Hq + h * gq + j2) * kHeadDim + c,
                          (size_t)a.B * a.Hq * kHeadDim);
     }
     return;
   }
   if (jj < gq)
-    store_head_out(val, out, ob, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c, (size_t)a.B * a.Hq * kHeadDim);
+    store_head_out(val, out, ob, fmt, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c, (size_t)a.B * a.Hq * kHeadDim);
 }
 
 hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
@@ -1067,10 +1067,10 @@ hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s, hipEvent
   return hipGetLastError();
 }
 
-hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, hipStream_t s) {
+hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, int fmt, hipStream_t s) {
   if (a.gq > 8) return hipErrorNotSupported;
   hipLaunchKernelGGL(merge_flat_kernel, dim3(a.B, a.H), dim3(128 * kMergeSlots), 0, s, a, a.grid_g, unrotate ? 1 : 0,
-                     out, ob);
+                     out, ob, fmt);
   return hipGetLastError();
 }
 

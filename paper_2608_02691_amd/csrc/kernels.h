@@ -64,14 +64,19 @@ hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s, hipEvent
 hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 size_t qop_bytes(int B, int H, int gq);
-// merges write fp32 head outputs to `out`, or (ob != NULL) the two bf16 terms of each value for
-// the output projection: ob[0 .. B*Hq*128) = hi, ob[B*Hq*128 ..) = lo
-hipError_t launch_merge(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, hipStream_t s);
-hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, hipStream_t s);
+// Head-output formats of the merges: fp32 to `out`, or for the output projection (to `ob`) two bf16
+// terms of each value (ob[0 .. B*Hq*128) = hi, ob[B*Hq*128 ..) = lo) or one fp16 term.
+enum OutFmt { kOutF32 = 0, kOutBf16x2 = 1, kOutF16 = 2 };
+hipError_t launch_merge(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, int fmt, hipStream_t s);
+hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, int fmt, hipStream_t s);
 int num_cus();                        // compute units of the current device
 int wo_slice(int K, int N, int B);    // K per work-group of the output projection
 int wo_ksplit(int K, int N, int B);   // K slices of the output projection (partial products in the workspace)
-hipError_t launch_wo_gemm(const uint16_t* ob, const uint16_t* W, float* y, float* partial, int B, int K,
-                          int N, int ksplit, hipStream_t s);
+// prepared: W is int2kv_prepare_wo output and ob one fp16 term; else W is bf16 row-major, ob two bf16 terms
+hipError_t launch_wo_gemm(const uint16_t* ob, const uint16_t* W, bool prepared, float* y, float* partial, int B,
+                          int K, int N, int ksplit, hipStream_t s);
+size_t prepared_wo_elems(int N, int K);  // fp16 elements of the prepared weights (rows padded to 128)
+hipError_t launch_prepare_wo(const uint16_t* W_o, const float* R_v, uint16_t* Wp, int N, int Hq, int H,
+                             hipStream_t s);
 
 }  // namespace int2kv

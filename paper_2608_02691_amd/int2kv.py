@@ -27,8 +27,14 @@ INT2KV_EUNSUPPORTED = -2
 INT2KV_EWORKSPACE = -3
 INT2KV_EHIP = -4
 
+INT2KV_WO_PLAIN = 0
+INT2KV_WO_FOLDED = 1
+INT2KV_WO_PREPARED = 2
+INT2KV_WO_PREPARED_FOLDED = 3
+
 EXPORTED = (
     "int2kv_last_error", "int2kv_version", "int2kv_pool_bytes", "int2kv_prepare_mu_rot", "int2kv_fold_wo",
+    "int2kv_prepared_wo_bytes", "int2kv_prepare_wo",
     "int2kv_quantize_pack_rotated", "int2kv_quantize_append", "int2kv_decode_workspace_bytes",
     "int2kv_decode", "int2kv_set_decode_tuning", "int2kv_set_decode_events",
 )
@@ -58,6 +64,8 @@ def load_library(path: str = LIB_PATH):
         "int2kv_pool_bytes": ([I, I], Z),
         "int2kv_prepare_mu_rot": ([P, P, P, I, S], I),
         "int2kv_fold_wo": ([P, P, P, I, I, I, S], I),
+        "int2kv_prepared_wo_bytes": ([I, I], Z),
+        "int2kv_prepare_wo": ([P, P, P, I, I, I, S], I),
         "int2kv_quantize_pack_rotated": ([ctypes.POINTER(_Cache), P, P, P, I, F, F, S], I),
         "int2kv_quantize_append": ([ctypes.POINTER(_Cache), P, P, P, I, P, P, P, F, F, S], I),
         "int2kv_decode_workspace_bytes": ([I, I, I, I, I], Z),
@@ -147,6 +155,30 @@ def int2kv_fold_wo(W_o: torch.Tensor, R_v: torch.Tensor, num_q_heads: int,
     return out
 
 
+def int2kv_prepared_wo_bytes(d_model: int, num_q_heads: int) -> int:
+    return load_library().int2kv_prepared_wo_bytes(d_model, num_q_heads)
+
+
+def int2kv_prepare_wo(W_o: torch.Tensor, R_v: Optional[torch.Tensor], num_q_heads: int,
+                      num_kv_heads: Optional[int] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Prepared (fp16, tiled) output-projection weights; R_v folds the value rotation in (None: no
+    fold, then num_kv_heads must be given). Returns a flat float16 tensor."""
+    d_model = W_o.shape[0]
+    H = R_v.shape[0] if R_v is not None else num_kv_heads
+    if H is None:
+        raise ValueError("num_kv_heads is required without R_v")
+    n = int2kv_prepared_wo_bytes(d_model, num_q_heads) // 2
+    if out is None:
+        out = torch.empty(n, dtype=torch.float16, device=W_o.device)
+    if out.numel() < n:
+        raise ValueError("out is smaller than int2kv_prepared_wo_bytes()")
+    st = load_library().int2kv_prepare_wo(_ptr(W_o, _BF16, "W_o"), _ptr(R_v, _F32, "R_v"),
+                                          _ptr(out, (torch.float16, torch.int16, torch.uint16), "out"), d_model,
+                                          num_q_heads, H, _stream())
+    _check(st, "int2kv_prepare_wo")
+    return out
+
+
 def int2kv_quantize_pack_rotated(cache: Int2KVCache, k_rot: torch.Tensor, v_rot: torch.Tensor,
                                  slot_mapping: torch.Tensor, clip_k: float = 1.0, clip_v: float = 1.0) -> None:
     n = slot_mapping.shape[0]
@@ -189,9 +221,19 @@ def int2kv_set_decode_events(before_scan: Optional[int], after_scan: Optional[in
 def int2kv_decode(cache: Int2KVCache, q: torch.Tensor, block_table: torch.Tensor, ctx_lens: torch.Tensor,
                   max_ctx: int, R_k: torch.Tensor, R_v: Optional[torch.Tensor], W_o: Optional[torch.Tensor] = None,
                   wo_is_folded: bool = False, out: Optional[torch.Tensor] = None,
-                  workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+                  workspace: Optional[torch.Tensor] = None, wo_format: Optional[int] = None,
+                  d_model: Optional[int] = None) -> torch.Tensor:
+    """wo_format (INT2KV_WO_*) overrides wo_is_folded; prepared weights (flat) need d_model."""
     B, Hq = q.shape[0], q.shape[1]
-    d_model = W_o.shape[0] if W_o is not None else 0
+    if wo_format is None:
+        wo_format = INT2KV_WO_FOLDED if wo_is_folded else INT2KV_WO_PLAIN
+    if W_o is None:
+        d_model = 0
+    elif wo_format >= INT2KV_WO_PREPARED:
+        if d_model is None:
+            raise ValueError("d_model is required with prepared W_o")
+    else:
+        d_model = W_o.shape[0]
     if out is None:
         shape = (B, d_model) if W_o is not None else (B, Hq, HEAD_DIM)
         out = torch.empty(shape, dtype=torch.float32, device=q.device)
@@ -201,7 +243,7 @@ def int2kv_decode(cache: Int2KVCache, q: torch.Tensor, block_table: torch.Tensor
     st = load_library().int2kv_decode(
         cache.desc, _ptr(q, _BF16, "q"), B, Hq, _ptr(block_table, _I32, "block_table"), block_table.shape[1],
         _ptr(ctx_lens, _I32, "ctx_lens"), max_ctx, _ptr(R_k, _F32, "R_k"), _ptr(R_v, _F32, "R_v"),
-        _ptr(W_o, _BF16, "W_o"), d_model, 1 if wo_is_folded else 0, _ptr(out, _F32, "out"),
+        _ptr(W_o, _BF16 + (torch.float16,), "W_o"), d_model, wo_format, _ptr(out, _F32, "out"),
         _ptr(workspace, (torch.uint8,), "workspace"), workspace.numel(), _stream())
     _check(st, "int2kv_decode")
     return out

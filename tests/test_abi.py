@@ -56,3 +56,25 @@ def test_null_cache_and_bad_arguments_return_errors_without_launch():
     assert lib.int2kv_set_decode_tuning(100, 0) == K.INT2KV_EINVAL
     assert lib.int2kv_set_decode_tuning(0, 7) == K.INT2KV_EINVAL
     assert lib.int2kv_set_decode_tuning(0, 0) == K.INT2KV_OK
+
+
+def test_prepared_wo_sizes_and_argument_errors():
+    lib = K.load_library()
+    # rows padded to a multiple of 128, fp16
+    assert K.int2kv_prepared_wo_bytes(5120, 40) == 5120 * 5120 * 2
+    assert K.int2kv_prepared_wo_bytes(200, 2) == 256 * 256 * 2
+    assert K.int2kv_prepared_wo_bytes(0, 2) == 0
+    assert lib.int2kv_prepare_wo(None, None, 4096, 128, 1, 1, None) == K.INT2KV_EINVAL  # NULL W_o
+    assert lib.int2kv_prepare_wo(4096, None, 1 << 20, 128, 3, 2, None) == K.INT2KV_EINVAL  # 3 % 2
+    assert lib.int2kv_prepare_wo(4096, None, 4104, 128, 1, 1, None) == K.INT2KV_EINVAL  # misaligned output
+    assert b"aligned" in lib.int2kv_last_error()
+    assert lib.int2kv_prepare_wo(4096, None, 4096 + 1024, 128, 1, 1, None) == K.INT2KV_EINVAL  # overlap
+    assert b"overlap" in lib.int2kv_last_error()
+
+
+def test_decode_rejects_unknown_weight_format_without_launch():
+    lib = K.load_library()
+    good = K._Cache(16, 4, 2, 16, 128, 32)
+    st = lib.int2kv_decode(ctypes.byref(good), 16, 1, 4, 16, 1, 16, 16, 16, 16, 16, 256, 4, 16, 256, 1 << 30, None)
+    assert st == K.INT2KV_EINVAL
+    assert b"wo_format" in lib.int2kv_last_error()

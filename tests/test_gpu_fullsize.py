@@ -50,7 +50,11 @@ def test_config1_full_decode_with_wo():
     Wf = K.int2kv_fold_wo(Wo, Rv, w.num_q_heads)
     worst_f = assert_rows_close(K.int2kv_decode(*args, W_o=Wf, wo_is_folded=True).cpu().numpy(), ref,
                                 what="config 1, folded W_O")
-    print(f"worst row error {worst:.2e} (plain W_O), {worst_f:.2e} (folded)", flush=True)
+    Wp = K.int2kv_prepare_wo(Wo, Rv, w.num_q_heads)
+    worst_p = assert_rows_close(K.int2kv_decode(*args, W_o=Wp, wo_format=K.INT2KV_WO_PREPARED_FOLDED,
+                                                d_model=w.W_o.shape[0]).cpu().numpy(), ref,
+                                what="config 1, prepared folded W_O")
+    print(f"worst row error {worst:.2e} (plain W_O), {worst_f:.2e} (folded), {worst_p:.2e} (prepared)", flush=True)
 
 
 def test_config2_long_context_sampled_heads():
@@ -110,15 +114,18 @@ def test_config3_prefill_append_then_decode():
 
 
 def test_config4_sampled_sequences():
-    """The benchmark workload (64 ragged sequences, 40/8 heads, folded W_O 5120^2) decoded whole on
-    the GPU; the shortest, the longest and two seeded other sequences are checked, each against
-    an oracle cache holding that sequence alone."""
+    """The benchmark workload (64 ragged sequences, 40/8 heads, W_O 5120^2 prepared with R_V folded
+    in, as the benchmark runs it; also row-major folded) decoded whole on the GPU; the shortest, the
+    longest and two seeded other sequences are checked, each against an oracle cache holding that
+    sequence alone."""
     print("\n[full] config 4", flush=True)
     w = W.make_workload(4)
     cache, Rk, Rv = gpu_build(w)
+    dargs = (cache, dev(w.q), dev(w.block_table), dev(w.ctx_lens), int(w.ctx_lens.max()), Rk, Rv)
+    Wp = K.int2kv_prepare_wo(dev(w.W_o), Rv, w.num_q_heads)
+    y = K.int2kv_decode(*dargs, W_o=Wp, wo_format=K.INT2KV_WO_PREPARED_FOLDED, d_model=w.W_o.shape[0]).cpu().numpy()
     Wf = K.int2kv_fold_wo(dev(w.W_o), Rv, w.num_q_heads)
-    y = K.int2kv_decode(cache, dev(w.q), dev(w.block_table), dev(w.ctx_lens), int(w.ctx_lens.max()), Rk, Rv,
-                        W_o=Wf, wo_is_folded=True).cpu().numpy()
+    y_f = K.int2kv_decode(*dargs, W_o=Wf, wo_is_folded=True).cpu().numpy()
     lens = w.ctx_lens
     rng = np.random.default_rng(4)
     picks = sorted({int(np.argmin(lens)), int(np.argmax(lens)), *rng.choice(w.batch, 2, replace=False).tolist()})
@@ -131,4 +138,5 @@ def test_config4_sampled_sequences():
         ref = O.decode(pool, w.q[b:b + 1], np.arange(nblk, dtype=np.int32)[None], np.array([L], np.int32),
                        w.R_k, w.R_v, w.W_o)
         worst = assert_rows_close(y[b:b + 1], ref, what=f"config 4 sequence {b} (L={L})")
-        print(f"sequence {b} (L={L}): worst row error {worst:.2e}", flush=True)
+        worst_f = assert_rows_close(y_f[b:b + 1], ref, what=f"config 4 sequence {b} (L={L}), row-major W_O")
+        print(f"sequence {b} (L={L}): worst row error {worst:.2e} (prepared), {worst_f:.2e} (row-major)", flush=True)

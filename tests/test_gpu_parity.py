@@ -110,6 +110,8 @@ DECODE_CASES = [
     (1, 2, 32, 16, [200, 64], None),
     (1, 2, 96, 8, [150, 20], None),
     (4, 2, 10, 2, [300, 17], 100),
+    # 256 row blocks of the output projection: one K slice, no arrival counting
+    (4, 1, 2, 1, [100], 32768),
 ]
 
 
@@ -139,6 +141,12 @@ def test_decode_matches_oracle(case, chunk, variant):
         Wf = K.int2kv_fold_wo(dev(w.W_o), dev(w.R_v), Hq)
         out_f = K.int2kv_decode(*args, W_o=Wf, wo_is_folded=True)
         assert_rows_close(out_f.cpu().numpy(), out_ref, what="decode with folded W_O")
+        for fold in (False, True):
+            Wp = K.int2kv_prepare_wo(dev(w.W_o), dev(w.R_v) if fold else None, Hq, num_kv_heads=H)
+            fmt = K.INT2KV_WO_PREPARED_FOLDED if fold else K.INT2KV_WO_PREPARED
+            out_p = K.int2kv_decode(*args, W_o=Wp, wo_format=fmt, d_model=dm)
+            assert_rows_close(out_p.cpu().numpy(), out_ref, what=f"decode with prepared W_O (fold={fold})")
+            assert torch.equal(out_p, K.int2kv_decode(*args, W_o=Wp, wo_format=fmt, d_model=dm))
 
 
 def test_fold_wo_matches_oracle():
@@ -149,6 +157,32 @@ def test_fold_wo_matches_oracle():
     # one bf16 rounding (half an ulp: 2^-8 relative) of an fp32 accumulation of 128 products
     # (absolute error ~1e-6 of the row scale, which matters only for entries near zero)
     assert np.all(np.abs(g - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-6 * np.abs(ref).max())
+
+
+def _untile_prepared(flat, n_rows, k):
+    """Row-major [n_rows padded to 128, k] view of prepared weights: tile (row block, k step) holds
+    eight 16 x 32 sub-tiles; in sub-tile a, lane r + 16 q carries row 16 a + r, columns 8 q .. 8 q + 7."""
+    npad = (n_rows + 127) // 128 * 128
+    t = flat.reshape(npad // 128, k // 32, 8, 4, 16, 8)  # row block, k step, a, q, r, e
+    return t.transpose(0, 2, 4, 1, 3, 5).reshape(npad, k)
+
+
+@pytest.mark.parametrize("fold", [False, True])
+def test_prepare_wo_layout_and_values(fold):
+    Hq, H, dm = 4, 2, 200
+    w = W.make_workload(1, batch=1, ctx=16, num_q_heads=Hq, num_kv_heads=H, d_model=dm)
+    got = K.int2kv_prepare_wo(dev(w.W_o), dev(w.R_v) if fold else None, Hq, num_kv_heads=H).cpu().numpy()
+    assert got.size == K.int2kv_prepared_wo_bytes(dm, Hq) // 2
+    Wr = _untile_prepared(got, dm, Hq * 128)
+    assert not np.any(Wr[dm:]), "padding rows must be zero"
+    if not fold:
+        # bf16 -> fp16 is exact in the normal range and rounds to nearest even below it
+        assert np.array_equal(Wr[:dm], O.bf16_to_f64(w.W_o).astype(np.float16))
+    else:
+        ref = O.fold_wo(w.W_o, w.R_v, Hq)
+        g = Wr[:dm].astype(np.float64)
+        # one fp16 rounding (2^-11 relative, 2^-25 absolute below 2^-14) of an fp32 accumulation
+        assert np.all(np.abs(g - ref) <= 2.0 ** -11 * np.abs(ref) + 2.0 ** -25 + 1e-6 * np.abs(ref).max())
 
 
 def test_out_of_range_blocks_and_lengths_are_clamped():
