@@ -558,48 +558,63 @@ constexpr int kWavesPerWG = 8;   // one wave per KV head of a head group
 
 typedef __attribute__((address_space(4))) const int32_t* cint_ptr;  // read through the scalar cache
 
-// First page of work-group g's range when P pages are split evenly over G groups.
-__host__ __device__ __forceinline__ int range_lo(int g, int P, int G) { return (int)(((long long)g * P) / G); }
+// Work split of the scan. Every sequence a work-group starts costs a prologue and a pipeline
+// refill (measured: about 4 us per extra segment, the time of ~6 pages), so the pages are split
+// evenly along a cost axis on which each non-empty sequence b occupies [c0(b), c1(b)): kSegCost
+// units of lead-in, then one unit per page (c1 - c0 = kSegCost + pages; empty sequences take no
+// room). Group g of G starts at cost x(g) = floor(g W / G), W = P + kSegCost * (non-empty
+// sequences); a start inside a lead-in maps to the sequence's first page. Ranges that take on
+// extra sequence starts thus get fewer pages.
+constexpr int kSegCost = 6;
 
 // Pages of every sequence and their exclusive prefix sums (prefix[B] = total pages), and for each
 // scan work-group g the sequence b holding the first page of its range with that sequence's page
 // range: wg_info[g] = {b, prefix[b], prefix[b + 1], lo(g)}, wg_info[G].w = P, and for every sequence
 // the first and last group whose range meets it (seq_wg[b] = {ga, gb}, {0, -1} when empty), so that
-// no later wave divides. Group g starts inside sequence b exactly
-// when prefix[b] <= lo(g) < prefix[b + 1], i.e. for g in [ceil(prefix[b] G / P), ...) while lo(g)
-// stays below prefix[b + 1], so every group is written once (by the thread owning b). One block
-// of 256 threads.
+// no later wave divides or searches. With x(g) <= T  <=>  g <= ceil((T + 1) G / W) - 1, the groups
+// starting in b's span are ceil(c0 G / W) .. ceil(c1 G / W) - 1, the group holding b's first page
+// is the last one with x(g) <= c0 + kSegCost, the one holding its last page the last with
+// x(g) <= c1 - 1. Every group below G starts in exactly one span (the spans tile [0, W)), so every
+// entry is written once, by the thread owning that sequence. One block of 256 threads.
 __device__ void page_prefix_block(const DecodeArgs& a) {
-  __shared__ int sums[256];
+  __shared__ int sums[256], cnts[256];
   const int tid = threadIdx.x;
   const int per = (a.B + 255) / 256;
   const int b0 = min(a.B, tid * per), b1 = min(a.B, b0 + per);
-  int s = 0;
-  for (int b = b0; b < b1; ++b) s += (seq_len_m(a, b) + kBlock - 1) >> 4;
+  int s = 0, c = 0;
+  for (int b = b0; b < b1; ++b) {
+    const int n = (seq_len_m(a, b) + kBlock - 1) >> 4;
+    s += n;
+    c += n > 0;
+  }
   sums[tid] = s;
+  cnts[tid] = c;
   __syncthreads();
   for (int off = 1; off < 256; off <<= 1) {
-    const int v = tid >= off ? sums[tid - off] : 0;
+    const int v = tid >= off ? sums[tid - off] : 0, u = tid >= off ? cnts[tid - off] : 0;
     __syncthreads();
     sums[tid] += v;
+    cnts[tid] += u;
     __syncthreads();
   }
   const int P = sums[255], G = a.grid_g;
-  int run = tid > 0 ? sums[tid - 1] : 0;
+  const long long W = (long long)P + (long long)kSegCost * cnts[255];
+  int run = tid > 0 ? sums[tid - 1] : 0, cnt = tid > 0 ? cnts[tid - 1] : 0;
   for (int b = b0; b < b1; ++b) {
     const int n = (seq_len_m(a, b) + kBlock - 1) >> 4;
     a.prefix[b] = run;
-    int ga = 0, gb = -1;  // groups whose ranges contain the sequence's first and last page
+    int ga = 0, gb = -1;
     if (n > 0) {
-      for (int g = (int)(((long long)run * G + P - 1) / P); g < G && range_lo(g, P, G) < run + n; ++g)
-        *reinterpret_cast<int4*>(a.wg_info + 4 * g) = make_int4(b, run, run + n, range_lo(g, P, G));
-      const int last = run + n - 1;
-      ga = (int)(((long long)run * G) / P);
-      while (ga > 0 && range_lo(ga, P, G) > run) --ga;
-      while (range_lo(ga + 1, P, G) <= run) ++ga;
-      gb = (int)(((long long)last * G) / P);
-      while (gb > 0 && range_lo(gb, P, G) > last) --gb;
-      while (range_lo(gb + 1, P, G) <= last) ++gb;
+      const long long c0 = run + (long long)kSegCost * cnt, c1 = c0 + kSegCost + n;
+      const int g1 = min(G - 1, (int)((c1 * G + W - 1) / W) - 1);
+      for (int g = (int)((c0 * G + W - 1) / W); g <= g1; ++g) {
+        const long long x = (long long)g * W / G;
+        const int lo = run + (int)min((long long)n - 1, max(0LL, x - c0 - kSegCost));
+        *reinterpret_cast<int4*>(a.wg_info + 4 * g) = make_int4(b, run, run + n, lo);
+      }
+      ga = min(G - 1, (int)(((c0 + kSegCost + 1) * G + W - 1) / W) - 1);
+      gb = g1;
+      ++cnt;
     }
     a.seq_wg[2 * b] = ga;
     a.seq_wg[2 * b + 1] = gb;
