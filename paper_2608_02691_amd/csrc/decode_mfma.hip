@@ -686,7 +686,8 @@ __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)
 // (m, l, O') per query head written to partial slot `slot`.
 template <bool WIDE>
 __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, int gs, int ge, int slot, int l,
-                                             uint8_t* stage_w, _Float16 (*p_w)[2][8][kBlock], float* al_w) {
+                                             uint8_t* stage_w, _Float16 (*p_w)[2][8][kBlock], float* al_w,
+                                             bool all_waves) {
   constexpr int NJ = ScanState<WIDE>::NJ, NT = ScanState<WIDE>::NT;
   const int lo = l & 15, hi = l >> 4;
   const int n = ge - gs;             // pages
@@ -837,6 +838,11 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   int k = 0;
   // steady groups of kUnroll steps (the slot and the X / Y register set repeat with that period)
   for (; k + kUnroll + kStages < nfull; k += kUnroll) {
+    // one barrier per group keeps the 8 waves (the 8 head records of each block, 12 KiB of
+    // contiguous memory) streaming close together in time: 1-2 us faster than free-running waves.
+    // Every wave of the work-group runs the same segments and trip counts (same page ranges); the
+    // barrier is skipped in work-groups where some waves have no KV head (all_waves is uniform).
+    if (all_waves) __builtin_amdgcn_s_barrier();
     static_for<kUnroll>([&](auto J) {
       if constexpr (decltype(J)::value % 2 == 0)
         step(J, T{}, X, Y, k);
@@ -935,6 +941,7 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   const int g = G % 8 == 0 ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
   const int h = blockIdx.y * kWavesPerWG + w;
+  const bool all_waves = a.H < kWavesPerWG || (int)(blockIdx.y + 1) * kWavesPerWG <= a.H;
   if (h >= a.H) return;
   const cint_ptr prefix = (cint_ptr)(uintptr_t)(a.prefix);
   const int P = prefix[a.B];
@@ -946,7 +953,7 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   for (int pos = s;;) {
     const int seg_end = min(e, Sb1);
     const int Sb2 = seg_end < e ? prefix[b + 2] : 0;  // next sequence's end, fetched ahead
-    scan_segment<WIDE>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w]);
+    scan_segment<WIDE>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w], all_waves);
     pos = seg_end;
     if (pos >= e) break;
     ++b;

@@ -108,6 +108,8 @@ DECODE_CASES = [
     (1, 1, 56, 8, [400], None),
     (1, 2, 64, 8, [257, 1], None),
     (1, 2, 32, 16, [200, 64], None),
+    # 12 KV heads: the second row of scan work-groups has 4 waves without a head
+    (1, 2, 24, 12, [300, 45], None),
     (1, 2, 96, 8, [150, 20], None),
     (4, 2, 10, 2, [300, 17], 100),
     # 256 row blocks of the output projection: one K slice, no arrival counting
