@@ -133,6 +133,9 @@ def main():
     ap.add_argument("--wo", choices=("prepared", "folded", "plain"), default="prepared",
                     help="output-projection weights: prepared fp16 tiles with R_V folded in (default), row-major "
                          "bf16 folded with R_V, or row-major bf16 W_O with the merge un-rotating o")
+    ap.add_argument("--separate", action="store_true",
+                    help="append and decode as two calls (default: int2kv_append_decode, the cache write beside "
+                         "the query preparation)")
     ap.add_argument("--event-every", type=int, default=10,
                     help="time the scan kernel with HIP events on every n-th timed step (events attached to a "
                          "dispatch add ~11 us of queue gaps to that step)")
@@ -209,9 +212,13 @@ def main():
     out = torch.empty((B, d_model) if d_model else (B, Hq, 128), dtype=torch.float32, device="cuda")
 
     def step():
-        K.int2kv_quantize_append(cache, k_last, v_last, slots_d, Rk, Rv, mu_rk)
-        K.int2kv_decode(cache, q, table, ctx, max_ctx, Rk, Rv, W_o=Wo, wo_format=wo_format, d_model=d_model, out=out,
-                        workspace=ws)
+        if args.separate:
+            K.int2kv_quantize_append(cache, k_last, v_last, slots_d, Rk, Rv, mu_rk)
+            K.int2kv_decode(cache, q, table, ctx, max_ctx, Rk, Rv, W_o=Wo, wo_format=wo_format, d_model=d_model,
+                            out=out, workspace=ws)
+        else:
+            K.int2kv_append_decode(cache, k_last, v_last, slots_d, mu_rk, q, table, ctx, max_ctx, Rk, Rv, W_o=Wo,
+                                   wo_format=wo_format, d_model=d_model, out=out, workspace=ws)
 
     for _ in range(args.warmup):
         step()
@@ -306,6 +313,8 @@ def main():
             "config_id": args.config, "batch": B, "num_q_heads": Hq, "num_kv_heads": H, "head_dim": 128, "block_size": 16,
             "group_size": 32, "sum_ctx": tokens, "max_ctx": max_ctx, "d_model": d_model,
             "chunk_tokens": args.chunk or "auto", "variant": args.variant or "auto",
+            "step_calls": ("int2kv_quantize_append + int2kv_decode" if args.separate else
+                           "int2kv_append_decode (cache write inside the preparation launch)"),
             "w_o": {"prepared": "W_O R_V folded, fp16 tiles (prepared once)",
                     "folded": "W_O R_V folded, bf16 row-major (prepared once)",
                     "plain": "W_O bf16 row-major after R_V^T"}[args.wo] if Wo is not None else None,

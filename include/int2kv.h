@@ -180,6 +180,22 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
                   int wo_format, float* out, void* workspace, size_t workspace_bytes,
                   hipStream_t stream);
 
+/* One decode step of a serving loop: the cache write of the current tokens
+ * (int2kv_quantize_append with k, v, slot_mapping, num_tokens, R_k, R_v, mu_rk, clip_k, clip_v)
+ * followed by int2kv_decode with the remaining arguments; the results are bit-identical to those
+ * two calls made in that order. With the matrix-core decode and at most 256 tokens, the cache
+ * write runs as extra work-groups of the decode's first launch, beside the query preparation
+ * (which does not read the cache), instead of as a launch of its own. R_v is required when
+ * num_tokens > 0 (the cache write uses it); num_tokens = 0 makes this int2kv_decode. Errors as
+ * for the two calls; nothing is launched on an argument error. */
+int int2kv_append_decode(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
+                         const int32_t* slot_mapping, int num_tokens, const float* mu_rk, float clip_k,
+                         float clip_v, const uint16_t* q, int batch, int num_q_heads,
+                         const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens,
+                         int max_ctx, const float* R_k, const float* R_v, const uint16_t* W_o,
+                         int d_model, int wo_format, float* out, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream);
+
 /* Measurement hook: when set (non-NULL), int2kv_decode attaches `before_scan` and `after_scan`
  * to the dispatch of the split-context scan kernel (hipExtLaunchKernel), so they mark that
  * kernel's own start and end and a caller can time it alone with hipEventElapsedTime, without

@@ -221,13 +221,34 @@ size_t int2kv_decode_workspace_bytes(int batch, int num_q_heads, int num_kv_head
   return make_plan(batch, num_q_heads, num_kv_heads, max_ctx, d_model).total;
 }
 
-int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
-                  const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens, int max_ctx,
-                  const float* R_k, const float* R_v, const uint16_t* W_o, int d_model, int wo_format, float* out,
-                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Appends of at most this many tokens run inside the decode's preparation launch.
+constexpr int kFusedAppendTokens = 256;
+
+// The cache write of int2kv_append_decode: its arguments, validated, and whether there is one.
+struct AppendStage {
+  const uint16_t *k = nullptr, *v = nullptr;
+  const int32_t* slots = nullptr;
+  int n = 0;
+  const float* mu_rk = nullptr;
+  float clip_k = 1.0f, clip_v = 1.0f;
+};
+
+int decode_impl(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
+                const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens, int max_ctx,
+                const float* R_k, const float* R_v, const uint16_t* W_o, int d_model, int wo_format, float* out,
+                void* workspace, size_t workspace_bytes, hipStream_t stream, const AppendStage* ap) {
   if (int st = check_cache(cache)) return st;
   if (batch < 0) return fail(INT2KV_EINVAL, "batch must be >= 0");
-  if (batch == 0) return ok();
+  if (batch == 0) {
+    if (!ap || ap->n == 0) return ok();
+    return hip_status(launch_append_mfma(view(cache), ap->k, ap->v, ap->slots, ap->n, R_k, R_v, ap->mu_rk, ap->clip_k,
+                                         ap->clip_v, stream),
+                      "append_decode/append");
+  }
   const int H = cache->num_kv_heads;
   if (num_q_heads <= 0 || num_q_heads % H) return fail(INT2KV_EINVAL, "num_q_heads must be a multiple of num_kv_heads");
   const int gq = num_q_heads / H;
@@ -279,11 +300,24 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
   a.grid_g = plan.grid_g;
 
   hipError_t e = hipSuccess;
+  // the cache write (int2kv_append_decode): a few tokens per sequence run as extra blocks of the
+  // matrix-core preparation launch, beside the query preparation (which does not read the cache);
+  // otherwise (long appends, vector-ALU decode) as its own launch first
+  AppendArgs apa{};
+  const bool fused_append = ap && ap->n > 0 && plan.variant == 2 && ap->n <= kFusedAppendTokens;
+  if (ap && ap->n > 0) {
+    apa = AppendArgs{view(cache), ap->k, ap->v, ap->slots, ap->n, R_k, R_v, ap->mu_rk, ap->clip_k, ap->clip_v, 0};
+    if (!fused_append) {
+      e = launch_append_mfma(view(cache), ap->k, ap->v, ap->slots, ap->n, R_k, R_v, ap->mu_rk, ap->clip_k, ap->clip_v,
+                             stream);
+      if (e != hipSuccess) return hip_status(e, "append_decode/append");
+    }
+  }
   if (plan.variant != 2) {
     e = launch_qrot(a, stream);
     if (e != hipSuccess) return hip_status(e, "decode/qrot");
   } else {
-    e = launch_qprep(a, stream);
+    e = launch_qprep(a, fused_append ? &apa : nullptr, stream);
     if (e != hipSuccess) return hip_status(e, "decode/qprep");
   }
   // the measurement events (if set) ride on the scan's own dispatch: they mark its start and end
@@ -304,6 +338,37 @@ int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int n
     if (e != hipSuccess) return hip_status(e, "decode/wo");
   }
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int int2kv_decode(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
+                  const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens, int max_ctx,
+                  const float* R_k, const float* R_v, const uint16_t* W_o, int d_model, int wo_format, float* out,
+                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return decode_impl(cache, q, batch, num_q_heads, block_table, max_blocks_per_seq, ctx_lens, max_ctx, R_k, R_v, W_o,
+                     d_model, wo_format, out, workspace, workspace_bytes, stream, nullptr);
+}
+
+int int2kv_append_decode(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v, const int32_t* slot_mapping,
+                         int num_tokens, const float* mu_rk, float clip_k, float clip_v, const uint16_t* q, int batch,
+                         int num_q_heads, const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens,
+                         int max_ctx, const float* R_k, const float* R_v, const uint16_t* W_o, int d_model,
+                         int wo_format, float* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (int st = check_cache(cache)) return st;
+  if (num_tokens < 0) return fail(INT2KV_EINVAL, "num_tokens must be >= 0");
+  AppendStage ap;
+  if (num_tokens > 0) {
+    if (!k || !v || !slot_mapping || !R_k || !R_v || !mu_rk) return fail(INT2KV_EINVAL, "NULL pointer argument");
+    if (!valid_clip(clip_k) || !valid_clip(clip_v)) return fail(INT2KV_EINVAL, "clip ratios must be in (0, 1]");
+    if (!aligned(k, 16) || !aligned(v, 16) || !aligned(R_k, 16) || !aligned(R_v, 16) || !aligned(mu_rk, 16))
+      return fail(INT2KV_EINVAL, "k, v, R_k, R_v and mu_rk must be 16-byte aligned");
+    ap = AppendStage{k, v, slot_mapping, num_tokens, mu_rk, clip_k, clip_v};
+  }
+  return decode_impl(cache, q, batch, num_q_heads, block_table, max_blocks_per_seq, ctx_lens, max_ctx, R_k, R_v, W_o,
+                     d_model, wo_format, out, workspace, workspace_bytes, stream, &ap);
 }
 
 }  // extern "C"

@@ -1,0 +1,299 @@
+// Append on the matrix cores (shared by the append kernel and the decode's preparation kernel).
+#pragma once
+#include "common.h"
+#include "kernels.h"
+
+namespace int2kv {
+
+// Append on the matrix cores: x R (x bf16 [n, H, 128], R fp32 [128, 128]) as bf16 MFMA with R split
+// into three bf16 terms (R = R_1 + R_2 + R_3 + O(2^-27 |R|): every product is exact and the sum is
+// an fp32 accumulation, like an fp32 GEMM), starting from - mu R_K for keys; then the group
+// quantizer and the packed stores. Work-group (KV head h, K or V, a stride of 16-token
+// tiles); R^T of the work-group's (h, K|V) is converted once into LDS as the B operand.
+// Tile layout: the product is formed transposed, D^T = R^T x^T, with R^T fragments as the A operand
+// and token rows as the B operand. D^T[channel][token] of m-tile p (channels 16p .. 16p + 15) sits
+// in lane token + 16 ((channel % 16) / 4), register channel % 4: lane (token, hi) holds channels
+// 16 p + 4 hi + j, so register j of tiles p = 0..7 gives the eight 2-bit codes of half 4 hi + j of
+// the packed layout, and the 32 channels of group g (tiles 2g, 2g + 1) sit in the four lanes of
+// one token, eight in each. The group parameters are then computed once per (token, group).
+typedef __bf16 ap_bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float ap_f4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kApWaves = 8;
+constexpr int kApDepth = 6;   // R^T fragments in flight
+constexpr int kApRow = 144;   // bf16 per LDS row of R^T (128 + 16 pad: conflict-free 16-byte reads)
+
+// x / 3 correctly rounded, as a product with RN(1/3) and one FMA correction: checked against the
+// correctly rounded quotient for every fp32 significand (so for every x whose intermediate values
+// stay normal: x == 0 or x >= 2^-100; the caller routes other x to a division).
+__device__ __forceinline__ float div3_rn(float x) {
+#pragma clang fp contract(off)
+  const float c = 0x1.555556p-2f;  // RN(1/3)
+  const float q0 = x * c;
+  const float r = __builtin_fmaf(-q0, 3.0f, x);
+  return __builtin_fmaf(r, c, q0);
+}
+
+// The quantizer's group parameters (bit-identical to int2_group_params): s = fp16((mx - mn) / 3)
+// with the division above, and 1/s from a table of the correctly rounded reciprocals of the 1024
+// normal fp16 significands (exact after the power-of-two scaling); zero, fp16-subnormal and
+// infinite scales and tiny ranges take the division.
+__device__ __forceinline__ void int2_group_params_fast(float mn, float mx, float clip, const float* recip_tab,
+                                                       uint32_t& s_bits, uint32_t& z_bits, float& zf, float& inv) {
+#pragma clang fp contract(off)
+  if (clip != 1.0f) {
+    mn = clip * mn;
+    mx = clip * mx;
+  }
+  const float range = mx - mn;
+  float s32;
+  if (range != 0.0f && range < 0x1p-100f)
+    s32 = range / 3.0f;
+  else
+    s32 = div3_rn(range);
+  const __half s = __float2half_rn(s32);
+  const __half z = __float2half_rn(mn);
+  s_bits = __half_as_ushort(s);
+  z_bits = __half_as_ushort(z);
+  zf = __half2float(z);
+  const uint32_t e16 = (s_bits >> 10) & 31u;
+  if (e16 == 0u || e16 == 31u) {  // zero, fp16-subnormal or infinite scale
+    const float sf = __half2float(s);
+    inv = sf > 0.0f ? 1.0f / sf : 0.0f;
+  } else {
+    inv = __builtin_ldexpf(recip_tab[s_bits & 1023u], 15 - (int)e16);
+  }
+}
+
+// Packed output of one lane for one 16-token tile: halves 4 hi .. 4 hi + 3 of its token (two per
+// word) and the scale / zero of group hi.
+struct ApOut {
+  uint32_t w01, w23, meta;
+};
+
+// Group quantizer of one 16-token tile held in the transposed layout above.
+__device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float clip, const float* recip_tab, int lo,
+                                               int hi) {
+  // group g = tiles 2g, 2g + 1: lane-local min/max of its eight values, then a reduce-scatter
+  // over the four lanes of the token (xor 32, then xor 16) leaves group hi's extremes in lane hi
+  const bool h1 = (hi & 2) != 0, h0 = (hi & 1) != 0;
+  float pmn[4], pmx[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    float a = __builtin_fminf(acc[2 * g][0], acc[2 * g][1]), b = __builtin_fmaxf(acc[2 * g][0], acc[2 * g][1]);
+    a = __builtin_fminf(a, __builtin_fminf(acc[2 * g][2], acc[2 * g][3]));
+    b = __builtin_fmaxf(b, __builtin_fmaxf(acc[2 * g][2], acc[2 * g][3]));
+    a = __builtin_fminf(a, __builtin_fminf(acc[2 * g + 1][0], acc[2 * g + 1][1]));
+    b = __builtin_fmaxf(b, __builtin_fmaxf(acc[2 * g + 1][0], acc[2 * g + 1][1]));
+    pmn[g] = __builtin_fminf(a, __builtin_fminf(acc[2 * g + 1][2], acc[2 * g + 1][3]));
+    pmx[g] = __builtin_fmaxf(b, __builtin_fmaxf(acc[2 * g + 1][2], acc[2 * g + 1][3]));
+  }
+  float mn, mx;
+  {
+    // keep groups 2 h1, 2 h1 + 1, send the other two to the lane 32 away
+    const float sn0 = h1 ? pmn[0] : pmn[2], sn1 = h1 ? pmn[1] : pmn[3];
+    const float sx0 = h1 ? pmx[0] : pmx[2], sx1 = h1 ? pmx[1] : pmx[3];
+    float kn0 = h1 ? pmn[2] : pmn[0], kn1 = h1 ? pmn[3] : pmn[1];
+    float kx0 = h1 ? pmx[2] : pmx[0], kx1 = h1 ? pmx[3] : pmx[1];
+    kn0 = __builtin_fminf(kn0, __shfl_xor(sn0, 32));
+    kn1 = __builtin_fminf(kn1, __shfl_xor(sn1, 32));
+    kx0 = __builtin_fmaxf(kx0, __shfl_xor(sx0, 32));
+    kx1 = __builtin_fmaxf(kx1, __shfl_xor(sx1, 32));
+    // keep group 2 h1 + h0, send the other to the lane 16 away
+    mn = __builtin_fminf(h0 ? kn1 : kn0, __shfl_xor(h0 ? kn0 : kn1, 16));
+    mx = __builtin_fmaxf(h0 ? kx1 : kx0, __shfl_xor(h0 ? kx0 : kx1, 16));
+  }
+  uint32_t s_bits, z_bits;
+  float zf, inv;
+  int2_group_params_fast(mn, mx, clip, recip_tab, s_bits, z_bits, zf, inv);
+  // every lane of the token gathers the four groups' zero and reciprocal scale
+  float zg[4], ig[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    zg[g] = __shfl(zf, lo + 16 * g);
+    ig[g] = __shfl(inv, lo + 16 * g);
+  }
+  // codes: half 4 hi + j of the token collects tiles p = 0..7 of register j at bits 2p, summed as
+  // exact small integers in fp32
+  float hf[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int p = 0; p < 8; ++p)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma clang fp contract(off)
+      const float t = (acc[p][j] - zg[p >> 1]) * ig[p >> 1];
+      const float c = __builtin_rintf(__builtin_amdgcn_fmed3f(t, 0.0f, 3.0f));
+      hf[j] = __builtin_fmaf(c, (float)(1 << (2 * p)), hf[j]);
+    }
+  const uint32_t q0 = (uint32_t)hf[0], q1 = (uint32_t)hf[1], q2 = (uint32_t)hf[2], q3 = (uint32_t)hf[3];
+  return ApOut{q0 | (q1 << 16), q2 | (q3 << 16), s_bits | (z_bits << 16)};
+}
+
+// Stores of one lane's ApOut into the record of its token's slot (skipped for slots out of range).
+__device__ __forceinline__ void store_tile(const ApOut& o, int slot, const CacheView& cv, int h, int kv, int nslots,
+                                           int hi) {
+  if (slot >= 0 && slot < nslots) {
+    const int blk = slot >> 4, t = slot & 15;
+    uint8_t* rec = cv.pool + ((size_t)blk * cv.num_kv_heads + h) * kRecord;
+    if (kv == 0) {
+      *reinterpret_cast<uint2*>(rec + kOffKCodes + 32 * t + 8 * hi) = make_uint2(o.w01, o.w23);
+      *reinterpret_cast<uint32_t*>(rec + kOffKMeta + 16 * t + 4 * hi) = o.meta;
+    } else {
+      uint8_t* vc = rec + kOffVCodes + 32 * 4 * hi + 2 * t;
+      *reinterpret_cast<uint16_t*>(vc) = (uint16_t)o.w01;
+      *reinterpret_cast<uint16_t*>(vc + 32) = (uint16_t)(o.w01 >> 16);
+      *reinterpret_cast<uint16_t*>(vc + 64) = (uint16_t)o.w23;
+      *reinterpret_cast<uint16_t*>(vc + 96) = (uint16_t)(o.w23 >> 16);
+      *reinterpret_cast<uint16_t*>(rec + kOffVScale + 32 * hi + 2 * t) = (uint16_t)o.meta;
+      *reinterpret_cast<uint16_t*>(rec + kOffVZero + 32 * hi + 2 * t) = (uint16_t)(o.meta >> 16);
+    }
+  }
+}
+
+// Each wave takes kApTiles consecutive 16-token tiles per step, so every R^T fragment read from
+// LDS feeds kApTiles products (two for long appends; one for short ones, which spreads the few
+// tiles over more waves).
+// LDS of one append work-group: R^T as three bf16 terms, then the reciprocal table.
+constexpr int kAppendLdsBytes = 3 * kHeadDim * kApRow * 2 + 1024 * 4;
+
+// One append work-group of kWaves waves: KV head h, K (kv = 0) or V (kv = 1), block bx of nbx
+// striding over the 16-token tiles; lds holds kAppendLdsBytes (16-byte aligned). Every thread of
+// the block must call it (it synchronizes once).
+template <int kApTiles, int kWaves>
+__device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t* __restrict__ k,
+                                             const uint16_t* __restrict__ v, const int32_t* __restrict__ slots,
+                                             int n, const float* __restrict__ R_k, const float* __restrict__ R_v,
+                                             const float* __restrict__ mu_rk, float clip_k, float clip_v, int bx,
+                                             int nbx, int h, int kv, uint8_t* lds) {
+  uint16_t(*rt)[kHeadDim][kApRow] = reinterpret_cast<uint16_t(*)[kHeadDim][kApRow]>(lds);  // [term][c][i] = R[i][c]
+  float* recip_tab = reinterpret_cast<float*>(lds + 3 * kHeadDim * kApRow * 2);  // RN(1 / (1 + m / 1024))
+  const int H = cv.num_kv_heads, tid = threadIdx.x;
+  const float* R = (kv == 0 ? R_k : R_v) + (size_t)h * kHeadDim * kHeadDim;
+  const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
+  const uint16_t* X = kv == 0 ? k : v;
+  constexpr int kStep = 16 * kApTiles;  // tokens per wave step
+  // the first step's operands and slots are fetched before R, so their latency overlaps R's
+  const int step0 = bx * kWaves + w;
+  ap_bf16x8_t X8[kApTiles][4];
+  int slot[kApTiles];
+#pragma unroll
+  for (int u = 0; u < kApTiles; ++u) {
+    const int tok = step0 * kStep + 16 * u + lo, tc = min(tok, n - 1);
+    const uint16_t* xrow = X + ((size_t)tc * H + h) * kHeadDim + 8 * hi;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) X8[u][ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
+    slot[u] = slots[tc];
+    if (tok >= n) slot[u] = -1;
+  }
+  {
+    // R^T as three bf16 terms: thread (c, i0) reads R[i0 .. i0 + 7][c] (coalesced over c) and
+    // splits each value by truncation: r = t0 + t1 + t2 exactly (t0 and t1 take the leading 8
+    // significant bits of r and of r - t0, the remainder has at most 8 left), then writes one
+    // 16-byte row piece per term (conflict-free)
+    constexpr int kIb = kWaves / 2;  // threads per channel c
+    const int c = tid & 127, ib = tid >> 7;
+#pragma unroll
+    for (int u = 0; u < 16 / kIb; ++u) {
+      const int i0 = 8 * (ib + kIb * u);
+      uint32_t t16[3][8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float r = R[(i0 + q) * kHeadDim + c];
+        const uint32_t b0 = __float_as_uint(r) & 0xFFFF0000u;
+        const float r1 = r - __uint_as_float(b0);
+        const uint32_t b1 = __float_as_uint(r1) & 0xFFFF0000u;
+        const float r2 = r1 - __uint_as_float(b1);
+        t16[0][q] = b0 >> 16;
+        t16[1][q] = b1 >> 16;
+        t16[2][q] = __float_as_uint(r2) >> 16;
+      }
+#pragma unroll
+      for (int term = 0; term < 3; ++term)
+        *reinterpret_cast<uint4*>(&rt[term][c][i0]) =
+            make_uint4(t16[term][0] | (t16[term][1] << 16), t16[term][2] | (t16[term][3] << 16),
+                       t16[term][4] | (t16[term][5] << 16), t16[term][6] | (t16[term][7] << 16));
+    }
+  }
+  for (int m = tid; m < 1024; m += 64 * kWaves) recip_tab[m] = 1.0f / (1.0f + (float)m * 0x1p-10f);
+  __syncthreads();
+  // lane (token lo, hi) holds channels 16 p + 4 hi + j of its token in register j of tile p
+  ap_f4_t sub[8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p)
+    sub[p] = kv == 0 ? -*reinterpret_cast<const ap_f4_t*>(mu_rk + (size_t)h * kHeadDim + 16 * p + 4 * hi)
+                     : ap_f4_t{0.f, 0.f, 0.f, 0.f};
+  const float clip = kv == 0 ? clip_k : clip_v;
+  const int nslots = cv.num_blocks * kBlock;
+  // software pipeline over the wave's steps: the next step's operands and slots are fetched while
+  // this one is computed (indexes clamped, so the fetch past the last step stays in bounds)
+  const int sstride = nbx * kWaves;
+  for (int st = step0; st * kStep < n; st += sstride) {
+    ap_bf16x8_t Xn[kApTiles][4];
+    int slotn[kApTiles];
+#pragma unroll
+    for (int u = 0; u < kApTiles; ++u) {
+      const int tok = (st + sstride) * kStep + 16 * u + lo, tc = min(tok, n - 1);
+      const uint16_t* xrow = X + ((size_t)tc * H + h) * kHeadDim + 8 * hi;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) Xn[u][ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
+      slotn[u] = slots[tc];
+    }
+    ap_f4_t acc[kApTiles][8];  // start at - mu R_K (keys) or 0 (values)
+#pragma unroll
+    for (int u = 0; u < kApTiles; ++u)
+#pragma unroll
+      for (int p = 0; p < 8; ++p) acc[u][p] = sub[p];
+    // the R^T fragments are the same for every step: an opaque offset keeps the compiler from
+    // hoisting all 96 of them into registers (which would cap occupancy at one wave per SIMD)
+    int boff = (lo * kApRow + 8 * hi) * 2;
+    asm volatile("" : "+v"(boff));
+    const uint8_t* rb = reinterpret_cast<const uint8_t*>(&rt[0][0][0]) + boff;
+    // fragment f = (term 2 - f / 32, k-step (f / 8) % 4, m-tile f % 8): smallest term first. The
+    // LDS reads run kApDepth fragments ahead of the matrix cores (the schedule is pinned below).
+    auto frag = [&](int f) {
+      const int term = 2 - f / 32, ks = (f / 8) % 4, p = f % 8;
+      return *reinterpret_cast<const ap_bf16x8_t*>(rb + ((term * kHeadDim + 16 * p) * kApRow + 32 * ks) * 2);
+    };
+    ap_bf16x8_t fr[kApDepth];
+#pragma unroll
+    for (int f = 0; f < kApDepth; ++f) fr[f] = frag(f);
+#pragma unroll
+    for (int f = 0; f < 96; ++f) {
+      const ap_bf16x8_t a = fr[f % kApDepth];
+      const int ks = (f / 8) % 4, p = f % 8;
+#pragma unroll
+      for (int u = 0; u < kApTiles; ++u)
+        acc[u][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, X8[u][ks], acc[u][p], 0, 0, 0);
+      if (f + kApDepth < 96) fr[f % kApDepth] = frag(f + kApDepth);
+    }
+#pragma unroll
+    for (int f = 0; f < kApDepth; ++f) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+#pragma unroll
+    for (int f = 0; f < 96; ++f) {
+      __builtin_amdgcn_sched_group_barrier(0x008, kApTiles, 0);  // MFMA
+      if (f + kApDepth < 96) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    ApOut out[kApTiles];
+#pragma unroll
+    for (int u = 0; u < kApTiles; ++u) out[u] = quantize_tile(acc[u], clip, recip_tab, lo, hi);
+    // the next step's loads are waited for here, before this step's stores: a wait placed after
+    // the (lane-conditional) stores would also wait for the stores to complete
+#pragma unroll
+    for (int u = 0; u < kApTiles; ++u) {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) asm volatile("" : "+v"(Xn[u][ks])::"memory");
+      asm volatile("" : "+v"(slotn[u])::"memory");
+    }
+#pragma unroll
+    for (int u = 0; u < kApTiles; ++u) store_tile(out[u], slot[u], cv, h, kv, nslots, hi);
+#pragma unroll
+    for (int u = 0; u < kApTiles; ++u) {
+      const int tok = (st + sstride) * kStep + 16 * u + lo;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) X8[u][ks] = Xn[u][ks];
+      slot[u] = tok < n ? slotn[u] : -1;
+    }
+  }
+}
+
+}  // namespace int2kv

@@ -15,6 +15,7 @@
 // are folded into the query operand (scaled by 2^e per channel, with sum_k A_k subtracted through
 // the accumulator's initial value); for the values they are removed from the accumulator at the
 // end (O = 2^e (D - sum_t w_t)), using the exact fp16 weights the matrix core multiplied.
+#include "append_core.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -100,11 +101,14 @@ constexpr int kQpSeqs = 8;
 constexpr int kQpRow = 136;  // bf16 per LDS row of R^T (128 + 8 pad: conflict-free 16-byte reads)
 typedef __bf16 qp_bf16x8_t __attribute__((ext_vector_type(8)));
 
-__device__ void qprep_block(const DecodeArgs& a, int blk, bool wide) {
-  __shared__ __attribute__((aligned(16))) uint16_t Rt[2][kHeadDim][kQpRow];     // [hi, lo][c][k] = R[k][c]
-  __shared__ __attribute__((aligned(16))) float qb[8 * kQpSeqs][kHeadDim + 4];  // q' rows
-  __shared__ int smax[8 * kQpSeqs];
-  __shared__ float sig[8 * kQpSeqs];
+// LDS of the query-operand role: R^T as bf16 hi / lo, the q' rows, per-row max and scale.
+constexpr int kQpLdsBytes = 2 * kHeadDim * kQpRow * 2 + 8 * kQpSeqs * (kHeadDim + 4) * 4 + 2 * 8 * kQpSeqs * 4;
+
+__device__ void qprep_block(const DecodeArgs& a, int blk, bool wide, uint8_t* lds) {
+  uint16_t(*Rt)[kHeadDim][kQpRow] = reinterpret_cast<uint16_t(*)[kHeadDim][kQpRow]>(lds);  // [hi, lo][c][k] = R[k][c]
+  float(*qb)[kHeadDim + 4] = reinterpret_cast<float(*)[kHeadDim + 4]>(lds + 2 * kHeadDim * kQpRow * 2);  // q' rows
+  int* smax = reinterpret_cast<int*>(lds + 2 * kHeadDim * kQpRow * 2 + 8 * kQpSeqs * (kHeadDim + 4) * 4);
+  float* sig = reinterpret_cast<float*>(smax + 8 * kQpSeqs);
   const int H = a.H, gq = a.gq, tid = threadIdx.x;
   const int h = blk % H, b0 = kQpSeqs * (blk / H), nseq = min(kQpSeqs, a.B - b0);
   const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
@@ -576,8 +580,9 @@ constexpr int kSegCost = 6;
 // is the last one with x(g) <= c0 + kSegCost, the one holding its last page the last with
 // x(g) <= c1 - 1. Every group below G starts in exactly one span (the spans tile [0, W)), so every
 // entry is written once, by the thread owning that sequence. One block of 256 threads.
-__device__ void page_prefix_block(const DecodeArgs& a) {
-  __shared__ int sums[256], cnts[256];
+__device__ void page_prefix_block(const DecodeArgs& a, uint8_t* lds) {
+  int* sums = reinterpret_cast<int*>(lds);
+  int* cnts = sums + 256;
   const int tid = threadIdx.x;
   const int per = (a.B + 255) / 256;
   const int b0 = min(a.B, tid * per), b1 = min(a.B, b0 + per);
@@ -633,8 +638,8 @@ __device__ void page_prefix_block(const DecodeArgs& a) {
 // address of block 0, for a block id outside the pool).
 constexpr int kPlPages = 1024;
 
-__device__ void page_list_block(const DecodeArgs& a, int b, int p0) {
-  __shared__ int red[256];
+__device__ void page_list_block(const DecodeArgs& a, int b, int p0, uint8_t* lds) {
+  int* red = reinterpret_cast<int*>(lds);
   const int tid = threadIdx.x;
   const int L = seq_len_m(a, b), np = (L + kBlock - 1) >> 4;
   if (p0 >= np) return;  // uniform over the block
@@ -667,17 +672,29 @@ __device__ void page_list_block(const DecodeArgs& a, int b, int p0) {
   }
 }
 
-// Block 0: page prefix sums (first, so it never waits for a free slot); blocks 1 .. nq: query
-// operands of KV head h for kQpSeqs sequences; the rest: the page list, kPlPages pages of one
-// sequence per block (nseg blocks per sequence).
-__global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int wide, int nq, int nseg) {
-  const int blk = blockIdx.x;
+// Blocks 0 .. nap - 1 (int2kv_append_decode): the cache write of the current tokens, one block per
+// (block of ap.nbx, KV head, K|V), four waves; it runs beside the roles below, which do not read
+// the cache. Then block nap: page prefix sums; nap + 1 .. nap + nq: query operands of KV head h for
+// kQpSeqs sequences; the rest: the page list, kPlPages pages of one sequence per block (nseg blocks
+// per sequence). Lower block ids are dispatched first. The roles share one LDS buffer.
+constexpr int kPrepLdsBytes = kAppendLdsBytes > kQpLdsBytes ? kAppendLdsBytes : kQpLdsBytes;
+
+__global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int wide, int nq, int nseg, AppendArgs ap, int nap) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kPrepLdsBytes];
+  int blk = blockIdx.x;
+  if (blk < nap) {
+    const int bx = blk % ap.nbx, r = blk / ap.nbx;
+    append_block<1, 4>(ap.cv, ap.k, ap.v, ap.slots, ap.n, ap.R_k, ap.R_v, ap.mu_rk, ap.clip_k, ap.clip_v, bx, ap.nbx,
+                       r % ap.cv.num_kv_heads, r / ap.cv.num_kv_heads, lds);
+    return;
+  }
+  blk -= nap;
   if (blk == 0)
-    page_prefix_block(a);
+    page_prefix_block(a, lds);
   else if (blk <= nq)
-    qprep_block(a, blk - 1, wide != 0);
+    qprep_block(a, blk - 1, wide != 0, lds);
   else
-    page_list_block(a, (blk - 1 - nq) / nseg, ((blk - 1 - nq) % nseg) * kPlPages);
+    page_list_block(a, (blk - 1 - nq) / nseg, ((blk - 1 - nq) % nseg) * kPlPages, lds);
 }
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -1068,13 +1085,21 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
     store_head_out(val, out, ob, fmt, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c, (size_t)a.B * a.Hq * kHeadDim);
 }
 
-hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s) {
+hipError_t launch_qprep(const DecodeArgs& a, const AppendArgs* ap, hipStream_t s) {
   if (a.gq > 8) return hipErrorNotSupported;
+  AppendArgs none{};
+  int nap = 0;
+  if (ap && ap->n > 0) {
+    none = *ap;
+    none.nbx = (ap->n + 16 * 4 - 1) / (16 * 4);  // one 16-token tile per wave and step
+    nap = none.nbx * ap->cv.num_kv_heads * 2;
+  }
   const int nq = a.H * ((a.B + kQpSeqs - 1) / kQpSeqs);
   const long long maxlen = min((long long)a.max_ctx, (long long)a.max_blocks * kBlock);
   const int maxp = (int)((maxlen + kBlock - 1) / kBlock);
   const int nseg = max(1, (maxp + kPlPages - 1) / kPlPages);
-  hipLaunchKernelGGL(qprep_kernel, dim3(1 + nq + a.B * nseg), dim3(256), 0, s, a, a.gq > 4 ? 1 : 0, nq, nseg);
+  hipLaunchKernelGGL(qprep_kernel, dim3(nap + 1 + nq + a.B * nseg), dim3(256), 0, s, a, a.gq > 4 ? 1 : 0, nq, nseg,
+                     none, nap);
   return hipGetLastError();
 }
 

@@ -61,7 +61,18 @@ constexpr int kPartStride = 132;  // m, l, 2 pad, O[128]
 hipError_t launch_qrot(const DecodeArgs& a, hipStream_t s);
 // ev0 / ev1 (may be null): events that track the scan kernel's own start and end
 hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
-hipError_t launch_qprep(const DecodeArgs& a, hipStream_t s);
+// Cache write of the current tokens run inside the preparation launch (int2kv_append_decode).
+struct AppendArgs {
+  CacheView cv;
+  const uint16_t *k, *v;
+  const int32_t* slots;
+  int n;
+  const float *R_k, *R_v, *mu_rk;
+  float clip_k, clip_v;
+  int nbx;  // blocks per (KV head, K|V), set by the launcher
+};
+// ap (may be null): the cache write to run beside the query preparation
+hipError_t launch_qprep(const DecodeArgs& a, const AppendArgs* ap, hipStream_t s);
 hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 size_t qop_bytes(int B, int H, int gq);
 // Head-output formats of the merges: fp32 to `out`, or for the output projection (to `ob`) two bf16

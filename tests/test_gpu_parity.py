@@ -208,3 +208,47 @@ def test_out_of_range_blocks_and_lengths_are_clamped():
     Vt = O.dequantize(vc, vs, vz)[keep] @ w.R_v[0].astype(np.float64).T
     ref0 = O.softmax_attention(O.bf16_to_f64(w.q)[0], Kt, Vt)
     assert_rows_close(out[0], ref0, what="skipped block")
+
+
+@pytest.mark.parametrize("variant", [1, 2])
+def test_append_decode_matches_separate_calls_and_oracle(variant):
+    """int2kv_append_decode (cache write on the side stream beside the query preparation) leaves the
+    same pool bytes and outputs as int2kv_quantize_append followed by int2kv_decode, and its output
+    matches the oracle's decode of the pool it wrote."""
+    print(f"\n[append_decode] variant={variant}", flush=True)
+    K.int2kv_set_decode_tuning(0, variant)
+    lens = np.array([300, 17, 1, 129, 64])
+    Hq, H, dm = 40, 8, 256
+    w = W.make_workload(4, batch=lens.size, ctx_lens=lens, num_q_heads=Hq, num_kv_heads=H, d_model=dm)
+    Rk, Rv = dev(w.R_k), dev(w.R_v)
+    mu_rk = K.int2kv_prepare_mu_rot(Rk, dev(w.mu))
+    caches = [K.Int2KVCache(w.num_blocks, H) for _ in range(2)]
+    k_last, v_last, s_last = [], [], []
+    for b in range(w.batch):
+        k, v = w.kv(b, as_torch=True)
+        L = int(lens[b])
+        slots = w.slot_mapping(b)
+        if L > 1:
+            for c in caches:
+                K.int2kv_quantize_append(c, k[:L - 1].cuda(), v[:L - 1].cuda(), dev(slots[:L - 1]), Rk, Rv, mu_rk)
+        k_last.append(k[L - 1])
+        v_last.append(v[L - 1])
+        s_last.append(slots[L - 1])
+    kl, vl = torch.stack(k_last).cuda(), torch.stack(v_last).cuda()
+    sl = dev(np.array(s_last, np.int32))
+    Wp = K.int2kv_prepare_wo(dev(w.W_o), Rv, Hq)
+    dargs = (dev(w.q), dev(w.block_table), dev(w.ctx_lens), int(lens.max()), Rk, Rv)
+    K.int2kv_quantize_append(caches[0], kl, vl, sl, Rk, Rv, mu_rk)
+    y0 = K.int2kv_decode(caches[0], *dargs, W_o=Wp, wo_format=K.INT2KV_WO_PREPARED_FOLDED, d_model=dm)
+    y1 = K.int2kv_append_decode(caches[1], kl, vl, sl, mu_rk, *dargs, W_o=Wp,
+                                wo_format=K.INT2KV_WO_PREPARED_FOLDED, d_model=dm)
+    torch.cuda.synchronize()
+    assert torch.equal(caches[0].pool, caches[1].pool)
+    assert torch.equal(y0, y1)
+    ref = O.decode(caches[1].pool.cpu().numpy(), w.q, w.block_table, w.ctx_lens, w.R_k, w.R_v, w.W_o)
+    worst = assert_rows_close(y1.cpu().numpy(), ref, what="append_decode")
+    # no new tokens: the plain decode
+    y2 = K.int2kv_append_decode(caches[1], kl[:0], vl[:0], sl[:0], mu_rk, *dargs, W_o=Wp,
+                                wo_format=K.INT2KV_WO_PREPARED_FOLDED, d_model=dm)
+    assert torch.equal(y2, y1)
+    print(f"worst row error {worst:.2e}", flush=True)
