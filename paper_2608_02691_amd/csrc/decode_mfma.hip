@@ -1006,7 +1006,10 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
     osum[jj] = 0.0f;
   }
   for (int gg = ga + sl; gg <= gb; gg += kMergeSlots) {
-    if (a.wg_info[4 * gg + 3] >= a.wg_info[4 * gg + 7]) continue;  // empty range wrote nothing
+    // the range bounds and the partial are loaded together (one round trip): slot gg + b exists for
+    // every group, and an empty range (which wrote nothing, so the slot holds stale values) is
+    // dropped by selects below, never multiplied
+    const int r0 = a.wg_info[4 * gg + 3], r1 = a.wg_info[4 * gg + 7];
     const float* base = a.part + ((size_t)(gg + b) * a.Hq + h * gq) * kPartStride;
     float mv[8], lv[8], ov[8];
 #pragma unroll
@@ -1016,15 +1019,16 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
       lv[jj] = pp[1];
       ov[jj] = pp[4 + c];
     }
+    const bool nonempty = r0 < r1;
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) {
       // a partial with no cached token has m = -inf (or the scan's finite floor) and l = 0
-      const bool valid = mv[jj] != -INFINITY;
+      const bool valid = nonempty && mv[jj] != -INFINITY;
       const float Mn = valid ? fmaxf(M[jj], mv[jj]) : M[jj];
       const float fa = valid ? __builtin_amdgcn_exp2f(M[jj] - Mn) : 1.0f;
       const float fb = valid ? __builtin_amdgcn_exp2f(mv[jj] - Mn) : 0.0f;
-      lsum[jj] = fmaf(lsum[jj], fa, fb * lv[jj]);
-      osum[jj] = fmaf(osum[jj], fa, fb * ov[jj]);
+      lsum[jj] = fmaf(lsum[jj], fa, valid ? fb * lv[jj] : 0.0f);
+      osum[jj] = fmaf(osum[jj], fa, valid ? fb * ov[jj] : 0.0f);
       M[jj] = Mn;
     }
   }
