@@ -985,10 +985,10 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
 // Block (sequence, KV head) of kMergeSlots x 128 threads: slot s merges the work-groups ga + s,
 // ga + s + kMergeSlots, ... (one round of loads for up to kMergeSlots work-groups), thread c of a
 // slot owns channel c; the slots are then combined in a fixed order through LDS (deterministic),
-// thread (c, s) finishing query head s. The un-rotation has the 128 threads of slot 0 share one
+// thread (c, s) finishing query heads s, s + kMergeSlots, ... The un-rotation has the 128 threads of slot 0 share one
 // pass over R_V (row c of R_V per thread) for all query heads.
-constexpr int kMergeSlots = 8;
 
+template <int kMergeSlots>
 __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArgs a, int G, int unrotate,
                                                                        float* __restrict__ out,
                                                                        uint16_t* __restrict__ ob, int fmt) {
@@ -1042,22 +1042,27 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
 #pragma unroll
   for (int jj = 0; jj < 8; ++jj) os[sl][jj][c] = osum[jj];
   __syncthreads();
-  // thread (c, s): query head s, channel c, the slots in a fixed order
-  const int jj = sl;
-  float Mx = -INFINITY;
+  // thread (c, s): query heads s, s + kMergeSlots, ..., channel c, the slots in a fixed order
+  float val[8 / kMergeSlots];
 #pragma unroll
-  for (int t = 0; t < kMergeSlots; ++t) Mx = fmaxf(Mx, ms[t][jj]);
-  float L = 0.0f, O = 0.0f;
+  for (int r = 0; r < 8 / kMergeSlots; ++r) {
+    const int jj = sl + kMergeSlots * r;
+    float Mx = -INFINITY;
 #pragma unroll
-  for (int t = 0; t < kMergeSlots; ++t) {
-    const float mt = ms[t][jj];
-    const float f = mt == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mt - Mx);
-    L = fmaf(f, ls[t][jj], L);
-    O = fmaf(f, os[t][jj][c], O);
+    for (int t = 0; t < kMergeSlots; ++t) Mx = fmaxf(Mx, ms[t][jj]);
+    float L = 0.0f, O = 0.0f;
+#pragma unroll
+    for (int t = 0; t < kMergeSlots; ++t) {
+      const float mt = ms[t][jj];
+      const float f = mt == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mt - Mx);
+      L = fmaf(f, ls[t][jj], L);
+      O = fmaf(f, os[t][jj][c], O);
+    }
+    val[r] = L > 0.0f ? O / L : 0.0f;
   }
-  float val = L > 0.0f ? O / L : 0.0f;
   if (unrotate) {
-    vs[jj][c] = val;
+#pragma unroll
+    for (int r = 0; r < 8 / kMergeSlots; ++r) vs[sl + kMergeSlots * r][c] = val[r];
     __syncthreads();
     if (sl == 0) {
       const float4* row = reinterpret_cast<const float4*>(a.R_v + ((size_t)h * kHeadDim + c) * kHeadDim);
@@ -1085,8 +1090,13 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
     }
     return;
   }
-  if (jj < gq)
-    store_head_out(val, out, ob, fmt, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c, (size_t)a.B * a.Hq * kHeadDim);
+#pragma unroll
+  for (int r = 0; r < 8 / kMergeSlots; ++r) {
+    const int jj = sl + kMergeSlots * r;
+    if (jj < gq)
+      store_head_out(val[r], out, ob, fmt, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c,
+                     (size_t)a.B * a.Hq * kHeadDim);
+  }
 }
 
 hipError_t launch_qprep(const DecodeArgs& a, const AppendArgs* ap, hipStream_t s) {
@@ -1120,8 +1130,14 @@ hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s, hipEvent
 
 hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, uint16_t* ob, int fmt, hipStream_t s) {
   if (a.gq > 8) return hipErrorNotSupported;
-  hipLaunchKernelGGL(merge_flat_kernel, dim3(a.B, a.H), dim3(128 * kMergeSlots), 0, s, a, a.grid_g, unrotate ? 1 : 0,
-                     out, ob, fmt);
+  // four slots when many sequences share the work-groups (short spans; fewer idle waves to
+  // dispatch), eight for few, long sequences (fewer rounds of loads)
+  if (a.B >= 32)
+    hipLaunchKernelGGL(merge_flat_kernel<4>, dim3(a.B, a.H), dim3(128 * 4), 0, s, a, a.grid_g, unrotate ? 1 : 0, out,
+                       ob, fmt);
+  else
+    hipLaunchKernelGGL(merge_flat_kernel<8>, dim3(a.B, a.H), dim3(128 * 8), 0, s, a, a.grid_g, unrotate ? 1 : 0, out,
+                       ob, fmt);
   return hipGetLastError();
 }
 
