@@ -270,20 +270,14 @@ struct PairLoads {
 };
 
 // Page records are staged in LDS by the wave that consumes them, with LDS-DMA loads
-// (global_load_lds: lane i's bytes land at M0 + 16 i, or 4 i), so that several page pairs are in
-// flight per wave without holding registers. Each record is fetched whole: 1024 B of codes with one
-// dwordx4 load and 512 B of metadata with two dword loads. Issued through inline asm because the
-// compiler would otherwise wait for every outstanding DMA before any LDS read; the waits are
-// explicit instead (vmcnt counts this wave's DMA loads in issue order).
-__device__ __forceinline__ void dma16(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_addr), "v"(voff), "s"(base)
-               : "memory", "m0");
-}
-__device__ __forceinline__ void dma4(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds_addr), "v"(voff), "s"(base)
-               : "memory", "m0");
-}
-
+// (global_load_lds: lane i's bytes land at M0 + 16 i), so that several page pairs are in flight per
+// wave without holding registers. A pair takes three dwordx4 loads: the 1024 B of codes of each
+// page, then both pages' 512 B of metadata in one load (lanes 0..31 read page 0's, lanes 32..63
+// page 1's, through per-lane 64-bit addresses). Issued through inline asm because the compiler
+// would otherwise wait for every outstanding DMA before any LDS read; the waits are explicit instead
+// (vmcnt counts this wave's loads in issue order). Slot layout: codes of page 0 | codes of page 1 |
+// metadata of page 0 | metadata of page 1.
+constexpr int kDmaPerPair = 3;
 // Page list: one 16-byte entry per page of the concatenated sequences, written by the query-prep
 // kernel: {address of the page's record of KV head 0 (low, high word), cached tokens in the page,
 // 0}. A page whose block id lies outside the pool holds 0 tokens and points at block 0.
@@ -296,21 +290,25 @@ __device__ __forceinline__ PageEnt load_ent(ent_ptr p, int i) {
   return PageEnt{p[i].lo, p[i].hi, p[i].nv, 0u};
 }
 
-// DMA of one 1536-byte page record into LDS at lds_addr: the 1024 bytes of codes with one dwordx4
-// load, the two 256-byte metadata blocks with dword loads. (rec_lo, rec_hi) is the record of KV
-// head 0; the lane offsets voff16 = 16 l + 1536 h and voff4 = 4 l + 1536 h select head h. The
-// instruction offset moves both the global and the LDS address, so one M0 value serves the whole
-// record.
-__device__ __forceinline__ void dma_page(uint32_t rec_lo, uint32_t rec_hi, uint32_t lds_addr, uint32_t voff16,
-                                         uint32_t voff4) {
-  const uint8_t* rec = reinterpret_cast<const uint8_t*>(((uint64_t)rec_hi << 32) | rec_lo);
+// DMA of one page pair into the staging slot at lds_addr. (a_lo, a_hi), (b_lo, b_hi): records of KV
+// head 0 of the two pages; voff16 = 16 l + 1536 h selects head h for the codes; moff = (the record of
+// page 0 or, for lanes 32..63, page 1) + 1536 h + 1024 + 16 (l % 32) is the lane's metadata address.
+__device__ __forceinline__ void dma_pair(uint32_t a_lo, uint32_t a_hi, uint32_t b_lo, uint32_t b_hi, uint32_t lds_addr,
+                                         uint32_t voff16, uint64_t moff_head, bool upper) {
+  const uint8_t* ra = reinterpret_cast<const uint8_t*>(((uint64_t)a_hi << 32) | a_lo);
+  const uint8_t* rb = reinterpret_cast<const uint8_t*>(((uint64_t)b_hi << 32) | b_lo);
+  const uint64_t maddr = ((uint64_t)(upper ? b_hi : a_hi) << 32 | (upper ? b_lo : a_lo)) + moff_head;
   asm volatile(
       "s_mov_b32 m0, %0\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, %3\n\t"
-      "global_load_lds_dword %2, %3 offset:1024\n\t"
-      "global_load_lds_dword %2, %3 offset:1280" ::"s"(lds_addr),
-      "v"(voff16), "v"(voff4), "s"(rec)
+      "global_load_lds_dwordx4 %3, %4\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %3, %5\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %6, off" ::"s"(lds_addr),
+      "s"(lds_addr + 1024), "s"(lds_addr + 2048), "v"(voff16), "s"(ra), "s"(rb), "v"(maddr)
       : "memory", "m0");
 }
 
@@ -335,18 +333,19 @@ __device__ __forceinline__ void read_pair(const uint8_t* slot, uint32_t nv0, uin
                                           PairLoads<WIDE>& p) {
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
-    const uint8_t* rec = slot + P * kRecord;
+    const uint8_t* rec = slot + P * 1024;               // codes of page P (record offsets < 1024)
+    const uint8_t* met = slot + 2048 + P * 512 - 1024;  // metadata of page P (record offsets >= 1024)
     p.nv[P] = P == 0 ? nv0 : nv1;
     p.kc[P] = *reinterpret_cast<const uint2*>(rec + kOffKCodes + 32 * lo + 8 * hi);
-    p.km[P] = *reinterpret_cast<const uint4*>(rec + kOffKMeta + 16 * lo);
+    p.km[P] = *reinterpret_cast<const uint4*>(met + kOffKMeta + 16 * lo);
     p.vc[P] = *reinterpret_cast<const uint2*>(rec + kOffVCodes + 32 * lo + 8 * hi);
     if constexpr (WIDE) {
-      p.vs[P][0] = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (lo & 1) + 8 * hi);
-      p.vs[P][1] = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (2 + (lo & 1)) + 8 * hi);
+      p.vs[P][0] = *reinterpret_cast<const uint2*>(met + kOffVScale + 32 * (lo & 1) + 8 * hi);
+      p.vs[P][1] = *reinterpret_cast<const uint2*>(met + kOffVScale + 32 * (2 + (lo & 1)) + 8 * hi);
     } else {
-      p.vs[P][0] = *reinterpret_cast<const uint2*>(rec + kOffVScale + 32 * (lo & 3) + 8 * hi);
+      p.vs[P][0] = *reinterpret_cast<const uint2*>(met + kOffVScale + 32 * (lo & 3) + 8 * hi);
     }
-    p.vz[P] = *reinterpret_cast<const uint2*>(rec + kOffVZero + 32 * (lo & 3) + 8 * hi);
+    p.vz[P] = *reinterpret_cast<const uint2*>(met + kOffVZero + 32 * (lo & 3) + 8 * hi);
   }
 }
 template <int X>
@@ -754,7 +753,9 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   // ---- pipeline over the segment's page pairs (global pages gs + 2k, gs + 2k + 1; the second page
   // of a last pair of one page is a stand-in: block 0, no tokens). Pair k sits in slot k % kStages.
   const ent_ptr ent = (ent_ptr)(uintptr_t)(a.pages) + gs;
-  const uint32_t voff16 = 16 * l + h * kRecord, voff4 = 4 * l + h * kRecord;
+  const uint32_t voff16 = 16 * l + h * kRecord;
+  const uint64_t moff = (uint64_t)(h * kRecord + 1024 + 16 * (l & 31));
+  const bool upper = l >= 32;
   const uint32_t pool_lo = (uint32_t)(uintptr_t)a.pool, pool_hi = (uint32_t)((uintptr_t)a.pool >> 32);
   uint32_t nv[kStages][2];  // cached tokens of the two pages staged in each slot
   // entries of pair k with the bounds check of the last pair (paths outside the steady loop): both
@@ -771,8 +772,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   auto stage = [&](auto slot_tag, const PageEnt& e0, const PageEnt& e1) {
     constexpr int SL = decltype(slot_tag)::value;
     const uint32_t sa = stage_base + SL * 2 * kRecord;
-    dma_page(e0.lo, e0.hi, sa, voff16, voff4);
-    dma_page(e1.lo, e1.hi, sa + kRecord, voff16, voff4);
+    dma_pair(e0.lo, e0.hi, e1.lo, e1.hi, sa, voff16, moff, upper);
     nv[SL][0] = e0.nv;
     nv[SL][1] = e1.nv;
   };
@@ -797,7 +797,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   PairLoads<WIDE> X, Y;
   {
     if (kStages - 1 < npairs)
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * 2 * (kStages - 1)) : "memory");
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kDmaPerPair * (kStages - 1)) : "memory");
     else
       wait_vm_all();
     read_pair(stage_w, nv[0][0], nv[0][1], lo, hi, X);
@@ -823,7 +823,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
     const bool more = STEADY || kk + 1 < npairs;
     if (more) {
       if (STEADY || kk + kStages < npairs)
-        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * 2 * (kStages - 1)) : "memory");
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kDmaPerPair * (kStages - 1)) : "memory");
       else
         wait_vm_all();
       read_pair(stage_w + SL * 2 * kRecord, nv[SL][0], nv[SL][1], lo, hi, nxt);
