@@ -145,7 +145,9 @@ __global__ __launch_bounds__(256) void wo_mfma_kernel(const uint16_t* __restrict
       if (b >= B) continue;
       float* dst = dst_base + (size_t)b * N + n;
       if (n + 3 < N && (N & 3) == 0) {
-        *reinterpret_cast<float4*>(dst) = make_float4(acc[a][t][0], acc[a][t][1], acc[a][t][2], acc[a][t][3]);
+        // non-temporal: the slices go out to memory now, while the weights stream, instead of staying
+        // dirty in the caches until the next step's scan evicts them (measured: scan 3 us faster)
+        __builtin_nontemporal_store(acc[a][t], reinterpret_cast<wo_f4_t*>(dst));
       } else {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
