@@ -23,18 +23,31 @@ def _default_tuning():
     yield
 
 
-def gpu_build(w, seqs=None):
-    """Cache written by the library, one append call per sequence (the prefill-sized path)."""
+def gpu_build(w, seqs=None, hold_last=False):
+    """Cache written by the library, one append call per sequence (the prefill-sized path). With
+    hold_last, every sequence's last token is left out and returned as the current tokens of a
+    decode step: (k, v, slots) for all sequences, plus mu R_K."""
     cache = K.Int2KVCache(w.num_blocks, w.num_kv_heads)
     Rk, Rv = dev(w.R_k), dev(w.R_v)
     mu_rk = K.int2kv_prepare_mu_rot(Rk, dev(w.mu))
+    last = ([], [], [])
     for b in (range(w.batch) if seqs is None else seqs):
         L = int(w.ctx_lens[b])
         if L == 0:
             continue
         k, v = w.kv(b, as_torch=True)
-        K.int2kv_quantize_append(cache, k.cuda(), v.cuda(), dev(w.slot_mapping(b)), Rk, Rv, mu_rk)
+        slots = w.slot_mapping(b)
+        n = L - 1 if hold_last else L
+        if n > 0:
+            K.int2kv_quantize_append(cache, k[:n].cuda(), v[:n].cuda(), dev(slots[:n]), Rk, Rv, mu_rk)
+        if hold_last:
+            last[0].append(k[L - 1])
+            last[1].append(v[L - 1])
+            last[2].append(slots[L - 1])
     torch.cuda.synchronize()
+    if hold_last:
+        cur = (torch.stack(last[0]).cuda(), torch.stack(last[1]).cuda(), dev(np.array(last[2], np.int32)))
+        return cache, Rk, Rv, cur, mu_rk
     return cache, Rk, Rv
 
 
@@ -115,15 +128,18 @@ def test_config3_prefill_append_then_decode():
 
 def test_config4_sampled_sequences():
     """The benchmark workload (64 ragged sequences, 40/8 heads, W_O 5120^2 prepared with R_V folded
-    in, as the benchmark runs it; also row-major folded) decoded whole on the GPU; the shortest, the
+    in) run as the benchmark runs it: every sequence but its last token prefilled, then
+    int2kv_append_decode (also a row-major folded W_O decode of the same cache); the shortest, the
     longest and two seeded other sequences are checked, each against an oracle cache holding that
     sequence alone."""
     print("\n[full] config 4", flush=True)
     w = W.make_workload(4)
-    cache, Rk, Rv = gpu_build(w)
+    cache, Rk, Rv, (kc, vc, sc), mu_rk = gpu_build(w, hold_last=True)
     dargs = (cache, dev(w.q), dev(w.block_table), dev(w.ctx_lens), int(w.ctx_lens.max()), Rk, Rv)
     Wp = K.int2kv_prepare_wo(dev(w.W_o), Rv, w.num_q_heads)
-    y = K.int2kv_decode(*dargs, W_o=Wp, wo_format=K.INT2KV_WO_PREPARED_FOLDED, d_model=w.W_o.shape[0]).cpu().numpy()
+    # the benchmark's step: the current tokens' cache write inside the decode's first launch
+    y = K.int2kv_append_decode(cache, kc, vc, sc, mu_rk, *dargs[1:], W_o=Wp, wo_format=K.INT2KV_WO_PREPARED_FOLDED,
+                               d_model=w.W_o.shape[0]).cpu().numpy()
     Wf = K.int2kv_fold_wo(dev(w.W_o), Rv, w.num_q_heads)
     y_f = K.int2kv_decode(*dargs, W_o=Wf, wo_is_folded=True).cpu().numpy()
     lens = w.ctx_lens
