@@ -21,7 +21,8 @@ scales and zeros are reproducible bit for bit:
 
 Q_2 is "group-wise affine INT2" (Sec. 5 implementation details, Table A). The
 paper gives no arithmetic for it; the reading used here (and by the library):
-per token and per group of 32 consecutive rotated channels, over fp32 inputs,
+per token and per group of G consecutive rotated channels (G = 32, or the paper's
+G = 128), over fp32 inputs,
     mn = min x, mx = max x;  if c != 1: mn = fp32(c*mn), mx = fp32(c*mx)
     s  = fp16_rne(fp32(fp32(mx - mn) / 3)),   z = fp16_rne(mn)
     inv = fp32(1 / s) if s > 0 else 0
@@ -29,13 +30,14 @@ per token and per group of 32 consecutive rotated channels, over fp32 inputs,
     dequant = code * s + z            (exact in fp64)
 The rotated tensor fed to Q_2 is the fp64 product rounded once to fp32.
 
-Packed cache layout (one 1536-byte record per physical block and KV head, the
-format the library writes; record address = pool + (block * H_kv + h) * 1536):
+Packed cache layout (one record per physical block and KV head, the format the
+library writes; NG = 128 / G groups per token; record address =
+pool + (block * H_kv + h) * R with R = 1024 + 128 * NG: 1536 bytes at G = 32, 1152 at G = 128):
     [   0,  512) K codes,  token-major: the 16-bit half m of token t at byte 32*t + 2*m
     [ 512, 1024) V codes,  half-major : the 16-bit half m of token t at byte 512 + 32*m + 2*t
-    [1024, 1280) K meta,   token t, group g at byte 1024 + 16*t + 4*g: fp16 scale, then fp16 zero
-    [1280, 1408) V scales, group g, token t at byte 1280 + 32*g + 2*t (fp16)
-    [1408, 1536) V zeros,  group g, token t at byte 1408 + 32*g + 2*t (fp16)
+    [1024, 1024 + 64 NG)       K meta,   token t, group g at 1024 + 4*NG*t + 4*g: fp16 scale, fp16 zero
+    [1024 + 64 NG, + 32 NG)    V scales, group g, token t at 1024 + 64*NG + 32*g + 2*t (fp16)
+    [1024 + 96 NG, + 32 NG)    V zeros,  group g, token t at 1024 + 96*NG + 32*g + 2*t (fp16)
 Inside a 16-bit half m, channel c = 16*p + m occupies bits 2p..2p+1 (little endian).
 
 Every function below is a plain definition; none is blocked, fused or reordered.
@@ -48,11 +50,27 @@ from __future__ import annotations
 import numpy as np
 
 HEAD_DIM = 128
-GROUP = 32
+GROUP = 32                      # default group size
 N_GROUPS = HEAD_DIM // GROUP
 BLOCK = 16
-RECORD_BYTES = 1536
+RECORD_BYTES = 1536             # record bytes at the default group size
 OFF_KC, OFF_VC, OFF_KM, OFF_VS, OFF_VZ = 0, 512, 1024, 1280, 1408
+GROUP_SIZES = (32, 128)
+
+
+def record_bytes(group: int = GROUP) -> int:
+    """Bytes of one (block, KV head) record: 1024 of codes and 128 of metadata per group and 16 tokens."""
+    if group not in GROUP_SIZES:
+        raise ValueError("group size must be 32 or 128")
+    return 1024 + 128 * (HEAD_DIM // group)
+
+
+def _layout(record: int):
+    """(groups per token, K meta, V scale and V zero offsets) of a record size."""
+    ng = (record - 1024) // 128
+    if record != 1024 + 128 * ng or ng not in (1, 4):
+        raise ValueError("unknown record size")
+    return ng, 1024, 1024 + 64 * ng, 1024 + 96 * ng
 
 
 # --------------------------------------------------------------------------- inputs
@@ -82,14 +100,16 @@ def rotate(v_bits: np.ndarray, R_v: np.ndarray) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------- quantizer
-def quantize(x: np.ndarray, clip: float = 1.0):
-    """Group-wise affine INT2 quantization of fp32 rows (last axis 128, groups of 32).
+def quantize(x: np.ndarray, clip: float = 1.0, group: int = GROUP):
+    """Group-wise affine INT2 quantization of fp32 rows (last axis 128, groups of `group`).
 
-    Returns (codes uint8 [..., 128], s float16 [..., 4], z float16 [..., 4])."""
+    Returns (codes uint8 [..., 128], s float16 [..., 128/group], z float16 [..., 128/group])."""
     x = np.asarray(x, dtype=np.float32)
     if x.shape[-1] != HEAD_DIM:
         raise ValueError("last axis must be 128")
-    xg = x.reshape(x.shape[:-1] + (N_GROUPS, GROUP))
+    if group not in GROUP_SIZES:
+        raise ValueError("group size must be 32 or 128")
+    xg = x.reshape(x.shape[:-1] + (HEAD_DIM // group, group))
     mn = xg.min(axis=-1)
     mx = xg.max(axis=-1)
     if clip != 1.0:
@@ -111,8 +131,9 @@ def quantize(x: np.ndarray, clip: float = 1.0):
 
 
 def dequantize(codes: np.ndarray, s: np.ndarray, z: np.ndarray) -> np.ndarray:
-    """code * s + z per group, fp64 (exact)."""
-    c = codes.astype(np.float64).reshape(codes.shape[:-1] + (N_GROUPS, GROUP))
+    """code * s + z per group, fp64 (exact); the group size follows from s (128 / s.shape[-1])."""
+    ng = s.shape[-1]
+    c = codes.astype(np.float64).reshape(codes.shape[:-1] + (ng, HEAD_DIM // ng))
     out = c * s.astype(np.float64)[..., None] + z.astype(np.float64)[..., None]
     return out.reshape(codes.shape)
 
@@ -136,8 +157,11 @@ def _codes_from_halves(halves: np.ndarray) -> np.ndarray:
 def write_records(pool: np.ndarray, slots: np.ndarray, kc, ks, kz, vc, vs, vz) -> None:
     """Store quantized tokens into the paged pool at the byte offsets of the layout above.
 
-    pool: uint8 [num_blocks, H, 1536]; slots: [n] distinct cache slots (block * 16 + row);
-    kc/vc: uint8 [n, H, 128]; ks/kz/vs/vz: float16 [n, H, 4]."""
+    pool: uint8 [num_blocks, H, record]; slots: [n] distinct cache slots (block * 16 + row);
+    kc/vc: uint8 [n, H, 128]; ks/kz/vs/vz: float16 [n, H, NG] with the pool's NG groups per token."""
+    ng, off_km, off_vs, off_vz = _layout(pool.shape[-1])
+    if ks.shape[-1] != ng:
+        raise ValueError("metadata groups do not match the pool's record")
     slots = np.asarray(slots, dtype=np.int64)
     if np.unique(slots).size != slots.size:
         raise ValueError("slots must be distinct")
@@ -152,42 +176,50 @@ def write_records(pool: np.ndarray, slots: np.ndarray, kc, ks, kz, vc, vs, vz) -
     vh = _halves_from_codes(vc).astype("<u2").view(np.uint8).reshape(n, H, 32)
     vidx = (OFF_VC + 2 * t)[:, None] + (32 * np.arange(16)[:, None] + np.arange(2)[None, :]).reshape(1, 32)
     pool[B_, H_, vidx[:, None, :]] = vh
-    # K meta: (s, z) of group g at 1024 + 16*t + 4*g
-    km = np.stack([ks, kz], axis=-1).astype("<f2").view(np.uint8).reshape(n, H, 16)
-    pool[B_, H_, (OFF_KM + 16 * t)[:, None, None] + np.arange(16)[None, None, :]] = km
+    # K meta: (s, z) of group g at 1024 + 4*NG*t + 4*g
+    km = np.stack([ks, kz], axis=-1).astype("<f2").view(np.uint8).reshape(n, H, 4 * ng)
+    pool[B_, H_, (off_km + 4 * ng * t)[:, None, None] + np.arange(4 * ng)[None, None, :]] = km
     # V scales / zeros: group g of token t at base + 32*g + 2*t
-    gidx = (32 * np.arange(N_GROUPS)[:, None] + np.arange(2)[None, :]).reshape(1, 8)
-    pool[B_, H_, ((OFF_VS + 2 * t)[:, None] + gidx)[:, None, :]] = \
-        np.ascontiguousarray(vs, dtype="<f2").view(np.uint8).reshape(n, H, 8)
-    pool[B_, H_, ((OFF_VZ + 2 * t)[:, None] + gidx)[:, None, :]] = \
-        np.ascontiguousarray(vz, dtype="<f2").view(np.uint8).reshape(n, H, 8)
+    gidx = (32 * np.arange(ng)[:, None] + np.arange(2)[None, :]).reshape(1, 2 * ng)
+    pool[B_, H_, ((off_vs + 2 * t)[:, None] + gidx)[:, None, :]] = \
+        np.ascontiguousarray(vs, dtype="<f2").view(np.uint8).reshape(n, H, 2 * ng)
+    pool[B_, H_, ((off_vz + 2 * t)[:, None] + gidx)[:, None, :]] = \
+        np.ascontiguousarray(vz, dtype="<f2").view(np.uint8).reshape(n, H, 2 * ng)
 
 
 def read_tokens(pool: np.ndarray, block_row: np.ndarray, length: int, h: int):
     """Unpack the first `length` tokens of one sequence and KV head.
 
-    Returns (kc, ks, kz, vc, vs, vz): codes uint8 [L, 128], metadata float16 [L, 4]."""
+    Returns (kc, ks, kz, vc, vs, vz): codes uint8 [L, 128], metadata float16 [L, NG]."""
+    ng, off_km, off_vs, off_vz = _layout(pool.shape[-1])
     nblk = (length + BLOCK - 1) // BLOCK
-    recs = pool[np.asarray(block_row[:nblk], dtype=np.int64), h]          # [nb, 1536]
+    recs = pool[np.asarray(block_row[:nblk], dtype=np.int64), h]          # [nb, record]
     kh = recs[:, OFF_KC:OFF_VC].copy().view("<u2").reshape(nblk, BLOCK, 16)          # [nb, t, m]
-    vh = recs[:, OFF_VC:OFF_KM].copy().view("<u2").reshape(nblk, 16, BLOCK).transpose(0, 2, 1)
-    km = recs[:, OFF_KM:OFF_VS].copy().view("<f2").reshape(nblk, BLOCK, N_GROUPS, 2)
-    vs = recs[:, OFF_VS:OFF_VZ].copy().view("<f2").reshape(nblk, N_GROUPS, BLOCK).transpose(0, 2, 1)
-    vz = recs[:, OFF_VZ:RECORD_BYTES].copy().view("<f2").reshape(nblk, N_GROUPS, BLOCK).transpose(0, 2, 1)
+    vh = recs[:, OFF_VC:off_km].copy().view("<u2").reshape(nblk, 16, BLOCK).transpose(0, 2, 1)
+    km = recs[:, off_km:off_vs].copy().view("<f2").reshape(nblk, BLOCK, ng, 2)
+    vs = recs[:, off_vs:off_vz].copy().view("<f2").reshape(nblk, ng, BLOCK).transpose(0, 2, 1)
+    vz = recs[:, off_vz:off_vz + 32 * ng].copy().view("<f2").reshape(nblk, ng, BLOCK).transpose(0, 2, 1)
     flat = lambda a: a.reshape((nblk * BLOCK,) + a.shape[2:])[:length]
     return (flat(_codes_from_halves(kh)), flat(km[..., 0]).astype(np.float16), flat(km[..., 1]).astype(np.float16),
             flat(_codes_from_halves(vh)), flat(vs).astype(np.float16), flat(vz).astype(np.float16))
 
 
-def new_pool(num_blocks: int, num_kv_heads: int) -> np.ndarray:
-    return np.zeros((num_blocks, num_kv_heads, RECORD_BYTES), dtype=np.uint8)
+def new_pool(num_blocks: int, num_kv_heads: int, group: int = GROUP) -> np.ndarray:
+    return np.zeros((num_blocks, num_kv_heads, record_bytes(group)), dtype=np.uint8)
+
+
+def pool_group(pool: np.ndarray) -> int:
+    """Group size of a pool, from its record size."""
+    return HEAD_DIM // _layout(pool.shape[-1])[0]
 
 
 # --------------------------------------------------------------------------- cache write
 def quantize_pack_rotated(pool, k_rot, v_rot, slots, clip_k=1.0, clip_v=1.0):
-    """Quantize already rotated (and, for keys, centered) fp32 rows and store them."""
-    kc, ks, kz = quantize(k_rot, clip_k)
-    vc, vs, vz = quantize(v_rot, clip_v)
+    """Quantize already rotated (and, for keys, centered) fp32 rows and store them (groups of the
+    pool's group size)."""
+    G = pool_group(pool)
+    kc, ks, kz = quantize(k_rot, clip_k, G)
+    vc, vs, vz = quantize(v_rot, clip_v, G)
     write_records(pool, slots, kc, ks, kz, vc, vs, vz)
     return kc, ks, kz, vc, vs, vz
 

@@ -84,34 +84,39 @@ def test_quantizer_hand_fixtures():
         assert np.array_equal(codes[0, :32], expect), case["name"]
 
 
-def test_quantizer_roundtrip_on_grid_inputs():
+@pytest.mark.parametrize("G", [32, 128])
+def test_quantizer_roundtrip_on_grid_inputs(G):
     """Groups that lie exactly on an INT2 grid (fp16-exact zero, power-of-two scale, codes 0 and 3
     present) quantize to the same codes, scale and zero, and dequantize exactly."""
     rng = np.random.default_rng(11)
-    n = 400
+    n, ng = 400, 128 // G
     codes = rng.integers(0, 4, size=(n, 128)).astype(np.uint8)
-    codes.reshape(n, 4, 32)[:, :, 0] = 0
-    codes.reshape(n, 4, 32)[:, :, 1] = 3
-    s = np.float16(2.0) ** rng.integers(-6, 3, size=(n, 4)).astype(np.float16)
-    z = (rng.integers(-512, 512, size=(n, 4)) / 64.0).astype(np.float16)
-    x = (codes.reshape(n, 4, 32) * s.astype(np.float64)[..., None] + z.astype(np.float64)[..., None])
+    codes.reshape(n, ng, G)[:, :, 0] = 0
+    codes.reshape(n, ng, G)[:, :, 1] = 3
+    s = np.float16(2.0) ** rng.integers(-6, 3, size=(n, ng)).astype(np.float16)
+    z = (rng.integers(-512, 512, size=(n, ng)) / 64.0).astype(np.float16)
+    x = (codes.reshape(n, ng, G) * s.astype(np.float64)[..., None] + z.astype(np.float64)[..., None])
     x = x.reshape(n, 128)
     assert np.array_equal(x.astype(np.float32).astype(np.float64), x)
-    c2, s2, z2 = O.quantize(x.astype(np.float32))
+    c2, s2, z2 = O.quantize(x.astype(np.float32), 1.0, G)
     assert np.array_equal(c2, codes)
     assert np.array_equal(s2, s) and np.array_equal(z2, z)
     assert np.array_equal(O.dequantize(c2, s2, z2), x)
 
 
-def test_quantizer_picks_nearest_level():
+@pytest.mark.parametrize("G", [32, 128])
+def test_quantizer_picks_nearest_level(G):
     """Brute force over the four levels: every code is a nearest level of its group's grid
-    (at fixed stored s, z); exact distance ties may go either way only within fp32 rounding."""
+    (at fixed stored s, z); exact distance ties may go either way only within fp32 rounding.
+    The group's scale is (max - min) / 3 over its G channels and its zero the minimum."""
     rng = np.random.default_rng(3)
     x = (rng.standard_normal((300, 128)) * rng.uniform(0.1, 5, size=(300, 1))).astype(np.float32)
     for clip in (1.0, 0.9):
-        codes, s, z = O.quantize(x, clip)
-        sg = np.repeat(s.astype(np.float64), 32, axis=-1)
-        zg = np.repeat(z.astype(np.float64), 32, axis=-1)
+        codes, s, z = O.quantize(x, clip, G)
+        xg = x.reshape(300, 128 // G, G).astype(np.float64)
+        assert np.array_equal(z, (np.float32(clip) * xg.min(-1).astype(np.float32)).astype(np.float16))
+        sg = np.repeat(s.astype(np.float64), G, axis=-1)
+        zg = np.repeat(z.astype(np.float64), G, axis=-1)
         levels = np.arange(4)[None, None, :] * sg[..., None] + zg[..., None]
         dist = np.abs(x.astype(np.float64)[..., None] - levels)
         chosen = np.take_along_axis(dist, codes[..., None].astype(np.int64), axis=-1)[..., 0]
@@ -119,17 +124,18 @@ def test_quantizer_picks_nearest_level():
         assert np.all(chosen <= dist.min(axis=-1) + slack)
 
 
-def test_quantizer_enumeration_on_tiny_groups():
+@pytest.mark.parametrize("G", [32, 128])
+def test_quantizer_enumeration_on_tiny_groups(G):
     """Enumerate all 4^6 code vectors of six free elements: the quantizer's choice minimises the
     squared reconstruction error at the group's fixed (s, z)."""
     rng = np.random.default_rng(17)
     grid = np.stack(np.meshgrid(*[np.arange(4)] * 6, indexing="ij"), axis=-1).reshape(-1, 6)
     for _ in range(20):
         x = np.zeros(128, dtype=np.float32)
-        g = rng.uniform(-3, 3, size=32).astype(np.float32)
-        x[:32] = g
-        x[32:] = rng.uniform(-1, 1, size=96).astype(np.float32)
-        codes, s, z = O.quantize(x[None])
+        g = rng.uniform(-3, 3, size=G).astype(np.float32)
+        x[:G] = g
+        x[G:] = rng.uniform(-1, 1, size=128 - G).astype(np.float32)
+        codes, s, z = O.quantize(x[None], 1.0, G)
         sf, zf = float(s[0, 0]), float(z[0, 0])
         free = g[:6].astype(np.float64)
         err = ((free[None, :] - (grid * sf + zf)) ** 2).sum(axis=1)
@@ -144,6 +150,13 @@ def test_degenerate_and_clip_extremes():
     assert s[0, 1] == 0 and z[0, 1] == np.float16(-3.5) and np.all(codes[0, 32:64] == 0)
     deq = O.dequantize(codes, s, z)
     assert np.all(deq[0, 32:64] == -3.5)
+    # one group of 128: a constant row is degenerate, and the group's range is the row's range
+    x = np.full((1, 128), 2.25, dtype=np.float32)
+    codes, s, z = O.quantize(x, 1.0, 128)
+    assert s.shape == (1, 1) and s[0, 0] == 0 and z[0, 0] == np.float16(2.25) and not codes.any()
+    x[0, 100] = 5.25  # range 3: s = 1, the one large value takes code 3 and the others 0
+    codes, s, z = O.quantize(x, 1.0, 128)
+    assert s[0, 0] == 1 and z[0, 0] == np.float16(2.25) and codes[0, 100] == 3 and codes.sum() == 3
 
 
 # ----------------------------------------------------------------------------- layout
@@ -178,13 +191,35 @@ def test_layout_hand_fixtures():
     assert not pool[0].any()
 
 
-def test_pack_unpack_roundtrip():
+def test_layout_group128_hand_fixture():
+    """Group size 128: a 1152-byte record whose metadata sits at 1024 + 4 t (K scale, K zero),
+    1088 + 2 t (V scale) and 1120 + 2 t (V zero); codes as at G = 32."""
+    pool = O.new_pool(2, 1, 128)
+    assert pool.shape[-1] == 1152 and O.pool_group(pool) == 128
+    kc = np.zeros((16, 1, 128), np.uint8)
+    vc = np.zeros_like(kc)
+    f = lambda v: np.full((16, 1, 1), v, np.float16)
+    ks, kz, vs, vz = f(0), f(0), f(0), f(0)
+    kc[5, 0, 17] = 3        # channel 17 = 16*1 + 1: half 1, bits 2..3 -> K half at 32*5 + 2 = 162: 0x0C
+    vc[2, 0, 3] = 1         # channel 3 = 16*0 + 3: half 3, bits 0..1 -> V half at 512 + 32*3 + 2*2 = 612: 0x01
+    ks[7, 0, 0], kz[7, 0, 0] = 1.0, -0.5    # 0x3C00, 0xB800 at 1024 + 28
+    vs[3, 0, 0], vz[15, 0, 0] = 2.0, 1.0    # 0x4000 at 1088 + 6; 0x3C00 at 1120 + 30
+    O.write_records(pool, np.arange(16) + 16, kc, ks, kz, vc, vs, vz)
+    expect = np.zeros(1152, np.uint8)
+    for off, val in {162: 0x0C, 612: 0x01, 1052: 0x00, 1053: 0x3C, 1054: 0x00, 1055: 0xB8, 1094: 0x00, 1095: 0x40,
+                     1150: 0x00, 1151: 0x3C}.items():
+        expect[off] = val
+    assert np.array_equal(pool[1, 0], expect) and not pool[0].any()
+
+
+@pytest.mark.parametrize("G", [32, 128])
+def test_pack_unpack_roundtrip(G):
     rng = np.random.default_rng(2)
-    n, H = 40, 3
-    pool = O.new_pool(8, H)
+    n, H, ng = 40, 3, 128 // G
+    pool = O.new_pool(8, H, G)
     slots = rng.permutation(8 * 16)[:n]
     kc, vc = (rng.integers(0, 4, size=(n, H, 128)).astype(np.uint8) for _ in range(2))
-    ks, kz, vs, vz = (rng.standard_normal((n, H, 4)).astype(np.float16) for _ in range(4))
+    ks, kz, vs, vz = (rng.standard_normal((n, H, ng)).astype(np.float16) for _ in range(4))
     O.write_records(pool, slots, kc, ks, kz, vc, vs, vz)
     for h in range(H):
         # read every block as one long "sequence" and pick the written slots back out
@@ -201,12 +236,14 @@ def test_bits_per_element_matches_paper():
     G, win, L = gold["group_size"], gold["sink_tokens"] + gold["recent_tokens"], gold["context_tokens"]
     bpe = (2 + 32 / G) * (L - win) / L + gold["bf16_bits"] * win / L
     assert abs(bpe - gold["bpe_reported"]) < 0.005
-    assert O.RECORD_BYTES * 8 / (16 * 2 * 128) == 2 + 32 / O.GROUP
+    for G in (32, 128):
+        assert O.record_bytes(G) * 8 / (16 * 2 * 128) == 2 + 32 / G  # 1536 and 1152 bytes
 
 
 # ----------------------------------------------------------------------------- attention
-def _grid_workload(seed, B, Hq, H, lens, d_model=None):
-    """Keys and values exactly on INT2 grids (so quantization is lossless), R = I, mu = 0."""
+def _grid_workload(seed, B, Hq, H, lens, d_model=None, G=32):
+    """Keys and values exactly on INT2 grids of group size G (so quantization is lossless), R = I,
+    mu = 0."""
     rng = np.random.default_rng(seed)
     nblk = [(L + 15) // 16 for L in lens]
     num_blocks = sum(nblk) + 3
@@ -217,16 +254,17 @@ def _grid_workload(seed, B, Hq, H, lens, d_model=None):
         table[b, :nblk[b]] = perm[cur:cur + nblk[b]]
         cur += nblk[b]
     I = np.repeat(np.eye(128, dtype=np.float32)[None], H, axis=0)
-    pool = O.new_pool(num_blocks, H)
+    pool = O.new_pool(num_blocks, H, G)
+    ng = 128 // G
     Ks, Vs = [], []
     for b in range(B):
         L = lens[b]
         def grid():
-            c = rng.integers(0, 4, size=(L, H, 4, 32))
+            c = rng.integers(0, 4, size=(L, H, ng, G))
             c[..., 0] = 0
             c[..., 1] = 3
-            s = 2.0 ** rng.integers(-3, 1, size=(L, H, 4, 1))
-            z = rng.integers(-16, 0, size=(L, H, 4, 1)) / 8.0
+            s = 2.0 ** rng.integers(-3, 1, size=(L, H, ng, 1))
+            z = rng.integers(-16, 0, size=(L, H, ng, 1)) / 8.0
             return (c * s + z).reshape(L, H, 128)
         K, V = grid(), grid()
         slots = (table[b, np.arange(L) // 16].astype(np.int64) * 16 + np.arange(L) % 16)
@@ -242,12 +280,13 @@ def _grid_workload(seed, B, Hq, H, lens, d_model=None):
     return pool, table, np.array(lens, np.int32), I, q, Ks, Vs, Wo
 
 
-def test_decode_reduces_to_textbook_attention():
+@pytest.mark.parametrize("G", [32, 128])
+def test_decode_reduces_to_textbook_attention(G):
     """R = I, mu = 0 and grid-exact keys/values: INT2 decode is plain scaled-dot-product
     attention with GQA (torch SDPA, fp64 CPU) followed by F.linear with W_O."""
     B, Hq, H = 3, 6, 2
     lens = [37, 16, 70]
-    pool, table, ctx, I, q, Ks, Vs, Wo = _grid_workload(0, B, Hq, H, lens, d_model=96)
+    pool, table, ctx, I, q, Ks, Vs, Wo = _grid_workload(0, B, Hq, H, lens, d_model=96, G=G)
     y, o = O.decode(pool, q, table, ctx, I, I, Wo, heads_out=True)
     qf = torch.from_numpy(O.bf16_to_f64(q))
     for b in range(B):
