@@ -12,8 +12,8 @@
  *       y = concat_j(o_j) W_O^T   (optional)
  *   Query head j reads KV head h(j) = floor(j / G_q), G_q = H_q / H_kv (GQA, Sec. 3).
  *
- * Q_2 is group-wise affine INT2 (Sec. 5 implementation details, Table A) over groups of 32
- * consecutive rotated channels of one token. The arithmetic, fixed for bit-exactness, is
+ * Q_2 is group-wise affine INT2 (Sec. 5 implementation details, Table A) over groups of G = 32
+ * or G = 128 (the paper's setting) consecutive rotated channels of one token. The arithmetic, fixed for bit-exactness, is
  * (all fp32, no contraction, round-to-nearest-even throughout):
  *       mn = min x, mx = max x;   if clip != 1: mn = clip*mn, mx = clip*mx
  *       s  = fp16(fp32(mx - mn) / 3),   z = fp16(mn)
@@ -26,19 +26,20 @@
  *   - bf16 and fp16 tensors are passed as uint16_t bit patterns; row-major, densely packed.
  *   - Return value: INT2KV_OK or a negative int2kv_status. On an argument error nothing is
  *     launched; int2kv_last_error() (thread-local) describes the last failure.
- *   - head_dim = 128, block_size = 16, group_size = 32 are the supported shapes.
+ *   - head_dim = 128, block_size = 16, group_size = 32 or 128 are the supported shapes.
  *
- * Packed cache (part of the bit-exact contract): the pool holds one 1536-byte record per
- * (physical block, KV head) at pool + (block * num_kv_heads + h) * 1536, 16-byte aligned.
- * Token row t (0..15) of a block and rotated channel c (0..127) are stored as
+ * Packed cache (part of the bit-exact contract): with NG = 128 / group_size groups per token,
+ * the pool holds one record of R = 1024 + 128 * NG bytes (1536 at G = 32, 1152 at G = 128; see
+ * int2kv_record_bytes) per (physical block, KV head) at pool + (block * num_kv_heads + h) * R,
+ * 16-byte aligned. Token row t (0..15) of a block and rotated channel c (0..127) are stored as
  *     [   0,  512) K codes, token-major: 16-bit half m of token t at byte 32*t + 2*m
  *     [ 512, 1024) V codes, half-major : 16-bit half m of token t at byte 512 + 32*m + 2*t
- *     [1024, 1280) K scale/zero: token t, group g at byte 1024 + 16*t + 4*g (fp16 s, fp16 z)
- *     [1280, 1408) V scales: group g, token t at byte 1280 + 32*g + 2*t (fp16)
- *     [1408, 1536) V zeros : group g, token t at byte 1408 + 32*g + 2*t (fp16)
+ *     [1024, 1024 + 64 NG) K scale/zero: token t, group g at 1024 + 4*NG*t + 4*g (fp16 s, fp16 z)
+ *     [1024 + 64 NG, ...)  V scales: group g, token t at 1024 + 64*NG + 32*g + 2*t (fp16)
+ *     [1024 + 96 NG, R)    V zeros : group g, token t at 1024 + 96*NG + 32*g + 2*t (fp16)
  *   where channel c = 16*p + m sits in half m at bits 2p..2p+1 (little endian), i.e. 2 bits
- *   per element plus 32 metadata bits per group: 3.0 bits per cached element at G = 32.
- *   A cache slot is block * 16 + t.
+ *   per element plus 32 metadata bits per group: 3.0 bits per cached element at G = 32, 2.25 at
+ *   G = 128. A cache slot is block * 16 + t.
  */
 #ifndef INT2KV_H
 #define INT2KV_H
@@ -53,8 +54,8 @@ extern "C" {
 
 #define INT2KV_HEAD_DIM 128
 #define INT2KV_BLOCK_SIZE 16
-#define INT2KV_GROUP_SIZE 32
-#define INT2KV_RECORD_BYTES 1536
+#define INT2KV_GROUP_SIZE 32    /* default group size; 128 is also supported */
+#define INT2KV_RECORD_BYTES 1536 /* record bytes at the default group size   */
 
 typedef enum {
   INT2KV_OK = 0,
@@ -64,16 +65,17 @@ typedef enum {
   INT2KV_EHIP = -4          /* a HIP launch reported an error                          */
 } int2kv_status;
 
-/* The paged INT2 cache. `pool` points to num_blocks * num_kv_heads * 1536 bytes (device,
- * 16-byte aligned). The caller zero-fills it once; every slot is rewritten in full by an
- * append, so no clearing is needed when blocks are reused. */
+/* The paged INT2 cache. `pool` points to num_blocks * num_kv_heads * int2kv_record_bytes(group_size)
+ * bytes (device, 16-byte aligned). The caller zero-fills it once; every slot is rewritten in full
+ * by an append, so no clearing is needed when blocks are reused. Decode over a cache with
+ * group_size 128 runs the vector-ALU scan (the matrix-core scan serves 32-channel groups). */
 typedef struct int2kv_cache {
   void* pool;
   int32_t num_blocks;
   int32_t num_kv_heads;
   int32_t block_size; /* must be 16  */
   int32_t head_dim;   /* must be 128 */
-  int32_t group_size; /* must be 32  */
+  int32_t group_size; /* 32 or 128   */
 } int2kv_cache;
 
 /* Thread-local description of the last non-OK status ("" if none). */
@@ -82,8 +84,11 @@ const char* int2kv_last_error(void);
 /* Library version string. */
 const char* int2kv_version(void);
 
-/* Bytes of the pool for the given shape (num_blocks * num_kv_heads * 1536). */
+/* Bytes of the pool for the given shape at group size 32 (num_blocks * num_kv_heads * 1536). */
 size_t int2kv_pool_bytes(int num_blocks, int num_kv_heads);
+
+/* Bytes of one (block, KV head) record: 1536 at group size 32, 1152 at 128, 0 otherwise. */
+size_t int2kv_record_bytes(int group_size);
 
 /* Rotated key mean mu_h R_{K,h}, precomputed once per KV head and subtracted right after the
  * key rotation in the cache write (Sec. 6 efficiency analysis; appendix key-mean

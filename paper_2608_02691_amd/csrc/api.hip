@@ -45,7 +45,7 @@ int check_cache(const int2kv_cache* c) {
   if (c->num_blocks <= 0 || c->num_kv_heads <= 0) return fail(INT2KV_EINVAL, "cache has no blocks or heads");
   if (c->block_size != kBlock) return fail(INT2KV_EUNSUPPORTED, "block_size must be 16");
   if (c->head_dim != kHeadDim) return fail(INT2KV_EUNSUPPORTED, "head_dim must be 128");
-  if (c->group_size != kGroup) return fail(INT2KV_EUNSUPPORTED, "group_size must be 32");
+  if (c->group_size != 32 && c->group_size != 128) return fail(INT2KV_EUNSUPPORTED, "group_size must be 32 or 128");
   if ((int64_t)c->num_blocks * kBlock > INT32_MAX) return fail(INT2KV_EUNSUPPORTED, "too many blocks for int32 slots");
   return INT2KV_OK;
 }
@@ -53,7 +53,7 @@ int check_cache(const int2kv_cache* c) {
 bool valid_clip(float c) { return c > 0.0f && c <= 1.0f; }
 
 CacheView view(const int2kv_cache* c) {
-  return CacheView{static_cast<uint8_t*>(c->pool), c->num_blocks, c->num_kv_heads};
+  return CacheView{static_cast<uint8_t*>(c->pool), c->num_blocks, c->num_kv_heads, kHeadDim / c->group_size};
 }
 
 }  // namespace
@@ -74,12 +74,13 @@ int int2kv::num_cus() {
 
 namespace {
 
-DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model) {
+DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model, int groups) {
   DecodePlan p{};
   const int gq = Hq / H;
-  // the matrix-core scan serves up to 8 query heads per KV head; wider groups use the vector-ALU scan
-  // (also when the tuning knob asks for the matrix-core one)
-  const bool mfma_ok = gq <= 8 && mfma_decode_available();
+  // the matrix-core scan serves up to 8 query heads per KV head and groups of 32 channels; wider
+  // head groups and 128-channel groups use the vector-ALU scan (also when the tuning knob asks for
+  // the matrix-core one)
+  const bool mfma_ok = gq <= 8 && groups == 4 && mfma_decode_available();
   p.variant = g_variant_override == 1 || !mfma_ok ? 1 : 2;
   int chunk = g_chunk_override;
   if (chunk <= 0) {
@@ -134,6 +135,10 @@ const char* int2kv_version(void) { return "int2kv 0.1 gfx950"; }
 size_t int2kv_pool_bytes(int num_blocks, int num_kv_heads) {
   if (num_blocks <= 0 || num_kv_heads <= 0) return 0;
   return (size_t)num_blocks * num_kv_heads * kRecord;
+}
+
+size_t int2kv_record_bytes(int group_size) {
+  return group_size == 32 ? (size_t)Rec<4>::kBytes : group_size == 128 ? (size_t)Rec<1>::kBytes : 0;
 }
 
 int int2kv_set_decode_events(hipEvent_t before_scan, hipEvent_t after_scan) {
@@ -218,7 +223,10 @@ size_t int2kv_decode_workspace_bytes(int batch, int num_q_heads, int num_kv_head
   if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads || max_ctx < 0 ||
       d_model < 0)
     return 0;
-  return make_plan(batch, num_q_heads, num_kv_heads, max_ctx, d_model).total;
+  // enough for either scan (the cache's group size picks one)
+  const size_t a = make_plan(batch, num_q_heads, num_kv_heads, max_ctx, d_model, 4).total;
+  const size_t b = make_plan(batch, num_q_heads, num_kv_heads, max_ctx, d_model, 1).total;
+  return a > b ? a : b;
 }
 
 }  // extern "C"
@@ -268,7 +276,7 @@ int decode_impl(const int2kv_cache* cache, const uint16_t* q, int batch, int num
   } else {
     d_model = 0;
   }
-  const DecodePlan plan = make_plan(batch, num_q_heads, H, max_ctx, d_model);
+  const DecodePlan plan = make_plan(batch, num_q_heads, H, max_ctx, d_model, kHeadDim / cache->group_size);
   if (!workspace || workspace_bytes < plan.total)
     return fail(INT2KV_EWORKSPACE, "workspace smaller than int2kv_decode_workspace_bytes()");
   if (!aligned(workspace, 256)) return fail(INT2KV_EINVAL, "workspace must be 256-byte aligned");
@@ -298,6 +306,7 @@ int decode_impl(const int2kv_cache* cache, const uint16_t* q, int batch, int num
   a.seq_wg = reinterpret_cast<int32_t*>(ws + plan.off_seqwg);
   a.pages = reinterpret_cast<uint32_t*>(ws + plan.off_pages);
   a.grid_g = plan.grid_g;
+  a.groups = kHeadDim / cache->group_size;
 
   hipError_t e = hipSuccess;
   // the cache write (int2kv_append_decode): a few tokens per sequence run as extra blocks of the

@@ -68,17 +68,37 @@ hipError_t launch_fold_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_f, 
 
 // ---------------------------------------------------------------------------------------------
 // Quantize one token row of K (threads 0..127) and V (threads 128..255) held one channel per
-// thread, and store it. All 256 threads of the block must call it (it synchronizes).
+// thread, and store it, with NG groups per token. All 256 threads of the block must call it (it
+// synchronizes).
+template <int NG>
 __device__ __forceinline__ void quantize_store_pair(float x, int slot, int h, float clip_k, float clip_v,
-                                                    const CacheView& cv, uint8_t (*codes)[kHeadDim]) {
+                                                    const CacheView& cv, uint8_t (*codes)[kHeadDim],
+                                                    float (*ext)[2][2]) {
+  using L = Rec<NG>;
   const int tid = threadIdx.x;
   const int row = tid >> 7;  // 0 = K, 1 = V
   const int c = tid & 127;
   float mn = x, mx = x;
+  if constexpr (NG == 4) {
 #pragma unroll
-  for (int off = 16; off >= 1; off >>= 1) {
-    mn = fminf(mn, __shfl_xor(mn, off, 32));
-    mx = fmaxf(mx, __shfl_xor(mx, off, 32));
+    for (int off = 16; off >= 1; off >>= 1) {
+      mn = fminf(mn, __shfl_xor(mn, off, 32));
+      mx = fmaxf(mx, __shfl_xor(mx, off, 32));
+    }
+  } else {
+    // one group of 128 channels: the row's two waves reduce, then exchange through LDS
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      mn = fminf(mn, __shfl_xor(mn, off));
+      mx = fmaxf(mx, __shfl_xor(mx, off));
+    }
+    if ((tid & 63) == 0) {
+      ext[row][(tid >> 6) & 1][0] = mn;
+      ext[row][(tid >> 6) & 1][1] = mx;
+    }
+    __syncthreads();
+    mn = fminf(ext[row][0][0], ext[row][1][0]);
+    mx = fmaxf(ext[row][0][1], ext[row][1][1]);
   }
   uint32_t s_bits, z_bits;
   float zf, inv;
@@ -88,7 +108,7 @@ __device__ __forceinline__ void quantize_store_pair(float x, int slot, int h, fl
   const bool ok = slot >= 0 && slot < cv.num_blocks * kBlock;
   if (ok) {
     const int blk = slot >> 4, t = slot & 15;
-    uint8_t* rec = cv.pool + ((size_t)blk * cv.num_kv_heads + h) * kRecord;
+    uint8_t* rec = cv.pool + ((size_t)blk * cv.num_kv_heads + h) * L::kBytes;
     if (c < 16) {
       uint32_t half = 0;
 #pragma unroll
@@ -96,13 +116,13 @@ __device__ __forceinline__ void quantize_store_pair(float x, int slot, int h, fl
       const int off = row == 0 ? kOffKCodes + 32 * t + 2 * c : kOffVCodes + 32 * c + 2 * t;
       *reinterpret_cast<uint16_t*>(rec + off) = static_cast<uint16_t>(half);
     }
-    if ((c & 31) == 0) {
-      const int g = c >> 5;
+    if ((c % L::kGroupSize) == 0) {
+      const int g = c / L::kGroupSize;
       if (row == 0) {
-        *reinterpret_cast<uint32_t*>(rec + kOffKMeta + 16 * t + 4 * g) = s_bits | (z_bits << 16);
+        *reinterpret_cast<uint32_t*>(rec + L::kOffKMeta + 4 * NG * t + 4 * g) = s_bits | (z_bits << 16);
       } else {
-        *reinterpret_cast<uint16_t*>(rec + kOffVScale + 32 * g + 2 * t) = static_cast<uint16_t>(s_bits);
-        *reinterpret_cast<uint16_t*>(rec + kOffVZero + 32 * g + 2 * t) = static_cast<uint16_t>(z_bits);
+        *reinterpret_cast<uint16_t*>(rec + L::kOffVScale + 32 * g + 2 * t) = static_cast<uint16_t>(s_bits);
+        *reinterpret_cast<uint16_t*>(rec + L::kOffVZero + 32 * g + 2 * t) = static_cast<uint16_t>(z_bits);
       }
     }
   }
@@ -110,26 +130,32 @@ __device__ __forceinline__ void quantize_store_pair(float x, int slot, int h, fl
 }
 
 // Quantize already rotated rows: block (token, KV head).
+template <int NG>
 __global__ __launch_bounds__(256) void pack_rotated_kernel(CacheView cv, const float* __restrict__ k_rot,
                                                             const float* __restrict__ v_rot,
                                                             const int32_t* __restrict__ slots, float clip_k,
                                                             float clip_v) {
   __shared__ uint8_t codes[2][kHeadDim];
+  __shared__ float ext[2][2][2];
   const int n = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
   const size_t base = ((size_t)n * cv.num_kv_heads + h) * kHeadDim + (tid & 127);
   const float x = tid < 128 ? k_rot[base] : v_rot[base];
-  quantize_store_pair(x, slots[n], h, clip_k, clip_v, cv, codes);
+  quantize_store_pair<NG>(x, slots[n], h, clip_k, clip_v, cv, codes, ext);
 }
 
 hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_rot, const int32_t* slots,
                                int n, float clip_k, float clip_v, hipStream_t s) {
-  hipLaunchKernelGGL(pack_rotated_kernel, dim3(n, c.num_kv_heads), dim3(256), 0, s, c, k_rot, v_rot, slots,
-                     clip_k, clip_v);
+  if (c.groups == 1)
+    hipLaunchKernelGGL(pack_rotated_kernel<1>, dim3(n, c.num_kv_heads), dim3(256), 0, s, c, k_rot, v_rot, slots,
+                       clip_k, clip_v);
+  else
+    hipLaunchKernelGGL(pack_rotated_kernel<4>, dim3(n, c.num_kv_heads), dim3(256), 0, s, c, k_rot, v_rot, slots,
+                       clip_k, clip_v);
   return hipGetLastError();
 }
 
 // Standalone append kernel: grid (blocks per (h, K|V), KV heads, K|V) of kApWaves waves.
-template <int kApTiles>
+template <int kApTiles, int NG>
 __global__ __launch_bounds__(512) void append_mfma_kernel(CacheView cv, const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v,
                                                            const int32_t* __restrict__ slots, int n,
@@ -138,7 +164,7 @@ __global__ __launch_bounds__(512) void append_mfma_kernel(CacheView cv, const ui
                                                            const float* __restrict__ mu_rk, float clip_k,
                                                            float clip_v) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[kAppendLdsBytes];
-  append_block<kApTiles, kApWaves>(cv, k, v, slots, n, R_k, R_v, mu_rk, clip_k, clip_v, (int)blockIdx.x,
+  append_block<kApTiles, kApWaves, NG>(cv, k, v, slots, n, R_k, R_v, mu_rk, clip_k, clip_v, (int)blockIdx.x,
                                    (int)gridDim.x, (int)blockIdx.y, (int)blockIdx.z, lds);
 }
 
@@ -152,13 +178,21 @@ hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v,
   const int tiles = (n + 15) / 16;
   if (tiles <= kApWaves * per_head) {
     const int nx = (tiles + kApWaves - 1) / kApWaves;
-    hipLaunchKernelGGL(append_mfma_kernel<1>, dim3(nx, c.num_kv_heads, 2), dim3(64 * kApWaves), 0, s, c, k, v,
-                       slots, n, R_k, R_v, mu_rk, clip_k, clip_v);
+    if (c.groups == 1)
+      hipLaunchKernelGGL((append_mfma_kernel<1, 1>), dim3(nx, c.num_kv_heads, 2), dim3(64 * kApWaves), 0, s, c, k, v,
+                         slots, n, R_k, R_v, mu_rk, clip_k, clip_v);
+    else
+      hipLaunchKernelGGL((append_mfma_kernel<1, 4>), dim3(nx, c.num_kv_heads, 2), dim3(64 * kApWaves), 0, s, c, k, v,
+                         slots, n, R_k, R_v, mu_rk, clip_k, clip_v);
   } else {
     const int steps = (tiles + 1) / 2;
     const int nx = min((steps + kApWaves - 1) / kApWaves, per_head);
-    hipLaunchKernelGGL(append_mfma_kernel<2>, dim3(nx, c.num_kv_heads, 2), dim3(64 * kApWaves), 0, s, c, k, v,
-                       slots, n, R_k, R_v, mu_rk, clip_k, clip_v);
+    if (c.groups == 1)
+      hipLaunchKernelGGL((append_mfma_kernel<2, 1>), dim3(nx, c.num_kv_heads, 2), dim3(64 * kApWaves), 0, s, c, k, v,
+                         slots, n, R_k, R_v, mu_rk, clip_k, clip_v);
+    else
+      hipLaunchKernelGGL((append_mfma_kernel<2, 4>), dim3(nx, c.num_kv_heads, 2), dim3(64 * kApWaves), 0, s, c, k, v,
+                         slots, n, R_k, R_v, mu_rk, clip_k, clip_v);
   }
   return hipGetLastError();
 }

@@ -72,8 +72,39 @@ struct ApOut {
 };
 
 // Group quantizer of one 16-token tile held in the transposed layout above.
+template <int NG>
 __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float clip, const float* recip_tab, int lo,
                                                int hi) {
+  if constexpr (NG == 1) {
+    // one group of 128 channels: the lane's 32 values, then the token's four lanes (xor 16, 32)
+    float mn = acc[0][0], mx = acc[0][0];
+#pragma unroll
+    for (int p = 0; p < 8; ++p)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        mn = __builtin_fminf(mn, acc[p][j]);
+        mx = __builtin_fmaxf(mx, acc[p][j]);
+      }
+    mn = __builtin_fminf(mn, __shfl_xor(mn, 16));
+    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 16));
+    mn = __builtin_fminf(mn, __shfl_xor(mn, 32));
+    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 32));
+    uint32_t s_bits, z_bits;
+    float zf, inv;
+    int2_group_params_fast(mn, mx, clip, recip_tab, s_bits, z_bits, zf, inv);
+    float hf[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < 8; ++p)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma clang fp contract(off)
+        const float t = (acc[p][j] - zf) * inv;
+        const float c = __builtin_rintf(__builtin_amdgcn_fmed3f(t, 0.0f, 3.0f));
+        hf[j] = __builtin_fmaf(c, (float)(1 << (2 * p)), hf[j]);
+      }
+    const uint32_t q0 = (uint32_t)hf[0], q1 = (uint32_t)hf[1], q2 = (uint32_t)hf[2], q3 = (uint32_t)hf[3];
+    return ApOut{q0 | (q1 << 16), q2 | (q3 << 16), s_bits | (z_bits << 16)};
+  }
   // group g = tiles 2g, 2g + 1: lane-local min/max of its eight values, then a reduce-scatter
   // over the four lanes of the token (xor 32, then xor 16) leaves group hi's extremes in lane hi
   const bool h1 = (hi & 2) != 0, h0 = (hi & 1) != 0;
@@ -130,22 +161,30 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
 }
 
 // Stores of one lane's ApOut into the record of its token's slot (skipped for slots out of range).
+// With one group per token (NG = 1) the four lanes of a token hold the same metadata; lane hi = 0
+// stores it.
+template <int NG>
 __device__ __forceinline__ void store_tile(const ApOut& o, int slot, const CacheView& cv, int h, int kv, int nslots,
                                            int hi) {
+  using L = Rec<NG>;
   if (slot >= 0 && slot < nslots) {
     const int blk = slot >> 4, t = slot & 15;
-    uint8_t* rec = cv.pool + ((size_t)blk * cv.num_kv_heads + h) * kRecord;
+    uint8_t* rec = cv.pool + ((size_t)blk * cv.num_kv_heads + h) * L::kBytes;
+    const bool meta = NG == 4 || hi == 0;
+    const int g = NG == 4 ? hi : 0;
     if (kv == 0) {
       *reinterpret_cast<uint2*>(rec + kOffKCodes + 32 * t + 8 * hi) = make_uint2(o.w01, o.w23);
-      *reinterpret_cast<uint32_t*>(rec + kOffKMeta + 16 * t + 4 * hi) = o.meta;
+      if (meta) *reinterpret_cast<uint32_t*>(rec + L::kOffKMeta + 4 * NG * t + 4 * g) = o.meta;
     } else {
       uint8_t* vc = rec + kOffVCodes + 32 * 4 * hi + 2 * t;
       *reinterpret_cast<uint16_t*>(vc) = (uint16_t)o.w01;
       *reinterpret_cast<uint16_t*>(vc + 32) = (uint16_t)(o.w01 >> 16);
       *reinterpret_cast<uint16_t*>(vc + 64) = (uint16_t)o.w23;
       *reinterpret_cast<uint16_t*>(vc + 96) = (uint16_t)(o.w23 >> 16);
-      *reinterpret_cast<uint16_t*>(rec + kOffVScale + 32 * hi + 2 * t) = (uint16_t)o.meta;
-      *reinterpret_cast<uint16_t*>(rec + kOffVZero + 32 * hi + 2 * t) = (uint16_t)(o.meta >> 16);
+      if (meta) {
+        *reinterpret_cast<uint16_t*>(rec + L::kOffVScale + 32 * g + 2 * t) = (uint16_t)o.meta;
+        *reinterpret_cast<uint16_t*>(rec + L::kOffVZero + 32 * g + 2 * t) = (uint16_t)(o.meta >> 16);
+      }
     }
   }
 }
@@ -159,7 +198,7 @@ constexpr int kAppendLdsBytes = 3 * kHeadDim * kApRow * 2 + 1024 * 4;
 // One append work-group of kWaves waves: KV head h, K (kv = 0) or V (kv = 1), block bx of nbx
 // striding over the 16-token tiles; lds holds kAppendLdsBytes (16-byte aligned). Every thread of
 // the block must call it (it synchronizes once).
-template <int kApTiles, int kWaves>
+template <int kApTiles, int kWaves, int NG>
 __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t* __restrict__ k,
                                              const uint16_t* __restrict__ v, const int32_t* __restrict__ slots,
                                              int n, const float* __restrict__ R_k, const float* __restrict__ R_v,
@@ -275,7 +314,7 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
     }
     ApOut out[kApTiles];
 #pragma unroll
-    for (int u = 0; u < kApTiles; ++u) out[u] = quantize_tile(acc[u], clip, recip_tab, lo, hi);
+    for (int u = 0; u < kApTiles; ++u) out[u] = quantize_tile<NG>(acc[u], clip, recip_tab, lo, hi);
     // the next step's loads are waited for here, before this step's stores: a wait placed after
     // the (lane-conditional) stores would also wait for the stores to complete
 #pragma unroll
@@ -285,7 +324,7 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
       asm volatile("" : "+v"(slotn[u])::"memory");
     }
 #pragma unroll
-    for (int u = 0; u < kApTiles; ++u) store_tile(out[u], slot[u], cv, h, kv, nslots, hi);
+    for (int u = 0; u < kApTiles; ++u) store_tile<NG>(out[u], slot[u], cv, h, kv, nslots, hi);
 #pragma unroll
     for (int u = 0; u < kApTiles; ++u) {
       const int tok = (st + sstride) * kStep + 16 * u + lo;

@@ -19,6 +19,21 @@ constexpr int kOffKMeta = 1024;   // [16 tok][4 groups] (fp16 s, fp16 z)
 constexpr int kOffVScale = 1280;  // [4 groups][16 tok] fp16
 constexpr int kOffVZero = 1408;   // [4 groups][16 tok] fp16
 
+// Record layout for NG groups per token: NG = 4 (groups of 32 channels, the constants above,
+// 1536-byte records) or NG = 1 (one group of 128 channels, 1152-byte records). Codes as above;
+// K (s, z) of token t and group g at kOffKMeta + 4 NG t + 4 g; V scale and zero of group g and
+// token t at kOffVScale + 32 g + 2 t and kOffVZero + 32 g + 2 t.
+template <int NG>
+struct Rec {
+  static constexpr int kGroupSize = kHeadDim / NG;
+  static constexpr int kOffKMeta = 1024;
+  static constexpr int kOffVScale = 1024 + 64 * NG;
+  static constexpr int kOffVZero = 1024 + 96 * NG;
+  static constexpr int kBytes = 1024 + 128 * NG;
+};
+static_assert(Rec<4>::kBytes == kRecord && Rec<4>::kOffVScale == kOffVScale && Rec<4>::kOffVZero == kOffVZero,
+              "the 32-channel layout");
+
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 // round to nearest even on the upper 16 bits (finite inputs)
 __device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {

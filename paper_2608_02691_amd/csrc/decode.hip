@@ -50,8 +50,11 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int MAXG>
+// NG groups per token (4 or 1). A lane's 32-channel quarter gk always carries its own q' sum; with
+// one group per token the four quarters share the token's (s, z), and the summed logit is the same.
+template <int MAXG, int NG>
 __global__ __launch_bounds__(256) void decode_split_valu_kernel(DecodeArgs a) {
+  using Lay = Rec<NG>;
   __shared__ float qs[MAXG][kHeadDim];
   __shared__ float qsum[MAXG][kGroups];
   __shared__ float pbuf[kWaves][MAXG][kBlock];
@@ -97,13 +100,14 @@ __global__ __launch_bounds__(256) void decode_split_valu_kernel(DecodeArgs a) {
   for (int pg = pg0 + w; pg < pg1; pg += kWaves) {
     const int blk = a.block_table[(size_t)b * a.max_blocks + pg];
     if (blk < 0 || blk >= a.num_blocks) continue;  // uniform per wave
-    const uint8_t* rec = a.pool + ((size_t)blk * a.H + h) * kRecord;
+    const uint8_t* rec = a.pool + ((size_t)blk * a.H + h) * Lay::kBytes;
 
     // ---- scores of token tq for every query head of the group
     const uint4* kc = reinterpret_cast<const uint4*>(rec + kOffKCodes + 32 * tq);
     const uint4 k0 = kc[0], k1 = kc[1];
     const uint32_t kw[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
-    const uint32_t meta = *reinterpret_cast<const uint32_t*>(rec + kOffKMeta + 16 * tq + 4 * gk);
+    const uint32_t meta =
+        *reinterpret_cast<const uint32_t*>(rec + Lay::kOffKMeta + 4 * NG * tq + 4 * (NG == 4 ? gk : 0));
     const float ks = f16_bits_to_f32(meta & 0xFFFF), kz = f16_bits_to_f32(meta >> 16);
     const int pos = pg * kBlock + tq;
     const bool valid = pos >= t0 && pos < t1;
@@ -152,8 +156,8 @@ __global__ __launch_bounds__(256) void decode_split_valu_kernel(DecodeArgs a) {
     const uint4 va = vc[0], vb = vc[1], vc2 = vc[2], vd = vc[3];  // halves m0 (tokens 0..15), m0+1
     const uint32_t hv0[8] = {va.x, va.y, va.z, va.w, vb.x, vb.y, vb.z, vb.w};
     const uint32_t hv1[8] = {vc2.x, vc2.y, vc2.z, vc2.w, vd.x, vd.y, vd.z, vd.w};
-    const uint4* vsp = reinterpret_cast<const uint4*>(rec + kOffVScale + 32 * gv);
-    const uint4* vzp = reinterpret_cast<const uint4*>(rec + kOffVZero + 32 * gv);
+    const uint4* vsp = reinterpret_cast<const uint4*>(rec + Lay::kOffVScale + 32 * (NG == 4 ? gv : 0));
+    const uint4* vzp = reinterpret_cast<const uint4*>(rec + Lay::kOffVZero + 32 * (NG == 4 ? gv : 0));
     const uint4 s0 = vsp[0], s1 = vsp[1], z0 = vzp[0], z1 = vzp[1];
     const uint32_t sw[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
     const uint32_t zw[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
@@ -216,18 +220,26 @@ __global__ __launch_bounds__(256) void decode_split_valu_kernel(DecodeArgs a) {
   }
 }
 
-hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+template <int NG>
+static void launch_valu_ng(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   dim3 grid(a.n_chunks, a.H, a.B);
   if (a.gq <= 1)
-    hipExtLaunchKernelGGL(decode_split_valu_kernel<1>, grid, dim3(256), 0, s, ev0, ev1, 0, a);
+    hipExtLaunchKernelGGL((decode_split_valu_kernel<1, NG>), grid, dim3(256), 0, s, ev0, ev1, 0, a);
   else if (a.gq <= 2)
-    hipExtLaunchKernelGGL(decode_split_valu_kernel<2>, grid, dim3(256), 0, s, ev0, ev1, 0, a);
+    hipExtLaunchKernelGGL((decode_split_valu_kernel<2, NG>), grid, dim3(256), 0, s, ev0, ev1, 0, a);
   else if (a.gq <= 4)
-    hipExtLaunchKernelGGL(decode_split_valu_kernel<4>, grid, dim3(256), 0, s, ev0, ev1, 0, a);
+    hipExtLaunchKernelGGL((decode_split_valu_kernel<4, NG>), grid, dim3(256), 0, s, ev0, ev1, 0, a);
   else if (a.gq <= 8)
-    hipExtLaunchKernelGGL(decode_split_valu_kernel<8>, grid, dim3(256), 0, s, ev0, ev1, 0, a);
+    hipExtLaunchKernelGGL((decode_split_valu_kernel<8, NG>), grid, dim3(256), 0, s, ev0, ev1, 0, a);
   else
-    hipExtLaunchKernelGGL(decode_split_valu_kernel<16>, grid, dim3(256), 0, s, ev0, ev1, 0, a);
+    hipExtLaunchKernelGGL((decode_split_valu_kernel<16, NG>), grid, dim3(256), 0, s, ev0, ev1, 0, a);
+}
+
+hipError_t launch_decode_split_valu(const DecodeArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  if (a.groups == 1)
+    launch_valu_ng<1>(a, s, ev0, ev1);
+  else
+    launch_valu_ng<4>(a, s, ev0, ev1);
   return hipGetLastError();
 }
 

@@ -683,7 +683,7 @@ __global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int wide, int 
   int blk = blockIdx.x;
   if (blk < nap) {
     const int bx = blk % ap.nbx, r = blk / ap.nbx;
-    append_block<1, 4>(ap.cv, ap.k, ap.v, ap.slots, ap.n, ap.R_k, ap.R_v, ap.mu_rk, ap.clip_k, ap.clip_v, bx, ap.nbx,
+    append_block<1, 4, 4>(ap.cv, ap.k, ap.v, ap.slots, ap.n, ap.R_k, ap.R_v, ap.mu_rk, ap.clip_k, ap.clip_v, bx, ap.nbx,
                        r % ap.cv.num_kv_heads, r / ap.cv.num_kv_heads, lds);
     return;
   }

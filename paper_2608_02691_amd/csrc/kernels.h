@@ -12,6 +12,7 @@ struct CacheView {
   uint8_t* pool;
   int num_blocks;
   int num_kv_heads;
+  int groups;  // groups per token: 4 (32 channels each) or 1 (128)
 };
 
 // ---- cache write (append.hip)
@@ -54,6 +55,7 @@ struct DecodeArgs {
   int32_t* seq_wg;   // [B][2]: first and last scan work-group whose range meets each sequence
   uint32_t* pages;   // page list of the matrix-core scan: [total pages + padding][4]
   int grid_g;      // work-groups of the matrix-core scan
+  int groups;      // groups per token of the cache (4 or 1)
 };
 
 constexpr int kPartStride = 132;  // m, l, 2 pad, O[128]

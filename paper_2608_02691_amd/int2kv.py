@@ -20,6 +20,7 @@ HEAD_DIM = 128
 BLOCK_SIZE = 16
 GROUP_SIZE = 32
 RECORD_BYTES = 1536
+RECORD_BYTES_BY_GROUP = {32: 1536, 128: 1152}
 
 INT2KV_OK = 0
 INT2KV_EINVAL = -1
@@ -33,7 +34,8 @@ INT2KV_WO_PREPARED = 2
 INT2KV_WO_PREPARED_FOLDED = 3
 
 EXPORTED = (
-    "int2kv_last_error", "int2kv_version", "int2kv_pool_bytes", "int2kv_prepare_mu_rot", "int2kv_fold_wo",
+    "int2kv_last_error", "int2kv_version", "int2kv_pool_bytes", "int2kv_record_bytes", "int2kv_prepare_mu_rot",
+    "int2kv_fold_wo",
     "int2kv_prepared_wo_bytes", "int2kv_prepare_wo",
     "int2kv_quantize_pack_rotated", "int2kv_quantize_append", "int2kv_decode_workspace_bytes",
     "int2kv_decode", "int2kv_append_decode", "int2kv_set_decode_tuning", "int2kv_set_decode_events",
@@ -62,6 +64,7 @@ def load_library(path: str = LIB_PATH):
         "int2kv_last_error": ([], ctypes.c_char_p),
         "int2kv_version": ([], ctypes.c_char_p),
         "int2kv_pool_bytes": ([I, I], Z),
+        "int2kv_record_bytes": ([I], Z),
         "int2kv_prepare_mu_rot": ([P, P, P, I, S], I),
         "int2kv_fold_wo": ([P, P, P, I, I, I, S], I),
         "int2kv_prepared_wo_bytes": ([I, I], Z),
@@ -111,21 +114,31 @@ _I32 = (torch.int32,)
 
 
 class Int2KVCache:
-    """The paged INT2 pool (uint8 [num_blocks, num_kv_heads, 1536]) and its C descriptor."""
+    """The paged INT2 pool (uint8 [num_blocks, num_kv_heads, record bytes]) and its C descriptor;
+    group_size 32 (1536-byte records) or 128 (1152-byte records)."""
 
-    def __init__(self, num_blocks: int, num_kv_heads: int, device="cuda", pool: Optional[torch.Tensor] = None):
+    def __init__(self, num_blocks: int, num_kv_heads: int, device="cuda", pool: Optional[torch.Tensor] = None,
+                 group_size: int = GROUP_SIZE):
+        rec = RECORD_BYTES_BY_GROUP.get(group_size)
+        if rec is None:
+            raise ValueError("group_size must be 32 or 128")
         if pool is None:
-            pool = torch.zeros((num_blocks, num_kv_heads, RECORD_BYTES), dtype=torch.uint8, device=device)
-        if pool.shape != (num_blocks, num_kv_heads, RECORD_BYTES) or pool.dtype != torch.uint8:
-            raise ValueError("pool must be uint8 [num_blocks, num_kv_heads, 1536]")
+            pool = torch.zeros((num_blocks, num_kv_heads, rec), dtype=torch.uint8, device=device)
+        if pool.shape != (num_blocks, num_kv_heads, rec) or pool.dtype != torch.uint8:
+            raise ValueError(f"pool must be uint8 [num_blocks, num_kv_heads, {rec}]")
         self.pool = pool
         self.num_blocks = num_blocks
         self.num_kv_heads = num_kv_heads
-        self._desc = _Cache(pool.data_ptr(), num_blocks, num_kv_heads, BLOCK_SIZE, HEAD_DIM, GROUP_SIZE)
+        self.group_size = group_size
+        self._desc = _Cache(pool.data_ptr(), num_blocks, num_kv_heads, BLOCK_SIZE, HEAD_DIM, group_size)
 
     @property
     def desc(self):
         return ctypes.byref(self._desc)
+
+
+def int2kv_record_bytes(group_size: int) -> int:
+    return load_library().int2kv_record_bytes(group_size)
 
 
 def int2kv_version() -> str:

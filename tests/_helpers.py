@@ -22,13 +22,14 @@ def dev(a: np.ndarray) -> torch.Tensor:
 
 
 def gpu_cache(pool: np.ndarray) -> K.Int2KVCache:
-    nb, H, _ = pool.shape
-    return K.Int2KVCache(nb, H, pool=torch.from_numpy(pool).cuda())
+    nb, H, rec = pool.shape
+    G = {1536: 32, 1152: 128}[rec]
+    return K.Int2KVCache(nb, H, pool=torch.from_numpy(pool).cuda(), group_size=G)
 
 
-def oracle_pool(w, seqs=None, clip_k=1.0, clip_v=1.0):
+def oracle_pool(w, seqs=None, clip_k=1.0, clip_v=1.0, group=32):
     """Oracle cache holding the given sequences of workload w (all by default)."""
-    pool = O.new_pool(w.num_blocks, w.num_kv_heads)
+    pool = O.new_pool(w.num_blocks, w.num_kv_heads, group)
     for b in (range(w.batch) if seqs is None else seqs):
         if int(w.ctx_lens[b]) == 0:
             continue
@@ -74,14 +75,15 @@ def compare_cache_writes(pool_gpu, pool_ref, slots, k_rot, v_rot):
     for name, (ci, si, zi), x in (("K", (0, 1, 2), k_rot), ("V", (3, 4, 5), v_rot)):
         cg, sg, zg = g[ci], g[si], g[zi]
         cr, sr, zr = r[ci], r[si], r[zi]
-        meta_diff = (sg != sr) | (zg != zr)                       # [n, H, 4]
+        meta_diff = (sg != sr) | (zg != zr)                       # [n, H, groups]
+        G = 128 // meta_diff.shape[-1]
         ulp = lambda a, b: np.abs(a.view(np.int16).astype(np.int32) - b.view(np.int16).astype(np.int32))
         assert np.all(ulp(sg, sr)[meta_diff] <= 1) and np.all(ulp(zg, zr)[meta_diff] <= 1), \
             f"{name}: scale/zero differ by more than one fp16 ulp"
         bad = cg != cr                                             # [n, H, 128]
-        grp_meta = np.repeat(meta_diff, 32, axis=-1)
-        s = np.repeat(sr.astype(np.float64), 32, axis=-1)
-        z = np.repeat(zr.astype(np.float64), 32, axis=-1)
+        grp_meta = np.repeat(meta_diff, G, axis=-1)
+        s = np.repeat(sr.astype(np.float64), G, axis=-1)
+        z = np.repeat(zr.astype(np.float64), G, axis=-1)
         t = np.where(s > 0, (x.astype(np.float64) - z) / np.where(s > 0, s, 1), 0)
         near_tie = np.abs(t - np.floor(t) - 0.5) < 1e-3
         unexplained = bad & ~grp_meta & ~near_tie

@@ -78,3 +78,13 @@ def test_decode_rejects_unknown_weight_format_without_launch():
     st = lib.int2kv_decode(ctypes.byref(good), 16, 1, 4, 16, 1, 16, 16, 16, 16, 16, 256, 4, 16, 256, 1 << 30, None)
     assert st == K.INT2KV_EINVAL
     assert b"wo_format" in lib.int2kv_last_error()
+
+
+def test_record_bytes_and_group_sizes():
+    assert K.int2kv_record_bytes(32) == 1536 == K.RECORD_BYTES_BY_GROUP[32]
+    assert K.int2kv_record_bytes(128) == 1152 == K.RECORD_BYTES_BY_GROUP[128]
+    assert K.int2kv_record_bytes(64) == 0
+    lib = K.load_library()
+    bad = K._Cache(16, 4, 2, 16, 128, 64)
+    st = lib.int2kv_quantize_append(ctypes.byref(bad), None, None, None, 4, None, None, None, 1.0, 1.0, None)
+    assert st == K.INT2KV_EUNSUPPORTED and b"group_size" in lib.int2kv_last_error()

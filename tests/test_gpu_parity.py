@@ -32,9 +32,10 @@ def _rotated_rows(w):
 
 
 # ----------------------------------------------------------------------------- cache write
+@pytest.mark.parametrize("G", [32, 128])
 @pytest.mark.parametrize("clip", [(1.0, 1.0), (0.96, 0.92)])
-def test_pack_rotated_is_bit_exact(clip):
-    print(f"\n[pack_rotated] clip={clip}", flush=True)
+def test_pack_rotated_is_bit_exact(clip, G):
+    print(f"\n[pack_rotated] clip={clip} G={G}", flush=True)
     w = W.make_workload(1, batch=3, ctx=None, ctx_lens=np.array([100, 1, 47]), num_q_heads=8, num_kv_heads=8)
     k_rot, v_rot, slots = _rotated_rows(w)
     # special rows: a degenerate group, a huge-range group, exact grid values
@@ -43,7 +44,7 @@ def test_pack_rotated_is_bit_exact(clip):
     k_rot[2, 1, 64:96] = (np.arange(32) % 4).astype(np.float32) * 0.5 - 1.0
     slots_in = slots.copy()
     slots_in[5] = -1  # skipped token
-    ref = O.new_pool(w.num_blocks, w.num_kv_heads)
+    ref = O.new_pool(w.num_blocks, w.num_kv_heads, G)
     keep = slots_in >= 0
     O.quantize_pack_rotated(ref, k_rot[keep], v_rot[keep], slots_in[keep], *clip)
     cache = gpu_cache(np.zeros_like(ref))
@@ -59,13 +60,14 @@ def test_prepare_mu_rot_matches_oracle():
     assert np.abs(mu_rk - ref).max() <= 1e-5 * np.abs(ref).max()
 
 
+@pytest.mark.parametrize("G", [32, 128])
 @pytest.mark.parametrize("clip", [(1.0, 1.0), (0.96, 0.92)])
-def test_append_matches_oracle_up_to_ties(clip):
-    print(f"\n[append] clip={clip}", flush=True)
+def test_append_matches_oracle_up_to_ties(clip, G):
+    print(f"\n[append] clip={clip} G={G}", flush=True)
     w = W.make_workload(4, batch=6, ctx_lens=np.array([700, 33, 1, 16, 250, 401]))
     k_rot, v_rot, slots = _rotated_rows(w)
-    ref = oracle_pool(w, clip_k=clip[0], clip_v=clip[1])
-    cache = K.Int2KVCache(w.num_blocks, w.num_kv_heads)
+    ref = oracle_pool(w, clip_k=clip[0], clip_v=clip[1], group=G)
+    cache = K.Int2KVCache(w.num_blocks, w.num_kv_heads, group_size=G)
     mu_rk = K.int2kv_prepare_mu_rot(dev(w.R_k), dev(w.mu))
     Rk, Rv = dev(w.R_k), dev(w.R_v)
     for b in range(w.batch):
@@ -75,15 +77,16 @@ def test_append_matches_oracle_up_to_ties(clip):
     print(stats, flush=True)
 
 
-def test_append_one_call_many_tokens_matches_oracle():
+@pytest.mark.parametrize("G", [32, 128])
+def test_append_one_call_many_tokens_matches_oracle(G):
     """All sequences in one call (the prefill-sized path), tokens in a shuffled order."""
     w = W.make_workload(3, batch=2, ctx=1200)
     k_rot, v_rot, slots = _rotated_rows(w)
-    ref = oracle_pool(w)
+    ref = oracle_pool(w, group=G)
     kk, vv = zip(*[w.kv(b) for b in range(w.batch)])
     k, v = np.concatenate(kk), np.concatenate(vv)
     perm = np.random.default_rng(0).permutation(slots.size)
-    cache = K.Int2KVCache(w.num_blocks, w.num_kv_heads)
+    cache = K.Int2KVCache(w.num_blocks, w.num_kv_heads, group_size=G)
     mu_rk = K.int2kv_prepare_mu_rot(dev(w.R_k), dev(w.mu))
     K.int2kv_quantize_append(cache, dev(k[perm]), dev(v[perm]), dev(slots[perm]), dev(w.R_k), dev(w.R_v), mu_rk)
     stats = compare_cache_writes(cache.pool.cpu().numpy(), ref, slots, k_rot, v_rot)
@@ -252,3 +255,63 @@ def test_append_decode_matches_separate_calls_and_oracle(variant):
                                 wo_format=K.INT2KV_WO_PREPARED_FOLDED, d_model=dm)
     assert torch.equal(y2, y1)
     print(f"worst row error {worst:.2e}", flush=True)
+
+
+# 128-channel groups (the paper's setting): the vector-ALU scan, with and without W_O and through
+# int2kv_append_decode
+G128_CASES = [
+    (1, 3, 8, 2, [1, 17, 300], None),
+    (4, 3, 10, 2, [1500, 2, 129], 256),
+    (1, 4, 32, 8, [1000, 33, 16, 0], 96),
+]
+
+
+@pytest.mark.parametrize("case", G128_CASES, ids=lambda c: f"cfg{c[0]}-B{c[1]}-{c[2]}x{c[3]}-dm{c[5]}")
+def test_decode_group128_matches_oracle(case):
+    cfg, B, Hq, H, lens, dm = case
+    print(f"\n[decode G=128] case={case}", flush=True)
+    w = W.make_workload(cfg, batch=B, ctx_lens=np.array(lens), num_q_heads=Hq, num_kv_heads=H, d_model=dm)
+    pool = oracle_pool(w, group=128)
+    ref = O.decode(pool, w.q, w.block_table, w.ctx_lens, w.R_k, w.R_v, w.W_o)
+    cache = gpu_cache(pool)
+    args = (cache, dev(w.q), dev(w.block_table), dev(w.ctx_lens), int(max(lens)), dev(w.R_k), dev(w.R_v))
+    out = K.int2kv_decode(*args, W_o=dev(w.W_o) if dm else None)
+    worst = assert_rows_close(out.cpu().numpy(), ref, what="decode G=128")
+    assert torch.equal(out, K.int2kv_decode(*args, W_o=dev(w.W_o) if dm else None))
+    if dm:
+        Wp = K.int2kv_prepare_wo(dev(w.W_o), dev(w.R_v), Hq)
+        out_p = K.int2kv_decode(*args, W_o=Wp, wo_format=K.INT2KV_WO_PREPARED_FOLDED, d_model=dm)
+        assert_rows_close(out_p.cpu().numpy(), ref, what="decode G=128, prepared W_O")
+    print(f"worst row error {worst:.2e}", flush=True)
+
+
+def test_append_decode_group128():
+    """int2kv_append_decode at G = 128 (cache write as its own launch before the vector-ALU decode)
+    leaves the pool and outputs of the two separate calls."""
+    lens = np.array([300, 17, 1, 129])
+    Hq, H = 16, 4
+    w = W.make_workload(1, batch=lens.size, ctx_lens=lens, num_q_heads=Hq, num_kv_heads=H)
+    Rk, Rv = dev(w.R_k), dev(w.R_v)
+    mu_rk = K.int2kv_prepare_mu_rot(Rk, dev(w.mu))
+    caches = [K.Int2KVCache(w.num_blocks, H, group_size=128) for _ in range(2)]
+    k_last, v_last, s_last = [], [], []
+    for b in range(w.batch):
+        k, v = w.kv(b, as_torch=True)
+        L = int(lens[b])
+        slots = w.slot_mapping(b)
+        if L > 1:
+            for c in caches:
+                K.int2kv_quantize_append(c, k[:L - 1].cuda(), v[:L - 1].cuda(), dev(slots[:L - 1]), Rk, Rv, mu_rk)
+        k_last.append(k[L - 1])
+        v_last.append(v[L - 1])
+        s_last.append(slots[L - 1])
+    kl, vl = torch.stack(k_last).cuda(), torch.stack(v_last).cuda()
+    sl = dev(np.array(s_last, np.int32))
+    dargs = (dev(w.q), dev(w.block_table), dev(w.ctx_lens), int(lens.max()), Rk, Rv)
+    K.int2kv_quantize_append(caches[0], kl, vl, sl, Rk, Rv, mu_rk)
+    y0 = K.int2kv_decode(caches[0], *dargs)
+    y1 = K.int2kv_append_decode(caches[1], kl, vl, sl, mu_rk, *dargs)
+    torch.cuda.synchronize()
+    assert torch.equal(caches[0].pool, caches[1].pool) and torch.equal(y0, y1)
+    ref = O.decode(caches[1].pool.cpu().numpy(), w.q, w.block_table, w.ctx_lens, w.R_k, w.R_v)
+    assert_rows_close(y1.cpu().numpy(), ref, what="append_decode G=128")
