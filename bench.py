@@ -83,7 +83,7 @@ class HipEvents:
             self.hip.hipEventDestroy(self.ct.c_void_p(b))
 
 
-def cpu_baseline(w, target_s):
+def cpu_baseline(w, target_s, group=32):
     """Time the CPU oracle's decode (with W_O) on a bounded sample of this workload's sequences."""
     from oracle import int2kv_oracle as O
     try:
@@ -97,7 +97,7 @@ def cpu_baseline(w, target_s):
     for b in range(w.batch):
         L = int(w.ctx_lens[b])
         nblk = (L + 15) // 16
-        pool = O.new_pool(nblk, w.num_kv_heads)
+        pool = O.new_pool(nblk, w.num_kv_heads, group)
         table = np.arange(nblk, dtype=np.int32)[None]
         k, v = w.kv(b)
         pos = np.arange(L)
@@ -133,6 +133,9 @@ def main():
     ap.add_argument("--wo", choices=("prepared", "folded", "plain"), default="prepared",
                     help="output-projection weights: prepared fp16 tiles with R_V folded in (default), row-major "
                          "bf16 folded with R_V, or row-major bf16 W_O with the merge un-rotating o")
+    ap.add_argument("--group", type=int, default=32, choices=(32, 128),
+                    help="INT2 group size of the cache (32; 128 is the paper's serving setting: 72 instead of 96 "
+                         "bytes per token and KV head)")
     ap.add_argument("--separate", action="store_true",
                     help="append and decode as two calls (default: int2kv_append_decode, the cache write beside "
                          "the query preparation)")
@@ -178,7 +181,7 @@ def main():
     log(f"workload cfg{args.config}: B={B} Hq={Hq} H={H} sum(L)={int(lens.sum())} max(L)={int(lens.max())}")
 
     dev = lambda a: torch.from_numpy(a.view(np.int16).copy() if a.dtype == np.uint16 else np.ascontiguousarray(a)).cuda()
-    cache = K.Int2KVCache(w.num_blocks, H)
+    cache = K.Int2KVCache(w.num_blocks, H, group_size=args.group)
     Rk, Rv = dev(w.R_k), dev(w.R_v)
     mu_rk = K.int2kv_prepare_mu_rot(Rk, dev(w.mu))
     q = dev(w.q)
@@ -284,10 +287,11 @@ def main():
 
     tokens = int(lens.sum())
     pages = int(((lens + 15) // 16).sum())
-    scan_bytes = 96 * H * tokens + 4 * pages
+    tok_bytes = 64 + 8 * (128 // args.group)  # K and V codes + one (s, z) fp16 pair per group each: 96 or 72
+    scan_bytes = tok_bytes * H * tokens + 4 * pages
     step_bytes = (scan_bytes + B * Hq * 256 + (B * d_model * 4 if d_model else B * Hq * 512)
                   + 2 * H * 128 * 128 * 4 + (2 * d_model * Hq * 128 if d_model else 0)
-                  + B * H * (512 + 96))
+                  + B * H * (512 + tok_bytes))
     scan_gbps = scan_bytes / (scan_ms * 1e-3) / 1e9
     step_gbps = step_bytes / (ms_step * 1e-3) / 1e9
     traffic = counter_traffic(f"decode_scan_cfg{args.config}", 1)
@@ -311,7 +315,7 @@ def main():
         "config": {
             "workload": w.cfg.name if not args.ctx else f"{w.cfg.name}; context set to a uniform {args.ctx}",
             "config_id": args.config, "batch": B, "num_q_heads": Hq, "num_kv_heads": H, "head_dim": 128, "block_size": 16,
-            "group_size": 32, "sum_ctx": tokens, "max_ctx": max_ctx, "d_model": d_model,
+            "group_size": args.group, "sum_ctx": tokens, "max_ctx": max_ctx, "d_model": d_model,
             "chunk_tokens": args.chunk or "auto", "variant": args.variant or "auto",
             "step_calls": ("int2kv_quantize_append + int2kv_decode" if args.separate else
                            "int2kv_append_decode (cache write inside the preparation launch)"),
@@ -335,7 +339,7 @@ def main():
         "context": {"hbm_copy_gbps": copy_gbps, "copy": "1 GiB device-to-device copy, read + write bytes"},
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.group)
     print(json.dumps(result), flush=True)
 
 

@@ -67,8 +67,7 @@ typedef enum {
 
 /* The paged INT2 cache. `pool` points to num_blocks * num_kv_heads * int2kv_record_bytes(group_size)
  * bytes (device, 16-byte aligned). The caller zero-fills it once; every slot is rewritten in full
- * by an append, so no clearing is needed when blocks are reused. Decode over a cache with
- * group_size 128 runs the vector-ALU scan (the matrix-core scan serves 32-channel groups). */
+ * by an append, so no clearing is needed when blocks are reused. */
 typedef struct int2kv_cache {
   void* pool;
   int32_t num_blocks;

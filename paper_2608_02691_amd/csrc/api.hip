@@ -77,10 +77,10 @@ namespace {
 DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model, int groups) {
   DecodePlan p{};
   const int gq = Hq / H;
-  // the matrix-core scan serves up to 8 query heads per KV head and groups of 32 channels; wider
-  // head groups and 128-channel groups use the vector-ALU scan (also when the tuning knob asks for
-  // the matrix-core one)
-  const bool mfma_ok = gq <= 8 && groups == 4 && mfma_decode_available();
+  // the matrix-core scan serves up to 8 query heads per KV head; wider groups use the vector-ALU
+  // scan (also when the tuning knob asks for the matrix-core one)
+  (void)groups;
+  const bool mfma_ok = gq <= 8 && mfma_decode_available();
   p.variant = g_variant_override == 1 || !mfma_ok ? 1 : 2;
   int chunk = g_chunk_override;
   if (chunk <= 0) {

@@ -293,23 +293,41 @@ __device__ __forceinline__ PageEnt load_ent(ent_ptr p, int i) {
 // DMA of one page pair into the staging slot at lds_addr. (a_lo, a_hi), (b_lo, b_hi): records of KV
 // head 0 of the two pages; voff16 = 16 l + 1536 h selects head h for the codes; moff = (the record of
 // page 0 or, for lanes 32..63, page 1) + 1536 h + 1024 + 16 (l % 32) is the lane's metadata address.
+// With one group per token (NG = 1) a page has 128 B of metadata: one dword load, lanes 0..31 and
+// 32..63 reading 4 bytes of page 0 and page 1.
+template <int NG>
 __device__ __forceinline__ void dma_pair(uint32_t a_lo, uint32_t a_hi, uint32_t b_lo, uint32_t b_hi, uint32_t lds_addr,
                                          uint32_t voff16, uint64_t moff_head, bool upper) {
   const uint8_t* ra = reinterpret_cast<const uint8_t*>(((uint64_t)a_hi << 32) | a_lo);
   const uint8_t* rb = reinterpret_cast<const uint8_t*>(((uint64_t)b_hi << 32) | b_lo);
   const uint64_t maddr = ((uint64_t)(upper ? b_hi : a_hi) << 32 | (upper ? b_lo : a_lo)) + moff_head;
-  asm volatile(
-      "s_mov_b32 m0, %0\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %3, %4\n\t"
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %3, %5\n\t"
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %6, off" ::"s"(lds_addr),
-      "s"(lds_addr + 1024), "s"(lds_addr + 2048), "v"(voff16), "s"(ra), "s"(rb), "v"(maddr)
-      : "memory", "m0");
+  if constexpr (NG == 4) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %3, %4\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %3, %5\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %6, off" ::"s"(lds_addr),
+        "s"(lds_addr + 1024), "s"(lds_addr + 2048), "v"(voff16), "s"(ra), "s"(rb), "v"(maddr)
+        : "memory", "m0");
+  } else {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %3, %4\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %3, %5\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dword %6, off" ::"s"(lds_addr),
+        "s"(lds_addr + 1024), "s"(lds_addr + 2048), "v"(voff16), "s"(ra), "s"(rb), "v"(maddr)
+        : "memory", "m0");
+  }
 }
 
 // Operands of one page pair read back from its staging slot. Tokens a page does not hold (past the
@@ -328,24 +346,34 @@ __device__ __forceinline__ void pin_pair(PairLoads<WIDE>& p) {
     if constexpr (WIDE) asm volatile("" : "+v"(p.vs[P][1].x), "+v"(p.vs[P][1].y));
   }
 }
-template <bool WIDE>
+// With one group per token (NG = 1) the token's single (s, z) is read into all four group slots:
+// the score sum_g s_g D_g + sum_g z_g Q_g then equals s D + z Q over the 128 channels, and the
+// value weights of every group column use the token's one scale and zero.
+template <bool WIDE, int NG>
 __device__ __forceinline__ void read_pair(const uint8_t* slot, uint32_t nv0, uint32_t nv1, int lo, int hi,
                                           PairLoads<WIDE>& p) {
+  using L = Rec<NG>;
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
-    const uint8_t* rec = slot + P * 1024;               // codes of page P (record offsets < 1024)
-    const uint8_t* met = slot + 2048 + P * 512 - 1024;  // metadata of page P (record offsets >= 1024)
+    const uint8_t* rec = slot + P * 1024;                    // codes of page P (record offsets < 1024)
+    const uint8_t* met = slot + 2048 + P * 128 * NG - 1024;  // metadata of page P (record offsets >= 1024)
     p.nv[P] = P == 0 ? nv0 : nv1;
     p.kc[P] = *reinterpret_cast<const uint2*>(rec + kOffKCodes + 32 * lo + 8 * hi);
-    p.km[P] = *reinterpret_cast<const uint4*>(met + kOffKMeta + 16 * lo);
-    p.vc[P] = *reinterpret_cast<const uint2*>(rec + kOffVCodes + 32 * lo + 8 * hi);
-    if constexpr (WIDE) {
-      p.vs[P][0] = *reinterpret_cast<const uint2*>(met + kOffVScale + 32 * (lo & 1) + 8 * hi);
-      p.vs[P][1] = *reinterpret_cast<const uint2*>(met + kOffVScale + 32 * (2 + (lo & 1)) + 8 * hi);
+    if constexpr (NG == 4) {
+      p.km[P] = *reinterpret_cast<const uint4*>(met + L::kOffKMeta + 16 * lo);
     } else {
-      p.vs[P][0] = *reinterpret_cast<const uint2*>(met + kOffVScale + 32 * (lo & 3) + 8 * hi);
+      const uint32_t m = *reinterpret_cast<const uint32_t*>(met + L::kOffKMeta + 4 * lo);
+      p.km[P] = make_uint4(m, m, m, m);
     }
-    p.vz[P] = *reinterpret_cast<const uint2*>(met + kOffVZero + 32 * (lo & 3) + 8 * hi);
+    p.vc[P] = *reinterpret_cast<const uint2*>(rec + kOffVCodes + 32 * lo + 8 * hi);
+    constexpr int gs = NG == 4 ? 32 : 0;  // bytes between the V metadata of consecutive groups
+    if constexpr (WIDE) {
+      p.vs[P][0] = *reinterpret_cast<const uint2*>(met + L::kOffVScale + gs * (lo & 1) + 8 * hi);
+      p.vs[P][1] = *reinterpret_cast<const uint2*>(met + L::kOffVScale + gs * (2 + (lo & 1)) + 8 * hi);
+    } else {
+      p.vs[P][0] = *reinterpret_cast<const uint2*>(met + L::kOffVScale + gs * (lo & 3) + 8 * hi);
+    }
+    p.vz[P] = *reinterpret_cast<const uint2*>(met + L::kOffVZero + gs * (lo & 3) + 8 * hi);
   }
 }
 template <int X>
@@ -657,7 +685,7 @@ __device__ void page_list_block(const DecodeArgs& a, int b, int p0, uint8_t* lds
 #pragma unroll
   for (int u = 0; u < 4; ++u) id[u] = 4 * tid + u < n ? row[4 * tid + u] : 0;
   const uint64_t pool = (uint64_t)(uintptr_t)a.pool;
-  const uint64_t stride = (uint64_t)a.H * kRecord;
+  const uint64_t stride = (uint64_t)a.H * (1024 + 128 * a.groups);
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const int i = 4 * tid + u;
@@ -683,8 +711,12 @@ __global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int wide, int 
   int blk = blockIdx.x;
   if (blk < nap) {
     const int bx = blk % ap.nbx, r = blk / ap.nbx;
-    append_block<1, 4, 4>(ap.cv, ap.k, ap.v, ap.slots, ap.n, ap.R_k, ap.R_v, ap.mu_rk, ap.clip_k, ap.clip_v, bx, ap.nbx,
-                       r % ap.cv.num_kv_heads, r / ap.cv.num_kv_heads, lds);
+    if (ap.cv.groups == 1)
+      append_block<1, 4, 1>(ap.cv, ap.k, ap.v, ap.slots, ap.n, ap.R_k, ap.R_v, ap.mu_rk, ap.clip_k, ap.clip_v, bx,
+                            ap.nbx, r % ap.cv.num_kv_heads, r / ap.cv.num_kv_heads, lds);
+    else
+      append_block<1, 4, 4>(ap.cv, ap.k, ap.v, ap.slots, ap.n, ap.R_k, ap.R_v, ap.mu_rk, ap.clip_k, ap.clip_v, bx,
+                            ap.nbx, r % ap.cv.num_kv_heads, r / ap.cv.num_kv_heads, lds);
     return;
   }
   blk -= nap;
@@ -700,7 +732,7 @@ __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)
 
 // One wave: KV head h of sequence b, global pages [gs, ge) (all of sequence b), with its partial
 // (m, l, O') per query head written to partial slot `slot`.
-template <bool WIDE>
+template <bool WIDE, int NG>
 __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, int gs, int ge, int slot, int l,
                                              uint8_t* stage_w, _Float16 (*p_w)[2][8][kBlock], float* al_w,
                                              bool all_waves) {
@@ -753,8 +785,8 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   // ---- pipeline over the segment's page pairs (global pages gs + 2k, gs + 2k + 1; the second page
   // of a last pair of one page is a stand-in: block 0, no tokens). Pair k sits in slot k % kStages.
   const ent_ptr ent = (ent_ptr)(uintptr_t)(a.pages) + gs;
-  const uint32_t voff16 = 16 * l + h * kRecord;
-  const uint64_t moff = (uint64_t)(h * kRecord + 1024 + 16 * (l & 31));
+  const uint32_t voff16 = 16 * l + h * Rec<NG>::kBytes;
+  const uint64_t moff = (uint64_t)(h * Rec<NG>::kBytes + 1024 + (NG == 4 ? 16 : 4) * (l & 31));
   const bool upper = l >= 32;
   const uint32_t pool_lo = (uint32_t)(uintptr_t)a.pool, pool_hi = (uint32_t)((uintptr_t)a.pool >> 32);
   uint32_t nv[kStages][2];  // cached tokens of the two pages staged in each slot
@@ -772,7 +804,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   auto stage = [&](auto slot_tag, const PageEnt& e0, const PageEnt& e1) {
     constexpr int SL = decltype(slot_tag)::value;
     const uint32_t sa = stage_base + SL * 2 * kRecord;
-    dma_pair(e0.lo, e0.hi, e1.lo, e1.hi, sa, voff16, moff, upper);
+    dma_pair<NG>(e0.lo, e0.hi, e1.lo, e1.hi, sa, voff16, moff, upper);
     nv[SL][0] = e0.nv;
     nv[SL][1] = e1.nv;
   };
@@ -800,7 +832,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kDmaPerPair * (kStages - 1)) : "memory");
     else
       wait_vm_all();
-    read_pair(stage_w, nv[0][0], nv[0][1], lo, hi, X);
+    read_pair<WIDE, NG>(stage_w, nv[0][0], nv[0][1], lo, hi, X);
     pin_pair(X);
     if (kStages < npairs) {
       PageEnt e0, e1;
@@ -826,7 +858,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
         asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kDmaPerPair * (kStages - 1)) : "memory");
       else
         wait_vm_all();
-      read_pair(stage_w + SL * 2 * kRecord, nv[SL][0], nv[SL][1], lo, hi, nxt);
+      read_pair<WIDE, NG>(stage_w + SL * 2 * kRecord, nv[SL][0], nv[SL][1], lo, hi, nxt);
       pin_pair(nxt);
       if (STEADY) {
         // The entries read one step ago are pinned (their wait placed) before the next loads issue:
@@ -944,7 +976,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
 // of one block together. A range crossing sequence boundaries is scanned segment by segment; the
 // partial of (group g, sequence b) goes to slot g + b, which is unique because the (g, b) pairs
 // that meet form a monotone staircase.
-template <bool WIDE>
+template <bool WIDE, int NG>
 __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t stage[kWavesPerWG][kStages][2][kRecord];
   __shared__ _Float16 p_lds[kWavesPerWG][2][2][8][kBlock];
@@ -970,7 +1002,7 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   for (int pos = s;;) {
     const int seg_end = min(e, Sb1);
     const int Sb2 = seg_end < e ? prefix[b + 2] : 0;  // next sequence's end, fetched ahead
-    scan_segment<WIDE>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w], all_waves);
+    scan_segment<WIDE, NG>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w], all_waves);
     pos = seg_end;
     if (pos >= e) break;
     ++b;
@@ -1121,10 +1153,14 @@ hipError_t launch_decode_split_mfma(const DecodeArgs& a, hipStream_t s, hipEvent
   if (a.gq > 8) return hipErrorNotSupported;
   dim3 grid(a.grid_g, (a.H + kWavesPerWG - 1) / kWavesPerWG);
   const int threads = 64 * min(a.H, kWavesPerWG);
-  if (a.gq > 4)
-    hipExtLaunchKernelGGL(decode_scan_flat_kernel<true>, grid, dim3(threads), 0, s, ev0, ev1, 0, a);
+  if (a.gq > 4 && a.groups == 1)
+    hipExtLaunchKernelGGL((decode_scan_flat_kernel<true, 1>), grid, dim3(threads), 0, s, ev0, ev1, 0, a);
+  else if (a.gq > 4)
+    hipExtLaunchKernelGGL((decode_scan_flat_kernel<true, 4>), grid, dim3(threads), 0, s, ev0, ev1, 0, a);
+  else if (a.groups == 1)
+    hipExtLaunchKernelGGL((decode_scan_flat_kernel<false, 1>), grid, dim3(threads), 0, s, ev0, ev1, 0, a);
   else
-    hipExtLaunchKernelGGL(decode_scan_flat_kernel<false>, grid, dim3(threads), 0, s, ev0, ev1, 0, a);
+    hipExtLaunchKernelGGL((decode_scan_flat_kernel<false, 4>), grid, dim3(threads), 0, s, ev0, ev1, 0, a);
   return hipGetLastError();
 }
 

@@ -257,19 +257,22 @@ def test_append_decode_matches_separate_calls_and_oracle(variant):
     print(f"worst row error {worst:.2e}", flush=True)
 
 
-# 128-channel groups (the paper's setting): the vector-ALU scan, with and without W_O and through
+# 128-channel groups (the paper's setting): both scans, with and without W_O and through
 # int2kv_append_decode
 G128_CASES = [
     (1, 3, 8, 2, [1, 17, 300], None),
+    (4, 2, 5, 1, [700, 64], None),
     (4, 3, 10, 2, [1500, 2, 129], 256),
     (1, 4, 32, 8, [1000, 33, 16, 0], 96),
 ]
 
 
+@pytest.mark.parametrize("variant", [1, 2])
 @pytest.mark.parametrize("case", G128_CASES, ids=lambda c: f"cfg{c[0]}-B{c[1]}-{c[2]}x{c[3]}-dm{c[5]}")
-def test_decode_group128_matches_oracle(case):
+def test_decode_group128_matches_oracle(case, variant):
     cfg, B, Hq, H, lens, dm = case
-    print(f"\n[decode G=128] case={case}", flush=True)
+    print(f"\n[decode G=128] case={case} variant={variant}", flush=True)
+    K.int2kv_set_decode_tuning(0, variant)
     w = W.make_workload(cfg, batch=B, ctx_lens=np.array(lens), num_q_heads=Hq, num_kv_heads=H, d_model=dm)
     pool = oracle_pool(w, group=128)
     ref = O.decode(pool, w.q, w.block_table, w.ctx_lens, w.R_k, w.R_v, w.W_o)
@@ -285,9 +288,11 @@ def test_decode_group128_matches_oracle(case):
     print(f"worst row error {worst:.2e}", flush=True)
 
 
-def test_append_decode_group128():
-    """int2kv_append_decode at G = 128 (cache write as its own launch before the vector-ALU decode)
-    leaves the pool and outputs of the two separate calls."""
+@pytest.mark.parametrize("variant", [1, 2])
+def test_append_decode_group128(variant):
+    """int2kv_append_decode at G = 128 (inside the preparation launch of the matrix-core decode, or
+    its own launch before the vector-ALU decode) leaves the pool and outputs of the two calls."""
+    K.int2kv_set_decode_tuning(0, variant)
     lens = np.array([300, 17, 1, 129])
     Hq, H = 16, 4
     w = W.make_workload(1, batch=lens.size, ctx_lens=lens, num_q_heads=Hq, num_kv_heads=H)
