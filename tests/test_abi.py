@@ -88,3 +88,24 @@ def test_record_bytes_and_group_sizes():
     bad = K._Cache(16, 4, 2, 16, 128, 64)
     st = lib.int2kv_quantize_append(ctypes.byref(bad), None, None, None, 4, None, None, None, 1.0, 1.0, None)
     assert st == K.INT2KV_EUNSUPPORTED and b"group_size" in lib.int2kv_last_error()
+
+
+def test_append_decode_rejects_bad_arguments_without_launch():
+    lib = K.load_library()
+    good = K._Cache(16, 4, 2, 16, 128, 32)
+    # tokens given but no key rows
+    st = lib.int2kv_append_decode(ctypes.byref(good), None, 16, 16, 4, 16, 1.0, 1.0, 16, 1, 4, 16, 1, 16, 16,
+                                  16, 16, None, 0, 0, 16, 256, 1 << 30, None)
+    assert st == K.INT2KV_EINVAL and b"NULL" in lib.int2kv_last_error()
+    # clip ratio out of range
+    st = lib.int2kv_append_decode(ctypes.byref(good), 16, 16, 16, 4, 16, 1.5, 1.0, 16, 1, 4, 16, 1, 16, 16,
+                                  16, 16, None, 0, 0, 16, 256, 1 << 30, None)
+    assert st == K.INT2KV_EINVAL and b"clip" in lib.int2kv_last_error()
+    # negative token count
+    st = lib.int2kv_append_decode(ctypes.byref(good), 16, 16, 16, -1, 16, 1.0, 1.0, 16, 1, 4, 16, 1, 16, 16,
+                                  16, 16, None, 0, 0, 16, 256, 1 << 30, None)
+    assert st == K.INT2KV_EINVAL
+    # decode arguments are checked too: a workspace that is too small
+    st = lib.int2kv_append_decode(ctypes.byref(good), 16, 16, 16, 4, 16, 1.0, 1.0, 16, 1, 4, 16, 1, 16, 16,
+                                  16, 16, None, 0, 0, 16, 256, 16, None)
+    assert st == K.INT2KV_EWORKSPACE
