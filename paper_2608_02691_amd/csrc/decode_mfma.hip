@@ -408,13 +408,14 @@ struct ScanState {
   float4_t wsum[NT];            // sum_t w_t of each column (every row); wide: groups gg, 2 + gg
   float4_t zl;                  // rows 0..3: sum_t p_t z_tg (row = group); rows 4..7: sum_t p_t
   float mref[NJ];
+  float Qz[NJ];                 // sum_k q'_jk of query head jq(hi, u) (used with one group per token)
   LandK lk;                     // landing constants
 };
 
 // Scores of one page pair, base-2 logits, -inf where masked: a2[P][u] for token lo of page P and
 // query head jq(hi, u). The accumulation chains of both pages are issued interleaved so that each
 // hides the others' latency.
-template <bool WIDE>
+template <bool WIDE, int NG>
 __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoads<WIDE>& cur, int lo,
                                         float (&a2)[2][ScanState<WIDE>::NJ]) {
   constexpr int NT = ScanState<WIDE>::NT, NJ = ScanState<WIDE>::NJ;
@@ -445,6 +446,21 @@ __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoa
 #pragma unroll
       for (int P = 0; P < 2; ++P) d[P][0] = mfma16(st.A[i], B[P][i], d[P][0]);
   }
+  if constexpr (NG == 1) {
+    // one (s, z) per token: score = s sum_g D_g + z Q_j (no matrix-core zero term)
+#pragma unroll
+    for (int P = 0; P < 2; ++P) {
+      const half2_t m = as_h2(cur.km[P].x);
+#pragma unroll
+      for (int u = 0; u < NJ; ++u) {
+        float Dg[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) Dg[g] = WIDE ? d[P][g >> 1][2 * u + (g & 1)] : d[P][0][g];
+        const float Ds = ((Dg[0] + Dg[1]) + Dg[2]) + Dg[3];
+        a2[P][u] = fmaf((float)m.x * Ds, st.invsig[u], (float)m.y * st.Qz[u]);
+      }
+    }
+  } else {
   // Zero term on the matrix cores: rows (j, 0) of zd = sum_g Q_jg z_tg, with z_tg exact in fp16 (the
   // B operand: z_t0..z_t3 of token t twice, for the high and the low term of Q)
   float4_t zd[2];
@@ -471,6 +487,7 @@ __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoa
       sd = fmaf((float)m[3].x, Dg[3], sd);
       a2[P][u] = fmaf(sd, st.invsig[u], zd[P][WIDE ? 2 * u : 0]);
     }
+  }
   }
   // tokens a page does not hold get -inf (a wave-uniform branch, taken only for partial pages)
   if (cur.nv[0] < (uint32_t)kBlock || cur.nv[1] < (uint32_t)kBlock) {
@@ -525,10 +542,12 @@ __device__ __forceinline__ void softmax_pair(ScanState<WIDE>& st, const float (&
 
 // Value accumulation of one pair: K = the pair's 32 tokens, N = the 16 columns, M = 8 tiles of 16
 // channels; p comes back from LDS in the layout of the B operand.
-template <bool WIDE>
+template <bool WIDE, int NG>
 __device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WIDE>& cur, int lo, int hi,
                                         const _Float16 (*p_w)[8][kBlock]) {
-  constexpr int NT = ScanState<WIDE>::NT;
+  // with one group per token every group column has the same weights: one weight operand (and one
+  // weight sum) serves all tiles
+  constexpr int NT = NG == 1 ? 1 : ScanState<WIDE>::NT;
   // A operand of the (Z, l) contraction: rows 0..3 hold z of group `row` (the V zeros this lane
   // already has, group lo & 3 = row), rows 4..7 hold 1.0, rows 8..15 zero
   const half2_t zmul = lo < 4 ? half2_t{(_Float16)1.0f, (_Float16)1.0f} : half2_t{(_Float16)0.0f, (_Float16)0.0f};
@@ -558,7 +577,7 @@ __device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WID
   // ALU beside them (measured: -2 % scan time at 5 query heads per KV head)
   __builtin_amdgcn_s_setprio(1);
 #define INT2KV_PV_TILE(MT)                                                                        \
-  st.acc[MT] = mfma16(v_operand<MT>(cur.vc[0], cur.vc[1], st.lk), Bw[WIDE ? (MT) >> 2 : 0], st.acc[MT]);
+  st.acc[MT] = mfma16(v_operand<MT>(cur.vc[0], cur.vc[1], st.lk), Bw[WIDE && NT == 2 ? (MT) >> 2 : 0], st.acc[MT]);
   INT2KV_PV_TILE(0)
   INT2KV_PV_TILE(1)
   INT2KV_PV_TILE(2)
@@ -780,6 +799,11 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   st.zl = float4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int u = 0; u < NJ; ++u) st.mref[u] = kMaxInit;
+#pragma unroll
+  for (int u = 0; u < NJ; ++u) {  // q' sums of the lane's score heads (rows of absent heads are zero)
+    const float4_t Q = *reinterpret_cast<const float4_t*>(cst + (WIDE ? 32 : 16) + 4 * (NJ * hi + u));
+    st.Qz[u] = ((Q[0] + Q[1]) + Q[2]) + Q[3];
+  }
   st.lk = land_constants();
 
   // ---- pipeline over the segment's page pairs (global pages gs + 2k, gs + 2k + 1; the second page
@@ -840,7 +864,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
       stage(std::integral_constant<int, 0>{}, e0, e1);
     }
     float a2[2][NJ];
-    qk_pair<WIDE>(st, X, lo, a2);
+    qk_pair<WIDE, NG>(st, X, lo, a2);
     softmax_pair<WIDE>(st, a2, lo, hi, p_w[0], al_w);
   }
   // Step J of an unrolled group that starts at pair k (k % kUnroll = 0): read pair kk + 1 =
@@ -877,9 +901,9 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
       }
     }
     float a2[2][NJ];
-    if (more) qk_pair<WIDE>(st, nxt, lo, a2);
+    if (more) qk_pair<WIDE, NG>(st, nxt, lo, a2);
     lds_sync_wave();
-    pv_pair<WIDE>(st, cur, lo, hi, p_w[kk & 1]);
+    pv_pair<WIDE, NG>(st, cur, lo, hi, p_w[kk & 1]);
     if (more) softmax_pair<WIDE>(st, a2, lo, hi, p_w[(kk + 1) & 1], al_w);
   };
   using T = std::true_type;
@@ -939,7 +963,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
     zc[0] = __shfl(odd ? st.zl[1] : st.zl[0], lo);  // group lo & 1
     zc[1] = __shfl(odd ? st.zl[3] : st.zl[2], lo);  // group 2 + (lo & 1)
     wc[0] = st.wsum[0][0];
-    wc[1] = st.wsum[NT - 1][0];
+    wc[1] = st.wsum[NG == 1 ? 0 : NT - 1][0];
   } else {
     const int g = lo & 3;
     const float zown = g == 0 ? st.zl[0] : g == 1 ? st.zl[1] : g == 2 ? st.zl[2] : st.zl[3];
