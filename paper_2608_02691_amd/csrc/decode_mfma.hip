@@ -1,7 +1,7 @@
 // Matrix-core split-context scan of the INT2 decode attention (gfx950, v_mfma_f32_16x16x32_f16).
 //
 // What is computed is the same as the vector-ALU scan (eq:int2_attention in the rotated-query
-// form of the appendix): a_s = (q R_K) . (c_s * s + z) / sqrt(d) per group of 32 channels, an
+// form of the appendix): a_s = (q R_K) . (c_s * s + z) / sqrt(d) per group (32 or 128 channels), an
 // online softmax, and O' = sum_s p_s (c_s * s + z) in R_V coordinates. The affine metadata is
 // factored out of both contractions so the 2-bit codes enter the matrix cores unchanged:
 //
@@ -248,7 +248,9 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, bool wide, uint8_t* ld
 }
 
 // ---------------------------------------------------------------------------------------------
-// Row layouts. The matrix cores contract over 32 channels, one quant group, while a group's scale
+// Row layouts (groups of 32 channels; with one 128-channel group per token the four 32-channel
+// blocks read that group's scale and zero, and the zero term is z * sum_k q'_jk with no product).
+// The matrix cores contract over 32 channels, one quant group, while a group's scale
 // multiplies only that group's partial dot product, so a score row serves one group: it is
 // nonzero only in that group's k block.
 //  * narrow (up to 4 query heads per KV head): row (j, g) = 4 j + g; the four k blocks accumulate
@@ -291,8 +293,9 @@ __device__ __forceinline__ PageEnt load_ent(ent_ptr p, int i) {
 }
 
 // DMA of one page pair into the staging slot at lds_addr. (a_lo, a_hi), (b_lo, b_hi): records of KV
-// head 0 of the two pages; voff16 = 16 l + 1536 h selects head h for the codes; moff = (the record of
-// page 0 or, for lanes 32..63, page 1) + 1536 h + 1024 + 16 (l % 32) is the lane's metadata address.
+// head 0 of the two pages; voff16 = 16 l + R h (R the record size) selects head h for the codes;
+// moff = (the record of page 0 or, for lanes 32..63, page 1) + R h + 1024 + 16 (l % 32) is the
+// lane's metadata address.
 // With one group per token (NG = 1) a page has 128 B of metadata: one dword load, lanes 0..31 and
 // 32..63 reading 4 bytes of page 0 and page 1.
 template <int NG>
