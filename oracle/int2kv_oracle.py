@@ -299,3 +299,60 @@ def fold_wo(W_o_bits: np.ndarray, R_v: np.ndarray, num_q_heads: int) -> np.ndarr
         cols = slice(j * HEAD_DIM, (j + 1) * HEAD_DIM)
         out[:, cols] = W[:, cols] @ R_v[j // gq].astype(np.float64)
     return out
+
+
+# --------------------------------------------------------------------------- BF16 windows
+# Sec. 4.1 and the implementation details of Sec. 5 keep the sink tokens (the first 64) and the
+# recent tokens (the last 256) out of INT2: their keys keep the centering and are stored in BF16,
+# their values are stored unchanged. Decode attends to the union of those window tokens and the
+# INT2 tokens; the softmax runs over all of them (the order of tokens does not matter). Readings
+# used here and by the library: the window row of a key is bf16_rne(fp32(k - mu)) in the model's
+# basis (R_K is orthogonal, so scores in either basis agree), the value row is v's bf16 bits.
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """fp32 values to bf16 bit patterns, round to nearest even (NaN not expected)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return r.astype(np.uint16)
+
+
+def window_write(win_k: np.ndarray, win_v: np.ndarray, k_bits: np.ndarray, v_bits: np.ndarray,
+                 mu: np.ndarray, rows: np.ndarray) -> None:
+    """Store tokens into the BF16 window. win_k, win_v: uint16 [n_rows, H, 128]; k_bits, v_bits:
+    bf16 [n, H, 128]; mu: fp32 [H, 128] key mean (model basis); rows[i] < 0 skips token i."""
+    k32 = bf16_to_f64(k_bits).astype(np.float32) - np.asarray(mu, dtype=np.float32)[None]
+    kc = f32_to_bf16_bits(k32)
+    for i, r in enumerate(np.asarray(rows)):
+        if r < 0:
+            continue
+        win_k[r] = kc[i]
+        win_v[r] = v_bits[i]
+
+
+def decode_window(pool, q_bits, block_table, ctx_lens, R_k, R_v, win_k, win_v, win_lens,
+                  W_o_bits=None):
+    """Decode over the INT2 tokens of each sequence (as `decode`) together with its window tokens.
+
+    win_k, win_v: uint16 [B, H, cap, 128] (rows written by window_write); win_lens: [B] tokens in
+    each sequence's window. Returns fp64 o [B, H_q, 128], or y [B, d_model] with W_o_bits."""
+    q = bf16_to_f64(q_bits)
+    B, Hq, d = q.shape
+    H = R_k.shape[0]
+    gq = Hq // H
+    o = np.zeros((B, Hq, d), dtype=np.float64)
+    for b in range(B):
+        L, W = int(ctx_lens[b]), int(win_lens[b])
+        for h in range(H):
+            Ks = [bf16_to_f64(win_k[b, h, :W])]
+            Vs = [bf16_to_f64(win_v[b, h, :W])]
+            if L > 0:
+                Kt, Vt = effective_kv(pool, block_table[b], L, h, R_k, R_v)
+                Ks.append(Kt)
+                Vs.append(Vt)
+            K, V = np.concatenate(Ks), np.concatenate(Vs)
+            if K.shape[0] == 0:
+                continue
+            js = slice(h * gq, (h + 1) * gq)
+            o[b, js] = softmax_attention(q[b, js], K, V)
+    if W_o_bits is None:
+        return o
+    return o.reshape(B, Hq * d) @ bf16_to_f64(W_o_bits).T

@@ -400,3 +400,89 @@ def test_workload_recipe():
     assert w4.ctx_lens.min() >= 512 and w4.ctx_lens.max() <= 32768
     used = np.concatenate([w4.block_table[b, :(w4.ctx_lens[b] + 15) // 16] for b in range(64)])
     assert np.unique(used).size == used.size == w4.num_blocks
+
+
+# --------------------------------------------------------------------------- BF16 windows
+def test_window_write_hand_fixture():
+    """Window rows (Sec. 4.1: window keys keep the centering, values unchanged), worked by hand:
+    k = 1.0, mu = 0.25 gives 0.75 (0x3F40); mu = 2^-9 gives 1 - 2^-9, the midpoint of 0x3F7F and
+    0x3F80, which rounds to the even 0x3F80; mu = 3 * 2^-10 gives 1 - 3 * 2^-10, nearer 0x3F7F.
+    A negative row writes nothing; values are copied bit for bit."""
+    H = 1
+    k = np.full((3, H, 128), 0x3F80, np.uint16)
+    v = np.arange(3 * H * 128, dtype=np.uint16).reshape(3, H, 128)
+    win_k = np.zeros((4, H, 128), np.uint16)
+    win_v = np.zeros((4, H, 128), np.uint16)
+    for mu_val, want in ((0.25, 0x3F40), (2.0 ** -9, 0x3F80), (3 * 2.0 ** -10, 0x3F7F)):
+        win_k[:] = 0
+        O.window_write(win_k, win_v, k, v, np.full((H, 128), mu_val, np.float32), np.array([2, -1, 0]))
+        assert (win_k[2] == want).all() and (win_k[0] == want).all()
+        assert (win_k[1] == 0).all() and (win_k[3] == 0).all()
+        assert np.array_equal(win_v[2], v[0]) and np.array_equal(win_v[0], v[2])
+
+
+def test_window_decode_ignores_key_centering():
+    """Window tokens only (no INT2 token): subtracting the key mean leaves the softmax unchanged
+    (Sec. 4.1), so the output is attention over the raw keys and values (torch SDPA in fp64), up
+    to the bf16 rounding of k - mu."""
+    rng = np.random.default_rng(5)
+    B, Hq, H, cap = 2, 4, 2, 24
+    lens = np.array([24, 7], np.int32)
+    k = W.f32_to_bf16_bits(rng.standard_normal((B, cap, H, 128)).astype(np.float32))
+    v = W.f32_to_bf16_bits(rng.standard_normal((B, cap, H, 128)).astype(np.float32))
+    mu = (0.5 * rng.standard_normal((H, 128))).astype(np.float32)
+    win_k = np.zeros((B, H, cap, 128), np.uint16)
+    win_v = np.zeros_like(win_k)
+    for b in range(B):
+        wk = np.zeros((cap, H, 128), np.uint16)
+        wv = np.zeros_like(wk)
+        O.window_write(wk, wv, k[b], v[b], mu, np.arange(cap))
+        win_k[b], win_v[b] = wk.transpose(1, 0, 2), wv.transpose(1, 0, 2)
+    q = W.f32_to_bf16_bits(rng.standard_normal((B, Hq, 128)).astype(np.float32))
+    I = np.repeat(np.eye(128, dtype=np.float32)[None], H, axis=0)
+    pool = O.new_pool(1, H)
+    o = O.decode_window(pool, q, np.zeros((B, 1), np.int32), np.zeros(B, np.int32), I, I,
+                        win_k, win_v, lens)
+    qf = torch.from_numpy(O.bf16_to_f64(q))
+    for b in range(B):
+        n = int(lens[b])
+        K = torch.from_numpy(O.bf16_to_f64(k[b, :n])).permute(1, 0, 2).repeat_interleave(Hq // H, dim=0)
+        V = torch.from_numpy(O.bf16_to_f64(v[b, :n])).permute(1, 0, 2).repeat_interleave(Hq // H, dim=0)
+        ref = torch.nn.functional.scaled_dot_product_attention(qf[b][:, None, :], K, V)[:, 0].numpy()
+        # |k - mu| < 4: bf16 rounding moves each score by at most 128 * 4 * 2^-8 * |q| / sqrt(128)
+        assert np.abs(o[b] - ref).max() < 0.1
+        assert np.abs(o[b] - ref).max() > 0.0
+
+
+@pytest.mark.parametrize("G", [32, 128])
+def test_window_and_int2_tokens_share_one_softmax(G):
+    """Window tokens and INT2 tokens of a sequence form one attention (the softmax runs over both):
+    with grid-exact INT2 tokens, R = I, mu = 0 and bf16-exact window rows, the output equals
+    torch SDPA over the concatenated tokens; a window of one token with no INT2 token returns that
+    token's value exactly."""
+    B, Hq, H = 3, 6, 2
+    lens = [37, 0, 20]
+    wl = np.array([5, 9, 1], np.int32)
+    cap = 9
+    pool, table, ctx, I, q, Ks, Vs, Wo = _grid_workload(1, B, Hq, H, lens, d_model=64, G=G)
+    rng = np.random.default_rng(2)
+    wk = (rng.integers(-64, 64, size=(B, H, cap, 128)) / 16.0).astype(np.float32)
+    wv = (rng.integers(-64, 64, size=(B, H, cap, 128)) / 16.0).astype(np.float32)
+    win_k, win_v = W.f32_to_bf16_bits(wk), W.f32_to_bf16_bits(wv)
+    y = O.decode_window(pool, q, table, ctx, I, I, win_k, win_v, wl, Wo)
+    o = O.decode_window(pool, q, table, ctx, I, I, win_k, win_v, wl)
+    qf = torch.from_numpy(O.bf16_to_f64(q))
+    for b in range(B):
+        K = np.concatenate([wk[b, :, :wl[b]], Ks[b].transpose(1, 0, 2)], axis=1)
+        V = np.concatenate([wv[b, :, :wl[b]], Vs[b].transpose(1, 0, 2)], axis=1)
+        K = torch.from_numpy(K.astype(np.float64)).repeat_interleave(Hq // H, dim=0)
+        V = torch.from_numpy(V.astype(np.float64)).repeat_interleave(Hq // H, dim=0)
+        ref = torch.nn.functional.scaled_dot_product_attention(qf[b][:, None, :], K, V)[:, 0].numpy()
+        assert np.abs(o[b] - ref).max() < 1e-12
+    one = O.decode_window(O.new_pool(1, H, G), q, np.zeros((B, 1), np.int32), np.zeros(B, np.int32), I, I,
+                          win_k, win_v, np.array([1, 1, 1], np.int32))
+    for b in range(B):
+        for j in range(Hq):
+            assert np.array_equal(one[b, j], wv[b, j // (Hq // H), 0].astype(np.float64))
+    y_ref = o.reshape(B, -1) @ O.bf16_to_f64(Wo).T
+    assert np.abs(y - y_ref).max() < 1e-12
