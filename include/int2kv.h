@@ -200,6 +200,35 @@ int int2kv_append_decode(const int2kv_cache* cache, const uint16_t* k, const uin
                          int d_model, int wo_format, float* out, void* workspace,
                          size_t workspace_bytes, hipStream_t stream);
 
+/* BF16 sink and recent windows (Sec. 4.1; Sec. 5 implementation details: the paper keeps the
+ * first 64 and the last 256 tokens of a sequence out of INT2). Window tokens keep the key
+ * centering and are held in BF16; their values are held unchanged. The window store is a caller
+ * buffer of rows, each row one token for every KV head: win[(row * H_kv + h) * 128 + c], bf16,
+ * 16-byte aligned; row b * win_cap + t is token t of sequence b in int2kv_decode_window.
+ *
+ * int2kv_window_write stores num_tokens tokens: win_k[row] = bf16_rne(fp32(k - mu)) (the key
+ * mean mu in the model's basis, fp32 [H_kv, 128]), win_v[row] = v (bit copy).
+ *   k, v     : bf16 [num_tokens, H_kv, 128]
+ *   rows     : int32 [num_tokens]; a negative row, or one >= num_rows, skips the token; rows must
+ *              be distinct
+ * num_tokens = 0 launches nothing. Returns INT2KV_EINVAL on NULL or misaligned pointers. */
+int int2kv_window_write(const uint16_t* k, const uint16_t* v, const int32_t* rows, int num_tokens,
+                        int num_kv_heads, const float* mu, uint16_t* win_k, uint16_t* win_v,
+                        int num_rows, hipStream_t stream);
+
+/* int2kv_decode over the INT2 tokens (block_table, ctx_lens) together with each sequence's window
+ * tokens (win_lens[b], clamped to [0, win_cap], rows b * win_cap .. of win_k / win_v): one softmax
+ * over both sets (eq:int2_attention, with the window tokens' keys and values as stored). The order
+ * of tokens does not matter, so the window may be a ring. Other arguments, results, workspace and
+ * errors as int2kv_decode; in addition R_v is required (the window's output joins the INT2 part in
+ * the R_V basis), win_cap must be in [1, 512], and win_k, win_v must be 16-byte aligned. */
+int int2kv_decode_window(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
+                         const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens,
+                         int max_ctx, const float* R_k, const float* R_v, const uint16_t* W_o,
+                         int d_model, int wo_format, const uint16_t* win_k, const uint16_t* win_v,
+                         const int32_t* win_lens, int win_cap, float* out, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream);
+
 /* Measurement hook: when set (non-NULL), int2kv_decode attaches `before_scan` and `after_scan`
  * to the dispatch of the split-context scan kernel (hipExtLaunchKernel), so they mark that
  * kernel's own start and end and a caller can time it alone with hipEventElapsedTime, without

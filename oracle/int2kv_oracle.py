@@ -332,8 +332,8 @@ def decode_window(pool, q_bits, block_table, ctx_lens, R_k, R_v, win_k, win_v, w
                   W_o_bits=None):
     """Decode over the INT2 tokens of each sequence (as `decode`) together with its window tokens.
 
-    win_k, win_v: uint16 [B, H, cap, 128] (rows written by window_write); win_lens: [B] tokens in
-    each sequence's window. Returns fp64 o [B, H_q, 128], or y [B, d_model] with W_o_bits."""
+    win_k, win_v: uint16 [B, cap, H, 128] (window row b * cap + t holds token t of sequence b, as
+    written by window_write); win_lens: [B] tokens in each sequence's window. Returns fp64 o [B, H_q, 128], or y [B, d_model] with W_o_bits."""
     q = bf16_to_f64(q_bits)
     B, Hq, d = q.shape
     H = R_k.shape[0]
@@ -342,8 +342,8 @@ def decode_window(pool, q_bits, block_table, ctx_lens, R_k, R_v, win_k, win_v, w
     for b in range(B):
         L, W = int(ctx_lens[b]), int(win_lens[b])
         for h in range(H):
-            Ks = [bf16_to_f64(win_k[b, h, :W])]
-            Vs = [bf16_to_f64(win_v[b, h, :W])]
+            Ks = [bf16_to_f64(win_k[b, :W, h])]
+            Vs = [bf16_to_f64(win_v[b, :W, h])]
             if L > 0:
                 Kt, Vt = effective_kv(pool, block_table[b], L, h, R_k, R_v)
                 Ks.append(Kt)

@@ -116,6 +116,8 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model, int groups)
   p.off_part = off;
   const size_t part_rows = p.variant == 2 ? (size_t)(p.grid_g + B) : (size_t)B * p.n_chunks;
   off = up(off + part_rows * Hq * kPartStride * sizeof(float));
+  p.off_win = off;  // BF16-window partials, [B, Hq, kPartStride]
+  off = up(off + (size_t)B * Hq * kPartStride * sizeof(float));
   p.off_o = off;
   if (d_model > 0) off = up(off + (size_t)B * Hq * kHeadDim * sizeof(float));
   p.off_wo = off;
@@ -245,10 +247,17 @@ struct AppendStage {
   float clip_k = 1.0f, clip_v = 1.0f;
 };
 
+struct WindowStage {
+  const uint16_t *k = nullptr, *v = nullptr;
+  const int32_t* lens = nullptr;
+  int cap = 0;
+};
+
 int decode_impl(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
                 const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens, int max_ctx,
                 const float* R_k, const float* R_v, const uint16_t* W_o, int d_model, int wo_format, float* out,
-                void* workspace, size_t workspace_bytes, hipStream_t stream, const AppendStage* ap) {
+                void* workspace, size_t workspace_bytes, hipStream_t stream, const AppendStage* ap,
+                const WindowStage* win = nullptr) {
   if (int st = check_cache(cache)) return st;
   if (batch < 0) return fail(INT2KV_EINVAL, "batch must be >= 0");
   if (batch == 0) {
@@ -307,6 +316,7 @@ int decode_impl(const int2kv_cache* cache, const uint16_t* q, int batch, int num
   a.pages = reinterpret_cast<uint32_t*>(ws + plan.off_pages);
   a.grid_g = plan.grid_g;
   a.groups = kHeadDim / cache->group_size;
+  a.wpart = win ? reinterpret_cast<float*>(ws + plan.off_win) : nullptr;
 
   hipError_t e = hipSuccess;
   // the cache write (int2kv_append_decode): a few tokens per sequence run as extra blocks of the
@@ -333,6 +343,10 @@ int decode_impl(const int2kv_cache* cache, const uint16_t* q, int batch, int num
   e = plan.variant == 2 ? launch_decode_split_mfma(a, stream, g_ev_before, g_ev_after)
                         : launch_decode_split_valu(a, stream, g_ev_before, g_ev_after);
   if (e != hipSuccess) return hip_status(e, "decode/split");
+  if (win) {
+    e = launch_window_attn(a, WindowArgs{win->k, win->v, win->lens, win->cap}, stream);
+    if (e != hipSuccess) return hip_status(e, "decode/window");
+  }
   const bool unrotate = !folded;
   // with W_O the merge writes each head output as the projection's operand: two bf16 terms (hi, lo)
   // for row-major bf16 weights, one fp16 term for prepared weights
@@ -378,6 +392,32 @@ int int2kv_append_decode(const int2kv_cache* cache, const uint16_t* k, const uin
   }
   return decode_impl(cache, q, batch, num_q_heads, block_table, max_blocks_per_seq, ctx_lens, max_ctx, R_k, R_v, W_o,
                      d_model, wo_format, out, workspace, workspace_bytes, stream, &ap);
+}
+
+int int2kv_decode_window(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
+                         const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens, int max_ctx,
+                         const float* R_k, const float* R_v, const uint16_t* W_o, int d_model, int wo_format,
+                         const uint16_t* win_k, const uint16_t* win_v, const int32_t* win_lens, int win_cap,
+                         float* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (int st = check_cache(cache)) return st;
+  if (!win_k || !win_v || !win_lens || !R_v) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (win_cap <= 0 || win_cap > kWinMaxCap) return fail(INT2KV_EINVAL, "win_cap must be in [1, 512]");
+  if (!aligned(win_k, 16) || !aligned(win_v, 16)) return fail(INT2KV_EINVAL, "win_k and win_v must be 16-byte aligned");
+  const WindowStage ws{win_k, win_v, win_lens, win_cap};
+  return decode_impl(cache, q, batch, num_q_heads, block_table, max_blocks_per_seq, ctx_lens, max_ctx, R_k, R_v, W_o,
+                     d_model, wo_format, out, workspace, workspace_bytes, stream, nullptr, &ws);
+}
+
+int int2kv_window_write(const uint16_t* k, const uint16_t* v, const int32_t* rows, int num_tokens, int num_kv_heads,
+                        const float* mu, uint16_t* win_k, uint16_t* win_v, int num_rows, hipStream_t stream) {
+  if (num_tokens < 0 || num_kv_heads <= 0 || num_rows < 0)
+    return fail(INT2KV_EINVAL, "num_tokens, num_rows must be >= 0 and num_kv_heads > 0");
+  if (num_tokens == 0) return ok();
+  if (!k || !v || !rows || !mu || !win_k || !win_v) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(mu, 16) || !aligned(win_k, 16) || !aligned(win_v, 16))
+    return fail(INT2KV_EINVAL, "k, v, mu, win_k and win_v must be 16-byte aligned");
+  return hip_status(launch_window_write(k, v, rows, num_tokens, num_kv_heads, mu, win_k, win_v, num_rows, stream),
+                    "window_write");
 }
 
 }  // extern "C"

@@ -258,9 +258,22 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeArgs a, int unrotate, 
     const int j = h * a.gq + jj;
     const float* part = a.part + ((size_t)b * a.n_chunks * a.Hq + j) * kPartStride;
     const size_t stride = (size_t)a.Hq * kPartStride;
-    float M = -INFINITY;
+    // the BF16-window partial (when there is one) joins the chunk partials
+    float wm = -INFINITY, wl = 0.0f, wo = 0.0f;
+    if (a.wpart) {
+      const float* wp = a.wpart + ((size_t)b * a.Hq + j) * kPartStride;
+      wm = wp[0];
+      wl = wp[1];
+      wo = wp[4 + c];
+    }
+    float M = wm;
     for (int i = 0; i < nch; ++i) M = fmaxf(M, part[i * stride]);
     float lsum = 0.0f, osum = 0.0f;
+    if (wm != -INFINITY) {
+      const float f = exp2f(wm - M);
+      lsum = f * wl;
+      osum = f * wo;
+    }
     for (int i = 0; i < nch; ++i) {
       const float mi = part[i * stride];
       const float f = mi == -INFINITY ? 0.0f : exp2f(mi - M);

@@ -1040,7 +1040,7 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
 }
 
 // Merge the partials of each (sequence, query head) over the work-groups whose ranges met the
-// sequence, then undo the value rotation (o = o' R_V^T, unless W_O arrives pre-folded).
+// sequence (and the BF16-window partial, when there is one), then undo the value rotation (o = o' R_V^T, unless W_O arrives pre-folded).
 // Block (sequence, KV head) of kMergeSlots x 128 threads: slot s merges the work-groups ga + s,
 // ga + s + kMergeSlots, ... (one round of loads for up to kMergeSlots work-groups), thread c of a
 // slot owns channel c; the slots are then combined in a fixed order through LDS (deterministic),
@@ -1063,6 +1063,19 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
     M[jj] = -INFINITY;
     lsum[jj] = 0.0f;
     osum[jj] = 0.0f;
+  }
+  if (a.wpart && sl == 0) {
+    // the BF16-window partial starts slot 0 (merging it into the empty state is taking it)
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      const float* pp = a.wpart + ((size_t)b * a.Hq + h * gq + min(jj, gq - 1)) * kPartStride;
+      const float mv = pp[0], lv = pp[1], ov = pp[4 + c];
+      if (mv != -INFINITY) {
+        M[jj] = mv;
+        lsum[jj] = lv;
+        osum[jj] = ov;
+      }
+    }
   }
   for (int gg = ga + sl; gg <= gb; gg += kMergeSlots) {
     // the range bounds and the partial are loaded together (one round trip): slot gg + b exists for

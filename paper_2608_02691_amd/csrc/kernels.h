@@ -32,7 +32,7 @@ struct DecodePlan {
   int variant;        // 1 = vector ALU, 2 = matrix core
   int wo_ksplit;
   int grid_g;         // work-groups of the matrix-core scan
-  size_t off_qrot, off_qop, off_prefix, off_wginfo, off_seqwg, off_pages, off_part, off_o, off_wo, total;
+  size_t off_qrot, off_qop, off_prefix, off_wginfo, off_seqwg, off_pages, off_part, off_win, off_o, off_wo, total;
 };
 
 struct DecodeArgs {
@@ -56,9 +56,23 @@ struct DecodeArgs {
   uint32_t* pages;   // page list of the matrix-core scan: [total pages + padding][4]
   int grid_g;      // work-groups of the matrix-core scan
   int groups;      // groups per token of the cache (4 or 1)
+  float* wpart;    // BF16-window partials [B, Hq, kPartStride] folded in by the merge, or null
 };
 
 constexpr int kPartStride = 132;  // m, l, 2 pad, O[128]
+
+// BF16 sink/recent window of each sequence: rows b * cap + t, each [H, 128] bf16
+struct WindowArgs {
+  const uint16_t *k, *v;
+  const int32_t* lens;  // [B] tokens in each window (clamped to [0, cap])
+  int cap;
+};
+constexpr int kWinMaxGq = 16;
+constexpr int kWinMaxCap = 512;
+hipError_t launch_window_write(const uint16_t* k, const uint16_t* v, const int32_t* rows, int n, int H, const float* mu,
+                               uint16_t* win_k, uint16_t* win_v, int num_rows, hipStream_t s);
+// window partials into a.wpart (needs a.R_v)
+hipError_t launch_window_attn(const DecodeArgs& a, const WindowArgs& w, hipStream_t s);
 
 hipError_t launch_qrot(const DecodeArgs& a, hipStream_t s);
 // ev0 / ev1 (may be null): events that track the scan kernel's own start and end

@@ -38,7 +38,8 @@ EXPORTED = (
     "int2kv_fold_wo",
     "int2kv_prepared_wo_bytes", "int2kv_prepare_wo",
     "int2kv_quantize_pack_rotated", "int2kv_quantize_append", "int2kv_decode_workspace_bytes",
-    "int2kv_decode", "int2kv_append_decode", "int2kv_set_decode_tuning", "int2kv_set_decode_events",
+    "int2kv_decode", "int2kv_append_decode", "int2kv_window_write", "int2kv_decode_window",
+    "int2kv_set_decode_tuning", "int2kv_set_decode_events",
 )
 
 
@@ -75,6 +76,9 @@ def load_library(path: str = LIB_PATH):
         "int2kv_decode": ([ctypes.POINTER(_Cache), P, I, I, P, I, P, I, P, P, P, I, I, P, P, Z, S], I),
         "int2kv_append_decode": ([ctypes.POINTER(_Cache), P, P, P, I, P, F, F, P, I, I, P, I, P, I, P, P, P, I, I, P,
                                   P, Z, S], I),
+        "int2kv_window_write": ([P, P, P, I, I, P, P, P, I, S], I),
+        "int2kv_decode_window": ([ctypes.POINTER(_Cache), P, I, I, P, I, P, I, P, P, P, I, I, P, P, P, I, P, P, Z,
+                                  S], I),
         "int2kv_set_decode_tuning": ([I, I], I),
         "int2kv_set_decode_events": ([P, P], I),
     }
@@ -296,4 +300,52 @@ def int2kv_append_decode(cache: Int2KVCache, k: torch.Tensor, v: torch.Tensor, s
         wo_format, _ptr(out, _F32, "out"), _ptr(workspace, (torch.uint8,), "workspace"), workspace.numel(),
         _stream())
     _check(st, "int2kv_append_decode")
+    return out
+
+
+def int2kv_window_write(k: torch.Tensor, v: torch.Tensor, rows: torch.Tensor, mu: torch.Tensor,
+                        win_k: torch.Tensor, win_v: torch.Tensor) -> None:
+    """Store tokens into a BF16 window: win_k[rows] = bf16(k - mu), win_v[rows] = v.
+    k, v: bf16 [n, H, 128]; rows: int32 [n]; mu: fp32 [H, 128]; win_k, win_v: bf16 [num_rows, H, 128]."""
+    n, H = rows.shape[0], mu.shape[0]
+    if k.numel() != n * H * HEAD_DIM or v.numel() != k.numel():
+        raise ValueError("k / v must be [n, num_kv_heads, 128]")
+    if win_k.shape != win_v.shape or win_k.numel() % (H * HEAD_DIM):
+        raise ValueError("win_k / win_v must be [num_rows, num_kv_heads, 128]")
+    st = load_library().int2kv_window_write(
+        _ptr(k, _BF16, "k"), _ptr(v, _BF16, "v"), _ptr(rows, _I32, "rows"), n, H, _ptr(mu, _F32, "mu"),
+        _ptr(win_k, _BF16, "win_k"), _ptr(win_v, _BF16, "win_v"), win_k.numel() // (H * HEAD_DIM), _stream())
+    _check(st, "int2kv_window_write")
+
+
+def int2kv_decode_window(cache: Int2KVCache, q: torch.Tensor, block_table: torch.Tensor, ctx_lens: torch.Tensor,
+                         max_ctx: int, R_k: torch.Tensor, R_v: torch.Tensor, win_k: torch.Tensor,
+                         win_v: torch.Tensor, win_lens: torch.Tensor, win_cap: int,
+                         W_o: Optional[torch.Tensor] = None, wo_format: int = INT2KV_WO_PLAIN,
+                         d_model: Optional[int] = None, out: Optional[torch.Tensor] = None,
+                         workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """int2kv_decode over the INT2 tokens and each sequence's BF16 window tokens (rows
+    b * win_cap + t of win_k / win_v, win_lens[b] of them). Prepared W_o (flat) needs d_model."""
+    B, Hq = q.shape[0], q.shape[1]
+    if win_k.numel() < B * win_cap * cache.num_kv_heads * HEAD_DIM or win_v.shape != win_k.shape:
+        raise ValueError("win_k / win_v must hold batch * win_cap rows of [num_kv_heads, 128]")
+    if W_o is None:
+        d_model = 0
+    elif wo_format < INT2KV_WO_PREPARED:
+        d_model = W_o.shape[0]
+    elif d_model is None:
+        raise ValueError("d_model is required with prepared W_o")
+    if out is None:
+        shape = (B, d_model) if W_o is not None else (B, Hq, HEAD_DIM)
+        out = torch.empty(shape, dtype=torch.float32, device=q.device)
+    need = int2kv_decode_workspace_bytes(B, Hq, cache.num_kv_heads, max_ctx, d_model)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
+    st = load_library().int2kv_decode_window(
+        cache.desc, _ptr(q, _BF16, "q"), B, Hq, _ptr(block_table, _I32, "block_table"), block_table.shape[1],
+        _ptr(ctx_lens, _I32, "ctx_lens"), max_ctx, _ptr(R_k, _F32, "R_k"), _ptr(R_v, _F32, "R_v"),
+        _ptr(W_o, _BF16 + (torch.float16,), "W_o"), d_model, wo_format, _ptr(win_k, _BF16, "win_k"),
+        _ptr(win_v, _BF16, "win_v"), _ptr(win_lens, _I32, "win_lens"), win_cap, _ptr(out, _F32, "out"),
+        _ptr(workspace, (torch.uint8,), "workspace"), workspace.numel(), _stream())
+    _check(st, "int2kv_decode_window")
     return out

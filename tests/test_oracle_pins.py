@@ -431,13 +431,11 @@ def test_window_decode_ignores_key_centering():
     k = W.f32_to_bf16_bits(rng.standard_normal((B, cap, H, 128)).astype(np.float32))
     v = W.f32_to_bf16_bits(rng.standard_normal((B, cap, H, 128)).astype(np.float32))
     mu = (0.5 * rng.standard_normal((H, 128))).astype(np.float32)
-    win_k = np.zeros((B, H, cap, 128), np.uint16)
+    win_k = np.zeros((B * cap, H, 128), np.uint16)
     win_v = np.zeros_like(win_k)
-    for b in range(B):
-        wk = np.zeros((cap, H, 128), np.uint16)
-        wv = np.zeros_like(wk)
-        O.window_write(wk, wv, k[b], v[b], mu, np.arange(cap))
-        win_k[b], win_v[b] = wk.transpose(1, 0, 2), wv.transpose(1, 0, 2)
+    O.window_write(win_k, win_v, k.reshape(B * cap, H, 128), v.reshape(B * cap, H, 128), mu,
+                   np.arange(B * cap))
+    win_k, win_v = win_k.reshape(B, cap, H, 128), win_v.reshape(B, cap, H, 128)
     q = W.f32_to_bf16_bits(rng.standard_normal((B, Hq, 128)).astype(np.float32))
     I = np.repeat(np.eye(128, dtype=np.float32)[None], H, axis=0)
     pool = O.new_pool(1, H)
@@ -468,7 +466,8 @@ def test_window_and_int2_tokens_share_one_softmax(G):
     rng = np.random.default_rng(2)
     wk = (rng.integers(-64, 64, size=(B, H, cap, 128)) / 16.0).astype(np.float32)
     wv = (rng.integers(-64, 64, size=(B, H, cap, 128)) / 16.0).astype(np.float32)
-    win_k, win_v = W.f32_to_bf16_bits(wk), W.f32_to_bf16_bits(wv)
+    win_k = W.f32_to_bf16_bits(wk.transpose(0, 2, 1, 3).copy())
+    win_v = W.f32_to_bf16_bits(wv.transpose(0, 2, 1, 3).copy())
     y = O.decode_window(pool, q, table, ctx, I, I, win_k, win_v, wl, Wo)
     o = O.decode_window(pool, q, table, ctx, I, I, win_k, win_v, wl)
     qf = torch.from_numpy(O.bf16_to_f64(q))
