@@ -139,6 +139,10 @@ def main():
     ap.add_argument("--separate", action="store_true",
                     help="append and decode as two calls (default: int2kv_append_decode, the cache write beside "
                          "the query preparation)")
+    ap.add_argument("--window", type=str, default="",
+                    help="SINK,RECENT: keep the first SINK and last RECENT tokens of each sequence in the BF16 "
+                         "window (the paper's serving setting is 64,256 with --group 128); the step is then "
+                         "int2kv_window_write + int2kv_quantize_append + int2kv_decode_window")
     ap.add_argument("--event-every", type=int, default=10,
                     help="time the scan kernel with HIP events on every n-th timed step (events attached to a "
                          "dispatch add ~11 us of queue gaps to that step)")
@@ -196,26 +200,57 @@ def main():
         Wo, wo_format = K.int2kv_fold_wo(Wo, Rv, Hq), K.INT2KV_WO_FOLDED
     k_last = torch.empty((B, H, 128), dtype=torch.bfloat16, device="cuda")
     v_last = torch.empty_like(k_last)
-    last_slots = np.array([w.slot_mapping(b, int(lens[b]) - 1)[0] for b in range(B)], np.int32)
+    # BF16 window (--window): tokens [0, sink) and [L - recent, L) of each sequence live in the window
+    # store (rows b * cap + t), the rest in the INT2 cache at positions 0 .. L - sink - recent - 1
+    sink, recent = (int(x) for x in args.window.split(",")) if args.window else (0, 0)
+    cap = sink + recent
+    lens_int2 = np.maximum(lens - cap, 0) if cap else lens
+    win_lens = np.minimum(lens, cap).astype(np.int32)
+    if cap:
+        win_k = torch.zeros((B * cap, H, 128), dtype=torch.bfloat16, device="cuda")
+        win_v = torch.zeros_like(win_k)
+        mu_d = dev(w.mu)
+        k_cur = torch.empty_like(k_last)
+        v_cur = torch.empty_like(k_last)
+        cur_rows = dev(np.array([b * cap + int(win_lens[b]) - 1 for b in range(B)], np.int32))
+        win_lens_d = dev(win_lens)
+    # the step re-appends the last INT2 token of each sequence (none, slot -1, when all are in the window)
+    last_slots = np.array([w.slot_mapping(b, int(lens_int2[b]) - 1)[0] if lens_int2[b] > 0 else -1
+                           for b in range(B)], np.int32)
     t0 = time.time()
     for b in range(B):
         k, v = w.kv(b, as_torch=True)
         L = int(lens[b])
         kd, vd = k.cuda(), v.cuda()
+        if cap:
+            n2 = int(lens_int2[b])
+            wi = torch.cat([torch.arange(0, min(sink, L)), torch.arange(max(L - recent, min(sink, L)), L)])
+            K.int2kv_window_write(kd[wi], vd[wi], dev(np.arange(b * cap, b * cap + wi.numel(), dtype=np.int32)),
+                                  mu_d, win_k, win_v)
+            k_cur[b], v_cur[b] = kd[L - 1], vd[L - 1]
+            kd, vd, L = kd[sink:sink + n2], vd[sink:sink + n2], n2
         if L > 1:
             K.int2kv_quantize_append(cache, kd[:L - 1], vd[:L - 1], dev(w.slot_mapping(b, 0, L - 1)), Rk, Rv, mu_rk)
-        k_last[b] = kd[L - 1]
-        v_last[b] = vd[L - 1]
+        if L > 0:
+            k_last[b] = kd[L - 1]
+            v_last[b] = vd[L - 1]
         if b % 8 == 7:
             torch.cuda.synchronize()
             log(f"prefilled {b + 1}/{B} sequences ({time.time() - t0:.1f} s)")
     slots_d = dev(last_slots)
-    max_ctx = int(lens.max())
+    max_ctx = int(lens_int2.max())
+    ctx = dev(lens_int2.astype(np.int32))
     ws = torch.empty(K.int2kv_decode_workspace_bytes(B, Hq, H, max_ctx, d_model), dtype=torch.uint8, device="cuda")
     out = torch.empty((B, d_model) if d_model else (B, Hq, 128), dtype=torch.float32, device="cuda")
 
     def step():
-        if args.separate:
+        if cap:
+            # the current token enters the recent ring, the token leaving it goes to INT2
+            K.int2kv_window_write(k_cur, v_cur, cur_rows, mu_d, win_k, win_v)
+            K.int2kv_quantize_append(cache, k_last, v_last, slots_d, Rk, Rv, mu_rk)
+            K.int2kv_decode_window(cache, q, table, ctx, max_ctx, Rk, Rv, win_k, win_v, win_lens_d, cap, W_o=Wo,
+                                   wo_format=wo_format, d_model=d_model, out=out, workspace=ws)
+        elif args.separate:
             K.int2kv_quantize_append(cache, k_last, v_last, slots_d, Rk, Rv, mu_rk)
             K.int2kv_decode(cache, q, table, ctx, max_ctx, Rk, Rv, W_o=Wo, wo_format=wo_format, d_model=d_model,
                             out=out, workspace=ws)
@@ -285,16 +320,20 @@ def main():
     copy_gbps = 3 * 2 * (1 << 30) / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del cp_src, cp_dst
 
-    tokens = int(lens.sum())
-    pages = int(((lens + 15) // 16).sum())
+    tokens = int(lens.sum())  # tokens attended (INT2 and window)
+    pages = int(((lens_int2 + 15) // 16).sum())
     tok_bytes = 64 + 8 * (128 // args.group)  # K and V codes + one (s, z) fp16 pair per group each: 96 or 72
-    scan_bytes = tok_bytes * H * tokens + 4 * pages
+    scan_bytes = tok_bytes * H * int(lens_int2.sum()) + 4 * pages
     step_bytes = (scan_bytes + B * Hq * 256 + (B * d_model * 4 if d_model else B * Hq * 512)
                   + 2 * H * 128 * 128 * 4 + (2 * d_model * Hq * 128 if d_model else 0)
                   + B * H * (512 + tok_bytes))
     scan_gbps = scan_bytes / (scan_ms * 1e-3) / 1e9
     step_gbps = step_bytes / (ms_step * 1e-3) / 1e9
-    traffic = counter_traffic(f"decode_scan_cfg{args.config}", 1)
+    if cap:
+        step_bytes += int(win_lens.sum()) * H * 512  # bf16 window keys and values
+    # the committed counters cover the default scan only (group 32, no window, the configuration's contexts)
+    traffic = (counter_traffic(f"decode_scan_cfg{args.config}", 1)
+               if args.group == 32 and not cap and not args.ctx else None)
 
     result = {
         "metric": METRIC,
@@ -317,8 +356,10 @@ def main():
             "config_id": args.config, "batch": B, "num_q_heads": Hq, "num_kv_heads": H, "head_dim": 128, "block_size": 16,
             "group_size": args.group, "sum_ctx": tokens, "max_ctx": max_ctx, "d_model": d_model,
             "chunk_tokens": args.chunk or "auto", "variant": args.variant or "auto",
-            "step_calls": ("int2kv_quantize_append + int2kv_decode" if args.separate else
+            "step_calls": ("int2kv_window_write + int2kv_quantize_append + int2kv_decode_window" if cap else
+                           "int2kv_quantize_append + int2kv_decode" if args.separate else
                            "int2kv_append_decode (cache write inside the preparation launch)"),
+            "bf16_window": f"{sink} sink + {recent} recent tokens" if cap else None,
             "w_o": {"prepared": "W_O R_V folded, fp16 tiles (prepared once)",
                     "folded": "W_O R_V folded, bf16 row-major (prepared once)",
                     "plain": "W_O bf16 row-major after R_V^T"}[args.wo] if Wo is not None else None,
@@ -338,7 +379,7 @@ def main():
         },
         "context": {"hbm_copy_gbps": copy_gbps, "copy": "1 GiB device-to-device copy, read + write bytes"},
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not cap:  # the oracle timing covers the INT2-only step
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.group)
     print(json.dumps(result), flush=True)
 

@@ -78,15 +78,24 @@ __global__ __launch_bounds__(256) void window_attn_kernel(DecodeArgs a, WindowAr
     float acc[kWinMaxGq];
 #pragma unroll
     for (int j = 0; j < kWinMaxGq; ++j) acc[j] = 0.0f;
-    for (int c8 = 0; c8 < kHeadDim / 8; ++c8) {
-      const uint4 u = kr[c8];
-      const float kf[8] = {bf_lo(u.x), bf_hi(u.x), bf_lo(u.y), bf_hi(u.y),
-                           bf_lo(u.z), bf_hi(u.z), bf_lo(u.w), bf_hi(u.w)};
+    // the key row in four quarters: the four 16-byte loads of a quarter are issued before its
+    // arithmetic (register arrays with static indices only, so nothing goes to scratch)
+    for (int c32 = 0; c32 < kHeadDim / 32; ++c32) {
+      uint4 row[4];
 #pragma unroll
-      for (int j = 0; j < kWinMaxGq; ++j) {
-        if (j < gq) {
+      for (int u4 = 0; u4 < 4; ++u4) row[u4] = kr[4 * c32 + u4];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc[j] = fmaf(qs[j][8 * c8 + e], kf[e], acc[j]);
+      for (int u4 = 0; u4 < 4; ++u4) {
+        const uint4 u = row[u4];
+        const float kf[8] = {bf_lo(u.x), bf_hi(u.x), bf_lo(u.y), bf_hi(u.y),
+                             bf_lo(u.z), bf_hi(u.z), bf_lo(u.w), bf_hi(u.w)};
+        const int c0 = 32 * c32 + 8 * u4;
+#pragma unroll
+        for (int j = 0; j < kWinMaxGq; ++j) {
+          if (j < gq) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[j] = fmaf(qs[j][c0 + e], kf[e], acc[j]);
+          }
         }
       }
     }
@@ -114,6 +123,8 @@ __global__ __launch_bounds__(256) void window_attn_kernel(DecodeArgs a, WindowAr
   float o[kWinMaxGq];
 #pragma unroll
   for (int j = 0; j < kWinMaxGq; ++j) o[j] = 0.0f;
+  // unrolled so that several value loads are in flight per thread
+#pragma unroll 8
   for (int t = par; t < W; t += 2) {
     const float vv = __uint_as_float((uint32_t)w.v[(((size_t)b * w.cap + t) * a.H + h) * kHeadDim + c] << 16);
 #pragma unroll
@@ -131,6 +142,7 @@ __global__ __launch_bounds__(256) void window_attn_kernel(DecodeArgs a, WindowAr
 #pragma unroll
   for (int r = 0; r < kWinMaxGq / 2; ++r) acc[r] = 0.0f;
   const float* Rv = a.R_v + (size_t)h * kHeadDim * kHeadDim;
+#pragma unroll 16
   for (int i = 0; i < kHeadDim; ++i) {
     const float rv = Rv[(size_t)i * kHeadDim + c];
 #pragma unroll
