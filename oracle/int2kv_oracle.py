@@ -333,14 +333,16 @@ def decode_window(pool, q_bits, block_table, ctx_lens, R_k, R_v, win_k, win_v, w
     """Decode over the INT2 tokens of each sequence (as `decode`) together with its window tokens.
 
     win_k, win_v: uint16 [B, cap, H, 128] (window row b * cap + t holds token t of sequence b, as
-    written by window_write); win_lens: [B] tokens in each sequence's window. Returns fp64 o [B, H_q, 128], or y [B, d_model] with W_o_bits."""
+    written by window_write); win_lens: [B] tokens in each sequence's window, clamped to [0, cap] (a
+    count outside that range means an empty or a full window). Returns fp64 o [B, H_q, 128], or
+    y [B, d_model] with W_o_bits."""
     q = bf16_to_f64(q_bits)
     B, Hq, d = q.shape
     H = R_k.shape[0]
     gq = Hq // H
     o = np.zeros((B, Hq, d), dtype=np.float64)
     for b in range(B):
-        L, W = int(ctx_lens[b]), int(win_lens[b])
+        L, W = int(ctx_lens[b]), min(max(int(win_lens[b]), 0), win_k.shape[1])
         for h in range(H):
             Ks = [bf16_to_f64(win_k[b, :W, h])]
             Vs = [bf16_to_f64(win_v[b, :W, h])]

@@ -62,10 +62,11 @@ def test_window_write_bit_exact():
 
 
 CASES = [
-    # (Hq, H, ctx lens, window lens, cap, d_model)
-    (8, 2, [300, 0, 17, 1, 129], [64, 5, 0, 320, 1], 320, 0),
-    (10, 2, [700, 0, 33], [100, 7, 0], 128, 96),
-    (24, 2, [250, 64], [30, 64], 64, 0),
+    # (Hq, H, ctx lens, window lens, cap, d_model); a sequence with neither window nor INT2 tokens,
+    # and window counts below 0 and above cap (clamped to an empty and a full window)
+    (8, 2, [300, 0, 17, 1, 129, 0], [64, 5, 0, 320, 1, 0], 320, 0),
+    (10, 2, [700, 0, 33, 40], [100, 7, 0, -3], 128, 96),
+    (24, 2, [250, 64, 10], [30, 64, 1000], 64, 0),
 ]
 
 
@@ -77,9 +78,10 @@ def test_decode_window_matches_oracle(case, variant, G):
     print(f"\n[decode window] case={case} variant={variant} G={G}", flush=True)
     K.int2kv_set_decode_tuning(0, variant)
     lens, wl = np.array(lens), np.array(wls, np.int32)
-    w = W.make_workload(1, batch=lens.size, ctx_lens=np.maximum(lens, wl), num_q_heads=Hq, num_kv_heads=H,
+    wl_rows = np.clip(wl, 0, cap)  # tokens actually stored in each window
+    w = W.make_workload(1, batch=lens.size, ctx_lens=np.maximum(lens, wl_rows), num_q_heads=Hq, num_kv_heads=H,
                         d_model=dm or None)
-    k, v, rows, wk_ref, wv_ref = _window(w, cap, wl)
+    k, v, rows, wk_ref, wv_ref = _window(w, cap, wl_rows)
     w.ctx_lens = lens.astype(np.int32)  # the INT2 part: the first lens[b] tokens
     pool = oracle_pool(w, group=G)
     win_k = wk_ref.reshape(w.batch, cap, H, 128)
