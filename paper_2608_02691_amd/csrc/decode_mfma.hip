@@ -545,12 +545,33 @@ __device__ __forceinline__ void softmax_pair(ScanState<WIDE>& st, const float (&
 
 // Value accumulation of one pair: K = the pair's 32 tokens, N = the 16 columns, M = 8 tiles of 16
 // channels; p comes back from LDS in the layout of the B operand.
+//
+// The weights w = p s enter the matrix cores as fp16. Lazy rescaling keeps p <= 2^tau = 256, so
+// w is finite for every scale s < 256. A pair holding a larger V scale (a rotated value range
+// above 768; detected by a wave vote) takes the scaled form: the codes land on the fp16 pattern
+// of 256 instead of 1.0 (A' = 256 (1 + c 2^-e), exact), the weights are w' = fp16(p s / 256)
+// formed in fp32 and the weight sums add 256 w'. The products A' w' are those of the plain form,
+// so both forms add into the same accumulators and the final correction
+// (O = 2^e (D - sum w) + Z) is unchanged. Only the weights and the landing base differ, so the
+// matrix-core chain is shared.
 template <bool WIDE, int NG>
 __device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WIDE>& cur, int lo, int hi,
                                         const _Float16 (*p_w)[8][kBlock]) {
   // with one group per token every group column has the same weights: one weight operand (and one
   // weight sum) serves all tiles
   constexpr int NT = NG == 1 ? 1 : ScanState<WIDE>::NT;
+  // largest V scale of the pair held by this lane (scales are never negative or NaN)
+  half2_t smax = __builtin_elementwise_max(as_h2(cur.vs[0][0].x), as_h2(cur.vs[0][0].y));
+#pragma unroll
+  for (int P = 0; P < 2; ++P)
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      if (P + t > 0)
+        smax = __builtin_elementwise_max(smax,
+                                         __builtin_elementwise_max(as_h2(cur.vs[P][t].x), as_h2(cur.vs[P][t].y)));
+  const bool big = __any((float)smax.x >= 256.0f || (float)smax.y >= 256.0f) != 0;
+  LandK lk = st.lk;
+  if (big) lk.one = 0x5C005C00u;  // fp16 256.0, twice
   // A operand of the (Z, l) contraction: rows 0..3 hold z of group `row` (the V zeros this lane
   // already has, group lo & 3 = row), rows 4..7 hold 1.0, rows 8..15 zero
   const half2_t zmul = lo < 4 ? half2_t{(_Float16)1.0f, (_Float16)1.0f} : half2_t{(_Float16)0.0f, (_Float16)0.0f};
@@ -559,20 +580,37 @@ __device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WID
   const half8_t Azl = __builtin_bit_cast(
       half8_t, u32x4_t{as_u(as_h2(cur.vz[0].x) * zmul + zadd), as_u(as_h2(cur.vz[0].y) * zmul + zadd),
                        as_u(as_h2(cur.vz[1].x) * zmul + zadd), as_u(as_h2(cur.vz[1].y) * zmul + zadd)});
-  const half8_t Aones = __builtin_bit_cast(half8_t, u32x4_t{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u});
+  const half8_t Aones = __builtin_bit_cast(half8_t, u32x4_t{lk.one, lk.one, lk.one, lk.one});
   // column lo: query head jc, probabilities of tokens 4hi..4hi+3 of both pages
   const int jc = WIDE ? lo >> 1 : lo >> 2;
   const uint2 pp0 = *reinterpret_cast<const uint2*>(&p_w[0][jc][4 * hi]);
   const uint2 pp1 = *reinterpret_cast<const uint2*>(&p_w[1][jc][4 * hi]);
   const half8_t Bp = __builtin_bit_cast(half8_t, u32x4_t{pp0.x, pp0.y, pp1.x, pp1.y});
+  uint32_t wv[NT][4];
+  const uint32_t pw[4] = {pp0.x, pp0.y, pp1.x, pp1.y};
+  if (__builtin_expect(big, 0)) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint2 sv = cur.vs[i >> 1][t];
+        const half2_t p = as_h2(pw[i]), s = as_h2(i & 1 ? sv.y : sv.x);
+        wv[t][i] = as_u(half2_t{(_Float16)((float)p.x * (float)s.x * 0x1p-8f),
+                                (_Float16)((float)p.y * (float)s.y * 0x1p-8f)});
+      }
+  } else {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint2 sv = cur.vs[i >> 1][t];
+        wv[t][i] = as_u(as_h2(pw[i]) * as_h2(i & 1 ? sv.y : sv.x));
+      }
+  }
   half8_t Bw[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    const half2_t w00 = as_h2(pp0.x) * as_h2(cur.vs[0][t].x);
-    const half2_t w01 = as_h2(pp0.y) * as_h2(cur.vs[0][t].y);
-    const half2_t w10 = as_h2(pp1.x) * as_h2(cur.vs[1][t].x);
-    const half2_t w11 = as_h2(pp1.y) * as_h2(cur.vs[1][t].y);
-    Bw[t] = __builtin_bit_cast(half8_t, u32x4_t{as_u(w00), as_u(w01), as_u(w10), as_u(w11)});
+    Bw[t] = __builtin_bit_cast(half8_t, u32x4_t{wv[t][0], wv[t][1], wv[t][2], wv[t][3]});
     st.wsum[t] = mfma16(Aones, Bw[t], st.wsum[t]);
   }
   st.zl = mfma16(Azl, Bp, st.zl);
@@ -580,7 +618,7 @@ __device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WID
   // ALU beside them (measured: -2 % scan time at 5 query heads per KV head)
   __builtin_amdgcn_s_setprio(1);
 #define INT2KV_PV_TILE(MT)                                                                        \
-  st.acc[MT] = mfma16(v_operand<MT>(cur.vc[0], cur.vc[1], st.lk), Bw[WIDE && NT == 2 ? (MT) >> 2 : 0], st.acc[MT]);
+  st.acc[MT] = mfma16(v_operand<MT>(cur.vc[0], cur.vc[1], lk), Bw[WIDE && NT == 2 ? (MT) >> 2 : 0], st.acc[MT]);
   INT2KV_PV_TILE(0)
   INT2KV_PV_TILE(1)
   INT2KV_PV_TILE(2)

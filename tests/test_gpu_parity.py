@@ -320,3 +320,34 @@ def test_append_decode_group128(variant):
     assert torch.equal(caches[0].pool, caches[1].pool) and torch.equal(y0, y1)
     ref = O.decode(caches[1].pool.cpu().numpy(), w.q, w.block_table, w.ctx_lens, w.R_k, w.R_v)
     assert_rows_close(y1.cpu().numpy(), ref, what="append_decode G=128")
+
+
+@pytest.mark.parametrize("G", [32, 128])
+@pytest.mark.parametrize("variant", [1, 2])
+def test_decode_large_value_and_key_ranges(G, variant):
+    """Value groups whose fp16 scale is far above 256 (rotated value ranges up to ~1e5) beside
+    ordinary tokens of the same pages, and key groups with wider ranges: the matrix-core scan's fp16
+    value weights p * s must not overflow (its scaled form takes such pairs). The keys of one token
+    in ten are scaled by 4 (logits of a few units: the matrix-core scan holds q' as an fp16 operand,
+    so its score error grows with the logit magnitude, about 2^-12 of it)."""
+    print(f"\n[decode large ranges] G={G} variant={variant}", flush=True)
+    K.int2kv_set_decode_tuning(0, variant)
+    w = W.make_workload(4, batch=3, ctx_lens=np.array([300, 47, 129]), num_q_heads=10, num_kv_heads=2)
+    pool = O.new_pool(w.num_blocks, w.num_kv_heads, G)
+    rng = np.random.default_rng(17)
+    big_scales = []
+    for b in range(w.batch):
+        k, v = w.kv(b)
+        k_rot = O.center_rotate(k, w.mu, w.R_k).astype(np.float32)
+        v_rot = O.rotate(v, w.R_v).astype(np.float32)
+        L = k.shape[0]
+        v_rot *= np.where(rng.random(L) < 0.3, 10.0 ** rng.uniform(2.0, 4.0, L), 1.0)[:, None, None].astype(np.float32)
+        k_rot *= np.where(rng.random(L) < 0.1, 4.0, 1.0)[:, None, None].astype(np.float32)
+        _, _, _, _, vs, _ = O.quantize_pack_rotated(pool, k_rot, v_rot, w.slot_mapping(b))
+        big_scales.append(vs.astype(np.float64).max())
+    assert max(big_scales) > 1000.0  # the case exercises the large-scale pairs
+    ref = O.decode(pool, w.q, w.block_table, w.ctx_lens, w.R_k, w.R_v)
+    out = K.int2kv_decode(gpu_cache(pool), dev(w.q), dev(w.block_table), dev(w.ctx_lens), int(w.ctx_lens.max()),
+                          dev(w.R_k), dev(w.R_v))
+    worst = assert_rows_close(out.cpu().numpy(), ref, what="decode, large ranges")
+    print(f"largest V scale {max(big_scales):.0f}; worst row error {worst:.2e}", flush=True)
