@@ -83,8 +83,9 @@ const char* int2kv_last_error(void);
 /* Library version string. */
 const char* int2kv_version(void);
 
-/* Bytes of the pool for the given shape at group size 32 (num_blocks * num_kv_heads * 1536). */
-size_t int2kv_pool_bytes(int num_blocks, int num_kv_heads);
+/* Bytes of the pool for the given shape: num_blocks * num_kv_heads * int2kv_record_bytes(group_size)
+ * (0 for a group size other than 32 or 128, or a non-positive count). */
+size_t int2kv_pool_bytes(int num_blocks, int num_kv_heads, int group_size);
 
 /* Bytes of one (block, KV head) record: 1536 at group size 32, 1152 at 128, 0 otherwise. */
 size_t int2kv_record_bytes(int group_size);
@@ -229,17 +230,21 @@ int int2kv_decode_window(const int2kv_cache* cache, const uint16_t* q, int batch
                          const int32_t* win_lens, int win_cap, float* out, void* workspace,
                          size_t workspace_bytes, hipStream_t stream);
 
-/* Measurement hook: when set (non-NULL), int2kv_decode attaches `before_scan` and `after_scan`
- * to the dispatch of the split-context scan kernel (hipExtLaunchKernel), so they mark that
- * kernel's own start and end and a caller can time it alone with hipEventElapsedTime, without
- * extra packets between the kernels. Pass NULLs to disable. The events are owned by the caller
- * and must outlive the calls that record them. */
+/* Measurement hook: when set (non-NULL), the calls this thread issues attach `before_scan` and
+ * `after_scan` to the dispatch of their dominant kernel (hipExtLaunchKernel): the split-context scan
+ * of int2kv_decode, int2kv_append_decode and int2kv_decode_window, the cache-write kernel of
+ * int2kv_quantize_append. They then mark that kernel's own start and end, and a caller can time it
+ * alone with hipEventElapsedTime, without extra packets between the kernels. Pass NULLs to disable.
+ * The setting is per calling thread. The events are owned by the caller and must outlive the calls
+ * that record them. */
 int int2kv_set_decode_events(hipEvent_t before_scan, hipEvent_t after_scan);
 
 /* Tuning knobs for measurement sweeps: context chunk in tokens (multiple of 64, 0 = automatic)
  * and decode kernel variant (0 = automatic, 1 = vector ALU, 2 = matrix core; the matrix-core scan
- * serves at most 8 query heads per KV head, wider groups always use the vector-ALU scan). Returns
- * INT2KV_EINVAL for out-of-range values. Workspace sizes depend on both. */
+ * serves at most 8 query heads per KV head, wider groups always use the vector-ALU scan). The
+ * setting applies to the calls of the calling thread only (thread-local), including
+ * int2kv_decode_workspace_bytes: size a workspace on the thread that decodes with it. Returns
+ * INT2KV_EINVAL for out-of-range values. */
 int int2kv_set_decode_tuning(int chunk_tokens, int variant);
 
 #ifdef __cplusplus

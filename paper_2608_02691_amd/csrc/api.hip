@@ -15,11 +15,13 @@ using namespace int2kv;
 
 namespace {
 
+// Per-thread state: the last error message, the measurement knobs (int2kv_set_decode_tuning,
+// int2kv_set_decode_events) of the calls this thread makes
 thread_local std::string g_last_error;
-int g_chunk_override = 0;
-int g_variant_override = 0;
-hipEvent_t g_ev_before = nullptr;
-hipEvent_t g_ev_after = nullptr;
+thread_local int g_chunk_override = 0;
+thread_local int g_variant_override = 0;
+thread_local hipEvent_t g_ev_before = nullptr;
+thread_local hipEvent_t g_ev_after = nullptr;
 
 int fail(int status, const std::string& msg) {
   g_last_error = msg;
@@ -134,9 +136,9 @@ const char* int2kv_last_error(void) { return g_last_error.c_str(); }
 
 const char* int2kv_version(void) { return "int2kv 0.1 gfx950"; }
 
-size_t int2kv_pool_bytes(int num_blocks, int num_kv_heads) {
+size_t int2kv_pool_bytes(int num_blocks, int num_kv_heads, int group_size) {
   if (num_blocks <= 0 || num_kv_heads <= 0) return 0;
-  return (size_t)num_blocks * num_kv_heads * kRecord;
+  return (size_t)num_blocks * num_kv_heads * int2kv_record_bytes(group_size);
 }
 
 size_t int2kv_record_bytes(int group_size) {
@@ -217,7 +219,7 @@ int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const u
   if (!aligned(k, 16) || !aligned(v, 16) || !aligned(R_k, 16) || !aligned(R_v, 16) || !aligned(mu_rk, 16))
     return fail(INT2KV_EINVAL, "k, v, R_k, R_v and mu_rk must be 16-byte aligned");
   hipError_t e = launch_append_mfma(view(cache), k, v, slot_mapping, num_tokens, R_k, R_v, mu_rk, clip_k, clip_v,
-                                    stream);
+                                    stream, g_ev_before, g_ev_after);
   return hip_status(e, "quantize_append");
 }
 

@@ -170,29 +170,30 @@ __global__ __launch_bounds__(512) void append_mfma_kernel(CacheView cv, const ui
 
 hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots, int n,
                               const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
-                              float clip_v, hipStream_t s) {
+                              float clip_v, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   if (n <= 0) return hipSuccess;
   // one work-group per CU (its R^T terms fill most of the LDS), each converting R once for many
   // steps; short appends take one tile per wave step
   const int per_head = max(1, 256 / (2 * c.num_kv_heads));
   const int tiles = (n + 15) / 16;
+  const dim3 block(64 * kApWaves);
   if (tiles <= kApWaves * per_head) {
-    const int nx = (tiles + kApWaves - 1) / kApWaves;
+    const dim3 grid((tiles + kApWaves - 1) / kApWaves, c.num_kv_heads, 2);
     if (c.groups == 1)
-      hipLaunchKernelGGL((append_mfma_kernel<1, 1>), dim3(nx, c.num_kv_heads, 2), dim3(64 * kApWaves), 0, s, c, k, v,
-                         slots, n, R_k, R_v, mu_rk, clip_k, clip_v);
+      hipExtLaunchKernelGGL((append_mfma_kernel<1, 1>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n, R_k, R_v,
+                            mu_rk, clip_k, clip_v);
     else
-      hipLaunchKernelGGL((append_mfma_kernel<1, 4>), dim3(nx, c.num_kv_heads, 2), dim3(64 * kApWaves), 0, s, c, k, v,
-                         slots, n, R_k, R_v, mu_rk, clip_k, clip_v);
+      hipExtLaunchKernelGGL((append_mfma_kernel<1, 4>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n, R_k, R_v,
+                            mu_rk, clip_k, clip_v);
   } else {
     const int steps = (tiles + 1) / 2;
-    const int nx = min((steps + kApWaves - 1) / kApWaves, per_head);
+    const dim3 grid(min((steps + kApWaves - 1) / kApWaves, per_head), c.num_kv_heads, 2);
     if (c.groups == 1)
-      hipLaunchKernelGGL((append_mfma_kernel<2, 1>), dim3(nx, c.num_kv_heads, 2), dim3(64 * kApWaves), 0, s, c, k, v,
-                         slots, n, R_k, R_v, mu_rk, clip_k, clip_v);
+      hipExtLaunchKernelGGL((append_mfma_kernel<2, 1>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n, R_k, R_v,
+                            mu_rk, clip_k, clip_v);
     else
-      hipLaunchKernelGGL((append_mfma_kernel<2, 4>), dim3(nx, c.num_kv_heads, 2), dim3(64 * kApWaves), 0, s, c, k, v,
-                         slots, n, R_k, R_v, mu_rk, clip_k, clip_v);
+      hipExtLaunchKernelGGL((append_mfma_kernel<2, 4>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n, R_k, R_v,
+                            mu_rk, clip_k, clip_v);
   }
   return hipGetLastError();
 }

@@ -21,9 +21,10 @@ hipError_t launch_fold_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_f, 
                           int H, hipStream_t s);
 hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_rot, const int32_t* slots,
                                int n, float clip_k, float clip_v, hipStream_t s);
+// ev0 / ev1 (may be null): events that track the append kernel's own start and end
 hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots,
                               int n, const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
-                              float clip_v, hipStream_t s);
+                              float clip_v, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 // ---- decode (decode.hip, decode_mfma.hip, wo_gemm.hip)
 struct DecodePlan {

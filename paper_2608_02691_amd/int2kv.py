@@ -64,7 +64,7 @@ def load_library(path: str = LIB_PATH):
     sig = {
         "int2kv_last_error": ([], ctypes.c_char_p),
         "int2kv_version": ([], ctypes.c_char_p),
-        "int2kv_pool_bytes": ([I, I], Z),
+        "int2kv_pool_bytes": ([I, I, I], Z),
         "int2kv_record_bytes": ([I], Z),
         "int2kv_prepare_mu_rot": ([P, P, P, I, S], I),
         "int2kv_fold_wo": ([P, P, P, I, I, I, S], I),
@@ -149,8 +149,8 @@ def int2kv_version() -> str:
     return load_library().int2kv_version().decode()
 
 
-def int2kv_pool_bytes(num_blocks: int, num_kv_heads: int) -> int:
-    return load_library().int2kv_pool_bytes(num_blocks, num_kv_heads)
+def int2kv_pool_bytes(num_blocks: int, num_kv_heads: int, group_size: int = GROUP_SIZE) -> int:
+    return load_library().int2kv_pool_bytes(num_blocks, num_kv_heads, group_size)
 
 
 def int2kv_prepare_mu_rot(R_k: torch.Tensor, mu: torch.Tensor, mu_rk: Optional[torch.Tensor] = None) -> torch.Tensor:

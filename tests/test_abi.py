@@ -30,6 +30,9 @@ def test_library_exports_every_declared_symbol():
 def test_version_and_sizes():
     assert "gfx950" in K.int2kv_version()
     assert K.int2kv_pool_bytes(10, 8) == 10 * 8 * 1536
+    assert K.int2kv_pool_bytes(10, 8, 32) == 10 * 8 * 1536
+    assert K.int2kv_pool_bytes(10, 8, 128) == 10 * 8 * 1152
+    assert K.int2kv_pool_bytes(10, 8, 64) == 0
     assert K.int2kv_pool_bytes(0, 8) == 0
     assert K.int2kv_decode_workspace_bytes(64, 40, 8, 32768, 5120) > 0
     assert K.int2kv_decode_workspace_bytes(2, 5, 2, 100, 0) == 0  # 5 % 2 != 0
@@ -109,3 +112,22 @@ def test_append_decode_rejects_bad_arguments_without_launch():
     st = lib.int2kv_append_decode(ctypes.byref(good), 16, 16, 16, 4, 16, 1.0, 1.0, 16, 1, 4, 16, 1, 16, 16,
                                   16, 16, None, 0, 0, 16, 256, 16, None)
     assert st == K.INT2KV_EWORKSPACE
+
+
+def test_tuning_knobs_are_per_thread():
+    """int2kv_set_decode_tuning on one thread does not change another thread's workspace plan."""
+    import threading
+    lib = K.load_library()
+    assert lib.int2kv_set_decode_tuning(0, 0) == K.INT2KV_OK
+    base = lib.int2kv_decode_workspace_bytes(4, 8, 2, 4096, 0)
+    seen = {}
+
+    def other():
+        assert lib.int2kv_set_decode_tuning(64, 1) == K.INT2KV_OK  # vector-ALU scan, 64-token chunks
+        seen["other"] = lib.int2kv_decode_workspace_bytes(4, 8, 2, 4096, 0)
+
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    assert seen["other"] != base
+    assert lib.int2kv_decode_workspace_bytes(4, 8, 2, 4096, 0) == base
