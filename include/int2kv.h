@@ -201,6 +201,27 @@ int int2kv_append_decode(const int2kv_cache* cache, const uint16_t* k, const uin
                          int d_model, int wo_format, float* out, void* workspace,
                          size_t workspace_bytes, hipStream_t stream);
 
+/* Bytes of the static scratch behind int2kv_append_decode_noalloc (64 MiB per GPU). */
+#define INT2KV_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* int2kv_append_decode without a workspace argument, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).
+ * The decode's workspace is a static device array of INT2KV_NOALLOC_SCRATCH_BYTES inside the
+ * library, one copy per GPU, held until the process ends; its device address is looked up once per
+ * device on the first call made there (hipGetSymbolAddress with that device current). The call
+ * allocates nothing and calls no allocating routine. Results, arguments and errors as
+ * int2kv_append_decode; in addition a call whose workspace (int2kv_decode_workspace_bytes of its
+ * sizes) exceeds the scratch returns INT2KV_EWORKSPACE without launching. Every call on a GPU shares
+ * that GPU's scratch and leaves its contents behind (nothing in it needs to start at zero): calls
+ * that overlap on one GPU (concurrent streams, or threads) race and must be serialized by the
+ * caller. */
+int int2kv_append_decode_noalloc(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
+                                 const int32_t* slot_mapping, int num_tokens, const float* mu_rk, float clip_k,
+                                 float clip_v, const uint16_t* q, int batch, int num_q_heads,
+                                 const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens,
+                                 int max_ctx, const float* R_k, const float* R_v, const uint16_t* W_o, int d_model,
+                                 int wo_format, float* out, hipStream_t stream);
+
 /* BF16 sink and recent windows (Sec. 4.1; Sec. 5 implementation details: the paper keeps the
  * first 64 and the last 256 tokens of a sequence out of INT2). Window tokens keep the key
  * centering and are held in BF16; their values are held unchanged. The window store is a caller

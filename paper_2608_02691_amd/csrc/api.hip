@@ -1,6 +1,7 @@
 // C-ABI front end: argument validation, workspace planning and kernel dispatch.
 // Every entry point validates on the host and returns a negative status without launching on
 // any argument error; nothing here allocates device memory or synchronizes.
+#include <mutex>
 #include <string>
 
 #include "../../include/int2kv.h"
@@ -126,6 +127,35 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model, int groups)
   if (d_model > 0 && p.wo_ksplit > 1) off = up(off + (size_t)p.wo_ksplit * B * d_model * sizeof(float));
   p.total = off;
   return p;
+}
+
+// Static scratch of the allocation-free decode step (int2kv_append_decode_noalloc): the decode's
+// workspace as a file-scope device array, one copy per GPU, held until the process ends. Host code
+// never uses the array's name as an address: the device address of each GPU's copy comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kScratchBytes = (size_t)INT2KV_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch's device address on the current device (looked up on the first call per device).
+int scratch_for_current_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(INT2KV_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(INT2KV_EUNSUPPORTED, "device index above 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return fail(INT2KV_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    if (!p) return fail(INT2KV_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return INT2KV_OK;
 }
 
 }  // namespace
@@ -394,6 +424,30 @@ int int2kv_append_decode(const int2kv_cache* cache, const uint16_t* k, const uin
   }
   return decode_impl(cache, q, batch, num_q_heads, block_table, max_blocks_per_seq, ctx_lens, max_ctx, R_k, R_v, W_o,
                      d_model, wo_format, out, workspace, workspace_bytes, stream, &ap);
+}
+
+int int2kv_append_decode_noalloc(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
+                                 const int32_t* slot_mapping, int num_tokens, const float* mu_rk, float clip_k,
+                                 float clip_v, const uint16_t* q, int batch, int num_q_heads,
+                                 const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens,
+                                 int max_ctx, const float* R_k, const float* R_v, const uint16_t* W_o, int d_model,
+                                 int wo_format, float* out, hipStream_t stream) {
+  if (int st = check_cache(cache)) return st;
+  // the workspace this call needs must fit the static scratch (checked before any HIP call)
+  const int H = cache->num_kv_heads;
+  const int dm = W_o ? d_model : 0;
+  if (batch > 0 && num_q_heads > 0 && num_q_heads % H == 0 && max_ctx >= 0 && dm >= 0) {
+    const size_t need = make_plan(batch, num_q_heads, H, max_ctx, dm, kHeadDim / cache->group_size).total;
+    if (need > kScratchBytes)
+      return fail(INT2KV_EWORKSPACE, "this decode needs " + std::to_string(need) +
+                                         " bytes of workspace, more than the static scratch holds (" +
+                                         std::to_string(kScratchBytes) + "); use int2kv_append_decode");
+  }
+  void* ws = nullptr;
+  if (int st = scratch_for_current_device(&ws)) return st;
+  return int2kv_append_decode(cache, k, v, slot_mapping, num_tokens, mu_rk, clip_k, clip_v, q, batch, num_q_heads,
+                              block_table, max_blocks_per_seq, ctx_lens, max_ctx, R_k, R_v, W_o, d_model, wo_format,
+                              out, ws, kScratchBytes, stream);
 }
 
 int int2kv_decode_window(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,

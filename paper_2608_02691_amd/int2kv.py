@@ -38,7 +38,8 @@ EXPORTED = (
     "int2kv_fold_wo",
     "int2kv_prepared_wo_bytes", "int2kv_prepare_wo",
     "int2kv_quantize_pack_rotated", "int2kv_quantize_append", "int2kv_decode_workspace_bytes",
-    "int2kv_decode", "int2kv_append_decode", "int2kv_window_write", "int2kv_decode_window",
+    "int2kv_decode", "int2kv_append_decode", "int2kv_append_decode_noalloc", "int2kv_window_write",
+    "int2kv_decode_window",
     "int2kv_set_decode_tuning", "int2kv_set_decode_events",
 )
 
@@ -76,6 +77,8 @@ def load_library(path: str = LIB_PATH):
         "int2kv_decode": ([ctypes.POINTER(_Cache), P, I, I, P, I, P, I, P, P, P, I, I, P, P, Z, S], I),
         "int2kv_append_decode": ([ctypes.POINTER(_Cache), P, P, P, I, P, F, F, P, I, I, P, I, P, I, P, P, P, I, I, P,
                                   P, Z, S], I),
+        "int2kv_append_decode_noalloc": ([ctypes.POINTER(_Cache), P, P, P, I, P, F, F, P, I, I, P, I, P, I, P, P, P,
+                                          I, I, P, S], I),
         "int2kv_window_write": ([P, P, P, I, I, P, P, P, I, S], I),
         "int2kv_decode_window": ([ctypes.POINTER(_Cache), P, I, I, P, I, P, I, P, P, P, I, I, P, P, P, I, P, P, Z,
                                   S], I),
@@ -300,6 +303,37 @@ def int2kv_append_decode(cache: Int2KVCache, k: torch.Tensor, v: torch.Tensor, s
         wo_format, _ptr(out, _F32, "out"), _ptr(workspace, (torch.uint8,), "workspace"), workspace.numel(),
         _stream())
     _check(st, "int2kv_append_decode")
+    return out
+
+
+def int2kv_append_decode_noalloc(cache: Int2KVCache, k: torch.Tensor, v: torch.Tensor, slot_mapping: torch.Tensor,
+                                 mu_rk: torch.Tensor, q: torch.Tensor, block_table: torch.Tensor,
+                                 ctx_lens: torch.Tensor, max_ctx: int, R_k: torch.Tensor, R_v: torch.Tensor,
+                                 W_o: Optional[torch.Tensor] = None, wo_format: int = INT2KV_WO_PLAIN,
+                                 d_model: Optional[int] = None, clip_k: float = 1.0, clip_v: float = 1.0,
+                                 out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """int2kv_append_decode with the library's static scratch as its workspace (no workspace
+    argument; the library allocates nothing). Prepared W_o (flat) needs d_model."""
+    n = slot_mapping.shape[0]
+    if k.numel() != n * cache.num_kv_heads * HEAD_DIM or v.numel() != k.numel():
+        raise ValueError("k / v must be [n, num_kv_heads, 128]")
+    B, Hq = q.shape[0], q.shape[1]
+    if W_o is None:
+        d_model = 0
+    elif wo_format < INT2KV_WO_PREPARED:
+        d_model = W_o.shape[0]
+    elif d_model is None:
+        raise ValueError("d_model is required with prepared W_o")
+    if out is None:
+        shape = (B, d_model) if W_o is not None else (B, Hq, HEAD_DIM)
+        out = torch.empty(shape, dtype=torch.float32, device=q.device)
+    st = load_library().int2kv_append_decode_noalloc(
+        cache.desc, _ptr(k, _BF16, "k"), _ptr(v, _BF16, "v"), _ptr(slot_mapping, _I32, "slot_mapping"), n,
+        _ptr(mu_rk, _F32, "mu_rk"), clip_k, clip_v, _ptr(q, _BF16, "q"), B, Hq,
+        _ptr(block_table, _I32, "block_table"), block_table.shape[1], _ptr(ctx_lens, _I32, "ctx_lens"), max_ctx,
+        _ptr(R_k, _F32, "R_k"), _ptr(R_v, _F32, "R_v"), _ptr(W_o, _BF16 + (torch.float16,), "W_o"), d_model,
+        wo_format, _ptr(out, _F32, "out"), _stream())
+    _check(st, "int2kv_append_decode_noalloc")
     return out
 
 

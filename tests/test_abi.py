@@ -131,3 +131,13 @@ def test_tuning_knobs_are_per_thread():
     t.join()
     assert seen["other"] != base
     assert lib.int2kv_decode_workspace_bytes(4, 8, 2, 4096, 0) == base
+
+
+def test_noalloc_rejects_workspace_beyond_the_static_scratch_without_launch():
+    """A decode whose workspace exceeds the 64 MiB static scratch is refused before any HIP call."""
+    lib = K.load_library()
+    cache = K._Cache(16, 1 << 20, 8, 16, 128, 32)  # pool pointer never dereferenced
+    st = lib.int2kv_append_decode_noalloc(ctypes.byref(cache), None, None, None, 0, None, 1.0, 1.0, 16, 4096, 40,
+                                          16, 1, 16, 1 << 20, 16, 16, None, 0, 0, 16, None)
+    assert st == K.INT2KV_EWORKSPACE
+    assert b"static scratch" in lib.int2kv_last_error()
