@@ -60,110 +60,253 @@ hipError_t launch_window_write(const uint16_t* k, const uint16_t* v, const int32
   return hipGetLastError();
 }
 
-// Block (sequence b, KV head h), 256 threads, up to kWinMaxGq query heads and kWinMaxCap tokens.
-// Scores: thread per token (its 256-byte key row against the group's queries, broadcast from
-// LDS), in base-2 units as the scan's; softmax statistics: 16 lanes per query head; values:
-// thread (channel, token parity); then o' = o R_V, the scan's value basis.
-__global__ __launch_bounds__(256) void window_attn_kernel(DecodeArgs a, WindowArgs w) {
-  __shared__ float qs[kWinMaxGq][kHeadDim];
-  __shared__ float sc[kWinMaxGq][kWinMaxCap];
-  __shared__ float ow[2][kWinMaxGq][kHeadDim];
-  const int b = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, gq = a.gq;
+// Window attention of one (sequence b, KV head h), NW waves, up to kWinMaxGq query heads and
+// kWinMaxCap window tokens. Each wave takes a contiguous share of the window (a multiple of 16
+// tokens) in passes of up to 64 tokens:
+//  * scores on the matrix cores: S[j][t] = q_j . k_t over the 128 channels, one 16 x 16 x 32 bf16
+//    product per 16 tokens and 32 channels (query rows are the A operand, 16 bytes of each key row
+//    per lane the B operand; bf16 products are exact, fp32 accumulation), in the scan's base-2 units;
+//  * online softmax over the wave's passes (row maxima and sums over the 16 lanes of a DPP row);
+//  * o_j = sum_t p_jt v_t on the vector ALU: lane l owns channels 2l, 2l + 1 (one 4-byte load per
+//    value row, so each row is read by the wave in one coalesced 256-byte access), p broadcast from
+//    LDS.
+// All of a pass's key and value loads are issued before its arithmetic. The waves' partials are then
+// combined in LDS (log-sum-exp) and rotated, o' = o R_V, into the scan's value basis, with the sum
+// over channels split across the block's threads; the result is one more (m, l, o') partial per
+// (sequence, query head) that the merges fold in.
+constexpr int kWinPass = 64;  // tokens per pass of a wave (four 16-token tiles)
+
+typedef __bf16 win_bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float win_f4_t __attribute__((ext_vector_type(4)));
+
+template <int NW>
+struct WinLds {
+  float p[NW][kWinPass][kWinMaxGq];     // p[t][j] of a wave's current pass
+  float alpha[NW][kWinMaxGq];           // rescale factor of the running sums of each row
+  float m[NW][kWinMaxGq], l[NW][kWinMaxGq];
+  float o[NW][kWinMaxGq][kHeadDim];     // wave partials (model basis, unnormalized)
+};
+
+__device__ __forceinline__ float win_row_max16(float x) {
+  x = fmaxf(x, __shfl_xor(x, 8, 16));
+  x = fmaxf(x, __shfl_xor(x, 4, 16));
+  x = fmaxf(x, __shfl_xor(x, 2, 16));
+  return fmaxf(x, __shfl_xor(x, 1, 16));
+}
+__device__ __forceinline__ float win_row_sum16(float x) {
+  x += __shfl_xor(x, 8, 16);
+  x += __shfl_xor(x, 4, 16);
+  x += __shfl_xor(x, 2, 16);
+  return x + __shfl_xor(x, 1, 16);
+}
+
+// NJ4 = ceil(gq / 4): groups of four query rows the arithmetic covers (rows >= gq are zero).
+template <int NW, int NJ4>
+__device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, int h, uint8_t* lds_raw) {
+  WinLds<NW>& L = *reinterpret_cast<WinLds<NW>*>(lds_raw);
+  constexpr int NJ = 4 * NJ4;
+  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
+  const int gq = a.gq, H = a.H;
   const int W = min(max(w.lens[b], 0), w.cap);
-  for (int i = tid; i < gq * kHeadDim; i += 256)
-    qs[i / kHeadDim][i % kHeadDim] = __uint_as_float((uint32_t)a.q[((size_t)b * a.Hq + h * gq) * kHeadDim + i] << 16);
-  __syncthreads();
-  for (int t = tid; t < W; t += 256) {
-    const uint4* kr = reinterpret_cast<const uint4*>(w.k + (((size_t)b * w.cap + t) * a.H + h) * kHeadDim);
-    float acc[kWinMaxGq];
+  const int per = ((W + NW - 1) / NW + 15) & ~15;  // tokens per wave
+  const int t0 = min(W, wave * per), t1 = min(W, t0 + per);
+  const size_t row_stride = (size_t)H * kHeadDim;  // elements between consecutive window rows
+  const uint16_t* kbase = w.k + ((size_t)b * w.cap * H + h) * kHeadDim;
+  const uint16_t* vbase = w.v + ((size_t)b * w.cap * H + h) * kHeadDim;
+  float run_m[4], run_l[4];  // rows 4 hi + i (lanes of a DPP row agree)
 #pragma unroll
-    for (int j = 0; j < kWinMaxGq; ++j) acc[j] = 0.0f;
-    // the key row in four quarters: the four 16-byte loads of a quarter are issued before its
-    // arithmetic (register arrays with static indices only, so nothing goes to scratch)
-    for (int c32 = 0; c32 < kHeadDim / 32; ++c32) {
-      uint4 row[4];
+  for (int i = 0; i < 4; ++i) {
+    run_m[i] = -INFINITY;
+    run_l[i] = 0.0f;
+  }
+  float oacc[NJ][2];
 #pragma unroll
-      for (int u4 = 0; u4 < 4; ++u4) row[u4] = kr[4 * c32 + u4];
+  for (int j = 0; j < NJ; ++j) oacc[j][0] = oacc[j][1] = 0.0f;
+  for (int p0 = t0; p0 < t1; p0 += kWinPass) {
+    const int nt = min(kWinPass, t1 - p0);
+    // every key and value load of the pass first (tokens past the share read the window's last
+    // row and get p = 0), then the query operand
+    win_bf16x8_t kr[4][4];
 #pragma unroll
-      for (int u4 = 0; u4 < 4; ++u4) {
-        const uint4 u = row[u4];
-        const float kf[8] = {bf_lo(u.x), bf_hi(u.x), bf_lo(u.y), bf_hi(u.y),
-                             bf_lo(u.z), bf_hi(u.z), bf_lo(u.w), bf_hi(u.w)};
-        const int c0 = 32 * c32 + 8 * u4;
+    for (int u = 0; u < 4; ++u) {
+      const int t = min(p0 + 16 * u + lo, W - 1);
 #pragma unroll
-        for (int j = 0; j < kWinMaxGq; ++j) {
-          if (j < gq) {
+      for (int ks = 0; ks < 4; ++ks)
+        kr[u][ks] = *reinterpret_cast<const win_bf16x8_t*>(kbase + (size_t)t * row_stride + 32 * ks + 8 * hi);
+    }
+    uint32_t vr[kWinPass];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[j] = fmaf(qs[j][c0 + e], kf[e], acc[j]);
-          }
-        }
+    for (int i = 0; i < kWinPass; ++i)
+      vr[i] = *reinterpret_cast<const uint32_t*>(vbase + (size_t)min(p0 + i, W - 1) * row_stride + 2 * l);
+    // query operand: lane (row lo, k block hi) holds q_lo[32 ks + 8 hi .. + 7]; rows >= gq are zero
+    win_bf16x8_t qa[4];
+    {
+      const int j = min(lo, gq - 1);
+      const uint16_t* qr = a.q + ((size_t)b * a.Hq + h * gq + j) * kHeadDim + 8 * hi;
+      const uint32_t keep = lo < gq ? ~0u : 0u;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const uint4 v = *reinterpret_cast<const uint4*>(qr + 32 * ks);
+        qa[ks] = __builtin_bit_cast(win_bf16x8_t, make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep));
+      }
+    }
+    // scores of rows 4 hi + r for token 16 u + lo of the pass, base-2 units, -inf past the share
+    float sc[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      win_f4_t d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[ks], kr[u][ks], d, 0, 0, 0);
+      const bool valid = 16 * u + lo < nt;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sc[u][r] = valid ? d[r] * kWinLogit2 : -INFINITY;
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float pm = win_row_max16(fmaxf(fmaxf(sc[0][r], sc[1][r]), fmaxf(sc[2][r], sc[3][r])));
+      const float mnew = fmaxf(run_m[r], pm);  // pm is finite: the pass holds a valid token
+      const float al = __builtin_amdgcn_exp2f(run_m[r] - mnew);
+      float rs = 0.0f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float p = __builtin_amdgcn_exp2f(sc[u][r] - mnew);
+        rs += p;
+        L.p[wave][16 * u + lo][4 * hi + r] = p;
+      }
+      run_l[r] = al * run_l[r] + win_row_sum16(rs);
+      run_m[r] = mnew;
+      if (lo == 0) L.alpha[wave][4 * hi + r] = al;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // o_j = alpha_j o_j + sum_t p_jt v_t on this lane's two channels (p = 0 past the share)
+#pragma unroll
+    for (int j4 = 0; j4 < NJ4; ++j4) {
+      const win_f4_t al = *reinterpret_cast<const win_f4_t*>(&L.alpha[wave][4 * j4]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        oacc[4 * j4 + r][0] *= al[r];
+        oacc[4 * j4 + r][1] *= al[r];
       }
     }
 #pragma unroll
-    for (int j = 0; j < kWinMaxGq; ++j)
-      if (j < gq) sc[j][t] = acc[j] * kWinLogit2;
-  }
-  __syncthreads();
-  const int jr = tid >> 4, lr = tid & 15;
-  float m = -INFINITY, l = 0.0f;
-  if (jr < gq) {
-    for (int t = lr; t < W; t += 16) m = fmaxf(m, sc[jr][t]);
+    for (int i = 0; i < kWinPass; ++i) {
+      const float v0 = __uint_as_float(vr[i] << 16), v1 = __uint_as_float(vr[i] & 0xFFFF0000u);
 #pragma unroll
-    for (int o = 8; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 16));
-    for (int t = lr; t < W; t += 16) {
-      const float p = exp2f(sc[jr][t] - m);
-      sc[jr][t] = p;
-      l += p;
+      for (int j4 = 0; j4 < NJ4; ++j4) {
+        const win_f4_t pt = *reinterpret_cast<const win_f4_t*>(&L.p[wave][i][4 * j4]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          oacc[4 * j4 + r][0] = fmaf(pt[r], v0, oacc[4 * j4 + r][0]);
+          oacc[4 * j4 + r][1] = fmaf(pt[r], v1, oacc[4 * j4 + r][1]);
+        }
+      }
     }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  // the rotation's R_V column slice of this thread, fetched now so its latency overlaps the combine:
+  // thread (c', part) sums channels part * kPerPart .. + kPerPart - 1 of o_j for column c'
+  constexpr int kThreads = 64 * NW;
+  constexpr int kParts = kThreads / kHeadDim, kPerPart = kHeadDim / kParts;
+  const int cc = tid % kHeadDim, part = tid / kHeadDim;
+  const float* Rv = a.R_v + (size_t)h * kHeadDim * kHeadDim + (size_t)part * kPerPart * kHeadDim + cc;
+  float rv[kPerPart];
 #pragma unroll
-    for (int o = 8; o > 0; o >>= 1) l += __shfl_xor(l, o, 16);
+  for (int i = 0; i < kPerPart; ++i) rv[i] = Rv[(size_t)i * kHeadDim];
+  // the wave's partial (a wave without tokens leaves m = -inf, l = 0, o = 0)
+  if (lo == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      L.m[wave][4 * hi + r] = run_m[r];
+      L.l[wave][4 * hi + r] = run_l[r];
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) *reinterpret_cast<float2*>(&L.o[wave][j][2 * l]) = make_float2(oacc[j][0], oacc[j][1]);
+  __syncthreads();
+  // combine the waves: o_j = sum_w 2^(m_wj - M_j) o_wj (then kept in L.o[0]), M_j, L_j
+  float* ob = &L.o[0][0][0];
+  constexpr int kPer = NJ * kHeadDim / kThreads > 0 ? NJ * kHeadDim / kThreads : 1;
+  float comb[kPer];
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) {
+    const int idx = tid + e * kThreads, j = idx / kHeadDim, c = idx % kHeadDim;
+    comb[e] = 0.0f;
+    if (j < NJ) {
+      float M = -INFINITY;
+#pragma unroll
+      for (int v = 0; v < NW; ++v) M = fmaxf(M, L.m[v][j]);
+      if (M > -INFINITY) {
+#pragma unroll
+        for (int v = 0; v < NW; ++v) comb[e] = fmaf(__builtin_amdgcn_exp2f(L.m[v][j] - M), L.o[v][j][c], comb[e]);
+      }
+    }
+  }
+  float Mj = -INFINITY, Lj = 0.0f;
+  if (tid < gq) {
+#pragma unroll
+    for (int v = 0; v < NW; ++v) Mj = fmaxf(Mj, L.m[v][tid]);
+    if (Mj > -INFINITY) {
+#pragma unroll
+      for (int v = 0; v < NW; ++v) Lj = fmaf(__builtin_amdgcn_exp2f(L.m[v][tid] - Mj), L.l[v][tid], Lj);
+    }
   }
   __syncthreads();
-  const int c = tid & 127, par = tid >> 7;
-  float o[kWinMaxGq];
 #pragma unroll
-  for (int j = 0; j < kWinMaxGq; ++j) o[j] = 0.0f;
-  // unrolled so that several value loads are in flight per thread
-#pragma unroll 8
-  for (int t = par; t < W; t += 2) {
-    const float vv = __uint_as_float((uint32_t)w.v[(((size_t)b * w.cap + t) * a.H + h) * kHeadDim + c] << 16);
-#pragma unroll
-    for (int j = 0; j < kWinMaxGq; ++j)
-      if (j < gq) o[j] = fmaf(sc[j][t], vv, o[j]);
-  }
-#pragma unroll
-  for (int j = 0; j < kWinMaxGq; ++j)
-    if (j < gq) ow[par][j][c] = o[j];
+  for (int e = 0; e < kPer; ++e)
+    if (tid + e * kThreads < NJ * kHeadDim) ob[tid + e * kThreads] = comb[e];
   __syncthreads();
-  for (int i = tid; i < gq * kHeadDim; i += 256) ow[0][i / kHeadDim][i % kHeadDim] += ow[1][i / kHeadDim][i % kHeadDim];
+  // o'_j[c'] = sum_c o_j[c] R_V[c][c']: each part's sums are added through LDS (the space of the
+  // other waves' partials is free again)
+  float acc[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) acc[j] = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kPerPart; ++i) {
+    const int c = part * kPerPart + i;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[j] = fmaf(ob[j * kHeadDim + c], rv[i], acc[j]);
+  }
+  float* red = &L.o[kParts > 1 ? 1 : 0][0][0];  // [part][j][c'] after the combined rows of L.o[0]
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) red[(part * NJ + j) * kHeadDim + cc] = acc[j];
   __syncthreads();
-  // o'[j][c] = sum_i o[j][i] R_V[i][c]: thread (c, par) for query heads par, par + 2, ...
-  float acc[kWinMaxGq / 2];
+  for (int idx = tid; idx < gq * kHeadDim; idx += kThreads) {
+    const int j = idx / kHeadDim, c = idx % kHeadDim;
+    float s = 0.0f;
 #pragma unroll
-  for (int r = 0; r < kWinMaxGq / 2; ++r) acc[r] = 0.0f;
-  const float* Rv = a.R_v + (size_t)h * kHeadDim * kHeadDim;
-#pragma unroll 16
-  for (int i = 0; i < kHeadDim; ++i) {
-    const float rv = Rv[(size_t)i * kHeadDim + c];
-#pragma unroll
-    for (int r = 0; r < kWinMaxGq / 2; ++r)
-      if (par + 2 * r < gq) acc[r] = fmaf(ow[0][par + 2 * r][i], rv, acc[r]);
+    for (int pp = 0; pp < kParts; ++pp) s += red[(pp * NJ + j) * kHeadDim + c];
+    a.wpart[((size_t)b * a.Hq + h * gq + j) * kPartStride + 4 + c] = s;
   }
-#pragma unroll
-  for (int r = 0; r < kWinMaxGq / 2; ++r) {
-    const int j = par + 2 * r;
-    if (j < gq) a.wpart[((size_t)b * a.Hq + h * gq + j) * kPartStride + 4 + c] = acc[r];
+  if (tid < gq) {
+    float* pp = a.wpart + ((size_t)b * a.Hq + h * gq + tid) * kPartStride;
+    pp[0] = Mj;
+    pp[1] = Lj;
   }
-  if (jr < gq && lr == 0) {
-    float* pp = a.wpart + ((size_t)b * a.Hq + h * gq + jr) * kPartStride;
-    pp[0] = W > 0 ? m : -INFINITY;
-    pp[1] = l;
-  }
+}
+
+constexpr int kWinWaves = 8;
+static_assert(sizeof(WinLds<kWinWaves>) <= 160 * 1024, "window block LDS");
+static_assert(kWinMaxCap <= kWinWaves * kWinPass * 4, "window passes");
+
+template <int NJ4>
+__global__ __launch_bounds__(64 * kWinWaves) void window_attn_kernel(DecodeArgs a, WindowArgs w) {
+  __shared__ __attribute__((aligned(16))) uint8_t win_lds[sizeof(WinLds<kWinWaves>)];
+  window_block<kWinWaves, NJ4>(a, w, blockIdx.x, blockIdx.y, win_lds);
 }
 
 hipError_t launch_window_attn(const DecodeArgs& a, const WindowArgs& w, hipStream_t s) {
   if (a.gq > kWinMaxGq || w.cap > kWinMaxCap) return hipErrorNotSupported;
-  hipLaunchKernelGGL(window_attn_kernel, dim3(a.B, a.H), dim3(256), 0, s, a, w);
+  const dim3 grid(a.B, a.H), block(64 * kWinWaves);
+  switch ((a.gq + 3) / 4) {
+    case 1: hipLaunchKernelGGL(window_attn_kernel<1>, grid, block, 0, s, a, w); break;
+    case 2: hipLaunchKernelGGL(window_attn_kernel<2>, grid, block, 0, s, a, w); break;
+    case 3: hipLaunchKernelGGL(window_attn_kernel<3>, grid, block, 0, s, a, w); break;
+    default: hipLaunchKernelGGL(window_attn_kernel<4>, grid, block, 0, s, a, w); break;
+  }
   return hipGetLastError();
 }
 
