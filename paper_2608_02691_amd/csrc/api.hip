@@ -119,8 +119,8 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model, int groups)
   p.off_part = off;
   const size_t part_rows = p.variant == 2 ? (size_t)(p.grid_g + B) : (size_t)B * p.n_chunks;
   off = up(off + part_rows * Hq * kPartStride * sizeof(float));
-  p.off_win = off;  // BF16-window partials, [B, Hq, kPartStride]
-  off = up(off + (size_t)B * Hq * kPartStride * sizeof(float));
+  p.off_win = off;  // BF16-window partials, [kWinSlices][B, Hq, kPartStride]
+  off = up(off + (size_t)kWinSlices * B * Hq * kPartStride * sizeof(float));
   p.off_o = off;
   if (d_model > 0) off = up(off + (size_t)B * Hq * kHeadDim * sizeof(float));
   p.off_wo = off;

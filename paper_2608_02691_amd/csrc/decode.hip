@@ -258,22 +258,26 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeArgs a, int unrotate, 
     const int j = h * a.gq + jj;
     const float* part = a.part + ((size_t)b * a.n_chunks * a.Hq + j) * kPartStride;
     const size_t stride = (size_t)a.Hq * kPartStride;
-    // the BF16-window partial (when there is one) joins the chunk partials
-    float wm = -INFINITY, wl = 0.0f, wo = 0.0f;
-    if (a.wpart) {
-      const float* wp = a.wpart + ((size_t)b * a.Hq + j) * kPartStride;
-      wm = wp[0];
-      wl = wp[1];
-      wo = wp[4 + c];
+    // the BF16-window partials (when there are some) join the chunk partials
+    float wm[kWinSlices], wl[kWinSlices], wo[kWinSlices];
+    float M = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < kWinSlices; ++s) {
+      wm[s] = -INFINITY;
+      wl[s] = wo[s] = 0.0f;
+      if (a.wpart) {
+        const float* wp = a.wpart + (((size_t)s * a.B + b) * a.Hq + j) * kPartStride;
+        wm[s] = wp[0];
+        wl[s] = wp[1];
+        wo[s] = wp[4 + c];
+      }
+      M = fmaxf(M, wm[s]);
     }
-    float M = wm;
     for (int i = 0; i < nch; ++i) M = fmaxf(M, part[i * stride]);
-    float lsum = 0.0f, osum = 0.0f;
-    if (wm != -INFINITY) {
-      const float f = exp2f(wm - M);
-      lsum = f * wl;
-      osum = f * wo;
-    }
+    float lsum = 0.0f, osum = 0.0f;  // osum: the INT2 part only (the window's o is in another basis)
+#pragma unroll
+    for (int s = 0; s < kWinSlices; ++s)
+      if (wm[s] != -INFINITY) lsum = fmaf(exp2f(wm[s] - M), wl[s], lsum);
     for (int i = 0; i < nch; ++i) {
       const float mi = part[i * stride];
       const float f = mi == -INFINITY ? 0.0f : exp2f(mi - M);
@@ -282,7 +286,35 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeArgs a, int unrotate, 
     }
     const float val = lsum > 0.0f ? osum / lsum : 0.0f;
     float res = val;
-    if (unrotate) {
+    if (a.wpart) {
+      // the window part (model basis) joins in the output's basis: o = o_int2 R_V^T + o_win, or
+      // o' = o_int2 + o_win R_V for a folded W_O
+      float ow = 0.0f;
+#pragma unroll
+      for (int s = 0; s < kWinSlices; ++s)
+        if (wm[s] != -INFINITY) ow = fmaf(exp2f(wm[s] - M), wo[s], ow);
+      ow = lsum > 0.0f ? ow / lsum : 0.0f;
+      const float oi = val;
+      os[c] = unrotate ? oi : ow;
+      __syncthreads();
+      float acc = unrotate ? ow : oi;
+      if (unrotate) {
+        const float4* row = reinterpret_cast<const float4*>(Rv + (size_t)c * kHeadDim);
+#pragma unroll 8
+        for (int i = 0; i < kHeadDim / 4; ++i) {
+          const float4 r = row[i];
+          acc = fmaf(os[4 * i], r.x, acc);
+          acc = fmaf(os[4 * i + 1], r.y, acc);
+          acc = fmaf(os[4 * i + 2], r.z, acc);
+          acc = fmaf(os[4 * i + 3], r.w, acc);
+        }
+      } else {
+#pragma unroll 8
+        for (int i = 0; i < kHeadDim; ++i) acc = fmaf(os[i], Rv[(size_t)i * kHeadDim + c], acc);
+      }
+      res = acc;
+      __syncthreads();
+    } else if (unrotate) {
       os[c] = val;
       __syncthreads();
       const float4* row = reinterpret_cast<const float4*>(Rv + (size_t)c * kHeadDim);

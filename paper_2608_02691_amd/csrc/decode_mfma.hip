@@ -547,31 +547,21 @@ __device__ __forceinline__ void softmax_pair(ScanState<WIDE>& st, const float (&
 // channels; p comes back from LDS in the layout of the B operand.
 //
 // The weights w = p s enter the matrix cores as fp16. Lazy rescaling keeps p <= 2^tau = 256, so
-// w is finite for every scale s < 256. A pair holding a larger V scale (a rotated value range
-// above 768; detected by a wave vote) takes the scaled form: the codes land on the fp16 pattern
-// of 256 instead of 1.0 (A' = 256 (1 + c 2^-e), exact), the weights are w' = fp16(p s / 256)
-// formed in fp32 and the weight sums add 256 w'. The products A' w' are those of the plain form,
-// so both forms add into the same accumulators and the final correction
-// (O = 2^e (D - sum w) + Z) is unchanged. Only the weights and the landing base differ, so the
-// matrix-core chain is shared.
-template <bool WIDE, int NG>
+// w is finite for every scale s < 256; a larger V scale (a rotated value range above 768) can make
+// it overflow to inf, which then shows in the weight sums. The scaled form (big, uniform over the
+// wave) keeps every weight finite: the codes land on the fp16 pattern of 256 instead of 1.0
+// (A' = 256 (1 + c 2^-e), exact), the weights are w' = fp16(p s / 256) formed in fp32 and the
+// weight sums add 256 w'. The products A' w' are those of the plain form and the final correction
+// (O = 2^e (D - sum w) + Z) is unchanged. The scan runs a segment in the plain form and repeats it
+// in the scaled form only when its sums came out non-finite.
+template <bool WIDE, int NG, bool big>
 __device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WIDE>& cur, int lo, int hi,
                                         const _Float16 (*p_w)[8][kBlock]) {
   // with one group per token every group column has the same weights: one weight operand (and one
   // weight sum) serves all tiles
   constexpr int NT = NG == 1 ? 1 : ScanState<WIDE>::NT;
-  // largest V scale of the pair held by this lane (scales are never negative or NaN)
-  half2_t smax = __builtin_elementwise_max(as_h2(cur.vs[0][0].x), as_h2(cur.vs[0][0].y));
-#pragma unroll
-  for (int P = 0; P < 2; ++P)
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-      if (P + t > 0)
-        smax = __builtin_elementwise_max(smax,
-                                         __builtin_elementwise_max(as_h2(cur.vs[P][t].x), as_h2(cur.vs[P][t].y)));
-  const bool big = __any((float)smax.x >= 256.0f || (float)smax.y >= 256.0f) != 0;
   LandK lk = st.lk;
-  if (big) lk.one = 0x5C005C00u;  // fp16 256.0, twice
+  if constexpr (big) lk.one = 0x5C005C00u;  // fp16 256.0, twice
   // A operand of the (Z, l) contraction: rows 0..3 hold z of group `row` (the V zeros this lane
   // already has, group lo & 3 = row), rows 4..7 hold 1.0, rows 8..15 zero
   const half2_t zmul = lo < 4 ? half2_t{(_Float16)1.0f, (_Float16)1.0f} : half2_t{(_Float16)0.0f, (_Float16)0.0f};
@@ -588,7 +578,7 @@ __device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WID
   const half8_t Bp = __builtin_bit_cast(half8_t, u32x4_t{pp0.x, pp0.y, pp1.x, pp1.y});
   uint32_t wv[NT][4];
   const uint32_t pw[4] = {pp0.x, pp0.y, pp1.x, pp1.y};
-  if (__builtin_expect(big, 0)) {
+  if constexpr (big) {
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -792,8 +782,10 @@ __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)
 
 // One wave: KV head h of sequence b, global pages [gs, ge) (all of sequence b), with its partial
 // (m, l, O') per query head written to partial slot `slot`.
-template <bool WIDE, int NG>
-__device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, int gs, int ge, int slot, int l,
+// big: every pair in the scaled value form (see pv_pair). Returns whether the segment's sums are
+// finite (uniform over the wave); with big they always are.
+template <bool WIDE, int NG, bool BIG>
+__device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, int gs, int ge, int slot, int l,
                                              uint8_t* stage_w, _Float16 (*p_w)[2][8][kBlock], float* al_w,
                                              bool all_waves) {
   constexpr int NJ = ScanState<WIDE>::NJ, NT = ScanState<WIDE>::NT;
@@ -944,7 +936,7 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
     float a2[2][NJ];
     if (more) qk_pair<WIDE, NG>(st, nxt, lo, a2);
     lds_sync_wave();
-    pv_pair<WIDE, NG>(st, cur, lo, hi, p_w[kk & 1]);
+    pv_pair<WIDE, NG, BIG>(st, cur, lo, hi, p_w[kk & 1]);
     if (more) softmax_pair<WIDE>(st, a2, lo, hi, p_w[(kk + 1) & 1], al_w);
   };
   using T = std::true_type;
@@ -1033,6 +1025,10 @@ __device__ __forceinline__ void scan_segment(const DecodeArgs& a, int b, int h, 
   INT2KV_OUT_TILE(7)
 #undef INT2KV_OUT_TILE
   wait_vm_all();
+  bool fin = true;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) fin = fin && __builtin_isfinite(st.wsum[t][0]);
+  return __any(!fin) == 0;
 }
 
 // Persistent, head-grouped scan: work-group g covers pages [lo(g), lo(g+1)) of the concatenation
@@ -1067,7 +1063,12 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   for (int pos = s;;) {
     const int seg_end = min(e, Sb1);
     const int Sb2 = seg_end < e ? prefix[b + 2] : 0;  // next sequence's end, fetched ahead
-    scan_segment<WIDE, NG>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w], all_waves);
+    // a segment whose value sums overflowed fp16 (V scales of 256 and more) is scanned again by this
+    // wave in the scaled form, without the steady loop's work-group barriers: every wave still
+    // executes the same number of barriers, so the others only wait for it at their next one
+    if (!scan_segment<WIDE, NG, false>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w],
+                                       all_waves))
+      scan_segment<WIDE, NG, true>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w], false);
     pos = seg_end;
     if (pos >= e) break;
     ++b;
@@ -1092,7 +1093,24 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
   __shared__ float ms[kMergeSlots][8], ls[kMergeSlots][8];
   __shared__ float os[kMergeSlots][8][kHeadDim];
   __shared__ float vs[8][kHeadDim];
+  __shared__ float wsh[8][kHeadDim];  // BF16-window part of each head output (model basis)
   const int b = blockIdx.x, h = blockIdx.y, c = threadIdx.x & 127, sl = threadIdx.x >> 7, gq = a.gq;
+  // the BF16-window partials of this thread's query heads (model basis), loaded first: kWinSlices
+  // partials per head, folded into one (m, l, o) below
+  constexpr int kR = 8 / kMergeSlots;
+  float wm[kR][kWinSlices], wl[kR][kWinSlices], wo[kR][kWinSlices];
+  if (a.wpart) {
+#pragma unroll
+    for (int r = 0; r < kR; ++r)
+#pragma unroll
+      for (int s = 0; s < kWinSlices; ++s) {
+        const float* pp =
+            a.wpart + (((size_t)s * a.B + b) * a.Hq + h * gq + min(sl + kMergeSlots * r, gq - 1)) * kPartStride;
+        wm[r][s] = pp[0];
+        wl[r][s] = pp[1];
+        wo[r][s] = pp[4 + c];
+      }
+  }
   // groups whose ranges meet the sequence, from the page-prefix block
   const int ga = a.seq_wg[2 * b], gb = a.seq_wg[2 * b + 1];
   float M[8], lsum[8], osum[8];
@@ -1101,19 +1119,6 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
     M[jj] = -INFINITY;
     lsum[jj] = 0.0f;
     osum[jj] = 0.0f;
-  }
-  if (a.wpart && sl == 0) {
-    // the BF16-window partial starts slot 0 (merging it into the empty state is taking it)
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
-      const float* pp = a.wpart + ((size_t)b * a.Hq + h * gq + min(jj, gq - 1)) * kPartStride;
-      const float mv = pp[0], lv = pp[1], ov = pp[4 + c];
-      if (mv != -INFINITY) {
-        M[jj] = mv;
-        lsum[jj] = lv;
-        osum[jj] = ov;
-      }
-    }
   }
   for (int gg = ga + sl; gg <= gb; gg += kMergeSlots) {
     // the range bounds and the partial are loaded together (one round trip): slot gg + b exists for
@@ -1153,14 +1158,18 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
   for (int jj = 0; jj < 8; ++jj) os[sl][jj][c] = osum[jj];
   __syncthreads();
   // thread (c, s): query heads s, s + kMergeSlots, ..., channel c, the slots in a fixed order
-  float val[8 / kMergeSlots];
+  float val[8 / kMergeSlots], wval[8 / kMergeSlots];
 #pragma unroll
   for (int r = 0; r < 8 / kMergeSlots; ++r) {
     const int jj = sl + kMergeSlots * r;
     float Mx = -INFINITY;
 #pragma unroll
     for (int t = 0; t < kMergeSlots; ++t) Mx = fmaxf(Mx, ms[t][jj]);
-    float L = 0.0f, O = 0.0f;
+    if (a.wpart) {
+#pragma unroll
+      for (int s = 0; s < kWinSlices; ++s) Mx = fmaxf(Mx, wm[r][s]);
+    }
+    float L = 0.0f, O = 0.0f, Ow = 0.0f;
 #pragma unroll
     for (int t = 0; t < kMergeSlots; ++t) {
       const float mt = ms[t][jj];
@@ -1168,43 +1177,74 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
       L = fmaf(f, ls[t][jj], L);
       O = fmaf(f, os[t][jj][c], O);
     }
-    val[r] = L > 0.0f ? O / L : 0.0f;
-  }
-  if (unrotate) {
+    if (a.wpart) {
 #pragma unroll
-    for (int r = 0; r < 8 / kMergeSlots; ++r) vs[sl + kMergeSlots * r][c] = val[r];
-    __syncthreads();
-    if (sl == 0) {
-      const float4* row = reinterpret_cast<const float4*>(a.R_v + ((size_t)h * kHeadDim + c) * kHeadDim);
-      float acc[8];
-#pragma unroll
-      for (int j2 = 0; j2 < 8; ++j2) acc[j2] = 0.0f;
-#pragma unroll 4
-      for (int i = 0; i < kHeadDim / 4; ++i) {
-        const float4 rr = row[i];
-#pragma unroll
-        for (int j2 = 0; j2 < 8; ++j2) {
-          if (j2 < gq) {
-            acc[j2] = fmaf(vs[j2][4 * i], rr.x, acc[j2]);
-            acc[j2] = fmaf(vs[j2][4 * i + 1], rr.y, acc[j2]);
-            acc[j2] = fmaf(vs[j2][4 * i + 2], rr.z, acc[j2]);
-            acc[j2] = fmaf(vs[j2][4 * i + 3], rr.w, acc[j2]);
-          }
-        }
+      for (int s = 0; s < kWinSlices; ++s) {
+        const float f = wm[r][s] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(wm[r][s] - Mx);
+        L = fmaf(f, wl[r][s], L);
+        Ow = fmaf(f, wo[r][s], Ow);
       }
+    }
+    val[r] = L > 0.0f ? O / L : 0.0f;
+    wval[r] = L > 0.0f ? Ow / L : 0.0f;
+  }
+  if (!a.wpart && !unrotate) {
 #pragma unroll
-      for (int j2 = 0; j2 < 8; ++j2)
-        if (j2 < gq)
-          store_head_out(acc[j2], out, ob, fmt, ((size_t)b * a.Hq + h * gq + j2) * kHeadDim + c,
-                         (size_t)a.B * a.Hq * kHeadDim);
+    for (int r = 0; r < 8 / kMergeSlots; ++r) {
+      const int jj = sl + kMergeSlots * r;
+      if (jj < gq)
+        store_head_out(val[r], out, ob, fmt, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c,
+                       (size_t)a.B * a.Hq * kHeadDim);
     }
     return;
   }
+  // The output's basis: o = o_int2 R_V^T (+ o_win, model basis) when the merge un-rotates, or
+  // o' = o_int2 + o_win R_V when the output projection is folded with R_V. Every thread (c, slot)
+  // sums the channels i of its slot's part of the product for all heads (all of its R_V loads issued
+  // together), and the parts are added through LDS.
+#pragma unroll
+  for (int r = 0; r < 8 / kMergeSlots; ++r) {
+    vs[sl + kMergeSlots * r][c] = val[r];
+    wsh[sl + kMergeSlots * r][c] = wval[r];
+  }
+  __syncthreads();
+  constexpr int kPart = kHeadDim / kMergeSlots;
+  const float* R = a.R_v + (size_t)h * kHeadDim * kHeadDim;
+  float rv[kPart];
+  if (unrotate) {
+    const float4* row = reinterpret_cast<const float4*>(R + (size_t)c * kHeadDim + sl * kPart);  // R_V[c][i]
+#pragma unroll
+    for (int i4 = 0; i4 < kPart / 4; ++i4) {
+      const float4 q4 = row[i4];
+      rv[4 * i4] = q4.x;
+      rv[4 * i4 + 1] = q4.y;
+      rv[4 * i4 + 2] = q4.z;
+      rv[4 * i4 + 3] = q4.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kPart; ++i) rv[i] = R[(size_t)(sl * kPart + i) * kHeadDim + c];  // R_V[i][c]
+  }
+  float acc[8];
+#pragma unroll
+  for (int j2 = 0; j2 < 8; ++j2) acc[j2] = 0.0f;
+  const float(*src)[kHeadDim] = unrotate ? vs : wsh;
+#pragma unroll
+  for (int i = 0; i < kPart; ++i)
+#pragma unroll
+    for (int j2 = 0; j2 < 8; ++j2) acc[j2] = fmaf(src[j2][sl * kPart + i], rv[i], acc[j2]);
+#pragma unroll
+  for (int j2 = 0; j2 < 8; ++j2) os[sl][j2][c] = acc[j2];  // the slots' partials are no longer needed
+  __syncthreads();
+  const float(*add)[kHeadDim] = unrotate ? wsh : vs;
 #pragma unroll
   for (int r = 0; r < 8 / kMergeSlots; ++r) {
     const int jj = sl + kMergeSlots * r;
+    float o = a.wpart ? add[jj][c] : 0.0f;
+#pragma unroll
+    for (int t = 0; t < kMergeSlots; ++t) o += os[t][jj][c];
     if (jj < gq)
-      store_head_out(val[r], out, ob, fmt, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c,
+      store_head_out(o, out, ob, fmt, ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c,
                      (size_t)a.B * a.Hq * kHeadDim);
   }
 }

@@ -60,8 +60,10 @@ hipError_t launch_window_write(const uint16_t* k, const uint16_t* v, const int32
   return hipGetLastError();
 }
 
-// Window attention of one (sequence b, KV head h), NW waves, up to kWinMaxGq query heads and
-// kWinMaxCap window tokens. Each wave takes a contiguous share of the window (a multiple of 16
+// Window attention of one slice of the window of (sequence b, KV head h): the window is cut into
+// kWinSlices slices, each a block of NW waves writing its own (m, l, o') partial (two blocks of a
+// CU then overlap one's loads with the other's arithmetic); up to kWinMaxGq query heads and
+// kWinMaxCap window tokens. Each wave takes a contiguous share of its slice (a multiple of 16
 // tokens) in passes of up to 64 tokens:
 //  * scores on the matrix cores: S[j][t] = q_j . k_t over the 128 channels, one 16 x 16 x 32 bf16
 //    product per 16 tokens and 32 channels (query rows are the A operand, 16 bytes of each key row
@@ -71,9 +73,10 @@ hipError_t launch_window_write(const uint16_t* k, const uint16_t* v, const int32
 //    value row, so each row is read by the wave in one coalesced 256-byte access), p broadcast from
 //    LDS.
 // All of a pass's key and value loads are issued before its arithmetic. The waves' partials are then
-// combined in LDS (log-sum-exp) and rotated, o' = o R_V, into the scan's value basis, with the sum
-// over channels split across the block's threads; the result is one more (m, l, o') partial per
-// (sequence, query head) that the merges fold in.
+// combined in LDS (log-sum-exp) into the slice's (m, l, o) partial, in the model's basis: the merges
+// fold the kWinSlices partials of a (sequence, query head) into the INT2 result in the basis of the
+// output (adding o after the INT2 part's un-rotation, or rotating o by R_V when the output
+// projection is folded with R_V).
 constexpr int kWinPass = 64;  // tokens per pass of a wave (four 16-token tiles)
 
 typedef __bf16 win_bf16x8_t __attribute__((ext_vector_type(8)));
@@ -102,14 +105,17 @@ __device__ __forceinline__ float win_row_sum16(float x) {
 
 // NJ4 = ceil(gq / 4): groups of four query rows the arithmetic covers (rows >= gq are zero).
 template <int NW, int NJ4>
-__device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, int h, uint8_t* lds_raw) {
+__device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, int h, int slice, uint8_t* lds_raw) {
   WinLds<NW>& L = *reinterpret_cast<WinLds<NW>*>(lds_raw);
   constexpr int NJ = 4 * NJ4;
   const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
   const int gq = a.gq, H = a.H;
   const int W = min(max(w.lens[b], 0), w.cap);
-  const int per = ((W + NW - 1) / NW + 15) & ~15;  // tokens per wave
-  const int t0 = min(W, wave * per), t1 = min(W, t0 + per);
+  // the slice's tokens, then this wave's share of them (multiples of 16 tokens)
+  const int half = ((W + kWinSlices - 1) / kWinSlices + 15) & ~15;
+  const int s0 = min(W, slice * half), s1 = min(W, s0 + half);
+  const int per = ((s1 - s0 + NW - 1) / NW + 15) & ~15;
+  const int t0 = min(s1, s0 + wave * per), t1 = min(s1, t0 + per);
   const size_t row_stride = (size_t)H * kHeadDim;  // elements between consecutive window rows
   const uint16_t* kbase = w.k + ((size_t)b * w.cap * H + h) * kHeadDim;
   const uint16_t* vbase = w.v + ((size_t)b * w.cap * H + h) * kHeadDim;
@@ -207,16 +213,8 @@ __device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, in
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
-  // the rotation's R_V column slice of this thread, fetched now so its latency overlaps the combine:
-  // thread (c', part) sums channels part * kPerPart .. + kPerPart - 1 of o_j for column c'
-  constexpr int kThreads = 64 * NW;
-  constexpr int kParts = kThreads / kHeadDim, kPerPart = kHeadDim / kParts;
-  const int cc = tid % kHeadDim, part = tid / kHeadDim;
-  const float* Rv = a.R_v + (size_t)h * kHeadDim * kHeadDim + (size_t)part * kPerPart * kHeadDim + cc;
-  float rv[kPerPart];
-#pragma unroll
-  for (int i = 0; i < kPerPart; ++i) rv[i] = Rv[(size_t)i * kHeadDim];
   // the wave's partial (a wave without tokens leaves m = -inf, l = 0, o = 0)
+  constexpr int kThreads = 64 * NW;
   if (lo == 0) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -227,80 +225,50 @@ __device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, in
 #pragma unroll
   for (int j = 0; j < NJ; ++j) *reinterpret_cast<float2*>(&L.o[wave][j][2 * l]) = make_float2(oacc[j][0], oacc[j][1]);
   __syncthreads();
-  // combine the waves: o_j = sum_w 2^(m_wj - M_j) o_wj (then kept in L.o[0]), M_j, L_j
-  float* ob = &L.o[0][0][0];
-  constexpr int kPer = NJ * kHeadDim / kThreads > 0 ? NJ * kHeadDim / kThreads : 1;
-  float comb[kPer];
-#pragma unroll
-  for (int e = 0; e < kPer; ++e) {
-    const int idx = tid + e * kThreads, j = idx / kHeadDim, c = idx % kHeadDim;
-    comb[e] = 0.0f;
-    if (j < NJ) {
-      float M = -INFINITY;
-#pragma unroll
-      for (int v = 0; v < NW; ++v) M = fmaxf(M, L.m[v][j]);
-      if (M > -INFINITY) {
-#pragma unroll
-        for (int v = 0; v < NW; ++v) comb[e] = fmaf(__builtin_amdgcn_exp2f(L.m[v][j] - M), L.o[v][j][c], comb[e]);
-      }
-    }
-  }
-  float Mj = -INFINITY, Lj = 0.0f;
-  if (tid < gq) {
-#pragma unroll
-    for (int v = 0; v < NW; ++v) Mj = fmaxf(Mj, L.m[v][tid]);
-    if (Mj > -INFINITY) {
-#pragma unroll
-      for (int v = 0; v < NW; ++v) Lj = fmaf(__builtin_amdgcn_exp2f(L.m[v][tid] - Mj), L.l[v][tid], Lj);
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int e = 0; e < kPer; ++e)
-    if (tid + e * kThreads < NJ * kHeadDim) ob[tid + e * kThreads] = comb[e];
-  __syncthreads();
-  // o'_j[c'] = sum_c o_j[c] R_V[c][c']: each part's sums are added through LDS (the space of the
-  // other waves' partials is free again)
-  float acc[NJ];
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) acc[j] = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kPerPart; ++i) {
-    const int c = part * kPerPart + i;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) acc[j] = fmaf(ob[j * kHeadDim + c], rv[i], acc[j]);
-  }
-  float* red = &L.o[kParts > 1 ? 1 : 0][0][0];  // [part][j][c'] after the combined rows of L.o[0]
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) red[(part * NJ + j) * kHeadDim + cc] = acc[j];
-  __syncthreads();
+  // combine the waves into the slice's partial: M_j = max_w m_wj, o_j = sum_w 2^(m_wj - M_j) o_wj,
+  // L_j likewise (model basis; the merges rotate it)
+  float* wp = a.wpart + (size_t)slice * a.B * a.Hq * kPartStride;  // this slice's partials
   for (int idx = tid; idx < gq * kHeadDim; idx += kThreads) {
     const int j = idx / kHeadDim, c = idx % kHeadDim;
-    float s = 0.0f;
+    float M = -INFINITY;
 #pragma unroll
-    for (int pp = 0; pp < kParts; ++pp) s += red[(pp * NJ + j) * kHeadDim + c];
-    a.wpart[((size_t)b * a.Hq + h * gq + j) * kPartStride + 4 + c] = s;
+    for (int v = 0; v < NW; ++v) M = fmaxf(M, L.m[v][j]);
+    float o = 0.0f;
+    if (M > -INFINITY) {
+#pragma unroll
+      for (int v = 0; v < NW; ++v) o = fmaf(__builtin_amdgcn_exp2f(L.m[v][j] - M), L.o[v][j][c], o);
+    }
+    wp[((size_t)b * a.Hq + h * gq + j) * kPartStride + 4 + c] = o;
   }
   if (tid < gq) {
-    float* pp = a.wpart + ((size_t)b * a.Hq + h * gq + tid) * kPartStride;
-    pp[0] = Mj;
-    pp[1] = Lj;
+    float M = -INFINITY, Ls = 0.0f;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) M = fmaxf(M, L.m[v][tid]);
+    if (M > -INFINITY) {
+#pragma unroll
+      for (int v = 0; v < NW; ++v) Ls = fmaf(__builtin_amdgcn_exp2f(L.m[v][tid] - M), L.l[v][tid], Ls);
+    }
+    float* pp = wp + ((size_t)b * a.Hq + h * gq + tid) * kPartStride;
+    pp[0] = M;
+    pp[1] = Ls;
   }
 }
 
-constexpr int kWinWaves = 8;
-static_assert(sizeof(WinLds<kWinWaves>) <= 160 * 1024, "window block LDS");
-static_assert(kWinMaxCap <= kWinWaves * kWinPass * 4, "window passes");
+constexpr int kWinWaves = 4;
+static_assert(2 * sizeof(WinLds<kWinWaves>) <= 160 * 1024, "two window blocks per CU");
+static_assert(kWinMaxCap <= kWinSlices * kWinWaves * kWinPass * 4, "window passes");
 
 template <int NJ4>
 __global__ __launch_bounds__(64 * kWinWaves) void window_attn_kernel(DecodeArgs a, WindowArgs w) {
   __shared__ __attribute__((aligned(16))) uint8_t win_lds[sizeof(WinLds<kWinWaves>)];
-  window_block<kWinWaves, NJ4>(a, w, blockIdx.x, blockIdx.y, win_lds);
+  // the KV heads of one (sequence, slice) are consecutive blocks, so the rows of a token (all heads,
+  // one contiguous 2 KiB span at 8 heads) are read at about the same time
+  window_block<kWinWaves, NJ4>(a, w, blockIdx.z, blockIdx.x, blockIdx.y, win_lds);
 }
 
 hipError_t launch_window_attn(const DecodeArgs& a, const WindowArgs& w, hipStream_t s) {
   if (a.gq > kWinMaxGq || w.cap > kWinMaxCap) return hipErrorNotSupported;
-  const dim3 grid(a.B, a.H), block(64 * kWinWaves);
+  const dim3 grid(a.H, kWinSlices, a.B), block(64 * kWinWaves);
   switch ((a.gq + 3) / 4) {
     case 1: hipLaunchKernelGGL(window_attn_kernel<1>, grid, block, 0, s, a, w); break;
     case 2: hipLaunchKernelGGL(window_attn_kernel<2>, grid, block, 0, s, a, w); break;
