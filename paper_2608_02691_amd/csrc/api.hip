@@ -119,8 +119,8 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model, int groups)
   p.off_part = off;
   const size_t part_rows = p.variant == 2 ? (size_t)(p.grid_g + B) : (size_t)B * p.n_chunks;
   off = up(off + part_rows * Hq * kPartStride * sizeof(float));
-  p.off_win = off;  // BF16-window partials, [kWinSlices][B, Hq, kPartStride]
-  off = up(off + (size_t)kWinSlices * B * Hq * kPartStride * sizeof(float));
+  p.off_win = off;  // BF16-window partials, [kWinMaxSlices][B, Hq, kPartStride]
+  off = up(off + (size_t)kWinMaxSlices * B * Hq * kPartStride * sizeof(float));
   p.off_o = off;
   if (d_model > 0) off = up(off + (size_t)B * Hq * kHeadDim * sizeof(float));
   p.off_wo = off;
@@ -349,6 +349,7 @@ int decode_impl(const int2kv_cache* cache, const uint16_t* q, int batch, int num
   a.grid_g = plan.grid_g;
   a.groups = kHeadDim / cache->group_size;
   a.wpart = win ? reinterpret_cast<float*>(ws + plan.off_win) : nullptr;
+  a.win_slices = win ? (win->cap + kWinSliceTokens - 1) / kWinSliceTokens : 0;
 
   hipError_t e = hipSuccess;
   // the cache write (int2kv_append_decode): a few tokens per sequence run as extra blocks of the

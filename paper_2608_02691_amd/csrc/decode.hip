@@ -259,13 +259,13 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeArgs a, int unrotate, 
     const float* part = a.part + ((size_t)b * a.n_chunks * a.Hq + j) * kPartStride;
     const size_t stride = (size_t)a.Hq * kPartStride;
     // the BF16-window partials (when there are some) join the chunk partials
-    float wm[kWinSlices], wl[kWinSlices], wo[kWinSlices];
+    float wm[kWinMaxSlices], wl[kWinMaxSlices], wo[kWinMaxSlices];
     float M = -INFINITY;
 #pragma unroll
-    for (int s = 0; s < kWinSlices; ++s) {
+    for (int s = 0; s < kWinMaxSlices; ++s) {
       wm[s] = -INFINITY;
       wl[s] = wo[s] = 0.0f;
-      if (a.wpart) {
+      if (a.wpart && s < a.win_slices) {
         const float* wp = a.wpart + (((size_t)s * a.B + b) * a.Hq + j) * kPartStride;
         wm[s] = wp[0];
         wl[s] = wp[1];
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeArgs a, int unrotate, 
     for (int i = 0; i < nch; ++i) M = fmaxf(M, part[i * stride]);
     float lsum = 0.0f, osum = 0.0f;  // osum: the INT2 part only (the window's o is in another basis)
 #pragma unroll
-    for (int s = 0; s < kWinSlices; ++s)
+    for (int s = 0; s < kWinMaxSlices; ++s)
       if (wm[s] != -INFINITY) lsum = fmaf(exp2f(wm[s] - M), wl[s], lsum);
     for (int i = 0; i < nch; ++i) {
       const float mi = part[i * stride];
@@ -291,7 +291,7 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeArgs a, int unrotate, 
       // o' = o_int2 + o_win R_V for a folded W_O
       float ow = 0.0f;
 #pragma unroll
-      for (int s = 0; s < kWinSlices; ++s)
+      for (int s = 0; s < kWinMaxSlices; ++s)
         if (wm[s] != -INFINITY) ow = fmaf(exp2f(wm[s] - M), wo[s], ow);
       ow = lsum > 0.0f ? ow / lsum : 0.0f;
       const float oi = val;

@@ -1095,18 +1095,19 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
   __shared__ float vs[8][kHeadDim];
   __shared__ float wsh[8][kHeadDim];  // BF16-window part of each head output (model basis)
   const int b = blockIdx.x, h = blockIdx.y, c = threadIdx.x & 127, sl = threadIdx.x >> 7, gq = a.gq;
-  // the BF16-window partials of this thread's query heads (model basis), loaded first: kWinSlices
-  // partials per head, folded into one (m, l, o) below
+  // the BF16-window partials of this thread's query heads (model basis, one per window slice), all
+  // loaded first (slices past win_slices read slice 0 and are dropped), folded in below
   constexpr int kR = 8 / kMergeSlots;
-  float wm[kR][kWinSlices], wl[kR][kWinSlices], wo[kR][kWinSlices];
+  float wm[kR][kWinMaxSlices], wl[kR][kWinMaxSlices], wo[kR][kWinMaxSlices];
   if (a.wpart) {
 #pragma unroll
     for (int r = 0; r < kR; ++r)
 #pragma unroll
-      for (int s = 0; s < kWinSlices; ++s) {
+      for (int s = 0; s < kWinMaxSlices; ++s) {
+        const int ss = s < a.win_slices ? s : 0;
         const float* pp =
-            a.wpart + (((size_t)s * a.B + b) * a.Hq + h * gq + min(sl + kMergeSlots * r, gq - 1)) * kPartStride;
-        wm[r][s] = pp[0];
+            a.wpart + (((size_t)ss * a.B + b) * a.Hq + h * gq + min(sl + kMergeSlots * r, gq - 1)) * kPartStride;
+        wm[r][s] = s < a.win_slices ? pp[0] : -INFINITY;
         wl[r][s] = pp[1];
         wo[r][s] = pp[4 + c];
       }
@@ -1167,7 +1168,7 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
     for (int t = 0; t < kMergeSlots; ++t) Mx = fmaxf(Mx, ms[t][jj]);
     if (a.wpart) {
 #pragma unroll
-      for (int s = 0; s < kWinSlices; ++s) Mx = fmaxf(Mx, wm[r][s]);
+      for (int s = 0; s < kWinMaxSlices; ++s) Mx = fmaxf(Mx, wm[r][s]);
     }
     float L = 0.0f, O = 0.0f, Ow = 0.0f;
 #pragma unroll
@@ -1179,7 +1180,7 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
     }
     if (a.wpart) {
 #pragma unroll
-      for (int s = 0; s < kWinSlices; ++s) {
+      for (int s = 0; s < kWinMaxSlices; ++s) {
         const float f = wm[r][s] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(wm[r][s] - Mx);
         L = fmaf(f, wl[r][s], L);
         Ow = fmaf(f, wo[r][s], Ow);

@@ -57,7 +57,8 @@ struct DecodeArgs {
   uint32_t* pages;   // page list of the matrix-core scan: [total pages + padding][4]
   int grid_g;      // work-groups of the matrix-core scan
   int groups;      // groups per token of the cache (4 or 1)
-  float* wpart;    // BF16-window partials [kWinSlices][B, Hq, kPartStride] folded in by the merge, or null
+  float* wpart;    // BF16-window partials [win_slices][B, Hq, kPartStride] folded in by the merge, or null
+  int win_slices;  // window slices of kWinSliceTokens tokens (ceil(win_cap / kWinSliceTokens))
 };
 
 constexpr int kPartStride = 132;  // m, l, 2 pad, O[128]
@@ -70,7 +71,8 @@ struct WindowArgs {
 };
 constexpr int kWinMaxGq = 16;
 constexpr int kWinMaxCap = 512;
-constexpr int kWinSlices = 2;  // window partials per (sequence, query head)
+constexpr int kWinSliceTokens = 128;                           // window tokens per partial
+constexpr int kWinMaxSlices = kWinMaxCap / kWinSliceTokens;    // window partials per (sequence, query head)
 hipError_t launch_window_write(const uint16_t* k, const uint16_t* v, const int32_t* rows, int n, int H, const float* mu,
                                uint16_t* win_k, uint16_t* win_v, int num_rows, hipStream_t s);
 // window partials into a.wpart (needs a.R_v)

@@ -60,34 +60,36 @@ hipError_t launch_window_write(const uint16_t* k, const uint16_t* v, const int32
   return hipGetLastError();
 }
 
-// Window attention of one slice of the window of (sequence b, KV head h): the window is cut into
-// kWinSlices slices, each a block of NW waves writing its own (m, l, o') partial (two blocks of a
-// CU then overlap one's loads with the other's arithmetic); up to kWinMaxGq query heads and
-// kWinMaxCap window tokens. Each wave takes a contiguous share of its slice (a multiple of 16
-// tokens) in passes of up to 64 tokens:
+// Window attention. The window of every sequence is cut into slices of kWinSliceTokens tokens; a
+// block covers one slice of one sequence for eight KV heads, wave w taking KV head w, so the block
+// reads the slice's rows whole (a token's eight head rows are one contiguous 2 KiB span) and every
+// wave writes the (m, l, o) partial of its (sequence, KV head, slice) with no exchange between waves.
+// Up to kWinMaxGq query heads and kWinMaxCap window tokens. A wave runs its slice in passes of
+// kWinPass tokens:
 //  * scores on the matrix cores: S[j][t] = q_j . k_t over the 128 channels, one 16 x 16 x 32 bf16
 //    product per 16 tokens and 32 channels (query rows are the A operand, 16 bytes of each key row
 //    per lane the B operand; bf16 products are exact, fp32 accumulation), in the scan's base-2 units;
-//  * online softmax over the wave's passes (row maxima and sums over the 16 lanes of a DPP row);
+//  * online softmax over the passes (row maxima and sums over the 16 lanes of a DPP row);
 //  * o_j = sum_t p_jt v_t on the vector ALU: lane l owns channels 2l, 2l + 1 (one 4-byte load per
 //    value row, so each row is read by the wave in one coalesced 256-byte access), p broadcast from
 //    LDS.
-// All of a pass's key and value loads are issued before its arithmetic. The waves' partials are then
-// combined in LDS (log-sum-exp) into the slice's (m, l, o) partial, in the model's basis: the merges
-// fold the kWinSlices partials of a (sequence, query head) into the INT2 result in the basis of the
-// output (adding o after the INT2 part's un-rotation, or rotating o by R_V when the output
-// projection is folded with R_V).
-constexpr int kWinPass = 64;  // tokens per pass of a wave (four 16-token tiles)
+// All of a pass's key and value loads are issued before its arithmetic. The partials are in the
+// model's basis: the merges fold the slices of a (sequence, query head) into the INT2 result in the
+// basis of the output (adding o after the INT2 part's un-rotation, or rotating o by R_V when the
+// output projection is folded with R_V).
+constexpr int kWinPass = 32;  // tokens per pass of a wave (two 16-token tiles)
+constexpr int kWinTiles = kWinPass / 16;
+constexpr int kWinWaves = 8;  // KV heads per block
+static_assert(kWinSliceTokens % kWinPass == 0 && kWinMaxSlices * kWinSliceTokens >= kWinMaxCap, "window slices");
 
 typedef __bf16 win_bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float win_f4_t __attribute__((ext_vector_type(4)));
 
-template <int NW>
+// LDS of a block: p[t][j] of each wave's current pass (the 16 rows of the score tile) and the rescale
+// factor of each row's running sums
 struct WinLds {
-  float p[NW][kWinPass][kWinMaxGq];     // p[t][j] of a wave's current pass
-  float alpha[NW][kWinMaxGq];           // rescale factor of the running sums of each row
-  float m[NW][kWinMaxGq], l[NW][kWinMaxGq];
-  float o[NW][kWinMaxGq][kHeadDim];     // wave partials (model basis, unnormalized)
+  float p[kWinWaves][kWinPass][kWinMaxGq];
+  float alpha[kWinWaves][kWinMaxGq];
 };
 
 __device__ __forceinline__ float win_row_max16(float x) {
@@ -103,19 +105,16 @@ __device__ __forceinline__ float win_row_sum16(float x) {
   return x + __shfl_xor(x, 1, 16);
 }
 
-// NJ4 = ceil(gq / 4): groups of four query rows the arithmetic covers (rows >= gq are zero).
-template <int NW, int NJ4>
-__device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, int h, int slice, uint8_t* lds_raw) {
-  WinLds<NW>& L = *reinterpret_cast<WinLds<NW>*>(lds_raw);
+// One wave: KV head h of sequence b, window slice `slice`. NJ4 = ceil(gq / 4): groups of four query
+// rows the arithmetic covers (rows >= gq are zero).
+template <int NJ4>
+__device__ void window_wave(const DecodeArgs& a, const WindowArgs& w, int b, int h, int slice, int wave, int l,
+                            WinLds& L) {
   constexpr int NJ = 4 * NJ4;
-  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
+  const int lo = l & 15, hi = l >> 4;
   const int gq = a.gq, H = a.H;
   const int W = min(max(w.lens[b], 0), w.cap);
-  // the slice's tokens, then this wave's share of them (multiples of 16 tokens)
-  const int half = ((W + kWinSlices - 1) / kWinSlices + 15) & ~15;
-  const int s0 = min(W, slice * half), s1 = min(W, s0 + half);
-  const int per = ((s1 - s0 + NW - 1) / NW + 15) & ~15;
-  const int t0 = min(s1, s0 + wave * per), t1 = min(s1, t0 + per);
+  const int t0 = min(W, slice * kWinSliceTokens), t1 = min(W, t0 + kWinSliceTokens);
   const size_t row_stride = (size_t)H * kHeadDim;  // elements between consecutive window rows
   const uint16_t* kbase = w.k + ((size_t)b * w.cap * H + h) * kHeadDim;
   const uint16_t* vbase = w.v + ((size_t)b * w.cap * H + h) * kHeadDim;
@@ -130,11 +129,11 @@ __device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, in
   for (int j = 0; j < NJ; ++j) oacc[j][0] = oacc[j][1] = 0.0f;
   for (int p0 = t0; p0 < t1; p0 += kWinPass) {
     const int nt = min(kWinPass, t1 - p0);
-    // every key and value load of the pass first (tokens past the share read the window's last
+    // every key and value load of the pass first (tokens past the slice read the window's last
     // row and get p = 0), then the query operand
-    win_bf16x8_t kr[4][4];
+    win_bf16x8_t kr[kWinTiles][4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < kWinTiles; ++u) {
       const int t = min(p0 + 16 * u + lo, W - 1);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
@@ -156,10 +155,10 @@ __device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, in
         qa[ks] = __builtin_bit_cast(win_bf16x8_t, make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep));
       }
     }
-    // scores of rows 4 hi + r for token 16 u + lo of the pass, base-2 units, -inf past the share
-    float sc[4][4];
+    // scores of rows 4 hi + r for token 16 u + lo of the pass, base-2 units, -inf past the slice
+    float sc[kWinTiles][4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < kWinTiles; ++u) {
       win_f4_t d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[ks], kr[u][ks], d, 0, 0, 0);
@@ -169,12 +168,15 @@ __device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, in
     }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float pm = win_row_max16(fmaxf(fmaxf(sc[0][r], sc[1][r]), fmaxf(sc[2][r], sc[3][r])));
+      float pm = sc[0][r];
+#pragma unroll
+      for (int u = 1; u < kWinTiles; ++u) pm = fmaxf(pm, sc[u][r]);
+      pm = win_row_max16(pm);
       const float mnew = fmaxf(run_m[r], pm);  // pm is finite: the pass holds a valid token
       const float al = __builtin_amdgcn_exp2f(run_m[r] - mnew);
       float rs = 0.0f;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < kWinTiles; ++u) {
         const float p = __builtin_amdgcn_exp2f(sc[u][r] - mnew);
         rs += p;
         L.p[wave][16 * u + lo][4 * hi + r] = p;
@@ -186,7 +188,7 @@ __device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, in
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // o_j = alpha_j o_j + sum_t p_jt v_t on this lane's two channels (p = 0 past the share)
+    // o_j = alpha_j o_j + sum_t p_jt v_t on this lane's two channels (p = 0 past the slice)
 #pragma unroll
     for (int j4 = 0; j4 < NJ4; ++j4) {
       const win_f4_t al = *reinterpret_cast<const win_f4_t*>(&L.alpha[wave][4 * j4]);
@@ -213,62 +215,36 @@ __device__ void window_block(const DecodeArgs& a, const WindowArgs& w, int b, in
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
-  // the wave's partial (a wave without tokens leaves m = -inf, l = 0, o = 0)
-  constexpr int kThreads = 64 * NW;
+  // the partial of (b, h, slice): an empty slice leaves m = -inf, l = 0, o = 0
+  float* wp = a.wpart + (((size_t)slice * a.B + b) * a.Hq + h * gq) * kPartStride;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    if (j < gq) *reinterpret_cast<float2*>(wp + (size_t)j * kPartStride + 4 + 2 * l) = make_float2(oacc[j][0], oacc[j][1]);
   if (lo == 0) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      L.m[wave][4 * hi + r] = run_m[r];
-      L.l[wave][4 * hi + r] = run_l[r];
+      const int j = 4 * hi + r;
+      if (j < gq) {
+        wp[(size_t)j * kPartStride] = run_m[r];
+        wp[(size_t)j * kPartStride + 1] = run_l[r];
+      }
     }
-  }
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) *reinterpret_cast<float2*>(&L.o[wave][j][2 * l]) = make_float2(oacc[j][0], oacc[j][1]);
-  __syncthreads();
-  // combine the waves into the slice's partial: M_j = max_w m_wj, o_j = sum_w 2^(m_wj - M_j) o_wj,
-  // L_j likewise (model basis; the merges rotate it)
-  float* wp = a.wpart + (size_t)slice * a.B * a.Hq * kPartStride;  // this slice's partials
-  for (int idx = tid; idx < gq * kHeadDim; idx += kThreads) {
-    const int j = idx / kHeadDim, c = idx % kHeadDim;
-    float M = -INFINITY;
-#pragma unroll
-    for (int v = 0; v < NW; ++v) M = fmaxf(M, L.m[v][j]);
-    float o = 0.0f;
-    if (M > -INFINITY) {
-#pragma unroll
-      for (int v = 0; v < NW; ++v) o = fmaf(__builtin_amdgcn_exp2f(L.m[v][j] - M), L.o[v][j][c], o);
-    }
-    wp[((size_t)b * a.Hq + h * gq + j) * kPartStride + 4 + c] = o;
-  }
-  if (tid < gq) {
-    float M = -INFINITY, Ls = 0.0f;
-#pragma unroll
-    for (int v = 0; v < NW; ++v) M = fmaxf(M, L.m[v][tid]);
-    if (M > -INFINITY) {
-#pragma unroll
-      for (int v = 0; v < NW; ++v) Ls = fmaf(__builtin_amdgcn_exp2f(L.m[v][tid] - M), L.l[v][tid], Ls);
-    }
-    float* pp = wp + ((size_t)b * a.Hq + h * gq + tid) * kPartStride;
-    pp[0] = M;
-    pp[1] = Ls;
   }
 }
 
-constexpr int kWinWaves = 4;
-static_assert(2 * sizeof(WinLds<kWinWaves>) <= 160 * 1024, "two window blocks per CU");
-static_assert(kWinMaxCap <= kWinSlices * kWinWaves * kWinPass * 4, "window passes");
-
+// Block (window slice, sequence, group of eight KV heads); four waves per SIMD (registers <= 128).
 template <int NJ4>
-__global__ __launch_bounds__(64 * kWinWaves) void window_attn_kernel(DecodeArgs a, WindowArgs w) {
-  __shared__ __attribute__((aligned(16))) uint8_t win_lds[sizeof(WinLds<kWinWaves>)];
-  // the KV heads of one (sequence, slice) are consecutive blocks, so the rows of a token (all heads,
-  // one contiguous 2 KiB span at 8 heads) are read at about the same time
-  window_block<kWinWaves, NJ4>(a, w, blockIdx.z, blockIdx.x, blockIdx.y, win_lds);
+__global__ __launch_bounds__(64 * kWinWaves) __attribute__((amdgpu_waves_per_eu(4)))
+void window_attn_kernel(DecodeArgs a, WindowArgs w) {
+  __shared__ __attribute__((aligned(16))) WinLds lds;
+  const int wave = threadIdx.x >> 6, h = blockIdx.z * kWinWaves + wave;
+  if (h >= a.H) return;
+  window_wave<NJ4>(a, w, blockIdx.y, h, blockIdx.x, wave, threadIdx.x & 63, lds);
 }
 
 hipError_t launch_window_attn(const DecodeArgs& a, const WindowArgs& w, hipStream_t s) {
   if (a.gq > kWinMaxGq || w.cap > kWinMaxCap) return hipErrorNotSupported;
-  const dim3 grid(a.H, kWinSlices, a.B), block(64 * kWinWaves);
+  const dim3 grid(a.win_slices, a.B, (a.H + kWinWaves - 1) / kWinWaves), block(64 * kWinWaves);
   switch ((a.gq + 3) / 4) {
     case 1: hipLaunchKernelGGL(window_attn_kernel<1>, grid, block, 0, s, a, w); break;
     case 2: hipLaunchKernelGGL(window_attn_kernel<2>, grid, block, 0, s, a, w); break;
