@@ -17,7 +17,9 @@ scales and zeros are reproducible bit for bit:
 * the rotated INT2 map, eq:rotated_int2_map: D_{R,c}(z) = Q_2(z R; c, G) R^T;
 * key centering, Sec. 4.1: keys enter as D_{R_K,c_K}(k - mu), values as D_{R_V,c_V}(v);
 * the INT2 attention of eq:int2_attention / eq:int2_residual_readout evaluated on
-  those effective keys and values (the main-text, inverse-rotation form).
+  those effective keys and values (the main-text, inverse-rotation form);
+* the output-error diagnostics of Sec. 3.2 (dy_K, dy_V, E_out, E_rec) and the appendix's RMS
+  output error relative to plain INT2.
 
 Q_2 is "group-wise affine INT2" (Sec. 5 implementation details, Table A). The
 paper gives no arithmetic for it; the reading used here (and by the library):
@@ -358,3 +360,71 @@ def decode_window(pool, q_bits, block_table, ctx_lens, R_k, R_v, win_k, win_v, w
     if W_o_bits is None:
         return o
     return o.reshape(B, Hq * d) @ bf16_to_f64(W_o_bits).T
+
+
+# --------------------------------------------------------------------------- output-error diagnostics
+# Sec. 3.2 traces the INT2 cache through attention and W_O: with full-precision keys and values
+# (k, v) the head output is y_j = (p_j^T V) W_{O,j}^T; with the cache's effective INT2 keys and
+# values it is y~_j = (p~_j^T V~) W_{O,j}^T, and the difference splits exactly into a key-induced
+# term (through the attention distribution) and a value-induced term:
+#     dy_K = ((p~ - p)^T V) W_{O,j}^T,   dy_V = (p~^T (V~ - V)) W_{O,j}^T,   y~ - y = dy_K + dy_V.
+# E_out = ||y~ - y||^2 (eq:output_error_objective) and E_rec = ||K - K~||_F^2 + ||V - V~||_F^2
+# (eq:raw_reconstruction_objective); the appendix reports the RMS output error of a method as a
+# percentage of plain INT2 (no rotation, no centering, no clipping): 100 sqrt(err / err_plain).
+def output_error(pool, k_list, v_list, q_bits, ctx_lens, block_table, R_k, R_v, mu, W_o_bits):
+    """Per (sequence b, query head j) output errors of the INT2 cache `pool` against the
+    full-precision keys and values it was written from (k_list[b], v_list[b]: bf16 [L_b, H, 128]).
+
+    Returns (dyK, dyV, stats): dyK, dyV fp64 [B, H_q, d_model]; stats fp64 [B, H_q, 4] =
+    (||dy_K + dy_V||^2, ||dy_K||^2, ||dy_V||^2, <dy_K, dy_V>). Sequences with no token give zeros."""
+    q = bf16_to_f64(q_bits)
+    B, Hq, d = q.shape
+    H = R_k.shape[0]
+    gq = Hq // H
+    W = bf16_to_f64(W_o_bits)
+    dm = W.shape[0]
+    dyK = np.zeros((B, Hq, dm))
+    dyV = np.zeros((B, Hq, dm))
+    for b in range(B):
+        L = int(ctx_lens[b])
+        if L == 0:
+            continue
+        K_all = bf16_to_f64(k_list[b])[:L]
+        V_all = bf16_to_f64(v_list[b])[:L]
+        for h in range(H):
+            Kc, Vt = effective_kv(pool, block_table[b], L, h, R_k, R_v)
+            Kt = Kc + mu[h].astype(np.float64)          # k~ = k^ R_K^T + mu
+            K, V = K_all[:, h], V_all[:, h]
+            for j in range(h * gq, (h + 1) * gq):
+                p = attention_probs(q[b, j][None], K)[0]
+                pt = attention_probs(q[b, j][None], Kt)[0]
+                Wj = W[:, j * HEAD_DIM:(j + 1) * HEAD_DIM]
+                dyK[b, j] = ((pt - p) @ V) @ Wj.T
+                dyV[b, j] = (pt @ (Vt - V)) @ Wj.T
+    dy = dyK + dyV
+    stats = np.stack([(dy * dy).sum(-1), (dyK * dyK).sum(-1), (dyV * dyV).sum(-1), (dyK * dyV).sum(-1)], axis=-1)
+    return dyK, dyV, stats
+
+
+def reconstruction_error(pool, k_bits, v_bits, slots, R_k, R_v, mu):
+    """Per token and KV head: (||k - k~||^2, ||v - v~||^2) of tokens stored at `slots`, with
+    k~ = k^ R_K^T + mu and v~ = v^ R_V^T read back from the pool (fp64, [n, H, 2])."""
+    k = bf16_to_f64(k_bits)
+    v = bf16_to_f64(v_bits)
+    n, H = k.shape[0], k.shape[1]
+    blocks = np.asarray(slots, dtype=np.int64) // BLOCK
+    rows = np.asarray(slots, dtype=np.int64) % BLOCK
+    out = np.zeros((n, H, 2))
+    for h in range(H):
+        for i in range(n):
+            kc, ks, kz, vc, vs, vz = read_tokens(pool, np.array([blocks[i]]), BLOCK, h)
+            kt = dequantize(kc, ks, kz)[rows[i]] @ R_k[h].astype(np.float64).T + mu[h].astype(np.float64)
+            vt = dequantize(vc, vs, vz)[rows[i]] @ R_v[h].astype(np.float64).T
+            out[i, h, 0] = ((k[i, h] - kt) ** 2).sum()
+            out[i, h, 1] = ((v[i, h] - vt) ** 2).sum()
+    return out
+
+
+def rms_percent(err, err_plain):
+    """RMS output error of a method as a percentage of plain INT2's (appendix per-head metric)."""
+    return 100.0 * np.sqrt(np.asarray(err, dtype=np.float64) / np.asarray(err_plain, dtype=np.float64))

@@ -485,3 +485,80 @@ def test_window_and_int2_tokens_share_one_softmax(G):
             assert np.array_equal(one[b, j], wv[b, j // (Hq // H), 0].astype(np.float64))
     y_ref = o.reshape(B, -1) @ O.bf16_to_f64(Wo).T
     assert np.abs(y - y_ref).max() < 1e-12
+
+
+# --------------------------------------------------------------------------- output-error diagnostics
+def _grid_rows(rng, n, H):
+    """bf16 rows whose every 32-channel group is z + code * s with s = 0.5, z = -1.5 (codes 0..3,
+    both 0 and 3 present): plain INT2 stores them without loss."""
+    c = rng.integers(0, 4, (n, H, 4, 32))
+    c[..., 0], c[..., 1] = 0, 3
+    return O.f32_to_bf16_bits((-1.5 + 0.5 * c).reshape(n, H, 128).astype(np.float32))
+
+
+def _diag_case(k, v, R_k, R_v, mu, q, W_o, L):
+    H = k.shape[1]
+    nblk = (L + 15) // 16
+    pool = O.new_pool(nblk, H)
+    table = np.arange(nblk, dtype=np.int32)[None]
+    O.quantize_append(pool, k, v, np.arange(L, dtype=np.int32), R_k, R_v, mu)
+    dyK, dyV, st = O.output_error(pool, [k], [v], q, np.array([L]), table, R_k, R_v, mu, W_o)
+    return pool, table, dyK, dyV, st
+
+
+def test_output_error_matches_int2_decode_minus_full_precision_readout():
+    """Sec. 3.2: dy_K + dy_V equals the INT2 decode's head output minus the full-precision head
+    output, each projected by its own W_{O,j} (independent paths: oracle decode vs plain softmax)."""
+    w = W.make_workload(1, batch=1, ctx=70, num_q_heads=4, num_kv_heads=2, d_model=48)
+    k, v = w.kv(0)
+    pool, table, dyK, dyV, st = _diag_case(k, v, w.R_k, w.R_v, w.mu, w.q, w.W_o, 70)
+    _, o_int2 = O.decode(pool, w.q, table, np.array([70]), w.R_k, w.R_v, w.W_o, heads_out=True)
+    q = O.bf16_to_f64(w.q)[0]
+    K, V, Wo = O.bf16_to_f64(k), O.bf16_to_f64(v), O.bf16_to_f64(w.W_o)
+    for j in range(4):
+        o_full = O.softmax_attention(q[j][None], K[:, j // 2], V[:, j // 2])[0]
+        want = (o_int2[0, j] - o_full) @ Wo[:, j * 128:(j + 1) * 128].T
+        assert np.abs(dyK[0, j] + dyV[0, j] - want).max() < 1e-10 * np.abs(want).max()
+    assert np.allclose(st[..., 0], st[..., 1] + st[..., 2] + 2 * st[..., 3], rtol=1e-12)
+    assert np.all(st[..., 1] > 0) and np.all(st[..., 2] > 0)
+
+
+def test_output_error_zero_terms_on_lossless_parts():
+    """Plain INT2 (R = I, mu = 0) of grid rows is lossless: grid keys and values give zero errors
+    and zero E_rec; grid keys alone zero the key term exactly, grid values alone the value term."""
+    rng = np.random.default_rng(3)
+    H, L, Hq, dm = 2, 40, 4, 24
+    I = np.stack([np.eye(128, dtype=np.float32)] * H)
+    mu0 = np.zeros((H, 128), np.float32)
+    q = O.f32_to_bf16_bits(rng.standard_normal((1, Hq, 128)).astype(np.float32))
+    W_o = O.f32_to_bf16_bits((rng.standard_normal((dm, Hq * 128)) * 0.1).astype(np.float32))
+    kg, vg = _grid_rows(rng, L, H), _grid_rows(rng, L, H)
+    kr = O.f32_to_bf16_bits(rng.standard_normal((L, H, 128)).astype(np.float32))
+    vr = O.f32_to_bf16_bits(rng.standard_normal((L, H, 128)).astype(np.float32))
+    pool, _, dyK, dyV, st = _diag_case(kg, vg, I, I, mu0, q, W_o, L)
+    assert not dyK.any() and not dyV.any() and not st.any()
+    assert not O.reconstruction_error(pool, kg, vg, np.arange(L), I, I, mu0).any()
+    _, _, dyK, dyV, _ = _diag_case(kg, vr, I, I, mu0, q, W_o, L)
+    assert not dyK.any() and np.abs(dyV).max() > 0
+    _, _, dyK, dyV, _ = _diag_case(kr, vg, I, I, mu0, q, W_o, L)
+    assert not dyV.any() and np.abs(dyK).max() > 0
+    assert np.all(O.rms_percent(st[..., 0] + 1.0, st[..., 0] + 1.0) == 100.0)
+
+
+def test_reconstruction_error_is_rotation_invariant():
+    """E_rec in the model's basis (k - k~ with k~ = k^ R^T + mu) equals the quantization error of the
+    rotated, centered rows, (k - mu) R - k^, because R is orthogonal (to the 2.4e-8 of its fp32
+    storage, hence the 1e-6 relative tolerance)."""
+    w = W.make_workload(1, batch=1, ctx=48, num_q_heads=2, num_kv_heads=2)
+    k, v = w.kv(0)
+    pool = O.new_pool(w.num_blocks, 2)
+    slots = w.slot_mapping(0)
+    O.quantize_append(pool, k, v, slots, w.R_k, w.R_v, w.mu)
+    got = O.reconstruction_error(pool, k, v, slots, w.R_k, w.R_v, w.mu)
+    xk = O.center_rotate(k, w.mu, w.R_k)
+    xv = O.rotate(v, w.R_v)
+    for h in range(2):
+        kc, ks, kz, vc, vs, vz = O.read_tokens(pool, w.block_table[0], 48, h)
+        ek = ((xk[:, h] - O.dequantize(kc, ks, kz)) ** 2).sum(-1)
+        ev = ((xv[:, h] - O.dequantize(vc, vs, vz)) ** 2).sum(-1)
+        assert np.allclose(got[:, h, 0], ek, rtol=1e-6) and np.allclose(got[:, h, 1], ev, rtol=1e-6)
