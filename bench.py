@@ -10,7 +10,9 @@ bf16. Inputs are seeded synthetic tensors already resident in HBM when timing st
 Timing: W untimed warm-up steps, then K steps back to back between two events (ms_per_step,
 value, gate), then a separate sample phase of --samples steps whose dominant kernel carries HIP
 events on its own dispatch; the median of those launches gives the roofline. --mode append times
-the prefill-sized cache write instead (configuration 3).
+the prefill-sized cache write instead (configuration 3); --mode outerr times the output-error
+diagnostics of Sec. 3.2 over the cache and the full-precision rows it was written from
+(configuration 1 by default when chosen), and reports their RMS output error relative to plain INT2.
 
 Prints one JSON line (rank 0). Progress goes to stderr.
 """
@@ -134,6 +136,31 @@ def cpu_baseline(w, target_s, group=32):
                       f"({tokens} KV-tokens, {elapsed:.1f} s, fp64 numpy)"}
 
 
+def cpu_baseline_outerr(w, target_s, group=32):
+    """Time the CPU oracle's output-error diagnostics on a bounded sample of the workload's sequences."""
+    from oracle import int2kv_oracle as O
+    tokens, elapsed, seqs = 0, 0.0, []
+    for b in range(w.batch):
+        L = int(w.ctx_lens[b])
+        nblk = (L + 15) // 16
+        pool = O.new_pool(nblk, w.num_kv_heads, group)
+        table = np.arange(nblk, dtype=np.int32)[None]
+        k, v = w.kv(b)
+        O.quantize_append(pool, k, v, np.arange(L, dtype=np.int32), w.R_k, w.R_v, w.mu)
+        t0 = time.perf_counter()
+        O.output_error(pool, [k], [v], w.q[b:b + 1], np.array([L], np.int32), table, w.R_k, w.R_v, w.mu, w.W_o)
+        elapsed += time.perf_counter() - t0
+        tokens += L
+        seqs.append(b)
+        log(f"cpu oracle: output error of sequence {b} ({L} tokens), {elapsed:.1f} s so far")
+        if elapsed >= target_s:
+            break
+    return {"value": tokens / elapsed, "unit": "KV-tokens/s (output-error diagnostics)", "cores": blas_threads(),
+            "kind": "oracle", "host_cpus": os.cpu_count(), "cpu_model": cpu_model(),
+            "sample": f"oracle output-error diagnostics (+W_O) of sequences {seqs[0]}..{seqs[-1]} of the same "
+                      f"workload ({tokens} KV-tokens, {elapsed:.1f} s, fp64 numpy)"}
+
+
 def cpu_baseline_append(w, target_s, group=32):
     """Time the CPU oracle's cache write (center, rotate, quantize, pack) on a bounded sample of the
     workload's sequences."""
@@ -163,10 +190,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--config", type=int, default=4)
-    ap.add_argument("--mode", choices=("decode", "append"), default="decode",
+    ap.add_argument("--config", type=int, default=None,
+                    help="workload configuration (default 4; 1 with --mode outerr)")
+    ap.add_argument("--mode", choices=("decode", "append", "outerr"), default="decode",
                     help="decode: one decode step (default); append: the cache write of every token of the "
-                         "workload in one int2kv_quantize_append call (configuration 3's prefill-sized append)")
+                         "workload in one int2kv_quantize_append call (configuration 3's prefill-sized append); "
+                         "outerr: one int2kv_output_error call (key- and value-induced output errors against the "
+                         "full-precision rows)")
     ap.add_argument("--chunk", type=int, default=0, help="context chunk in tokens (0 = automatic)")
     ap.add_argument("--variant", type=int, default=0, help="decode scan variant (0 auto, 1 VALU, 2 MFMA)")
     ap.add_argument("--wo", choices=("prepared", "folded", "plain"), default="prepared",
@@ -223,6 +253,8 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes_read": n, "bytes_written": n, "launches": 3}), flush=True)
         return
+    if args.config is None:
+        args.config = 1 if args.mode == "outerr" else 4
     K.int2kv_set_decode_tuning(args.chunk, args.variant)
     clip_k, clip_v = (float(x) for x in args.clip.split(","))
     w = W.make_workload(args.config, ctx=args.ctx or None)
@@ -248,7 +280,61 @@ def main():
         if ev_box["ev"] is not None:
             K.int2kv_set_decode_events(None, None)
 
-    if append_mode:
+    outerr_mode = args.mode == "outerr"
+    diag = None
+    if outerr_mode:
+        if d_model == 0:
+            raise SystemExit("--mode outerr needs a configuration with W_O (1 or 4)")
+        # the cache and the bf16 rows it was written from (row b * row_cap + t), plus a plain INT2
+        # cache (identity rotations, no centering) of the same tokens for the relative metric
+        row_cap = int(lens.max())
+        k_rows = torch.zeros((B * row_cap, H, 128), dtype=torch.bfloat16, device="cuda")
+        v_rows = torch.zeros_like(k_rows)
+        plain = K.Int2KVCache(w.num_blocks, H, group_size=args.group)
+        eye = torch.eye(128, dtype=torch.float32, device="cuda").expand(H, 128, 128).contiguous()
+        zero_mu = torch.zeros((H, 128), dtype=torch.float32, device="cuda")
+        for b in range(B):
+            k, v = w.kv(b, as_torch=True)
+            L = int(lens[b])
+            kd, vd = k.cuda(), v.cuda()
+            k_rows[b * row_cap:b * row_cap + L] = kd
+            v_rows[b * row_cap:b * row_cap + L] = vd
+            sl = dev(w.slot_mapping(b))
+            K.int2kv_quantize_append(cache, kd, vd, sl, Rk, Rv, mu_rk, clip_k, clip_v)
+            K.int2kv_quantize_append(plain, kd, vd, sl, eye, eye, zero_mu, 1.0, 1.0)
+        torch.cuda.synchronize()
+        log(f"prefilled {B} sequences and their bf16 rows")
+        q = dev(w.q)
+        table = dev(w.block_table)
+        Wo = dev(w.W_o)
+        ctx = dev(w.ctx_lens.astype(np.int32))
+        max_ctx = int(lens.max())
+        ws = torch.empty(K.int2kv_output_error_workspace_bytes(B, Hq, H, max_ctx, d_model), dtype=torch.uint8,
+                         device="cuda")
+        stats = torch.empty((B, Hq, 4), dtype=torch.float32, device="cuda")
+        oe_args = (q, table, ctx, max_ctx, Rk, Rv, k_rows, v_rows, row_cap, Wo)
+
+        def step():
+            with_events(lambda: K.int2kv_output_error(cache, *oe_args, workspace=ws, stats=stats))
+
+        dom_name = "output-error scan (outerr_scan_kernel)"
+        pages = int(((lens + 15) // 16).sum())
+        dom_bytes = (tok_bytes + 512) * H * int(lens.sum()) + 4 * pages
+        step_bytes = dom_bytes + 2 * d_model * Hq * 128 + R_bytes + B * Hq * 256 + B * Hq * 16
+        tokens = int(lens.sum())
+        # the per-head metric: RMS output error of the rotated cache as a percentage of plain INT2's
+        st_rot = K.int2kv_output_error(cache, *oe_args).cpu().double().numpy()
+        st_plain = K.int2kv_output_error(plain, *oe_args).cpu().double().numpy()
+        pct = 100.0 * np.sqrt(st_rot[..., 0] / st_plain[..., 0])
+        share_k = st_rot[..., 1] / st_rot[..., 0]
+        diag = {"what": "E_out of the cache per (sequence, query head) against plain INT2 of the same tokens "
+                        "(identity rotations, no centering, no clipping), from int2kv_output_error",
+                "rms_percent_of_plain_int2": {"median": float(np.median(pct)), "mean": float(pct.mean()),
+                                              "p90": float(np.percentile(pct, 90))},
+                "key_share_of_e_out_median": float(np.median(share_k)),
+                "cross_term_over_e_out_median": float(np.median(st_rot[..., 3] / st_rot[..., 0]))}
+        del plain
+    elif append_mode:
         # every token of every sequence in one call, into an empty permuted pool; repeated steps
         # rewrite the same slots
         kk, vv, ss = [], [], []
@@ -429,7 +515,8 @@ def main():
 
     dom_gbps = dom_bytes / (dom_ms * 1e-3) / 1e9
     step_gbps = step_bytes / (ms_step * 1e-3) / 1e9
-    key = (f"append_cfg{args.config}" if append_mode else f"decode_scan_cfg{args.config}")
+    key = (f"append_cfg{args.config}" if append_mode else
+           f"outerr_scan_cfg{args.config}" if outerr_mode else f"decode_scan_cfg{args.config}")
     counters = (committed_counters(key)
                 if args.group == 32 and not args.window and not args.ctx and args.clip == "1,1" else None)
     caches = ("flushed (1 GiB read) before every step and sample" if args.flush_mall
@@ -437,6 +524,8 @@ def main():
                    "back to back")
     if append_mode:
         step_calls = "int2kv_quantize_append (all tokens in one call)"
+    elif outerr_mode:
+        step_calls = "int2kv_output_error (statistics only)"
     elif args.window:
         step_calls = "int2kv_window_write + int2kv_quantize_append + int2kv_decode_window"
     elif args.separate:
@@ -446,7 +535,8 @@ def main():
     result = {
         "metric": METRIC,
         "value": tokens / (ms_step * 1e-3),
-        "unit": "appended KV-tokens/s" if append_mode else "KV-tokens/s",
+        "unit": ("appended KV-tokens/s" if append_mode else
+                 "KV-tokens/s (output-error diagnostics)" if outerr_mode else "KV-tokens/s"),
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -472,7 +562,8 @@ def main():
             "chunk_tokens": args.chunk or "auto", "variant": args.variant or "auto", "step_calls": step_calls,
             "bf16_window": (f"{args.window.split(',')[0]} sink + {args.window.split(',')[1]} recent tokens"
                             if args.window else None),
-            "w_o": None if append_mode or not d_model else {
+            "w_o": None if append_mode or not d_model else "W_O bf16 row-major (per query head slices)"
+            if outerr_mode else {
                 "prepared": "W_O R_V folded, fp16 tiles (prepared once)",
                 "folded": "W_O R_V folded, bf16 row-major (prepared once)",
                 "plain": "W_O bf16 row-major after R_V^T"}[args.wo],
@@ -492,11 +583,15 @@ def main():
         },
         "context": {"hbm_copy_gbps": copy_gbps, "copy": "1 GiB device-to-device copy, read + write bytes"},
     }
+    if diag is not None:
+        result["diagnostics"] = diag
+        result["dtype"] = "int2 codes with fp16 scale/zero and bf16 rows; fp32 vector arithmetic"
     if counters and counters.get("mfma_busy_frac") is not None:
         result["roofline"]["mfma_busy_frac"] = counters["mfma_busy_frac"]
     if not args.no_cpu_baseline and not args.window:  # the oracle timing covers the INT2-only step
-        result["cpu_baseline"] = (cpu_baseline_append(w, args.cpu_seconds, args.group) if append_mode
-                                  else cpu_baseline(w, args.cpu_seconds, args.group))
+        result["cpu_baseline"] = (cpu_baseline_append(w, args.cpu_seconds, args.group) if append_mode else
+                                  cpu_baseline_outerr(w, args.cpu_seconds, args.group) if outerr_mode else
+                                  cpu_baseline(w, args.cpu_seconds, args.group))
     print(json.dumps(result), flush=True)
 
 

@@ -155,6 +155,18 @@ int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const u
                            const float* R_v, const float* mu_rk, float clip_k, float clip_v,
                            hipStream_t stream);
 
+/* int2kv_quantize_append that also reports each token's reconstruction error, for the diagnostics of
+ * Sec. 3.2 (E_rec, eq:raw_reconstruction_objective): err[(i * H_kv + h) * 2 + 0] = ||x - x^||^2 of
+ * the key and [... + 1] of the value of token i, KV head h, where x is the library's fp32 rotated
+ * (and, for keys, centered) row and x^ its dequantized INT2 row; since R_K, R_V are orthogonal this
+ * is ||k - k~||^2 (k~ = k^ R_K^T + mu) and ||v - v~||^2 in the model's basis. err: fp32
+ * [num_tokens, H_kv, 2], written for every token (also for skipped slots). Cache bytes are those of
+ * int2kv_quantize_append. */
+int int2kv_quantize_append_error(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
+                                 const int32_t* slot_mapping, int num_tokens, const float* R_k,
+                                 const float* R_v, const float* mu_rk, float clip_k, float clip_v,
+                                 float* err, hipStream_t stream);
+
 /* Workspace bytes int2kv_decode needs for these sizes (d_model = 0 when W_O is not applied). */
 size_t int2kv_decode_workspace_bytes(int batch, int num_q_heads, int num_kv_heads, int max_ctx,
                                      int d_model);
@@ -251,10 +263,36 @@ int int2kv_decode_window(const int2kv_cache* cache, const uint16_t* q, int batch
                          const int32_t* win_lens, int win_cap, float* out, void* workspace,
                          size_t workspace_bytes, hipStream_t stream);
 
+/* Output-error diagnostics of the INT2 cache (Sec. 3.2; appendix output-space error metrics):
+ * for every sequence b and query head j, with p the attention of q_j over the full-precision keys
+ * k, p~ over the cache's effective INT2 keys k~ = k^ R_K^T + mu, V the full-precision values and V~
+ * the effective INT2 values v^ R_V^T,
+ *     dy_K = ((p~ - p)^T V) W_{O,j}^T,   dy_V = (p~^T (V~ - V)) W_{O,j}^T,
+ * so that y~_j - y_j = dy_K + dy_V exactly (the key- and value-induced output errors), and
+ *     stats[(b * H_q + j) * 4 + {0, 1, 2, 3}] = ||dy_K + dy_V||^2 (E_out), ||dy_K||^2, ||dy_V||^2,
+ *                                              <dy_K, dy_V>.
+ *   k_rows, v_rows : bf16 full-precision keys (raw, not centered) and values, row b * row_cap + t
+ *                    holding token t of sequence b for every KV head ([rows, H_kv, 128]), the
+ *                    tokens the cache holds at block_table / ctx_lens (lengths are also clamped to
+ *                    row_cap)
+ *   W_o            : bf16 [d_model, H_q * 128] row-major (required)
+ *   dy             : fp32 [B, H_q, 2, d_model] (dy_K, dy_V) or NULL
+ *   workspace      : int2kv_output_error_workspace_bytes(...) bytes, 256-byte aligned
+ * Other arguments as int2kv_decode; up to 16 query heads per KV head. Scores and sums run in fp32
+ * (INT2 scores with the rotated query, as the vector-ALU decode). */
+size_t int2kv_output_error_workspace_bytes(int batch, int num_q_heads, int num_kv_heads, int max_ctx,
+                                           int d_model);
+int int2kv_output_error(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
+                        const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens,
+                        int max_ctx, const float* R_k, const float* R_v, const uint16_t* k_rows,
+                        const uint16_t* v_rows, int row_cap, const uint16_t* W_o, int d_model,
+                        float* stats, float* dy, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+
 /* Measurement hook: when set (non-NULL), the calls this thread issues attach `before_scan` and
  * `after_scan` to the dispatch of their dominant kernel (hipExtLaunchKernel): the split-context scan
  * of int2kv_decode, int2kv_append_decode and int2kv_decode_window, the cache-write kernel of
- * int2kv_quantize_append. They then mark that kernel's own start and end, and a caller can time it
+ * int2kv_quantize_append(_error), the diagnostics scan of int2kv_output_error. They then mark that kernel's own start and end, and a caller can time it
  * alone with hipEventElapsedTime, without extra packets between the kernels. Pass NULLs to disable.
  * The setting is per calling thread. The events are owned by the caller and must outlive the calls
  * that record them. */

@@ -253,6 +253,22 @@ int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const u
   return hip_status(e, "quantize_append");
 }
 
+int int2kv_quantize_append_error(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
+                                 const int32_t* slot_mapping, int num_tokens, const float* R_k, const float* R_v,
+                                 const float* mu_rk, float clip_k, float clip_v, float* err, hipStream_t stream) {
+  if (int st = check_cache(cache)) return st;
+  if (num_tokens < 0) return fail(INT2KV_EINVAL, "num_tokens must be >= 0");
+  if (num_tokens == 0) return ok();
+  if (!k || !v || !slot_mapping || !R_k || !R_v || !mu_rk || !err) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (!valid_clip(clip_k) || !valid_clip(clip_v)) return fail(INT2KV_EINVAL, "clip ratios must be in (0, 1]");
+  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(R_k, 16) || !aligned(R_v, 16) || !aligned(mu_rk, 16))
+    return fail(INT2KV_EINVAL, "k, v, R_k, R_v and mu_rk must be 16-byte aligned");
+  if (!aligned(err, 4)) return fail(INT2KV_EINVAL, "err must be 4-byte aligned");
+  hipError_t e = launch_append_mfma(view(cache), k, v, slot_mapping, num_tokens, R_k, R_v, mu_rk, clip_k, clip_v,
+                                    stream, g_ev_before, g_ev_after, err);
+  return hip_status(e, "quantize_append_error");
+}
+
 size_t int2kv_decode_workspace_bytes(int batch, int num_q_heads, int num_kv_heads, int max_ctx, int d_model) {
   if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads || max_ctx < 0 ||
       d_model < 0)
@@ -475,6 +491,101 @@ int int2kv_window_write(const uint16_t* k, const uint16_t* v, const int32_t* row
     return fail(INT2KV_EINVAL, "k, v, mu, win_k and win_v must be 16-byte aligned");
   return hip_status(launch_window_write(k, v, rows, num_tokens, num_kv_heads, mu, win_k, win_v, num_rows, stream),
                     "window_write");
+}
+
+}  // extern "C"
+
+namespace {
+
+// Workspace of int2kv_output_error: q R_K, the chunk partials, the output differences, the partial
+// statistics of each W_O row tile; chunk as the vector-ALU decode's automatic choice.
+struct OePlan {
+  int chunk, n_chunks, ntiles;
+  size_t off_qrot, off_part, off_dov, off_spart, total;
+};
+
+OePlan make_oe_plan(int B, int Hq, int H, int max_ctx, int d_model) {
+  OePlan p{};
+  int chunk = 4096;
+  const long long units = (long long)B * H;
+  while (chunk > 512 && units * ((max_ctx + chunk - 1) / chunk) < 1024) chunk /= 2;
+  p.chunk = chunk;
+  p.n_chunks = max_ctx > 0 ? (max_ctx + chunk - 1) / chunk : 1;
+  p.ntiles = (d_model + 127) / 128;
+  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+  size_t off = 0;
+  p.off_qrot = off;
+  off = up(off + (size_t)B * Hq * kHeadDim * sizeof(float));
+  p.off_part = off;
+  off = up(off + (size_t)B * p.n_chunks * Hq * kOePartStride * sizeof(float));
+  p.off_dov = off;
+  off = up(off + (size_t)B * Hq * 2 * kHeadDim * sizeof(float));
+  p.off_spart = off;
+  off = up(off + (size_t)B * Hq * p.ntiles * 4 * sizeof(float));
+  p.total = off;
+  return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t int2kv_output_error_workspace_bytes(int batch, int num_q_heads, int num_kv_heads, int max_ctx, int d_model) {
+  if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads || max_ctx < 0 ||
+      d_model <= 0)
+    return 0;
+  return make_oe_plan(batch, num_q_heads, num_kv_heads, max_ctx, d_model).total;
+}
+
+int int2kv_output_error(const int2kv_cache* cache, const uint16_t* q, int batch, int num_q_heads,
+                        const int32_t* block_table, int max_blocks_per_seq, const int32_t* ctx_lens, int max_ctx,
+                        const float* R_k, const float* R_v, const uint16_t* k_rows, const uint16_t* v_rows,
+                        int row_cap, const uint16_t* W_o, int d_model, float* stats, float* dy, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  if (int st = check_cache(cache)) return st;
+  if (batch <= 0 || batch > 65535) return fail(INT2KV_EINVAL, "batch must be in [1, 65535]");
+  const int H = cache->num_kv_heads;
+  if (num_q_heads <= 0 || num_q_heads % H) return fail(INT2KV_EINVAL, "num_q_heads must be a multiple of num_kv_heads");
+  const int gq = num_q_heads / H;
+  if (gq > 16) return fail(INT2KV_EUNSUPPORTED, "at most 16 query heads per KV head");
+  if (max_blocks_per_seq <= 0 || max_ctx < 0 || row_cap <= 0 || d_model <= 0)
+    return fail(INT2KV_EINVAL, "bad max_blocks_per_seq / max_ctx / row_cap / d_model");
+  if (!q || !block_table || !ctx_lens || !R_k || !R_v || !k_rows || !v_rows || !W_o || !stats)
+    return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (!aligned(q, 16) || !aligned(R_k, 16) || !aligned(R_v, 16) || !aligned(k_rows, 16) || !aligned(v_rows, 16) ||
+      !aligned(W_o, 16) || !aligned(stats, 16) || (dy && !aligned(dy, 16)))
+    return fail(INT2KV_EINVAL, "q, R_k, R_v, k_rows, v_rows, W_o, stats and dy must be 16-byte aligned");
+  const OePlan plan = make_oe_plan(batch, num_q_heads, H, max_ctx, d_model);
+  if (!workspace || workspace_bytes < plan.total)
+    return fail(INT2KV_EWORKSPACE, "workspace smaller than int2kv_output_error_workspace_bytes()");
+  if (!aligned(workspace, 256)) return fail(INT2KV_EINVAL, "workspace must be 256-byte aligned");
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  OutErrArgs e{};
+  DecodeArgs& a = e.a;
+  a.pool = static_cast<const uint8_t*>(cache->pool);
+  a.num_blocks = cache->num_blocks;
+  a.H = H;
+  a.q = q;
+  a.B = batch;
+  a.Hq = num_q_heads;
+  a.gq = gq;
+  a.block_table = block_table;
+  a.max_blocks = max_blocks_per_seq;
+  a.ctx_lens = ctx_lens;
+  a.max_ctx = max_ctx;
+  a.R_k = R_k;
+  a.R_v = R_v;
+  a.qrot = reinterpret_cast<float*>(ws + plan.off_qrot);
+  a.chunk_tokens = plan.chunk;
+  a.n_chunks = plan.n_chunks;
+  a.groups = kHeadDim / cache->group_size;
+  e.k_rows = k_rows;
+  e.v_rows = v_rows;
+  e.row_cap = row_cap;
+  e.part = reinterpret_cast<float*>(ws + plan.off_part);
+  e.dov = reinterpret_cast<float*>(ws + plan.off_dov);
+  e.spart = reinterpret_cast<float*>(ws + plan.off_spart);
+  return hip_status(launch_output_error(e, W_o, d_model, stats, dy, stream, g_ev_before, g_ev_after), "output_error");
 }
 
 }  // extern "C"

@@ -155,45 +155,55 @@ hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_r
 }
 
 // Standalone append kernel: grid (blocks per (h, K|V), KV heads, K|V) of kApWaves waves.
-template <int kApTiles, int NG>
+template <int kApTiles, int NG, bool ERR = false>
 __global__ __launch_bounds__(512) void append_mfma_kernel(CacheView cv, const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v,
                                                            const int32_t* __restrict__ slots, int n,
                                                            const float* __restrict__ R_k,
                                                            const float* __restrict__ R_v,
                                                            const float* __restrict__ mu_rk, float clip_k,
-                                                           float clip_v) {
+                                                           float clip_v, float* __restrict__ err) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[kAppendLdsBytes];
-  append_block<kApTiles, kApWaves, NG>(cv, k, v, slots, n, R_k, R_v, mu_rk, clip_k, clip_v, (int)blockIdx.x,
-                                   (int)gridDim.x, (int)blockIdx.y, (int)blockIdx.z, lds);
+  append_block<kApTiles, kApWaves, NG, ERR>(cv, k, v, slots, n, R_k, R_v, mu_rk, clip_k, clip_v, (int)blockIdx.x,
+                                        (int)gridDim.x, (int)blockIdx.y, (int)blockIdx.z, lds, err);
 }
 
 hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots, int n,
                               const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
-                              float clip_v, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+                              float clip_v, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, float* err) {
   if (n <= 0) return hipSuccess;
   // one work-group per CU (its R^T terms fill most of the LDS), each converting R once for many
   // steps; short appends take one tile per wave step
   const int per_head = max(1, 256 / (2 * c.num_kv_heads));
   const int tiles = (n + 15) / 16;
   const dim3 block(64 * kApWaves);
+  // the instantiation: one or two tiles per wave step, 4 or 1 groups per token, with or without the
+  // reconstruction error
+  auto go = [&](auto tiles_tag, auto ng_tag, dim3 grid) {
+    constexpr int T = decltype(tiles_tag)::value, NG = decltype(ng_tag)::value;
+    if (err)
+      hipExtLaunchKernelGGL((append_mfma_kernel<T, NG, true>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n,
+                            R_k, R_v, mu_rk, clip_k, clip_v, err);
+    else
+      hipExtLaunchKernelGGL((append_mfma_kernel<T, NG, false>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n,
+                            R_k, R_v, mu_rk, clip_k, clip_v, err);
+  };
+  using One = std::integral_constant<int, 1>;
+  using Two = std::integral_constant<int, 2>;
+  using Four = std::integral_constant<int, 4>;
   if (tiles <= kApWaves * per_head) {
     const dim3 grid((tiles + kApWaves - 1) / kApWaves, c.num_kv_heads, 2);
     if (c.groups == 1)
-      hipExtLaunchKernelGGL((append_mfma_kernel<1, 1>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n, R_k, R_v,
-                            mu_rk, clip_k, clip_v);
+      go(One{}, One{}, grid);
     else
-      hipExtLaunchKernelGGL((append_mfma_kernel<1, 4>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n, R_k, R_v,
-                            mu_rk, clip_k, clip_v);
+      go(One{}, Four{}, grid);
   } else {
     const int steps = (tiles + 1) / 2;
     const dim3 grid(min((steps + kApWaves - 1) / kApWaves, per_head), c.num_kv_heads, 2);
     if (c.groups == 1)
-      hipExtLaunchKernelGGL((append_mfma_kernel<2, 1>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n, R_k, R_v,
-                            mu_rk, clip_k, clip_v);
+      go(Two{}, One{}, grid);
     else
-      hipExtLaunchKernelGGL((append_mfma_kernel<2, 4>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n, R_k, R_v,
-                            mu_rk, clip_k, clip_v);
+      go(Two{}, Four{}, grid);
   }
   return hipGetLastError();
 }

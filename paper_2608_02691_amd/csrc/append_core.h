@@ -69,10 +69,13 @@ __device__ __forceinline__ void int2_group_params_fast(float mn, float mx, float
 // word) and the scale / zero of group hi.
 struct ApOut {
   uint32_t w01, w23, meta;
+  float err;  // with ERR: squared reconstruction error of the token's 128 channels (every lane of it)
 };
 
 // Group quantizer of one 16-token tile held in the transposed layout above.
-template <int NG>
+// With ERR, also the token's squared reconstruction error sum_c (x_c - (code_c s + z))^2 in fp32
+// (the rotated basis, where it equals the model basis' ||k - k~||^2: R is orthogonal).
+template <int NG, bool ERR = false>
 __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float clip, const float* recip_tab, int lo,
                                                int hi) {
   if constexpr (NG == 1) {
@@ -93,6 +96,8 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
     float zf, inv;
     int2_group_params_fast(mn, mx, clip, recip_tab, s_bits, z_bits, zf, inv);
     float hf[4] = {0.f, 0.f, 0.f, 0.f};
+    float e = 0.0f;
+    const float sf = __half2float(__ushort_as_half((unsigned short)s_bits));
 #pragma unroll
     for (int p = 0; p < 8; ++p)
 #pragma unroll
@@ -101,9 +106,17 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
         const float t = (acc[p][j] - zf) * inv;
         const float c = __builtin_rintf(__builtin_amdgcn_fmed3f(t, 0.0f, 3.0f));
         hf[j] = __builtin_fmaf(c, (float)(1 << (2 * p)), hf[j]);
+        if constexpr (ERR) {
+          const float d = acc[p][j] - __builtin_fmaf(c, sf, zf);
+          e = __builtin_fmaf(d, d, e);
+        }
       }
+    if constexpr (ERR) {
+      e += __shfl_xor(e, 16);
+      e += __shfl_xor(e, 32);
+    }
     const uint32_t q0 = (uint32_t)hf[0], q1 = (uint32_t)hf[1], q2 = (uint32_t)hf[2], q3 = (uint32_t)hf[3];
-    return ApOut{q0 | (q1 << 16), q2 | (q3 << 16), s_bits | (z_bits << 16)};
+    return ApOut{q0 | (q1 << 16), q2 | (q3 << 16), s_bits | (z_bits << 16), e};
   }
   // group g = tiles 2g, 2g + 1: lane-local min/max of its eight values, then a reduce-scatter
   // over the four lanes of the token (xor 32, then xor 16) leaves group hi's extremes in lane hi
@@ -138,15 +151,18 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
   float zf, inv;
   int2_group_params_fast(mn, mx, clip, recip_tab, s_bits, z_bits, zf, inv);
   // every lane of the token gathers the four groups' zero and reciprocal scale
-  float zg[4], ig[4];
+  float zg[4], ig[4], sg[4];
+  const float sfo = __half2float(__ushort_as_half((unsigned short)s_bits));
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
     zg[g] = __shfl(zf, lo + 16 * g);
     ig[g] = __shfl(inv, lo + 16 * g);
+    if constexpr (ERR) sg[g] = __shfl(sfo, lo + 16 * g);
   }
   // codes: half 4 hi + j of the token collects tiles p = 0..7 of register j at bits 2p, summed as
   // exact small integers in fp32
   float hf[4] = {0.f, 0.f, 0.f, 0.f};
+  float e = 0.0f;
 #pragma unroll
   for (int p = 0; p < 8; ++p)
 #pragma unroll
@@ -155,9 +171,17 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
       const float t = (acc[p][j] - zg[p >> 1]) * ig[p >> 1];
       const float c = __builtin_rintf(__builtin_amdgcn_fmed3f(t, 0.0f, 3.0f));
       hf[j] = __builtin_fmaf(c, (float)(1 << (2 * p)), hf[j]);
+      if constexpr (ERR) {
+        const float d = acc[p][j] - __builtin_fmaf(c, sg[p >> 1], zg[p >> 1]);
+        e = __builtin_fmaf(d, d, e);
+      }
     }
+  if constexpr (ERR) {
+    e += __shfl_xor(e, 16);
+    e += __shfl_xor(e, 32);
+  }
   const uint32_t q0 = (uint32_t)hf[0], q1 = (uint32_t)hf[1], q2 = (uint32_t)hf[2], q3 = (uint32_t)hf[3];
-  return ApOut{q0 | (q1 << 16), q2 | (q3 << 16), s_bits | (z_bits << 16)};
+  return ApOut{q0 | (q1 << 16), q2 | (q3 << 16), s_bits | (z_bits << 16), e};
 }
 
 // Stores of one lane's ApOut into the record of its token's slot (skipped for slots out of range).
@@ -198,12 +222,13 @@ constexpr int kAppendLdsBytes = 3 * kHeadDim * kApRow * 2 + 1024 * 4;
 // One append work-group of kWaves waves: KV head h, K (kv = 0) or V (kv = 1), block bx of nbx
 // striding over the 16-token tiles; lds holds kAppendLdsBytes (16-byte aligned). Every thread of
 // the block must call it (it synchronizes once).
-template <int kApTiles, int kWaves, int NG>
+// With ERR, err[(token * H + h) * 2 + kv] receives each token's squared reconstruction error.
+template <int kApTiles, int kWaves, int NG, bool ERR = false>
 __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t* __restrict__ k,
                                              const uint16_t* __restrict__ v, const int32_t* __restrict__ slots,
                                              int n, const float* __restrict__ R_k, const float* __restrict__ R_v,
                                              const float* __restrict__ mu_rk, float clip_k, float clip_v, int bx,
-                                             int nbx, int h, int kv, uint8_t* lds) {
+                                             int nbx, int h, int kv, uint8_t* lds, float* __restrict__ err = nullptr) {
   uint16_t(*rt)[kHeadDim][kApRow] = reinterpret_cast<uint16_t(*)[kHeadDim][kApRow]>(lds);  // [term][c][i] = R[i][c]
   float* recip_tab = reinterpret_cast<float*>(lds + 3 * kHeadDim * kApRow * 2);  // RN(1 / (1 + m / 1024))
   const int H = cv.num_kv_heads, tid = threadIdx.x;
@@ -314,7 +339,7 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
     }
     ApOut out[kApTiles];
 #pragma unroll
-    for (int u = 0; u < kApTiles; ++u) out[u] = quantize_tile<NG>(acc[u], clip, recip_tab, lo, hi);
+    for (int u = 0; u < kApTiles; ++u) out[u] = quantize_tile<NG, ERR>(acc[u], clip, recip_tab, lo, hi);
     // the next step's loads are waited for here, before this step's stores: a wait placed after
     // the (lane-conditional) stores would also wait for the stores to complete
 #pragma unroll
@@ -325,6 +350,13 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
     }
 #pragma unroll
     for (int u = 0; u < kApTiles; ++u) store_tile<NG>(out[u], slot[u], cv, h, kv, nslots, hi);
+    if constexpr (ERR) {
+#pragma unroll
+      for (int u = 0; u < kApTiles; ++u) {
+        const int tok = st * kStep + 16 * u + lo;
+        if (hi == 0 && tok < n) err[((size_t)tok * H + h) * 2 + kv] = out[u].err;
+      }
+    }
 #pragma unroll
     for (int u = 0; u < kApTiles; ++u) {
       const int tok = (st + sstride) * kStep + 16 * u + lo;

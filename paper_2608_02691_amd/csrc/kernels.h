@@ -24,7 +24,8 @@ hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_r
 // ev0 / ev1 (may be null): events that track the append kernel's own start and end
 hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots,
                               int n, const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
-                              float clip_v, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+                              float clip_v, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr,
+                              float* err = nullptr);  // err: [n, H, 2] squared reconstruction errors
 
 // ---- decode (decode.hip, decode_mfma.hip, wo_gemm.hip)
 struct DecodePlan {
@@ -109,5 +110,19 @@ hipError_t launch_wo_gemm(const uint16_t* ob, const uint16_t* W, bool prepared, 
 size_t prepared_wo_elems(int N, int K);  // fp16 elements of the prepared weights (rows padded to 128)
 hipError_t launch_prepare_wo(const uint16_t* W_o, const float* R_v, uint16_t* Wp, int N, int Hq, int H,
                              hipStream_t s);
+
+// ---- output-error diagnostics (outerr.hip)
+constexpr int kOePartStride = 4 + 3 * kHeadDim;  // m1, l1, m2, l2, A1[128], A2[128], A3[128]
+struct OutErrArgs {
+  DecodeArgs a;                 // cache, queries, block table, lengths, R_K, R_V, qrot, chunking
+  const uint16_t *k_rows, *v_rows;  // full-precision keys and values, row b * row_cap + t, [H, 128]
+  int row_cap;
+  float* part;                  // [B, n_chunks, Hq, kOePartStride]
+  float* dov;                   // [B, Hq, 2, 128]: o2 - o1, o3 - o2 (model basis)
+  float* spart;                 // [B, Hq, row tiles, 4]
+};
+// stats: [B, Hq, 4]; dy (may be null): [B, Hq, 2, d_model]; ev0 / ev1 track the scan kernel
+hipError_t launch_output_error(const OutErrArgs& e, const uint16_t* W_o, int d_model, float* stats, float* dy,
+                               hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
 }  // namespace int2kv

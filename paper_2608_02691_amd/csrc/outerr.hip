@@ -1,0 +1,447 @@
+// Output-error diagnostics of the INT2 cache (Sec. 3.2; appendix output-space error metrics).
+//
+// For every sequence b and query head j, against the full-precision keys and values the cache was
+// written from:
+//   o1 = p^T V         full-precision keys and values (p = softmax of q.k / sqrt(d)),
+//   o2 = p~^T V        INT2 keys (p~ = softmax of q.k~ / sqrt(d)), full-precision values,
+//   o3 = p~^T V~       INT2 keys and values (the INT2 decode),
+// then dy_K = (o2 - o1) W_{O,j}^T and dy_V = (o3 - o2) W_{O,j}^T (so y~ - y = dy_K + dy_V), and the
+// four statistics (||dy_K + dy_V||^2, ||dy_K||^2, ||dy_V||^2, <dy_K, dy_V>).
+//
+// Kernels: a split-context scan (block = context chunk x KV head x sequence, four waves, a page of
+// 16 tokens per wave step) that runs both softmaxes over the chunk and accumulates the three value
+// sums; a merge of the chunk partials that also undoes the value rotation of o3 (o3 = o3' R_V^T);
+// the per-head projection by W_{O,j} (block = query head x 128 rows of W_O, all sequences) with
+// partial statistics per row tile; and the sum of those partials. The INT2 scores use the rotated
+// query (q R_K) . k^, the full-precision ones q . k with the raw keys: both softmaxes are invariant
+// to the key offset mu, which the effective keys k~ = k^ R_K^T + mu carry.
+#include "common.h"
+#include "kernels.h"
+
+namespace int2kv {
+
+namespace {
+
+constexpr float kOeLogit2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
+constexpr int kOeWaves = 4;
+constexpr int kOeTile = 128;                       // W_O rows per projection block
+
+__device__ __forceinline__ int oe_seq_len(const OutErrArgs& e, int b) {
+  int L = e.a.ctx_lens[b];
+  L = min(L, e.a.max_ctx);
+  L = min(L, e.a.max_blocks * kBlock);
+  L = min(L, e.row_cap);
+  return max(L, 0);
+}
+
+__device__ __forceinline__ void oe_wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+}  // namespace
+
+// Block (chunk, KV head h, sequence b). Lane roles as in the vector-ALU decode scan: for the scores,
+// token tq = l / 4 of the page and 32-channel quarter gk = l % 4; for the values, channels 2l, 2l+1.
+template <int MAXG, int NG>
+__global__ __launch_bounds__(256) void outerr_scan_kernel(OutErrArgs e) {
+  using Lay = Rec<NG>;
+  const DecodeArgs& a = e.a;
+  __shared__ float qf[MAXG][kHeadDim];       // q (model basis), base-2 logit units
+  __shared__ float qr[MAXG][kHeadDim];       // q R_K, base-2 logit units
+  __shared__ float qsum[MAXG][kGroups];      // sums of q R_K over each 32-channel quarter
+  __shared__ float pb[kOeWaves][2][MAXG][kBlock];   // p of both softmaxes for the page
+  __shared__ float wst[kOeWaves][MAXG][4];
+  __shared__ float wout[kOeWaves][3][MAXG][kHeadDim];
+
+  const int chunk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int L = oe_seq_len(e, b);
+  const int t0 = chunk * a.chunk_tokens;
+  const int gq = a.gq, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+  if (t0 >= L) {
+    // a chunk past the context: an empty partial (m = -inf) that the merge drops
+    for (int i = tid; i < gq; i += blockDim.x) {
+      float* dst = e.part + (((size_t)b * a.n_chunks + chunk) * a.Hq + h * gq + i) * kOePartStride;
+      dst[0] = -INFINITY;
+      dst[2] = -INFINITY;
+    }
+    return;
+  }
+  const int t1 = min(L, t0 + a.chunk_tokens);
+  for (int i = tid; i < gq * kHeadDim; i += blockDim.x) {
+    const int jj = i / kHeadDim, c = i % kHeadDim;
+    const size_t q = ((size_t)b * a.Hq + h * gq + jj) * kHeadDim + c;
+    qr[jj][c] = a.qrot[q] * kOeLogit2;
+    qf[jj][c] = bf16_bits_to_f32(a.q[q]) * kOeLogit2;
+  }
+  __syncthreads();
+  if (tid < gq * kGroups) {
+    const int jj = tid / kGroups, g = tid % kGroups;
+    float acc = 0.0f;
+    for (int c = 0; c < kGroup; ++c) acc += qr[jj][g * kGroup + c];
+    qsum[jj][g] = acc;
+  }
+  __syncthreads();
+
+  // running states: (m, l) of both softmaxes, and the three value sums of channels 2l, 2l+1
+  float m1[MAXG], l1[MAXG], m2[MAXG], l2[MAXG], o[3][MAXG][2];
+#pragma unroll
+  for (int j = 0; j < MAXG; ++j) {
+    m1[j] = m2[j] = -INFINITY;
+    l1[j] = l2[j] = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 3; ++r) o[r][j][0] = o[r][j][1] = 0.0f;
+  }
+  const int tq = l >> 2, gk = l & 3;
+  const int c0 = 2 * l, m0 = c0 & 15, pv = c0 >> 4, gv = c0 >> 5;
+  const size_t row_stride = (size_t)a.H * kHeadDim;
+  const uint16_t* krow0 = e.k_rows + ((size_t)b * e.row_cap * a.H + h) * kHeadDim;
+  const uint16_t* vrow0 = e.v_rows + ((size_t)b * e.row_cap * a.H + h) * kHeadDim;
+
+  const int pg0 = t0 / kBlock, pg1 = (t1 + kBlock - 1) / kBlock;
+  for (int pg = pg0 + w; pg < pg1; pg += kOeWaves) {
+    const int blk = a.block_table[(size_t)b * a.max_blocks + pg];
+    if (blk < 0 || blk >= a.num_blocks) continue;  // uniform per wave
+    const uint8_t* rec = a.pool + ((size_t)blk * a.H + h) * Lay::kBytes;
+    const int pos = pg * kBlock + tq;
+    const bool valid = pos >= t0 && pos < t1;
+    const int posc = min(max(pos, t0), t1 - 1);  // a row inside the caller's store
+
+    // ---- INT2 scores: token tq, quarter gk (codes, then the affine metadata factored out)
+    const uint4* kc = reinterpret_cast<const uint4*>(rec + kOffKCodes + 32 * tq);
+    const uint4 k0 = kc[0], k1 = kc[1];
+    const uint32_t kw[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
+    const uint32_t meta =
+        *reinterpret_cast<const uint32_t*>(rec + Lay::kOffKMeta + 4 * NG * tq + 4 * (NG == 4 ? gk : 0));
+    const float ks = f16_bits_to_f32(meta & 0xFFFF), kz = f16_bits_to_f32(meta >> 16);
+    float codes[kGroup];
+#pragma unroll
+    for (int mm = 0; mm < 16; ++mm) {
+      const uint32_t half = (kw[mm >> 1] >> (16 * (mm & 1))) & 0xFFFF;
+      codes[mm] = static_cast<float>((half >> (4 * gk)) & 3);           // channel 16 (2 gk) + mm
+      codes[16 + mm] = static_cast<float>((half >> (4 * gk + 2)) & 3);  // channel 16 (2 gk + 1) + mm
+    }
+    // ---- full-precision scores: the token's raw key row, channels 32 gk .. 32 gk + 31
+    float kf[32];
+    {
+      const uint4* kp = reinterpret_cast<const uint4*>(krow0 + (size_t)posc * row_stride + 32 * gk);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint4 x = kp[u];
+        const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          kf[8 * u + 2 * i] = __uint_as_float(xs[i] << 16);
+          kf[8 * u + 2 * i + 1] = __uint_as_float(xs[i] & 0xFFFF0000u);
+        }
+      }
+    }
+    float al1[MAXG], al2[MAXG];
+#pragma unroll
+    for (int j = 0; j < MAXG; ++j) {
+      al1[j] = al2[j] = 1.0f;
+      if (j >= gq) continue;
+      float d2 = 0.0f, d1 = 0.0f;
+#pragma unroll
+      for (int mm = 0; mm < 16; ++mm) {
+        d2 = fmaf(qr[j][32 * gk + mm], codes[mm], d2);
+        d2 = fmaf(qr[j][32 * gk + 16 + mm], codes[16 + mm], d2);
+      }
+#pragma unroll
+      for (int c = 0; c < 32; ++c) d1 = fmaf(qf[j][32 * gk + c], kf[c], d1);
+      float s2 = ks * d2 + kz * qsum[j][gk];
+      float s1 = d1;
+      s2 += __shfl_xor(s2, 1);
+      s2 += __shfl_xor(s2, 2);
+      s1 += __shfl_xor(s1, 1);
+      s1 += __shfl_xor(s1, 2);
+      s1 = valid ? s1 : -INFINITY;
+      s2 = valid ? s2 : -INFINITY;
+      float x1 = s1, x2 = s2;
+#pragma unroll
+      for (int off = 4; off < 64; off <<= 1) {
+        x1 = fmaxf(x1, __shfl_xor(x1, off));
+        x2 = fmaxf(x2, __shfl_xor(x2, off));
+      }
+      const float n1 = fmaxf(m1[j], x1), n2 = fmaxf(m2[j], x2);
+      al1[j] = n1 == -INFINITY ? 1.0f : exp2f(m1[j] - n1);
+      al2[j] = n2 == -INFINITY ? 1.0f : exp2f(m2[j] - n2);
+      const float p1 = valid ? exp2f(s1 - n1) : 0.0f, p2 = valid ? exp2f(s2 - n2) : 0.0f;
+      float ps1 = gk == 0 ? p1 : 0.0f, ps2 = gk == 0 ? p2 : 0.0f;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        ps1 += __shfl_xor(ps1, off);
+        ps2 += __shfl_xor(ps2, off);
+      }
+      l1[j] = l1[j] * al1[j] + ps1;
+      l2[j] = l2[j] * al2[j] + ps2;
+      m1[j] = n1;
+      m2[j] = n2;
+      if (gk == 0) {
+        pb[w][0][j][tq] = p1;
+        pb[w][1][j][tq] = p2;
+      }
+    }
+    oe_wave_sync();
+
+    // ---- values of channels c0, c0 + 1: INT2 (R_V basis) and full precision (model basis)
+    const uint4* vc = reinterpret_cast<const uint4*>(rec + kOffVCodes + 32 * m0);
+    const uint4 va = vc[0], vb = vc[1], vc2 = vc[2], vd = vc[3];  // halves m0 (tokens 0..15), m0 + 1
+    const uint32_t hv0[8] = {va.x, va.y, va.z, va.w, vb.x, vb.y, vb.z, vb.w};
+    const uint32_t hv1[8] = {vc2.x, vc2.y, vc2.z, vc2.w, vd.x, vd.y, vd.z, vd.w};
+    const uint4* vsp = reinterpret_cast<const uint4*>(rec + Lay::kOffVScale + 32 * (NG == 4 ? gv : 0));
+    const uint4* vzp = reinterpret_cast<const uint4*>(rec + Lay::kOffVZero + 32 * (NG == 4 ? gv : 0));
+    const uint4 s0 = vsp[0], s1 = vsp[1], z0 = vzp[0], z1 = vzp[1];
+    const uint32_t sw[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+    const uint32_t zw[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+    uint32_t vf[kBlock];
+#pragma unroll
+    for (int t = 0; t < kBlock; ++t) {
+      const int pt = min(max(pg * kBlock + t, t0), t1 - 1);
+      vf[t] = *reinterpret_cast<const uint32_t*>(vrow0 + (size_t)pt * row_stride + c0);
+    }
+#pragma unroll
+    for (int j = 0; j < MAXG; ++j) {
+#pragma unroll
+      for (int cc = 0; cc < 2; ++cc) {
+        o[0][j][cc] *= al1[j];
+        o[1][j][cc] *= al2[j];
+        o[2][j][cc] *= al2[j];
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < kBlock; ++t) {
+      const int sh = 16 * (t & 1);
+      const float vs = f16_bits_to_f32((sw[t >> 1] >> sh) & 0xFFFF);
+      const float vz = f16_bits_to_f32((zw[t >> 1] >> sh) & 0xFFFF);
+      const float x0 = fmaf(static_cast<float>((hv0[t >> 1] >> (sh + 2 * pv)) & 3), vs, vz);
+      const float x1 = fmaf(static_cast<float>((hv1[t >> 1] >> (sh + 2 * pv)) & 3), vs, vz);
+      const float r0 = __uint_as_float(vf[t] << 16), r1 = __uint_as_float(vf[t] & 0xFFFF0000u);
+#pragma unroll
+      for (int j = 0; j < MAXG; ++j) {
+        if (j < gq) {
+          const float p1 = pb[w][0][j][t], p2 = pb[w][1][j][t];
+          o[0][j][0] = fmaf(p1, r0, o[0][j][0]);
+          o[0][j][1] = fmaf(p1, r1, o[0][j][1]);
+          o[1][j][0] = fmaf(p2, r0, o[1][j][0]);
+          o[1][j][1] = fmaf(p2, r1, o[1][j][1]);
+          o[2][j][0] = fmaf(p2, x0, o[2][j][0]);
+          o[2][j][1] = fmaf(p2, x1, o[2][j][1]);
+        }
+      }
+    }
+    oe_wave_sync();
+  }
+
+  // ---- merge the four wave states into the chunk's partial
+#pragma unroll
+  for (int j = 0; j < MAXG; ++j) {
+    if (j < gq) {
+      if (l == 0) {
+        wst[w][j][0] = m1[j];
+        wst[w][j][1] = l1[j];
+        wst[w][j][2] = m2[j];
+        wst[w][j][3] = l2[j];
+      }
+#pragma unroll
+      for (int r = 0; r < 3; ++r) {
+        wout[w][r][j][c0] = o[r][j][0];
+        wout[w][r][j][c0 + 1] = o[r][j][1];
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < gq * kHeadDim; i += blockDim.x) {
+    const int j = i / kHeadDim, c = i % kHeadDim;
+    float M1 = -INFINITY, M2 = -INFINITY;
+#pragma unroll
+    for (int ww = 0; ww < kOeWaves; ++ww) {
+      M1 = fmaxf(M1, wst[ww][j][0]);
+      M2 = fmaxf(M2, wst[ww][j][2]);
+    }
+    float L1 = 0.0f, L2 = 0.0f, A[3] = {0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int ww = 0; ww < kOeWaves; ++ww) {
+      const float f1 = wst[ww][j][0] == -INFINITY ? 0.0f : exp2f(wst[ww][j][0] - M1);
+      const float f2 = wst[ww][j][2] == -INFINITY ? 0.0f : exp2f(wst[ww][j][2] - M2);
+      L1 = fmaf(f1, wst[ww][j][1], L1);
+      L2 = fmaf(f2, wst[ww][j][3], L2);
+      A[0] = fmaf(f1, wout[ww][0][j][c], A[0]);
+      A[1] = fmaf(f2, wout[ww][1][j][c], A[1]);
+      A[2] = fmaf(f2, wout[ww][2][j][c], A[2]);
+    }
+    float* dst = e.part + (((size_t)b * a.n_chunks + chunk) * a.Hq + h * gq + j) * kOePartStride;
+    if (c == 0) {
+      dst[0] = M1;
+      dst[1] = L1;
+      dst[2] = M2;
+      dst[3] = L2;
+    }
+#pragma unroll
+    for (int r = 0; r < 3; ++r) dst[4 + r * kHeadDim + c] = A[r];
+  }
+}
+
+// Block (sequence b, KV head h), thread c: the chunk partials of each query head merged into
+// o1, o2 (model basis) and o3' (R_V basis), o3 = o3' R_V^T, then do = (o2 - o1, o3 - o2).
+__global__ __launch_bounds__(128) void outerr_merge_kernel(OutErrArgs e) {
+  const DecodeArgs& a = e.a;
+  __shared__ float os[kHeadDim];
+  const int b = blockIdx.x, h = blockIdx.y, c = threadIdx.x, gq = a.gq;
+  const int L = oe_seq_len(e, b);
+  const int nch = (L + a.chunk_tokens - 1) / a.chunk_tokens;
+  const float* Rv = a.R_v + (size_t)h * kHeadDim * kHeadDim;
+  for (int jj = 0; jj < gq; ++jj) {
+    const int j = h * gq + jj;
+    const float* part = e.part + ((size_t)b * a.n_chunks * a.Hq + j) * kOePartStride;
+    const size_t stride = (size_t)a.Hq * kOePartStride;
+    float M1 = -INFINITY, M2 = -INFINITY;
+    for (int i = 0; i < nch; ++i) {
+      M1 = fmaxf(M1, part[i * stride]);
+      M2 = fmaxf(M2, part[i * stride + 2]);
+    }
+    float L1 = 0.0f, L2 = 0.0f, A0 = 0.0f, A1 = 0.0f, A2 = 0.0f;
+    for (int i = 0; i < nch; ++i) {
+      const float* p = part + i * stride;
+      const float f1 = p[0] == -INFINITY ? 0.0f : exp2f(p[0] - M1);
+      const float f2 = p[2] == -INFINITY ? 0.0f : exp2f(p[2] - M2);
+      L1 = fmaf(f1, p[1], L1);
+      L2 = fmaf(f2, p[3], L2);
+      A0 = fmaf(f1, p[4 + c], A0);
+      A1 = fmaf(f2, p[4 + kHeadDim + c], A1);
+      A2 = fmaf(f2, p[4 + 2 * kHeadDim + c], A2);
+    }
+    const float o1 = L1 > 0.0f ? A0 / L1 : 0.0f;
+    const float o2 = L2 > 0.0f ? A1 / L2 : 0.0f;
+    os[c] = L2 > 0.0f ? A2 / L2 : 0.0f;
+    __syncthreads();
+    const float4* row = reinterpret_cast<const float4*>(Rv + (size_t)c * kHeadDim);
+    float o3 = 0.0f;
+#pragma unroll 8
+    for (int i = 0; i < kHeadDim / 4; ++i) {
+      const float4 r = row[i];
+      o3 = fmaf(os[4 * i], r.x, o3);
+      o3 = fmaf(os[4 * i + 1], r.y, o3);
+      o3 = fmaf(os[4 * i + 2], r.z, o3);
+      o3 = fmaf(os[4 * i + 3], r.w, o3);
+    }
+    __syncthreads();
+    float* d = e.dov + ((size_t)b * a.Hq + j) * 2 * kHeadDim;
+    d[c] = o2 - o1;
+    d[kHeadDim + c] = o3 - o2;
+  }
+}
+
+// Block (query head j, tile of kOeTile rows of W_O), thread r = one row: dy[b][j][{K, V}][row] =
+// do[b][j][{K, V}] . W_O[row][j * 128 ..] for every sequence, and the tile's partial statistics.
+__global__ __launch_bounds__(kOeTile) void outerr_proj_kernel(OutErrArgs e, const uint16_t* __restrict__ W_o,
+                                                              int d_model, float* __restrict__ dy,
+                                                              float* __restrict__ spart, int ntiles) {
+  const DecodeArgs& a = e.a;
+  __shared__ float ds[2][kHeadDim];
+  __shared__ float red[kOeTile / 64][4];
+  const int j = blockIdx.x, tile = blockIdx.y, tid = threadIdx.x, r = tile * kOeTile + tid;
+  const bool have = r < d_model;
+  // the row's 128 weights of head j (bf16 -> fp32), read once for all sequences
+  float wr[kHeadDim];
+  {
+    const uint4* wp = reinterpret_cast<const uint4*>(W_o + (size_t)(have ? r : 0) * a.Hq * kHeadDim +
+                                                     (size_t)j * kHeadDim);
+#pragma unroll
+    for (int u = 0; u < kHeadDim / 8; ++u) {
+      const uint4 x = wp[u];
+      const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        wr[8 * u + 2 * i] = __uint_as_float(xs[i] << 16);
+        wr[8 * u + 2 * i + 1] = __uint_as_float(xs[i] & 0xFFFF0000u);
+      }
+    }
+  }
+  for (int b = 0; b < a.B; ++b) {
+    __syncthreads();
+    const float* d = e.dov + ((size_t)b * a.Hq + j) * 2 * kHeadDim;
+    ds[0][tid] = d[tid];
+    ds[1][tid] = d[kHeadDim + tid];
+    __syncthreads();
+    float yk = 0.0f, yv = 0.0f;
+#pragma unroll
+    for (int c = 0; c < kHeadDim; ++c) {
+      yk = fmaf(ds[0][c], wr[c], yk);
+      yv = fmaf(ds[1][c], wr[c], yv);
+    }
+    if (!have) yk = yv = 0.0f;
+    if (dy && have) {
+      float* o = dy + ((size_t)b * a.Hq + j) * 2 * d_model;
+      o[r] = yk;
+      o[d_model + r] = yv;
+    }
+    float st[4] = {(yk + yv) * (yk + yv), yk * yk, yv * yv, yk * yv};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) st[s] += __shfl_xor(st[s], off);
+    }
+    if ((tid & 63) == 0) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) red[tid >> 6][s] = st[s];
+    }
+    __syncthreads();
+    if (tid < 4) {
+      float v = 0.0f;
+#pragma unroll
+      for (int wv = 0; wv < kOeTile / 64; ++wv) v += red[wv][tid];
+      spart[(((size_t)b * a.Hq + j) * ntiles + tile) * 4 + tid] = v;
+    }
+  }
+}
+
+// Thread per (b, j): the four statistics summed over the row tiles in order (deterministic).
+__global__ __launch_bounds__(256) void outerr_stats_kernel(const float* __restrict__ spart, float* __restrict__ stats,
+                                                           int n, int ntiles) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int t = 0; t < ntiles; ++t)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) s[k] += spart[((size_t)i * ntiles + t) * 4 + k];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) stats[(size_t)i * 4 + k] = s[k];
+}
+
+template <int NG>
+static void launch_oe_scan(const OutErrArgs& e, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const DecodeArgs& a = e.a;
+  dim3 grid(a.n_chunks, a.H, a.B);
+  if (a.gq <= 1)
+    hipExtLaunchKernelGGL((outerr_scan_kernel<1, NG>), grid, dim3(256), 0, s, ev0, ev1, 0, e);
+  else if (a.gq <= 2)
+    hipExtLaunchKernelGGL((outerr_scan_kernel<2, NG>), grid, dim3(256), 0, s, ev0, ev1, 0, e);
+  else if (a.gq <= 4)
+    hipExtLaunchKernelGGL((outerr_scan_kernel<4, NG>), grid, dim3(256), 0, s, ev0, ev1, 0, e);
+  else if (a.gq <= 8)
+    hipExtLaunchKernelGGL((outerr_scan_kernel<8, NG>), grid, dim3(256), 0, s, ev0, ev1, 0, e);
+  else
+    hipExtLaunchKernelGGL((outerr_scan_kernel<16, NG>), grid, dim3(256), 0, s, ev0, ev1, 0, e);
+}
+
+hipError_t launch_output_error(const OutErrArgs& e, const uint16_t* W_o, int d_model, float* stats, float* dy,
+                               hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const DecodeArgs& a = e.a;
+  hipError_t err = launch_qrot(a, s);
+  if (err != hipSuccess) return err;
+  if (a.groups == 1)
+    launch_oe_scan<1>(e, s, ev0, ev1);
+  else
+    launch_oe_scan<4>(e, s, ev0, ev1);
+  hipLaunchKernelGGL(outerr_merge_kernel, dim3(a.B, a.H), dim3(128), 0, s, e);
+  const int ntiles = (d_model + kOeTile - 1) / kOeTile;
+  hipLaunchKernelGGL(outerr_proj_kernel, dim3(a.Hq, ntiles), dim3(kOeTile), 0, s, e, W_o, d_model, dy, e.spart,
+                     ntiles);
+  const int n = a.B * a.Hq;
+  hipLaunchKernelGGL(outerr_stats_kernel, dim3((n + 255) / 256), dim3(256), 0, s, e.spart, stats, n, ntiles);
+  return hipGetLastError();
+}
+
+}  // namespace int2kv

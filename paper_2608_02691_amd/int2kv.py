@@ -40,7 +40,8 @@ EXPORTED = (
     "int2kv_quantize_pack_rotated", "int2kv_quantize_append", "int2kv_decode_workspace_bytes",
     "int2kv_decode", "int2kv_append_decode", "int2kv_append_decode_noalloc", "int2kv_window_write",
     "int2kv_decode_window",
-    "int2kv_set_decode_tuning", "int2kv_set_decode_events",
+    "int2kv_set_decode_tuning", "int2kv_set_decode_events", "int2kv_quantize_append_error",
+    "int2kv_output_error_workspace_bytes", "int2kv_output_error",
 )
 
 
@@ -83,6 +84,10 @@ def load_library(path: str = LIB_PATH):
         "int2kv_decode_window": ([ctypes.POINTER(_Cache), P, I, I, P, I, P, I, P, P, P, I, I, P, P, P, I, P, P, Z,
                                   S], I),
         "int2kv_set_decode_tuning": ([I, I], I),
+        "int2kv_quantize_append_error": ([ctypes.POINTER(_Cache), P, P, P, I, P, P, P, F, F, P, S], I),
+        "int2kv_output_error_workspace_bytes": ([I, I, I, I, I], Z),
+        "int2kv_output_error": ([ctypes.POINTER(_Cache), P, I, I, P, I, P, I, P, P, P, P, I, P, I, P, P, P, Z, S],
+                                I),
         "int2kv_set_decode_events": ([P, P], I),
     }
     for name, (args, res) in sig.items():
@@ -383,3 +388,51 @@ def int2kv_decode_window(cache: Int2KVCache, q: torch.Tensor, block_table: torch
         _ptr(workspace, (torch.uint8,), "workspace"), workspace.numel(), _stream())
     _check(st, "int2kv_decode_window")
     return out
+
+
+def int2kv_quantize_append_error(cache: Int2KVCache, k: torch.Tensor, v: torch.Tensor, slot_mapping: torch.Tensor,
+                                 R_k: torch.Tensor, R_v: torch.Tensor, mu_rk: torch.Tensor, clip_k: float = 1.0,
+                                 clip_v: float = 1.0, err: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """int2kv_quantize_append plus each token's squared reconstruction error: fp32 [n, H, 2] (key, value)."""
+    n = slot_mapping.shape[0]
+    if k.numel() != n * cache.num_kv_heads * HEAD_DIM or v.numel() != k.numel():
+        raise ValueError("k / v must be [n, num_kv_heads, 128]")
+    if err is None:
+        err = torch.empty((n, cache.num_kv_heads, 2), dtype=torch.float32, device=k.device)
+    st = load_library().int2kv_quantize_append_error(
+        cache.desc, _ptr(k, _BF16, "k"), _ptr(v, _BF16, "v"), _ptr(slot_mapping, _I32, "slot_mapping"), n,
+        _ptr(R_k, _F32, "R_k"), _ptr(R_v, _F32, "R_v"), _ptr(mu_rk, _F32, "mu_rk"), clip_k, clip_v,
+        _ptr(err, _F32, "err"), _stream())
+    _check(st, "int2kv_quantize_append_error")
+    return err
+
+
+def int2kv_output_error_workspace_bytes(batch: int, num_q_heads: int, num_kv_heads: int, max_ctx: int,
+                                        d_model: int) -> int:
+    return load_library().int2kv_output_error_workspace_bytes(batch, num_q_heads, num_kv_heads, max_ctx, d_model)
+
+
+def int2kv_output_error(cache: Int2KVCache, q: torch.Tensor, block_table: torch.Tensor, ctx_lens: torch.Tensor,
+                        max_ctx: int, R_k: torch.Tensor, R_v: torch.Tensor, k_rows: torch.Tensor,
+                        v_rows: torch.Tensor, row_cap: int, W_o: torch.Tensor, want_dy: bool = False,
+                        workspace: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None):
+    """Output-error diagnostics: returns stats fp32 [B, H_q, 4] (||dy||^2, ||dy_K||^2, ||dy_V||^2,
+    <dy_K, dy_V>) and, with want_dy, dy fp32 [B, H_q, 2, d_model] (dy_K, dy_V)."""
+    B, Hq = q.shape[0], q.shape[1]
+    d_model = W_o.shape[0]
+    if stats is None:
+        stats = torch.empty((B, Hq, 4), dtype=torch.float32, device=q.device)
+    elif stats.numel() != B * Hq * 4:
+        raise ValueError("stats must hold [B, H_q, 4] floats")
+    dy = torch.empty((B, Hq, 2, d_model), dtype=torch.float32, device=q.device) if want_dy else None
+    need = int2kv_output_error_workspace_bytes(B, Hq, cache.num_kv_heads, max_ctx, d_model)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
+    st = load_library().int2kv_output_error(
+        cache.desc, _ptr(q, _BF16, "q"), B, Hq, _ptr(block_table, _I32, "block_table"), block_table.shape[1],
+        _ptr(ctx_lens, _I32, "ctx_lens"), max_ctx, _ptr(R_k, _F32, "R_k"), _ptr(R_v, _F32, "R_v"),
+        _ptr(k_rows, _BF16, "k_rows"), _ptr(v_rows, _BF16, "v_rows"), row_cap, _ptr(W_o, _BF16, "W_o"), d_model,
+        _ptr(stats, _F32, "stats"), _ptr(dy, _F32, "dy"), _ptr(workspace, (torch.uint8,), "workspace"),
+        workspace.numel(), _stream())
+    _check(st, "int2kv_output_error")
+    return (stats, dy) if want_dy else stats
