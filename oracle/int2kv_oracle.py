@@ -19,7 +19,17 @@ scales and zeros are reproducible bit for bit:
 * the INT2 attention of eq:int2_attention / eq:int2_residual_readout evaluated on
   those effective keys and values (the main-text, inverse-rotation form);
 * the output-error diagnostics of Sec. 3.2 (dy_K, dy_V, E_out, E_rec) and the appendix's RMS
-  output error relative to plain INT2.
+  output error relative to plain INT2;
+* the cache write fed with pre-RoPE keys (appendix, key-mean estimation: the mean is subtracted
+  from post-RoPE keys before rotation), and the normalized Sylvester Hadamard matrix, the QuaRot
+  base rotation (Sec. 2, Sec. 5 baselines).
+
+RoPE is the model's, not the paper's; the reading used here (and by the library): rotate-half
+pairing, channel i with channel i + 64 (i < 64), at the token's position p with a caller-given
+fp32 table cs[p] = (cos theta_{p,0..63}, sin theta_{p,0..63}):
+    y_i = x_i cos - x_{i+64} sin,   y_{i+64} = x_{i+64} cos + x_i sin,
+each evaluated in fp64 (both products exact: 8 by 24 significant bits) and rounded once to bf16
+(nearest even): the post-RoPE key is a bf16 tensor, as the serving engine hands it to the cache.
 
 Q_2 is "group-wise affine INT2" (Sec. 5 implementation details, Table A). The
 paper gives no arithmetic for it; the reading used here (and by the library):
@@ -315,6 +325,52 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
     r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
     return r.astype(np.uint16)
+
+
+def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """fp64 values to bf16 bit patterns, rounded once to nearest even (NaN and overflow not
+    expected). The value is scaled by a power of two onto its bf16 quantum (8 significant bits for
+    normal values, 2^-133 below 2^-126), rounded to an integer with np.rint (ties to even, exact in
+    fp64), and scaled back; the result is an fp32 value whose upper 16 bits are the bf16 pattern."""
+    x = np.asarray(x, dtype=np.float64)
+    _, e = np.frexp(x)                        # |x| in [2^(e-1), 2^e)
+    q = np.ldexp(1.0, np.maximum(e, -125) - 8)  # bf16 quantum at x's binade
+    r = np.rint(x / q) * q
+    u = r.astype(np.float32).view(np.uint32)
+    return (u >> 16).astype(np.uint16)
+
+
+def rope_values(k_bits: np.ndarray, positions: np.ndarray, cos_sin: np.ndarray) -> np.ndarray:
+    """RoPE of bf16 rows at their positions, fp64 and unrounded (rotate-half pairing of the
+    reading above). k_bits: [n, H, 128]; positions: int [n]; cos_sin: fp32 [max_pos, 128]."""
+    x = bf16_to_f64(k_bits)
+    cs = np.asarray(cos_sin, dtype=np.float64)[np.asarray(positions, dtype=np.int64)]  # [n, 128]
+    c, s = cs[:, None, :HEAD_DIM // 2], cs[:, None, HEAD_DIM // 2:]
+    x1, x2 = x[..., :HEAD_DIM // 2], x[..., HEAD_DIM // 2:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def rope(k_bits: np.ndarray, positions: np.ndarray, cos_sin: np.ndarray) -> np.ndarray:
+    """Post-RoPE keys as bf16 bit patterns: rope_values rounded once to bf16."""
+    return f64_to_bf16_bits(rope_values(k_bits, positions, cos_sin))
+
+
+def hadamard(n: int = HEAD_DIM) -> np.ndarray:
+    """The normalized Sylvester Hadamard matrix H_n / sqrt(n) (fp64): entry (i, j) is
+    (-1)^popcount(i & j) / sqrt(n). Orthogonal and symmetric; the QuaRot base rotation."""
+    i = np.arange(n)
+    bits = np.bitwise_and(i[:, None], i[None, :])
+    parity = np.zeros_like(bits)
+    while np.any(bits):
+        parity ^= bits & 1
+        bits >>= 1
+    return np.where(parity == 1, -1.0, 1.0) / np.sqrt(n)
+
+
+def quantize_append_rope(pool, k_bits, v_bits, slots, positions, cos_sin, R_k, R_v, mu, clip_k=1.0, clip_v=1.0):
+    """Cache write fed with pre-RoPE keys: the keys are first turned into their post-RoPE bf16
+    rows (rope above), then written as quantize_append writes them ((k - mu) R_K, v R_V)."""
+    quantize_append(pool, rope(k_bits, positions, cos_sin), v_bits, slots, R_k, R_v, mu, clip_k, clip_v)
 
 
 def window_write(win_k: np.ndarray, win_v: np.ndarray, k_bits: np.ndarray, v_bits: np.ndarray,

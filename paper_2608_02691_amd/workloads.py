@@ -56,6 +56,15 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
     return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
 
 
+def rope_cos_sin(max_pos: int, theta: float = 1.0e6, head_dim: int = HEAD_DIM) -> np.ndarray:
+    """RoPE table fp32 [max_pos, head_dim]: cos of the angles p * theta^(-2 i / head_dim) in the
+    first half, their sines in the second (i < head_dim / 2; angles formed and evaluated in fp64,
+    then rounded to fp32). theta = 1e6 is the Qwen3 base."""
+    inv = theta ** (-np.arange(0, head_dim, 2, dtype=np.float64) / head_dim)
+    ang = np.arange(max_pos, dtype=np.float64)[:, None] * inv[None, :]
+    return np.concatenate([np.cos(ang), np.sin(ang)], axis=1).astype(np.float32)
+
+
 def haar_orthogonal(rng: np.random.Generator, n: int = HEAD_DIM) -> np.ndarray:
     """Haar-distributed orthogonal matrix (fp64): QR of a Gaussian, signs of diag(R) folded into Q."""
     g = rng.standard_normal((n, n))

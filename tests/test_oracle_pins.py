@@ -562,3 +562,119 @@ def test_reconstruction_error_is_rotation_invariant():
         ek = ((xk[:, h] - O.dequantize(kc, ks, kz)) ** 2).sum(-1)
         ev = ((xv[:, h] - O.dequantize(vc, vs, vz)) ** 2).sum(-1)
         assert np.allclose(got[:, h, 0], ek, rtol=1e-6) and np.allclose(got[:, h, 1], ev, rtol=1e-6)
+
+
+# ----------------------------------------------------------------------------- RoPE, Hadamard
+def _bf16_exact(x):
+    """Reference bf16 rounding (nearest even) of fp64 values by exact rational arithmetic."""
+    from fractions import Fraction
+    import math
+    out = []
+    for v in np.asarray(x, dtype=np.float64).ravel():
+        fv = Fraction(float(v))
+        if fv == 0:
+            out.append(0x8000 if math.copysign(1.0, v) < 0 else 0)
+            continue
+        e = math.frexp(abs(float(v)))[1]
+        q = Fraction(2) ** (max(e, -125) - 8)
+        t = fv / q
+        n = math.floor(t)
+        rem = t - n
+        if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+            n += 1
+        r = float(n * q)
+        out.append(int(np.array([r], np.float32).view(np.uint32)[0] >> 16))
+    return np.array(out, np.uint16).reshape(np.shape(x))
+
+
+def test_f64_to_bf16_matches_exact_rounding():
+    """The bf16 rounding of fp64 values against exact rational rounding: random values over many
+    binades, values on bf16 rounding midpoints (ties to even both ways) and one fp64 ulp either
+    side of them, fp32-only subnormal range and signed zeros."""
+    rng = np.random.default_rng(7)
+    vals = [rng.standard_normal(2000) * np.exp2(rng.integers(-40, 40, 2000))]
+    # midpoints between consecutive bf16 values: m = (2j + 1) * 2^(e - 9) with 8-bit j
+    j = rng.integers(128, 256, 500)
+    e = rng.integers(-20, 20, 500)
+    mid = (2.0 * j + 1.0) * np.exp2(e - 9.0)
+    vals += [mid, -mid, np.nextafter(mid, np.inf), np.nextafter(mid, -np.inf)]
+    vals += [np.array([0.0, -0.0, 2.0 ** -130, 3 * 2.0 ** -134, -2.0 ** -127 * 1.00390625, 1e-40])]
+    x = np.concatenate(vals)
+    assert np.array_equal(O.f64_to_bf16_bits(x), _bf16_exact(x))
+
+
+def test_f64_to_bf16_agrees_with_fp32_rounding_on_fp32_values():
+    """On fp32-representable values the fp64 rounding is the fp32 one (the bias-and-shift rounding
+    of f32_to_bf16_bits, a different method)."""
+    rng = np.random.default_rng(8)
+    x = (rng.standard_normal(20000) * np.exp2(rng.integers(-30, 30, 20000))).astype(np.float32)
+    assert np.array_equal(O.f64_to_bf16_bits(x.astype(np.float64)), O.f32_to_bf16_bits(x))
+
+
+def test_rope_is_complex_multiplication():
+    """RoPE with rotate-half pairing is the complex product (x_i + i x_{i+64}) e^{i theta}: the
+    same fp64 values computed as numpy complex multiplication, then rounded to bf16."""
+    rng = np.random.default_rng(9)
+    n, H = 40, 3
+    k = W.f32_to_bf16_bits(rng.standard_normal((n, H, 128)).astype(np.float32) * 3)
+    cs = W.rope_cos_sin(4096)
+    pos = rng.integers(0, 4096, n)
+    x = O.bf16_to_f64(k)
+    z = x[..., :64] + 1j * x[..., 64:]
+    rot = cs[pos, :64].astype(np.float64) + 1j * cs[pos, 64:].astype(np.float64)
+    zr = z * rot[:, None, :]
+    ref = np.concatenate([zr.real, zr.imag], axis=-1)
+    assert np.array_equal(O.rope_values(k, pos, cs), ref)
+    assert np.array_equal(O.rope(k, pos, cs), O.f64_to_bf16_bits(ref))
+
+
+def test_rope_relative_position_and_norm():
+    """RoPE's defining properties with an exact-angle table: scores depend only on the position
+    difference, and every pair (i, i + 64) keeps its norm; position 0 is the identity."""
+    rng = np.random.default_rng(10)
+    q = W.f32_to_bf16_bits(rng.standard_normal((1, 1, 128)).astype(np.float32))
+    k = W.f32_to_bf16_bits(rng.standard_normal((1, 1, 128)).astype(np.float32))
+    inv = 1.0e6 ** (-np.arange(0, 128, 2) / 128.0)
+    ang = np.arange(600)[:, None] * inv[None]
+    cs = np.concatenate([np.cos(ang), np.sin(ang)], axis=1)        # fp64 table
+    s1 = (O.rope_values(q, [37], cs) * O.rope_values(k, [5], cs)).sum()
+    s2 = (O.rope_values(q, [537], cs) * O.rope_values(k, [505], cs)).sum()
+    assert abs(s1 - s2) <= 1e-12 * abs(s1)
+    y = O.rope_values(k, [333], cs)
+    x = O.bf16_to_f64(k)
+    assert np.allclose(y[..., :64] ** 2 + y[..., 64:] ** 2, x[..., :64] ** 2 + x[..., 64:] ** 2, rtol=1e-13)
+    cs32 = W.rope_cos_sin(8)
+    assert np.array_equal(O.rope(k, [0], cs32), k)
+
+
+def test_hadamard_is_sylvester_and_orthogonal():
+    """H_128 / sqrt(128): equal to scipy's Hadamard matrix (Sylvester construction) scaled,
+    orthogonal, symmetric, and equal to the fast Walsh-Hadamard transform (butterflies)."""
+    from scipy.linalg import hadamard as scipy_hadamard
+    Hm = O.hadamard(128)
+    assert np.array_equal(Hm * np.sqrt(128.0), scipy_hadamard(128).astype(np.float64))
+    assert np.abs(Hm @ Hm.T - np.eye(128)).max() <= 1e-14
+    assert np.array_equal(Hm, Hm.T)
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((5, 128))
+    y = x.copy()
+    h = 1
+    while h < 128:                                  # in-place butterflies
+        for i in range(0, 128, 2 * h):
+            a, b = y[:, i:i + h].copy(), y[:, i + h:i + 2 * h].copy()
+            y[:, i:i + h], y[:, i + h:i + 2 * h] = a + b, a - b
+        h *= 2
+    assert np.allclose(x @ Hm, y / np.sqrt(128.0), rtol=0, atol=1e-12)
+
+
+def test_quantize_append_rope_at_position_zero_is_plain_append():
+    """At position 0 (cos 1, sin 0) the RoPE cache write stores exactly the plain cache write's
+    bytes: the fused RoPE changes nothing else."""
+    w = W.make_workload(1, batch=1, ctx=40, num_q_heads=4, num_kv_heads=2)
+    k, v = w.kv(0)
+    slots = w.slot_mapping(0)
+    a = O.new_pool(w.num_blocks, 2)
+    b = O.new_pool(w.num_blocks, 2)
+    O.quantize_append(a, k, v, slots, w.R_k, w.R_v, w.mu)
+    O.quantize_append_rope(b, k, v, slots, np.zeros(len(k), np.int64), W.rope_cos_sin(4), w.R_k, w.R_v, w.mu)
+    assert np.array_equal(a, b)
