@@ -197,6 +197,11 @@ def main():
                          "workload in one int2kv_quantize_append call (configuration 3's prefill-sized append); "
                          "outerr: one int2kv_output_error call (key- and value-induced output errors against the "
                          "full-precision rows)")
+    ap.add_argument("--rope", action="store_true",
+                    help="append mode: the keys enter pre-RoPE and the write applies RoPE at each token's position "
+                         "(int2kv_quantize_append_rope, fp32 cos/sin table of theta 1e6)")
+    ap.add_argument("--hadamard", action="store_true",
+                    help="append mode: rotate keys and values by the in-kernel Hadamard matrix instead of R_K, R_V")
     ap.add_argument("--chunk", type=int, default=0, help="context chunk in tokens (0 = automatic)")
     ap.add_argument("--variant", type=int, default=0, help="decode scan variant (0 auto, 1 VALU, 2 MFMA)")
     ap.add_argument("--wo", choices=("prepared", "folded", "plain"), default="prepared",
@@ -346,12 +351,28 @@ def main():
         k_all, v_all = torch.cat(kk).cuda(), torch.cat(vv).cuda()
         slots_all = dev(np.concatenate(ss))
         n_tok = int(slots_all.numel())
+        flags = (K.INT2KV_HADAMARD_K | K.INT2KV_HADAMARD_V) if args.hadamard else 0
+        if args.hadamard:
+            Hd = K.hadamard_rotation(H)
+            mu_rk = K.int2kv_prepare_mu_rot(Hd, dev(w.mu))
+        pos_all = cs_tab = None
+        if args.rope:
+            pos_all = dev(np.concatenate([np.arange(int(lens[b]), dtype=np.int32) for b in range(B)]))
+            cs_tab = dev(W.rope_cos_sin(int(lens.max())))
 
-        def step():
-            with_events(lambda: K.int2kv_quantize_append(cache, k_all, v_all, slots_all, Rk, Rv, mu_rk, clip_k, clip_v))
+        if args.rope or args.hadamard:
+            def step():
+                with_events(lambda: K.int2kv_quantize_append_rope(
+                    cache, k_all, v_all, slots_all, pos_all, cs_tab, None if args.hadamard else Rk,
+                    None if args.hadamard else Rv, mu_rk, clip_k, clip_v, flags=flags))
+        else:
+            def step():
+                with_events(lambda: K.int2kv_quantize_append(cache, k_all, v_all, slots_all, Rk, Rv, mu_rk, clip_k,
+                                                             clip_v))
 
         dom_name = "cache write (append_mfma_kernel)"
-        dom_bytes = n_tok * H * (512 + tok_bytes) + 4 * n_tok + R_bytes + H * 128 * 4
+        dom_bytes = (n_tok * H * (512 + tok_bytes) + 4 * n_tok + (0 if args.hadamard else R_bytes) + H * 128 * 4
+                     + (4 * n_tok + int(lens.max()) * 512 if args.rope else 0))
         step_bytes = dom_bytes
         tokens = n_tok
         max_ctx = 0
@@ -518,11 +539,15 @@ def main():
     key = (f"append_cfg{args.config}" if append_mode else
            f"outerr_scan_cfg{args.config}" if outerr_mode else f"decode_scan_cfg{args.config}")
     counters = (committed_counters(key)
-                if args.group == 32 and not args.window and not args.ctx and args.clip == "1,1" else None)
+                if args.group == 32 and not args.window and not args.ctx and args.clip == "1,1"
+                and not args.rope and not args.hadamard else None)
     caches = ("flushed (1 GiB read) before every step and sample" if args.flush_mall
               else f"warm, after {args.warmup + args.steps + (args.steady_steps if steady_ms else 0)} steps "
                    "back to back")
-    if append_mode:
+    if append_mode and (args.rope or args.hadamard):
+        step_calls = ("int2kv_quantize_append_rope (all tokens in one call" + (", RoPE at positions 0..L-1" if args.rope
+                      else "") + (", in-kernel Hadamard rotation" if args.hadamard else "") + ")")
+    elif append_mode:
         step_calls = "int2kv_quantize_append (all tokens in one call)"
     elif outerr_mode:
         step_calls = "int2kv_output_error (statistics only)"
@@ -588,7 +613,8 @@ def main():
         result["dtype"] = "int2 codes with fp16 scale/zero and bf16 rows; fp32 vector arithmetic"
     if counters and counters.get("mfma_busy_frac") is not None:
         result["roofline"]["mfma_busy_frac"] = counters["mfma_busy_frac"]
-    if not args.no_cpu_baseline and not args.window:  # the oracle timing covers the INT2-only step
+    # the oracle timing covers the INT2-only step with dense rotations and post-RoPE keys
+    if not args.no_cpu_baseline and not args.window and not args.rope and not args.hadamard:
         result["cpu_baseline"] = (cpu_baseline_append(w, args.cpu_seconds, args.group) if append_mode else
                                   cpu_baseline_outerr(w, args.cpu_seconds, args.group) if outerr_mode else
                                   cpu_baseline(w, args.cpu_seconds, args.group))

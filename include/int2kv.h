@@ -155,6 +155,35 @@ int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const u
                            const float* R_v, const float* mu_rk, float clip_k, float clip_v,
                            hipStream_t stream);
 
+/* Flags of int2kv_quantize_append_rope: rotate keys (values) by the normalized Sylvester Hadamard
+ * matrix H_128 / sqrt(128), entry (i, c) = (-1)^popcount(i & c) / sqrt(128), instead of R_K (R_V),
+ * the QuaRot base rotation (Sec. 2; Sec. 5 baselines). The library applies it without reading a
+ * matrix: the +-1 entries are exact matrix-core operands (one pass instead of the three of a dense
+ * fp32 R) and the fp32 sum is scaled by RN(1 / sqrt(128)). Readers (decode, fold, mu_rot) take the
+ * dense fp32 matrix with entries +-RN(1 / sqrt(128)), which is the same rotation. */
+#define INT2KV_HADAMARD_K 1
+#define INT2KV_HADAMARD_V 2
+
+/* Cache write fed with pre-RoPE keys (appendix, key-mean estimation and application: the mean is
+ * subtracted from the post-RoPE key, then rotated and quantized), fused in one kernel:
+ *     k_rope = bf16(RoPE(k, positions[i])),  stored: Q2((k_rope - mu) R_K) and Q2(v R_V),
+ * RoPE with rotate-half pairs (i, i + 64), i < 64, from the caller's table:
+ *     y_i = x_i cos_i - x_{i+64} sin_i,   y_{i+64} = x_{i+64} cos_i + x_i sin_i,
+ * each evaluated exactly in fp64 (bf16 x fp32 products) and rounded once to bf16, nearest even.
+ *   positions   : int32 [num_tokens], the tokens' positions; NULL = keys are already post-RoPE (the
+ *                 write then equals int2kv_quantize_append, or its Hadamard form with flags)
+ *   cos_sin     : fp32 [max_pos, 128], row p = (cos theta_{p,0..63}, sin theta_{p,0..63})
+ *   flags       : INT2KV_HADAMARD_K / INT2KV_HADAMARD_V (the matching R may then be NULL)
+ *   k_rope_out  : optional bf16 [num_tokens, H_kv, 128]: the post-RoPE keys (for the BF16 window)
+ * A token whose position lies outside [0, max_pos) is skipped: no cache write and no k_rope_out row.
+ * Other arguments as int2kv_quantize_append (mu_rk = mu R_K, with the dense Hadamard under
+ * INT2KV_HADAMARD_K). */
+int int2kv_quantize_append_rope(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
+                                const int32_t* slot_mapping, const int32_t* positions, int num_tokens,
+                                const float* cos_sin, int max_pos, const float* R_k, const float* R_v,
+                                const float* mu_rk, float clip_k, float clip_v, int flags, uint16_t* k_rope_out,
+                                hipStream_t stream);
+
 /* int2kv_quantize_append that also reports each token's reconstruction error, for the diagnostics of
  * Sec. 3.2 (E_rec, eq:raw_reconstruction_objective): err[(i * H_kv + h) * 2 + 0] = ||x - x^||^2 of
  * the key and [... + 1] of the value of token i, KV head h, where x is the library's fp32 rotated

@@ -253,6 +253,36 @@ int int2kv_quantize_append(const int2kv_cache* cache, const uint16_t* k, const u
   return hip_status(e, "quantize_append");
 }
 
+int int2kv_quantize_append_rope(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
+                                const int32_t* slot_mapping, const int32_t* positions, int num_tokens,
+                                const float* cos_sin, int max_pos, const float* R_k, const float* R_v,
+                                const float* mu_rk, float clip_k, float clip_v, int flags, uint16_t* k_rope_out,
+                                hipStream_t stream) {
+  if (int st = check_cache(cache)) return st;
+  if (num_tokens < 0) return fail(INT2KV_EINVAL, "num_tokens must be >= 0");
+  if (flags & ~(INT2KV_HADAMARD_K | INT2KV_HADAMARD_V)) return fail(INT2KV_EINVAL, "unknown flags");
+  if (num_tokens == 0) return ok();
+  const bool had_k = flags & INT2KV_HADAMARD_K, had_v = flags & INT2KV_HADAMARD_V;
+  if (!k || !v || !slot_mapping || !mu_rk || (!had_k && !R_k) || (!had_v && !R_v))
+    return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (positions && (!cos_sin || max_pos <= 0)) return fail(INT2KV_EINVAL, "RoPE needs cos_sin and max_pos > 0");
+  if (k_rope_out && !positions) return fail(INT2KV_EINVAL, "k_rope_out needs positions");
+  if (!valid_clip(clip_k) || !valid_clip(clip_v)) return fail(INT2KV_EINVAL, "clip ratios must be in (0, 1]");
+  if (!aligned(k, 16) || !aligned(v, 16) || (!had_k && !aligned(R_k, 16)) || (!had_v && !aligned(R_v, 16)) ||
+      !aligned(mu_rk, 16) || (cos_sin && !aligned(cos_sin, 16)) || (k_rope_out && !aligned(k_rope_out, 16)))
+    return fail(INT2KV_EINVAL, "k, v, R_k, R_v, mu_rk, cos_sin and k_rope_out must be 16-byte aligned");
+  AppendOptions o;
+  o.positions = positions;
+  o.cos_sin = positions ? cos_sin : nullptr;
+  o.max_pos = positions ? max_pos : 0;
+  o.k_rope_out = k_rope_out;
+  o.hadamard = (had_k ? 1 : 0) | (had_v ? 2 : 0);
+  hipError_t e = launch_append_mfma(view(cache), k, v, slot_mapping, num_tokens, had_k ? nullptr : R_k,
+                                    had_v ? nullptr : R_v, mu_rk, clip_k, clip_v, stream, g_ev_before, g_ev_after,
+                                    nullptr, &o);
+  return hip_status(e, "quantize_append_rope");
+}
+
 int int2kv_quantize_append_error(const int2kv_cache* cache, const uint16_t* k, const uint16_t* v,
                                  const int32_t* slot_mapping, int num_tokens, const float* R_k, const float* R_v,
                                  const float* mu_rk, float clip_k, float clip_v, float* err, hipStream_t stream) {

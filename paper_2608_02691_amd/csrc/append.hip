@@ -155,22 +155,32 @@ hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_r
 }
 
 // Standalone append kernel: grid (blocks per (h, K|V), KV heads, K|V) of kApWaves waves.
-template <int kApTiles, int NG, bool ERR = false>
+template <int kApTiles, int NG, bool ERR = false, bool ROPE = false>
 __global__ __launch_bounds__(512) void append_mfma_kernel(CacheView cv, const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v,
                                                            const int32_t* __restrict__ slots, int n,
                                                            const float* __restrict__ R_k,
                                                            const float* __restrict__ R_v,
                                                            const float* __restrict__ mu_rk, float clip_k,
-                                                           float clip_v, float* __restrict__ err) {
+                                                           float clip_v, float* __restrict__ err, ApOpts opt) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[kAppendLdsBytes];
-  append_block<kApTiles, kApWaves, NG, ERR>(cv, k, v, slots, n, R_k, R_v, mu_rk, clip_k, clip_v, (int)blockIdx.x,
-                                        (int)gridDim.x, (int)blockIdx.y, (int)blockIdx.z, lds, err);
+  append_block<kApTiles, kApWaves, NG, ERR, ROPE>(cv, k, v, slots, n, R_k, R_v, mu_rk, clip_k, clip_v,
+                                                  (int)blockIdx.x, (int)gridDim.x, (int)blockIdx.y, (int)blockIdx.z,
+                                                  lds, err, opt);
 }
 
 hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots, int n,
                               const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
-                              float clip_v, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, float* err) {
+                              float clip_v, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1, float* err,
+                              const AppendOptions* o) {
+  ApOpts opt{};
+  if (o) {
+    opt.pos = o->positions;
+    opt.cos_sin = o->cos_sin;
+    opt.max_pos = o->max_pos;
+    opt.k_out = o->k_rope_out;
+    opt.had = o->hadamard;
+  }
   if (n <= 0) return hipSuccess;
   // one work-group per CU (its R^T terms fill most of the LDS), each converting R once for many
   // steps; short appends take one tile per wave step
@@ -181,12 +191,15 @@ hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v,
   // reconstruction error
   auto go = [&](auto tiles_tag, auto ng_tag, dim3 grid) {
     constexpr int T = decltype(tiles_tag)::value, NG = decltype(ng_tag)::value;
-    if (err)
+    if (opt.pos)
+      hipExtLaunchKernelGGL((append_mfma_kernel<T, NG, false, true>), grid, block, 0, s, ev0, ev1, 0, c, k, v,
+                            slots, n, R_k, R_v, mu_rk, clip_k, clip_v, err, opt);
+    else if (err)
       hipExtLaunchKernelGGL((append_mfma_kernel<T, NG, true>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n,
-                            R_k, R_v, mu_rk, clip_k, clip_v, err);
+                            R_k, R_v, mu_rk, clip_k, clip_v, err, opt);
     else
       hipExtLaunchKernelGGL((append_mfma_kernel<T, NG, false>), grid, block, 0, s, ev0, ev1, 0, c, k, v, slots, n,
-                            R_k, R_v, mu_rk, clip_k, clip_v, err);
+                            R_k, R_v, mu_rk, clip_k, clip_v, err, opt);
   };
   using One = std::integral_constant<int, 1>;
   using Two = std::integral_constant<int, 2>;

@@ -1,5 +1,7 @@
 // Append on the matrix cores (shared by the append kernel and the decode's preparation kernel).
 #pragma once
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -213,6 +215,77 @@ __device__ __forceinline__ void store_tile(const ApOut& o, int slot, const Cache
   }
 }
 
+// Optional stages of the cache write. RoPE (with ROPE): the keys arrive pre-RoPE and each token is
+// turned at its position into its post-RoPE bf16 row first (rotate-half pairs (i, i + 64); each
+// output evaluated in fp64, where both products are exact, and rounded once to bf16), optionally
+// stored to k_out. Hadamard (bit 0 of had for keys, bit 1 for values): the rotation is
+// H_128 / sqrt(128) instead of R; its +-1 entries are exact bf16 operands, so one matrix-core pass
+// replaces the three-term split, and the fp32 sum is scaled by RN(2^-3.5) afterwards.
+struct ApOpts {
+  const int32_t* pos = nullptr;    // token positions (ROPE)
+  const float* cos_sin = nullptr;  // fp32 [max_pos, 128]: cos of the 64 angles, then their sines
+  int max_pos = 0;
+  uint16_t* k_out = nullptr;       // post-RoPE keys, bf16 [n, H, 128], or null
+  int had = 0;
+};
+
+constexpr float kHadScale = 0x1.6a09e6p-4f;  // RN(1 / sqrt(128))
+
+// fp64 to bf16, nearest even, in two steps that cannot double-round: to fp32 by rounding to odd
+// (round toward zero, then set the last bit when inexact; Boldo and Melquiond's rounding to odd),
+// then to bf16 by nearest even, which is exact rounding because fp32 keeps 16 more bits.
+__device__ __forceinline__ uint32_t f64_to_bf16_rne(double d) {
+  float r = (float)d;
+  if ((double)r != d) {
+    uint32_t b = __float_as_uint(r);
+    if (fabs((double)r) > fabs(d)) b -= 1u;  // rounded away from zero: one ulp back toward it
+    r = __uint_as_float(b | 1u);
+  }
+  return f32_to_bf16_rne(r);
+}
+
+// RoPE of one lane's slice of a token row in place: X[ks] holds channels 32 ks + 8 hi + e
+// (e = 0..7), so pairs (i, i + 64) are (X[ks][e], X[ks + 2][e]) for ks = 0, 1; cs points at the
+// token's table row.
+__device__ __forceinline__ void rope_lane(ap_bf16x8_t (&X)[4], const float* __restrict__ cs, int hi) {
+#pragma clang fp contract(off)
+  float c[2][8], sn[2][8];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const float4* cp = reinterpret_cast<const float4*>(cs + 32 * ks + 8 * hi);
+    const float4* sp = reinterpret_cast<const float4*>(cs + 64 + 32 * ks + 8 * hi);
+    const float4 c0 = cp[0], c1 = cp[1], s0 = sp[0], s1 = sp[1];
+    c[ks][0] = c0.x; c[ks][1] = c0.y; c[ks][2] = c0.z; c[ks][3] = c0.w;
+    c[ks][4] = c1.x; c[ks][5] = c1.y; c[ks][6] = c1.z; c[ks][7] = c1.w;
+    sn[ks][0] = s0.x; sn[ks][1] = s0.y; sn[ks][2] = s0.z; sn[ks][3] = s0.w;
+    sn[ks][4] = s1.x; sn[ks][5] = s1.y; sn[ks][6] = s1.z; sn[ks][7] = s1.w;
+  }
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    uint4 a = __builtin_bit_cast(uint4, X[ks]), b = __builtin_bit_cast(uint4, X[ks + 2]);
+    uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t oa = 0u, ob = 0u;
+#pragma unroll
+      for (int hlf = 0; hlf < 2; ++hlf) {
+        const int e = 2 * q + hlf;
+        const double x1 = (double)__uint_as_float((aw[q] >> (16 * hlf)) << 16);
+        const double x2 = (double)__uint_as_float((bw[q] >> (16 * hlf)) << 16);
+        const double cc = (double)c[ks][e], ss = (double)sn[ks][e];
+        const double y1 = x1 * cc - x2 * ss;  // exact products, one rounding
+        const double y2 = x2 * cc + x1 * ss;
+        oa |= f64_to_bf16_rne(y1) << (16 * hlf);
+        ob |= f64_to_bf16_rne(y2) << (16 * hlf);
+      }
+      aw[q] = oa;
+      bw[q] = ob;
+    }
+    X[ks] = __builtin_bit_cast(ap_bf16x8_t, make_uint4(aw[0], aw[1], aw[2], aw[3]));
+    X[ks + 2] = __builtin_bit_cast(ap_bf16x8_t, make_uint4(bw[0], bw[1], bw[2], bw[3]));
+  }
+}
+
 // Each wave takes kApTiles consecutive 16-token tiles per step, so every R^T fragment read from
 // LDS feeds kApTiles products (two for long appends; one for short ones, which spreads the few
 // tiles over more waves).
@@ -223,23 +296,27 @@ constexpr int kAppendLdsBytes = 3 * kHeadDim * kApRow * 2 + 1024 * 4;
 // striding over the 16-token tiles; lds holds kAppendLdsBytes (16-byte aligned). Every thread of
 // the block must call it (it synchronizes once).
 // With ERR, err[(token * H + h) * 2 + kv] receives each token's squared reconstruction error.
-template <int kApTiles, int kWaves, int NG, bool ERR = false>
+// With ROPE, opt carries the positions and table (keys only); opt.had selects the Hadamard rotation.
+template <int kApTiles, int kWaves, int NG, bool ERR = false, bool ROPE = false>
 __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t* __restrict__ k,
                                              const uint16_t* __restrict__ v, const int32_t* __restrict__ slots,
                                              int n, const float* __restrict__ R_k, const float* __restrict__ R_v,
                                              const float* __restrict__ mu_rk, float clip_k, float clip_v, int bx,
-                                             int nbx, int h, int kv, uint8_t* lds, float* __restrict__ err = nullptr) {
+                                             int nbx, int h, int kv, uint8_t* lds, float* __restrict__ err = nullptr,
+                                             const ApOpts& opt = ApOpts{}) {
   uint16_t(*rt)[kHeadDim][kApRow] = reinterpret_cast<uint16_t(*)[kHeadDim][kApRow]>(lds);  // [term][c][i] = R[i][c]
   float* recip_tab = reinterpret_cast<float*>(lds + 3 * kHeadDim * kApRow * 2);  // RN(1 / (1 + m / 1024))
   const int H = cv.num_kv_heads, tid = threadIdx.x;
-  const float* R = (kv == 0 ? R_k : R_v) + (size_t)h * kHeadDim * kHeadDim;
+  const bool had = ((opt.had >> kv) & 1) != 0;
+  const float* R = had ? nullptr : (kv == 0 ? R_k : R_v) + (size_t)h * kHeadDim * kHeadDim;
+  const bool rope = ROPE && kv == 0;
   const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
   const uint16_t* X = kv == 0 ? k : v;
   constexpr int kStep = 16 * kApTiles;  // tokens per wave step
   // the first step's operands and slots are fetched before R, so their latency overlaps R's
   const int step0 = bx * kWaves + w;
   ap_bf16x8_t X8[kApTiles][4];
-  int slot[kApTiles];
+  int slot[kApTiles], pos[kApTiles];
 #pragma unroll
   for (int u = 0; u < kApTiles; ++u) {
     const int tok = step0 * kStep + 16 * u + lo, tc = min(tok, n - 1);
@@ -248,8 +325,22 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
     for (int ks = 0; ks < 4; ++ks) X8[u][ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
     slot[u] = slots[tc];
     if (tok >= n) slot[u] = -1;
+    pos[u] = rope ? opt.pos[tc] : 0;
   }
-  {
+  if (had) {
+    // H^T = H: thread (c, i0) writes entries (i0 .. i0 + 7, c) = (-1)^popcount(i & c) as bf16 +-1
+    constexpr int kIb = kWaves / 2;
+    const int c = tid & 127, ib = tid >> 7;
+#pragma unroll
+    for (int u = 0; u < 16 / kIb; ++u) {
+      const int i0 = 8 * (ib + kIb * u);
+      uint32_t t16[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) t16[q] = (__builtin_popcount((i0 + q) & c) & 1) ? 0xBF80u : 0x3F80u;
+      *reinterpret_cast<uint4*>(&rt[0][c][i0]) =
+          make_uint4(t16[0] | (t16[1] << 16), t16[2] | (t16[3] << 16), t16[4] | (t16[5] << 16), t16[6] | (t16[7] << 16));
+    }
+  } else {
     // R^T as three bf16 terms: thread (c, i0) reads R[i0 .. i0 + 7][c] (coalesced over c) and
     // splits each value by truncation: r = t0 + t1 + t2 exactly (t0 and t1 take the leading 8
     // significant bits of r and of r - t0, the remainder has at most 8 left), then writes one
@@ -292,8 +383,23 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
   // this one is computed (indexes clamped, so the fetch past the last step stays in bounds)
   const int sstride = nbx * kWaves;
   for (int st = step0; st * kStep < n; st += sstride) {
+    if (rope) {
+      // this step's keys become post-RoPE rows; a position outside the table skips the token
+#pragma unroll
+      for (int u = 0; u < kApTiles; ++u) {
+        const int tok = st * kStep + 16 * u + lo;
+        const bool ok = pos[u] >= 0 && pos[u] < opt.max_pos;
+        if (!ok) slot[u] = -1;
+        rope_lane(X8[u], opt.cos_sin + (size_t)(ok ? pos[u] : 0) * kHeadDim, hi);
+        if (opt.k_out && ok && tok < n) {
+          uint16_t* orow = opt.k_out + ((size_t)tok * H + h) * kHeadDim + 8 * hi;
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) *reinterpret_cast<ap_bf16x8_t*>(orow + 32 * ks) = X8[u][ks];
+        }
+      }
+    }
     ap_bf16x8_t Xn[kApTiles][4];
-    int slotn[kApTiles];
+    int slotn[kApTiles], posn[kApTiles];
 #pragma unroll
     for (int u = 0; u < kApTiles; ++u) {
       const int tok = (st + sstride) * kStep + 16 * u + lo, tc = min(tok, n - 1);
@@ -301,12 +407,13 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) Xn[u][ks] = *reinterpret_cast<const ap_bf16x8_t*>(xrow + 32 * ks);
       slotn[u] = slots[tc];
+      posn[u] = rope ? opt.pos[tc] : 0;
     }
-    ap_f4_t acc[kApTiles][8];  // start at - mu R_K (keys) or 0 (values)
+    ap_f4_t acc[kApTiles][8];  // start at - mu R_K (keys) or 0 (values); 0 for the Hadamard product
 #pragma unroll
     for (int u = 0; u < kApTiles; ++u)
 #pragma unroll
-      for (int p = 0; p < 8; ++p) acc[u][p] = sub[p];
+      for (int p = 0; p < 8; ++p) acc[u][p] = had ? ap_f4_t{0.f, 0.f, 0.f, 0.f} : sub[p];
     // the R^T fragments are the same for every step: an opaque offset keeps the compiler from
     // hoisting all 96 of them into registers (which would cap occupancy at one wave per SIMD)
     int boff = (lo * kApRow + 8 * hi) * 2;
@@ -318,24 +425,39 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
       const int term = 2 - f / 32, ks = (f / 8) % 4, p = f % 8;
       return *reinterpret_cast<const ap_bf16x8_t*>(rb + ((term * kHeadDim + 16 * p) * kApRow + 32 * ks) * 2);
     };
-    ap_bf16x8_t fr[kApDepth];
+    // fragments F0 .. 95: all three terms (F0 = 0) or the Hadamard's single +-1 term (F0 = 64)
+    auto mfma_pass = [&](auto f0_tag) {
+      constexpr int F0 = decltype(f0_tag)::value;
+      ap_bf16x8_t fr[kApDepth];
 #pragma unroll
-    for (int f = 0; f < kApDepth; ++f) fr[f] = frag(f);
+      for (int f = 0; f < kApDepth; ++f) fr[f] = frag(F0 + f);
 #pragma unroll
-    for (int f = 0; f < 96; ++f) {
-      const ap_bf16x8_t a = fr[f % kApDepth];
-      const int ks = (f / 8) % 4, p = f % 8;
+      for (int f = F0; f < 96; ++f) {
+        const ap_bf16x8_t a = fr[(f - F0) % kApDepth];
+        const int ks = (f / 8) % 4, p = f % 8;
+#pragma unroll
+        for (int u = 0; u < kApTiles; ++u)
+          acc[u][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, X8[u][ks], acc[u][p], 0, 0, 0);
+        if (f + kApDepth < 96) fr[(f - F0) % kApDepth] = frag(f + kApDepth);
+      }
+#pragma unroll
+      for (int f = 0; f < kApDepth; ++f) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+#pragma unroll
+      for (int f = F0; f < 96; ++f) {
+        __builtin_amdgcn_sched_group_barrier(0x008, kApTiles, 0);  // MFMA
+        if (f + kApDepth < 96) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+    };
+    if (had) {
+      mfma_pass(std::integral_constant<int, 64>{});
 #pragma unroll
       for (int u = 0; u < kApTiles; ++u)
-        acc[u][p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, X8[u][ks], acc[u][p], 0, 0, 0);
-      if (f + kApDepth < 96) fr[f % kApDepth] = frag(f + kApDepth);
-    }
 #pragma unroll
-    for (int f = 0; f < kApDepth; ++f) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+        for (int p = 0; p < 8; ++p)
 #pragma unroll
-    for (int f = 0; f < 96; ++f) {
-      __builtin_amdgcn_sched_group_barrier(0x008, kApTiles, 0);  // MFMA
-      if (f + kApDepth < 96) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          for (int j = 0; j < 4; ++j) acc[u][p][j] = __builtin_fmaf(acc[u][p][j], kHadScale, sub[p][j]);
+    } else {
+      mfma_pass(std::integral_constant<int, 0>{});
     }
     ApOut out[kApTiles];
 #pragma unroll
@@ -347,6 +469,7 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) asm volatile("" : "+v"(Xn[u][ks])::"memory");
       asm volatile("" : "+v"(slotn[u])::"memory");
+      if (rope) asm volatile("" : "+v"(posn[u])::"memory");
     }
 #pragma unroll
     for (int u = 0; u < kApTiles; ++u) store_tile<NG>(out[u], slot[u], cv, h, kv, nslots, hi);
@@ -363,6 +486,7 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) X8[u][ks] = Xn[u][ks];
       slot[u] = tok < n ? slotn[u] : -1;
+      pos[u] = posn[u];
     }
   }
 }

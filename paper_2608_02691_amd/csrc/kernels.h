@@ -21,11 +21,21 @@ hipError_t launch_fold_wo(const uint16_t* W_o, const float* R_v, uint16_t* W_f, 
                           int H, hipStream_t s);
 hipError_t launch_pack_rotated(CacheView c, const float* k_rot, const float* v_rot, const int32_t* slots,
                                int n, float clip_k, float clip_v, hipStream_t s);
+// Optional stages of the cache write: RoPE of pre-RoPE keys (positions non-null) and the Hadamard
+// rotation in place of R_K (hadamard bit 0) and / or R_V (bit 1).
+struct AppendOptions {
+  const int32_t* positions = nullptr;
+  const float* cos_sin = nullptr;
+  int max_pos = 0;
+  uint16_t* k_rope_out = nullptr;
+  int hadamard = 0;
+};
 // ev0 / ev1 (may be null): events that track the append kernel's own start and end
 hipError_t launch_append_mfma(CacheView c, const uint16_t* k, const uint16_t* v, const int32_t* slots,
                               int n, const float* R_k, const float* R_v, const float* mu_rk, float clip_k,
                               float clip_v, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr,
-                              float* err = nullptr);  // err: [n, H, 2] squared reconstruction errors
+                              float* err = nullptr,  // err: [n, H, 2] squared reconstruction errors
+                              const AppendOptions* opts = nullptr);
 
 // ---- decode (decode.hip, decode_mfma.hip, wo_gemm.hip)
 struct DecodePlan {

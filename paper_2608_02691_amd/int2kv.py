@@ -8,6 +8,7 @@ HIP library is missing, importing any entry point raises.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 from typing import Optional
 
@@ -41,7 +42,7 @@ EXPORTED = (
     "int2kv_decode", "int2kv_append_decode", "int2kv_append_decode_noalloc", "int2kv_window_write",
     "int2kv_decode_window",
     "int2kv_set_decode_tuning", "int2kv_set_decode_events", "int2kv_quantize_append_error",
-    "int2kv_output_error_workspace_bytes", "int2kv_output_error",
+    "int2kv_output_error_workspace_bytes", "int2kv_output_error", "int2kv_quantize_append_rope",
 )
 
 
@@ -86,6 +87,7 @@ def load_library(path: str = LIB_PATH):
         "int2kv_set_decode_tuning": ([I, I], I),
         "int2kv_quantize_append_error": ([ctypes.POINTER(_Cache), P, P, P, I, P, P, P, F, F, P, S], I),
         "int2kv_output_error_workspace_bytes": ([I, I, I, I, I], Z),
+        "int2kv_quantize_append_rope": ([ctypes.POINTER(_Cache), P, P, P, P, I, P, I, P, P, P, F, F, I, P, S], I),
         "int2kv_output_error": ([ctypes.POINTER(_Cache), P, I, I, P, I, P, I, P, P, P, P, I, P, I, P, P, P, Z, S],
                                 I),
         "int2kv_set_decode_events": ([P, P], I),
@@ -436,3 +438,41 @@ def int2kv_output_error(cache: Int2KVCache, q: torch.Tensor, block_table: torch.
         workspace.numel(), _stream())
     _check(st, "int2kv_output_error")
     return (stats, dy) if want_dy else stats
+
+
+INT2KV_HADAMARD_K = 1
+INT2KV_HADAMARD_V = 2
+
+
+def int2kv_quantize_append_rope(cache: Int2KVCache, k: torch.Tensor, v: torch.Tensor, slot_mapping: torch.Tensor,
+                                positions: Optional[torch.Tensor], cos_sin: Optional[torch.Tensor],
+                                R_k: Optional[torch.Tensor], R_v: Optional[torch.Tensor], mu_rk: torch.Tensor,
+                                clip_k: float = 1.0, clip_v: float = 1.0, flags: int = 0,
+                                k_rope_out: Optional[torch.Tensor] = None) -> None:
+    """Cache write of pre-RoPE keys (positions and an fp32 [max_pos, 128] cos/sin table), with the
+    Hadamard rotation in place of R_K / R_V under INT2KV_HADAMARD_K / _V."""
+    n = slot_mapping.shape[0]
+    if k.numel() != n * cache.num_kv_heads * HEAD_DIM or v.numel() != k.numel():
+        raise ValueError("k / v must be [n, num_kv_heads, 128]")
+    if positions is not None and positions.numel() != n:
+        raise ValueError("positions must hold one position per token")
+    max_pos = cos_sin.shape[0] if cos_sin is not None else 0
+    st = load_library().int2kv_quantize_append_rope(
+        cache.desc, _ptr(k, _BF16, "k"), _ptr(v, _BF16, "v"), _ptr(slot_mapping, _I32, "slot_mapping"),
+        _ptr(positions, _I32, "positions"), n, _ptr(cos_sin, _F32, "cos_sin"), max_pos, _ptr(R_k, _F32, "R_k"),
+        _ptr(R_v, _F32, "R_v"), _ptr(mu_rk, _F32, "mu_rk"), clip_k, clip_v, flags,
+        _ptr(k_rope_out, _BF16, "k_rope_out"), _stream())
+    _check(st, "int2kv_quantize_append_rope")
+
+
+def hadamard_rotation(num_heads: int, device="cuda") -> torch.Tensor:
+    """The dense fp32 form of the library's Hadamard rotation, [num_heads, 128, 128]: entries
+    (-1)^popcount(i & c) * RN(1 / sqrt(128)), as the decode and the other readers take it."""
+    i = torch.arange(HEAD_DIM)
+    x = i[:, None] & i[None, :]
+    par = torch.zeros_like(x)
+    for b in range(7):
+        par ^= (x >> b) & 1
+    scale = torch.tensor(1.0 / math.sqrt(HEAD_DIM), dtype=torch.float32)
+    H = torch.where(par == 1, -scale, scale)
+    return H[None].expand(num_heads, HEAD_DIM, HEAD_DIM).contiguous().to(device)

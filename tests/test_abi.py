@@ -141,3 +141,23 @@ def test_noalloc_rejects_workspace_beyond_the_static_scratch_without_launch():
                                           16, 1, 16, 1 << 20, 16, 16, None, 0, 0, 16, None)
     assert st == K.INT2KV_EWORKSPACE
     assert b"static scratch" in lib.int2kv_last_error()
+
+
+def test_rope_write_rejects_bad_arguments_without_launch():
+    """int2kv_quantize_append_rope validates flags, rotations and the RoPE table on the host."""
+    lib = K.load_library()
+    cache = K._Cache(16, 1 << 20, 8, 16, 128, 32)  # pool pointer never dereferenced
+    p = 1 << 20  # aligned stand-in pointers, never dereferenced on a rejected call
+
+    def call(R_k, R_v, positions, cos_sin, max_pos, flags, k_out=None):
+        return lib.int2kv_quantize_append_rope(ctypes.byref(cache), p, p, p, positions, 4, cos_sin, max_pos, R_k, R_v,
+                                               p, 1.0, 1.0, flags, k_out, None)
+
+    assert call(p, p, None, None, 0, 4) == K.INT2KV_EINVAL                      # unknown flag
+    assert b"flags" in lib.int2kv_last_error()
+    assert call(None, p, None, None, 0, 0) == K.INT2KV_EINVAL                   # R_K missing, no flag
+    assert call(p, None, None, None, 0, K.INT2KV_HADAMARD_K) == K.INT2KV_EINVAL  # R_V missing
+    assert call(p, p, p, None, 16, 0) == K.INT2KV_EINVAL                        # positions without table
+    assert call(p, p, p, p, 0, 0) == K.INT2KV_EINVAL                            # empty table
+    assert call(p, p, None, None, 0, 0, k_out=p) == K.INT2KV_EINVAL             # k_rope_out without RoPE
+    assert call(p, p, p, p + 4, 16, 0) == K.INT2KV_EINVAL                       # misaligned table
