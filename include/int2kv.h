@@ -318,6 +318,68 @@ int int2kv_output_error(const int2kv_cache* cache, const uint16_t* q, int batch,
                         float* stats, float* dy, void* workspace, size_t workspace_bytes,
                         hipStream_t stream);
 
+/* ---- OptR offline calibration (Sec. 4.2 - 4.5; Algorithm 1 of the appendix), fp64 on the GPU.
+ * For every KV head h the corrected rotations R = R^0 exp(A - A^T) (eq:OptR_skew) are fitted to
+ * calibration traces: first A_K on the key objective (eq:OptR_key_loss)
+ *     L_K = mean over rows (t, j) of KL(p_t || p^K_t) + lambda_K ||((p^K_t - p_t)^T V) W_{O,j}^T||^2 / d_model,
+ * then A_V on the value objective (eq:OptR_value_loss) under the selected key rotation's
+ * probabilities p^K-hat:
+ *     L_V = mean over rows of ||(p^K-hat_t^T (V~ - V)) W_{O,j}^T||^2 / d_model.
+ * Rows: query heads j of the KV head's group at the final n_last positions t of each sequence,
+ * attending causally (s <= t). Effective keys k~ = Q2((k - mu) R_K) R_K^T and values
+ * v~ = Q2(v R_V) R_V^T use the cache's own quantizer on the fp32 rounding of the rotated rows
+ * (group_size, clip ratios); tokens s < sink and s > t - recent stay in full precision (BF16
+ * windows). Gradients pass the quantizer by the straight-through estimator of eq:OptR_ste: an
+ * element's gradient passes when it lies inside its group's clipped range [c mn, c mx]; scale and
+ * zero are held fixed. The optimizer is Adam (betas 0.9 / 0.999, eps 1e-8, learning rate lr); the
+ * iterate with the lowest held-out objective among A = 0 and every eval_every-th step is kept.
+ * All arithmetic is fp64; inputs stay as given (bf16 traces, fp32 R^0 and mu). */
+typedef struct int2kv_optr_traces {
+  const uint16_t* k;          /* device bf16 [T, H_kv, 128]: keys (post-RoPE, raw) */
+  const uint16_t* v;          /* device bf16 [T, H_kv, 128]: values */
+  const uint16_t* q;          /* device bf16 [T, H_q, 128]: queries (post-RoPE) */
+  const int32_t* seq_starts;  /* HOST int32 [num_seqs + 1]: token offsets, seq_starts[0] = 0,
+                                 sequences of 0 .. 4096 tokens */
+  int num_seqs;
+} int2kv_optr_traces;
+
+typedef struct int2kv_optr_config {
+  int num_kv_heads, num_q_heads, d_model, group_size; /* group_size 32 or 128 */
+  float clip_k, clip_v;                               /* the paper's setting: 0.96, 0.92 */
+  double lambda_k;                                    /* 1.0 */
+  int n_last, sink, recent;                           /* 64, 64, 256 */
+  int steps, eval_every;                              /* 80, 20 */
+  double lr;                                          /* 0.02 */
+} int2kv_optr_config;
+
+/* Workspace bytes of the calls below (heldout may be NULL for the loss calls); 0 on bad arguments. */
+size_t int2kv_optr_workspace_bytes(const int2kv_optr_config* cfg, const int2kv_optr_traces* calib,
+                                   const int2kv_optr_traces* heldout);
+/* Per-channel key mean per KV head (appendix, key-mean estimation): mu[h][c] = fp32(fp64 mean over
+ * the num_tokens keys k [T, H_kv, 128] bf16). */
+int int2kv_optr_key_mean(const uint16_t* k, int num_tokens, int num_kv_heads, float* mu, hipStream_t stream);
+/* L_K of every KV head at generators A (device fp64 [H_kv, 128, 128]) into loss (device fp64 [H_kv]),
+ * and dL_K/dA into grad (device fp64 [H_kv, 128, 128]) unless grad is NULL. R0_k: fp32 [H_kv, 128, 128];
+ * mu: fp32 [H_kv, 128]; W_o: bf16 [d_model, H_q * 128]. */
+int int2kv_optr_key_loss(const int2kv_optr_config* cfg, const int2kv_optr_traces* traces, const float* R0_k,
+                         const float* mu, const uint16_t* W_o, const double* A, double* loss, double* grad,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+/* L_V at generators A_v under the key probabilities of generators A_k, and dL_V/dA_v. */
+int int2kv_optr_value_loss(const int2kv_optr_config* cfg, const int2kv_optr_traces* traces, const float* R0_k,
+                           const double* A_k, const float* mu, const float* R0_v, const uint16_t* W_o,
+                           const double* A_v, double* loss, double* grad, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream);
+/* Algorithm 1 for every KV head at once: R_k, R_v (device fp32 [H_kv, 128, 128]) receive the
+ * selected R^0 exp(A - A^T); A_k, A_v (device fp64, may be NULL) the selected generators; history
+ * (device fp64, may be NULL) [2][H_kv][steps + 1 + steps / eval_every]: for keys, then values, the
+ * training objective before each step followed by the held-out objectives at A = 0 and every
+ * eval_every-th step. The host tables of both trace sets are uploaded at the start (the call waits
+ * for that copy); the rest runs asynchronously on stream. */
+int int2kv_optr_calibrate(const int2kv_optr_config* cfg, const int2kv_optr_traces* calib,
+                          const int2kv_optr_traces* heldout, const float* R0_k, const float* R0_v, const float* mu,
+                          const uint16_t* W_o, float* R_k, float* R_v, double* A_k, double* A_v, double* history,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Measurement hook: when set (non-NULL), the calls this thread issues attach `before_scan` and
  * `after_scan` to the dispatch of their dominant kernel (hipExtLaunchKernel): the split-context scan
  * of int2kv_decode, int2kv_append_decode and int2kv_decode_window, the cache-write kernel of

@@ -619,3 +619,218 @@ int int2kv_output_error(const int2kv_cache* cache, const uint16_t* q, int batch,
 }
 
 }  // extern "C"
+
+// ---- OptR offline calibration
+namespace {
+
+struct OptrLayout {
+  size_t shared, set_c, set_h, state, total;
+};
+
+struct SetDims {
+  int T = 0, nseq = 0, nrows = 0;
+  long long pel = 0;
+};
+
+int check_traces(const int2kv_optr_traces* t, const int2kv_optr_config* c, SetDims& d, const char* what) {
+  if (!t || !t->k || !t->v || !t->q || !t->seq_starts || t->num_seqs <= 0)
+    return fail(INT2KV_EINVAL, std::string(what) + ": NULL pointer or no sequences");
+  if (t->seq_starts[0] != 0) return fail(INT2KV_EINVAL, std::string(what) + ": seq_starts[0] must be 0");
+  const int gq = c->num_q_heads / c->num_kv_heads;
+  d = SetDims{};
+  for (int i = 0; i < t->num_seqs; ++i) {
+    const int len = t->seq_starts[i + 1] - t->seq_starts[i];
+    if (len < 0 || len > kCalMaxLen)
+      return fail(INT2KV_EINVAL, std::string(what) + ": sequence lengths must be in [0, 4096]");
+    const int rows = (len < c->n_last ? len : c->n_last) * gq;
+    d.nrows += rows;
+    d.pel += (long long)rows * len;
+  }
+  d.T = t->seq_starts[t->num_seqs];
+  d.nseq = t->num_seqs;
+  if (!aligned(t->k, 4) || !aligned(t->v, 4)) return fail(INT2KV_EINVAL, std::string(what) + ": k, v must be 4-byte aligned");
+  return INT2KV_OK;
+}
+
+int check_config(const int2kv_optr_config* c) {
+  if (!c) return fail(INT2KV_EINVAL, "config is NULL");
+  if (c->num_kv_heads <= 0 || c->num_q_heads <= 0 || c->num_q_heads % c->num_kv_heads)
+    return fail(INT2KV_EINVAL, "num_q_heads must be a positive multiple of num_kv_heads");
+  if (c->d_model <= 0) return fail(INT2KV_EINVAL, "d_model must be positive");
+  if (c->group_size != 32 && c->group_size != 128) return fail(INT2KV_EUNSUPPORTED, "group_size must be 32 or 128");
+  if (!valid_clip(c->clip_k) || !valid_clip(c->clip_v)) return fail(INT2KV_EINVAL, "clip ratios must be in (0, 1]");
+  if (c->n_last <= 0 || c->sink < 0 || c->recent < 0) return fail(INT2KV_EINVAL, "bad n_last / sink / recent");
+  if (c->steps < 0 || c->eval_every <= 0 || !(c->lr > 0.0) || !(c->lambda_k >= 0.0)) return fail(INT2KV_EINVAL, "bad steps / eval_every / lr");
+  return INT2KV_OK;
+}
+
+OptrLayout optr_layout(const int2kv_optr_config* c, const SetDims& dc, const SetDims* dh) {
+  OptrLayout L{};
+  const int H = c->num_kv_heads;
+  L.shared = cal_shared_bytes(H, c->num_q_heads);
+  L.set_c = cal_set_bytes(dc.T, dc.nseq, dc.nrows, dc.pel, H);
+  L.set_h = dh ? cal_set_bytes(dh->T, dh->nseq, dh->nrows, dh->pel, H) : 0;
+  // optimizer state: A, A_best, m, v, grad ([H, 128, 128] each), best loss and loss ([H] each)
+  L.state = 5 * (size_t)H * kHeadDim * kHeadDim * 8 + 2 * 256 + 2 * (size_t)H * 8;
+  L.total = L.shared + L.set_c + L.set_h + L.state + 1024;
+  return L;
+}
+
+CalCfg make_cal_cfg(const int2kv_optr_config* c, const float* mu, const float* R0k, const float* R0v) {
+  CalCfg g{};
+  g.H = c->num_kv_heads;
+  g.Hq = c->num_q_heads;
+  g.gq = g.Hq / g.H;
+  g.dm = c->d_model;
+  g.ng = kHeadDim / c->group_size;
+  g.clip_k = c->clip_k;
+  g.clip_v = c->clip_v;
+  g.lam = c->lambda_k;
+  g.sink = c->sink;
+  g.recent = c->recent;
+  g.n_last = c->n_last;
+  g.mu = mu;
+  g.R0k = R0k;
+  g.R0v = R0v;
+  return g;
+}
+
+uint8_t* align256(void* p) {
+  return reinterpret_cast<uint8_t*>((reinterpret_cast<uintptr_t>(p) + 255) & ~uintptr_t(255));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t int2kv_optr_workspace_bytes(const int2kv_optr_config* cfg, const int2kv_optr_traces* calib,
+                                   const int2kv_optr_traces* heldout) {
+  if (check_config(cfg)) return 0;
+  SetDims dc, dh;
+  if (check_traces(calib, cfg, dc, "calib")) return 0;
+  if (heldout && check_traces(heldout, cfg, dh, "heldout")) return 0;
+  return optr_layout(cfg, dc, heldout ? &dh : nullptr).total;
+}
+
+int int2kv_optr_key_mean(const uint16_t* k, int num_tokens, int num_kv_heads, float* mu, hipStream_t stream) {
+  if (!k || !mu || num_tokens <= 0 || num_kv_heads <= 0) return fail(INT2KV_EINVAL, "bad key-mean arguments");
+  return hip_status(cal_key_mean(k, num_tokens, num_kv_heads, mu, stream), "optr_key_mean");
+}
+
+// Shared front part of the loss entry points: validation, layout, the set and the Gram matrices.
+static int optr_setup(const int2kv_optr_config* cfg, const int2kv_optr_traces* tr, const float* mu,
+                      const float* R0_k, const float* R0_v, const uint16_t* W_o, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream, CalCfg& g, CalSet& set, uint8_t*& state) {
+  if (int st = check_config(cfg)) return st;
+  SetDims d;
+  if (int st = check_traces(tr, cfg, d, "traces")) return st;
+  if (!mu || !R0_k || !R0_v || !W_o) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  const OptrLayout L = optr_layout(cfg, d, nullptr);
+  if (!workspace || workspace_bytes < L.total) return fail(INT2KV_EWORKSPACE, "workspace smaller than int2kv_optr_workspace_bytes()");
+  uint8_t* base = align256(workspace);
+  g = make_cal_cfg(cfg, mu, R0_k, R0_v);
+  cal_bind_shared(g, base);
+  hipError_t e = cal_bind_set(set, base + L.shared, tr->k, tr->v, tr->q, tr->seq_starts, tr->num_seqs, g.H, g.gq,
+                              g.n_last, stream);
+  if (e == hipSuccess) e = cal_gram(g, W_o, stream);
+  state = base + L.shared + L.set_c;
+  return hip_status(e, "optr setup");
+}
+
+int int2kv_optr_key_loss(const int2kv_optr_config* cfg, const int2kv_optr_traces* traces, const float* R0_k,
+                         const float* mu, const uint16_t* W_o, const double* A, double* loss, double* grad,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!A || !loss) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  CalCfg g;
+  CalSet set;
+  uint8_t* state;
+  if (int st = optr_setup(cfg, traces, mu, R0_k, R0_k, W_o, workspace, workspace_bytes, stream, g, set, state)) return st;
+  return hip_status(cal_key_loss(g, set, A, loss, grad, stream), "optr_key_loss");
+}
+
+int int2kv_optr_value_loss(const int2kv_optr_config* cfg, const int2kv_optr_traces* traces, const float* R0_k,
+                           const double* A_k, const float* mu, const float* R0_v, const uint16_t* W_o,
+                           const double* A_v, double* loss, double* grad, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream) {
+  if (!A_k || !A_v || !loss) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  CalCfg g;
+  CalSet set;
+  uint8_t* state;
+  if (int st = optr_setup(cfg, traces, mu, R0_k, R0_v, W_o, workspace, workspace_bytes, stream, g, set, state)) return st;
+  hipError_t e = cal_key_probs(g, set, A_k, stream);
+  if (e == hipSuccess) e = cal_value_loss(g, set, A_v, loss, grad, stream);
+  return hip_status(e, "optr_value_loss");
+}
+
+int int2kv_optr_calibrate(const int2kv_optr_config* cfg, const int2kv_optr_traces* calib,
+                          const int2kv_optr_traces* heldout, const float* R0_k, const float* R0_v, const float* mu,
+                          const uint16_t* W_o, float* R_k, float* R_v, double* A_k, double* A_v, double* history,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (int st = check_config(cfg)) return st;
+  SetDims dc, dh;
+  if (int st = check_traces(calib, cfg, dc, "calib")) return st;
+  if (int st = check_traces(heldout, cfg, dh, "heldout")) return st;
+  if (!mu || !R0_k || !R0_v || !W_o || !R_k || !R_v) return fail(INT2KV_EINVAL, "NULL pointer argument");
+  if (!aligned(R_k, 16) || !aligned(R_v, 16)) return fail(INT2KV_EINVAL, "R_k and R_v must be 16-byte aligned");
+  const OptrLayout L = optr_layout(cfg, dc, &dh);
+  if (!workspace || workspace_bytes < L.total) return fail(INT2KV_EWORKSPACE, "workspace smaller than int2kv_optr_workspace_bytes()");
+  uint8_t* base = align256(workspace);
+  CalCfg g = make_cal_cfg(cfg, mu, R0_k, R0_v);
+  cal_bind_shared(g, base);
+  CalSet sc, sh;
+  hipError_t e = cal_bind_set(sc, base + L.shared, calib->k, calib->v, calib->q, calib->seq_starts, calib->num_seqs,
+                              g.H, g.gq, g.n_last, stream);
+  if (e == hipSuccess)
+    e = cal_bind_set(sh, base + L.shared + L.set_c, heldout->k, heldout->v, heldout->q, heldout->seq_starts,
+                     heldout->num_seqs, g.H, g.gq, g.n_last, stream);
+  if (e == hipSuccess) e = cal_gram(g, W_o, stream);
+  if (e != hipSuccess) return hip_status(e, "optr_calibrate setup");
+  const size_t nA = (size_t)g.H * kHeadDim * kHeadDim;
+  double* st = reinterpret_cast<double*>(base + L.shared + L.set_c + L.set_h);
+  double *A = st, *Abest = st + nA, *m = st + 2 * nA, *v = st + 3 * nA, *gr = st + 4 * nA;
+  double *best = st + 5 * nA, *loss = best + g.H;
+  const int steps = cfg->steps, ev = cfg->eval_every, n_eval = 1 + steps / ev, hstride = steps + n_eval;
+  auto record = [&](int phase, int idx) {
+    return history ? cal_record(loss, history + (size_t)phase * g.H * hstride + idx, hstride, g.H, stream)
+                   : hipSuccess;
+  };
+  for (int phase = 0; phase < 2 && e == hipSuccess; ++phase) {
+    const bool value = phase == 1;
+    auto eval = [&](CalSet& set, double* gradp) {
+      return value ? cal_value_loss(g, set, A, loss, gradp, stream) : cal_key_loss(g, set, A, loss, gradp, stream);
+    };
+    if (value) {  // the selected key rotation's probabilities on both sets
+      e = cal_key_probs(g, sc, A_k ? A_k : Abest, stream);
+      if (e == hipSuccess) e = cal_key_probs(g, sh, A_k ? A_k : Abest, stream);
+    }
+    if (e == hipSuccess) e = cal_fill(A, 4 * nA, 0.0, stream);  // A, A_best, m, v
+    if (e == hipSuccess) e = cal_fill(best, g.H, INFINITY, stream);
+    if (e == hipSuccess) e = eval(sh, nullptr);
+    if (e == hipSuccess) e = record(phase, steps);
+    if (e == hipSuccess) e = cal_select(A, loss, best, Abest, g.H, stream);
+    for (int i = 1; i <= steps && e == hipSuccess; ++i) {
+      e = eval(sc, gr);
+      if (e == hipSuccess) e = record(phase, i - 1);
+      if (e == hipSuccess) e = cal_adam(A, gr, m, v, (int)nA, i, cfg->lr, stream);
+      if (e == hipSuccess && i % ev == 0) {
+        e = eval(sh, nullptr);
+        if (e == hipSuccess) e = record(phase, steps + i / ev);
+        if (e == hipSuccess) e = cal_select(A, loss, best, Abest, g.H, stream);
+      }
+    }
+    if (e != hipSuccess) break;
+    if (!value) {
+      e = cal_rotation_out(g, Abest, false, R_k, stream);
+      // the value phase reads the selected key generator from A_best before resetting it
+      if (e == hipSuccess && A_k)
+        e = hipMemcpyAsync(A_k, Abest, nA * sizeof(double), hipMemcpyDeviceToDevice, stream);
+    } else {
+      e = cal_rotation_out(g, Abest, true, R_v, stream);
+      if (e == hipSuccess && A_v)
+        e = hipMemcpyAsync(A_v, Abest, nA * sizeof(double), hipMemcpyDeviceToDevice, stream);
+    }
+  }
+  return hip_status(e, "optr_calibrate");
+}
+
+}  // extern "C"

@@ -135,4 +135,58 @@ struct OutErrArgs {
 hipError_t launch_output_error(const OutErrArgs& e, const uint16_t* W_o, int d_model, float* stats, float* dy,
                                hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
+// ---- OptR offline calibration (optr.hip): fp64 throughout
+constexpr int kCalMaxLen = 4096;  // tokens per calibration sequence
+constexpr int kCalSplit = 16;     // token slices of the rotation-gradient reduction
+constexpr int kCalScratch = 6;    // 128 x 128 scratch matrices per KV head of the matrix functions
+struct CalSeq {
+  int start, len, t0, row0;  // first token, length, first query position, first row
+  long long p0;              // offset of the sequence's [rows][len] block of per-row token weights
+};
+// One trace set (calibration or held-out): inputs and its per-set buffers.
+struct CalSet {
+  const uint16_t *k, *v, *q;       // bf16 [T, H, 128], [T, H, 128], [T, Hq, 128]
+  int T, nseq, nrows;              // nrows: query rows of one KV head
+  long long pelems;                // per KV head: sum over sequences of rows * len
+  CalSeq* seqs;                    // [nseq]
+  int* row_seq;                    // [nrows]: sequence of each row
+  double *zhat, *xeff, *gx, *gz;   // [T, H, 128]: dequantized rotated rows, effective rows, gradients
+  uint8_t* mask;                   // [T, H, 128]: straight-through mask
+  double* pd;                      // [H, pelems]: logit gradients (key loss) or key probabilities (value loss)
+  double* wrow;                    // [H, nrows, 128]: value-loss row weights
+  double* lrow;                    // [H, nrows]: per-row losses
+};
+struct CalCfg {
+  int H, Hq, gq, dm, ng;  // ng: quantizer groups per token (4 or 1)
+  float clip_k, clip_v;
+  double lam;
+  int sink, recent, n_last;
+  const float* mu;        // [H, 128]
+  const float *R0k, *R0v; // fp32 [H, 128, 128]
+  double* gram;           // [Hq, 128, 128]: W_{O,j}^T W_{O,j}
+  double *R, *Rt;         // [H, 128, 128]: the current rotation and its transpose
+  double* ex;             // [H, kCalScratch, 128, 128]
+  double* drp;            // [kCalSplit, H, 128, 128]
+  double* dr;             // [H, 128, 128]
+};
+size_t cal_set_bytes(int T, int nseq, int nrows, long long pelems, int H);
+size_t cal_shared_bytes(int H, int Hq);
+// carves a set's buffers from base and uploads its sequence and row tables (host starts [nseq + 1])
+hipError_t cal_bind_set(CalSet& set, uint8_t* base, const uint16_t* k, const uint16_t* v, const uint16_t* q,
+                        const int32_t* starts_host, int nseq, int H, int gq, int n_last, hipStream_t s);
+void cal_bind_shared(CalCfg& c, uint8_t* base);
+hipError_t cal_gram(const CalCfg& c, const uint16_t* W_o, hipStream_t s);
+// loss[h] (device) of every KV head at generators A [H, 128, 128]; grad (may be null) receives dL/dA
+hipError_t cal_key_loss(const CalCfg& c, CalSet& set, const double* A, double* loss, double* grad, hipStream_t s);
+hipError_t cal_key_probs(const CalCfg& c, CalSet& set, const double* A, hipStream_t s);
+hipError_t cal_value_loss(const CalCfg& c, CalSet& set, const double* A, double* loss, double* grad, hipStream_t s);
+hipError_t cal_adam(double* A, const double* g, double* m, double* v, int n, int step, double lr, hipStream_t s);
+// per head: when loss[h] < best[h], best[h] = loss[h] and A_best[h] = A[h]
+hipError_t cal_select(const double* A, const double* loss, double* best, double* A_best, int H, hipStream_t s);
+hipError_t cal_fill(double* p, size_t n, double v, hipStream_t s);
+hipError_t cal_record(const double* loss, double* dst, int stride, int H, hipStream_t s);  // dst[h * stride] = loss[h]
+// R0 exp(A - A^T) rounded to fp32
+hipError_t cal_rotation_out(const CalCfg& c, const double* A, bool value, float* out, hipStream_t s);
+hipError_t cal_key_mean(const uint16_t* k, int T, int H, float* mu, hipStream_t s);
+
 }  // namespace int2kv

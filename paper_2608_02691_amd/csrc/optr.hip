@@ -1,0 +1,810 @@
+// OptR offline calibration on the GPU (Sec. 4.2 - 4.5; Algorithm 1 of the appendix), in fp64.
+//
+// Per KV head h, with R = R^0 exp(A - A^T):
+//   rows:        x_s = k_s - mu (keys) or v_s (values), bf16 inputs, exact in fp64
+//   rotation:    z_s = x_s R, rounded to fp32 and quantized by the cache's quantizer (codes, fp16
+//                scale and zero); zhat_s = code * s + z (exact); mask = element inside its group's
+//                clipped range [c mn, c mx] (the straight-through estimator of eq:OptR_ste)
+//   effective:   xeff_s = zhat_s R^T
+//   key loss:    rows (t, j) over the final n_last positions; logits over s <= t with xeff for
+//                tokens read from INT2 (sink <= s <= t - recent) and x otherwise;
+//                KL(p || p^K) + lambda ||(p^K - p)^T V W_{O,j}^T||^2 / d_model, averaged over rows,
+//                the output term as dO^T M_j dO with the Gram matrix M_j = W_{O,j}^T W_{O,j}
+//   value loss:  ||p^Khat^T (Veff - V) W_{O,j}^T||^2 / d_model under fixed key probabilities
+// Gradients by hand: dL/dlogit, then dL/dxeff (per token, summed over its rows), dL/dzhat =
+// G R masked, dL/dR = X^T (mask . G R) + G^T Zhat, dL/dE = R0^T dL/dR for E = exp(S), dL/dS as the
+// Frechet derivative of exp at S^T applied to dL/dE (the upper-right block of the exponential of
+// [[S^T, dL/dE], [0, S^T]]), and dL/dA = dL/dS - dL/dS^T.
+// exp: scaling by 2^-s until ||S||_1 <= 1/2, a Taylor polynomial of 14 terms (truncation below
+// 1e-17 relative), then s squarings; one work-group per KV head, products through LDS tiles.
+#include <vector>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace int2kv {
+
+namespace {
+
+constexpr int kD = kHeadDim;
+constexpr int kMat = kD * kD;
+constexpr int kRotTile = 16;   // tokens per rotation work-group
+constexpr int kExpTerms = 14;
+constexpr int kExpThreads = 1024;
+constexpr double kInvSqrtD = 0.08838834764831845;  // 1 / sqrt(128)
+
+__device__ __forceinline__ double bf16d(uint16_t b) { return (double)__uint_as_float((uint32_t)b << 16); }
+
+__device__ __forceinline__ double wave_sum(double x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+// block-wide reductions over blockDim.x threads (a multiple of 64, at most 1024); red: 16 doubles
+__device__ double block_sum(double x, double* red) {
+  x = wave_sum(x);
+  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = x;
+  __syncthreads();
+  double t = 0.0;
+  for (int i = 0; i < nw; ++i) t += red[i];  // fixed order: deterministic
+  return t;
+}
+
+__device__ double block_max(double x, double* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x = fmax(x, __shfl_xor(x, off));
+  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = x;
+  __syncthreads();
+  double t = red[0];
+  for (int i = 1; i < nw; ++i) t = fmax(t, red[i]);
+  return t;
+}
+
+__device__ __forceinline__ bool int2_token(int s, int t, int sink, int recent) {
+  return s >= sink && s <= t - recent;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Rotation and quantization: block (16-token tile, KV head), thread = channel.
+__global__ __launch_bounds__(128) void cal_rotq_kernel(CalSet S, CalCfg c, int value) {
+  __shared__ double xs[kRotTile][kD];
+  __shared__ float red[2][kRotTile][2];
+  const int h = blockIdx.y, col = threadIdx.x, s0 = blockIdx.x * kRotTile;
+  const int n = min(kRotTile, S.T - s0);
+  const uint16_t* X = value ? S.v : S.k;
+  const double muc = value ? 0.0 : (double)c.mu[h * kD + col];
+  for (int t = 0; t < kRotTile; ++t)
+    xs[t][col] = t < n ? bf16d(X[((size_t)(s0 + t) * c.H + h) * kD + col]) - muc : 0.0;
+  __syncthreads();
+  const double* R = c.R + (size_t)h * kMat;
+  double z[kRotTile];
+#pragma unroll
+  for (int t = 0; t < kRotTile; ++t) z[t] = 0.0;
+  for (int i = 0; i < kD; ++i) {
+    const double r = R[i * kD + col];
+#pragma unroll
+    for (int t = 0; t < kRotTile; ++t) z[t] = fma(xs[t][i], r, z[t]);
+  }
+  const float clip = value ? c.clip_v : c.clip_k;
+  __syncthreads();  // xs is reused for zhat below
+#pragma unroll
+  for (int t = 0; t < kRotTile; ++t) {
+    const float x = (float)z[t];
+    float mn = x, mx = x;
+    if (c.ng == 4) {
+#pragma unroll
+      for (int off = 16; off >= 1; off >>= 1) {
+        mn = fminf(mn, __shfl_xor(mn, off, 32));
+        mx = fmaxf(mx, __shfl_xor(mx, off, 32));
+      }
+    } else {
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        mn = fminf(mn, __shfl_xor(mn, off));
+        mx = fmaxf(mx, __shfl_xor(mx, off));
+      }
+      if ((col & 63) == 0) {
+        red[col >> 6][t][0] = mn;
+        red[col >> 6][t][1] = mx;
+      }
+      __syncthreads();
+      mn = fminf(red[0][t][0], red[1][t][0]);
+      mx = fmaxf(red[0][t][1], red[1][t][1]);
+    }
+    uint32_t s_bits, z_bits;
+    float zf, inv;
+    int2_group_params(mn, mx, clip, s_bits, z_bits, zf, inv);
+    const uint32_t code = int2_code(x, zf, inv);
+    const double zh = (double)code * (double)__half2float(__ushort_as_half((unsigned short)s_bits)) + (double)zf;
+    float lo = mn, hi = mx;
+    if (clip != 1.0f) {
+#pragma clang fp contract(off)
+      lo = clip * mn;
+      hi = clip * mx;
+    }
+    xs[t][col] = zh;
+    if (t < n) {
+      const size_t o = ((size_t)(s0 + t) * c.H + h) * kD + col;
+      S.zhat[o] = zh;
+      S.mask[o] = (x >= lo && x <= hi) ? 1 : 0;
+    }
+  }
+  __syncthreads();
+  // effective rows: zhat R^T, i.e. sum_i zhat[i] Rt[i][col]
+  const double* Rt = c.Rt + (size_t)h * kMat;
+#pragma unroll
+  for (int t = 0; t < kRotTile; ++t) z[t] = 0.0;
+  for (int i = 0; i < kD; ++i) {
+    const double r = Rt[i * kD + col];
+#pragma unroll
+    for (int t = 0; t < kRotTile; ++t) z[t] = fma(xs[t][i], r, z[t]);
+  }
+  for (int t = 0; t < n; ++t) S.xeff[((size_t)(s0 + t) * c.H + h) * kD + col] = z[t];
+}
+
+// ---------------------------------------------------------------------------------------------
+// Key objective of one row (t, j) and its logit gradients, or (probs) the key probabilities only.
+// Block (row, KV head) of 256 threads.
+__global__ __launch_bounds__(256) void cal_attn_kernel(CalSet S, CalCfg c, int probs_only) {
+  __shared__ double af[kCalMaxLen], ak[kCalMaxLen], gg[kCalMaxLen];
+  __shared__ double qv[kD], dov[2][kD], uv[kD];
+  __shared__ double red[16];
+  const int row = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+  const CalSeq sq = S.seqs[S.row_seq[row]];
+  const int local = row - sq.row0, t = sq.t0 + local / c.gq, jj = local % c.gq, j = h * c.gq + jj;
+  const int a0 = sq.start, L = sq.len;
+  if (tid < kD) qv[tid] = bf16d(S.q[((size_t)(a0 + t) * c.Hq + j) * kD + tid]);
+  __syncthreads();
+  const double mu0 = (double)c.mu[h * kD + 2 * l], mu1 = (double)c.mu[h * kD + 2 * l + 1];
+  const double q0 = qv[2 * l], q1 = qv[2 * l + 1];
+  for (int s = w; s <= t; s += 4) {
+    const size_t o = ((size_t)(a0 + s) * c.H + h) * kD + 2 * l;
+    const uint32_t kk = *reinterpret_cast<const uint32_t*>(S.k + o);
+    const double k0 = (double)__uint_as_float(kk << 16) - mu0, k1 = (double)__uint_as_float(kk & 0xFFFF0000u) - mu1;
+    const double f = wave_sum(q0 * k0 + q1 * k1) * kInvSqrtD;
+    double g = f;
+    if (int2_token(s, t, c.sink, c.recent)) g = wave_sum(q0 * S.xeff[o] + q1 * S.xeff[o + 1]) * kInvSqrtD;
+    if (l == 0) {
+      af[s] = f;
+      ak[s] = g;
+    }
+  }
+  __syncthreads();
+  double mf = -INFINITY, mk = -INFINITY;
+  for (int s = tid; s <= t; s += blockDim.x) {
+    mf = fmax(mf, af[s]);
+    mk = fmax(mk, ak[s]);
+  }
+  mf = block_max(mf, red);
+  mk = block_max(mk, red);
+  double zf = 0.0, zk = 0.0;
+  for (int s = tid; s <= t; s += blockDim.x) {
+    zf += exp(af[s] - mf);
+    zk += exp(ak[s] - mk);
+  }
+  zf = block_sum(zf, red);
+  zk = block_sum(zk, red);
+  const double lsf = mf + log(zf), lsk = mk + log(zk);
+  double* pd = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)local * L;
+  if (probs_only) {
+    for (int s = tid; s < L; s += blockDim.x)
+      pd[s] = (s <= t && int2_token(s, t, c.sink, c.recent)) ? exp(ak[s] - lsk) : 0.0;
+    return;
+  }
+  // KL(p || p^K) and the probabilities (af <- p, ak <- p^K)
+  double kl = 0.0;
+  for (int s = tid; s <= t; s += blockDim.x) {
+    const double lp = af[s] - lsf, lq = ak[s] - lsk, p = exp(lp);
+    kl += p * (lp - lq);
+    af[s] = p;
+    ak[s] = exp(lq);
+  }
+  kl = block_sum(kl, red);
+  // dO = sum_s (p^K - p) v_s: thread (channel, half of the tokens)
+  {
+    const int col = tid & 127, half = tid >> 7;
+    double acc = 0.0;
+    for (int s = half; s <= t; s += 2) acc += (ak[s] - af[s]) * bf16d(S.v[((size_t)(a0 + s) * c.H + h) * kD + col]);
+    dov[half][col] = acc;
+  }
+  __syncthreads();
+  if (tid < kD) dov[0][tid] += dov[1][tid];
+  __syncthreads();
+  // u = M_j dO (M symmetric: column reads), E = dO . u / d_model
+  double e = 0.0;
+  if (tid < kD) {
+    const double* M = c.gram + (size_t)j * kMat;
+    double u = 0.0;
+    for (int b = 0; b < kD; ++b) u = fma(M[b * kD + tid], dov[0][b], u);
+    uv[tid] = u;
+    e = u * dov[0][tid];
+  }
+  e = block_sum(e, red) / (double)c.dm;
+  if (tid == 0) S.lrow[(size_t)h * S.nrows + row] = kl + c.lam * e;
+  // g_s = 2 u . v_s / d_model, gbar = sum_s p^K_s g_s
+  const double u0 = uv[2 * l], u1 = uv[2 * l + 1];
+  for (int s = w; s <= t; s += 4) {
+    const uint32_t vv = *reinterpret_cast<const uint32_t*>(S.v + ((size_t)(a0 + s) * c.H + h) * kD + 2 * l);
+    const double g = wave_sum(u0 * (double)__uint_as_float(vv << 16) + u1 * (double)__uint_as_float(vv & 0xFFFF0000u));
+    if (l == 0) gg[s] = 2.0 * g / (double)c.dm;
+  }
+  __syncthreads();
+  double gb = 0.0;
+  for (int s = tid; s <= t; s += blockDim.x) gb += ak[s] * gg[s];
+  gb = block_sum(gb, red);
+  const double inv_rows = 1.0 / (double)S.nrows;
+  for (int s = tid; s < L; s += blockDim.x) {
+    double d = 0.0;
+    if (s <= t && int2_token(s, t, c.sink, c.recent))
+      d = ((ak[s] - af[s]) + c.lam * ak[s] * (gg[s] - gb)) * inv_rows;
+    pd[s] = d;
+  }
+}
+
+// Value objective of one row under the stored key probabilities: block (row, KV head), thread =
+// channel. Also the row's weight 2 M_j dO / (d_model rows) for the gradient.
+__global__ __launch_bounds__(128) void cal_vrow_kernel(CalSet S, CalCfg c) {
+  __shared__ double dov[kD];
+  __shared__ double red[16];
+  const int row = blockIdx.x, h = blockIdx.y, col = threadIdx.x;
+  const CalSeq sq = S.seqs[S.row_seq[row]];
+  const int local = row - sq.row0, t = sq.t0 + local / c.gq, jj = local % c.gq, j = h * c.gq + jj;
+  const double* pd = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)local * sq.len;
+  double acc = 0.0;
+  for (int s = 0; s <= t; ++s) {
+    const double p = pd[s];
+    if (p != 0.0) {
+      const size_t o = ((size_t)(sq.start + s) * c.H + h) * kD + col;
+      acc += p * (S.xeff[o] - bf16d(S.v[o]));
+    }
+  }
+  dov[col] = acc;
+  __syncthreads();
+  const double* M = c.gram + (size_t)j * kMat;
+  double u = 0.0;
+  for (int b = 0; b < kD; ++b) u = fma(M[b * kD + col], dov[b], u);
+  const double e = block_sum(u * acc, red) / (double)c.dm;
+  if (col == 0) S.lrow[(size_t)h * S.nrows + row] = e;
+  S.wrow[((size_t)h * S.nrows + row) * kD + col] = 2.0 * u / ((double)c.dm * (double)S.nrows);
+}
+
+// Gradient w.r.t. the effective rows: gx[s] = sum over the rows r of s's sequence of pd[r][s] y_r
+// with y_r = q_r / sqrt(d) (keys) or the row weight (values). Block (token, KV head).
+__global__ __launch_bounds__(128) void cal_gx_kernel(CalSet S, CalCfg c, int value) {
+  const int s = blockIdx.x, h = blockIdx.y, col = threadIdx.x;
+  int lo = 0, hi = S.nseq - 1;  // the sequence holding token s
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (S.seqs[mid].start <= s) lo = mid; else hi = mid - 1;
+  }
+  const CalSeq sq = S.seqs[lo];
+  const int sl = s - sq.start;
+  double acc = 0.0;
+  if (sl >= 0 && sl < sq.len) {
+    const int nr = (sq.len - sq.t0) * c.gq;
+    const double* pd = S.pd + (size_t)h * S.pelems + sq.p0 + sl;
+    for (int lr = max(0, (sl - sq.t0) * c.gq); lr < nr; ++lr) {
+      const double p = pd[(size_t)lr * sq.len];
+      if (p == 0.0) continue;  // uniform per block
+      double y;
+      if (value) {
+        y = S.wrow[((size_t)h * S.nrows + sq.row0 + lr) * kD + col];
+      } else {
+        const int t = sq.t0 + lr / c.gq, j = h * c.gq + lr % c.gq;
+        y = bf16d(S.q[((size_t)(sq.start + t) * c.Hq + j) * kD + col]) * kInvSqrtD;
+      }
+      acc = fma(p, y, acc);
+    }
+  }
+  S.gx[((size_t)s * c.H + h) * kD + col] = acc;
+}
+
+// gz = mask . (gx R): block (16-token tile, KV head), thread = channel.
+__global__ __launch_bounds__(128) void cal_gz_kernel(CalSet S, CalCfg c) {
+  __shared__ double gs[kRotTile][kD];
+  const int h = blockIdx.y, col = threadIdx.x, s0 = blockIdx.x * kRotTile;
+  const int n = min(kRotTile, S.T - s0);
+  for (int t = 0; t < kRotTile; ++t) gs[t][col] = t < n ? S.gx[((size_t)(s0 + t) * c.H + h) * kD + col] : 0.0;
+  __syncthreads();
+  const double* R = c.R + (size_t)h * kMat;
+  double z[kRotTile];
+#pragma unroll
+  for (int t = 0; t < kRotTile; ++t) z[t] = 0.0;
+  for (int i = 0; i < kD; ++i) {
+    const double r = R[i * kD + col];
+#pragma unroll
+    for (int t = 0; t < kRotTile; ++t) z[t] = fma(gs[t][i], r, z[t]);
+  }
+  for (int t = 0; t < n; ++t) {
+    const size_t o = ((size_t)(s0 + t) * c.H + h) * kD + col;
+    S.gz[o] = S.mask[o] ? z[t] : 0.0;
+  }
+}
+
+// Partial dL/dR over a token slice: sum_s x_s[a] gz_s[b] + gx_s[a] zhat_s[b], block (16 rows a,
+// KV head, slice), thread = column b.
+__global__ __launch_bounds__(128) void cal_dr_kernel(CalSet S, CalCfg c, int value) {
+  const int a0 = blockIdx.x * 16, h = blockIdx.y, sp = blockIdx.z, b = threadIdx.x;
+  const int s_lo = (int)((long long)S.T * sp / kCalSplit), s_hi = (int)((long long)S.T * (sp + 1) / kCalSplit);
+  __shared__ double xa[16], ga[16];
+  double acc[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.0;
+  const uint16_t* X = value ? S.v : S.k;
+  for (int s = s_lo; s < s_hi; ++s) {
+    const size_t base = ((size_t)s * c.H + h) * kD;
+    __syncthreads();
+    if (b < 16) {
+      xa[b] = bf16d(X[base + a0 + b]) - (value ? 0.0 : (double)c.mu[h * kD + a0 + b]);
+      ga[b] = S.gx[base + a0 + b];
+    }
+    __syncthreads();
+    const double gzb = S.gz[base + b], zb = S.zhat[base + b];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = fma(xa[i], gzb, fma(ga[i], zb, acc[i]));
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) c.drp[(((size_t)sp * c.H + h) * kD + a0 + i) * kD + b] = acc[i];
+}
+
+__global__ __launch_bounds__(256) void cal_dr_reduce_kernel(CalCfg c) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x, n = (size_t)c.H * kMat;
+  if (i >= n) return;
+  double acc = 0.0;
+  for (int sp = 0; sp < kCalSplit; ++sp) acc += c.drp[(size_t)sp * n + i];
+  c.dr[i] = acc;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Matrix functions: one work-group of 1024 threads per KV head; thread (4 rows, 4 columns) of a
+// 128 x 128 product, operands staged through LDS in 16-wide slices.
+struct ExpLds {
+  double as[kD][17];
+  double bs[16][kD];
+  double red[16];
+};
+
+// acc += op(A) B for 128 x 128 fp64 matrices in global memory (op(A) = A or A^T). Ends with a
+// barrier, so the caller may overwrite A or B right after.
+__device__ void wg_gemm(const double* A, bool ta, const double* B, double (&acc)[4][4], ExpLds& sm) {
+  const int tid = threadIdx.x, tr = tid >> 5, tc = tid & 31;
+  for (int k0 = 0; k0 < kD; k0 += 16) {
+    for (int e = tid; e < kD * 16; e += kExpThreads) {
+      const int r = e >> 4, kk = e & 15;
+      sm.as[r][kk] = ta ? A[(k0 + kk) * kD + r] : A[r * kD + k0 + kk];
+      const int kb = e >> 7, cb = e & 127;
+      sm.bs[kb][cb] = B[(k0 + kb) * kD + cb];
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int kk = 0; kk < 16; ++kk) {
+      double av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = sm.as[4 * tr + i][kk];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) bv[i] = sm.bs[kk][4 * tc + i];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[i][q] = fma(av[i], bv[q], acc[i][q]);
+    }
+    __syncthreads();
+  }
+}
+
+__device__ __forceinline__ void zero4(double (&a)[4][4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a[i][q] = 0.0;
+}
+
+// X <- (A - A^T) * 2^-sc with sc the smallest scaling giving ||X||_1 <= 1/2 (returned); with
+// transpose, X <- (A - A^T)^T * 2^-sc.
+__device__ int wg_skew_scaled(const double* A, double* X, bool transpose, ExpLds& sm) {
+  const int tid = threadIdx.x;
+  double colsum = 0.0;
+  if (tid < kD)
+    for (int r = 0; r < kD; ++r) colsum += fabs(A[r * kD + tid] - A[tid * kD + r]);
+  const double nrm = block_max(tid < kD ? colsum : 0.0, sm.red);
+  int sc = 0;
+  while (sc < 60 && ldexp(nrm, -sc) > 0.5) ++sc;
+  const double f = ldexp(1.0, -sc);
+  for (int e = tid; e < kMat; e += kExpThreads) {
+    const int r = e >> 7, cc = e & 127;
+    const double s = A[r * kD + cc] - A[cc * kD + r];
+    X[e] = (transpose ? -s : s) * f;
+  }
+  __syncthreads();
+  return sc;
+}
+
+// Forward: R = R0 exp(A - A^T) and Rt = R^T (fp64) for every head.
+__global__ __launch_bounds__(kExpThreads) void cal_expm_kernel(CalCfg c, const double* __restrict__ Aall, int value) {
+  __shared__ ExpLds sm;
+  const int h = blockIdx.x, tid = threadIdx.x, tr = tid >> 5, tc = tid & 31;
+  double* ex = c.ex + (size_t)h * kCalScratch * kMat;
+  double *X = ex, *P = ex + kMat, *R0 = ex + 2 * kMat;
+  const float* R0f = (value ? c.R0v : c.R0k) + (size_t)h * kMat;
+  for (int e = tid; e < kMat; e += kExpThreads) {
+    R0[e] = (double)R0f[e];
+    P[e] = (e >> 7) == (e & 127) ? 1.0 : 0.0;
+  }
+  const int sc = wg_skew_scaled(Aall + (size_t)h * kMat, X, false, sm);
+  double acc[4][4];
+  for (int k = kExpTerms; k >= 1; --k) {  // P <- I + X P / k
+    zero4(acc);
+    wg_gemm(X, false, P, acc, sm);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = 4 * tr + i, cc = 4 * tc + q;
+        P[r * kD + cc] = (r == cc ? 1.0 : 0.0) + acc[i][q] / (double)k;
+      }
+    __syncthreads();
+  }
+  for (int i = 0; i < sc; ++i) {  // P <- P P
+    zero4(acc);
+    wg_gemm(P, false, P, acc, sm);
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) P[(4 * tr + a) * kD + 4 * tc + q] = acc[a][q];
+    __syncthreads();
+  }
+  zero4(acc);
+  wg_gemm(R0, false, P, acc, sm);
+  double* R = c.R + (size_t)h * kMat;
+  double* Rt = c.Rt + (size_t)h * kMat;
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = 4 * tr + a, cc = 4 * tc + q;
+      R[r * kD + cc] = acc[a][q];
+      Rt[cc * kD + r] = acc[a][q];
+    }
+}
+
+// Backward: grad = dS - dS^T with dS = L_exp(S^T, R0^T dR), S = A - A^T, for every head.
+__global__ __launch_bounds__(kExpThreads) void cal_expm_grad_kernel(CalCfg c, const double* __restrict__ Aall,
+                                                                   int value, double* __restrict__ grad) {
+  __shared__ ExpLds sm;
+  const int h = blockIdx.x, tid = threadIdx.x, tr = tid >> 5, tc = tid & 31;
+  double* ex = c.ex + (size_t)h * kCalScratch * kMat;
+  double *X = ex, *P1 = ex + kMat, *R0 = ex + 2 * kMat, *P2 = ex + 3 * kMat, *Gs = ex + 4 * kMat;
+  const float* R0f = (value ? c.R0v : c.R0k) + (size_t)h * kMat;
+  for (int e = tid; e < kMat; e += kExpThreads) {
+    R0[e] = (double)R0f[e];
+    P1[e] = (e >> 7) == (e & 127) ? 1.0 : 0.0;
+    P2[e] = 0.0;
+  }
+  const int sc = wg_skew_scaled(Aall + (size_t)h * kMat, X, true, sm);
+  const double f = ldexp(1.0, -sc);
+  double acc[4][4];
+  zero4(acc);
+  wg_gemm(R0, true, c.dr + (size_t)h * kMat, acc, sm);  // G_E = R0^T dR, scaled like X
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) Gs[(4 * tr + a) * kD + 4 * tc + q] = acc[a][q] * f;
+  __syncthreads();
+  // Taylor on the block matrix [[X, Gs], [0, X]]: (P1, P2) <- (I + X P1 / k, (X P2 + Gs P1) / k),
+  // one product sum at a time (T1 holds X P1 until P2 is formed)
+  double* T1 = ex + 5 * kMat;
+  for (int k = kExpTerms; k >= 1; --k) {
+    zero4(acc);
+    wg_gemm(X, false, P1, acc, sm);
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) T1[(4 * tr + a) * kD + 4 * tc + q] = acc[a][q];
+    zero4(acc);
+    wg_gemm(X, false, P2, acc, sm);
+    wg_gemm(Gs, false, P1, acc, sm);
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = 4 * tr + a, cc = 4 * tc + q;
+        P2[r * kD + cc] = acc[a][q] / (double)k;
+        P1[r * kD + cc] = (r == cc ? 1.0 : 0.0) + T1[r * kD + cc] / (double)k;  // own elements of T1
+      }
+    __syncthreads();
+  }
+  for (int i = 0; i < sc; ++i) {  // (P1, P2) <- (P1 P1, P1 P2 + P2 P1)
+    zero4(acc);
+    wg_gemm(P1, false, P1, acc, sm);
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) T1[(4 * tr + a) * kD + 4 * tc + q] = acc[a][q];
+    zero4(acc);
+    wg_gemm(P1, false, P2, acc, sm);
+    wg_gemm(P2, false, P1, acc, sm);
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = 4 * tr + a, cc = 4 * tc + q;
+        P2[r * kD + cc] = acc[a][q];
+        P1[r * kD + cc] = T1[r * kD + cc];
+      }
+    __syncthreads();
+  }
+  double* g = grad + (size_t)h * kMat;
+  for (int e = tid; e < kMat; e += kExpThreads) {
+    const int r = e >> 7, cc = e & 127;
+    g[e] = P2[r * kD + cc] - P2[cc * kD + r];
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void cal_loss_kernel(const double* __restrict__ lrow, int nrows,
+                                                       double* __restrict__ loss) {
+  __shared__ double red[16];
+  const int h = blockIdx.x;
+  double acc = 0.0;
+  for (int r = threadIdx.x; r < nrows; r += blockDim.x) acc += lrow[(size_t)h * nrows + r];
+  acc = block_sum(acc, red);
+  if (threadIdx.x == 0) loss[h] = acc / (double)nrows;
+}
+
+// Adam as torch.optim.Adam (betas 0.9, 0.999, eps 1e-8, no weight decay): m <- m + (1 - b1)(g - m),
+// v <- b2 v + (1 - b2) g^2, A <- A - (lr / (1 - b1^t)) m / (sqrt(v) / sqrt(1 - b2^t) + eps).
+__global__ __launch_bounds__(256) void cal_adam_kernel(double* A, const double* g, double* m, double* v, int n,
+                                                       double step_size, double bc2_sqrt, double lr) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  (void)lr;
+  const double gi = g[i];
+  const double mi = m[i] + (1.0 - 0.9) * (gi - m[i]);
+  const double vi = v[i] * 0.999 + (1.0 - 0.999) * gi * gi;
+  m[i] = mi;
+  v[i] = vi;
+  A[i] -= step_size * mi / (sqrt(vi) / bc2_sqrt + 1e-8);
+}
+
+__global__ __launch_bounds__(1024) void cal_select_kernel(const double* A, const double* loss, double* best,
+                                                          double* A_best) {
+  const int h = blockIdx.x;
+  const bool take = loss[h] < best[h];
+  __syncthreads();  // every thread has read best[h] before thread 0 may replace it
+  if (!take) return;
+  for (int e = threadIdx.x; e < kMat; e += blockDim.x) A_best[(size_t)h * kMat + e] = A[(size_t)h * kMat + e];
+  if (threadIdx.x == 0) best[h] = loss[h];
+}
+
+__global__ __launch_bounds__(64) void cal_record_kernel(const double* __restrict__ loss, double* __restrict__ dst,
+                                                        int stride, int H) {
+  const int h = threadIdx.x;
+  if (h < H) dst[(size_t)h * stride] = loss[h];
+}
+
+__global__ __launch_bounds__(256) void cal_fill_kernel(double* p, size_t n, double v) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+__global__ __launch_bounds__(256) void cal_to_f32_kernel(const double* __restrict__ src, float* __restrict__ dst,
+                                                         size_t n) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = (float)src[i];
+}
+
+// W_{O,j}^T W_{O,j}: block (query head j, row a), thread = column b.
+__global__ __launch_bounds__(128) void cal_gram_kernel(const uint16_t* __restrict__ W, int dm, int Hq,
+                                                       double* __restrict__ gram) {
+  const int j = blockIdx.x, a = blockIdx.y, b = threadIdx.x;
+  const size_t ld = (size_t)Hq * kD;
+  double acc = 0.0;
+  for (int r = 0; r < dm; ++r) {
+    const uint16_t* wr = W + (size_t)r * ld + (size_t)j * kD;
+    acc = fma(bf16d(wr[a]), bf16d(wr[b]), acc);
+  }
+  gram[((size_t)j * kD + a) * kD + b] = acc;
+}
+
+// Per-channel mean of the keys: block = KV head, thread = channel (sequential fp64 sum).
+__global__ __launch_bounds__(128) void cal_key_mean_kernel(const uint16_t* __restrict__ k, int T, int H,
+                                                           float* __restrict__ mu) {
+  const int h = blockIdx.x, col = threadIdx.x;
+  double acc = 0.0;
+  for (int s = 0; s < T; ++s) acc += bf16d(k[((size_t)s * H + h) * kD + col]);
+  mu[h * kD + col] = (float)(acc / (double)T);
+}
+
+size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
+
+}  // namespace
+
+size_t cal_set_bytes(int T, int nseq, int nrows, long long pelems, int H) {
+  const size_t rows = (size_t)T * H * kD;
+  return up256(sizeof(CalSeq) * (size_t)nseq) + up256(sizeof(int) * (size_t)nrows) + 4 * up256(rows * 8) +
+         up256(rows) + up256((size_t)H * pelems * 8) + up256((size_t)H * nrows * kD * 8) + up256((size_t)H * nrows * 8);
+}
+
+size_t cal_shared_bytes(int H, int Hq) {
+  return up256((size_t)Hq * kMat * 8) + 2 * up256((size_t)H * kMat * 8) + up256((size_t)H * kCalScratch * kMat * 8) +
+         up256((size_t)kCalSplit * H * kMat * 8) + up256((size_t)H * kMat * 8);
+}
+
+hipError_t cal_bind_set(CalSet& set, uint8_t* base, const uint16_t* k, const uint16_t* v, const uint16_t* q,
+                        const int32_t* starts_host, int nseq, int H, int gq, int n_last, hipStream_t s) {
+  std::vector<CalSeq> seqs(nseq);
+  std::vector<int> row_seq;
+  long long pel = 0;
+  int rows = 0;
+  for (int i = 0; i < nseq; ++i) {
+    CalSeq& c = seqs[i];
+    c.start = starts_host[i];
+    c.len = starts_host[i + 1] - starts_host[i];
+    c.t0 = c.len > n_last ? c.len - n_last : 0;
+    c.row0 = rows;
+    c.p0 = pel;
+    const int nr = (c.len - c.t0) * gq;
+    for (int r = 0; r < nr; ++r) row_seq.push_back(i);
+    rows += nr;
+    pel += (long long)nr * c.len;
+  }
+  set.k = k;
+  set.v = v;
+  set.q = q;
+  set.T = starts_host[nseq] - starts_host[0];
+  set.nseq = nseq;
+  set.nrows = rows;
+  set.pelems = pel;
+  const size_t nrow_el = (size_t)set.T * H * kD;
+  uint8_t* p = base;
+  set.seqs = reinterpret_cast<CalSeq*>(p);
+  p += up256(sizeof(CalSeq) * (size_t)nseq);
+  set.row_seq = reinterpret_cast<int*>(p);
+  p += up256(sizeof(int) * (size_t)rows);
+  set.zhat = reinterpret_cast<double*>(p);
+  p += up256(nrow_el * 8);
+  set.xeff = reinterpret_cast<double*>(p);
+  p += up256(nrow_el * 8);
+  set.gx = reinterpret_cast<double*>(p);
+  p += up256(nrow_el * 8);
+  set.gz = reinterpret_cast<double*>(p);
+  p += up256(nrow_el * 8);
+  set.mask = p;
+  p += up256(nrow_el);
+  set.pd = reinterpret_cast<double*>(p);
+  p += up256((size_t)H * pel * 8);
+  set.wrow = reinterpret_cast<double*>(p);
+  p += up256((size_t)H * rows * kD * 8);
+  set.lrow = reinterpret_cast<double*>(p);
+  hipError_t e = hipMemcpyAsync(set.seqs, seqs.data(), sizeof(CalSeq) * nseq, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && rows > 0)
+    e = hipMemcpyAsync(set.row_seq, row_seq.data(), sizeof(int) * rows, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);  // the host tables go out of scope
+  return e;
+}
+
+void cal_bind_shared(CalCfg& c, uint8_t* base) {
+  uint8_t* p = base;
+  c.gram = reinterpret_cast<double*>(p);
+  p += up256((size_t)c.Hq * kMat * 8);
+  c.R = reinterpret_cast<double*>(p);
+  p += up256((size_t)c.H * kMat * 8);
+  c.Rt = reinterpret_cast<double*>(p);
+  p += up256((size_t)c.H * kMat * 8);
+  c.ex = reinterpret_cast<double*>(p);
+  p += up256((size_t)c.H * kCalScratch * kMat * 8);
+  c.drp = reinterpret_cast<double*>(p);
+  p += up256((size_t)kCalSplit * c.H * kMat * 8);
+  c.dr = reinterpret_cast<double*>(p);
+}
+
+hipError_t cal_gram(const CalCfg& c, const uint16_t* W_o, hipStream_t s) {
+  hipLaunchKernelGGL(cal_gram_kernel, dim3(c.Hq, kD), dim3(kD), 0, s, W_o, c.dm, c.Hq, c.gram);
+  return hipGetLastError();
+}
+
+static void rot_and_quant(const CalCfg& c, CalSet& set, const double* A, int value, hipStream_t s) {
+  hipLaunchKernelGGL(cal_expm_kernel, dim3(c.H), dim3(kExpThreads), 0, s, c, A, value);
+  if (set.T > 0)
+    hipLaunchKernelGGL(cal_rotq_kernel, dim3((set.T + kRotTile - 1) / kRotTile, c.H), dim3(kD), 0, s, set, c, value);
+}
+
+static void backward(const CalCfg& c, CalSet& set, const double* A, int value, double* grad, hipStream_t s) {
+  if (set.T > 0) {
+    hipLaunchKernelGGL(cal_gx_kernel, dim3(set.T, c.H), dim3(kD), 0, s, set, c, value);
+    hipLaunchKernelGGL(cal_gz_kernel, dim3((set.T + kRotTile - 1) / kRotTile, c.H), dim3(kD), 0, s, set, c);
+    hipLaunchKernelGGL(cal_dr_kernel, dim3(kD / 16, c.H, kCalSplit), dim3(kD), 0, s, set, c, value);
+  } else {
+    hipLaunchKernelGGL(cal_fill_kernel, dim3((unsigned)((kCalSplit * (size_t)c.H * kMat + 255) / 256)), dim3(256), 0,
+                       s, c.drp, kCalSplit * (size_t)c.H * kMat, 0.0);
+  }
+  hipLaunchKernelGGL(cal_dr_reduce_kernel, dim3((unsigned)(((size_t)c.H * kMat + 255) / 256)), dim3(256), 0, s, c);
+  hipLaunchKernelGGL(cal_expm_grad_kernel, dim3(c.H), dim3(kExpThreads), 0, s, c, A, value, grad);
+}
+
+hipError_t cal_key_loss(const CalCfg& c, CalSet& set, const double* A, double* loss, double* grad, hipStream_t s) {
+  rot_and_quant(c, set, A, 0, s);
+  if (set.nrows > 0) {
+    hipLaunchKernelGGL(cal_attn_kernel, dim3(set.nrows, c.H), dim3(256), 0, s, set, c, 0);
+    hipLaunchKernelGGL(cal_loss_kernel, dim3(c.H), dim3(256), 0, s, set.lrow, set.nrows, loss);
+  } else {
+    hipLaunchKernelGGL(cal_fill_kernel, dim3(1), dim3(256), 0, s, loss, (size_t)c.H, 0.0);
+  }
+  if (grad) {
+    if (set.nrows == 0) {
+      hipLaunchKernelGGL(cal_fill_kernel, dim3((unsigned)(((size_t)c.H * kMat + 255) / 256)), dim3(256), 0, s, grad,
+                         (size_t)c.H * kMat, 0.0);
+      return hipGetLastError();
+    }
+    backward(c, set, A, 0, grad, s);
+  }
+  return hipGetLastError();
+}
+
+hipError_t cal_key_probs(const CalCfg& c, CalSet& set, const double* A, hipStream_t s) {
+  rot_and_quant(c, set, A, 0, s);
+  if (set.nrows > 0) hipLaunchKernelGGL(cal_attn_kernel, dim3(set.nrows, c.H), dim3(256), 0, s, set, c, 1);
+  return hipGetLastError();
+}
+
+hipError_t cal_value_loss(const CalCfg& c, CalSet& set, const double* A, double* loss, double* grad, hipStream_t s) {
+  rot_and_quant(c, set, A, 1, s);
+  if (set.nrows > 0) {
+    hipLaunchKernelGGL(cal_vrow_kernel, dim3(set.nrows, c.H), dim3(kD), 0, s, set, c);
+    hipLaunchKernelGGL(cal_loss_kernel, dim3(c.H), dim3(256), 0, s, set.lrow, set.nrows, loss);
+  } else {
+    hipLaunchKernelGGL(cal_fill_kernel, dim3(1), dim3(256), 0, s, loss, (size_t)c.H, 0.0);
+  }
+  if (grad) {
+    if (set.nrows == 0) {
+      hipLaunchKernelGGL(cal_fill_kernel, dim3((unsigned)(((size_t)c.H * kMat + 255) / 256)), dim3(256), 0, s, grad,
+                         (size_t)c.H * kMat, 0.0);
+      return hipGetLastError();
+    }
+    backward(c, set, A, 1, grad, s);
+  }
+  return hipGetLastError();
+}
+
+hipError_t cal_adam(double* A, const double* g, double* m, double* v, int n, int step, double lr, hipStream_t s) {
+  const double bc1 = 1.0 - pow(0.9, (double)step), bc2 = 1.0 - pow(0.999, (double)step);
+  hipLaunchKernelGGL(cal_adam_kernel, dim3((n + 255) / 256), dim3(256), 0, s, A, g, m, v, n, lr / bc1, sqrt(bc2), lr);
+  return hipGetLastError();
+}
+
+hipError_t cal_select(const double* A, const double* loss, double* best, double* A_best, int H, hipStream_t s) {
+  hipLaunchKernelGGL(cal_select_kernel, dim3(H), dim3(1024), 0, s, A, loss, best, A_best);
+  return hipGetLastError();
+}
+
+hipError_t cal_record(const double* loss, double* dst, int stride, int H, hipStream_t s) {
+  for (int h0 = 0; h0 < H; h0 += 64)
+    hipLaunchKernelGGL(cal_record_kernel, dim3(1), dim3(64), 0, s, loss + h0, dst + (size_t)h0 * stride, stride,
+                       min(64, H - h0));
+  return hipGetLastError();
+}
+
+hipError_t cal_fill(double* p, size_t n, double v, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(cal_fill_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t cal_rotation_out(const CalCfg& c, const double* A, bool value, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(cal_expm_kernel, dim3(c.H), dim3(kExpThreads), 0, s, c, A, value ? 1 : 0);
+  const size_t n = (size_t)c.H * kMat;
+  hipLaunchKernelGGL(cal_to_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, c.R, out, n);
+  return hipGetLastError();
+}
+
+hipError_t cal_key_mean(const uint16_t* k, int T, int H, float* mu, hipStream_t s) {
+  hipLaunchKernelGGL(cal_key_mean_kernel, dim3(H), dim3(kD), 0, s, k, T, H, mu);
+  return hipGetLastError();
+}
+
+}  // namespace int2kv

@@ -43,12 +43,27 @@ EXPORTED = (
     "int2kv_decode_window",
     "int2kv_set_decode_tuning", "int2kv_set_decode_events", "int2kv_quantize_append_error",
     "int2kv_output_error_workspace_bytes", "int2kv_output_error", "int2kv_quantize_append_rope",
+    "int2kv_optr_workspace_bytes", "int2kv_optr_key_mean", "int2kv_optr_key_loss", "int2kv_optr_value_loss",
+    "int2kv_optr_calibrate",
 )
 
 
 class _Cache(ctypes.Structure):
     _fields_ = [("pool", ctypes.c_void_p), ("num_blocks", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("block_size", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("group_size", ctypes.c_int32)]
+
+
+class _OptrTraces(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("q", ctypes.c_void_p),
+                ("seq_starts", ctypes.POINTER(ctypes.c_int32)), ("num_seqs", ctypes.c_int32)]
+
+
+class _OptrConfig(ctypes.Structure):
+    _fields_ = [("num_kv_heads", ctypes.c_int32), ("num_q_heads", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("group_size", ctypes.c_int32), ("clip_k", ctypes.c_float), ("clip_v", ctypes.c_float),
+                ("lambda_k", ctypes.c_double), ("n_last", ctypes.c_int32), ("sink", ctypes.c_int32),
+                ("recent", ctypes.c_int32), ("steps", ctypes.c_int32), ("eval_every", ctypes.c_int32),
+                ("lr", ctypes.c_double)]
 
 
 _lib = None
@@ -87,6 +102,15 @@ def load_library(path: str = LIB_PATH):
         "int2kv_set_decode_tuning": ([I, I], I),
         "int2kv_quantize_append_error": ([ctypes.POINTER(_Cache), P, P, P, I, P, P, P, F, F, P, S], I),
         "int2kv_output_error_workspace_bytes": ([I, I, I, I, I], Z),
+        "int2kv_optr_workspace_bytes": ([ctypes.POINTER(_OptrConfig), ctypes.POINTER(_OptrTraces),
+                                         ctypes.POINTER(_OptrTraces)], Z),
+        "int2kv_optr_key_mean": ([P, I, I, P, S], I),
+        "int2kv_optr_key_loss": ([ctypes.POINTER(_OptrConfig), ctypes.POINTER(_OptrTraces), P, P, P, P, P, P, P, Z, S],
+                                 I),
+        "int2kv_optr_value_loss": ([ctypes.POINTER(_OptrConfig), ctypes.POINTER(_OptrTraces), P, P, P, P, P, P, P, P,
+                                    P, Z, S], I),
+        "int2kv_optr_calibrate": ([ctypes.POINTER(_OptrConfig), ctypes.POINTER(_OptrTraces),
+                                   ctypes.POINTER(_OptrTraces), P, P, P, P, P, P, P, P, P, P, Z, S], I),
         "int2kv_quantize_append_rope": ([ctypes.POINTER(_Cache), P, P, P, P, I, P, I, P, P, P, F, F, I, P, S], I),
         "int2kv_output_error": ([ctypes.POINTER(_Cache), P, I, I, P, I, P, I, P, P, P, P, I, P, I, P, P, P, Z, S],
                                 I),
@@ -476,3 +500,99 @@ def hadamard_rotation(num_heads: int, device="cuda") -> torch.Tensor:
     scale = torch.tensor(1.0 / math.sqrt(HEAD_DIM), dtype=torch.float32)
     H = torch.where(par == 1, -scale, scale)
     return H[None].expand(num_heads, HEAD_DIM, HEAD_DIM).contiguous().to(device)
+
+
+# ---------------------------------------------------------------------------------------------
+# OptR offline calibration
+_F64 = (torch.float64,)
+
+
+class OptrTraces:
+    """Calibration traces on the device: k, v bf16 [T, H_kv, 128], q bf16 [T, H_q, 128], and the
+    sequences' token offsets (host int32 [N + 1], starting at 0)."""
+
+    def __init__(self, k: torch.Tensor, v: torch.Tensor, q: torch.Tensor, seq_starts):
+        import numpy as np
+        self.k, self.v, self.q = k, v, q
+        self._starts = np.ascontiguousarray(np.asarray(seq_starts, dtype=np.int32))
+        if self._starts[-1] != k.shape[0] or v.shape != k.shape or q.shape[0] != k.shape[0]:
+            raise ValueError("k, v, q must hold seq_starts[-1] tokens")
+        self.desc = _OptrTraces(_ptr(k, _BF16, "k"), _ptr(v, _BF16, "v"), _ptr(q, _BF16, "q"),
+                                self._starts.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), len(self._starts) - 1)
+
+
+def optr_config(num_kv_heads: int, num_q_heads: int, d_model: int, group_size: int = 128, clip_k: float = 0.96,
+                clip_v: float = 0.92, lambda_k: float = 1.0, n_last: int = 64, sink: int = 64, recent: int = 256,
+                steps: int = 80, eval_every: int = 20, lr: float = 0.02):
+    """Calibration settings (defaults: the paper's)."""
+    return _OptrConfig(num_kv_heads, num_q_heads, d_model, group_size, clip_k, clip_v, lambda_k, n_last, sink,
+                       recent, steps, eval_every, lr)
+
+
+def int2kv_optr_workspace_bytes(cfg, calib: OptrTraces, heldout: Optional[OptrTraces] = None) -> int:
+    n = load_library().int2kv_optr_workspace_bytes(ctypes.byref(cfg), ctypes.byref(calib.desc),
+                                                   ctypes.byref(heldout.desc) if heldout else None)
+    if n == 0:
+        raise ValueError("int2kv_optr_workspace_bytes: " + (load_library().int2kv_last_error() or b"").decode())
+    return n
+
+
+def _workspace(n, device):
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def int2kv_optr_key_mean(k: torch.Tensor) -> torch.Tensor:
+    T, H = k.shape[0], k.shape[1]
+    mu = torch.empty((H, HEAD_DIM), dtype=torch.float32, device=k.device)
+    _check(load_library().int2kv_optr_key_mean(_ptr(k, _BF16, "k"), T, H, _ptr(mu, _F32, "mu"), _stream()),
+           "int2kv_optr_key_mean")
+    return mu
+
+
+def int2kv_optr_key_loss(cfg, traces: OptrTraces, R0_k, mu, W_o, A, want_grad: bool = True):
+    """(loss [H] fp64, grad [H, 128, 128] fp64 or None) of the key objective at generators A."""
+    H = cfg.num_kv_heads
+    loss = torch.empty(H, dtype=torch.float64, device=A.device)
+    grad = torch.empty((H, HEAD_DIM, HEAD_DIM), dtype=torch.float64, device=A.device) if want_grad else None
+    n = int2kv_optr_workspace_bytes(cfg, traces)
+    ws = _workspace(n, A.device)
+    _check(load_library().int2kv_optr_key_loss(
+        ctypes.byref(cfg), ctypes.byref(traces.desc), _ptr(R0_k, _F32, "R0_k"), _ptr(mu, _F32, "mu"),
+        _ptr(W_o, _BF16, "W_o"), _ptr(A, _F64, "A"), _ptr(loss, _F64, "loss"), _ptr(grad, _F64, "grad"),
+        _ptr(ws, (torch.uint8,), "ws"), n, _stream()), "int2kv_optr_key_loss")
+    return loss, grad
+
+
+def int2kv_optr_value_loss(cfg, traces: OptrTraces, R0_k, A_k, mu, R0_v, W_o, A_v, want_grad: bool = True):
+    H = cfg.num_kv_heads
+    loss = torch.empty(H, dtype=torch.float64, device=A_v.device)
+    grad = torch.empty((H, HEAD_DIM, HEAD_DIM), dtype=torch.float64, device=A_v.device) if want_grad else None
+    n = int2kv_optr_workspace_bytes(cfg, traces)
+    ws = _workspace(n, A_v.device)
+    _check(load_library().int2kv_optr_value_loss(
+        ctypes.byref(cfg), ctypes.byref(traces.desc), _ptr(R0_k, _F32, "R0_k"), _ptr(A_k, _F64, "A_k"),
+        _ptr(mu, _F32, "mu"), _ptr(R0_v, _F32, "R0_v"), _ptr(W_o, _BF16, "W_o"), _ptr(A_v, _F64, "A_v"),
+        _ptr(loss, _F64, "loss"), _ptr(grad, _F64, "grad"), _ptr(ws, (torch.uint8,), "ws"), n, _stream()),
+        "int2kv_optr_value_loss")
+    return loss, grad
+
+
+def int2kv_optr_calibrate(cfg, calib: OptrTraces, heldout: OptrTraces, R0_k, R0_v, mu, W_o,
+                          workspace: Optional[torch.Tensor] = None):
+    """Algorithm 1 for every KV head: returns dict(R_k, R_v (fp32), A_k, A_v (fp64), history (fp64
+    [2, H, steps + 1 + steps // eval_every]))."""
+    H = cfg.num_kv_heads
+    dev = R0_k.device
+    R_k = torch.empty((H, HEAD_DIM, HEAD_DIM), dtype=torch.float32, device=dev)
+    R_v = torch.empty_like(R_k)
+    A_k = torch.empty((H, HEAD_DIM, HEAD_DIM), dtype=torch.float64, device=dev)
+    A_v = torch.empty_like(A_k)
+    hist = torch.empty((2, H, cfg.steps + 1 + cfg.steps // cfg.eval_every), dtype=torch.float64, device=dev)
+    n = int2kv_optr_workspace_bytes(cfg, calib, heldout)
+    ws = workspace if workspace is not None else _workspace(n, dev)
+    _check(load_library().int2kv_optr_calibrate(
+        ctypes.byref(cfg), ctypes.byref(calib.desc), ctypes.byref(heldout.desc), _ptr(R0_k, _F32, "R0_k"),
+        _ptr(R0_v, _F32, "R0_v"), _ptr(mu, _F32, "mu"), _ptr(W_o, _BF16, "W_o"), _ptr(R_k, _F32, "R_k"),
+        _ptr(R_v, _F32, "R_v"), _ptr(A_k, _F64, "A_k"), _ptr(A_v, _F64, "A_v"), _ptr(hist, _F64, "history"),
+        _ptr(ws, (torch.uint8,), "ws"), ws.numel(), _stream()), "int2kv_optr_calibrate")
+    return dict(R_k=R_k, R_v=R_v, A_k=A_k, A_v=A_v, history=hist)

@@ -161,3 +161,24 @@ def test_rope_write_rejects_bad_arguments_without_launch():
     assert call(p, p, p, p, 0, 0) == K.INT2KV_EINVAL                            # empty table
     assert call(p, p, None, None, 0, 0, k_out=p) == K.INT2KV_EINVAL             # k_rope_out without RoPE
     assert call(p, p, p, p + 4, 16, 0) == K.INT2KV_EINVAL                       # misaligned table
+
+
+def test_optr_workspace_query_validates_on_the_host():
+    """int2kv_optr_workspace_bytes reads only the host tables: 0 for bad settings or sequences,
+    a positive size otherwise (the device pointers are stand-ins, never dereferenced)."""
+    import numpy as np
+    lib = K.load_library()
+    starts = np.array([0, 100, 250], np.int32)
+    tr = K._OptrTraces(1 << 20, 1 << 20, 1 << 20, starts.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), 2)
+    cfg = K.optr_config(2, 8, 64)
+    assert lib.int2kv_optr_workspace_bytes(ctypes.byref(cfg), ctypes.byref(tr), None) > 0
+    assert lib.int2kv_optr_workspace_bytes(ctypes.byref(cfg), ctypes.byref(tr), ctypes.byref(tr)) > \
+        lib.int2kv_optr_workspace_bytes(ctypes.byref(cfg), ctypes.byref(tr), None)
+    for bad in (K.optr_config(2, 7, 64), K.optr_config(2, 8, 64, group_size=64), K.optr_config(2, 8, 64, clip_k=0.0),
+                K.optr_config(2, 8, 64, n_last=0), K.optr_config(2, 8, 64, eval_every=0),
+                K.optr_config(2, 8, 64, lr=0.0)):
+        assert lib.int2kv_optr_workspace_bytes(ctypes.byref(bad), ctypes.byref(tr), None) == 0
+    long_starts = np.array([0, 5000], np.int32)  # a sequence beyond 4096 tokens
+    tr2 = K._OptrTraces(1 << 20, 1 << 20, 1 << 20, long_starts.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), 1)
+    assert lib.int2kv_optr_workspace_bytes(ctypes.byref(cfg), ctypes.byref(tr2), None) == 0
+    assert b"4096" in lib.int2kv_last_error()

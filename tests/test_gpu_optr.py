@@ -1,0 +1,126 @@
+"""GPU parity of the OptR calibration (Sec. 4.2 - 4.5, Algorithm 1) against the CPU oracle: the key
+mean, both objectives and their gradients at several generators (group sizes 32 / 128, clipped
+and unclipped, with and without BF16 windows), and a short calibration run step by step.
+
+Both sides compute in fp64 and quantize the fp32 rounding of the rotated rows with the same
+quantizer, so codes agree unless a rotated value sits within an fp64 rounding of an fp32 rounding
+boundary; the objectives then agree to summation-order error (about 1e-13 relative), bounded
+here by LOSS_RTOL, and the gradients (by hand on the GPU, by automatic differentiation in the
+oracle) to GRAD_RTOL in norm."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import optr_oracle as P
+from paper_2608_02691_amd import int2kv as K
+from paper_2608_02691_amd import workloads as W
+
+from _helpers import dev
+
+pytestmark = pytest.mark.gpu
+
+LOSS_RTOL = 1e-9
+GRAD_RTOL = 1e-7
+
+
+def _structured(lens, seed, H=2, Hq=8):
+    """Traces with four high-variance channels (std 8) in keys, values and queries."""
+    rng = np.random.default_rng(seed)
+    T = sum(lens)
+    scale = np.ones(128)
+    scale[[3, 50, 77, 100]] = 8.0
+    f = lambda x: W.f32_to_bf16_bits(x.astype(np.float32))
+    k = f(rng.standard_normal((T, H, 128)) * scale + 2.0)
+    v = f(rng.standard_normal((T, H, 128)) * scale[::-1])
+    q = f(rng.standard_normal((T, Hq, 128)) * scale * 0.3)
+    return k, v, q, np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+
+
+def _traces(data):
+    k, v, q, st = data
+    return K.OptrTraces(dev(k), dev(v), dev(q), st)
+
+
+def _setup(R0_identity=False):
+    w = W.make_workload(1, batch=1, ctx=16, num_q_heads=8, num_kv_heads=2, d_model=96)
+    R0k = np.broadcast_to(np.eye(128, dtype=np.float32), (2, 128, 128)).copy() if R0_identity else w.R_k
+    R0v = np.broadcast_to(np.eye(128, dtype=np.float32), (2, 128, 128)).copy() if R0_identity else w.R_v
+    return w, R0k, R0v
+
+
+def test_key_mean_matches_oracle():
+    k, _, _, _ = _structured([300, 211], 1)
+    got = K.int2kv_optr_key_mean(dev(k)).cpu().numpy()
+    ref = P.key_mean(k)
+    # both round an fp64 mean to fp32; summation orders differ by far less than an fp32 ulp
+    ulp = np.abs(got.view(np.int32).astype(np.int64) - ref.view(np.int32).astype(np.int64))
+    assert ulp.max() <= 1
+
+
+CASES = [  # (group, clip_k, clip_v, sink, recent, R0 identity)
+    (32, 1.0, 1.0, 0, 0, False),
+    (32, 0.96, 0.92, 4, 16, True),
+    (128, 0.96, 0.92, 0, 0, False),
+    (128, 1.0, 1.0, 8, 24, True),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"G{c[0]}-clip{c[1]}-win{c[3]}+{c[4]}-eye{int(c[5])}")
+def test_objectives_and_gradients_match_oracle(case):
+    G, ck, cv, sink, recent, eye = case
+    print(f"\n[optr loss] {case}", flush=True)
+    w, R0k, R0v = _setup(eye)
+    data = _structured([130, 77, 45], 2)
+    k, v, q, st = data
+    tr = _traces(data)
+    mu = P.key_mean(k)
+    cfg = K.optr_config(2, 8, 96, group_size=G, clip_k=ck, clip_v=cv, lambda_k=0.7, n_last=20, sink=sink,
+                        recent=recent)
+    rng = np.random.default_rng(3)
+    for scale in (0.0, 0.02):
+        A = rng.standard_normal((2, 128, 128)) * scale
+        Av = rng.standard_normal((2, 128, 128)) * scale
+        lk, gk = K.int2kv_optr_key_loss(cfg, tr, dev(R0k), dev(mu), dev(w.W_o), dev(A))
+        lv, gv = K.int2kv_optr_value_loss(cfg, tr, dev(R0k), dev(A), dev(mu), dev(R0v), dev(w.W_o), dev(Av))
+        lk, gk, lv, gv = (x.cpu().numpy() for x in (lk, gk, lv, gv))
+        for h in range(2):
+            kw = dict(group=G, n_last=20, sink=sink, recent=recent)
+            At = torch.from_numpy(A[h].copy()).requires_grad_(True)
+            L = P.key_loss(At, R0k, k, v, q, st, mu, w.W_o, h, 4, lam=0.7, clip=ck, **kw)
+            L.backward()
+            assert abs(lk[h] - float(L)) <= LOSS_RTOL * abs(float(L)), (h, lk[h], float(L))
+            g = At.grad.numpy()
+            assert np.linalg.norm(gk[h] - g) <= GRAD_RTOL * np.linalg.norm(g), (h, np.linalg.norm(gk[h] - g))
+            probs = P.key_probs(R0k, A[h], k, q, st, mu, h, 4, clip=ck, **kw)
+            Bt = torch.from_numpy(Av[h].copy()).requires_grad_(True)
+            Lv = P.value_loss(Bt, R0v, v, st, probs, w.W_o, h, 4, clip=cv, **kw)
+            Lv.backward()
+            assert abs(lv[h] - float(Lv)) <= LOSS_RTOL * abs(float(Lv)), (h, lv[h], float(Lv))
+            gvr = Bt.grad.numpy()
+            assert np.linalg.norm(gv[h] - gvr) <= GRAD_RTOL * np.linalg.norm(gvr)
+        print(f"scale {scale}: key loss {lk}, value loss {lv}", flush=True)
+
+
+def test_calibration_matches_oracle_step_by_step():
+    """Algorithm 1, 10 steps with held-out evaluation every 5: the training and held-out objectives
+    of every step, and the selected rotations, against the oracle run per head."""
+    print("\n[optr calibrate]", flush=True)
+    w, R0k, R0v = _setup(True)
+    calib, held = _structured([150, 120], 7), _structured([140, 130], 8)
+    mu = P.key_mean(calib[0])
+    cfg = K.optr_config(2, 8, 96, group_size=32, clip_k=0.96, clip_v=0.92, lambda_k=1.0, n_last=16, sink=4,
+                        recent=16, steps=10, eval_every=5, lr=0.02)
+    out = K.int2kv_optr_calibrate(cfg, _traces(calib), _traces(held), dev(R0k), dev(R0v), dev(mu), dev(w.W_o))
+    hist = out["history"].cpu().numpy()
+    for h in range(2):
+        ref = P.calibrate_head(R0k, R0v, calib, held, mu, w.W_o, h, 4, lam=1.0, clip_k=0.96, clip_v=0.92, group=32,
+                               n_last=16, sink=4, recent=16, steps=10, lr=0.02, eval_every=5)
+        for phase, curve, heldv in ((0, ref["key_curve"], ref["heldout_k"]), (1, ref["value_curve"], ref["heldout_v"])):
+            got = hist[phase, h]
+            np.testing.assert_allclose(got[:10], curve, rtol=1e-7)
+            np.testing.assert_allclose(got[10:], heldv, rtol=1e-7)
+        np.testing.assert_allclose(out["A_k"][h].cpu().numpy(), ref["A_k"], rtol=0, atol=1e-9)
+        np.testing.assert_allclose(out["A_v"][h].cpu().numpy(), ref["A_v"], rtol=0, atol=1e-9)
+        np.testing.assert_allclose(out["R_k"][h].cpu().numpy(), ref["R_k"].astype(np.float32), rtol=0, atol=2e-7)
+        np.testing.assert_allclose(out["R_v"][h].cpu().numpy(), ref["R_v"].astype(np.float32), rtol=0, atol=2e-7)
+        print(f"head {h}: key {hist[0, h, :3]}..., value {hist[1, h, :3]}...", flush=True)
