@@ -185,6 +185,100 @@ def cpu_baseline_append(w, target_s, group=32):
                       f"({tokens} tokens x {w.num_kv_heads} KV heads, {elapsed:.1f} s, fp64/fp32 numpy)"}
 
 
+def run_calibrate(args):
+    """OptR offline calibration (Algorithm 1) of --layers Qwen3-8B-shaped layers (8 KV heads, 32
+    query heads, d_model 4096 each) at the paper's settings (group 128, clips 0.96 / 0.92, 64 sink
+    and 256 recent BF16 tokens, final 64 query positions, 80 Adam steps per rotation at lr 0.02,
+    held-out selection every 20 steps, lambda_K = 1) on seeded traces: 7 calibration sequences of
+    328..560 tokens and 6 held-out sequences of 400..640 tokens. Every layer's heads are calibrated
+    in the same launches (the KV-head axis spans the layers). One timed unit is one whole
+    calibration."""
+    import torch
+    from paper_2608_02691_amd import int2kv as K
+    from paper_2608_02691_amd import workloads as W
+    torch.cuda.set_device(0)
+    L = args.layers
+    H, Hq, dm = 8 * L, 32 * L, 4096
+    kc, vc, qc, sc = W.calibration_traces(7, (328, 560), H, Hq, seed=1)
+    kh, vh, qh, sh = W.calibration_traces(6, (400, 640), H, Hq, seed=2)
+    calib = K.OptrTraces(kc.cuda(), vc.cuda(), qc.cuda(), sc)
+    held = K.OptrTraces(kh.cuda(), vh.cuda(), qh.cuda(), sh)
+    R0k = torch.from_numpy(W.haar_rotations(H, 3)).cuda()
+    R0v = torch.from_numpy(W.haar_rotations(H, 4)).cuda()
+    g = torch.Generator().manual_seed(5)
+    # each layer's W_O [4096, 32 * 128]: the layers side by side along the columns
+    W_o = (torch.randn((dm, Hq * 128), generator=g) / np.sqrt(dm)).to(torch.bfloat16).cuda()
+    mu = K.int2kv_optr_key_mean(calib.k)
+    cfg = K.optr_config(H, Hq, dm)
+    n_ws = K.int2kv_optr_workspace_bytes(cfg, calib, held)
+    ws = torch.empty(n_ws, dtype=torch.uint8, device="cuda")
+    log(f"calibrate: {L} layers = {H} KV heads, calib {int(sc[-1])} / held-out {int(sh[-1])} tokens, "
+        f"workspace {n_ws / 2**30:.2f} GiB")
+    run = lambda: K.int2kv_optr_calibrate(cfg, calib, held, R0k, R0v, mu, W_o, workspace=ws)
+    warm = max(1, min(args.warmup, 2))
+    steps = max(1, min(args.steps, 5))
+    for _ in range(warm):
+        out = run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        out = run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    hist = out["history"].cpu().numpy()
+    n_ev = 1 + cfg.steps // cfg.eval_every
+    held_k, held_v = hist[0, :, cfg.steps:], hist[1, :, cfg.steps:]
+    sel_k = held_k.min(axis=1) / held_k[:, 0]
+    sel_v = held_v.min(axis=1) / held_v[:, 0]
+    log(f"calibration: {ms:.1f} ms; held-out objective of the selected rotation over the base: keys median "
+        f"{np.median(sel_k):.3f}, values median {np.median(sel_v):.3f}")
+    result = {
+        "metric": "OptR offline calibration (Algorithm 1) throughput, 1 MI355X",
+        "value": H / (ms * 1e-3),
+        "unit": "calibrated KV heads/s",
+        "n_gpus": 1, "steps": steps, "warmup": warm, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64 (bf16 traces, fp32 R0; INT2 quantizer on fp32 rows)",
+        "data": "synthetic (seeded traces; no model weights)",
+        "config": {"workload": f"OptR calibration of {L} Qwen3-8B-shaped layers (8 KV / 32 query heads, d_model 4096)",
+                   "kv_heads": H, "calib_tokens": int(sc[-1]), "heldout_tokens": int(sh[-1]), "group_size": 128,
+                   "clip": [0.96, 0.92], "window": [64, 256], "n_last": 64, "adam_steps": [cfg.steps, cfg.steps],
+                   "lr": cfg.lr, "eval_every": cfg.eval_every, "lambda_k": cfg.lambda_k},
+        "selection": {"heldout_key_ratio_median": float(np.median(sel_k)),
+                      "heldout_value_ratio_median": float(np.median(sel_v)),
+                      "what": "held-out objective of the selected rotation over that of the base rotation R0"},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline_calibrate(kc, vc, qc, sc, kh, vh, qh, sh, R0k.cpu().numpy(),
+                                                        R0v.cpu().numpy(), mu.cpu().numpy(), W_o, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline_calibrate(kc, vc, qc, sc, kh, vh, qh, sh, R0k, R0v, mu, W_o, target_s):
+    """The oracle's calibration of KV head 0 (its own 4 query heads and its W_O columns), with the
+    steps cut to fit the time budget; scaled to whole calibrations (80 + 80 steps) per second."""
+    from oracle import optr_oracle as P
+    import torch
+    bits = lambda t: t.view(torch.int16).numpy().view(np.uint16)
+    c0 = (bits(kc[:, :1]), bits(vc[:, :1]), bits(qc[:, :4]), sc)
+    h0 = (bits(kh[:, :1]), bits(vh[:, :1]), bits(qh[:, :4]), sh)
+    Wo = bits(W_o[:, :4 * 128].cpu().contiguous())
+    t0 = time.perf_counter()
+    steps = 2
+    P.calibrate_head(R0k[:1], R0v[:1], c0, h0, mu[:1], Wo, 0, 4, lam=1.0, clip_k=0.96, clip_v=0.92, group=128,
+                     n_last=64, sink=64, recent=256, steps=steps, lr=0.02, eval_every=steps)
+    el = time.perf_counter() - t0
+    # one oracle step (loss + gradient) costs about one held-out evaluation plus its backward; scale
+    # the 2 + 2 steps and 2 + 2 evaluations measured to 80 + 80 steps and 5 + 5 evaluations
+    per_head = el * (160 + 10) / (2 * steps + 4)
+    log(f"cpu oracle: {2 * steps} calibration steps of one KV head in {el:.1f} s -> {per_head:.1f} s per head")
+    return {"value": 1.0 / per_head, "unit": "calibrated KV heads/s", "cores": blas_threads(), "kind": "oracle",
+            "host_cpus": os.cpu_count(), "cpu_model": cpu_model(),
+            "sample": f"oracle calibrate_head of KV head 0 with {steps} + {steps} steps and {2 + 2} held-out "
+                      f"evaluations ({el:.1f} s, fp64 torch), scaled to 80 + 80 steps and 5 + 5 evaluations"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -192,11 +286,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--config", type=int, default=None,
                     help="workload configuration (default 4; 1 with --mode outerr)")
-    ap.add_argument("--mode", choices=("decode", "append", "outerr"), default="decode",
+    ap.add_argument("--layers", type=int, default=36,
+                    help="calibrate mode: decoder layers calibrated at once (8 KV heads each)")
+    ap.add_argument("--mode", choices=("decode", "append", "outerr", "calibrate"), default="decode",
                     help="decode: one decode step (default); append: the cache write of every token of the "
                          "workload in one int2kv_quantize_append call (configuration 3's prefill-sized append); "
                          "outerr: one int2kv_output_error call (key- and value-induced output errors against the "
-                         "full-precision rows)")
+                         "full-precision rows); calibrate: OptR's offline calibration (Algorithm 1) of --layers "
+                         "Qwen3-8B-shaped layers on synthetic traces")
     ap.add_argument("--rope", action="store_true",
                     help="append mode: the keys enter pre-RoPE and the write applies RoPE at each token's position "
                          "(int2kv_quantize_append_rope, fp32 cos/sin table of theta 1e6)")
@@ -257,6 +354,9 @@ def main():
             dst_t.copy_(src_t)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes_read": n, "bytes_written": n, "launches": 3}), flush=True)
+        return
+    if args.mode == "calibrate":
+        run_calibrate(args)
         return
     if args.config is None:
         args.config = 1 if args.mode == "outerr" else 4

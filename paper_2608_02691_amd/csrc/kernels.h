@@ -147,6 +147,7 @@ struct CalSeq {
 struct CalSet {
   const uint16_t *k, *v, *q;       // bf16 [T, H, 128], [T, H, 128], [T, Hq, 128]
   int T, nseq, nrows;              // nrows: query rows of one KV head
+  int maxlen;                      // longest sequence
   long long pelems;                // per KV head: sum over sequences of rows * len
   CalSeq* seqs;                    // [nseq]
   int* row_seq;                    // [nrows]: sequence of each row

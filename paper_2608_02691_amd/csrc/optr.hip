@@ -151,7 +151,10 @@ __global__ __launch_bounds__(128) void cal_rotq_kernel(CalSet S, CalCfg c, int v
 // Key objective of one row (t, j) and its logit gradients, or (probs) the key probabilities only.
 // Block (row, KV head) of 256 threads.
 __global__ __launch_bounds__(256) void cal_attn_kernel(CalSet S, CalCfg c, int probs_only) {
-  __shared__ double af[kCalMaxLen], ak[kCalMaxLen], gg[kCalMaxLen];
+  // logits and gradients of the row's tokens: 3 x maxlen doubles of dynamic LDS (sized to the
+  // set's longest sequence, so that several rows share a compute unit)
+  extern __shared__ double cal_dyn[];
+  double *af = cal_dyn, *ak = cal_dyn + S.maxlen, *gg = cal_dyn + 2 * S.maxlen;
   __shared__ double qv[kD], dov[2][kD], uv[kD];
   __shared__ double red[16];
   const int row = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
@@ -274,34 +277,60 @@ __global__ __launch_bounds__(128) void cal_vrow_kernel(CalSet S, CalCfg c) {
 }
 
 // Gradient w.r.t. the effective rows: gx[s] = sum over the rows r of s's sequence of pd[r][s] y_r
-// with y_r = q_r / sqrt(d) (keys) or the row weight (values). Block (token, KV head).
-__global__ __launch_bounds__(128) void cal_gx_kernel(CalSet S, CalCfg c, int value) {
-  const int s = blockIdx.x, h = blockIdx.y, col = threadIdx.x;
-  int lo = 0, hi = S.nseq - 1;  // the sequence holding token s
+// with y_r = q_r / sqrt(d) (keys) or the row weight (values): per sequence the product
+// P^T Y of its [rows x len] weights and [rows x 128] row vectors. Block (32-token tile, KV head)
+// of 256 threads, 16 rows at a time through LDS; thread (token tt, 16 channels).
+constexpr int kGxTok = 32, kGxRows = 16;
+__global__ __launch_bounds__(256) void cal_gx_kernel(CalSet S, CalCfg c, int value) {
+  __shared__ double ps[kGxRows][kGxTok];
+  __shared__ double ys[kGxRows][kD];
+  const int h = blockIdx.y, tid = threadIdx.x, s0 = blockIdx.x * kGxTok;
+  const int tt = tid >> 3, cg = tid & 7;
+  double acc[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.0;
+  int lo = 0, hi = S.nseq - 1;  // the sequence holding token s0
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (S.seqs[mid].start <= s) lo = mid; else hi = mid - 1;
+    if (S.seqs[mid].start <= s0) lo = mid; else hi = mid - 1;
   }
-  const CalSeq sq = S.seqs[lo];
-  const int sl = s - sq.start;
-  double acc = 0.0;
-  if (sl >= 0 && sl < sq.len) {
+  for (int n = lo; n < S.nseq && S.seqs[n].start < s0 + kGxTok; ++n) {
+    const CalSeq sq = S.seqs[n];
     const int nr = (sq.len - sq.t0) * c.gq;
-    const double* pd = S.pd + (size_t)h * S.pelems + sq.p0 + sl;
-    for (int lr = max(0, (sl - sq.t0) * c.gq); lr < nr; ++lr) {
-      const double p = pd[(size_t)lr * sq.len];
-      if (p == 0.0) continue;  // uniform per block
-      double y;
-      if (value) {
-        y = S.wrow[((size_t)h * S.nrows + sq.row0 + lr) * kD + col];
-      } else {
-        const int t = sq.t0 + lr / c.gq, j = h * c.gq + lr % c.gq;
-        y = bf16d(S.q[((size_t)(sq.start + t) * c.Hq + j) * kD + col]) * kInvSqrtD;
+    const double* pd = S.pd + (size_t)h * S.pelems + sq.p0;
+    for (int r0 = 0; r0 < nr; r0 += kGxRows) {
+      __syncthreads();
+      for (int e = tid; e < kGxRows * kGxTok; e += 256) {
+        const int i = e / kGxTok, x = e % kGxTok, sl = s0 + x - sq.start;
+        ps[i][x] = (r0 + i < nr && sl >= 0 && sl < sq.len) ? pd[(size_t)(r0 + i) * sq.len + sl] : 0.0;
       }
-      acc = fma(p, y, acc);
+      for (int e = tid; e < kGxRows * kD; e += 256) {
+        const int i = e / kD, col = e % kD, lr = r0 + i;
+        double y = 0.0;
+        if (lr < nr) {
+          if (value) {
+            y = S.wrow[((size_t)h * S.nrows + sq.row0 + lr) * kD + col];
+          } else {
+            const int t = sq.t0 + lr / c.gq, j = h * c.gq + lr % c.gq;
+            y = bf16d(S.q[((size_t)(sq.start + t) * c.Hq + j) * kD + col]) * kInvSqrtD;
+          }
+        }
+        ys[i][col] = y;
+      }
+      __syncthreads();
+#pragma unroll 4
+      for (int i = 0; i < kGxRows; ++i) {
+        const double p = ps[i][tt];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[q] = fma(p, ys[i][cg * 16 + q], acc[q]);
+      }
     }
   }
-  S.gx[((size_t)s * c.H + h) * kD + col] = acc;
+  if (s0 + tt < S.T) {
+    double* out = S.gx + ((size_t)(s0 + tt) * c.H + h) * kD + cg * 16;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) out[q] = acc[q];
+  }
 }
 
 // gz = mask . (gx R): block (16-token tile, KV head), thread = channel.
@@ -640,7 +669,7 @@ hipError_t cal_bind_set(CalSet& set, uint8_t* base, const uint16_t* k, const uin
   std::vector<CalSeq> seqs(nseq);
   std::vector<int> row_seq;
   long long pel = 0;
-  int rows = 0;
+  int rows = 0, maxlen = 0;
   for (int i = 0; i < nseq; ++i) {
     CalSeq& c = seqs[i];
     c.start = starts_host[i];
@@ -648,6 +677,7 @@ hipError_t cal_bind_set(CalSet& set, uint8_t* base, const uint16_t* k, const uin
     c.t0 = c.len > n_last ? c.len - n_last : 0;
     c.row0 = rows;
     c.p0 = pel;
+    maxlen = c.len > maxlen ? c.len : maxlen;
     const int nr = (c.len - c.t0) * gq;
     for (int r = 0; r < nr; ++r) row_seq.push_back(i);
     rows += nr;
@@ -660,6 +690,7 @@ hipError_t cal_bind_set(CalSet& set, uint8_t* base, const uint16_t* k, const uin
   set.nseq = nseq;
   set.nrows = rows;
   set.pelems = pel;
+  set.maxlen = maxlen;
   const size_t nrow_el = (size_t)set.T * H * kD;
   uint8_t* p = base;
   set.seqs = reinterpret_cast<CalSeq*>(p);
@@ -708,6 +739,14 @@ hipError_t cal_gram(const CalCfg& c, const uint16_t* W_o, hipStream_t s) {
   return hipGetLastError();
 }
 
+static size_t attn_lds(const CalSet& set) {
+  const size_t bytes = 3 * (size_t)(set.maxlen > 0 ? set.maxlen : 1) * sizeof(double);
+  if (bytes > 48 * 1024)  // beyond the default dynamic LDS limit: raise it for this kernel (up to 96 KiB)
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&cal_attn_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  return bytes;
+}
+
 static void rot_and_quant(const CalCfg& c, CalSet& set, const double* A, int value, hipStream_t s) {
   hipLaunchKernelGGL(cal_expm_kernel, dim3(c.H), dim3(kExpThreads), 0, s, c, A, value);
   if (set.T > 0)
@@ -716,7 +755,7 @@ static void rot_and_quant(const CalCfg& c, CalSet& set, const double* A, int val
 
 static void backward(const CalCfg& c, CalSet& set, const double* A, int value, double* grad, hipStream_t s) {
   if (set.T > 0) {
-    hipLaunchKernelGGL(cal_gx_kernel, dim3(set.T, c.H), dim3(kD), 0, s, set, c, value);
+    hipLaunchKernelGGL(cal_gx_kernel, dim3((set.T + kGxTok - 1) / kGxTok, c.H), dim3(256), 0, s, set, c, value);
     hipLaunchKernelGGL(cal_gz_kernel, dim3((set.T + kRotTile - 1) / kRotTile, c.H), dim3(kD), 0, s, set, c);
     hipLaunchKernelGGL(cal_dr_kernel, dim3(kD / 16, c.H, kCalSplit), dim3(kD), 0, s, set, c, value);
   } else {
@@ -730,7 +769,7 @@ static void backward(const CalCfg& c, CalSet& set, const double* A, int value, d
 hipError_t cal_key_loss(const CalCfg& c, CalSet& set, const double* A, double* loss, double* grad, hipStream_t s) {
   rot_and_quant(c, set, A, 0, s);
   if (set.nrows > 0) {
-    hipLaunchKernelGGL(cal_attn_kernel, dim3(set.nrows, c.H), dim3(256), 0, s, set, c, 0);
+    hipLaunchKernelGGL(cal_attn_kernel, dim3(set.nrows, c.H), dim3(256), attn_lds(set), s, set, c, 0);
     hipLaunchKernelGGL(cal_loss_kernel, dim3(c.H), dim3(256), 0, s, set.lrow, set.nrows, loss);
   } else {
     hipLaunchKernelGGL(cal_fill_kernel, dim3(1), dim3(256), 0, s, loss, (size_t)c.H, 0.0);
@@ -748,7 +787,7 @@ hipError_t cal_key_loss(const CalCfg& c, CalSet& set, const double* A, double* l
 
 hipError_t cal_key_probs(const CalCfg& c, CalSet& set, const double* A, hipStream_t s) {
   rot_and_quant(c, set, A, 0, s);
-  if (set.nrows > 0) hipLaunchKernelGGL(cal_attn_kernel, dim3(set.nrows, c.H), dim3(256), 0, s, set, c, 1);
+  if (set.nrows > 0) hipLaunchKernelGGL(cal_attn_kernel, dim3(set.nrows, c.H), dim3(256), attn_lds(set), s, set, c, 1);
   return hipGetLastError();
 }
 

@@ -239,3 +239,32 @@ def make_workload(cfg_id: int, *, batch: Optional[int] = None, ctx: Optional[int
     seq_ss = streams[_S_SEQ].spawn(B)
     return Workload(cfg=cfg, ctx_lens=lens, block_table=table, num_blocks=num_blocks, R_k=R_k, R_v=R_v,
                     mu=mu, q=q, W_o=W_o, key_offsets=offsets, _seq_ss=seq_ss)
+
+
+def calibration_traces(num_seqs: int, len_range: tuple, num_kv_heads: int, num_q_heads: int, seed: int,
+                       n_offset_channels: int = 3, offset_range: tuple = (10.0, 30.0)):
+    """Seeded stand-in for the paper's calibration and held-out trace sets (appendix, calibration
+    details: a few prompts of at least 328 tokens each, their Q/K/V of every layer). Lengths are
+    uniform in len_range; keys are N(0, 1) plus constant offsets on n_offset_channels seeded
+    channels per KV head (as in the decode workloads), values and queries N(0, 1); all bf16.
+    Returns (k [T, H, 128], v [T, H, 128], q [T, H_q, 128]) as torch bf16 CPU tensors and the
+    token offsets seq_starts (int32 [num_seqs + 1])."""
+    rng = np.random.default_rng(SEED_BASE + 1000 + seed)
+    lens = rng.integers(len_range[0], len_range[1], size=num_seqs, endpoint=True)
+    starts = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    T = int(starts[-1])
+    offsets = torch.zeros((num_kv_heads, HEAD_DIM))
+    for h in range(num_kv_heads):
+        ch = rng.choice(HEAD_DIM, size=n_offset_channels, replace=False)
+        offsets[h, ch] = torch.from_numpy(rng.uniform(*offset_range, size=n_offset_channels)).float()
+    g = torch.Generator().manual_seed(int(rng.integers(0, 2**62)))
+    k = (torch.randn((T, num_kv_heads, HEAD_DIM), generator=g) + offsets[None]).to(torch.bfloat16)
+    v = torch.randn((T, num_kv_heads, HEAD_DIM), generator=g).to(torch.bfloat16)
+    q = torch.randn((T, num_q_heads, HEAD_DIM), generator=g).to(torch.bfloat16)
+    return k, v, q, starts
+
+
+def haar_rotations(num_heads: int, seed: int) -> np.ndarray:
+    """Seeded Haar-random rotations fp32 [num_heads, 128, 128] (base rotations R^0)."""
+    rng = np.random.default_rng(SEED_BASE + 2000 + seed)
+    return np.stack([haar_orthogonal(rng) for _ in range(num_heads)]).astype(np.float32)
