@@ -119,6 +119,10 @@ DecodePlan make_plan(int B, int Hq, int H, int max_ctx, int d_model, int groups)
   p.off_part = off;
   const size_t part_rows = p.variant == 2 ? (size_t)(p.grid_g + B) : (size_t)B * p.n_chunks;
   off = up(off + part_rows * Hq * kPartStride * sizeof(float));
+  // two-stage merge of the matrix-core scan for few, long sequences: folded slot ranges
+  p.s1 = p.variant == 2 && (long long)B * H < kMerge2MaxUnits ? kMerge2Ranges : 0;
+  p.off_part2 = off;
+  off = up(off + (size_t)B * p.s1 * Hq * kPartStride * sizeof(float));
   p.off_win = off;  // BF16-window partials, [kWinMaxSlices][B, Hq, kPartStride]
   off = up(off + (size_t)kWinMaxSlices * B * Hq * kPartStride * sizeof(float));
   p.off_o = off;
@@ -386,6 +390,8 @@ int decode_impl(const int2kv_cache* cache, const uint16_t* q, int batch, int num
   a.qrot = reinterpret_cast<float*>(ws + plan.off_qrot);
   a.qop = ws + plan.off_qop;
   a.part = reinterpret_cast<float*>(ws + plan.off_part);
+  a.s1 = plan.s1;
+  a.part2 = plan.s1 ? reinterpret_cast<float*>(ws + plan.off_part2) : nullptr;
   a.chunk_tokens = plan.chunk_tokens;
   a.n_chunks = plan.n_chunks;
   a.prefix = reinterpret_cast<int32_t*>(ws + plan.off_prefix);

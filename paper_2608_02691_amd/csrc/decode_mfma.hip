@@ -689,10 +689,20 @@ __device__ void page_prefix_block(const DecodeArgs& a, uint8_t* lds) {
     if (n > 0) {
       const long long c0 = run + (long long)kSegCost * cnt, c1 = c0 + kSegCost + n;
       const int g1 = min(G - 1, (int)((c1 * G + W - 1) / W) - 1);
-      for (int g = (int)((c0 * G + W - 1) / W); g <= g1; ++g) {
-        const long long x = (long long)g * W / G;
-        const int lo = run + (int)min((long long)n - 1, max(0LL, x - c0 - kSegCost));
+      // x(g) = floor(g W / G), stepped by quotient and remainder: one division for the whole loop
+      // (a long sequence spans every group, and a 64-bit division per group costs microseconds)
+      int g = (int)((c0 * G + W - 1) / W);
+      const long long wq = W / G, wr = W % G;
+      long long xq = (long long)g * wq + ((long long)g * wr) / G, xr = ((long long)g * wr) % G;
+      for (; g <= g1; ++g) {
+        const int lo = run + (int)min((long long)n - 1, max(0LL, xq - c0 - kSegCost));
         *reinterpret_cast<int4*>(a.wg_info + 4 * g) = make_int4(b, run, run + n, lo);
+        xq += wq;
+        xr += wr;
+        if (xr >= G) {
+          xr -= G;
+          ++xq;
+        }
       }
       ga = min(G - 1, (int)(((c0 + kSegCost + 1) * G + W - 1) / W) - 1);
       gb = g1;
@@ -1086,6 +1096,76 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
 // thread (c, s) finishing query heads s, s + kMergeSlots, ... The un-rotation has the 128 threads of slot 0 share one
 // pass over R_V (row c of R_V per thread) for all query heads.
 
+// First stage of the two-stage merge (few, long sequences): block (sequence b, KV head h, range z)
+// folds the work-group slots ga + z n .. ga + z n + n - 1 of the sequence (n = ceil(G / s1)) into
+// one partial per query head, in slot order, and writes it to part2 (m = -inf for an empty range).
+// Thread (channel c, slot lane sl) takes every eighth slot; the lanes are combined in a fixed order.
+__global__ __launch_bounds__(1024) void merge_stage1_kernel(DecodeArgs a, int G) {
+  __shared__ float ms[8][8], ls[8][8];
+  __shared__ float os[8][8][kHeadDim];
+  const int b = blockIdx.x, h = blockIdx.y, z = blockIdx.z, c = threadIdx.x & 127, sl = threadIdx.x >> 7;
+  const int gq = a.gq, per = (G + a.s1 - 1) / a.s1;
+  const int ga = a.seq_wg[2 * b], gb = a.seq_wg[2 * b + 1];
+  const int lo = ga + z * per, hi = min(gb, lo + per - 1);
+  float M[8], lsum[8], osum[8];
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) {
+    M[jj] = -INFINITY;
+    lsum[jj] = 0.0f;
+    osum[jj] = 0.0f;
+  }
+  for (int gg = lo + sl; gg <= hi; gg += 8) {
+    const int r0 = a.wg_info[4 * gg + 3], r1 = a.wg_info[4 * gg + 7];
+    const float* base = a.part + ((size_t)(gg + b) * a.Hq + h * gq) * kPartStride;
+    float mv[8], lv[8], ov[8];
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      const float* pp = base + min(jj, gq - 1) * kPartStride;
+      mv[jj] = pp[0];
+      lv[jj] = pp[1];
+      ov[jj] = pp[4 + c];
+    }
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      const bool valid = r0 < r1 && mv[jj] != -INFINITY;
+      const float Mn = valid ? fmaxf(M[jj], mv[jj]) : M[jj];
+      const float fa = valid ? __builtin_amdgcn_exp2f(M[jj] - Mn) : 1.0f;
+      const float fb = valid ? __builtin_amdgcn_exp2f(mv[jj] - Mn) : 0.0f;
+      lsum[jj] = fmaf(lsum[jj], fa, valid ? fb * lv[jj] : 0.0f);
+      osum[jj] = fmaf(osum[jj], fa, valid ? fb * ov[jj] : 0.0f);
+      M[jj] = Mn;
+    }
+  }
+  if (c == 0) {
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      ms[sl][jj] = M[jj];
+      ls[sl][jj] = lsum[jj];
+    }
+  }
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) os[sl][jj][c] = osum[jj];
+  __syncthreads();
+  const int jj = sl;  // thread (c, sl) finishes query head sl
+  if (jj >= gq) return;
+  float Mx = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) Mx = fmaxf(Mx, ms[t][jj]);
+  float L = 0.0f, O = 0.0f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    const float f = ms[t][jj] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(ms[t][jj] - Mx);
+    L = fmaf(f, ls[t][jj], L);
+    O = fmaf(f, os[t][jj][c], O);
+  }
+  float* dst = a.part2 + ((size_t)(b * a.s1 + z) * a.Hq + h * gq + jj) * kPartStride;
+  if (c == 0) {
+    dst[0] = Mx;
+    dst[1] = L;
+  }
+  dst[4 + c] = O;
+}
+
 template <int kMergeSlots>
 __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArgs a, int G, int unrotate,
                                                                        float* __restrict__ out,
@@ -1112,8 +1192,14 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
         wo[r][s] = pp[4 + c];
       }
   }
-  // groups whose ranges meet the sequence, from the page-prefix block
-  const int ga = a.seq_wg[2 * b], gb = a.seq_wg[2 * b + 1];
+  // groups whose ranges meet the sequence, from the page-prefix block; in the second stage of the
+  // two-stage merge, the sequence's folded slot ranges instead
+  const bool st2 = a.s1 > 0;
+  const int ga = st2 ? 0 : a.seq_wg[2 * b], gb = st2 ? a.s1 - 1 : a.seq_wg[2 * b + 1];
+  auto slot_base = [&](int gg) {
+    return st2 ? a.part2 + ((size_t)(b * a.s1 + gg) * a.Hq + h * gq) * kPartStride
+               : a.part + ((size_t)(gg + b) * a.Hq + h * gq) * kPartStride;
+  };
   float M[8], lsum[8], osum[8];
 #pragma unroll
   for (int jj = 0; jj < 8; ++jj) {
@@ -1121,21 +1207,8 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
     lsum[jj] = 0.0f;
     osum[jj] = 0.0f;
   }
-  for (int gg = ga + sl; gg <= gb; gg += kMergeSlots) {
-    // the range bounds and the partial are loaded together (one round trip): slot gg + b exists for
-    // every group, and an empty range (which wrote nothing, so the slot holds stale values) is
-    // dropped by selects below, never multiplied
-    const int r0 = a.wg_info[4 * gg + 3], r1 = a.wg_info[4 * gg + 7];
-    const float* base = a.part + ((size_t)(gg + b) * a.Hq + h * gq) * kPartStride;
-    float mv[8], lv[8], ov[8];
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {  // every load first, then the arithmetic (no load behind a test)
-      const float* pp = base + min(jj, gq - 1) * kPartStride;
-      mv[jj] = pp[0];
-      lv[jj] = pp[1];
-      ov[jj] = pp[4 + c];
-    }
-    const bool nonempty = r0 < r1;
+  // rounds of kMergeSlots slots; a long sequence (many groups) loads two rounds per trip
+  auto merge_round = [&](const float (&mv)[8], const float (&lv)[8], const float (&ov)[8], bool nonempty) {
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) {
       // a partial with no cached token has m = -inf (or the scan's finite floor) and l = 0
@@ -1147,6 +1220,32 @@ __global__ __launch_bounds__(128 * kMergeSlots) void merge_flat_kernel(DecodeArg
       osum[jj] = fmaf(osum[jj], fa, valid ? fb * ov[jj] : 0.0f);
       M[jj] = Mn;
     }
+  };
+  for (int gg = ga + sl; gg <= gb; gg += 2 * kMergeSlots) {
+    // the range bounds and the partials are loaded together (one round trip): slot gg + b exists
+    // for every group, and an empty range (which wrote nothing, so the slot holds stale values) is
+    // dropped by selects below, never multiplied; a second slot past gb is loaded as slot gg and
+    // dropped
+    const int g2 = gg + kMergeSlots <= gb ? gg + kMergeSlots : gg;
+    // stage-2 ranges are never stale (an empty one was written with m = -inf)
+    const int r0 = st2 ? 0 : a.wg_info[4 * gg + 3], r1 = st2 ? 1 : a.wg_info[4 * gg + 7];
+    const int r2 = st2 ? 0 : a.wg_info[4 * g2 + 3], r3 = st2 ? 1 : a.wg_info[4 * g2 + 7];
+    const float* base = slot_base(gg);
+    const float* base2 = slot_base(g2);
+    float mv[8], lv[8], ov[8], mv2[8], lv2[8], ov2[8];
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {  // every load first, then the arithmetic (no load behind a test)
+      const float* pp = base + min(jj, gq - 1) * kPartStride;
+      const float* p2 = base2 + min(jj, gq - 1) * kPartStride;
+      mv[jj] = pp[0];
+      lv[jj] = pp[1];
+      ov[jj] = pp[4 + c];
+      mv2[jj] = p2[0];
+      lv2[jj] = p2[1];
+      ov2[jj] = p2[4 + c];
+    }
+    merge_round(mv, lv, ov, r0 < r1);
+    merge_round(mv2, lv2, ov2, g2 != gg && r2 < r3);
   }
   if (c == 0) {
 #pragma unroll
@@ -1287,7 +1386,14 @@ hipError_t launch_merge_flat(const DecodeArgs& a, bool unrotate, float* out, uin
   if (a.gq > 8) return hipErrorNotSupported;
   // four slots when many sequences share the work-groups (short spans; fewer idle waves to
   // dispatch), eight for few, long sequences (fewer rounds of loads)
-  if (a.B >= 32)
+  if (a.s1 > 0) {
+    // few, long sequences: every range of slots folded by its own block first, so that the
+    // partials stream through B x H x s1 blocks instead of B x H
+    DecodeArgs a1 = a;
+    hipLaunchKernelGGL(merge_stage1_kernel, dim3(a.B, a.H, a.s1), dim3(1024), 0, s, a1, a.grid_g);
+    hipLaunchKernelGGL(merge_flat_kernel<8>, dim3(a.B, a.H), dim3(128 * 8), 0, s, a, a.grid_g, unrotate ? 1 : 0, out,
+                       ob, fmt);
+  } else if (a.B >= 32)
     hipLaunchKernelGGL(merge_flat_kernel<4>, dim3(a.B, a.H), dim3(128 * 4), 0, s, a, a.grid_g, unrotate ? 1 : 0, out,
                        ob, fmt);
   else

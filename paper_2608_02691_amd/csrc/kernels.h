@@ -44,7 +44,9 @@ struct DecodePlan {
   int variant;        // 1 = vector ALU, 2 = matrix core
   int wo_ksplit;
   int grid_g;         // work-groups of the matrix-core scan
-  size_t off_qrot, off_qop, off_prefix, off_wginfo, off_seqwg, off_pages, off_part, off_win, off_o, off_wo, total;
+  int s1;             // slot ranges per sequence of the two-stage merge (0: one stage)
+  size_t off_qrot, off_qop, off_prefix, off_wginfo, off_seqwg, off_pages, off_part, off_part2, off_win, off_o,
+      off_wo, total;
 };
 
 struct DecodeArgs {
@@ -69,6 +71,8 @@ struct DecodeArgs {
   int grid_g;      // work-groups of the matrix-core scan
   int groups;      // groups per token of the cache (4 or 1)
   float* wpart;    // BF16-window partials [win_slices][B, Hq, kPartStride] folded in by the merge, or null
+  float* part2;    // two-stage merge (few, long sequences): [B, s1, Hq, kPartStride] folded slot ranges
+  int s1;          // slot ranges per sequence of the two-stage merge (0: one stage)
   int win_slices;  // window slices of kWinSliceTokens tokens (ceil(win_cap / kWinSliceTokens))
 };
 
@@ -83,6 +87,8 @@ struct WindowArgs {
 constexpr int kWinMaxGq = 16;
 constexpr int kWinMaxCap = 512;
 constexpr int kWinSliceTokens = 128;                           // window tokens per partial
+constexpr int kMerge2Ranges = 16;      // slot ranges per sequence in the two-stage merge
+constexpr int kMerge2MaxUnits = 128;   // two-stage merge when batch x KV heads is below this
 constexpr int kWinMaxSlices = kWinMaxCap / kWinSliceTokens;    // window partials per (sequence, query head)
 hipError_t launch_window_write(const uint16_t* k, const uint16_t* v, const int32_t* rows, int n, int H, const float* mu,
                                uint16_t* win_k, uint16_t* win_v, int num_rows, hipStream_t s);
