@@ -681,6 +681,9 @@ __device__ void page_prefix_block(const DecodeArgs& a, uint8_t* lds) {
   }
   const int P = sums[255], G = a.grid_g;
   const long long W = (long long)P + (long long)kSegCost * cnts[255];
+  // few sequences: their group entries are filled by the whole block below (a long sequence spans
+  // hundreds of groups, too many for one thread)
+  const bool coop = a.B <= 8;
   int run = tid > 0 ? sums[tid - 1] : 0, cnt = tid > 0 ? cnts[tid - 1] : 0;
   for (int b = b0; b < b1; ++b) {
     const int n = (seq_len_m(a, b) + kBlock - 1) >> 4;
@@ -691,7 +694,7 @@ __device__ void page_prefix_block(const DecodeArgs& a, uint8_t* lds) {
       const int g1 = min(G - 1, (int)((c1 * G + W - 1) / W) - 1);
       // x(g) = floor(g W / G), stepped by quotient and remainder: one division for the whole loop
       // (a long sequence spans every group, and a 64-bit division per group costs microseconds)
-      int g = (int)((c0 * G + W - 1) / W);
+      int g = coop ? g1 + 1 : (int)((c0 * G + W - 1) / W);
       const long long wq = W / G, wr = W % G;
       long long xq = (long long)g * wq + ((long long)g * wr) / G, xr = ((long long)g * wr) % G;
       for (; g <= g1; ++g) {
@@ -711,6 +714,21 @@ __device__ void page_prefix_block(const DecodeArgs& a, uint8_t* lds) {
     a.seq_wg[2 * b] = ga;
     a.seq_wg[2 * b + 1] = gb;
     run += n;
+  }
+  if (coop) {
+    // per = 1 here, so the exclusive prefixes of sequence b are the scan's entries at b - 1
+    for (int b = 0; b < a.B; ++b) {
+      const int n = (seq_len_m(a, b) + kBlock - 1) >> 4;
+      if (n == 0) continue;  // uniform
+      const int rb = b > 0 ? sums[b - 1] : 0, cb = b > 0 ? cnts[b - 1] : 0;
+      const long long c0 = rb + (long long)kSegCost * cb, c1 = c0 + kSegCost + n;
+      const int g1 = min(G - 1, (int)((c1 * G + W - 1) / W) - 1);
+      for (int g = (int)((c0 * G + W - 1) / W) + tid; g <= g1; g += 256) {
+        const long long x = (long long)g * W / G;
+        const int lo = rb + (int)min((long long)n - 1, max(0LL, x - c0 - kSegCost));
+        *reinterpret_cast<int4*>(a.wg_info + 4 * g) = make_int4(b, rb, rb + n, lo);
+      }
+    }
   }
   if (tid == 255) {
     a.prefix[a.B] = P;
