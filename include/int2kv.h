@@ -333,10 +333,11 @@ int int2kv_output_error(const int2kv_cache* cache, const uint16_t* q, int batch,
  * element's gradient passes when it lies inside its group's clipped range [c mn, c mx]; scale and
  * zero are held fixed. The optimizer is Adam (betas 0.9 / 0.999, eps 1e-8, learning rate lr); the
  * iterate with the lowest held-out objective among A = 0 and every eval_every-th step is kept.
- * All arithmetic is fp64; inputs stay as given (bf16 traces, fp32 R^0 and mu). */
+ * All arithmetic is fp64; inputs stay as given (bf16 traces, fp32 R^0 and mu). Up to 16 query heads
+ * per KV head. */
 typedef struct int2kv_optr_traces {
-  const uint16_t* k;          /* device bf16 [T, H_kv, 128]: keys (post-RoPE, raw) */
-  const uint16_t* v;          /* device bf16 [T, H_kv, 128]: values */
+  const uint16_t* k;          /* device bf16 [T, H_kv, 128]: keys (post-RoPE, raw); 16-byte aligned */
+  const uint16_t* v;          /* device bf16 [T, H_kv, 128]: values; 16-byte aligned */
   const uint16_t* q;          /* device bf16 [T, H_q, 128]: queries (post-RoPE) */
   const int32_t* seq_starts;  /* HOST int32 [num_seqs + 1]: token offsets, seq_starts[0] = 0,
                                  sequences of 0 .. 4096 tokens */

@@ -654,7 +654,7 @@ int check_traces(const int2kv_optr_traces* t, const int2kv_optr_config* c, SetDi
   }
   d.T = t->seq_starts[t->num_seqs];
   d.nseq = t->num_seqs;
-  if (!aligned(t->k, 4) || !aligned(t->v, 4)) return fail(INT2KV_EINVAL, std::string(what) + ": k, v must be 4-byte aligned");
+  if (!aligned(t->k, 16) || !aligned(t->v, 16)) return fail(INT2KV_EINVAL, std::string(what) + ": k, v must be 16-byte aligned");
   return INT2KV_OK;
 }
 
@@ -662,6 +662,7 @@ int check_config(const int2kv_optr_config* c) {
   if (!c) return fail(INT2KV_EINVAL, "config is NULL");
   if (c->num_kv_heads <= 0 || c->num_q_heads <= 0 || c->num_q_heads % c->num_kv_heads)
     return fail(INT2KV_EINVAL, "num_q_heads must be a positive multiple of num_kv_heads");
+  if (c->num_q_heads / c->num_kv_heads > 16) return fail(INT2KV_EUNSUPPORTED, "at most 16 query heads per KV head");
   if (c->d_model <= 0) return fail(INT2KV_EINVAL, "d_model must be positive");
   if (c->group_size != 32 && c->group_size != 128) return fail(INT2KV_EUNSUPPORTED, "group_size must be 32 or 128");
   if (!valid_clip(c->clip_k) || !valid_clip(c->clip_v)) return fail(INT2KV_EINVAL, "clip ratios must be in (0, 1]");

@@ -154,13 +154,17 @@ struct CalSet {
   const uint16_t *k, *v, *q;       // bf16 [T, H, 128], [T, H, 128], [T, Hq, 128]
   int T, nseq, nrows;              // nrows: query rows of one KV head
   int maxlen;                      // longest sequence
+  int ntiles;                      // row tiles of the objective kernels
+  int4* tiles;                     // [ntiles]: (sequence, first row, rows, position of the first row)
   long long pelems;                // per KV head: sum over sequences of rows * len
   CalSeq* seqs;                    // [nseq]
   int* row_seq;                    // [nrows]: sequence of each row
   double *zhat, *xeff, *gx, *gz;   // [T, H, 128]: dequantized rotated rows, effective rows, gradients
   uint8_t* mask;                   // [T, H, 128]: straight-through mask
-  double* pd;                      // [H, pelems]: logit gradients (key loss) or key probabilities (value loss)
-  double* wrow;                    // [H, nrows, 128]: value-loss row weights
+  double* pd;                      // [H, pelems]: key probabilities, then logit gradients (key loss)
+  double* pf;                      // [H, pelems]: full-precision probabilities (key loss)
+  double* wrow;                    // [H, nrows, 128]: dO per row, then the value-loss row weights
+  double* urow;                    // [H, nrows, 128]: M_j dO per row (key loss)
   double* lrow;                    // [H, nrows]: per-row losses
 };
 struct CalCfg {

@@ -148,132 +148,379 @@ __global__ __launch_bounds__(128) void cal_rotq_kernel(CalSet S, CalCfg c, int v
 }
 
 // ---------------------------------------------------------------------------------------------
-// Key objective of one row (t, j) and its logit gradients, or (probs) the key probabilities only.
-// Block (row, KV head) of 256 threads.
-__global__ __launch_bounds__(256) void cal_attn_kernel(CalSet S, CalCfg c, int probs_only) {
-  // logits and gradients of the row's tokens: 3 x maxlen doubles of dynamic LDS (sized to the
-  // set's longest sequence, so that several rows share a compute unit)
-  extern __shared__ double cal_dyn[];
-  double *af = cal_dyn, *ak = cal_dyn + S.maxlen, *gg = cal_dyn + 2 * S.maxlen;
-  __shared__ double qv[kD], dov[2][kD], uv[kD];
-  __shared__ double red[16];
-  const int row = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-  const CalSeq sq = S.seqs[S.row_seq[row]];
-  const int local = row - sq.row0, t = sq.t0 + local / c.gq, jj = local % c.gq, j = h * c.gq + jj;
-  const int a0 = sq.start, L = sq.len;
-  if (tid < kD) qv[tid] = bf16d(S.q[((size_t)(a0 + t) * c.Hq + j) * kD + tid]);
-  __syncthreads();
-  const double mu0 = (double)c.mu[h * kD + 2 * l], mu1 = (double)c.mu[h * kD + 2 * l + 1];
-  const double q0 = qv[2 * l], q1 = qv[2 * l + 1];
-  for (int s = w; s <= t; s += 4) {
-    const size_t o = ((size_t)(a0 + s) * c.H + h) * kD + 2 * l;
-    const uint32_t kk = *reinterpret_cast<const uint32_t*>(S.k + o);
-    const double k0 = (double)__uint_as_float(kk << 16) - mu0, k1 = (double)__uint_as_float(kk & 0xFFFF0000u) - mu1;
-    const double f = wave_sum(q0 * k0 + q1 * k1) * kInvSqrtD;
-    double g = f;
-    if (int2_token(s, t, c.sink, c.recent)) g = wave_sum(q0 * S.xeff[o] + q1 * S.xeff[o + 1]) * kInvSqrtD;
-    if (l == 0) {
-      af[s] = f;
-      ak[s] = g;
+// Objectives per query position: block (position p, KV head h) handles the G_q rows (t, j) of that
+// position, one thread per token for the logits (each key row is read once for the whole group,
+// no cross-lane reductions per token). MAXG >= G_q.
+
+// Block-wide max / sum of MAXG values per thread; red: [16][MAXG] doubles.
+template <int MAXG, bool MAX>
+__device__ void block_reduce_n(double (&x)[MAXG], double* red) {
+#pragma unroll
+  for (int j = 0; j < MAXG; ++j)
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const double y = __shfl_xor(x[j], off);
+      x[j] = MAX ? fmax(x[j], y) : x[j] + y;
     }
-  }
+  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
   __syncthreads();
-  double mf = -INFINITY, mk = -INFINITY;
-  for (int s = tid; s <= t; s += blockDim.x) {
-    mf = fmax(mf, af[s]);
-    mk = fmax(mk, ak[s]);
-  }
-  mf = block_max(mf, red);
-  mk = block_max(mk, red);
-  double zf = 0.0, zk = 0.0;
-  for (int s = tid; s <= t; s += blockDim.x) {
-    zf += exp(af[s] - mf);
-    zk += exp(ak[s] - mk);
-  }
-  zf = block_sum(zf, red);
-  zk = block_sum(zk, red);
-  const double lsf = mf + log(zf), lsk = mk + log(zk);
-  double* pd = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)local * L;
-  if (probs_only) {
-    for (int s = tid; s < L; s += blockDim.x)
-      pd[s] = (s <= t && int2_token(s, t, c.sink, c.recent)) ? exp(ak[s] - lsk) : 0.0;
-    return;
-  }
-  // KL(p || p^K) and the probabilities (af <- p, ak <- p^K)
-  double kl = 0.0;
-  for (int s = tid; s <= t; s += blockDim.x) {
-    const double lp = af[s] - lsf, lq = ak[s] - lsk, p = exp(lp);
-    kl += p * (lp - lq);
-    af[s] = p;
-    ak[s] = exp(lq);
-  }
-  kl = block_sum(kl, red);
-  // dO = sum_s (p^K - p) v_s: thread (channel, half of the tokens)
-  {
-    const int col = tid & 127, half = tid >> 7;
-    double acc = 0.0;
-    for (int s = half; s <= t; s += 2) acc += (ak[s] - af[s]) * bf16d(S.v[((size_t)(a0 + s) * c.H + h) * kD + col]);
-    dov[half][col] = acc;
-  }
+  if ((threadIdx.x & 63) == 0)
+#pragma unroll
+    for (int j = 0; j < MAXG; ++j) red[w * MAXG + j] = x[j];
   __syncthreads();
-  if (tid < kD) dov[0][tid] += dov[1][tid];
-  __syncthreads();
-  // u = M_j dO (M symmetric: column reads), E = dO . u / d_model
-  double e = 0.0;
-  if (tid < kD) {
-    const double* M = c.gram + (size_t)j * kMat;
-    double u = 0.0;
-    for (int b = 0; b < kD; ++b) u = fma(M[b * kD + tid], dov[0][b], u);
-    uv[tid] = u;
-    e = u * dov[0][tid];
-  }
-  e = block_sum(e, red) / (double)c.dm;
-  if (tid == 0) S.lrow[(size_t)h * S.nrows + row] = kl + c.lam * e;
-  // g_s = 2 u . v_s / d_model, gbar = sum_s p^K_s g_s
-  const double u0 = uv[2 * l], u1 = uv[2 * l + 1];
-  for (int s = w; s <= t; s += 4) {
-    const uint32_t vv = *reinterpret_cast<const uint32_t*>(S.v + ((size_t)(a0 + s) * c.H + h) * kD + 2 * l);
-    const double g = wave_sum(u0 * (double)__uint_as_float(vv << 16) + u1 * (double)__uint_as_float(vv & 0xFFFF0000u));
-    if (l == 0) gg[s] = 2.0 * g / (double)c.dm;
-  }
-  __syncthreads();
-  double gb = 0.0;
-  for (int s = tid; s <= t; s += blockDim.x) gb += ak[s] * gg[s];
-  gb = block_sum(gb, red);
-  const double inv_rows = 1.0 / (double)S.nrows;
-  for (int s = tid; s < L; s += blockDim.x) {
-    double d = 0.0;
-    if (s <= t && int2_token(s, t, c.sink, c.recent))
-      d = ((ak[s] - af[s]) + c.lam * ak[s] * (gg[s] - gb)) * inv_rows;
-    pd[s] = d;
+#pragma unroll
+  for (int j = 0; j < MAXG; ++j) {
+    double t = red[j];
+    for (int i = 1; i < nw; ++i) t = MAX ? fmax(t, red[i * MAXG + j]) : t + red[i * MAXG + j];  // fixed order
+    x[j] = t;
   }
 }
 
-// Value objective of one row under the stored key probabilities: block (row, KV head), thread =
-// channel. Also the row's weight 2 M_j dO / (d_model rows) for the gradient.
-__global__ __launch_bounds__(128) void cal_vrow_kernel(CalSet S, CalCfg c) {
-  __shared__ double dov[kD];
-  __shared__ double red[16];
-  const int row = blockIdx.x, h = blockIdx.y, col = threadIdx.x;
-  const CalSeq sq = S.seqs[S.row_seq[row]];
-  const int local = row - sq.row0, t = sq.t0 + local / c.gq, jj = local % c.gq, j = h * c.gq + jj;
-  const double* pd = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)local * sq.len;
-  double acc = 0.0;
-  for (int s = 0; s <= t; ++s) {
-    const double p = pd[s];
-    if (p != 0.0) {
-      const size_t o = ((size_t)(sq.start + s) * c.H + h) * kD + col;
-      acc += p * (S.xeff[o] - bf16d(S.v[o]));
+// The per-position kernels take a tile of up to kTileRows rows: 16 / G_q consecutive query
+// positions of one sequence with all their query heads (tiles[i] = (sequence, first row, rows,
+// position of the first row)), so each key and value row is loaded once for the whole tile.
+// Row r of a tile is position t_first + r / G_q, query head h G_q + r % G_q.
+constexpr int kTileRows = 16;
+constexpr int kTileThreads = 256;  // threads of the tile kernels; one token per thread per chunk
+constexpr int kDlStride = 18;      // doubles per token of the staged differences (16-byte rows, 4-way writes)
+
+// dO accumulation layout of the tile kernels: thread (column pair cp = tid % 64, quarter qt =
+// tid / 64 of each token chunk), acc[r][0..1] = rows r, columns 2 cp and 2 cp + 1. Sums the four
+// quarters in the fixed order (q0 + q2) + (q1 + q3) through buf (2 R 128 doubles of LDS, free on
+// entry) and stores rows r < nr at out + r 128.
+template <int R>
+__device__ __forceinline__ void sum_quarters_store(double (&acc)[R][2], double* buf, double* out, int nr) {
+  const int cp = threadIdx.x & 63, qt = threadIdx.x >> 6;
+  double2* b2 = reinterpret_cast<double2*>(buf);
+  __syncthreads();
+  if (qt >= 2)
+#pragma unroll
+    for (int r = 0; r < R; ++r) b2[((qt - 2) * R + r) * (kD / 2) + cp] = make_double2(acc[r][0], acc[r][1]);
+  __syncthreads();
+  if (qt < 2)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const double2 o = b2[(qt * R + r) * (kD / 2) + cp];
+      acc[r][0] += o.x;
+      acc[r][1] += o.y;
+    }
+  __syncthreads();
+  if (qt == 1)
+#pragma unroll
+    for (int r = 0; r < R; ++r) b2[r * (kD / 2) + cp] = make_double2(acc[r][0], acc[r][1]);
+  __syncthreads();
+  if (qt == 0)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const double2 o = b2[r * (kD / 2) + cp];
+      if (r < nr)
+        reinterpret_cast<double2*>(out + (size_t)r * kD)[cp] = make_double2(acc[r][0] + o.x, acc[r][1] + o.y);
+    }
+}
+
+// acc[r][.] += d[r] (w0, w1) for one token, d = the token's staged row of R doubles (16-byte aligned).
+template <int R>
+__device__ __forceinline__ void acc_token(double (&acc)[R][2], const double* d, double w0, double w1) {
+  const double2* d2 = reinterpret_cast<const double2*>(d);
+#pragma unroll
+  for (int r2 = 0; r2 < R / 2; ++r2) {
+    const double2 x = d2[r2];
+    acc[2 * r2][0] = fma(x.x, w0, acc[2 * r2][0]);
+    acc[2 * r2][1] = fma(x.x, w1, acc[2 * r2][1]);
+    acc[2 * r2 + 1][0] = fma(x.y, w0, acc[2 * r2 + 1][0]);
+    acc[2 * r2 + 1][1] = fma(x.y, w1, acc[2 * r2 + 1][1]);
+  }
+}
+
+// Forward of the key objective on a tile: logits over the full-precision and the effective keys,
+// both softmaxes, KL(p || p^K) into lrow, p into pf and p^K into pd (per row, every token of the
+// sequence; 0 past the row's position), and dO = sum_s (p^K - p) v_s into wrow. With probs_only:
+// pd = p^K on the tokens read from INT2 and 0 elsewhere, nothing else. Block (tile, KV head).
+__global__ __launch_bounds__(kTileThreads) void cal_pos_fwd_kernel(CalSet S, CalCfg c, int probs_only) {
+  constexpr int R = kTileRows;
+  __shared__ double qs[R][kD];
+  __shared__ double mus[kD];
+  __shared__ double red[16 * R];
+  __shared__ __align__(16) double dl[kTileThreads * kDlStride];
+  const int h = blockIdx.y, tid = threadIdx.x, gq = c.gq;
+  const int4 tile = S.tiles[blockIdx.x];
+  const CalSeq sq = S.seqs[tile.x];
+  const int row0 = tile.y, nr = tile.z, tf = tile.w, a0 = sq.start, L = sq.len;
+  const int tmax = tf + (nr - 1) / gq;
+  for (int e = tid; e < R * kD; e += blockDim.x) {
+    const int r = e / kD, col = e % kD;
+    qs[r][col] = r < nr ? bf16d(S.q[((size_t)(a0 + tf + r / gq) * c.Hq + h * gq + r % gq) * kD + col]) : 0.0;
+  }
+  if (tid < kD) mus[tid] = (double)c.mu[h * kD + tid];
+  __syncthreads();
+  // rows of the tile are consecutive rows of the sequence's [rows][len] blocks
+  double* pdb = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;  // row r at + r L
+  double* pfb = S.pf + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
+  double mf[R], mk[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) mf[r] = mk[r] = -INFINITY;
+  for (int s = tid; s <= tmax; s += blockDim.x) {
+    const bool any_q2 = int2_token(s, tmax, c.sink, c.recent);  // some row reads s from INT2
+    const size_t o = ((size_t)(a0 + s) * c.H + h) * kD;
+    const uint4* kr = reinterpret_cast<const uint4*>(S.k + o);
+    const double2* xr = reinterpret_cast<const double2*>(S.xeff + o);
+    double af[R], ak[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) af[r] = ak[r] = 0.0;
+    for (int c8 = 0; c8 < kD / 8; ++c8) {
+      const uint4 kk = kr[c8];
+      const uint32_t kw[4] = {kk.x, kk.y, kk.z, kk.w};
+      double kd[8], xd[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        kd[2 * i] = (double)__uint_as_float(kw[i] << 16) - mus[8 * c8 + 2 * i];
+        kd[2 * i + 1] = (double)__uint_as_float(kw[i] & 0xFFFF0000u) - mus[8 * c8 + 2 * i + 1];
+      }
+      if (any_q2) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const double2 x2 = xr[4 * c8 + i];
+          xd[2 * i] = x2.x;
+          xd[2 * i + 1] = x2.y;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (r >= nr) continue;  // uniform
+#pragma unroll
+        for (int i = 0; i < 8; ++i) af[r] = fma(qs[r][8 * c8 + i], kd[i], af[r]);
+        if (any_q2) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) ak[r] = fma(qs[r][8 * c8 + i], xd[i], ak[r]);
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (r >= nr) continue;
+      const int tr = tf + r / gq;
+      if (s > tr) continue;  // past the row's position
+      const double f = af[r] * kInvSqrtD;
+      const double g = int2_token(s, tr, c.sink, c.recent) ? ak[r] * kInvSqrtD : f;
+      pfb[(size_t)r * L + s] = f;  // logits first; this thread rewrites them below
+      pdb[(size_t)r * L + s] = g;
+      mf[r] = fmax(mf[r], f);
+      mk[r] = fmax(mk[r], g);
     }
   }
-  dov[col] = acc;
-  __syncthreads();
+  block_reduce_n<R, true>(mf, red);
+  block_reduce_n<R, true>(mk, red);
+  double zf[R], zk[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) zf[r] = zk[r] = 0.0;
+  for (int s = tid; s <= tmax; s += blockDim.x)
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (r >= nr || s > tf + r / gq) continue;
+      zf[r] += exp(pfb[(size_t)r * L + s] - mf[r]);
+      zk[r] += exp(pdb[(size_t)r * L + s] - mk[r]);
+    }
+  block_reduce_n<R, false>(zf, red);
+  block_reduce_n<R, false>(zk, red);
+  double kl[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    kl[r] = 0.0;
+    zf[r] = mf[r] + log(zf[r]);  // log-sum-exp
+    zk[r] = mk[r] + log(zk[r]);
+  }
+  // probabilities chunk by chunk (one token per thread); dO = sum_s (p^K - p) v_s accumulates from
+  // the chunk's differences staged in LDS (p and p^K are 0 past a row's position)
+  const int cp = tid & 63, qt = tid >> 6;
+  double acc[R][2];
+#pragma unroll
+  for (int r = 0; r < R; ++r) acc[r][0] = acc[r][1] = 0.0;
+  for (int base = 0; base < L; base += kTileThreads) {
+    const int s = base + tid;
+    if (s < L) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        double pv = 0.0, pk = 0.0;
+        if (r < nr) {
+          const int tr = tf + r / gq;
+          if (s <= tr) {
+            const double lp = pfb[(size_t)r * L + s] - zf[r], lq = pdb[(size_t)r * L + s] - zk[r];
+            pv = exp(lp);
+            pk = exp(lq);
+            kl[r] += pv * (lp - lq);
+          }
+          pfb[(size_t)r * L + s] = pv;
+          pdb[(size_t)r * L + s] = probs_only ? (s <= tr && int2_token(s, tr, c.sink, c.recent) ? pk : 0.0) : pk;
+        }
+        dl[tid * kDlStride + r] = pk - pv;
+      }
+    }
+    if (probs_only || base > tmax) continue;  // uniform
+    __syncthreads();
+    const int end = min(kTileThreads, tmax + 1 - base);
+    for (int j = qt; j < end; j += 4) {
+      const uint32_t vv =
+          *reinterpret_cast<const uint32_t*>(S.v + ((size_t)(a0 + base + j) * c.H + h) * kD + 2 * cp);
+      acc_token<R>(acc, dl + j * kDlStride, (double)__uint_as_float(vv << 16),
+                   (double)__uint_as_float(vv & 0xFFFF0000u));
+    }
+    __syncthreads();
+  }
+  if (probs_only) return;  // uniform
+  block_reduce_n<R, false>(kl, red);
+  sum_quarters_store<R>(acc, dl, S.wrow + ((size_t)h * S.nrows + row0) * kD, nr);
+  if (tid == 0)
+    for (int r = 0; r < nr; ++r) S.lrow[(size_t)h * S.nrows + row0 + r] = kl[r];
+}
+
+// Value objective on a tile: dO_V = sum_s p^K-hat_s (v~_s - v_s) into wrow (pd holds p^K-hat on the
+// tokens read from INT2, 0 elsewhere). Block (tile, KV head); pd is staged through LDS by token chunk.
+__global__ __launch_bounds__(kTileThreads) void cal_pos_val_kernel(CalSet S, CalCfg c) {
+  constexpr int R = kTileRows;
+  __shared__ __align__(16) double dl[kTileThreads * kDlStride];
+  const int h = blockIdx.y, tid = threadIdx.x, gq = c.gq;
+  const int4 tile = S.tiles[blockIdx.x];
+  const CalSeq sq = S.seqs[tile.x];
+  const int row0 = tile.y, nr = tile.z, tf = tile.w, a0 = sq.start, L = sq.len;
+  const int tmax = tf + (nr - 1) / gq;
+  const double* pdb = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
+  const int cp = tid & 63, qt = tid >> 6;
+  double acc[R][2];
+#pragma unroll
+  for (int r = 0; r < R; ++r) acc[r][0] = acc[r][1] = 0.0;
+  for (int base = 0; base <= tmax; base += kTileThreads) {
+    const int end = min(kTileThreads, tmax + 1 - base);
+    for (int e = tid; e < R * kTileThreads; e += kTileThreads) {
+      const int r = e / kTileThreads, j = e % kTileThreads;
+      dl[j * kDlStride + r] = r < nr && j < end ? pdb[(size_t)r * L + base + j] : 0.0;
+    }
+    __syncthreads();
+    for (int j = qt; j < end; j += 4) {
+      const size_t o = ((size_t)(a0 + base + j) * c.H + h) * kD + 2 * cp;
+      const double2 x = *reinterpret_cast<const double2*>(S.xeff + o);
+      const uint32_t vv = *reinterpret_cast<const uint32_t*>(S.v + o);
+      acc_token<R>(acc, dl + j * kDlStride, x.x - (double)__uint_as_float(vv << 16),
+                   x.y - (double)__uint_as_float(vv & 0xFFFF0000u));
+    }
+    __syncthreads();
+  }
+  sum_quarters_store<R>(acc, dl, S.wrow + ((size_t)h * S.nrows + row0) * kD, nr);
+}
+
+// u = M_j dO for the rows of query head j (M_j = W_{O,j}^T W_{O,j}, symmetric), E = dO . u / d_model.
+// Keys: urow = u, lrow += lambda E. Values: wrow = 2 u / (d_model rows), lrow = E. Block (query head j,
+// 32 positions), thread (row r, 16 columns); M_j streams through LDS 16 rows at a time.
+constexpr int kUTile = 32;
+__global__ __launch_bounds__(256) void cal_u_kernel(CalSet S, CalCfg c, int value) {
+  __shared__ double ds[kUTile][kD + 1];
+  __shared__ double ms[16][kD];
+  const int j = blockIdx.x, h = j / c.gq, jj = j % c.gq, tid = threadIdx.x;
+  const int npos = S.nrows / c.gq, p0 = blockIdx.y * kUTile;
+  const int r = tid >> 3, cg = tid & 7;
+  for (int e = tid; e < kUTile * kD; e += blockDim.x) {
+    const int rr = e / kD, col = e % kD, pp = p0 + rr;
+    ds[rr][col] = pp < npos ? S.wrow[((size_t)h * S.nrows + (size_t)pp * c.gq + jj) * kD + col] : 0.0;
+  }
+  double acc[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.0;
   const double* M = c.gram + (size_t)j * kMat;
-  double u = 0.0;
-  for (int b = 0; b < kD; ++b) u = fma(M[b * kD + col], dov[b], u);
-  const double e = block_sum(u * acc, red) / (double)c.dm;
-  if (col == 0) S.lrow[(size_t)h * S.nrows + row] = e;
-  S.wrow[((size_t)h * S.nrows + row) * kD + col] = 2.0 * u / ((double)c.dm * (double)S.nrows);
+  for (int b0 = 0; b0 < kD; b0 += 16) {
+    __syncthreads();
+    for (int e = tid; e < 16 * kD; e += blockDim.x) ms[e / kD][e % kD] = M[(size_t)(b0 + e / kD) * kD + e % kD];
+    __syncthreads();
+#pragma unroll 4
+    for (int b = 0; b < 16; ++b) {
+      const double d = ds[r][b0 + b];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[i] = fma(d, ms[b][cg * 16 + i], acc[i]);
+    }
+  }
+  double e = 0.0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) e = fma(ds[r][cg * 16 + i], acc[i], e);
+  e += __shfl_xor(e, 1);
+  e += __shfl_xor(e, 2);
+  e += __shfl_xor(e, 4);
+  const int pp = p0 + r;
+  if (pp >= npos) return;
+  const size_t row = (size_t)h * S.nrows + (size_t)pp * c.gq + jj;
+  const double dm = (double)c.dm;
+  if (value) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) S.wrow[row * kD + cg * 16 + i] = 2.0 * acc[i] / (dm * (double)S.nrows);
+    if (cg == 0) S.lrow[row] = e / dm;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) S.urow[row * kD + cg * 16 + i] = acc[i];
+    if (cg == 0) S.lrow[row] += c.lam * e / dm;
+  }
+}
+
+// Logit gradients of the key objective on a tile: g_s = 2 u . v_s / d_model, gbar = sum_s p^K_s g_s,
+// pd = ((p^K - p) + lambda p^K (g - gbar)) / rows on the tokens read from INT2, 0 elsewhere.
+// Block (tile, KV head), one thread per token.
+__global__ __launch_bounds__(kTileThreads) void cal_pos_grad_kernel(CalSet S, CalCfg c) {
+  constexpr int R = kTileRows;
+  __shared__ double us[R][kD];
+  __shared__ double red[16 * R];
+  const int h = blockIdx.y, tid = threadIdx.x, gq = c.gq;
+  const int4 tile = S.tiles[blockIdx.x];
+  const CalSeq sq = S.seqs[tile.x];
+  const int row0 = tile.y, nr = tile.z, tf = tile.w, a0 = sq.start, L = sq.len;
+  const int tmax = tf + (nr - 1) / gq;
+  for (int e = tid; e < R * kD; e += blockDim.x) {
+    const int r = e / kD, col = e % kD;
+    us[r][col] = r < nr ? S.urow[((size_t)h * S.nrows + row0 + r) * kD + col] : 0.0;
+  }
+  __syncthreads();
+  double* pdb = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
+  double* pfb = S.pf + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
+  const double two_dm = 2.0 / (double)c.dm;
+  double gb[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) gb[r] = 0.0;
+  for (int s = tid; s <= tmax; s += blockDim.x) {
+    const uint4* vr = reinterpret_cast<const uint4*>(S.v + ((size_t)(a0 + s) * c.H + h) * kD);
+    double g[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) g[r] = 0.0;
+    for (int c8 = 0; c8 < kD / 8; ++c8) {
+      const uint4 vv = vr[c8];
+      const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+      double vd[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        vd[2 * i] = (double)__uint_as_float(vw[i] << 16);
+        vd[2 * i + 1] = (double)__uint_as_float(vw[i] & 0xFFFF0000u);
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (r >= nr) continue;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) g[r] = fma(us[r][8 * c8 + i], vd[i], g[r]);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (r >= nr || s > tf + r / gq) continue;
+      const double pk = pdb[(size_t)r * L + s], gs = two_dm * g[r];
+      gb[r] += pk * gs;
+      pfb[(size_t)r * L + s] = (pk - pfb[(size_t)r * L + s]) + c.lam * pk * gs;  // this thread's token
+    }
+  }
+  block_reduce_n<R, false>(gb, red);
+  const double inv_rows = 1.0 / (double)S.nrows;
+  for (int s = tid; s < L; s += blockDim.x) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (r >= nr) continue;
+      const int tr = tf + r / gq;
+      const bool q2 = s <= tr && int2_token(s, tr, c.sink, c.recent);
+      const double pk = pdb[(size_t)r * L + s];
+      pdb[(size_t)r * L + s] = q2 ? (pfb[(size_t)r * L + s] - c.lam * pk * gb[r]) * inv_rows : 0.0;
+    }
+  }
 }
 
 // Gradient w.r.t. the effective rows: gx[s] = sum over the rows r of s's sequence of pd[r][s] y_r
@@ -655,8 +902,9 @@ size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 
 size_t cal_set_bytes(int T, int nseq, int nrows, long long pelems, int H) {
   const size_t rows = (size_t)T * H * kD;
-  return up256(sizeof(CalSeq) * (size_t)nseq) + up256(sizeof(int) * (size_t)nrows) + 4 * up256(rows * 8) +
-         up256(rows) + up256((size_t)H * pelems * 8) + up256((size_t)H * nrows * kD * 8) + up256((size_t)H * nrows * 8);
+  return up256(sizeof(CalSeq) * (size_t)nseq) + up256(sizeof(int4) * (size_t)nrows) + up256(sizeof(int) * (size_t)nrows) + 4 * up256(rows * 8) +
+         up256(rows) + 2 * up256((size_t)H * pelems * 8) + 2 * up256((size_t)H * nrows * kD * 8) +
+         up256((size_t)H * nrows * 8);
 }
 
 size_t cal_shared_bytes(int H, int Hq) {
@@ -691,10 +939,22 @@ hipError_t cal_bind_set(CalSet& set, uint8_t* base, const uint16_t* k, const uin
   set.nrows = rows;
   set.pelems = pel;
   set.maxlen = maxlen;
+  // tiles of up to kTileRows rows: 16 / gq positions of one sequence at a time
+  std::vector<int4> tiles;
+  const int per = gq >= kTileRows ? 1 : kTileRows / gq;
+  for (int i = 0; i < nseq; ++i) {
+    const CalSeq& cs = seqs[i];
+    const int npos = cs.len - cs.t0;
+    for (int pp = 0; pp < npos; pp += per)
+      tiles.push_back(make_int4(i, cs.row0 + pp * gq, min(per, npos - pp) * gq, cs.t0 + pp));
+  }
+  set.ntiles = (int)tiles.size();
   const size_t nrow_el = (size_t)set.T * H * kD;
   uint8_t* p = base;
   set.seqs = reinterpret_cast<CalSeq*>(p);
   p += up256(sizeof(CalSeq) * (size_t)nseq);
+  set.tiles = reinterpret_cast<int4*>(p);
+  p += up256(sizeof(int4) * (size_t)rows);
   set.row_seq = reinterpret_cast<int*>(p);
   p += up256(sizeof(int) * (size_t)rows);
   set.zhat = reinterpret_cast<double*>(p);
@@ -709,12 +969,18 @@ hipError_t cal_bind_set(CalSet& set, uint8_t* base, const uint16_t* k, const uin
   p += up256(nrow_el);
   set.pd = reinterpret_cast<double*>(p);
   p += up256((size_t)H * pel * 8);
+  set.pf = reinterpret_cast<double*>(p);
+  p += up256((size_t)H * pel * 8);
   set.wrow = reinterpret_cast<double*>(p);
+  p += up256((size_t)H * rows * kD * 8);
+  set.urow = reinterpret_cast<double*>(p);
   p += up256((size_t)H * rows * kD * 8);
   set.lrow = reinterpret_cast<double*>(p);
   hipError_t e = hipMemcpyAsync(set.seqs, seqs.data(), sizeof(CalSeq) * nseq, hipMemcpyHostToDevice, s);
   if (e == hipSuccess && rows > 0)
     e = hipMemcpyAsync(set.row_seq, row_seq.data(), sizeof(int) * rows, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && !tiles.empty())
+    e = hipMemcpyAsync(set.tiles, tiles.data(), sizeof(int4) * tiles.size(), hipMemcpyHostToDevice, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);  // the host tables go out of scope
   return e;
 }
@@ -739,14 +1005,6 @@ hipError_t cal_gram(const CalCfg& c, const uint16_t* W_o, hipStream_t s) {
   return hipGetLastError();
 }
 
-static size_t attn_lds(const CalSet& set) {
-  const size_t bytes = 3 * (size_t)(set.maxlen > 0 ? set.maxlen : 1) * sizeof(double);
-  if (bytes > 48 * 1024)  // beyond the default dynamic LDS limit: raise it for this kernel (up to 96 KiB)
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&cal_attn_kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-  return bytes;
-}
-
 static void rot_and_quant(const CalCfg& c, CalSet& set, const double* A, int value, hipStream_t s) {
   hipLaunchKernelGGL(cal_expm_kernel, dim3(c.H), dim3(kExpThreads), 0, s, c, A, value);
   if (set.T > 0)
@@ -766,10 +1024,21 @@ static void backward(const CalCfg& c, CalSet& set, const double* A, int value, d
   hipLaunchKernelGGL(cal_expm_grad_kernel, dim3(c.H), dim3(kExpThreads), 0, s, c, A, value, grad);
 }
 
+// the tile kernels: one block per (tile, KV head)
+#define CAL_POS_LAUNCH(KERNEL, ...) \
+  hipLaunchKernelGGL(KERNEL, dim3(set.ntiles, c.H), dim3(kTileThreads), 0, s, __VA_ARGS__)
+
+static void u_launch(const CalCfg& c, const CalSet& set, int value, hipStream_t s) {
+  const int npos = set.nrows / c.gq;
+  hipLaunchKernelGGL(cal_u_kernel, dim3(c.Hq, (npos + kUTile - 1) / kUTile), dim3(256), 0, s, set, c, value);
+}
+
 hipError_t cal_key_loss(const CalCfg& c, CalSet& set, const double* A, double* loss, double* grad, hipStream_t s) {
   rot_and_quant(c, set, A, 0, s);
   if (set.nrows > 0) {
-    hipLaunchKernelGGL(cal_attn_kernel, dim3(set.nrows, c.H), dim3(256), attn_lds(set), s, set, c, 0);
+    CAL_POS_LAUNCH(cal_pos_fwd_kernel, set, c, 0);
+    u_launch(c, set, 0, s);
+    if (grad) CAL_POS_LAUNCH(cal_pos_grad_kernel, set, c);
     hipLaunchKernelGGL(cal_loss_kernel, dim3(c.H), dim3(256), 0, s, set.lrow, set.nrows, loss);
   } else {
     hipLaunchKernelGGL(cal_fill_kernel, dim3(1), dim3(256), 0, s, loss, (size_t)c.H, 0.0);
@@ -787,14 +1056,15 @@ hipError_t cal_key_loss(const CalCfg& c, CalSet& set, const double* A, double* l
 
 hipError_t cal_key_probs(const CalCfg& c, CalSet& set, const double* A, hipStream_t s) {
   rot_and_quant(c, set, A, 0, s);
-  if (set.nrows > 0) hipLaunchKernelGGL(cal_attn_kernel, dim3(set.nrows, c.H), dim3(256), attn_lds(set), s, set, c, 1);
+  if (set.nrows > 0) CAL_POS_LAUNCH(cal_pos_fwd_kernel, set, c, 1);
   return hipGetLastError();
 }
 
 hipError_t cal_value_loss(const CalCfg& c, CalSet& set, const double* A, double* loss, double* grad, hipStream_t s) {
   rot_and_quant(c, set, A, 1, s);
   if (set.nrows > 0) {
-    hipLaunchKernelGGL(cal_vrow_kernel, dim3(set.nrows, c.H), dim3(kD), 0, s, set, c);
+    CAL_POS_LAUNCH(cal_pos_val_kernel, set, c);
+    u_launch(c, set, 1, s);
     hipLaunchKernelGGL(cal_loss_kernel, dim3(c.H), dim3(256), 0, s, set.lrow, set.nrows, loss);
   } else {
     hipLaunchKernelGGL(cal_fill_kernel, dim3(1), dim3(256), 0, s, loss, (size_t)c.H, 0.0);
