@@ -640,44 +640,71 @@ __global__ __launch_bounds__(256) void cal_dr_reduce_kernel(CalCfg c) {
 // Matrix functions: one work-group of 1024 threads per KV head; thread (4 rows, 4 columns) of a
 // 128 x 128 product, operands staged through LDS in 16-wide slices.
 struct ExpLds {
-  double as[kD][17];
-  double bs[16][kD];
+  double at[16][kD];  // op(A)^T chunk: at[k][r] = op(A)[r][k0 + k]
+  double bs[16][kD];  // B chunk: bs[k][c] = B[k0 + k][c]
   double red[16];
 };
 
-// acc += op(A) B for 128 x 128 fp64 matrices in global memory (op(A) = A or A^T). Ends with a
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+// Output fragment of wg_gemm: a thread's acc[t][v] is the element (frag_row(v), frag_col(t)) of the
+// 128 x 128 product. Wave w covers rows 16 (w / 2) .. + 15 and columns 64 (w % 2) .. + 63 as four
+// 16 x 16 matrix-core tiles; lane l holds rows l / 16 + 4 v, column l % 16 of tile t.
+__device__ __forceinline__ int frag_row(int v) {
+  return 16 * (threadIdx.x >> 7) + ((threadIdx.x & 63) >> 4) + 4 * v;
+}
+__device__ __forceinline__ int frag_col(int t) {
+  return 64 * ((threadIdx.x >> 6) & 1) + 16 * t + (threadIdx.x & 15);
+}
+
+// Fragment element (t, v) sits at offset frag_base() + frag_step(t, v) of a row-major 128 x 128 matrix.
+__device__ __forceinline__ unsigned frag_base() { return (unsigned)(frag_row(0) * kD + frag_col(0)); }
+constexpr unsigned frag_step(int t, int v) { return (unsigned)(4 * v * kD + 16 * t); }
+
+// M[fragment] = acc * scale (+ I when add_identity).
+__device__ __forceinline__ void frag_store(double* __restrict__ M, const f64x4 (&acc)[4], double scale,
+                                           bool add_identity) {
+  unsigned fb = frag_base();
+  // computed here, at the store: hoisted out of the callers' loops, the 32 addresses would not
+  // fit the register budget of a 1024-thread block
+  asm volatile("" : "+v"(fb));
+  double* __restrict__ Mf = M + fb;
+  const int r0 = frag_row(0), c0 = frag_col(0);
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      Mf[frag_step(t, v)] = (add_identity && r0 + 4 * v == c0 + 16 * t ? 1.0 : 0.0) + acc[t][v] * scale;
+}
+
+// acc += op(A) B for 128 x 128 fp64 matrices in global memory (op(A) = A or A^T) on the fp64
+// matrix cores (16 x 16 x 4 steps), 16-deep chunks of A and B staged through LDS. Ends with a
 // barrier, so the caller may overwrite A or B right after.
-__device__ void wg_gemm(const double* A, bool ta, const double* B, double (&acc)[4][4], ExpLds& sm) {
-  const int tid = threadIdx.x, tr = tid >> 5, tc = tid & 31;
+__device__ __forceinline__ void wg_gemm(const double* A, bool ta, const double* B, f64x4 (&acc)[4], ExpLds& sm) {
+  const int tid = threadIdx.x, l = tid & 63;
+  const int ar = 16 * (tid >> 7) + (l & 15), kl = l >> 4, bc = 64 * ((tid >> 6) & 1) + (l & 15);
+#pragma unroll 1
   for (int k0 = 0; k0 < kD; k0 += 16) {
     for (int e = tid; e < kD * 16; e += kExpThreads) {
-      const int r = e >> 4, kk = e & 15;
-      sm.as[r][kk] = ta ? A[(k0 + kk) * kD + r] : A[r * kD + k0 + kk];
-      const int kb = e >> 7, cb = e & 127;
-      sm.bs[kb][cb] = B[(k0 + kb) * kD + cb];
+      const int kk = e >> 7, r = e & 127;
+      sm.at[kk][r] = ta ? A[(k0 + kk) * kD + r] : A[r * kD + k0 + kk];
+      sm.bs[kk][r] = B[(k0 + kk) * kD + r];
     }
     __syncthreads();
-#pragma unroll 2
-    for (int kk = 0; kk < 16; ++kk) {
-      double av[4], bv[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) av[i] = sm.as[4 * tr + i][kk];
+    for (int k4 = 0; k4 < 16; k4 += 4) {
+      const double av = sm.at[k4 + kl][ar];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) bv[i] = sm.bs[kk][4 * tc + i];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) acc[i][q] = fma(av[i], bv[q], acc[i][q]);
+      for (int t = 0; t < 4; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, sm.bs[k4 + kl][bc + 16 * t], acc[t], 0, 0, 0);
     }
     __syncthreads();
   }
 }
 
-__device__ __forceinline__ void zero4(double (&a)[4][4]) {
+__device__ __forceinline__ void zero4(f64x4 (&a)[4]) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) a[i][q] = 0.0;
+  for (int t = 0; t < 4; ++t) a[t] = f64x4{0.0, 0.0, 0.0, 0.0};
 }
 
 // X <- (A - A^T) * 2^-sc with sc the smallest scaling giving ||X||_1 <= 1/2 (returned); with
@@ -703,7 +730,7 @@ __device__ int wg_skew_scaled(const double* A, double* X, bool transpose, ExpLds
 // Forward: R = R0 exp(A - A^T) and Rt = R^T (fp64) for every head.
 __global__ __launch_bounds__(kExpThreads) void cal_expm_kernel(CalCfg c, const double* __restrict__ Aall, int value) {
   __shared__ ExpLds sm;
-  const int h = blockIdx.x, tid = threadIdx.x, tr = tid >> 5, tc = tid & 31;
+  const int h = blockIdx.x, tid = threadIdx.x;
   double* ex = c.ex + (size_t)h * kCalScratch * kMat;
   double *X = ex, *P = ex + kMat, *R0 = ex + 2 * kMat;
   const float* R0f = (value ? c.R0v : c.R0k) + (size_t)h * kMat;
@@ -712,47 +739,36 @@ __global__ __launch_bounds__(kExpThreads) void cal_expm_kernel(CalCfg c, const d
     P[e] = (e >> 7) == (e & 127) ? 1.0 : 0.0;
   }
   const int sc = wg_skew_scaled(Aall + (size_t)h * kMat, X, false, sm);
-  double acc[4][4];
+  f64x4 acc[4];
   for (int k = kExpTerms; k >= 1; --k) {  // P <- I + X P / k
     zero4(acc);
     wg_gemm(X, false, P, acc, sm);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r = 4 * tr + i, cc = 4 * tc + q;
-        P[r * kD + cc] = (r == cc ? 1.0 : 0.0) + acc[i][q] / (double)k;
-      }
+    frag_store(P, acc, 1.0 / (double)k, true);
     __syncthreads();
   }
   for (int i = 0; i < sc; ++i) {  // P <- P P
     zero4(acc);
     wg_gemm(P, false, P, acc, sm);
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) P[(4 * tr + a) * kD + 4 * tc + q] = acc[a][q];
+    frag_store(P, acc, 1.0, false);
     __syncthreads();
   }
   zero4(acc);
   wg_gemm(R0, false, P, acc, sm);
   double* R = c.R + (size_t)h * kMat;
   double* Rt = c.Rt + (size_t)h * kMat;
+  frag_store(R, acc, 1.0, false);
+  const int r0 = frag_row(0), c0 = frag_col(0);
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int t = 0; t < 4; ++t)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = 4 * tr + a, cc = 4 * tc + q;
-      R[r * kD + cc] = acc[a][q];
-      Rt[cc * kD + r] = acc[a][q];
-    }
+    for (int v = 0; v < 4; ++v) Rt[(unsigned)((c0 + 16 * t) * kD + r0 + 4 * v)] = acc[t][v];
 }
 
 // Backward: grad = dS - dS^T with dS = L_exp(S^T, R0^T dR), S = A - A^T, for every head.
 __global__ __launch_bounds__(kExpThreads) void cal_expm_grad_kernel(CalCfg c, const double* __restrict__ Aall,
                                                                    int value, double* __restrict__ grad) {
   __shared__ ExpLds sm;
-  const int h = blockIdx.x, tid = threadIdx.x, tr = tid >> 5, tc = tid & 31;
+  const int h = blockIdx.x, tid = threadIdx.x;
   double* ex = c.ex + (size_t)h * kCalScratch * kMat;
   double *X = ex, *P1 = ex + kMat, *R0 = ex + 2 * kMat, *P2 = ex + 3 * kMat, *Gs = ex + 4 * kMat;
   const float* R0f = (value ? c.R0v : c.R0k) + (size_t)h * kMat;
@@ -763,55 +779,31 @@ __global__ __launch_bounds__(kExpThreads) void cal_expm_grad_kernel(CalCfg c, co
   }
   const int sc = wg_skew_scaled(Aall + (size_t)h * kMat, X, true, sm);
   const double f = ldexp(1.0, -sc);
-  double acc[4][4];
+  f64x4 acc[4], t1[4];
   zero4(acc);
   wg_gemm(R0, true, c.dr + (size_t)h * kMat, acc, sm);  // G_E = R0^T dR, scaled like X
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) Gs[(4 * tr + a) * kD + 4 * tc + q] = acc[a][q] * f;
+  frag_store(Gs, acc, f, false);
   __syncthreads();
-  // Taylor on the block matrix [[X, Gs], [0, X]]: (P1, P2) <- (I + X P1 / k, (X P2 + Gs P1) / k),
-  // one product sum at a time (T1 holds X P1 until P2 is formed)
-  double* T1 = ex + 5 * kMat;
+  // Taylor on the block matrix [[X, Gs], [0, X]]: (P1, P2) <- (I + X P1 / k, (X P2 + Gs P1) / k);
+  // t1 holds X P1 in registers until P2 is formed
   for (int k = kExpTerms; k >= 1; --k) {
-    zero4(acc);
-    wg_gemm(X, false, P1, acc, sm);
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) T1[(4 * tr + a) * kD + 4 * tc + q] = acc[a][q];
+    zero4(t1);
+    wg_gemm(X, false, P1, t1, sm);
     zero4(acc);
     wg_gemm(X, false, P2, acc, sm);
     wg_gemm(Gs, false, P1, acc, sm);
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r = 4 * tr + a, cc = 4 * tc + q;
-        P2[r * kD + cc] = acc[a][q] / (double)k;
-        P1[r * kD + cc] = (r == cc ? 1.0 : 0.0) + T1[r * kD + cc] / (double)k;  // own elements of T1
-      }
+    frag_store(P2, acc, 1.0 / (double)k, false);
+    frag_store(P1, t1, 1.0 / (double)k, true);
     __syncthreads();
   }
   for (int i = 0; i < sc; ++i) {  // (P1, P2) <- (P1 P1, P1 P2 + P2 P1)
-    zero4(acc);
-    wg_gemm(P1, false, P1, acc, sm);
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) T1[(4 * tr + a) * kD + 4 * tc + q] = acc[a][q];
+    zero4(t1);
+    wg_gemm(P1, false, P1, t1, sm);
     zero4(acc);
     wg_gemm(P1, false, P2, acc, sm);
     wg_gemm(P2, false, P1, acc, sm);
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r = 4 * tr + a, cc = 4 * tc + q;
-        P2[r * kD + cc] = acc[a][q];
-        P1[r * kD + cc] = T1[r * kD + cc];
-      }
+    frag_store(P2, acc, 1.0, false);
+    frag_store(P1, t1, 1.0, false);
     __syncthreads();
   }
   double* g = grad + (size_t)h * kMat;
