@@ -308,26 +308,26 @@ __device__ __forceinline__ void dma_pair(uint32_t a_lo, uint32_t a_hi, uint32_t 
     asm volatile(
         "s_mov_b32 m0, %0\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %3, %4\n\t"
+        "global_load_lds_dwordx4 %3, %4 nt\n\t"
         "s_mov_b32 m0, %1\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %3, %5\n\t"
+        "global_load_lds_dwordx4 %3, %5 nt\n\t"
         "s_mov_b32 m0, %2\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %6, off" ::"s"(lds_addr),
+        "global_load_lds_dwordx4 %6, off nt" ::"s"(lds_addr),
         "s"(lds_addr + 1024), "s"(lds_addr + 2048), "v"(voff16), "s"(ra), "s"(rb), "v"(maddr)
         : "memory", "m0");
   } else {
     asm volatile(
         "s_mov_b32 m0, %0\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %3, %4\n\t"
+        "global_load_lds_dwordx4 %3, %4 nt\n\t"
         "s_mov_b32 m0, %1\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %3, %5\n\t"
+        "global_load_lds_dwordx4 %3, %5 nt\n\t"
         "s_mov_b32 m0, %2\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dword %6, off" ::"s"(lds_addr),
+        "global_load_lds_dword %6, off nt" ::"s"(lds_addr),
         "s"(lds_addr + 1024), "s"(lds_addr + 2048), "v"(voff16), "s"(ra), "s"(rb), "v"(maddr)
         : "memory", "m0");
   }
