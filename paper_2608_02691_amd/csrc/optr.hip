@@ -31,6 +31,14 @@ constexpr int kMat = kD * kD;
 constexpr int kRotTile = 16;   // tokens per rotation work-group
 constexpr int kExpTerms = 14;
 constexpr int kExpThreads = 1024;
+
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+// fp64 matrix-core step D += A B for 16 x 4 by 4 x 16 operands: lane l holds A[l % 16][l / 16] and
+// B[l / 16][l % 16]; D[l / 16 + 4 v][l % 16] is element v of its accumulator.
+__device__ __forceinline__ f64x4 mfma64(double a, double b, f64x4 d) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, d, 0, 0, 0);
+}
 constexpr double kInvSqrtD = 0.08838834764831845;  // 1 / sqrt(128)
 
 __device__ __forceinline__ double bf16d(uint16_t b) { return (double)__uint_as_float((uint32_t)b << 16); }
@@ -525,58 +533,98 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_grad_kernel(CalSet S, Ca
 
 // Gradient w.r.t. the effective rows: gx[s] = sum over the rows r of s's sequence of pd[r][s] y_r
 // with y_r = q_r / sqrt(d) (keys) or the row weight (values): per sequence the product
-// P^T Y of its [rows x len] weights and [rows x 128] row vectors. Block (32-token tile, KV head)
-// of 256 threads, 16 rows at a time through LDS; thread (token tt, 16 channels).
-constexpr int kGxTok = 32, kGxRows = 16;
+// P^T Y of its [rows x len] weights and [rows x 128] row vectors, on the fp64 matrix cores. Block
+// (64-token tile, KV head) of four waves, wave w: tokens 16 w .. + 15 x all 128 channels (eight
+// 16 x 16 tiles); 16 rows at a time through LDS, the next chunk fetched into registers while the
+// matrix cores run on the current one.
+constexpr int kGxTok = 64, kGxRows = 16;
+constexpr int kGxPs = kGxTok + 16, kGxYs = kD + 16;  // padded LDS rows: lane groups l / 16 on other banks
 __global__ __launch_bounds__(256) void cal_gx_kernel(CalSet S, CalCfg c, int value) {
-  __shared__ double ps[kGxRows][kGxTok];
-  __shared__ double ys[kGxRows][kD];
+  __shared__ double ps[kGxRows][kGxPs];
+  __shared__ double ys[kGxRows][kGxYs];
   const int h = blockIdx.y, tid = threadIdx.x, s0 = blockIdx.x * kGxTok;
-  const int tt = tid >> 3, cg = tid & 7;
-  double acc[16];
+  const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
+  f64x4 acc[8];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc[i] = 0.0;
+  for (int t = 0; t < 8; ++t) acc[t] = f64x4{0.0, 0.0, 0.0, 0.0};
   int lo = 0, hi = S.nseq - 1;  // the sequence holding token s0
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
     if (S.seqs[mid].start <= s0) lo = mid; else hi = mid - 1;
   }
-  for (int n = lo; n < S.nseq && S.seqs[n].start < s0 + kGxTok; ++n) {
-    const CalSeq sq = S.seqs[n];
-    const int nr = (sq.len - sq.t0) * c.gq;
+  // chunk (sequence n, rows r0 .. r0 + 15) into registers: 4 weights and 8 row entries per thread
+  double pr[4], yr[8];
+  auto fetch = [&](const CalSeq& sq, int nr, int r0) {
     const double* pd = S.pd + (size_t)h * S.pelems + sq.p0;
-    for (int r0 = 0; r0 < nr; r0 += kGxRows) {
-      __syncthreads();
-      for (int e = tid; e < kGxRows * kGxTok; e += 256) {
-        const int i = e / kGxTok, x = e % kGxTok, sl = s0 + x - sq.start;
-        ps[i][x] = (r0 + i < nr && sl >= 0 && sl < sq.len) ? pd[(size_t)(r0 + i) * sq.len + sl] : 0.0;
-      }
-      for (int e = tid; e < kGxRows * kD; e += 256) {
-        const int i = e / kD, col = e % kD, lr = r0 + i;
-        double y = 0.0;
-        if (lr < nr) {
-          if (value) {
-            y = S.wrow[((size_t)h * S.nrows + sq.row0 + lr) * kD + col];
-          } else {
-            const int t = sq.t0 + lr / c.gq, j = h * c.gq + lr % c.gq;
-            y = bf16d(S.q[((size_t)(sq.start + t) * c.Hq + j) * kD + col]) * kInvSqrtD;
-          }
-        }
-        ys[i][col] = y;
-      }
-      __syncthreads();
-#pragma unroll 4
-      for (int i = 0; i < kGxRows; ++i) {
-        const double p = ps[i][tt];
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[q] = fma(p, ys[i][cg * 16 + q], acc[q]);
+    for (int u = 0; u < 4; ++u) {
+      const int e = tid + 256 * u, i = e / kGxTok, x = e % kGxTok, sl = s0 + x - sq.start;
+      pr[u] = (r0 + i < nr && sl >= 0 && sl < sq.len) ? pd[(size_t)(r0 + i) * sq.len + sl] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = tid + 256 * u, i = e / kD, col = e % kD, lr = r0 + i;
+      double y = 0.0;
+      if (lr < nr) {
+        if (value) {
+          y = S.wrow[((size_t)h * S.nrows + sq.row0 + lr) * kD + col];
+        } else {
+          const int t = sq.t0 + lr / c.gq, j = h * c.gq + lr % c.gq;
+          y = bf16d(S.q[((size_t)(sq.start + t) * c.Hq + j) * kD + col]) * kInvSqrtD;
+        }
       }
+      yr[u] = y;
+    }
+  };
+  int n = lo, r0 = 0;
+  CalSeq sq = S.seqs[n];
+  int nr = (sq.len - sq.t0) * c.gq;
+  // the chunks: rows of every sequence that meets the tile, in order
+  auto valid = [&]() { return n < S.nseq && sq.start < s0 + kGxTok; };
+  auto advance = [&]() {
+    r0 += kGxRows;
+    while (valid() && r0 >= nr) {
+      if (++n >= S.nseq) break;
+      sq = S.seqs[n];
+      nr = (sq.len - sq.t0) * c.gq;
+      r0 = 0;
+    }
+  };
+  if (valid() && nr == 0) {  // a sequence without query rows contributes nothing
+    r0 = -kGxRows;
+    advance();
+  }
+  if (valid()) fetch(sq, nr, r0);
+  while (valid()) {
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = tid + 256 * u;
+      ps[e / kGxTok][e % kGxTok] = pr[u];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = tid + 256 * u;
+      ys[e / kD][e % kD] = yr[u];
+    }
+    __syncthreads();
+    advance();
+    if (valid()) fetch(sq, nr, r0);
+#pragma unroll
+    for (int k4 = 0; k4 < kGxRows; k4 += 4) {
+      const double a = ps[k4 + lk][16 * w + li];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) acc[t] = mfma64(a, ys[k4 + lk][16 * t + li], acc[t]);
     }
   }
-  if (s0 + tt < S.T) {
-    double* out = S.gx + ((size_t)(s0 + tt) * c.H + h) * kD + cg * 16;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) out[q] = acc[q];
+  for (int v = 0; v < 4; ++v) {
+    const int s = s0 + 16 * w + lk + 4 * v;
+    if (s < S.T) {
+      double* out = S.gx + ((size_t)s * c.H + h) * kD + li;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) out[16 * t] = acc[t][v];
+    }
   }
 }
 
@@ -645,8 +693,6 @@ struct ExpLds {
   double red[16];
 };
 
-typedef double f64x4 __attribute__((ext_vector_type(4)));
-
 // Output fragment of wg_gemm: a thread's acc[t][v] is the element (frag_row(v), frag_col(t)) of the
 // 128 x 128 product. Wave w covers rows 16 (w / 2) .. + 15 and columns 64 (w % 2) .. + 63 as four
 // 16 x 16 matrix-core tiles; lane l holds rows l / 16 + 4 v, column l % 16 of tile t.
@@ -696,7 +742,7 @@ __device__ __forceinline__ void wg_gemm(const double* A, bool ta, const double* 
       const double av = sm.at[k4 + kl][ar];
 #pragma unroll
       for (int t = 0; t < 4; ++t)
-        acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, sm.bs[k4 + kl][bc + 16 * t], acc[t], 0, 0, 0);
+        acc[t] = mfma64(av, sm.bs[k4 + kl][bc + 16 * t], acc[t]);
     }
     __syncthreads();
   }
