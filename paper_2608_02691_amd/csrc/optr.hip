@@ -184,201 +184,279 @@ __device__ void block_reduce_n(double (&x)[MAXG], double* red) {
   }
 }
 
-// The per-position kernels take a tile of up to kTileRows rows: 16 / G_q consecutive query
-// positions of one sequence with all their query heads (tiles[i] = (sequence, first row, rows,
-// position of the first row)), so each key and value row is loaded once for the whole tile.
-// Row r of a tile is position t_first + r / G_q, query head h G_q + r % G_q.
+// The tile kernels take a tile of up to kTileRows rows: 16 / G_q consecutive query positions of
+// one sequence with all their query heads (tiles[i] = (sequence, first row, rows, position of the
+// first row)), so each key and value row is loaded once for the whole tile. Row r of a tile is
+// position t_first + r / G_q, query head h G_q + r % G_q. The row x token and row x channel
+// products run on the fp64 matrix cores with the tile's 16 rows as the M dimension.
 constexpr int kTileRows = 16;
-constexpr int kTileThreads = 256;  // threads of the tile kernels; one token per thread per chunk
-constexpr int kDlStride = 18;      // doubles per token of the staged differences (16-byte rows, 4-way writes)
+constexpr int kTileThreads = 256;  // four waves; one token per thread in the softmax passes
+constexpr int kDlStride = 18;      // doubles per token of the staged row weights (16-byte rows)
 
-// dO accumulation layout of the tile kernels: thread (column pair cp = tid % 64, quarter qt =
-// tid / 64 of each token chunk), acc[r][0..1] = rows r, columns 2 cp and 2 cp + 1. Sums the four
-// quarters in the fixed order (q0 + q2) + (q1 + q3) through buf (2 R 128 doubles of LDS, free on
-// entry) and stores rows r < nr at out + r 128.
-template <int R>
-__device__ __forceinline__ void sum_quarters_store(double (&acc)[R][2], double* buf, double* out, int nr) {
-  const int cp = threadIdx.x & 63, qt = threadIdx.x >> 6;
-  double2* b2 = reinterpret_cast<double2*>(buf);
-  __syncthreads();
-  if (qt >= 2)
+__device__ __forceinline__ void bf16x8_to_f64(uint4 u, double (&d)[8]) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-    for (int r = 0; r < R; ++r) b2[((qt - 2) * R + r) * (kD / 2) + cp] = make_double2(acc[r][0], acc[r][1]);
-  __syncthreads();
-  if (qt < 2)
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const double2 o = b2[(qt * R + r) * (kD / 2) + cp];
-      acc[r][0] += o.x;
-      acc[r][1] += o.y;
-    }
-  __syncthreads();
-  if (qt == 1)
-#pragma unroll
-    for (int r = 0; r < R; ++r) b2[r * (kD / 2) + cp] = make_double2(acc[r][0], acc[r][1]);
-  __syncthreads();
-  if (qt == 0)
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const double2 o = b2[r * (kD / 2) + cp];
-      if (r < nr)
-        reinterpret_cast<double2*>(out + (size_t)r * kD)[cp] = make_double2(acc[r][0] + o.x, acc[r][1] + o.y);
-    }
-}
-
-// acc[r][.] += d[r] (w0, w1) for one token, d = the token's staged row of R doubles (16-byte aligned).
-template <int R>
-__device__ __forceinline__ void acc_token(double (&acc)[R][2], const double* d, double w0, double w1) {
-  const double2* d2 = reinterpret_cast<const double2*>(d);
-#pragma unroll
-  for (int r2 = 0; r2 < R / 2; ++r2) {
-    const double2 x = d2[r2];
-    acc[2 * r2][0] = fma(x.x, w0, acc[2 * r2][0]);
-    acc[2 * r2][1] = fma(x.x, w1, acc[2 * r2][1]);
-    acc[2 * r2 + 1][0] = fma(x.y, w0, acc[2 * r2 + 1][0]);
-    acc[2 * r2 + 1][1] = fma(x.y, w1, acc[2 * r2 + 1][1]);
+  for (int i = 0; i < 4; ++i) {
+    d[2 * i] = (double)__uint_as_float(w[i] << 16);
+    d[2 * i + 1] = (double)__uint_as_float(w[i] & 0xFFFF0000u);
   }
 }
+
+// Row operand of a tile in matrix-core form: lane (li, lk) holds x[row li][32 lk + m], m = 0..31, for
+// the contraction over 128 channels taken as 32 steps m whose 4-deep slices are channels 32 k + m
+// (k = 0..3); rows li >= nr are zero. From bf16 (queries) or fp64 (row vectors) storage.
+__device__ __forceinline__ void rows_operand_bf16(const uint16_t* row, bool ok, int lk, double (&x)[32]) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    double d[8];
+    bf16x8_to_f64(ok ? *reinterpret_cast<const uint4*>(row + 32 * lk + 8 * g) : make_uint4(0, 0, 0, 0), d);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[8 * g + i] = d[i];
+  }
+}
+
+// Logits of 16 rows against the 16 tokens of a tile (token li of this lane's B operand): acc +=
+// x . y_token with y the token's bf16 row; the same slice convention as rows_operand_*.
+__device__ __forceinline__ f64x4 dot_tokens_bf16(const double (&x)[32], const uint16_t* yrow, bool ok, int lk) {
+  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    double d[8];
+    bf16x8_to_f64(ok ? *reinterpret_cast<const uint4*>(yrow + 32 * lk + 8 * g) : make_uint4(0, 0, 0, 0), d);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc = mfma64(x[8 * g + i], d[i], acc);
+  }
+  return acc;
+}
+__device__ __forceinline__ f64x4 dot_tokens_f64(const double (&x)[32], const double* yrow, bool ok, int lk) {
+  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+  const double2* y2 = reinterpret_cast<const double2*>(yrow + 32 * lk);
+#pragma unroll
+  for (int g = 0; g < 16; ++g) {
+    const double2 y = ok ? y2[g] : make_double2(0.0, 0.0);
+    acc = mfma64(x[2 * g], y.x, acc);
+    acc = mfma64(x[2 * g + 1], y.y, acc);
+  }
+  return acc;
+}
+
+// Row x channel accumulation: acc[t] (t = 0..7) += A B with A[row li][token lk] = a and
+// B[token lk][column li] = y[t], the token's channel 8 li + t. Result element v of acc[t]: row
+// lk + 4 v, channel 8 li + t.
+__device__ __forceinline__ void acc_channels(f64x4 (&acc)[8], double a, const double (&y)[8]) {
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = mfma64(a, y[t], acc[t]);
+}
+
+// Sums the four waves' channel accumulators in the fixed order (w0 + w2) + (w1 + w3) through buf
+// (32 KiB of LDS, free on entry) and stores rows r < nr at out + r 128 (row lk + 4 v, channel 8 li + t).
+__device__ __forceinline__ void sum_waves_store(f64x4 (&acc)[8], double* buf, double* out, int nr) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, li = l & 15, lk = l >> 4;
+  __syncthreads();
+  if (w >= 2)
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) buf[((w - 2) * 32 + 4 * t + v) * 64 + l] = acc[t][v];
+  __syncthreads();
+  if (w < 2)
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[t][v] += buf[(w * 32 + 4 * t + v) * 64 + l];
+  __syncthreads();
+  if (w == 1)
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) buf[(4 * t + v) * 64 + l] = acc[t][v];
+  __syncthreads();
+  if (w == 0)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int r = lk + 4 * v;
+      double o[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) o[t] = acc[t][v] + buf[(4 * t + v) * 64 + l];
+      if (r < nr) {
+        double2* dst = reinterpret_cast<double2*>(out + (size_t)r * kD + 8 * li);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dst[i] = make_double2(o[2 * i], o[2 * i + 1]);
+      }
+    }
+}
+
+// Row maxima from the matrix-core layout (m4[v]: this lane's value for row lk + 4 v): over the 16
+// lanes of each lk group, then over the four waves through red4 ([4][16] doubles). Returns the
+// maxima of rows 4 w .. 4 w + 3, the rows wave w owns in the softmax passes.
+__device__ __forceinline__ void rows_max(const double (&m4)[4], double* red4, double (&m)[4]) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, li = l & 15, lk = l >> 4;
+  double x[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    x[v] = m4[v];
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) x[v] = fmax(x[v], __shfl_xor(x[v], off));
+  }
+  __syncthreads();
+  if (li == 0)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) red4[w * 16 + lk + 4 * v] = x[v];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 4 * w + i;
+    m[i] = fmax(fmax(red4[r], red4[16 + r]), fmax(red4[32 + r], red4[48 + r]));
+  }
+}
+
+// The tile's 4-token steps of a 256-token chunk for wave w: tokens 64 w + k4 + lk, k4 = 0, 4, ..., 60,
+// those below end.
 
 // Forward of the key objective on a tile: logits over the full-precision and the effective keys,
 // both softmaxes, KL(p || p^K) into lrow, p into pf and p^K into pd (per row, every token of the
 // sequence; 0 past the row's position), and dO = sum_s (p^K - p) v_s into wrow. With probs_only:
 // pd = p^K on the tokens read from INT2 and 0 elsewhere, nothing else. Block (tile, KV head).
+// Logits: q.(k - mu) = q.k - q.mu, with q.mu once per row.
 __global__ __launch_bounds__(kTileThreads) void cal_pos_fwd_kernel(CalSet S, CalCfg c, int probs_only) {
   constexpr int R = kTileRows;
-  __shared__ double qs[R][kD];
-  __shared__ double mus[kD];
-  __shared__ double red[16 * R];
+  __shared__ double qmu[R];
+  __shared__ double red4[2][4 * R];
   __shared__ __align__(16) double dl[kTileThreads * kDlStride];
   const int h = blockIdx.y, tid = threadIdx.x, gq = c.gq;
+  const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
   const int4 tile = S.tiles[blockIdx.x];
   const CalSeq sq = S.seqs[tile.x];
   const int row0 = tile.y, nr = tile.z, tf = tile.w, a0 = sq.start, L = sq.len;
   const int tmax = tf + (nr - 1) / gq;
-  for (int e = tid; e < R * kD; e += blockDim.x) {
-    const int r = e / kD, col = e % kD;
-    qs[r][col] = r < nr ? bf16d(S.q[((size_t)(a0 + tf + r / gq) * c.Hq + h * gq + r % gq) * kD + col]) : 0.0;
-  }
-  if (tid < kD) mus[tid] = (double)c.mu[h * kD + tid];
-  __syncthreads();
   // rows of the tile are consecutive rows of the sequence's [rows][len] blocks
   double* pdb = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;  // row r at + r L
   double* pfb = S.pf + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
-  double mf[R], mk[R];
+  double qa[32];
+  rows_operand_bf16(S.q + ((size_t)(a0 + tf + li / gq) * c.Hq + h * gq + li % gq) * kD, li < nr, lk, qa);
+  {
+    double t = 0.0;
 #pragma unroll
-  for (int r = 0; r < R; ++r) mf[r] = mk[r] = -INFINITY;
-  for (int s = tid; s <= tmax; s += blockDim.x) {
-    const bool any_q2 = int2_token(s, tmax, c.sink, c.recent);  // some row reads s from INT2
+    for (int m = 0; m < 32; ++m) t = fma(qa[m], (double)c.mu[h * kD + 32 * lk + m], t);
+    t += __shfl_xor(t, 16);
+    t += __shfl_xor(t, 32);
+    if (w == 0 && lk == 0) qmu[li] = t;
+  }
+  __syncthreads();
+  // logits: wave w takes the 16-token tiles w, w + 4, ...; lane (li, lk) ends with rows lk + 4 v of
+  // token 16 tt + li
+  double m4f[4], m4k[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) m4f[v] = m4k[v] = -INFINITY;
+  for (int tt = w; 16 * tt <= tmax; tt += 4) {
+    const int s = 16 * tt + li;
+    const bool ok = s <= tmax;
     const size_t o = ((size_t)(a0 + s) * c.H + h) * kD;
-    const uint4* kr = reinterpret_cast<const uint4*>(S.k + o);
-    const double2* xr = reinterpret_cast<const double2*>(S.xeff + o);
-    double af[R], ak[R];
+    const f64x4 af = dot_tokens_bf16(qa, S.k + o, ok, lk);
+    // some row reads a token of this tile from INT2 (uniform over the wave)
+    const bool any_q2 = 16 * tt + 15 >= c.sink && 16 * tt <= tmax - c.recent;
+    f64x4 ak = {0.0, 0.0, 0.0, 0.0};
+    if (any_q2) ak = dot_tokens_f64(qa, S.xeff + o, ok, lk);
 #pragma unroll
-    for (int r = 0; r < R; ++r) af[r] = ak[r] = 0.0;
-    for (int c8 = 0; c8 < kD / 8; ++c8) {
-      const uint4 kk = kr[c8];
-      const uint32_t kw[4] = {kk.x, kk.y, kk.z, kk.w};
-      double kd[8], xd[8];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        kd[2 * i] = (double)__uint_as_float(kw[i] << 16) - mus[8 * c8 + 2 * i];
-        kd[2 * i + 1] = (double)__uint_as_float(kw[i] & 0xFFFF0000u) - mus[8 * c8 + 2 * i + 1];
+    for (int v = 0; v < 4; ++v) {
+      const int r = lk + 4 * v, tr = tf + r / gq;
+      if (r < nr && s <= tr) {
+        const double f = (af[v] - qmu[r]) * kInvSqrtD;
+        const double g = int2_token(s, tr, c.sink, c.recent) ? ak[v] * kInvSqrtD : f;
+        pfb[(size_t)r * L + s] = f;
+        pdb[(size_t)r * L + s] = g;
+        m4f[v] = fmax(m4f[v], f);
+        m4k[v] = fmax(m4k[v], g);
       }
-      if (any_q2) {
+    }
+  }
+  // softmax passes: wave w owns rows rb .. rb + 3 (rb = 4 w), lane l the tokens l, l + 64, ...
+  const int rb = 4 * w;
+  double mf[4], mk[4];
+  rows_max(m4f, red4[0], mf);  // its barriers also make the logits visible to the whole block
+  rows_max(m4k, red4[1], mk);
+  int tr4[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) tr4[i] = rb + i < nr ? tf + (rb + i) / gq : -1;  // last position of each row
+  // e = exp(logit - row max) in place of the logits, the row sums z and, for KL(p || p^K) =
+  // sum_s p_s (f_s - g_s) - (lse_f - lse_k), the sums sum_s e^f_s (f_s - g_s)
+  double zf[4], zk[4], sfg[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) zf[i] = zk[i] = sfg[i] = 0.0;
+  for (int s = l; s <= tmax; s += 64)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (s > tr4[i]) continue;
+      const size_t o = (size_t)(rb + i) * L + s;
+      const double f = pfb[o], g = pdb[o];
+      const double ef = exp(f - mf[i]), ek = exp(g - mk[i]);
+      pfb[o] = ef;  // this lane's own elements
+      pdb[o] = ek;
+      zf[i] += ef;
+      zk[i] += ek;
+      sfg[i] = fma(ef, f - g, sfg[i]);
+    }
+  double kl[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    zf[i] = wave_sum(zf[i]);
+    zk[i] = wave_sum(zk[i]);
+    sfg[i] = wave_sum(sfg[i]);
+    kl[i] = sfg[i] / zf[i] - ((mf[i] + log(zf[i])) - (mk[i] + log(zk[i])));
+    zf[i] = 1.0 / zf[i];  // from here on the reciprocals
+    zk[i] = 1.0 / zk[i];
+  }
+  // probabilities by 256-token chunk (four tokens per lane); dO = sum_s (p^K - p) v_s accumulates
+  // from the chunk's differences staged in LDS (p and p^K are 0 past a row's position)
+  f64x4 acc[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = f64x4{0.0, 0.0, 0.0, 0.0};
+  for (int base = 0; base < L; base += kTileThreads) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = 64 * q + l, s = base + j;
+      double d[4] = {0.0, 0.0, 0.0, 0.0};
+      if (s < L) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const double2 x2 = xr[4 * c8 + i];
-          xd[2 * i] = x2.x;
-          xd[2 * i + 1] = x2.y;
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        if (r >= nr) continue;  // uniform
-#pragma unroll
-        for (int i = 0; i < 8; ++i) af[r] = fma(qs[r][8 * c8 + i], kd[i], af[r]);
-        if (any_q2) {
-#pragma unroll
-          for (int i = 0; i < 8; ++i) ak[r] = fma(qs[r][8 * c8 + i], xd[i], ak[r]);
-        }
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      if (r >= nr) continue;
-      const int tr = tf + r / gq;
-      if (s > tr) continue;  // past the row's position
-      const double f = af[r] * kInvSqrtD;
-      const double g = int2_token(s, tr, c.sink, c.recent) ? ak[r] * kInvSqrtD : f;
-      pfb[(size_t)r * L + s] = f;  // logits first; this thread rewrites them below
-      pdb[(size_t)r * L + s] = g;
-      mf[r] = fmax(mf[r], f);
-      mk[r] = fmax(mk[r], g);
-    }
-  }
-  block_reduce_n<R, true>(mf, red);
-  block_reduce_n<R, true>(mk, red);
-  double zf[R], zk[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) zf[r] = zk[r] = 0.0;
-  for (int s = tid; s <= tmax; s += blockDim.x)
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      if (r >= nr || s > tf + r / gq) continue;
-      zf[r] += exp(pfb[(size_t)r * L + s] - mf[r]);
-      zk[r] += exp(pdb[(size_t)r * L + s] - mk[r]);
-    }
-  block_reduce_n<R, false>(zf, red);
-  block_reduce_n<R, false>(zk, red);
-  double kl[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    kl[r] = 0.0;
-    zf[r] = mf[r] + log(zf[r]);  // log-sum-exp
-    zk[r] = mk[r] + log(zk[r]);
-  }
-  // probabilities chunk by chunk (one token per thread); dO = sum_s (p^K - p) v_s accumulates from
-  // the chunk's differences staged in LDS (p and p^K are 0 past a row's position)
-  const int cp = tid & 63, qt = tid >> 6;
-  double acc[R][2];
-#pragma unroll
-  for (int r = 0; r < R; ++r) acc[r][0] = acc[r][1] = 0.0;
-  for (int base = 0; base < L; base += kTileThreads) {
-    const int s = base + tid;
-    if (s < L) {
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        double pv = 0.0, pk = 0.0;
-        if (r < nr) {
-          const int tr = tf + r / gq;
-          if (s <= tr) {
-            const double lp = pfb[(size_t)r * L + s] - zf[r], lq = pdb[(size_t)r * L + s] - zk[r];
-            pv = exp(lp);
-            pk = exp(lq);
-            kl[r] += pv * (lp - lq);
+          if (tr4[i] < 0) continue;  // a row past the tile
+          const size_t o = (size_t)(rb + i) * L + s;
+          double pv = 0.0, pk = 0.0;
+          if (s <= tr4[i]) {
+            pv = pfb[o] * zf[i];
+            pk = pdb[o] * zk[i];
           }
-          pfb[(size_t)r * L + s] = pv;
-          pdb[(size_t)r * L + s] = probs_only ? (s <= tr && int2_token(s, tr, c.sink, c.recent) ? pk : 0.0) : pk;
+          pfb[o] = pv;
+          pdb[o] = probs_only ? (s <= tr4[i] && int2_token(s, tr4[i], c.sink, c.recent) ? pk : 0.0) : pk;
+          d[i] = pk - pv;
         }
-        dl[tid * kDlStride + r] = pk - pv;
+      }
+      if (!probs_only) {
+        double2* dj = reinterpret_cast<double2*>(dl + j * kDlStride + rb);
+        dj[0] = make_double2(d[0], d[1]);
+        dj[1] = make_double2(d[2], d[3]);
       }
     }
     if (probs_only || base > tmax) continue;  // uniform
     __syncthreads();
     const int end = min(kTileThreads, tmax + 1 - base);
-    for (int j = qt; j < end; j += 4) {
-      const uint32_t vv =
-          *reinterpret_cast<const uint32_t*>(S.v + ((size_t)(a0 + base + j) * c.H + h) * kD + 2 * cp);
-      acc_token<R>(acc, dl + j * kDlStride, (double)__uint_as_float(vv << 16),
-                   (double)__uint_as_float(vv & 0xFFFF0000u));
+    for (int k4 = 0; k4 < 64 && 64 * w + k4 < end; k4 += 4) {
+      const int j = 64 * w + k4 + lk;
+      const bool ok = j < end;
+      double y[8];
+      bf16x8_to_f64(ok ? *reinterpret_cast<const uint4*>(S.v + ((size_t)(a0 + base + j) * c.H + h) * kD + 8 * li)
+                       : make_uint4(0, 0, 0, 0),
+                    y);
+      acc_channels(acc, ok ? dl[j * kDlStride + li] : 0.0, y);
     }
     __syncthreads();
   }
   if (probs_only) return;  // uniform
-  block_reduce_n<R, false>(kl, red);
-  sum_quarters_store<R>(acc, dl, S.wrow + ((size_t)h * S.nrows + row0) * kD, nr);
-  if (tid == 0)
-    for (int r = 0; r < nr; ++r) S.lrow[(size_t)h * S.nrows + row0 + r] = kl[r];
+  sum_waves_store(acc, dl, S.wrow + ((size_t)h * S.nrows + row0) * kD, nr);
+  if (l == 0)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (rb + i < nr) S.lrow[(size_t)h * S.nrows + row0 + rb + i] = kl[i];
 }
 
 // Value objective on a tile: dO_V = sum_s p^K-hat_s (v~_s - v_s) into wrow (pd holds p^K-hat on the
@@ -387,15 +465,15 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_val_kernel(CalSet S, Cal
   constexpr int R = kTileRows;
   __shared__ __align__(16) double dl[kTileThreads * kDlStride];
   const int h = blockIdx.y, tid = threadIdx.x, gq = c.gq;
+  const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
   const int4 tile = S.tiles[blockIdx.x];
   const CalSeq sq = S.seqs[tile.x];
   const int row0 = tile.y, nr = tile.z, tf = tile.w, a0 = sq.start, L = sq.len;
   const int tmax = tf + (nr - 1) / gq;
   const double* pdb = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
-  const int cp = tid & 63, qt = tid >> 6;
-  double acc[R][2];
+  f64x4 acc[8];
 #pragma unroll
-  for (int r = 0; r < R; ++r) acc[r][0] = acc[r][1] = 0.0;
+  for (int t = 0; t < 8; ++t) acc[t] = f64x4{0.0, 0.0, 0.0, 0.0};
   for (int base = 0; base <= tmax; base += kTileThreads) {
     const int end = min(kTileThreads, tmax + 1 - base);
     for (int e = tid; e < R * kTileThreads; e += kTileThreads) {
@@ -403,16 +481,24 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_val_kernel(CalSet S, Cal
       dl[j * kDlStride + r] = r < nr && j < end ? pdb[(size_t)r * L + base + j] : 0.0;
     }
     __syncthreads();
-    for (int j = qt; j < end; j += 4) {
-      const size_t o = ((size_t)(a0 + base + j) * c.H + h) * kD + 2 * cp;
-      const double2 x = *reinterpret_cast<const double2*>(S.xeff + o);
-      const uint32_t vv = *reinterpret_cast<const uint32_t*>(S.v + o);
-      acc_token<R>(acc, dl + j * kDlStride, x.x - (double)__uint_as_float(vv << 16),
-                   x.y - (double)__uint_as_float(vv & 0xFFFF0000u));
+    for (int k4 = 0; k4 < 64 && 64 * w + k4 < end; k4 += 4) {
+      const int j = 64 * w + k4 + lk;
+      const bool ok = j < end;
+      const size_t o = ((size_t)(a0 + base + j) * c.H + h) * kD + 8 * li;
+      double y[8];
+      bf16x8_to_f64(ok ? *reinterpret_cast<const uint4*>(S.v + o) : make_uint4(0, 0, 0, 0), y);
+      const double2* x2 = reinterpret_cast<const double2*>(S.xeff + o);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const double2 x = ok ? x2[i] : make_double2(0.0, 0.0);
+        y[2 * i] = x.x - y[2 * i];
+        y[2 * i + 1] = x.y - y[2 * i + 1];
+      }
+      acc_channels(acc, ok ? dl[j * kDlStride + li] : 0.0, y);
     }
     __syncthreads();
   }
-  sum_quarters_store<R>(acc, dl, S.wrow + ((size_t)h * S.nrows + row0) * kD, nr);
+  sum_waves_store(acc, dl, S.wrow + ((size_t)h * S.nrows + row0) * kD, nr);
 }
 
 // u = M_j dO for the rows of query head j (M_j = W_{O,j}^T W_{O,j}, symmetric), E = dO . u / d_model.
@@ -467,59 +553,56 @@ __global__ __launch_bounds__(256) void cal_u_kernel(CalSet S, CalCfg c, int valu
 
 // Logit gradients of the key objective on a tile: g_s = 2 u . v_s / d_model, gbar = sum_s p^K_s g_s,
 // pd = ((p^K - p) + lambda p^K (g - gbar)) / rows on the tokens read from INT2, 0 elsewhere.
-// Block (tile, KV head), one thread per token.
+// Block (tile, KV head); u . v_s on the fp64 matrix cores (16-token tiles per wave), then one thread
+// per token.
 __global__ __launch_bounds__(kTileThreads) void cal_pos_grad_kernel(CalSet S, CalCfg c) {
   constexpr int R = kTileRows;
-  __shared__ double us[R][kD];
   __shared__ double red[16 * R];
   const int h = blockIdx.y, tid = threadIdx.x, gq = c.gq;
+  const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
   const int4 tile = S.tiles[blockIdx.x];
   const CalSeq sq = S.seqs[tile.x];
   const int row0 = tile.y, nr = tile.z, tf = tile.w, a0 = sq.start, L = sq.len;
   const int tmax = tf + (nr - 1) / gq;
-  for (int e = tid; e < R * kD; e += blockDim.x) {
-    const int r = e / kD, col = e % kD;
-    us[r][col] = r < nr ? S.urow[((size_t)h * S.nrows + row0 + r) * kD + col] : 0.0;
-  }
-  __syncthreads();
   double* pdb = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
   double* pfb = S.pf + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
+  double ua[32];
+  {
+    const bool ok = li < nr;
+    const double* ur = S.urow + ((size_t)h * S.nrows + row0 + (ok ? li : 0)) * kD + 32 * lk;
+#pragma unroll
+    for (int m = 0; m < 32; ++m) ua[m] = ok ? ur[m] : 0.0;
+  }
   const double two_dm = 2.0 / (double)c.dm;
-  double gb[R];
+  double gb4[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int tt = w; 16 * tt <= tmax; tt += 4) {
+    const int s = 16 * tt + li;
+    const bool ok = s <= tmax;
+    const f64x4 g = dot_tokens_bf16(ua, S.v + ((size_t)(a0 + s) * c.H + h) * kD, ok, lk);
 #pragma unroll
-  for (int r = 0; r < R; ++r) gb[r] = 0.0;
-  for (int s = tid; s <= tmax; s += blockDim.x) {
-    const uint4* vr = reinterpret_cast<const uint4*>(S.v + ((size_t)(a0 + s) * c.H + h) * kD);
-    double g[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) g[r] = 0.0;
-    for (int c8 = 0; c8 < kD / 8; ++c8) {
-      const uint4 vv = vr[c8];
-      const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
-      double vd[8];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        vd[2 * i] = (double)__uint_as_float(vw[i] << 16);
-        vd[2 * i + 1] = (double)__uint_as_float(vw[i] & 0xFFFF0000u);
+    for (int v = 0; v < 4; ++v) {
+      const int r = lk + 4 * v;
+      if (r < nr && s <= tf + r / gq) {
+        const double pk = pdb[(size_t)r * L + s], gs = two_dm * g[v];
+        gb4[v] += pk * gs;
+        pfb[(size_t)r * L + s] = (pk - pfb[(size_t)r * L + s]) + c.lam * pk * gs;
       }
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        if (r >= nr) continue;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) g[r] = fma(us[r][8 * c8 + i], vd[i], g[r]);
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      if (r >= nr || s > tf + r / gq) continue;
-      const double pk = pdb[(size_t)r * L + s], gs = two_dm * g[r];
-      gb[r] += pk * gs;
-      pfb[(size_t)r * L + s] = (pk - pfb[(size_t)r * L + s]) + c.lam * pk * gs;  // this thread's token
     }
   }
-  block_reduce_n<R, false>(gb, red);
+  // gbar per row: over the 16 lanes of each lk group, then the four waves (fixed order)
+#pragma unroll
+  for (int v = 0; v < 4; ++v)
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) gb4[v] += __shfl_xor(gb4[v], off);
+  if (li == 0)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) red[w * 16 + lk + 4 * v] = gb4[v];
+  __syncthreads();  // also makes the pf updates visible to the whole block
+  double gb[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) gb[r] = (red[r] + red[32 + r]) + (red[16 + r] + red[48 + r]);
   const double inv_rows = 1.0 / (double)S.nrows;
-  for (int s = tid; s < L; s += blockDim.x) {
+  for (int s = tid; s < L; s += kTileThreads) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       if (r >= nr) continue;
