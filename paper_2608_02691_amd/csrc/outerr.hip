@@ -283,54 +283,50 @@ __global__ __launch_bounds__(256) void outerr_scan_kernel(OutErrArgs e) {
   }
 }
 
-// Block (sequence b, KV head h), thread c: the chunk partials of each query head merged into
-// o1, o2 (model basis) and o3' (R_V basis), o3 = o3' R_V^T, then do = (o2 - o1, o3 - o2).
+// Block (sequence b, query head j), thread c: the chunk partials of the head merged into o1, o2
+// (model basis) and o3' (R_V basis), o3 = o3' R_V^T, then do = (o2 - o1, o3 - o2).
 __global__ __launch_bounds__(128) void outerr_merge_kernel(OutErrArgs e) {
   const DecodeArgs& a = e.a;
   __shared__ float os[kHeadDim];
-  const int b = blockIdx.x, h = blockIdx.y, c = threadIdx.x, gq = a.gq;
+  const int b = blockIdx.x, j = blockIdx.y, c = threadIdx.x, h = j / a.gq;
   const int L = oe_seq_len(e, b);
   const int nch = (L + a.chunk_tokens - 1) / a.chunk_tokens;
   const float* Rv = a.R_v + (size_t)h * kHeadDim * kHeadDim;
-  for (int jj = 0; jj < gq; ++jj) {
-    const int j = h * gq + jj;
-    const float* part = e.part + ((size_t)b * a.n_chunks * a.Hq + j) * kOePartStride;
-    const size_t stride = (size_t)a.Hq * kOePartStride;
-    float M1 = -INFINITY, M2 = -INFINITY;
-    for (int i = 0; i < nch; ++i) {
-      M1 = fmaxf(M1, part[i * stride]);
-      M2 = fmaxf(M2, part[i * stride + 2]);
-    }
-    float L1 = 0.0f, L2 = 0.0f, A0 = 0.0f, A1 = 0.0f, A2 = 0.0f;
-    for (int i = 0; i < nch; ++i) {
-      const float* p = part + i * stride;
-      const float f1 = p[0] == -INFINITY ? 0.0f : exp2f(p[0] - M1);
-      const float f2 = p[2] == -INFINITY ? 0.0f : exp2f(p[2] - M2);
-      L1 = fmaf(f1, p[1], L1);
-      L2 = fmaf(f2, p[3], L2);
-      A0 = fmaf(f1, p[4 + c], A0);
-      A1 = fmaf(f2, p[4 + kHeadDim + c], A1);
-      A2 = fmaf(f2, p[4 + 2 * kHeadDim + c], A2);
-    }
-    const float o1 = L1 > 0.0f ? A0 / L1 : 0.0f;
-    const float o2 = L2 > 0.0f ? A1 / L2 : 0.0f;
-    os[c] = L2 > 0.0f ? A2 / L2 : 0.0f;
-    __syncthreads();
-    const float4* row = reinterpret_cast<const float4*>(Rv + (size_t)c * kHeadDim);
-    float o3 = 0.0f;
-#pragma unroll 8
-    for (int i = 0; i < kHeadDim / 4; ++i) {
-      const float4 r = row[i];
-      o3 = fmaf(os[4 * i], r.x, o3);
-      o3 = fmaf(os[4 * i + 1], r.y, o3);
-      o3 = fmaf(os[4 * i + 2], r.z, o3);
-      o3 = fmaf(os[4 * i + 3], r.w, o3);
-    }
-    __syncthreads();
-    float* d = e.dov + ((size_t)b * a.Hq + j) * 2 * kHeadDim;
-    d[c] = o2 - o1;
-    d[kHeadDim + c] = o3 - o2;
+  const float* part = e.part + ((size_t)b * a.n_chunks * a.Hq + j) * kOePartStride;
+  const size_t stride = (size_t)a.Hq * kOePartStride;
+  float M1 = -INFINITY, M2 = -INFINITY;
+  for (int i = 0; i < nch; ++i) {
+    M1 = fmaxf(M1, part[i * stride]);
+    M2 = fmaxf(M2, part[i * stride + 2]);
   }
+  float L1 = 0.0f, L2 = 0.0f, A0 = 0.0f, A1 = 0.0f, A2 = 0.0f;
+  for (int i = 0; i < nch; ++i) {
+    const float* p = part + i * stride;
+    const float f1 = p[0] == -INFINITY ? 0.0f : exp2f(p[0] - M1);
+    const float f2 = p[2] == -INFINITY ? 0.0f : exp2f(p[2] - M2);
+    L1 = fmaf(f1, p[1], L1);
+    L2 = fmaf(f2, p[3], L2);
+    A0 = fmaf(f1, p[4 + c], A0);
+    A1 = fmaf(f2, p[4 + kHeadDim + c], A1);
+    A2 = fmaf(f2, p[4 + 2 * kHeadDim + c], A2);
+  }
+  const float o1 = L1 > 0.0f ? A0 / L1 : 0.0f;
+  const float o2 = L2 > 0.0f ? A1 / L2 : 0.0f;
+  os[c] = L2 > 0.0f ? A2 / L2 : 0.0f;
+  __syncthreads();
+  const float4* row = reinterpret_cast<const float4*>(Rv + (size_t)c * kHeadDim);
+  float o3 = 0.0f;
+#pragma unroll 8
+  for (int i = 0; i < kHeadDim / 4; ++i) {
+    const float4 r = row[i];
+    o3 = fmaf(os[4 * i], r.x, o3);
+    o3 = fmaf(os[4 * i + 1], r.y, o3);
+    o3 = fmaf(os[4 * i + 2], r.z, o3);
+    o3 = fmaf(os[4 * i + 3], r.w, o3);
+  }
+  float* d = e.dov + ((size_t)b * a.Hq + j) * 2 * kHeadDim;
+  d[c] = o2 - o1;
+  d[kHeadDim + c] = o3 - o2;
 }
 
 // Block (query head j, tile of kOeTile rows of W_O), thread r = one row: dy[b][j][{K, V}][row] =
@@ -435,7 +431,7 @@ hipError_t launch_output_error(const OutErrArgs& e, const uint16_t* W_o, int d_m
     launch_oe_scan<1>(e, s, ev0, ev1);
   else
     launch_oe_scan<4>(e, s, ev0, ev1);
-  hipLaunchKernelGGL(outerr_merge_kernel, dim3(a.B, a.H), dim3(128), 0, s, e);
+  hipLaunchKernelGGL(outerr_merge_kernel, dim3(a.B, a.Hq), dim3(128), 0, s, e);
   const int ntiles = (d_model + kOeTile - 1) / kOeTile;
   hipLaunchKernelGGL(outerr_proj_kernel, dim3(a.Hq, ntiles), dim3(kOeTile), 0, s, e, W_o, d_model, dy, e.spart,
                      ntiles);
