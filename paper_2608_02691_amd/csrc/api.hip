@@ -547,7 +547,7 @@ OePlan make_oe_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   while (chunk > 512 && units * ((max_ctx + chunk - 1) / chunk) < 1024) chunk /= 2;
   p.chunk = chunk;
   p.n_chunks = max_ctx > 0 ? (max_ctx + chunk - 1) / chunk : 1;
-  p.ntiles = (d_model + 127) / 128;
+  p.ntiles = (d_model + kOeRowTile - 1) / kOeRowTile;
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   size_t off = 0;
   p.off_qrot = off;

@@ -129,13 +129,14 @@ hipError_t launch_prepare_wo(const uint16_t* W_o, const float* R_v, uint16_t* Wp
 
 // ---- output-error diagnostics (outerr.hip)
 constexpr int kOePartStride = 4 + 3 * kHeadDim;  // m1, l1, m2, l2, A1[128], A2[128], A3[128]
+constexpr int kOeRowTile = 128;  // W_O rows per output-error projection block (a statistics partial each)
 struct OutErrArgs {
   DecodeArgs a;                 // cache, queries, block table, lengths, R_K, R_V, qrot, chunking
   const uint16_t *k_rows, *v_rows;  // full-precision keys and values, row b * row_cap + t, [H, 128]
   int row_cap;
   float* part;                  // [B, n_chunks, Hq, kOePartStride]
   float* dov;                   // [B, Hq, 2, 128]: o2 - o1, o3 - o2 (model basis)
-  float* spart;                 // [B, Hq, row tiles, 4]
+  float* spart;                 // [B, Hq, row tiles of kOeRowTile rows, 4]
 };
 // stats: [B, Hq, 4]; dy (may be null): [B, Hq, 2, d_model]; ev0 / ev1 track the scan kernel
 hipError_t launch_output_error(const OutErrArgs& e, const uint16_t* W_o, int d_model, float* stats, float* dy,

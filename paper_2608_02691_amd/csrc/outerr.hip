@@ -24,7 +24,6 @@ namespace {
 
 constexpr float kOeLogit2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
 constexpr int kOeWaves = 4;
-constexpr int kOeTile = 128;                       // W_O rows per projection block
 
 __device__ __forceinline__ int oe_seq_len(const OutErrArgs& e, int b) {
   int L = e.a.ctx_lens[b];
@@ -329,81 +328,130 @@ __global__ __launch_bounds__(128) void outerr_merge_kernel(OutErrArgs e) {
   d[kHeadDim + c] = o3 - o2;
 }
 
-// Block (query head j, tile of kOeTile rows of W_O), thread r = one row: dy[b][j][{K, V}][row] =
-// do[b][j][{K, V}] . W_O[row][j * 128 ..] for every sequence, and the tile's partial statistics.
-__global__ __launch_bounds__(kOeTile) void outerr_proj_kernel(OutErrArgs e, const uint16_t* __restrict__ W_o,
-                                                              int d_model, float* __restrict__ dy,
-                                                              float* __restrict__ spart, int ntiles) {
+typedef float oe_f4_t __attribute__((ext_vector_type(4)));
+
+// Block (query head j, tile of kOeRowTile rows of W_O), four waves: dy[b][j][{K, V}][row] =
+// do[b][j][{K, V}] . W_O[row][j * 128 ..] for every sequence, and the tile's partial statistics, on
+// the fp32 matrix cores (16 x 16 x 4 steps: lane l holds A[l % 16][l / 16] and B[l / 16][l % 16],
+// D[4 (l / 16) + v][l % 16] is element v of its accumulator). M: the 2B rows m = 2 b + {0: K, 1: V}
+// of do, 16 at a time; N: wave w's two 16-row tiles of the block's rows; K: the head's 128
+// channels, step s taking channels 32 (l / 16) + s, so that each lane reads 32 contiguous channels
+// of its do and W_O rows.
+constexpr int kOeNT = kOeRowTile / 64;  // 16-row N tiles per wave
+__global__ __launch_bounds__(256) void outerr_proj_kernel(OutErrArgs e, const uint16_t* __restrict__ W_o,
+                                                          int d_model, float* __restrict__ dy,
+                                                          float* __restrict__ spart, int ntiles) {
   const DecodeArgs& a = e.a;
-  __shared__ float ds[2][kHeadDim];
-  __shared__ float red[kOeTile / 64][4];
-  const int j = blockIdx.x, tile = blockIdx.y, tid = threadIdx.x, r = tile * kOeTile + tid;
-  const bool have = r < d_model;
-  // the row's 128 weights of head j (bf16 -> fp32), read once for all sequences
-  float wr[kHeadDim];
-  {
-    const uint4* wp = reinterpret_cast<const uint4*>(W_o + (size_t)(have ? r : 0) * a.Hq * kHeadDim +
-                                                     (size_t)j * kHeadDim);
+  __shared__ float red[4][8][4];  // [wave][sequence of the M tile][statistic]
+  const int j = blockIdx.x, tile = blockIdx.y, tid = threadIdx.x;
+  const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
+  int n[kOeNT];
+  bool have[kOeNT];
+  float wb[kOeNT][32];
 #pragma unroll
-    for (int u = 0; u < kHeadDim / 8; ++u) {
-      const uint4 x = wp[u];
+  for (int nt = 0; nt < kOeNT; ++nt) {
+    n[nt] = tile * kOeRowTile + 16 * (kOeNT * w + nt) + li;  // this lane's W_O row of N tile nt
+    have[nt] = n[nt] < d_model;
+    const uint4* wp = reinterpret_cast<const uint4*>(W_o + (size_t)(have[nt] ? n[nt] : 0) * a.Hq * kHeadDim +
+                                                     (size_t)j * kHeadDim + 32 * lk);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint4 x = have[nt] ? wp[u] : make_uint4(0, 0, 0, 0);
       const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        wr[8 * u + 2 * i] = __uint_as_float(xs[i] << 16);
-        wr[8 * u + 2 * i + 1] = __uint_as_float(xs[i] & 0xFFFF0000u);
+        wb[nt][8 * u + 2 * i] = __uint_as_float(xs[i] << 16);
+        wb[nt][8 * u + 2 * i + 1] = __uint_as_float(xs[i] & 0xFFFF0000u);
       }
     }
   }
-  for (int b = 0; b < a.B; ++b) {
+  const int M = 2 * a.B;
+  for (int m0 = 0; m0 < M; m0 += 16) {
+    const int m = m0 + li, mc = m < M ? m : 0;
+    float da[32];
+    {
+      const float4* dp = reinterpret_cast<const float4*>(
+          e.dov + (((size_t)(mc >> 1) * a.Hq + j) * 2 + (mc & 1)) * kHeadDim + 32 * lk);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float4 x = m < M ? dp[u] : make_float4(0.f, 0.f, 0.f, 0.f);
+        da[4 * u] = x.x;
+        da[4 * u + 1] = x.y;
+        da[4 * u + 2] = x.z;
+        da[4 * u + 3] = x.w;
+      }
+    }
+    oe_f4_t acc[kOeNT];
+#pragma unroll
+    for (int nt = 0; nt < kOeNT; ++nt) acc[nt] = oe_f4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 32; ++s)
+#pragma unroll
+      for (int nt = 0; nt < kOeNT; ++nt) acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(da[s], wb[nt][s], acc[nt], 0, 0, 0);
+    // acc[nt][v]: do row m0 + 4 lk + v, i.e. sequence m0 / 2 + 2 lk + v / 2, K (v even) or V (v odd)
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb) {
+      const int b = m0 / 2 + 2 * lk + hb;
+      float st[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int nt = 0; nt < kOeNT; ++nt) {
+        const float yk = acc[nt][2 * hb], yv = acc[nt][2 * hb + 1];  // 0 past d_model or past the batch
+        if (dy && have[nt] && b < a.B) {
+          float* o = dy + ((size_t)b * a.Hq + j) * 2 * d_model;
+          o[n[nt]] = yk;
+          o[d_model + n[nt]] = yv;
+        }
+        st[0] += (yk + yv) * (yk + yv);
+        st[1] += yk * yk;
+        st[2] += yv * yv;
+        st[3] += yk * yv;
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) st[k] += __shfl_xor(st[k], off);
+      if (li == 0)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) red[w][2 * lk + hb][k] = st[k];
+    }
     __syncthreads();
-    const float* d = e.dov + ((size_t)b * a.Hq + j) * 2 * kHeadDim;
-    ds[0][tid] = d[tid];
-    ds[1][tid] = d[kHeadDim + tid];
-    __syncthreads();
-    float yk = 0.0f, yv = 0.0f;
-#pragma unroll
-    for (int c = 0; c < kHeadDim; ++c) {
-      yk = fmaf(ds[0][c], wr[c], yk);
-      yv = fmaf(ds[1][c], wr[c], yv);
-    }
-    if (!have) yk = yv = 0.0f;
-    if (dy && have) {
-      float* o = dy + ((size_t)b * a.Hq + j) * 2 * d_model;
-      o[r] = yk;
-      o[d_model + r] = yv;
-    }
-    float st[4] = {(yk + yv) * (yk + yv), yk * yk, yv * yv, yk * yv};
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) st[s] += __shfl_xor(st[s], off);
-    }
-    if ((tid & 63) == 0) {
-#pragma unroll
-      for (int s = 0; s < 4; ++s) red[tid >> 6][s] = st[s];
+    if (tid < 32) {
+      const int bb = tid >> 2, k = tid & 3, b = m0 / 2 + bb;
+      if (b < a.B)
+        spart[(((size_t)b * a.Hq + j) * ntiles + tile) * 4 + k] =
+            ((red[0][bb][k] + red[1][bb][k]) + red[2][bb][k]) + red[3][bb][k];
     }
     __syncthreads();
-    if (tid < 4) {
-      float v = 0.0f;
-#pragma unroll
-      for (int wv = 0; wv < kOeTile / 64; ++wv) v += red[wv][tid];
-      spart[(((size_t)b * a.Hq + j) * ntiles + tile) * 4 + tid] = v;
-    }
   }
 }
 
-// Thread per (b, j): the four statistics summed over the row tiles in order (deterministic).
+// Wave per (b, j): lane t sums the row tiles t, t + 64, ... in order, then a fixed butterfly over
+// the lanes (deterministic).
 __global__ __launch_bounds__(256) void outerr_stats_kernel(const float* __restrict__ spart, float* __restrict__ stats,
                                                            int n, int ntiles) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int t = 0; t < ntiles; ++t)
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), l = threadIdx.x & 63;
+  if (i >= n) return;  // uniform over the wave
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int t = l; t < ntiles; t += 64) {
+    const float4 x = *reinterpret_cast<const float4*>(spart + ((size_t)i * ntiles + t) * 4);
+    s.x += x.x;
+    s.y += x.y;
+    s.z += x.z;
+    s.w += x.w;
+  }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) s[k] += spart[((size_t)i * ntiles + t) * 4 + k];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) stats[(size_t)i * 4 + k] = s[k];
+  for (int off = 32; off > 0; off >>= 1) {
+    s.x += __shfl_xor(s.x, off);
+    s.y += __shfl_xor(s.y, off);
+    s.z += __shfl_xor(s.z, off);
+    s.w += __shfl_xor(s.w, off);
+  }
+  if (l == 0) {  // the caller's stats need only 4-byte alignment
+    stats[(size_t)i * 4] = s.x;
+    stats[(size_t)i * 4 + 1] = s.y;
+    stats[(size_t)i * 4 + 2] = s.z;
+    stats[(size_t)i * 4 + 3] = s.w;
+  }
 }
 
 template <int NG>
@@ -432,11 +480,11 @@ hipError_t launch_output_error(const OutErrArgs& e, const uint16_t* W_o, int d_m
   else
     launch_oe_scan<4>(e, s, ev0, ev1);
   hipLaunchKernelGGL(outerr_merge_kernel, dim3(a.B, a.Hq), dim3(128), 0, s, e);
-  const int ntiles = (d_model + kOeTile - 1) / kOeTile;
-  hipLaunchKernelGGL(outerr_proj_kernel, dim3(a.Hq, ntiles), dim3(kOeTile), 0, s, e, W_o, d_model, dy, e.spart,
+  const int ntiles = (d_model + kOeRowTile - 1) / kOeRowTile;
+  hipLaunchKernelGGL(outerr_proj_kernel, dim3(a.Hq, ntiles), dim3(256), 0, s, e, W_o, d_model, dy, e.spart,
                      ntiles);
   const int n = a.B * a.Hq;
-  hipLaunchKernelGGL(outerr_stats_kernel, dim3((n + 255) / 256), dim3(256), 0, s, e.spart, stats, n, ntiles);
+  hipLaunchKernelGGL(outerr_stats_kernel, dim3((n + 3) / 4), dim3(256), 0, s, e.spart, stats, n, ntiles);
   return hipGetLastError();
 }
 
