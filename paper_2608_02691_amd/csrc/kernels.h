@@ -86,10 +86,11 @@ struct WindowArgs {
 };
 constexpr int kWinMaxGq = 16;
 constexpr int kWinMaxCap = 512;
-constexpr int kWinSliceTokens = 128;                           // window tokens per partial
+constexpr int kWinSliceTokens = 96;                            // window tokens per partial
 constexpr int kMerge2Ranges = 16;      // slot ranges per sequence in the two-stage merge
 constexpr int kMerge2MaxUnits = 128;   // two-stage merge when batch x KV heads is below this
-constexpr int kWinMaxSlices = kWinMaxCap / kWinSliceTokens;    // window partials per (sequence, query head)
+// window partials per (sequence, query head)
+constexpr int kWinMaxSlices = (kWinMaxCap + kWinSliceTokens - 1) / kWinSliceTokens;
 hipError_t launch_window_write(const uint16_t* k, const uint16_t* v, const int32_t* rows, int n, int H, const float* mu,
                                uint16_t* win_k, uint16_t* win_v, int num_rows, hipStream_t s);
 // window partials into a.wpart (needs a.R_v)

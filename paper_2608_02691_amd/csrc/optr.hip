@@ -156,33 +156,7 @@ __global__ __launch_bounds__(128) void cal_rotq_kernel(CalSet S, CalCfg c, int v
 }
 
 // ---------------------------------------------------------------------------------------------
-// Objectives per query position: block (position p, KV head h) handles the G_q rows (t, j) of that
-// position, one thread per token for the logits (each key row is read once for the whole group,
-// no cross-lane reductions per token). MAXG >= G_q.
-
-// Block-wide max / sum of MAXG values per thread; red: [16][MAXG] doubles.
-template <int MAXG, bool MAX>
-__device__ void block_reduce_n(double (&x)[MAXG], double* red) {
-#pragma unroll
-  for (int j = 0; j < MAXG; ++j)
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      const double y = __shfl_xor(x[j], off);
-      x[j] = MAX ? fmax(x[j], y) : x[j] + y;
-    }
-  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0)
-#pragma unroll
-    for (int j = 0; j < MAXG; ++j) red[w * MAXG + j] = x[j];
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < MAXG; ++j) {
-    double t = red[j];
-    for (int i = 1; i < nw; ++i) t = MAX ? fmax(t, red[i * MAXG + j]) : t + red[i * MAXG + j];  // fixed order
-    x[j] = t;
-  }
-}
+// The objectives over row tiles.
 
 // The tile kernels take a tile of up to kTileRows rows: 16 / G_q consecutive query positions of
 // one sequence with all their query heads (tiles[i] = (sequence, first row, rows, position of the

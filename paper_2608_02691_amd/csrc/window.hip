@@ -92,19 +92,6 @@ struct WinLds {
   float alpha[kWinWaves][kWinMaxGq];
 };
 
-__device__ __forceinline__ float win_row_max16(float x) {
-  x = fmaxf(x, __shfl_xor(x, 8, 16));
-  x = fmaxf(x, __shfl_xor(x, 4, 16));
-  x = fmaxf(x, __shfl_xor(x, 2, 16));
-  return fmaxf(x, __shfl_xor(x, 1, 16));
-}
-__device__ __forceinline__ float win_row_sum16(float x) {
-  x += __shfl_xor(x, 8, 16);
-  x += __shfl_xor(x, 4, 16);
-  x += __shfl_xor(x, 2, 16);
-  return x + __shfl_xor(x, 1, 16);
-}
-
 // One wave: KV head h of sequence b, window slice `slice`. NJ4 = ceil(gq / 4): groups of four query
 // rows the arithmetic covers (rows >= gq are zero).
 template <int NJ4>
@@ -171,7 +158,7 @@ __device__ void window_wave(const DecodeArgs& a, const WindowArgs& w, int b, int
       float pm = sc[0][r];
 #pragma unroll
       for (int u = 1; u < kWinTiles; ++u) pm = fmaxf(pm, sc[u][r]);
-      pm = win_row_max16(pm);
+      pm = row_max16(pm);
       const float mnew = fmaxf(run_m[r], pm);  // pm is finite: the pass holds a valid token
       const float al = __builtin_amdgcn_exp2f(run_m[r] - mnew);
       float rs = 0.0f;
@@ -181,7 +168,7 @@ __device__ void window_wave(const DecodeArgs& a, const WindowArgs& w, int b, int
         rs += p;
         L.p[wave][16 * u + lo][4 * hi + r] = p;
       }
-      run_l[r] = al * run_l[r] + win_row_sum16(rs);
+      run_l[r] = al * run_l[r] + row_sum16(rs);
       run_m[r] = mnew;
       if (lo == 0) L.alpha[wave][4 * hi + r] = al;
     }
