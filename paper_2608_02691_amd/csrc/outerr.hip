@@ -33,6 +33,33 @@ __device__ __forceinline__ int oe_seq_len(const OutErrArgs& e, int b) {
   return max(L, 0);
 }
 
+// sum over the 4 lanes of a DPP quad (quad_perm [1, 0, 3, 2] then [2, 3, 0, 1]); every lane gets it
+__device__ __forceinline__ float quad_sum4(float x) {
+  x += dppf<0xB1>(x);
+  return x + dppf<0x4E>(x);
+}
+// max over the four tokens of a DPP row (lanes 4 tq + gk; rotations by 4 and 8 lanes)
+__device__ __forceinline__ float row_max_tokens(float x) {
+  x = fmaxf(x, dppf<0x124>(x));
+  return fmaxf(x, dppf<0x128>(x));
+}
+// max over the four DPP rows of values that are already uniform within each row (lanes 0, 16, 32
+// and 48 read out as scalars)
+__device__ __forceinline__ float rows_max4(float x) {
+  const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 0));
+  const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 16));
+  const float c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 32));
+  const float d = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 48));
+  return fmaxf(fmaxf(a, b), fmaxf(c, d));
+}
+__device__ __forceinline__ float rows_sum4(float x) {
+  const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 0));
+  const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 16));
+  const float c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 32));
+  const float d = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 48));
+  return (a + b) + (c + d);
+}
+
 __device__ __forceinline__ void oe_wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -50,7 +77,7 @@ __global__ __launch_bounds__(256) void outerr_scan_kernel(OutErrArgs e) {
   __shared__ float qf[MAXG][kHeadDim];       // q (model basis), base-2 logit units
   __shared__ float qr[MAXG][kHeadDim];       // q R_K, base-2 logit units
   __shared__ float qsum[MAXG][kGroups];      // sums of q R_K over each 32-channel quarter
-  __shared__ float pb[kOeWaves][2][MAXG][kBlock];   // p of both softmaxes for the page
+  __shared__ float pb[kOeWaves][2][kBlock][MAXG];   // p of both softmaxes for the page (token-major)
   __shared__ float wst[kOeWaves][MAXG][4];
   __shared__ float wout[kOeWaves][3][MAXG][kHeadDim];
 
@@ -149,37 +176,27 @@ __global__ __launch_bounds__(256) void outerr_scan_kernel(OutErrArgs e) {
       }
 #pragma unroll
       for (int c = 0; c < 32; ++c) d1 = fmaf(qf[j][32 * gk + c], kf[c], d1);
-      float s2 = ks * d2 + kz * qsum[j][gk];
-      float s1 = d1;
-      s2 += __shfl_xor(s2, 1);
-      s2 += __shfl_xor(s2, 2);
-      s1 += __shfl_xor(s1, 1);
-      s1 += __shfl_xor(s1, 2);
+      // the token's scores: sums over its four quarter lanes (a DPP quad)
+      float s2 = quad_sum4(ks * d2 + kz * qsum[j][gk]);
+      float s1 = quad_sum4(d1);
       s1 = valid ? s1 : -INFINITY;
       s2 = valid ? s2 : -INFINITY;
-      float x1 = s1, x2 = s2;
-#pragma unroll
-      for (int off = 4; off < 64; off <<= 1) {
-        x1 = fmaxf(x1, __shfl_xor(x1, off));
-        x2 = fmaxf(x2, __shfl_xor(x2, off));
-      }
+      // page maxima: over the four tokens of each DPP row, then the rows
+      const float x1 = rows_max4(row_max_tokens(s1)), x2 = rows_max4(row_max_tokens(s2));
       const float n1 = fmaxf(m1[j], x1), n2 = fmaxf(m2[j], x2);
       al1[j] = n1 == -INFINITY ? 1.0f : exp2f(m1[j] - n1);
       al2[j] = n2 == -INFINITY ? 1.0f : exp2f(m2[j] - n2);
       const float p1 = valid ? exp2f(s1 - n1) : 0.0f, p2 = valid ? exp2f(s2 - n2) : 0.0f;
-      float ps1 = gk == 0 ? p1 : 0.0f, ps2 = gk == 0 ? p2 : 0.0f;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        ps1 += __shfl_xor(ps1, off);
-        ps2 += __shfl_xor(ps2, off);
-      }
+      // page sums of p: one lane per token (gk = 0), over each DPP row, then the rows
+      const float ps1 = rows_sum4(row_sum16(gk == 0 ? p1 : 0.0f));
+      const float ps2 = rows_sum4(row_sum16(gk == 0 ? p2 : 0.0f));
       l1[j] = l1[j] * al1[j] + ps1;
       l2[j] = l2[j] * al2[j] + ps2;
       m1[j] = n1;
       m2[j] = n2;
       if (gk == 0) {
-        pb[w][0][j][tq] = p1;
-        pb[w][1][j][tq] = p2;
+        pb[w][0][tq][j] = p1;
+        pb[w][1][tq][j] = p2;
       }
     }
     oe_wave_sync();
@@ -220,7 +237,7 @@ __global__ __launch_bounds__(256) void outerr_scan_kernel(OutErrArgs e) {
 #pragma unroll
       for (int j = 0; j < MAXG; ++j) {
         if (j < gq) {
-          const float p1 = pb[w][0][j][t], p2 = pb[w][1][j][t];
+          const float p1 = pb[w][0][t][j], p2 = pb[w][1][t][j];
           o[0][j][0] = fmaf(p1, r0, o[0][j][0]);
           o[0][j][1] = fmaf(p1, r1, o[0][j][1]);
           o[1][j][0] = fmaf(p2, r0, o[1][j][0]);
