@@ -67,12 +67,14 @@ CASES = [
     (8, 2, [300, 0, 17, 1, 129, 0], [64, 5, 0, 320, 1, 0], 320, 0),
     (10, 2, [700, 0, 33, 40], [100, 7, 0, -3], 128, 96),
     (24, 2, [250, 64, 10], [30, 64, 1000], 64, 0),
+    # the largest window (512 tokens: every slice of the window attention, the last one partial)
+    (8, 2, [40, 600, 3], [512, 200, 511], 512, 0),
 ]
 
 
 @pytest.mark.parametrize("G", [32, 128])
 @pytest.mark.parametrize("variant", [1, 2])
-@pytest.mark.parametrize("case", CASES, ids=["gqa4", "gqa5_wo", "gqa12"])
+@pytest.mark.parametrize("case", CASES, ids=["gqa4", "gqa5_wo", "gqa12", "gqa4_cap512"])
 def test_decode_window_matches_oracle(case, variant, G):
     Hq, H, lens, wls, cap, dm = case
     print(f"\n[decode window] case={case} variant={variant} G={G}", flush=True)
