@@ -146,7 +146,7 @@ hipError_t launch_output_error(const OutErrArgs& e, const uint16_t* W_o, int d_m
 // ---- OptR offline calibration (optr.hip): fp64 throughout
 constexpr int kCalMaxLen = 4096;  // tokens per calibration sequence
 constexpr int kCalSplit = 16;     // token slices of the rotation-gradient reduction
-constexpr int kCalScratch = 6;    // 128 x 128 scratch matrices per KV head of the matrix functions
+constexpr int kCalScratch = 11;   // 128 x 128 scratch matrices per KV head of the matrix functions
 struct CalSeq {
   int start, len, t0, row0;  // first token, length, first query position, first row
   long long p0;              // offset of the sequence's [rows][len] block of per-row token weights

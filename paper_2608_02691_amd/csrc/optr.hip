@@ -780,6 +780,32 @@ __device__ __forceinline__ void frag_store(double* __restrict__ M, const f64x4 (
       Mf[frag_step(t, v)] = (add_identity && r0 + 4 * v == c0 + 16 * t ? 1.0 : 0.0) + acc[t][v] * scale;
 }
 
+// M[fragment] = acc + c0 I + c1 A1 + c2 A2 + c3 A3, the A's read at the thread's own fragment elements.
+__device__ __forceinline__ void frag_store_lin(double* __restrict__ M, const f64x4 (&acc)[4], double c0,
+                                               const double* A1, double c1, const double* A2, double c2,
+                                               const double* A3, double c3) {
+  unsigned fb = frag_base();
+  asm volatile("" : "+v"(fb));  // as in frag_store
+  const int r0 = frag_row(0), c0c = frag_col(0);
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const unsigned o = fb + frag_step(t, v);
+      M[o] = (r0 + 4 * v == c0c + 16 * t ? c0 : 0.0) + acc[t][v] + c1 * A1[o] + c2 * A2[o] + c3 * A3[o];
+    }
+}
+
+// Truncated Taylor series of exp (degree kExpTerms = 14) in Paterson-Stockmeyer form: with Y = X^4,
+// sum_k X^k / k! = ((B_3 Y + B_2) Y + B_1) Y + B_0, B_i = sum_{j<4} X^j / (4 i + j)! (1/15! taken as 0),
+// so the powers X^2, X^3, X^4 and three Horner steps take six products instead of fourteen.
+__device__ __forceinline__ void taylor_coeffs(double (&cf)[16]) {
+  cf[0] = 1.0;
+#pragma unroll
+  for (int k = 1; k <= kExpTerms; ++k) cf[k] = cf[k - 1] / (double)k;
+  cf[15] = 0.0;
+}
+
 // acc += op(A) B for 128 x 128 fp64 matrices in global memory (op(A) = A or A^T) on the fp64
 // matrix cores (16 x 16 x 4 steps), 16-deep chunks of A and B staged through LDS. Ends with a
 // barrier, so the caller may overwrite A or B right after.
@@ -836,17 +862,31 @@ __global__ __launch_bounds__(kExpThreads) void cal_expm_kernel(CalCfg c, const d
   const int h = blockIdx.x, tid = threadIdx.x;
   double* ex = c.ex + (size_t)h * kCalScratch * kMat;
   double *X = ex, *P = ex + kMat, *R0 = ex + 2 * kMat;
+  double *X2 = ex + 5 * kMat, *X3 = ex + 6 * kMat, *X4 = ex + 7 * kMat;
   const float* R0f = (value ? c.R0v : c.R0k) + (size_t)h * kMat;
-  for (int e = tid; e < kMat; e += kExpThreads) {
-    R0[e] = (double)R0f[e];
-    P[e] = (e >> 7) == (e & 127) ? 1.0 : 0.0;
-  }
+  for (int e = tid; e < kMat; e += kExpThreads) R0[e] = (double)R0f[e];
   const int sc = wg_skew_scaled(Aall + (size_t)h * kMat, X, false, sm);
+  double cf[16];
+  taylor_coeffs(cf);
   f64x4 acc[4];
-  for (int k = kExpTerms; k >= 1; --k) {  // P <- I + X P / k
+  zero4(acc);
+  wg_gemm(X, false, X, acc, sm);
+  frag_store(X2, acc, 1.0, false);
+  __syncthreads();
+  zero4(acc);
+  wg_gemm(X2, false, X, acc, sm);
+  frag_store(X3, acc, 1.0, false);
+  zero4(acc);
+  wg_gemm(X2, false, X2, acc, sm);
+  frag_store(X4, acc, 1.0, false);
+  __syncthreads();
+  for (int e = tid; e < kMat; e += kExpThreads)  // P = B_3
+    P[e] = ((e >> 7) == (e & 127) ? cf[12] : 0.0) + cf[13] * X[e] + cf[14] * X2[e] + cf[15] * X3[e];
+  __syncthreads();
+  for (int i = 2; i >= 0; --i) {  // P <- P X^4 + B_i
     zero4(acc);
-    wg_gemm(X, false, P, acc, sm);
-    frag_store(P, acc, 1.0 / (double)k, true);
+    wg_gemm(P, false, X4, acc, sm);
+    frag_store_lin(P, acc, cf[4 * i], X, cf[4 * i + 1], X2, cf[4 * i + 2], X3, cf[4 * i + 3]);
     __syncthreads();
   }
   for (int i = 0; i < sc; ++i) {  // P <- P P
@@ -867,36 +907,67 @@ __global__ __launch_bounds__(kExpThreads) void cal_expm_kernel(CalCfg c, const d
     for (int v = 0; v < 4; ++v) Rt[(unsigned)((c0 + 16 * t) * kD + r0 + 4 * v)] = acc[t][v];
 }
 
-// Backward: grad = dS - dS^T with dS = L_exp(S^T, R0^T dR), S = A - A^T, for every head.
+// Backward: grad = dS - dS^T with dS = L_exp(S^T, R0^T dR), S = A - A^T, for every head: the top
+// right block of exp([[X, G], [0, X]]) (X = S^T, G = R0^T dR, both scaled by 2^-sc), whose powers
+// are [[X^k, D_k], [0, X^k]] with D_{a+b} = X^a D_b + D_a X^b; the Taylor polynomial of the block
+// matrix in the Paterson-Stockmeyer form above, then sc squarings.
 __global__ __launch_bounds__(kExpThreads) void cal_expm_grad_kernel(CalCfg c, const double* __restrict__ Aall,
                                                                    int value, double* __restrict__ grad) {
   __shared__ ExpLds sm;
   const int h = blockIdx.x, tid = threadIdx.x;
   double* ex = c.ex + (size_t)h * kCalScratch * kMat;
   double *X = ex, *P1 = ex + kMat, *R0 = ex + 2 * kMat, *P2 = ex + 3 * kMat, *Gs = ex + 4 * kMat;
+  double *X2 = ex + 5 * kMat, *X3 = ex + 6 * kMat, *X4 = ex + 7 * kMat;
+  double *D2 = ex + 8 * kMat, *D3 = ex + 9 * kMat, *D4 = ex + 10 * kMat;
   const float* R0f = (value ? c.R0v : c.R0k) + (size_t)h * kMat;
-  for (int e = tid; e < kMat; e += kExpThreads) {
-    R0[e] = (double)R0f[e];
-    P1[e] = (e >> 7) == (e & 127) ? 1.0 : 0.0;
-    P2[e] = 0.0;
-  }
+  for (int e = tid; e < kMat; e += kExpThreads) R0[e] = (double)R0f[e];
   const int sc = wg_skew_scaled(Aall + (size_t)h * kMat, X, true, sm);
   const double f = ldexp(1.0, -sc);
+  double cf[16];
+  taylor_coeffs(cf);
   f64x4 acc[4], t1[4];
   zero4(acc);
   wg_gemm(R0, true, c.dr + (size_t)h * kMat, acc, sm);  // G_E = R0^T dR, scaled like X
   frag_store(Gs, acc, f, false);
   __syncthreads();
-  // Taylor on the block matrix [[X, Gs], [0, X]]: (P1, P2) <- (I + X P1 / k, (X P2 + Gs P1) / k);
-  // t1 holds X P1 in registers until P2 is formed
-  for (int k = kExpTerms; k >= 1; --k) {
+  // M^2: (X^2, X G + G X)
+  zero4(acc);
+  wg_gemm(X, false, X, acc, sm);
+  frag_store(X2, acc, 1.0, false);
+  zero4(acc);
+  wg_gemm(X, false, Gs, acc, sm);
+  wg_gemm(Gs, false, X, acc, sm);
+  frag_store(D2, acc, 1.0, false);
+  __syncthreads();
+  // M^3 = M^2 M: (X^2 X, X^2 G + D_2 X); M^4 = M^2 M^2: (X^2 X^2, X^2 D_2 + D_2 X^2)
+  zero4(acc);
+  wg_gemm(X2, false, X, acc, sm);
+  frag_store(X3, acc, 1.0, false);
+  zero4(acc);
+  wg_gemm(X2, false, Gs, acc, sm);
+  wg_gemm(D2, false, X, acc, sm);
+  frag_store(D3, acc, 1.0, false);
+  zero4(acc);
+  wg_gemm(X2, false, X2, acc, sm);
+  frag_store(X4, acc, 1.0, false);
+  zero4(acc);
+  wg_gemm(X2, false, D2, acc, sm);
+  wg_gemm(D2, false, X2, acc, sm);
+  frag_store(D4, acc, 1.0, false);
+  __syncthreads();
+  for (int e = tid; e < kMat; e += kExpThreads) {  // (P1, P2) = B_3
+    P1[e] = ((e >> 7) == (e & 127) ? cf[12] : 0.0) + cf[13] * X[e] + cf[14] * X2[e] + cf[15] * X3[e];
+    P2[e] = cf[13] * Gs[e] + cf[14] * D2[e] + cf[15] * D3[e];
+  }
+  __syncthreads();
+  for (int i = 2; i >= 0; --i) {  // (P1, P2) <- (P1 X^4, P1 D_4 + P2 X^4) + B_i
     zero4(t1);
-    wg_gemm(X, false, P1, t1, sm);
+    wg_gemm(P1, false, X4, t1, sm);
     zero4(acc);
-    wg_gemm(X, false, P2, acc, sm);
-    wg_gemm(Gs, false, P1, acc, sm);
-    frag_store(P2, acc, 1.0 / (double)k, false);
-    frag_store(P1, t1, 1.0 / (double)k, true);
+    wg_gemm(P1, false, D4, acc, sm);
+    wg_gemm(P2, false, X4, acc, sm);
+    frag_store_lin(P2, acc, 0.0, Gs, cf[4 * i + 1], D2, cf[4 * i + 2], D3, cf[4 * i + 3]);
+    frag_store_lin(P1, t1, cf[4 * i], X, cf[4 * i + 1], X2, cf[4 * i + 2], X3, cf[4 * i + 3]);
     __syncthreads();
   }
   for (int i = 0; i < sc; ++i) {  // (P1, P2) <- (P1 P1, P1 P2 + P2 P1)
