@@ -28,7 +28,6 @@ namespace {
 
 constexpr int kD = kHeadDim;
 constexpr int kMat = kD * kD;
-constexpr int kRotTile = 16;   // tokens per rotation work-group
 constexpr int kExpTerms = 14;
 constexpr int kExpThreads = 1024;
 
@@ -77,82 +76,141 @@ __device__ __forceinline__ bool int2_token(int s, int t, int sink, int recent) {
   return s >= sink && s <= t - recent;
 }
 
-// ---------------------------------------------------------------------------------------------
-// Rotation and quantization: block (16-token tile, KV head), thread = channel.
-__global__ __launch_bounds__(128) void cal_rotq_kernel(CalSet S, CalCfg c, int value) {
-  __shared__ double xs[kRotTile][kD];
-  __shared__ float red[2][kRotTile][2];
-  const int h = blockIdx.y, col = threadIdx.x, s0 = blockIdx.x * kRotTile;
-  const int n = min(kRotTile, S.T - s0);
-  const uint16_t* X = value ? S.v : S.k;
-  const double muc = value ? 0.0 : (double)c.mu[h * kD + col];
-  for (int t = 0; t < kRotTile; ++t)
-    xs[t][col] = t < n ? bf16d(X[((size_t)(s0 + t) * c.H + h) * kD + col]) - muc : 0.0;
-  __syncthreads();
-  const double* R = c.R + (size_t)h * kMat;
-  double z[kRotTile];
+__device__ __forceinline__ void bf16x8_to_f64(uint4 u, double (&d)[8]) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-  for (int t = 0; t < kRotTile; ++t) z[t] = 0.0;
-  for (int i = 0; i < kD; ++i) {
-    const double r = R[i * kD + col];
-#pragma unroll
-    for (int t = 0; t < kRotTile; ++t) z[t] = fma(xs[t][i], r, z[t]);
+  for (int i = 0; i < 4; ++i) {
+    d[2 * i] = (double)__uint_as_float(w[i] << 16);
+    d[2 * i + 1] = (double)__uint_as_float(w[i] & 0xFFFF0000u);
   }
-  const float clip = value ? c.clip_v : c.clip_k;
-  __syncthreads();  // xs is reused for zhat below
+}
+
+// ---------------------------------------------------------------------------------------------
+// Rows times a 128 x 128 matrix on the fp64 matrix cores, as out^T = Bm^T y^T: M = the 128 output
+// channels (eight 16-row tiles), N = the wave's 16 rows y (lane l holds row l % 16), K = the 128
+// input channels. The lane's B operand at step s is ya[s] = y[row][k(s)], k(4 q + d) = 32 (l / 16) +
+// 4 q + d (KMAP 0: each lane reads 32 contiguous channels of its row) or 16 q + 4 d + l / 16 (KMAP 1:
+// the channels this layout leaves in a lane, see below); Bm goes through Bs (LDS, 16 rows x
+// kBsStride) 16 rows at a time. Result element v of acc[ct]: channel 16 ct + l / 16 + 4 v of row
+// l % 16. Contains block barriers: every thread of the block calls it.
+constexpr int kBsStride = 132;  // doubles per staged row (lane groups l / 16 two banks apart)
+template <int KMAP>
+__device__ __forceinline__ void mat_t_rows(const double (&ya)[32], const double* __restrict__ Bm, double* Bs,
+                                           f64x4 (&acc)[8]) {
+  const int tid = threadIdx.x, l = tid & 63, li = l & 15, lk = l >> 4;
 #pragma unroll
-  for (int t = 0; t < kRotTile; ++t) {
-    const float x = (float)z[t];
-    float mn = x, mx = x;
-    if (c.ng == 4) {
-#pragma unroll
-      for (int off = 16; off >= 1; off >>= 1) {
-        mn = fminf(mn, __shfl_xor(mn, off, 32));
-        mx = fmaxf(mx, __shfl_xor(mx, off, 32));
-      }
-    } else {
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) {
-        mn = fminf(mn, __shfl_xor(mn, off));
-        mx = fmaxf(mx, __shfl_xor(mx, off));
-      }
-      if ((col & 63) == 0) {
-        red[col >> 6][t][0] = mn;
-        red[col >> 6][t][1] = mx;
-      }
-      __syncthreads();
-      mn = fminf(red[0][t][0], red[1][t][0]);
-      mx = fmaxf(red[0][t][1], red[1][t][1]);
+  for (int q = 0; q < 8; ++q) {  // unrolled: ya is indexed by q
+    __syncthreads();
+    for (int e = tid; e < 16 * kD; e += blockDim.x) {
+      const int rr = e >> 7, col = e & 127;
+      const int krow = KMAP == 0 ? 32 * (rr >> 2) + 4 * q + (rr & 3) : 16 * q + rr;
+      Bs[rr * kBsStride + col] = Bm[krow * kD + col];
     }
+    __syncthreads();
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const double b = ya[4 * q + d];
+      const double* br = Bs + (KMAP == 0 ? 4 * lk + d : 4 * d + lk) * kBsStride + li;
+#pragma unroll
+      for (int ct = 0; ct < 8; ++ct) acc[ct] = mfma64(br[16 * ct], b, acc[ct]);
+    }
+  }
+}
+
+// y's 32 channels 32 (l / 16) .. + 31 of a row of fp64 storage (zero when !ok).
+__device__ __forceinline__ void row_operand_f64(const double* row, bool ok, double (&ya)[32]) {
+  const double2* r2 = reinterpret_cast<const double2*>(row + 32 * ((threadIdx.x & 63) >> 4));
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const double2 x = ok ? r2[i] : make_double2(0.0, 0.0);
+    ya[2 * i] = x.x;
+    ya[2 * i + 1] = x.y;
+  }
+}
+
+// Rotation and quantization: zhat (the dequantized codes of (x - mu) R, fp64), the in-range mask, and
+// the effective rows zhat R^T. Block (64 tokens, KV head), wave w: tokens 16 w .. + 15 (one per lane
+// l % 16), every lane group l / 16 a quarter of the channels. A token's quantization group is spread
+// over its four lane groups: min / max through two cross-group exchanges.
+constexpr int kRotTile = 64;  // tokens per rotation work-group
+__global__ __launch_bounds__(256) void cal_rotq_kernel(CalSet S, CalCfg c, int value) {
+  __shared__ double Bs[16 * kBsStride];
+  const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
+  const int tok = blockIdx.x * kRotTile + 16 * w + li;
+  const bool ok = tok < S.T;
+  const size_t rowo = ((size_t)(ok ? tok : 0) * c.H + h) * kD;
+  const uint16_t* X = value ? S.v : S.k;
+  double ya[32];
+  {
+    const uint4* xr = reinterpret_cast<const uint4*>(X + rowo + 32 * lk);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      double d[8];
+      bf16x8_to_f64(ok ? xr[g] : make_uint4(0, 0, 0, 0), d);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        ya[8 * g + i] = ok ? d[i] - (value ? 0.0 : (double)c.mu[h * kD + 32 * lk + 8 * g + i]) : 0.0;
+    }
+  }
+  f64x4 acc[8];
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct) acc[ct] = f64x4{0.0, 0.0, 0.0, 0.0};
+  mat_t_rows<0>(ya, c.R + (size_t)h * kMat, Bs, acc);  // z = (x - mu) R: channel 16 ct + lk + 4 v
+  const float clip = value ? c.clip_v : c.clip_k;
+  // groups: 32 channels (tiles 2 g, 2 g + 1) or all 128 (one group)
+  const int ng = c.ng, tpg = 8 / ng;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    if (g >= ng) break;
+    float mn = INFINITY, mx = -INFINITY;
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) {
+      if (ct / tpg != g) continue;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float x = (float)acc[ct][v];
+        mn = fminf(mn, x);
+        mx = fmaxf(mx, x);
+      }
+    }
+    mn = fminf(mn, __shfl_xor(mn, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mn = fminf(mn, __shfl_xor(mn, 32));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
     uint32_t s_bits, z_bits;
     float zf, inv;
     int2_group_params(mn, mx, clip, s_bits, z_bits, zf, inv);
-    const uint32_t code = int2_code(x, zf, inv);
-    const double zh = (double)code * (double)__half2float(__ushort_as_half((unsigned short)s_bits)) + (double)zf;
+    const double sd = (double)__half2float(__ushort_as_half((unsigned short)s_bits));
     float lo = mn, hi = mx;
     if (clip != 1.0f) {
 #pragma clang fp contract(off)
       lo = clip * mn;
       hi = clip * mx;
     }
-    xs[t][col] = zh;
-    if (t < n) {
-      const size_t o = ((size_t)(s0 + t) * c.H + h) * kD + col;
-      S.zhat[o] = zh;
-      S.mask[o] = (x >= lo && x <= hi) ? 1 : 0;
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) {
+      if (ct / tpg != g) continue;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float x = (float)acc[ct][v];
+        const double zh = (double)int2_code(x, zf, inv) * sd + (double)zf;
+        ya[4 * ct + v] = zh;  // the B operand of the second product (KMAP 1)
+        if (ok) {
+          const size_t o = rowo + 16 * ct + lk + 4 * v;
+          S.zhat[o] = zh;
+          S.mask[o] = (x >= lo && x <= hi) ? 1 : 0;
+        }
+      }
     }
   }
-  __syncthreads();
-  // effective rows: zhat R^T, i.e. sum_i zhat[i] Rt[i][col]
-  const double* Rt = c.Rt + (size_t)h * kMat;
 #pragma unroll
-  for (int t = 0; t < kRotTile; ++t) z[t] = 0.0;
-  for (int i = 0; i < kD; ++i) {
-    const double r = Rt[i * kD + col];
+  for (int ct = 0; ct < 8; ++ct) acc[ct] = f64x4{0.0, 0.0, 0.0, 0.0};
+  mat_t_rows<1>(ya, c.Rt + (size_t)h * kMat, Bs, acc);  // effective rows zhat R^T
+  if (ok)
 #pragma unroll
-    for (int t = 0; t < kRotTile; ++t) z[t] = fma(xs[t][i], r, z[t]);
-  }
-  for (int t = 0; t < n; ++t) S.xeff[((size_t)(s0 + t) * c.H + h) * kD + col] = z[t];
+    for (int ct = 0; ct < 8; ++ct)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) S.xeff[rowo + 16 * ct + lk + 4 * v] = acc[ct][v];
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -167,14 +225,6 @@ constexpr int kTileRows = 16;
 constexpr int kTileThreads = 256;  // four waves; one token per thread in the softmax passes
 constexpr int kDlStride = 18;      // doubles per token of the staged row weights (16-byte rows)
 
-__device__ __forceinline__ void bf16x8_to_f64(uint4 u, double (&d)[8]) {
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    d[2 * i] = (double)__uint_as_float(w[i] << 16);
-    d[2 * i + 1] = (double)__uint_as_float(w[i] & 0xFFFF0000u);
-  }
-}
 
 // Row operand of a tile in matrix-core form: lane (li, lk) holds x[row li][32 lk + m], m = 0..31, for
 // the contraction over 128 channels taken as 32 steps m whose 4-deep slices are channels 32 k + m
@@ -477,51 +527,47 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_val_kernel(CalSet S, Cal
 
 // u = M_j dO for the rows of query head j (M_j = W_{O,j}^T W_{O,j}, symmetric), E = dO . u / d_model.
 // Keys: urow = u, lrow += lambda E. Values: wrow = 2 u / (d_model rows), lrow = E. Block (query head j,
-// 32 positions), thread (row r, 16 columns); M_j streams through LDS 16 rows at a time.
-constexpr int kUTile = 32;
+// 64 positions), the layout of the rotation kernel with positions as rows (a row's four lane groups
+// are in one wave, each reads dO at its own output channels before writing them).
+constexpr int kUTile = 64;
 __global__ __launch_bounds__(256) void cal_u_kernel(CalSet S, CalCfg c, int value) {
-  __shared__ double ds[kUTile][kD + 1];
-  __shared__ double ms[16][kD];
+  __shared__ double Bs[16 * kBsStride];
   const int j = blockIdx.x, h = j / c.gq, jj = j % c.gq, tid = threadIdx.x;
-  const int npos = S.nrows / c.gq, p0 = blockIdx.y * kUTile;
-  const int r = tid >> 3, cg = tid & 7;
-  for (int e = tid; e < kUTile * kD; e += blockDim.x) {
-    const int rr = e / kD, col = e % kD, pp = p0 + rr;
-    ds[rr][col] = pp < npos ? S.wrow[((size_t)h * S.nrows + (size_t)pp * c.gq + jj) * kD + col] : 0.0;
-  }
-  double acc[16];
+  const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
+  const int npos = S.nrows / c.gq, pp = blockIdx.y * kUTile + 16 * w + li;
+  const bool ok = pp < npos;
+  const size_t row = (size_t)h * S.nrows + (size_t)(ok ? pp : 0) * c.gq + jj;
+  double ya[32];
+  row_operand_f64(S.wrow + row * kD, ok, ya);
+  f64x4 acc[8];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc[i] = 0.0;
-  const double* M = c.gram + (size_t)j * kMat;
-  for (int b0 = 0; b0 < kD; b0 += 16) {
-    __syncthreads();
-    for (int e = tid; e < 16 * kD; e += blockDim.x) ms[e / kD][e % kD] = M[(size_t)(b0 + e / kD) * kD + e % kD];
-    __syncthreads();
-#pragma unroll 4
-    for (int b = 0; b < 16; ++b) {
-      const double d = ds[r][b0 + b];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[i] = fma(d, ms[b][cg * 16 + i], acc[i]);
-    }
-  }
+  for (int ct = 0; ct < 8; ++ct) acc[ct] = f64x4{0.0, 0.0, 0.0, 0.0};
+  mat_t_rows<0>(ya, c.gram + (size_t)j * kMat, Bs, acc);
   double e = 0.0;
+  if (ok)
 #pragma unroll
-  for (int i = 0; i < 16; ++i) e = fma(ds[r][cg * 16 + i], acc[i], e);
-  e += __shfl_xor(e, 1);
-  e += __shfl_xor(e, 2);
-  e += __shfl_xor(e, 4);
-  const int pp = p0 + r;
-  if (pp >= npos) return;
-  const size_t row = (size_t)h * S.nrows + (size_t)pp * c.gq + jj;
+    for (int ct = 0; ct < 8; ++ct)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) e = fma(S.wrow[row * kD + 16 * ct + lk + 4 * v], acc[ct][v], e);
+  e += __shfl_xor(e, 16);
+  e += __shfl_xor(e, 32);
+  if (!ok) return;
   const double dm = (double)c.dm;
-  if (value) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) S.wrow[row * kD + cg * 16 + i] = 2.0 * acc[i] / (dm * (double)S.nrows);
-    if (cg == 0) S.lrow[row] = e / dm;
-  } else {
+  for (int ct = 0; ct < 8; ++ct)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) S.urow[row * kD + cg * 16 + i] = acc[i];
-    if (cg == 0) S.lrow[row] += c.lam * e / dm;
+    for (int v = 0; v < 4; ++v) {
+      const size_t o = row * kD + 16 * ct + lk + 4 * v;
+      if (value)
+        S.wrow[o] = 2.0 * acc[ct][v] / (dm * (double)S.nrows);
+      else
+        S.urow[o] = acc[ct][v];
+    }
+  if (lk == 0) {
+    if (value)
+      S.lrow[row] = e / dm;
+    else
+      S.lrow[row] += c.lam * e / dm;
   }
 }
 
@@ -685,52 +731,73 @@ __global__ __launch_bounds__(256) void cal_gx_kernel(CalSet S, CalCfg c, int val
   }
 }
 
-// gz = mask . (gx R): block (16-token tile, KV head), thread = channel.
-__global__ __launch_bounds__(128) void cal_gz_kernel(CalSet S, CalCfg c) {
-  __shared__ double gs[kRotTile][kD];
-  const int h = blockIdx.y, col = threadIdx.x, s0 = blockIdx.x * kRotTile;
-  const int n = min(kRotTile, S.T - s0);
-  for (int t = 0; t < kRotTile; ++t) gs[t][col] = t < n ? S.gx[((size_t)(s0 + t) * c.H + h) * kD + col] : 0.0;
-  __syncthreads();
-  const double* R = c.R + (size_t)h * kMat;
-  double z[kRotTile];
+// gz = mask . (gx R): block (64 tokens, KV head), the layout of the rotation kernel.
+__global__ __launch_bounds__(256) void cal_gz_kernel(CalSet S, CalCfg c) {
+  __shared__ double Bs[16 * kBsStride];
+  const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
+  const int tok = blockIdx.x * kRotTile + 16 * w + li;
+  const bool ok = tok < S.T;
+  const size_t rowo = ((size_t)(ok ? tok : 0) * c.H + h) * kD;
+  double ya[32];
+  row_operand_f64(S.gx + rowo, ok, ya);
+  f64x4 acc[8];
 #pragma unroll
-  for (int t = 0; t < kRotTile; ++t) z[t] = 0.0;
-  for (int i = 0; i < kD; ++i) {
-    const double r = R[i * kD + col];
+  for (int ct = 0; ct < 8; ++ct) acc[ct] = f64x4{0.0, 0.0, 0.0, 0.0};
+  mat_t_rows<0>(ya, c.R + (size_t)h * kMat, Bs, acc);
+  if (ok)
 #pragma unroll
-    for (int t = 0; t < kRotTile; ++t) z[t] = fma(gs[t][i], r, z[t]);
-  }
-  for (int t = 0; t < n; ++t) {
-    const size_t o = ((size_t)(s0 + t) * c.H + h) * kD + col;
-    S.gz[o] = S.mask[o] ? z[t] : 0.0;
-  }
+    for (int ct = 0; ct < 8; ++ct)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const size_t o = rowo + 16 * ct + lk + 4 * v;
+        S.gz[o] = S.mask[o] ? acc[ct][v] : 0.0;
+      }
 }
 
-// Partial dL/dR over a token slice: sum_s x_s[a] gz_s[b] + gx_s[a] zhat_s[b], block (16 rows a,
-// KV head, slice), thread = column b.
-__global__ __launch_bounds__(128) void cal_dr_kernel(CalSet S, CalCfg c, int value) {
-  const int a0 = blockIdx.x * 16, h = blockIdx.y, sp = blockIdx.z, b = threadIdx.x;
+// Partial dL/dR over a token slice: sum_s x_s[a] gz_s[b] + gx_s[a] zhat_s[b] on the fp64 matrix
+// cores (M = a, N = b, K = the slice's tokens, four per step). Block (KV head, slice) of eight
+// waves, wave w: rows a = 16 w .. + 15 and all 128 columns; 16-token chunks of the four operands
+// staged in LDS.
+constexpr int kDrChunk = 16, kDrStride = 132;
+__global__ __launch_bounds__(512) void cal_dr_kernel(CalSet S, CalCfg c, int value) {
+  __shared__ double xs[kDrChunk][kDrStride], gxs[kDrChunk][kDrStride];
+  __shared__ double gzs[kDrChunk][kDrStride], zs[kDrChunk][kDrStride];
+  const int h = blockIdx.x, sp = blockIdx.y, tid = threadIdx.x;
+  const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
   const int s_lo = (int)((long long)S.T * sp / kCalSplit), s_hi = (int)((long long)S.T * (sp + 1) / kCalSplit);
-  __shared__ double xa[16], ga[16];
-  double acc[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) acc[i] = 0.0;
   const uint16_t* X = value ? S.v : S.k;
-  for (int s = s_lo; s < s_hi; ++s) {
-    const size_t base = ((size_t)s * c.H + h) * kD;
+  f64x4 acc[8];
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct) acc[ct] = f64x4{0.0, 0.0, 0.0, 0.0};
+  for (int s0 = s_lo; s0 < s_hi; s0 += kDrChunk) {
     __syncthreads();
-    if (b < 16) {
-      xa[b] = bf16d(X[base + a0 + b]) - (value ? 0.0 : (double)c.mu[h * kD + a0 + b]);
-      ga[b] = S.gx[base + a0 + b];
+    for (int e = tid; e < kDrChunk * kD; e += blockDim.x) {
+      const int t = e >> 7, col = e & 127, s = s0 + t;
+      const bool ok = s < s_hi;
+      const size_t o = ((size_t)(ok ? s : s_lo) * c.H + h) * kD + col;
+      xs[t][col] = ok ? bf16d(X[o]) - (value ? 0.0 : (double)c.mu[h * kD + col]) : 0.0;
+      gxs[t][col] = ok ? S.gx[o] : 0.0;
+      gzs[t][col] = ok ? S.gz[o] : 0.0;
+      zs[t][col] = ok ? S.zhat[o] : 0.0;
     }
     __syncthreads();
-    const double gzb = S.gz[base + b], zb = S.zhat[base + b];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) acc[i] = fma(xa[i], gzb, fma(ga[i], zb, acc[i]));
+    for (int k4 = 0; k4 < kDrChunk; k4 += 4) {
+      const int t = k4 + lk;
+      const double ax = xs[t][16 * w + li], ag = gxs[t][16 * w + li];
+#pragma unroll
+      for (int ct = 0; ct < 8; ++ct) {
+        acc[ct] = mfma64(ax, gzs[t][16 * ct + li], acc[ct]);
+        acc[ct] = mfma64(ag, zs[t][16 * ct + li], acc[ct]);
+      }
+    }
   }
+  // element v of acc[ct]: row a = 16 w + lk + 4 v, column b = 16 ct + li
+  double* out = c.drp + ((size_t)sp * c.H + h) * kMat;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) c.drp[(((size_t)sp * c.H + h) * kD + a0 + i) * kD + b] = acc[i];
+  for (int ct = 0; ct < 8; ++ct)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) out[(16 * w + lk + 4 * v) * kD + 16 * ct + li] = acc[ct][v];
 }
 
 __global__ __launch_bounds__(256) void cal_dr_reduce_kernel(CalCfg c) {
@@ -742,8 +809,8 @@ __global__ __launch_bounds__(256) void cal_dr_reduce_kernel(CalCfg c) {
 }
 
 // ---------------------------------------------------------------------------------------------
-// Matrix functions: one work-group of 1024 threads per KV head; thread (4 rows, 4 columns) of a
-// 128 x 128 product, operands staged through LDS in 16-wide slices.
+// Matrix functions: one work-group of 1024 threads per KV head; 128 x 128 products on the fp64
+// matrix cores, operands staged through LDS in 16-deep slices.
 struct ExpLds {
   double at[16][kD];  // op(A)^T chunk: at[k][r] = op(A)[r][k0 + k]
   double bs[16][kD];  // B chunk: bs[k][c] = B[k0 + k][c]
@@ -1174,14 +1241,14 @@ hipError_t cal_gram(const CalCfg& c, const uint16_t* W_o, hipStream_t s) {
 static void rot_and_quant(const CalCfg& c, CalSet& set, const double* A, int value, hipStream_t s) {
   hipLaunchKernelGGL(cal_expm_kernel, dim3(c.H), dim3(kExpThreads), 0, s, c, A, value);
   if (set.T > 0)
-    hipLaunchKernelGGL(cal_rotq_kernel, dim3((set.T + kRotTile - 1) / kRotTile, c.H), dim3(kD), 0, s, set, c, value);
+    hipLaunchKernelGGL(cal_rotq_kernel, dim3((set.T + kRotTile - 1) / kRotTile, c.H), dim3(256), 0, s, set, c, value);
 }
 
 static void backward(const CalCfg& c, CalSet& set, const double* A, int value, double* grad, hipStream_t s) {
   if (set.T > 0) {
     hipLaunchKernelGGL(cal_gx_kernel, dim3((set.T + kGxTok - 1) / kGxTok, c.H), dim3(256), 0, s, set, c, value);
-    hipLaunchKernelGGL(cal_gz_kernel, dim3((set.T + kRotTile - 1) / kRotTile, c.H), dim3(kD), 0, s, set, c);
-    hipLaunchKernelGGL(cal_dr_kernel, dim3(kD / 16, c.H, kCalSplit), dim3(kD), 0, s, set, c, value);
+    hipLaunchKernelGGL(cal_gz_kernel, dim3((set.T + kRotTile - 1) / kRotTile, c.H), dim3(256), 0, s, set, c);
+    hipLaunchKernelGGL(cal_dr_kernel, dim3(c.H, kCalSplit), dim3(512), 0, s, set, c, value);
   } else {
     hipLaunchKernelGGL(cal_fill_kernel, dim3((unsigned)((kCalSplit * (size_t)c.H * kMat + 255) / 256)), dim3(256), 0,
                        s, c.drp, kCalSplit * (size_t)c.H * kMat, 0.0);
