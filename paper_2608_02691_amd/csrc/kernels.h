@@ -161,8 +161,8 @@ struct CalSet {
   long long pelems;                // per KV head: sum over sequences of rows * len
   CalSeq* seqs;                    // [nseq]
   int* row_seq;                    // [nrows]: sequence of each row
-  double *zhat, *xeff, *gx, *gz;   // [T, H, 128]: dequantized rotated rows, effective rows, gradients
-  uint8_t* mask;                   // [T, H, 128]: straight-through mask
+  double *zhat, *xeff, *gx, *gz;   // [H, T, 128]: dequantized rotated rows, effective rows, gradients
+  uint8_t* mask;                   // [H, T, 128]: straight-through mask
   double* pd;                      // [H, pelems]: key probabilities, then logit gradients (key loss)
   double* pf;                      // [H, pelems]: full-precision probabilities (key loss)
   double* wrow;                    // [H, nrows, 128]: dO per row, then the value-loss row weights

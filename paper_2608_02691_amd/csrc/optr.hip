@@ -72,6 +72,10 @@ __device__ double block_max(double x, double* red) {
   return t;
 }
 
+// Offset of token s, KV head h in the per-head rows of the workspace ([H, T, 128]: each head's
+// rows contiguous), as against the traces' [T, H, 128].
+__device__ __forceinline__ size_t hrow(const CalSet& S, int s, int h) { return ((size_t)h * S.T + s) * kD; }
+
 __device__ __forceinline__ bool int2_token(int s, int t, int sink, int recent) {
   return s >= sink && s <= t - recent;
 }
@@ -138,11 +142,11 @@ __global__ __launch_bounds__(256) void cal_rotq_kernel(CalSet S, CalCfg c, int v
   const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
   const int tok = blockIdx.x * kRotTile + 16 * w + li;
   const bool ok = tok < S.T;
-  const size_t rowo = ((size_t)(ok ? tok : 0) * c.H + h) * kD;
+  const size_t xo = ((size_t)(ok ? tok : 0) * c.H + h) * kD, rowo = hrow(S, ok ? tok : 0, h);
   const uint16_t* X = value ? S.v : S.k;
   double ya[32];
   {
-    const uint4* xr = reinterpret_cast<const uint4*>(X + rowo + 32 * lk);
+    const uint4* xr = reinterpret_cast<const uint4*>(X + xo + 32 * lk);
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       double d[8];
@@ -380,7 +384,7 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_fwd_kernel(CalSet S, Cal
     // some row reads a token of this tile from INT2 (uniform over the wave)
     const bool any_q2 = 16 * tt + 15 >= c.sink && 16 * tt <= tmax - c.recent;
     f64x4 ak = {0.0, 0.0, 0.0, 0.0};
-    if (any_q2) ak = dot_tokens_f64(qa, S.xeff + o, ok, lk);
+    if (any_q2) ak = dot_tokens_f64(qa, S.xeff + hrow(S, ok ? a0 + s : a0, h), ok, lk);
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int r = lk + 4 * v, tr = tf + r / gq;
@@ -511,7 +515,7 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_val_kernel(CalSet S, Cal
       const size_t o = ((size_t)(a0 + base + j) * c.H + h) * kD + 8 * li;
       double y[8];
       bf16x8_to_f64(ok ? *reinterpret_cast<const uint4*>(S.v + o) : make_uint4(0, 0, 0, 0), y);
-      const double2* x2 = reinterpret_cast<const double2*>(S.xeff + o);
+      const double2* x2 = reinterpret_cast<const double2*>(S.xeff + hrow(S, ok ? a0 + base + j : a0, h) + 8 * li);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const double2 x = ok ? x2[i] : make_double2(0.0, 0.0);
@@ -724,7 +728,7 @@ __global__ __launch_bounds__(256) void cal_gx_kernel(CalSet S, CalCfg c, int val
   for (int v = 0; v < 4; ++v) {
     const int s = s0 + 16 * w + lk + 4 * v;
     if (s < S.T) {
-      double* out = S.gx + ((size_t)s * c.H + h) * kD + li;
+      double* out = S.gx + hrow(S, s, h) + li;
 #pragma unroll
       for (int t = 0; t < 8; ++t) out[16 * t] = acc[t][v];
     }
@@ -737,7 +741,7 @@ __global__ __launch_bounds__(256) void cal_gz_kernel(CalSet S, CalCfg c) {
   const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
   const int tok = blockIdx.x * kRotTile + 16 * w + li;
   const bool ok = tok < S.T;
-  const size_t rowo = ((size_t)(ok ? tok : 0) * c.H + h) * kD;
+  const size_t rowo = hrow(S, ok ? tok : 0, h);
   double ya[32];
   row_operand_f64(S.gx + rowo, ok, ya);
   f64x4 acc[8];
@@ -774,11 +778,11 @@ __global__ __launch_bounds__(512) void cal_dr_kernel(CalSet S, CalCfg c, int val
     for (int e = tid; e < kDrChunk * kD; e += blockDim.x) {
       const int t = e >> 7, col = e & 127, s = s0 + t;
       const bool ok = s < s_hi;
-      const size_t o = ((size_t)(ok ? s : s_lo) * c.H + h) * kD + col;
+      const size_t o = ((size_t)(ok ? s : s_lo) * c.H + h) * kD + col, io = hrow(S, ok ? s : s_lo, h) + col;
       xs[t][col] = ok ? bf16d(X[o]) - (value ? 0.0 : (double)c.mu[h * kD + col]) : 0.0;
-      gxs[t][col] = ok ? S.gx[o] : 0.0;
-      gzs[t][col] = ok ? S.gz[o] : 0.0;
-      zs[t][col] = ok ? S.zhat[o] : 0.0;
+      gxs[t][col] = ok ? S.gx[io] : 0.0;
+      gzs[t][col] = ok ? S.gz[io] : 0.0;
+      zs[t][col] = ok ? S.zhat[io] : 0.0;
     }
     __syncthreads();
 #pragma unroll
