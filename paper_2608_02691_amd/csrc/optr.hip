@@ -133,11 +133,11 @@ __device__ __forceinline__ void row_operand_f64(const double* row, bool ok, doub
 }
 
 // Rotation and quantization: zhat (the dequantized codes of (x - mu) R, fp64), the in-range mask, and
-// the effective rows zhat R^T. Block (64 tokens, KV head), wave w: tokens 16 w .. + 15 (one per lane
+// the effective rows zhat R^T. Block (128 tokens, KV head), wave w: tokens 16 w .. + 15 (one per lane
 // l % 16), every lane group l / 16 a quarter of the channels. A token's quantization group is spread
 // over its four lane groups: min / max through two cross-group exchanges.
-constexpr int kRotTile = 64;  // tokens per rotation work-group
-__global__ __launch_bounds__(256) void cal_rotq_kernel(CalSet S, CalCfg c, int value) {
+constexpr int kRotTile = 128;  // tokens per rotation work-group (eight waves of 16)
+__global__ __launch_bounds__(512) void cal_rotq_kernel(CalSet S, CalCfg c, int value) {
   __shared__ double Bs[16 * kBsStride];
   const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
   const int tok = blockIdx.x * kRotTile + 16 * w + li;
@@ -736,10 +736,11 @@ __global__ __launch_bounds__(256) void cal_gx_kernel(CalSet S, CalCfg c, int val
 }
 
 // gz = mask . (gx R): block (64 tokens, KV head), the layout of the rotation kernel.
+constexpr int kGzTile = 64;
 __global__ __launch_bounds__(256) void cal_gz_kernel(CalSet S, CalCfg c) {
   __shared__ double Bs[16 * kBsStride];
   const int h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
-  const int tok = blockIdx.x * kRotTile + 16 * w + li;
+  const int tok = blockIdx.x * kGzTile + 16 * w + li;
   const bool ok = tok < S.T;
   const size_t rowo = hrow(S, ok ? tok : 0, h);
   double ya[32];
@@ -1245,13 +1246,13 @@ hipError_t cal_gram(const CalCfg& c, const uint16_t* W_o, hipStream_t s) {
 static void rot_and_quant(const CalCfg& c, CalSet& set, const double* A, int value, hipStream_t s) {
   hipLaunchKernelGGL(cal_expm_kernel, dim3(c.H), dim3(kExpThreads), 0, s, c, A, value);
   if (set.T > 0)
-    hipLaunchKernelGGL(cal_rotq_kernel, dim3((set.T + kRotTile - 1) / kRotTile, c.H), dim3(256), 0, s, set, c, value);
+    hipLaunchKernelGGL(cal_rotq_kernel, dim3((set.T + kRotTile - 1) / kRotTile, c.H), dim3(512), 0, s, set, c, value);
 }
 
 static void backward(const CalCfg& c, CalSet& set, const double* A, int value, double* grad, hipStream_t s) {
   if (set.T > 0) {
     hipLaunchKernelGGL(cal_gx_kernel, dim3((set.T + kGxTok - 1) / kGxTok, c.H), dim3(256), 0, s, set, c, value);
-    hipLaunchKernelGGL(cal_gz_kernel, dim3((set.T + kRotTile - 1) / kRotTile, c.H), dim3(256), 0, s, set, c);
+    hipLaunchKernelGGL(cal_gz_kernel, dim3((set.T + kGzTile - 1) / kGzTile, c.H), dim3(256), 0, s, set, c);
     hipLaunchKernelGGL(cal_dr_kernel, dim3(c.H, kCalSplit), dim3(512), 0, s, set, c, value);
   } else {
     hipLaunchKernelGGL(cal_fill_kernel, dim3((unsigned)((kCalSplit * (size_t)c.H * kMat + 255) / 256)), dim3(256), 0,
