@@ -632,7 +632,16 @@ def main():
     c1.record()
     torch.cuda.synchronize()
     copy_gbps = 3 * 2 * (1 << 30) / (c0.elapsed_time(c1) * 1e-3) / 1e9
-    del cp_src, cp_dst
+    # and a read-only stream of the same 1 GiB (torch's sum over int64 words: plain loads)
+    rd = cp_src.view(torch.int64)
+    rd.sum()
+    c0.record()
+    for _ in range(3):
+        rd.sum()
+    c1.record()
+    torch.cuda.synchronize()
+    read_gbps = 3 * (1 << 30) / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del cp_src, cp_dst, rd
 
     dom_gbps = dom_bytes / (dom_ms * 1e-3) / 1e9
     step_gbps = step_bytes / (ms_step * 1e-3) / 1e9
@@ -706,7 +715,8 @@ def main():
             "timed_launches": args.samples,
             "caches": caches,
         },
-        "context": {"hbm_copy_gbps": copy_gbps, "copy": "1 GiB device-to-device copy, read + write bytes"},
+        "context": {"hbm_copy_gbps": copy_gbps, "copy": "1 GiB device-to-device copy, read + write bytes",
+                    "hbm_read_gbps": read_gbps, "read": "torch sum over the same 1 GiB (plain loads), bytes read"},
     }
     if diag is not None:
         result["diagnostics"] = diag
