@@ -124,3 +124,40 @@ def test_calibration_matches_oracle_step_by_step():
         np.testing.assert_allclose(out["R_k"][h].cpu().numpy(), ref["R_k"].astype(np.float32), rtol=0, atol=2e-7)
         np.testing.assert_allclose(out["R_v"][h].cpu().numpy(), ref["R_v"].astype(np.float32), rtol=0, atol=2e-7)
         print(f"head {h}: key {hist[0, h, :3]}..., value {hist[1, h, :3]}...", flush=True)
+
+
+@pytest.mark.parametrize("gq", [1, 3, 16])
+def test_objectives_other_query_groups_match_oracle(gq):
+    """The row tiles hold 16 / G_q positions of G_q query heads: one query head per KV head (16
+    positions per tile), three (five positions, one row of the 16 unused) and sixteen (one position);
+    sequences shorter than and longer than the final-position count, G = 128 with windows."""
+    print(f"\n[optr loss gq={gq}]", flush=True)
+    H, Hq = 2, 2 * gq
+    w = W.make_workload(1, batch=1, ctx=16, num_q_heads=Hq, num_kv_heads=H, d_model=64)
+    data = _structured([90, 13, 41], 11, H=H, Hq=Hq)
+    k, v, q, st = data
+    tr = _traces(data)
+    mu = P.key_mean(k)
+    kw = dict(group=128, n_last=20, sink=2, recent=5)
+    cfg = K.optr_config(H, Hq, 64, group_size=128, clip_k=0.96, clip_v=0.92, lambda_k=0.5, n_last=20, sink=2,
+                        recent=5)
+    rng = np.random.default_rng(12)
+    A = rng.standard_normal((H, 128, 128)) * 0.02
+    Av = rng.standard_normal((H, 128, 128)) * 0.02
+    lk, gk = K.int2kv_optr_key_loss(cfg, tr, dev(w.R_k), dev(mu), dev(w.W_o), dev(A))
+    lv, gv = K.int2kv_optr_value_loss(cfg, tr, dev(w.R_k), dev(A), dev(mu), dev(w.R_v), dev(w.W_o), dev(Av))
+    lk, gk, lv, gv = (x.cpu().numpy() for x in (lk, gk, lv, gv))
+    for h in range(H):
+        At = torch.from_numpy(A[h].copy()).requires_grad_(True)
+        L = P.key_loss(At, w.R_k, k, v, q, st, mu, w.W_o, h, gq, lam=0.5, clip=0.96, **kw)
+        L.backward()
+        assert abs(lk[h] - float(L.detach())) <= LOSS_RTOL * abs(float(L.detach())), (h, lk[h], float(L.detach()))
+        g = At.grad.numpy()
+        assert np.linalg.norm(gk[h] - g) <= GRAD_RTOL * np.linalg.norm(g)
+        probs = P.key_probs(w.R_k, A[h], k, q, st, mu, h, gq, clip=0.96, **kw)
+        Bt = torch.from_numpy(Av[h].copy()).requires_grad_(True)
+        Lv = P.value_loss(Bt, w.R_v, v, st, probs, w.W_o, h, gq, clip=0.92, **kw)
+        Lv.backward()
+        assert abs(lv[h] - float(Lv.detach())) <= LOSS_RTOL * abs(float(Lv.detach()))
+        gvr = Bt.grad.numpy()
+        assert np.linalg.norm(gv[h] - gvr) <= GRAD_RTOL * np.linalg.norm(gvr)
