@@ -740,6 +740,7 @@ static int optr_setup(const int2kv_optr_config* cfg, const int2kv_optr_traces* t
   hipError_t e = cal_bind_set(set, base + L.shared, tr->k, tr->v, tr->q, tr->seq_starts, tr->num_seqs, g.H, g.gq,
                               g.n_last, stream);
   if (e == hipSuccess) e = cal_gram(g, W_o, stream);
+  if (e == hipSuccess) e = cal_prepare_set(g, set, stream);
   state = base + L.shared + L.set_c;
   return hip_status(e, "optr setup");
 }
@@ -791,6 +792,8 @@ int int2kv_optr_calibrate(const int2kv_optr_config* cfg, const int2kv_optr_trace
     e = cal_bind_set(sh, base + L.shared + L.set_c, heldout->k, heldout->v, heldout->q, heldout->seq_starts,
                      heldout->num_seqs, g.H, g.gq, g.n_last, stream);
   if (e == hipSuccess) e = cal_gram(g, W_o, stream);
+  if (e == hipSuccess) e = cal_prepare_set(g, sc, stream);
+  if (e == hipSuccess) e = cal_prepare_set(g, sh, stream);
   if (e != hipSuccess) return hip_status(e, "optr_calibrate setup");
   const size_t nA = (size_t)g.H * kHeadDim * kHeadDim;
   double* st = reinterpret_cast<double*>(base + L.shared + L.set_c + L.set_h);

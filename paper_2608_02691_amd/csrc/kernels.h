@@ -163,8 +163,15 @@ struct CalSet {
   int* row_seq;                    // [nrows]: sequence of each row
   double *zhat, *xeff, *gx, *gz;   // [H, T, 128]: dequantized rotated rows, effective rows, gradients
   uint8_t* mask;                   // [H, T, 128]: straight-through mask
-  double* pd;                      // [H, pelems]: key probabilities, then logit gradients (key loss)
-  double* pf;                      // [H, pelems]: full-precision probabilities (key loss)
+  double* pd;                      // [H, pelems]: key probabilities, then logit gradients, on the tokens
+                                   // read from INT2 (zero elsewhere, set once)
+  double* pf;                      // [H, pelems]: scratch of the key-loss gradient
+  double* fc;                      // [H, pelems]: full-precision logits f (rotation-independent, set once)
+  double* pc;                      // [H, pelems]: full-precision probabilities p = softmax(f) (set once)
+  double* rc;                      // [H, nrows, 2]: per row lse_f and LW (log-sum-exp of f over the row's
+                                   // BF16-window tokens, -inf when none) (set once)
+  double* wt;                      // [H, nrows, 128]: per row sum over its window tokens of exp(f - LW) v (set once)
+  double* erow;                    // [H, nrows]: exp(LW - lse_k) of the latest key forward
   double* wrow;                    // [H, nrows, 128]: dO per row, then the value-loss row weights
   double* urow;                    // [H, nrows, 128]: M_j dO per row (key loss)
   double* lrow;                    // [H, nrows]: per-row losses
@@ -190,6 +197,8 @@ hipError_t cal_bind_set(CalSet& set, uint8_t* base, const uint16_t* k, const uin
 void cal_bind_shared(CalCfg& c, uint8_t* base);
 hipError_t cal_gram(const CalCfg& c, const uint16_t* W_o, hipStream_t s);
 // loss[h] (device) of every KV head at generators A [H, 128, 128]; grad (may be null) receives dL/dA
+// The rotation-independent part of the key objective for a bound set (after cal_bind_set, before any loss).
+hipError_t cal_prepare_set(const CalCfg& c, CalSet& set, hipStream_t s);
 hipError_t cal_key_loss(const CalCfg& c, CalSet& set, const double* A, double* loss, double* grad, hipStream_t s);
 hipError_t cal_key_probs(const CalCfg& c, CalSet& set, const double* A, hipStream_t s);
 hipError_t cal_value_loss(const CalCfg& c, CalSet& set, const double* A, double* loss, double* grad, hipStream_t s);

@@ -277,8 +277,10 @@ __device__ __forceinline__ void acc_channels(f64x4 (&acc)[8], double a, const do
 }
 
 // Sums the four waves' channel accumulators in the fixed order (w0 + w2) + (w1 + w3) through buf
-// (32 KiB of LDS, free on entry) and stores rows r < nr at out + r 128 (row lk + 4 v, channel 8 li + t).
-__device__ __forceinline__ void sum_waves_store(f64x4 (&acc)[8], double* buf, double* out, int nr) {
+// (32 KiB of LDS, free on entry) and stores rows r < nr at out + r 128 (row lk + 4 v, channel 8 li + t),
+// plus add_w[r] times row r of add when add is given (add_w visible to wave 0 at entry).
+__device__ __forceinline__ void sum_waves_store(f64x4 (&acc)[8], double* buf, double* out, int nr,
+                                                const double* add = nullptr, const double* add_w = nullptr) {
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63, li = l & 15, lk = l >> 4;
   __syncthreads();
   if (w >= 2)
@@ -306,6 +308,9 @@ __device__ __forceinline__ void sum_waves_store(f64x4 (&acc)[8], double* buf, do
       double o[8];
 #pragma unroll
       for (int t = 0; t < 8; ++t) o[t] = acc[t][v] + buf[(4 * t + v) * 64 + l];
+      if (r < nr && add)
+#pragma unroll
+        for (int t = 0; t < 8; ++t) o[t] = fma(add_w[r], add[(size_t)r * kD + 8 * li + t], o[t]);
       if (r < nr) {
         double2* dst = reinterpret_cast<double2*>(out + (size_t)r * kD + 8 * li);
 #pragma unroll
@@ -341,15 +346,16 @@ __device__ __forceinline__ void rows_max(const double (&m4)[4], double* red4, do
 // The tile's 4-token steps of a 256-token chunk for wave w: tokens 64 w + k4 + lk, k4 = 0, 4, ..., 60,
 // those below end.
 
-// Forward of the key objective on a tile: logits over the full-precision and the effective keys,
-// both softmaxes, KL(p || p^K) into lrow, p into pf and p^K into pd (per row, every token of the
-// sequence; 0 past the row's position), and dO = sum_s (p^K - p) v_s into wrow. With probs_only:
-// pd = p^K on the tokens read from INT2 and 0 elsewhere, nothing else. Block (tile, KV head).
-// Logits: q.(k - mu) = q.k - q.mu, with q.mu once per row.
-__global__ __launch_bounds__(kTileThreads) void cal_pos_fwd_kernel(CalSet S, CalCfg c, int probs_only) {
+// The rotation-independent part of the key objective, once per set: for every row the full-precision
+// logits f_s = q.(k_s - mu)/sqrt(d) over its tokens s <= t_r (fc; q.(k - mu) = q.k - q.mu with q.mu once
+// per row), p = softmax(f) (pc), lse_f and LW = log-sum-exp of f over the row's tokens held in BF16
+// windows (-inf when none) (rc), and W~ = sum over those tokens of exp(f_s - LW) v_s (wt). A window
+// token keeps g_s = f_s under every rotation, so the key forward needs only these sums for them.
+// Block (tile, KV head), the layout of the key forward.
+__global__ __launch_bounds__(kTileThreads) void cal_const_kernel(CalSet S, CalCfg c) {
   constexpr int R = kTileRows;
   __shared__ double qmu[R];
-  __shared__ double red4[2][4 * R];
+  __shared__ double red4[4 * R];
   __shared__ __align__(16) double dl[kTileThreads * kDlStride];
   const int h = blockIdx.y, tid = threadIdx.x, gq = c.gq;
   const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
@@ -357,9 +363,8 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_fwd_kernel(CalSet S, Cal
   const CalSeq sq = S.seqs[tile.x];
   const int row0 = tile.y, nr = tile.z, tf = tile.w, a0 = sq.start, L = sq.len;
   const int tmax = tf + (nr - 1) / gq;
-  // rows of the tile are consecutive rows of the sequence's [rows][len] blocks
-  double* pdb = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;  // row r at + r L
-  double* pfb = S.pf + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
+  const size_t pb = (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;  // row r at + r L
+  double *fcb = S.fc + pb, *pcb = S.pc + pb;
   double qa[32];
   rows_operand_bf16(S.q + ((size_t)(a0 + tf + li / gq) * c.Hq + h * gq + li % gq) * kD, li < nr, lk, qa);
   {
@@ -371,101 +376,71 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_fwd_kernel(CalSet S, Cal
     if (w == 0 && lk == 0) qmu[li] = t;
   }
   __syncthreads();
-  // logits: wave w takes the 16-token tiles w, w + 4, ...; lane (li, lk) ends with rows lk + 4 v of
-  // token 16 tt + li
-  double m4f[4], m4k[4];
+  double m4f[4];
 #pragma unroll
-  for (int v = 0; v < 4; ++v) m4f[v] = m4k[v] = -INFINITY;
+  for (int v = 0; v < 4; ++v) m4f[v] = -INFINITY;
   for (int tt = w; 16 * tt <= tmax; tt += 4) {
     const int s = 16 * tt + li;
     const bool ok = s <= tmax;
-    const size_t o = ((size_t)(a0 + s) * c.H + h) * kD;
-    const f64x4 af = dot_tokens_bf16(qa, S.k + o, ok, lk);
-    // some row reads a token of this tile from INT2 (uniform over the wave)
-    const bool any_q2 = 16 * tt + 15 >= c.sink && 16 * tt <= tmax - c.recent;
-    f64x4 ak = {0.0, 0.0, 0.0, 0.0};
-    if (any_q2) ak = dot_tokens_f64(qa, S.xeff + hrow(S, ok ? a0 + s : a0, h), ok, lk);
+    const f64x4 af = dot_tokens_bf16(qa, S.k + ((size_t)(a0 + s) * c.H + h) * kD, ok, lk);
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int r = lk + 4 * v, tr = tf + r / gq;
       if (r < nr && s <= tr) {
         const double f = (af[v] - qmu[r]) * kInvSqrtD;
-        const double g = int2_token(s, tr, c.sink, c.recent) ? ak[v] * kInvSqrtD : f;
-        pfb[(size_t)r * L + s] = f;
-        pdb[(size_t)r * L + s] = g;
+        fcb[(size_t)r * L + s] = f;
         m4f[v] = fmax(m4f[v], f);
-        m4k[v] = fmax(m4k[v], g);
       }
     }
   }
-  // softmax passes: wave w owns rows rb .. rb + 3 (rb = 4 w), lane l the tokens l, l + 64, ...
   const int rb = 4 * w;
-  double mf[4], mk[4];
-  rows_max(m4f, red4[0], mf);  // its barriers also make the logits visible to the whole block
-  rows_max(m4k, red4[1], mk);
+  double mf[4];
+  rows_max(m4f, red4, mf);  // its barriers also make the logits visible to the whole block
   int tr4[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) tr4[i] = rb + i < nr ? tf + (rb + i) / gq : -1;  // last position of each row
-  // e = exp(logit - row max) in place of the logits, the row sums z and, for KL(p || p^K) =
-  // sum_s p_s (f_s - g_s) - (lse_f - lse_k), the sums sum_s e^f_s (f_s - g_s)
-  double zf[4], zk[4], sfg[4];
+  for (int i = 0; i < 4; ++i) tr4[i] = rb + i < nr ? tf + (rb + i) / gq : -1;
+  double zf[4], zw[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) zf[i] = zk[i] = sfg[i] = 0.0;
+  for (int i = 0; i < 4; ++i) zf[i] = zw[i] = 0.0;
   for (int s = l; s <= tmax; s += 64)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       if (s > tr4[i]) continue;
-      const size_t o = (size_t)(rb + i) * L + s;
-      const double f = pfb[o], g = pdb[o];
-      const double ef = exp(f - mf[i]), ek = exp(g - mk[i]);
-      pfb[o] = ef;  // this lane's own elements
-      pdb[o] = ek;
-      zf[i] += ef;
-      zk[i] += ek;
-      sfg[i] = fma(ef, f - g, sfg[i]);
+      const double e = exp(fcb[(size_t)(rb + i) * L + s] - mf[i]);
+      zf[i] += e;
+      if (!int2_token(s, tr4[i], c.sink, c.recent)) zw[i] += e;
     }
-  double kl[4];
+  double lse[4], lw[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     zf[i] = wave_sum(zf[i]);
-    zk[i] = wave_sum(zk[i]);
-    sfg[i] = wave_sum(sfg[i]);
-    kl[i] = sfg[i] / zf[i] - ((mf[i] + log(zf[i])) - (mk[i] + log(zk[i])));
-    zf[i] = 1.0 / zf[i];  // from here on the reciprocals
-    zk[i] = 1.0 / zk[i];
+    zw[i] = wave_sum(zw[i]);
+    lse[i] = mf[i] + log(zf[i]);
+    lw[i] = zw[i] > 0.0 ? mf[i] + log(zw[i]) : -INFINITY;
   }
-  // probabilities by 256-token chunk (four tokens per lane); dO = sum_s (p^K - p) v_s accumulates
-  // from the chunk's differences staged in LDS (p and p^K are 0 past a row's position)
+  // p, and W~ from the window tokens' weights exp(f - LW) staged in LDS by 256-token chunk
   f64x4 acc[8];
 #pragma unroll
   for (int t = 0; t < 8; ++t) acc[t] = f64x4{0.0, 0.0, 0.0, 0.0};
-  for (int base = 0; base < L; base += kTileThreads) {
+  for (int base = 0; base <= tmax; base += kTileThreads) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int j = 64 * q + l, s = base + j;
       double d[4] = {0.0, 0.0, 0.0, 0.0};
-      if (s < L) {
+      if (s <= tmax) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          if (tr4[i] < 0) continue;  // a row past the tile
+          if (s > tr4[i]) continue;
           const size_t o = (size_t)(rb + i) * L + s;
-          double pv = 0.0, pk = 0.0;
-          if (s <= tr4[i]) {
-            pv = pfb[o] * zf[i];
-            pk = pdb[o] * zk[i];
-          }
-          pfb[o] = pv;
-          pdb[o] = probs_only ? (s <= tr4[i] && int2_token(s, tr4[i], c.sink, c.recent) ? pk : 0.0) : pk;
-          d[i] = pk - pv;
+          const double f = fcb[o];
+          pcb[o] = exp(f - lse[i]);
+          if (!int2_token(s, tr4[i], c.sink, c.recent)) d[i] = exp(f - lw[i]);  // lw finite: a window token
         }
       }
-      if (!probs_only) {
-        double2* dj = reinterpret_cast<double2*>(dl + j * kDlStride + rb);
-        dj[0] = make_double2(d[0], d[1]);
-        dj[1] = make_double2(d[2], d[3]);
-      }
+      double2* dj = reinterpret_cast<double2*>(dl + j * kDlStride + rb);
+      dj[0] = make_double2(d[0], d[1]);
+      dj[1] = make_double2(d[2], d[3]);
     }
-    if (probs_only || base > tmax) continue;  // uniform
     __syncthreads();
     const int end = min(kTileThreads, tmax + 1 - base);
     for (int k4 = 0; k4 < 64 && 64 * w + k4 < end; k4 += 4) {
@@ -479,16 +454,157 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_fwd_kernel(CalSet S, Cal
     }
     __syncthreads();
   }
-  if (probs_only) return;  // uniform
-  sum_waves_store(acc, dl, S.wrow + ((size_t)h * S.nrows + row0) * kD, nr);
+  sum_waves_store(acc, dl, S.wt + ((size_t)h * S.nrows + row0) * kD, nr);
   if (l == 0)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      if (rb + i < nr) S.lrow[(size_t)h * S.nrows + row0 + rb + i] = kl[i];
+      if (rb + i < nr) {
+        S.rc[((size_t)h * S.nrows + row0 + rb + i) * 2] = lse[i];
+        S.rc[((size_t)h * S.nrows + row0 + rb + i) * 2 + 1] = lw[i];
+      }
+}
+
+// Forward of the key objective on a tile, with the rotation-independent part from cal_const_kernel.
+// Logits g = q.x~/sqrt(d) on the tokens read from INT2 (elsewhere g = f); the softmax p^K over all
+// tokens, the window tokens entering as one term exp(LW - mk); KL(p || p^K) = sum_INT2 p (f - g) +
+// lse_k - lse_f into lrow (p sums to one); p^K on the INT2 tokens into pd (the rest of pd stays zero);
+// dO = sum_INT2 (p^K - p) v + (exp(LW - lse_k) - exp(LW - lse_f)) W~ into wrow and exp(LW - lse_k)
+// into erow. With probs_only: pd only. Block (tile, KV head); every pass covers only the tokens
+// s_lo .. s_hi some row of the tile reads from INT2.
+__global__ __launch_bounds__(kTileThreads) void cal_pos_fwd_kernel(CalSet S, CalCfg c, int probs_only) {
+  constexpr int R = kTileRows;
+  __shared__ double red4[4 * R];
+  __shared__ double dw[R];  // exp(LW - lse_k) - exp(LW - lse_f) per row
+  __shared__ __align__(16) double dl[kTileThreads * kDlStride];
+  const int h = blockIdx.y, tid = threadIdx.x, gq = c.gq;
+  const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
+  const int4 tile = S.tiles[blockIdx.x];
+  const CalSeq sq = S.seqs[tile.x];
+  const int row0 = tile.y, nr = tile.z, tf = tile.w, a0 = sq.start, L = sq.len;
+  const int tmax = tf + (nr - 1) / gq;
+  const int s_lo = c.sink, s_hi = tmax - c.recent;
+  const size_t pb = (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;  // row r at + r L
+  double* pdb = S.pd + pb;
+  const double *fcb = S.fc + pb, *pcb = S.pc + pb;
+  double qa[32];
+  rows_operand_bf16(S.q + ((size_t)(a0 + tf + li / gq) * c.Hq + h * gq + li % gq) * kD, li < nr, lk, qa);
+  // logits on the INT2 tokens: wave w takes the 16-token tiles w, w + 4, ... that meet s_lo .. s_hi;
+  // lane (li, lk) ends with rows lk + 4 v of token 16 tt + li
+  double m4k[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) m4k[v] = -INFINITY;
+  for (int tt = w; 16 * tt <= s_hi; tt += 4) {
+    if (16 * tt + 15 < s_lo) continue;  // uniform over the wave
+    const int s = 16 * tt + li;
+    const bool ok = s <= tmax;
+    const f64x4 ak = dot_tokens_f64(qa, S.xeff + hrow(S, ok ? a0 + s : a0, h), ok, lk);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int r = lk + 4 * v, tr = tf + r / gq;
+      if (r < nr && int2_token(s, tr, c.sink, c.recent)) {
+        const double g = ak[v] * kInvSqrtD;
+        pdb[(size_t)r * L + s] = g;
+        m4k[v] = fmax(m4k[v], g);
+      }
+    }
+  }
+  // softmax passes: wave w owns rows rb .. rb + 3 (rb = 4 w), lane l the tokens s_lo + l, + 64, ...
+  const int rb = 4 * w;
+  double mk[4];
+  rows_max(m4k, red4, mk);  // its barriers also make the logits visible to the whole block
+  int tr4[4];
+  double lsf[4], lw[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bool ok = rb + i < nr;
+    tr4[i] = ok ? tf + (rb + i) / gq : -1;
+    const size_t ro = ((size_t)h * S.nrows + row0 + (ok ? rb + i : 0)) * 2;
+    lsf[i] = S.rc[ro];
+    lw[i] = S.rc[ro + 1];
+    mk[i] = fmax(mk[i], lw[i]);  // finite: a row has INT2 or window tokens
+  }
+  // e = exp(g - mk) in place of the logits, the row sums and sum_INT2 p (f - g)
+  double zk[4], klp[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) zk[i] = klp[i] = 0.0;
+  for (int s = s_lo + l; s <= s_hi; s += 64)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (tr4[i] < 0 || !int2_token(s, tr4[i], c.sink, c.recent)) continue;
+      const size_t o = (size_t)(rb + i) * L + s;
+      const double g = pdb[o], e = exp(g - mk[i]);
+      pdb[o] = e;  // this lane's own elements
+      zk[i] += e;
+      klp[i] = fma(pcb[o], fcb[o] - g, klp[i]);
+    }
+  double kl[4], er[4], rden[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    zk[i] = wave_sum(zk[i]);
+    klp[i] = wave_sum(klp[i]);
+    const bool win = lw[i] != -INFINITY;
+    const double den = zk[i] + (win ? exp(lw[i] - mk[i]) : 0.0);
+    const double lsk = mk[i] + log(den);
+    kl[i] = klp[i] + (lsk - lsf[i]);
+    er[i] = win ? exp(lw[i] - lsk) : 0.0;
+    if (l == 0 && rb + i < nr) dw[rb + i] = er[i] - (win ? exp(lw[i] - lsf[i]) : 0.0);
+    rden[i] = 1.0 / den;
+  }
+  // p^K = e / den on the INT2 tokens by 256-token chunk (four tokens per lane); dO over them from the
+  // differences p^K - p staged in LDS
+  f64x4 acc[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = f64x4{0.0, 0.0, 0.0, 0.0};
+  for (int base = s_lo; base <= s_hi; base += kTileThreads) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = 64 * q + l, s = base + j;
+      double d[4] = {0.0, 0.0, 0.0, 0.0};
+      if (s <= s_hi) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (tr4[i] < 0 || !int2_token(s, tr4[i], c.sink, c.recent)) continue;
+          const size_t o = (size_t)(rb + i) * L + s;
+          const double pk = pdb[o] * rden[i];
+          pdb[o] = pk;
+          d[i] = pk - pcb[o];
+        }
+      }
+      if (!probs_only) {
+        double2* dj = reinterpret_cast<double2*>(dl + j * kDlStride + rb);
+        dj[0] = make_double2(d[0], d[1]);
+        dj[1] = make_double2(d[2], d[3]);
+      }
+    }
+    if (probs_only) continue;  // uniform
+    __syncthreads();
+    const int end = min(kTileThreads, s_hi + 1 - base);
+    for (int k4 = 0; k4 < 64 && 64 * w + k4 < end; k4 += 4) {
+      const int j = 64 * w + k4 + lk;
+      const bool ok = j < end;
+      double y[8];
+      bf16x8_to_f64(ok ? *reinterpret_cast<const uint4*>(S.v + ((size_t)(a0 + base + j) * c.H + h) * kD + 8 * li)
+                       : make_uint4(0, 0, 0, 0),
+                    y);
+      acc_channels(acc, ok ? dl[j * kDlStride + li] : 0.0, y);
+    }
+    __syncthreads();
+  }
+  if (probs_only) return;  // uniform
+  sum_waves_store(acc, dl, S.wrow + ((size_t)h * S.nrows + row0) * kD, nr, S.wt + ((size_t)h * S.nrows + row0) * kD,
+                  dw);  // + dw W~ per row
+  if (l == 0)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (rb + i < nr) {
+        S.lrow[(size_t)h * S.nrows + row0 + rb + i] = kl[i];
+        S.erow[(size_t)h * S.nrows + row0 + rb + i] = er[i];
+      }
 }
 
 // Value objective on a tile: dO_V = sum_s p^K-hat_s (v~_s - v_s) into wrow (pd holds p^K-hat on the
-// tokens read from INT2, 0 elsewhere). Block (tile, KV head); pd is staged through LDS by token chunk.
+// tokens read from INT2, 0 elsewhere). Block (tile, KV head); pd is staged through LDS by token chunk
+// over the tokens s_lo .. s_hi some row of the tile reads from INT2.
 __global__ __launch_bounds__(kTileThreads) void cal_pos_val_kernel(CalSet S, CalCfg c) {
   constexpr int R = kTileRows;
   __shared__ __align__(16) double dl[kTileThreads * kDlStride];
@@ -498,12 +614,13 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_val_kernel(CalSet S, Cal
   const CalSeq sq = S.seqs[tile.x];
   const int row0 = tile.y, nr = tile.z, tf = tile.w, a0 = sq.start, L = sq.len;
   const int tmax = tf + (nr - 1) / gq;
+  const int s_lo = c.sink, s_hi = tmax - c.recent;
   const double* pdb = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
   f64x4 acc[8];
 #pragma unroll
   for (int t = 0; t < 8; ++t) acc[t] = f64x4{0.0, 0.0, 0.0, 0.0};
-  for (int base = 0; base <= tmax; base += kTileThreads) {
-    const int end = min(kTileThreads, tmax + 1 - base);
+  for (int base = s_lo; base <= s_hi; base += kTileThreads) {
+    const int end = min(kTileThreads, s_hi + 1 - base);
     for (int e = tid; e < R * kTileThreads; e += kTileThreads) {
       const int r = e / kTileThreads, j = e % kTileThreads;
       dl[j * kDlStride + r] = r < nr && j < end ? pdb[(size_t)r * L + base + j] : 0.0;
@@ -575,45 +692,65 @@ __global__ __launch_bounds__(256) void cal_u_kernel(CalSet S, CalCfg c, int valu
   }
 }
 
-// Logit gradients of the key objective on a tile: g_s = 2 u . v_s / d_model, gbar = sum_s p^K_s g_s,
-// pd = ((p^K - p) + lambda p^K (g - gbar)) / rows on the tokens read from INT2, 0 elsewhere.
-// Block (tile, KV head); u . v_s on the fp64 matrix cores (16-token tiles per wave), then one thread
-// per token.
+// Logit gradients of the key objective on a tile: G_s = 2 u . v_s / d_model, gbar = sum over all tokens of
+// p^K_s G_s (the window tokens as exp(LW - lse_k) 2 u . W~ / d_model), and on the tokens read from INT2
+// pd = ((p^K - p) + lambda p^K (G - gbar)) / rows (zero elsewhere, untouched). Block (tile, KV head);
+// u . v_s on the fp64 matrix cores (16-token tiles per wave) over the INT2 span s_lo .. s_hi only.
 __global__ __launch_bounds__(kTileThreads) void cal_pos_grad_kernel(CalSet S, CalCfg c) {
   constexpr int R = kTileRows;
   __shared__ double red[16 * R];
+  __shared__ double gbw[R];  // window part of gbar per row
   const int h = blockIdx.y, tid = threadIdx.x, gq = c.gq;
   const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
   const int4 tile = S.tiles[blockIdx.x];
   const CalSeq sq = S.seqs[tile.x];
   const int row0 = tile.y, nr = tile.z, tf = tile.w, a0 = sq.start, L = sq.len;
   const int tmax = tf + (nr - 1) / gq;
-  double* pdb = S.pd + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
-  double* pfb = S.pf + (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
+  const int s_lo = c.sink, s_hi = tmax - c.recent;
+  const size_t pb = (size_t)h * S.pelems + sq.p0 + (size_t)(row0 - sq.row0) * L;
+  double* pdb = S.pd + pb;
+  double* pfb = S.pf + pb;
+  const double* pcb = S.pc + pb;
+  const double* urw = S.urow + ((size_t)h * S.nrows + row0) * kD;
+  const double two_dm = 2.0 / (double)c.dm;
+  {
+    // u . W~ for row tid / 16, eight channels per lane, reduced over the row's 16 lanes
+    const int r = tid >> 4, c8 = 8 * (tid & 15);
+    double d = 0.0;
+    if (r < nr) {
+      const double* wtr = S.wt + ((size_t)h * S.nrows + row0 + r) * kD + c8;
+#pragma unroll
+      for (int m = 0; m < 8; ++m) d = fma(urw[(size_t)r * kD + c8 + m], wtr[m], d);
+    }
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) d += __shfl_xor(d, off);
+    if ((tid & 15) == 0) gbw[r] = r < nr ? S.erow[(size_t)h * S.nrows + row0 + r] * two_dm * d : 0.0;
+  }
   double ua[32];
   {
     const bool ok = li < nr;
-    const double* ur = S.urow + ((size_t)h * S.nrows + row0 + (ok ? li : 0)) * kD + 32 * lk;
+    const double* ur = urw + (size_t)(ok ? li : 0) * kD + 32 * lk;
 #pragma unroll
     for (int m = 0; m < 32; ++m) ua[m] = ok ? ur[m] : 0.0;
   }
-  const double two_dm = 2.0 / (double)c.dm;
   double gb4[4] = {0.0, 0.0, 0.0, 0.0};
-  for (int tt = w; 16 * tt <= tmax; tt += 4) {
+  for (int tt = w; 16 * tt <= s_hi; tt += 4) {
+    if (16 * tt + 15 < s_lo) continue;  // uniform over the wave
     const int s = 16 * tt + li;
     const bool ok = s <= tmax;
-    const f64x4 g = dot_tokens_bf16(ua, S.v + ((size_t)(a0 + s) * c.H + h) * kD, ok, lk);
+    const f64x4 g = dot_tokens_bf16(ua, S.v + ((size_t)(a0 + (ok ? s : 0)) * c.H + h) * kD, ok, lk);
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int r = lk + 4 * v;
-      if (r < nr && s <= tf + r / gq) {
-        const double pk = pdb[(size_t)r * L + s], gs = two_dm * g[v];
-        gb4[v] += pk * gs;
-        pfb[(size_t)r * L + s] = (pk - pfb[(size_t)r * L + s]) + c.lam * pk * gs;
+      if (r < nr && int2_token(s, tf + r / gq, c.sink, c.recent)) {
+        const size_t o = (size_t)r * L + s;
+        const double pk = pdb[o], gs = two_dm * g[v];
+        gb4[v] = fma(pk, gs, gb4[v]);
+        pfb[o] = (pk - pcb[o]) + c.lam * pk * gs;
       }
     }
   }
-  // gbar per row: over the 16 lanes of each lk group, then the four waves (fixed order)
+  // gbar per row: over the 16 lanes of each lk group, then the four waves (fixed order), then the window
 #pragma unroll
   for (int v = 0; v < 4; ++v)
 #pragma unroll
@@ -621,19 +758,17 @@ __global__ __launch_bounds__(kTileThreads) void cal_pos_grad_kernel(CalSet S, Ca
   if (li == 0)
 #pragma unroll
     for (int v = 0; v < 4; ++v) red[w * 16 + lk + 4 * v] = gb4[v];
-  __syncthreads();  // also makes the pf updates visible to the whole block
+  __syncthreads();  // also makes the pf updates and gbw visible to the whole block
   double gb[R];
 #pragma unroll
-  for (int r = 0; r < R; ++r) gb[r] = (red[r] + red[32 + r]) + (red[16 + r] + red[48 + r]);
+  for (int r = 0; r < R; ++r) gb[r] = ((red[r] + red[32 + r]) + (red[16 + r] + red[48 + r])) + gbw[r];
   const double inv_rows = 1.0 / (double)S.nrows;
-  for (int s = tid; s < L; s += kTileThreads) {
+  for (int s = s_lo + tid; s <= s_hi; s += kTileThreads) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      if (r >= nr) continue;
-      const int tr = tf + r / gq;
-      const bool q2 = s <= tr && int2_token(s, tr, c.sink, c.recent);
-      const double pk = pdb[(size_t)r * L + s];
-      pdb[(size_t)r * L + s] = q2 ? (pfb[(size_t)r * L + s] - c.lam * pk * gb[r]) * inv_rows : 0.0;
+      if (r >= nr || !int2_token(s, tf + r / gq, c.sink, c.recent)) continue;
+      const size_t o = (size_t)r * L + s;
+      pdb[o] = (pfb[o] - c.lam * pdb[o] * gb[r]) * inv_rows;
     }
   }
 }
@@ -1141,8 +1276,8 @@ size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 size_t cal_set_bytes(int T, int nseq, int nrows, long long pelems, int H) {
   const size_t rows = (size_t)T * H * kD;
   return up256(sizeof(CalSeq) * (size_t)nseq) + up256(sizeof(int4) * (size_t)nrows) + up256(sizeof(int) * (size_t)nrows) + 4 * up256(rows * 8) +
-         up256(rows) + 2 * up256((size_t)H * pelems * 8) + 2 * up256((size_t)H * nrows * kD * 8) +
-         up256((size_t)H * nrows * 8);
+         up256(rows) + 4 * up256((size_t)H * pelems * 8) + 3 * up256((size_t)H * nrows * kD * 8) +
+         up256((size_t)H * nrows * 16) + 2 * up256((size_t)H * nrows * 8);
 }
 
 size_t cal_shared_bytes(int H, int Hq) {
@@ -1209,6 +1344,16 @@ hipError_t cal_bind_set(CalSet& set, uint8_t* base, const uint16_t* k, const uin
   p += up256((size_t)H * pel * 8);
   set.pf = reinterpret_cast<double*>(p);
   p += up256((size_t)H * pel * 8);
+  set.fc = reinterpret_cast<double*>(p);
+  p += up256((size_t)H * pel * 8);
+  set.pc = reinterpret_cast<double*>(p);
+  p += up256((size_t)H * pel * 8);
+  set.rc = reinterpret_cast<double*>(p);
+  p += up256((size_t)H * rows * 16);
+  set.wt = reinterpret_cast<double*>(p);
+  p += up256((size_t)H * rows * kD * 8);
+  set.erow = reinterpret_cast<double*>(p);
+  p += up256((size_t)H * rows * 8);
   set.wrow = reinterpret_cast<double*>(p);
   p += up256((size_t)H * rows * kD * 8);
   set.urow = reinterpret_cast<double*>(p);
@@ -1269,6 +1414,14 @@ static void backward(const CalCfg& c, CalSet& set, const double* A, int value, d
 static void u_launch(const CalCfg& c, const CalSet& set, int value, hipStream_t s) {
   const int npos = set.nrows / c.gq;
   hipLaunchKernelGGL(cal_u_kernel, dim3(c.Hq, (npos + kUTile - 1) / kUTile), dim3(256), 0, s, set, c, value);
+}
+
+hipError_t cal_prepare_set(const CalCfg& c, CalSet& set, hipStream_t s) {
+  if (set.nrows == 0) return hipSuccess;
+  const size_t n = (size_t)c.H * set.pelems;
+  hipLaunchKernelGGL(cal_fill_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, set.pd, n, 0.0);
+  CAL_POS_LAUNCH(cal_const_kernel, set, c);
+  return hipGetLastError();
 }
 
 hipError_t cal_key_loss(const CalCfg& c, CalSet& set, const double* A, double* loss, double* grad, hipStream_t s) {
