@@ -300,10 +300,13 @@ __device__ __forceinline__ PageEnt load_ent(ent_ptr p, int i) {
 // 32..63 reading 4 bytes of page 0 and page 1.
 template <int NG>
 __device__ __forceinline__ void dma_pair(uint32_t a_lo, uint32_t a_hi, uint32_t b_lo, uint32_t b_hi, uint32_t lds_addr,
-                                         uint32_t voff16, uint64_t moff_head, bool upper) {
+                                         uint32_t voff16, uint64_t moff_head, uint64_t upper_mask) {
   const uint8_t* ra = reinterpret_cast<const uint8_t*>(((uint64_t)a_hi << 32) | a_lo);
   const uint8_t* rb = reinterpret_cast<const uint8_t*>(((uint64_t)b_hi << 32) | b_lo);
-  const uint64_t maddr = ((uint64_t)(upper ? b_hi : a_hi) << 32 | (upper ? b_lo : a_lo)) + moff_head;
+  // lanes 32..63 address page b: a + ((b - a) & mask) with the wave-uniform difference formed on the
+  // scalar unit and a loop-invariant per-lane mask (two ANDs and two adds on the vector unit)
+  const uint64_t a64 = ((uint64_t)a_hi << 32) | a_lo, d64 = (((uint64_t)b_hi << 32) | b_lo) - a64;
+  const uint64_t maddr = a64 + ((d64 & upper_mask) + moff_head);
   if constexpr (NG == 4) {
     asm volatile(
         "s_mov_b32 m0, %0\n\t"
@@ -341,12 +344,24 @@ __device__ __forceinline__ void dma_pair(uint32_t a_lo, uint32_t a_hi, uint32_t 
 // wait for those loads too, since scalar loads return out of order).
 template <bool WIDE>
 __device__ __forceinline__ void pin_pair(PairLoads<WIDE>& p) {
+  typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+  typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
-    asm volatile("" : "+v"(p.kc[P].x), "+v"(p.kc[P].y), "+v"(p.vc[P].x), "+v"(p.vc[P].y));
-    asm volatile("" : "+v"(p.km[P].x), "+v"(p.km[P].y), "+v"(p.km[P].z), "+v"(p.km[P].w));
-    asm volatile("" : "+v"(p.vs[P][0].x), "+v"(p.vs[P][0].y), "+v"(p.vz[P].x), "+v"(p.vz[P].y));
-    if constexpr (WIDE) asm volatile("" : "+v"(p.vs[P][1].x), "+v"(p.vs[P][1].y));
+    u2v kc = __builtin_bit_cast(u2v, p.kc[P]), vc = __builtin_bit_cast(u2v, p.vc[P]);
+    u4v km = __builtin_bit_cast(u4v, p.km[P]);
+    u2v vs0 = __builtin_bit_cast(u2v, p.vs[P][0]), vz = __builtin_bit_cast(u2v, p.vz[P]);
+    asm volatile("" : "+v"(kc), "+v"(vc), "+v"(km), "+v"(vs0), "+v"(vz));
+    p.kc[P] = __builtin_bit_cast(uint2, kc);
+    p.vc[P] = __builtin_bit_cast(uint2, vc);
+    p.km[P] = __builtin_bit_cast(uint4, km);
+    p.vs[P][0] = __builtin_bit_cast(uint2, vs0);
+    p.vz[P] = __builtin_bit_cast(uint2, vz);
+    if constexpr (WIDE) {
+      u2v vs1 = __builtin_bit_cast(u2v, p.vs[P][1]);
+      asm volatile("" : "+v"(vs1));
+      p.vs[P][1] = __builtin_bit_cast(uint2, vs1);
+    }
   }
 }
 // With one group per token (NG = 1) the token's single (s, z) is read into all four group slots:
@@ -465,15 +480,11 @@ __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoa
     }
   } else {
   // Zero term on the matrix cores: rows (j, 0) of zd = sum_g Q_jg z_tg, with z_tg exact in fp16 (the
-  // B operand: z_t0..z_t3 of token t twice, for the high and the low term of Q)
+  // B operand is the token's (s, z) pairs as loaded; the query operand is zero at the s positions)
   float4_t zd[2];
 #pragma unroll
-  for (int P = 0; P < 2; ++P) {
-    const uint32_t z01 = __builtin_amdgcn_perm(cur.km[P].y, cur.km[P].x, 0x07060302u);
-    const uint32_t z23 = __builtin_amdgcn_perm(cur.km[P].w, cur.km[P].z, 0x07060302u);
-    zd[P] = mfma16(st.Azq, __builtin_bit_cast(half8_t, u32x4_t{z01, z23, z01, z23}),
-                   float4_t{0.f, 0.f, 0.f, 0.f});
-  }
+  for (int P = 0; P < 2; ++P)
+    zd[P] = mfma16(st.Azq, __builtin_bit_cast(half8_t, cur.km[P]), float4_t{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
     const half2_t m[4] = {as_h2(cur.km[P].x), as_h2(cur.km[P].y), as_h2(cur.km[P].z), as_h2(cur.km[P].w)};
@@ -840,16 +851,20 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
     st.invsig[0] = cst[32 + hi];
   }
   {
-    // zero-term operand: lane l < 16 holds row m = l; the rows (j, 0) carry the group sums of q'_j
+    // zero-term operand against the token's metadata as it sits in registers (B rows k = 8 q + i:
+    // s_0, z_0, s_1, z_1, .., z_3 for every q): the rows (j, 0) carry the group sums of q'_j at the z
+    // positions, the high fp16 term in lanes 0..15 (k 1, 3, 5, 7), the low term in lanes 16..31
+    // (k 9, 11, 13, 15); every other entry zero
     const int m = l & 15, j = WIDE ? m >> 1 : m >> 2;
-    const bool zrow = l < 16 && (WIDE ? (m & 1) == 0 : (m & 3) == 0);
+    const bool zrow = l < 32 && (WIDE ? (m & 1) == 0 : (m & 3) == 0);
     const float4_t Q = *reinterpret_cast<const float4_t*>(cst + (WIDE ? 32 : 16) + 4 * j);
     half8_t z;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const _Float16 qh = (_Float16)Q[g];
-      z[g] = zrow ? qh : (_Float16)0.0f;
-      z[4 + g] = zrow ? (_Float16)(Q[g] - (float)qh) : (_Float16)0.0f;
+      const _Float16 term = l < 16 ? qh : (_Float16)(Q[g] - (float)qh);
+      z[2 * g] = (_Float16)0.0f;
+      z[2 * g + 1] = zrow ? term : (_Float16)0.0f;
     }
     st.Azq = z;
   }
@@ -872,7 +887,8 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
   const ent_ptr ent = (ent_ptr)(uintptr_t)(a.pages) + gs;
   const uint32_t voff16 = 16 * l + h * Rec<NG>::kBytes;
   const uint64_t moff = (uint64_t)(h * Rec<NG>::kBytes + 1024 + (NG == 4 ? 16 : 4) * (l & 31));
-  const bool upper = l >= 32;
+  uint64_t upper = l >= 32 ? ~0ull : 0ull;  // lanes reading page b's metadata
+  asm volatile("" : "+v"(upper));             // an opaque mask: ANDs, not selects
   const uint32_t pool_lo = (uint32_t)(uintptr_t)a.pool, pool_hi = (uint32_t)((uintptr_t)a.pool >> 32);
   uint32_t nv[kStages][2];  // cached tokens of the two pages staged in each slot
   // entries of pair k with the bounds check of the last pair (paths outside the steady loop): both
