@@ -267,7 +267,7 @@ struct PairLoads {
   uint4 km[2];  // K scale/zero of token lo, groups 0..3
   uint2 vc[2];  // V codes of half lo, tokens 4hi..4hi+3
   uint2 vs[2][WIDE ? 2 : 1];  // V scales, tokens 4hi..4hi+3: group lo&3 (narrow); lo&1, 2+(lo&1) (wide)
-  uint2 vz[2];  // V zeros of group lo&3, tokens 4hi..4hi+3
+  uint2 vz[2];  // (Z, l) operand rows: V zeros of group lo (lo < 4), 1.0 (lo 4..7), 0 (lo 8..15)
   uint32_t nv[2];  // wave-uniform: cached tokens of each page (16 for a full page)
 };
 
@@ -369,7 +369,7 @@ __device__ __forceinline__ void pin_pair(PairLoads<WIDE>& p) {
 // value weights of every group column use the token's one scale and zero.
 template <bool WIDE, int NG>
 __device__ __forceinline__ void read_pair(const uint8_t* slot, uint32_t nv0, uint32_t nv1, int lo, int hi,
-                                          PairLoads<WIDE>& p) {
+                                          const uint8_t* czb, PairLoads<WIDE>& p) {
   using L = Rec<NG>;
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
@@ -391,7 +391,9 @@ __device__ __forceinline__ void read_pair(const uint8_t* slot, uint32_t nv0, uin
     } else {
       p.vs[P][0] = *reinterpret_cast<const uint2*>(met + L::kOffVScale + gs * (lo & 3) + 8 * hi);
     }
-    p.vz[P] = *reinterpret_cast<const uint2*>(met + L::kOffVZero + gs * (lo & 3) + 8 * hi);
+    // lanes 0..3: the zeros of group lo; lanes 4..15 read the constant rows of the (Z, l) operand
+    const uint8_t* vzb = lo < 4 ? slot + 2048 - 1024 + L::kOffVZero + gs * (lo & 3) + 8 * hi : czb;
+    p.vz[P] = *reinterpret_cast<const uint2*>(vzb + P * 128 * NG);
   }
 }
 template <int X>
@@ -421,17 +423,18 @@ struct ScanState {
   float4_t cinit[NT];           // accumulator start of the score tiles (rows 4hi..4hi+3)
   half8_t Azq;                  // zero-term operand: row (j, 0) holds sum_{k in g} q'_jk, g = 0..3, as
                                 // two fp16 terms (k = 0..3 high, 4..7 low); every other entry zero
-  float invsig[NJ];
+  float invsig[NJ];              // 1 / sigma of query head jq(hi, u) (1 for absent heads)
+  float thr[NJ];                 // (mref + tau) sigma: the lazy-rescale threshold on the scaled logits
   float4_t acc[8];              // O' tiles: channels 16 mt + 4hi + r, column lo
   float4_t wsum[NT];            // sum_t w_t of each column (every row); wide: groups gg, 2 + gg
   float4_t zl;                  // rows 0..3: sum_t p_t z_tg (row = group); rows 4..7: sum_t p_t
   float mref[NJ];
-  float Qz[NJ];                 // sum_k q'_jk of query head jq(hi, u) (used with one group per token)
+  float Qz[NJ];                 // sigma sum_k q'_jk of query head jq(hi, u) (used with one group per token)
   LandK lk;                     // landing constants
 };
 
-// Scores of one page pair, base-2 logits, -inf where masked: a2[P][u] for token lo of page P and
-// query head jq(hi, u). The accumulation chains of both pages are issued interleaved so that each
+// Scores of one page pair, base-2 logits times sigma (the query operand's scale), -inf where masked:
+// a2[P][u] for token lo of page P and query head jq(hi, u). The accumulation chains of both pages are issued interleaved so that each
 // hides the others' latency.
 template <bool WIDE, int NG>
 __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoads<WIDE>& cur, int lo,
@@ -475,7 +478,7 @@ __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoa
 #pragma unroll
         for (int g = 0; g < 4; ++g) Dg[g] = WIDE ? d[P][g >> 1][2 * u + (g & 1)] : d[P][0][g];
         const float Ds = ((Dg[0] + Dg[1]) + Dg[2]) + Dg[3];
-        a2[P][u] = fmaf((float)m.x * Ds, st.invsig[u], (float)m.y * st.Qz[u]);
+        a2[P][u] = fmaf((float)m.x, Ds, (float)m.y * st.Qz[u]);
       }
     }
   } else {
@@ -495,11 +498,10 @@ __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoa
       float Dg[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) Dg[g] = WIDE ? d[P][g >> 1][2 * u + (g & 1)] : d[P][0][g];
-      float sd = fmaf((float)m[0].x, Dg[0], 0.0f);
+      float sd = fmaf((float)m[0].x, Dg[0], zd[P][WIDE ? 2 * u : 0]);
       sd = fmaf((float)m[1].x, Dg[1], sd);
       sd = fmaf((float)m[2].x, Dg[2], sd);
-      sd = fmaf((float)m[3].x, Dg[3], sd);
-      a2[P][u] = fmaf(sd, st.invsig[u], zd[P][WIDE ? 2 * u : 0]);
+      a2[P][u] = fmaf((float)m[3].x, Dg[3], sd);
     }
   }
   }
@@ -525,14 +527,15 @@ __device__ __forceinline__ void softmax_pair(ScanState<WIDE>& st, const float (&
 #pragma unroll
   for (int P = 0; P < 2; ++P)
 #pragma unroll
-    for (int u = 0; u < NJ; ++u) need |= a2[P][u] > st.mref[u] + kRescaleTau;
+    for (int u = 0; u < NJ; ++u) need |= a2[P][u] > st.thr[u];
   if (__any(need)) {
 #pragma unroll
     for (int u = 0; u < NJ; ++u) {
-      const float pm = row_max16(fmaxf(a2[0][u], a2[1][u]));
+      const float pm = row_max16(fmaxf(a2[0][u], a2[1][u])) * st.invsig[u];  // exact: a power of two
       const float mnew = pm > st.mref[u] + kRescaleTau ? pm : st.mref[u];
       const float al = __builtin_amdgcn_exp2f(st.mref[u] - mnew);
       st.mref[u] = mnew;
+      st.thr[u] = (mnew + kRescaleTau) / st.invsig[u];
       if (lo == 0) al_w[NJ * hi + u] = al;
     }
     lds_sync_wave();
@@ -548,7 +551,7 @@ __device__ __forceinline__ void softmax_pair(ScanState<WIDE>& st, const float (&
   for (int P = 0; P < 2; ++P) {
 #pragma unroll
     for (int u = 0; u < NJ; ++u) {
-      const float p = __builtin_amdgcn_exp2f(a2[P][u] - st.mref[u]);
+      const float p = __builtin_amdgcn_exp2f(fmaf(a2[P][u], st.invsig[u], -st.mref[u]));
       p_w[P][NJ * hi + u][lo] = (_Float16)p;
     }
   }
@@ -573,14 +576,9 @@ __device__ __forceinline__ void pv_pair(ScanState<WIDE>& st, const PairLoads<WID
   constexpr int NT = NG == 1 ? 1 : ScanState<WIDE>::NT;
   LandK lk = st.lk;
   if constexpr (big) lk.one = 0x5C005C00u;  // fp16 256.0, twice
-  // A operand of the (Z, l) contraction: rows 0..3 hold z of group `row` (the V zeros this lane
-  // already has, group lo & 3 = row), rows 4..7 hold 1.0, rows 8..15 zero
-  const half2_t zmul = lo < 4 ? half2_t{(_Float16)1.0f, (_Float16)1.0f} : half2_t{(_Float16)0.0f, (_Float16)0.0f};
-  const half2_t zadd = (lo >= 4 && lo < 8) ? half2_t{(_Float16)1.0f, (_Float16)1.0f}
-                                           : half2_t{(_Float16)0.0f, (_Float16)0.0f};
-  const half8_t Azl = __builtin_bit_cast(
-      half8_t, u32x4_t{as_u(as_h2(cur.vz[0].x) * zmul + zadd), as_u(as_h2(cur.vz[0].y) * zmul + zadd),
-                       as_u(as_h2(cur.vz[1].x) * zmul + zadd), as_u(as_h2(cur.vz[1].y) * zmul + zadd)});
+  // A operand of the (Z, l) contraction: rows 0..3 hold z of group `row`, rows 4..7 hold 1.0, rows
+  // 8..15 zero, all as read from LDS (see read_pair)
+  const half8_t Azl = __builtin_bit_cast(half8_t, u32x4_t{cur.vz[0].x, cur.vz[0].y, cur.vz[1].x, cur.vz[1].y});
   const half8_t Aones = __builtin_bit_cast(half8_t, u32x4_t{lk.one, lk.one, lk.one, lk.one});
   // column lo: query head jc, probabilities of tokens 4hi..4hi+3 of both pages
   const int jc = WIDE ? lo >> 1 : lo >> 2;
@@ -826,7 +824,7 @@ __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)
 template <bool WIDE, int NG, bool BIG>
 __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, int gs, int ge, int slot, int l,
                                              uint8_t* stage_w, _Float16 (*p_w)[2][8][kBlock], float* al_w,
-                                             bool all_waves) {
+                                             uint8_t* cz_w, bool all_waves) {
   constexpr int NJ = ScanState<WIDE>::NJ, NT = ScanState<WIDE>::NT;
   const int lo = l & 15, hi = l >> 4;
   const int n = ge - gs;             // pages
@@ -845,10 +843,10 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
     st.cinit[0] = *reinterpret_cast<const float4_t*>(cst + 4 * hi);       // D01 rows 4hi..4hi+3
     st.cinit[1] = *reinterpret_cast<const float4_t*>(cst + 16 + 4 * hi);  // D23 rows 4hi..4hi+3
 #pragma unroll
-    for (int u = 0; u < 2; ++u) st.invsig[u] = cst[64 + 2 * hi + u];
+    for (int u = 0; u < 2; ++u) st.invsig[u] = cst[64 + 2 * hi + u] > 0.0f ? cst[64 + 2 * hi + u] : 1.0f;
   } else {
     st.cinit[0] = *reinterpret_cast<const float4_t*>(cst + 4 * hi);
-    st.invsig[0] = cst[32 + hi];
+    st.invsig[0] = cst[32 + hi] > 0.0f ? cst[32 + hi] : 1.0f;
   }
   {
     // zero-term operand against the token's metadata as it sits in registers (B rows k = 8 q + i:
@@ -858,11 +856,13 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
     const int m = l & 15, j = WIDE ? m >> 1 : m >> 2;
     const bool zrow = l < 32 && (WIDE ? (m & 1) == 0 : (m & 3) == 0);
     const float4_t Q = *reinterpret_cast<const float4_t*>(cst + (WIDE ? 32 : 16) + 4 * j);
+    const float isj = cst[(WIDE ? 64 : 32) + j], sg = isj > 0.0f ? 1.0f / isj : 1.0f;  // sigma: a power of two
     half8_t z;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const _Float16 qh = (_Float16)Q[g];
-      const _Float16 term = l < 16 ? qh : (_Float16)(Q[g] - (float)qh);
+      const float qs = Q[g] * sg;
+      const _Float16 qh = (_Float16)qs;
+      const _Float16 term = l < 16 ? qh : (_Float16)(qs - (float)qh);
       z[2 * g] = (_Float16)0.0f;
       z[2 * g + 1] = zrow ? term : (_Float16)0.0f;
     }
@@ -874,13 +874,22 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
   for (int t = 0; t < NT; ++t) st.wsum[t] = float4_t{0.f, 0.f, 0.f, 0.f};
   st.zl = float4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int u = 0; u < NJ; ++u) st.mref[u] = kMaxInit;
+  for (int u = 0; u < NJ; ++u) {
+    st.mref[u] = kMaxInit;
+    st.thr[u] = (kMaxInit + kRescaleTau) / st.invsig[u];  // -inf or below every real scaled score
+  }
 #pragma unroll
   for (int u = 0; u < NJ; ++u) {  // q' sums of the lane's score heads (rows of absent heads are zero)
     const float4_t Q = *reinterpret_cast<const float4_t*>(cst + (WIDE ? 32 : 16) + 4 * (NJ * hi + u));
-    st.Qz[u] = ((Q[0] + Q[1]) + Q[2]) + Q[3];
+    st.Qz[u] = (((Q[0] + Q[1]) + Q[2]) + Q[3]) / st.invsig[u];
   }
   st.lk = land_constants();
+  // the wave's constant rows of the (Z, l) operand, at both page offsets: fp16 1.0 x 4, then 0 x 4
+  if (l < 4)
+    *reinterpret_cast<uint2*>(cz_w + (l >> 1) * 128 * NG + 8 * (l & 1)) =
+        (l & 1) ? make_uint2(0u, 0u) : make_uint2(0x3C003C00u, 0x3C003C00u);
+  lds_sync_wave();
+  const uint8_t* czb = cz_w + (lo < 8 ? 0 : 8);
 
   // ---- pipeline over the segment's page pairs (global pages gs + 2k, gs + 2k + 1; the second page
   // of a last pair of one page is a stand-in: block 0, no tokens). Pair k sits in slot k % kStages.
@@ -933,7 +942,7 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kDmaPerPair * (kStages - 1)) : "memory");
     else
       wait_vm_all();
-    read_pair<WIDE, NG>(stage_w, nv[0][0], nv[0][1], lo, hi, X);
+    read_pair<WIDE, NG>(stage_w, nv[0][0], nv[0][1], lo, hi, czb, X);
     pin_pair(X);
     if (kStages < npairs) {
       PageEnt e0, e1;
@@ -959,7 +968,7 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
         asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kDmaPerPair * (kStages - 1)) : "memory");
       else
         wait_vm_all();
-      read_pair<WIDE, NG>(stage_w + SL * 2 * kRecord, nv[SL][0], nv[SL][1], lo, hi, nxt);
+      read_pair<WIDE, NG>(stage_w + SL * 2 * kRecord, nv[SL][0], nv[SL][1], lo, hi, czb, nxt);
       pin_pair(nxt);
       if (STEADY) {
         // The entries read one step ago are pinned (their wait placed) before the next loads issue:
@@ -1086,6 +1095,7 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
   __shared__ __attribute__((aligned(16))) uint8_t stage[kWavesPerWG][kStages][2][kRecord];
   __shared__ _Float16 p_lds[kWavesPerWG][2][2][8][kBlock];
   __shared__ float al_lds[kWavesPerWG][8];
+  __shared__ __attribute__((aligned(16))) uint8_t cz_lds[kWavesPerWG][128 * NG + 16];
 
   // Work-groups are dispatched round-robin over the 8 XCDs (each with its own L2). Range g goes to
   // the work-group dispatched as blockIdx.x with g = (x % 8) (G / 8) + x / 8, so that each XCD scans
@@ -1111,8 +1121,9 @@ __global__ __launch_bounds__(512, 1) void decode_scan_flat_kernel(DecodeArgs a) 
     // wave in the scaled form, without the steady loop's work-group barriers: every wave still
     // executes the same number of barriers, so the others only wait for it at their next one
     if (!scan_segment<WIDE, NG, false>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w],
-                                       all_waves))
-      scan_segment<WIDE, NG, true>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w], false);
+                                       cz_lds[w], all_waves))
+      scan_segment<WIDE, NG, true>(a, b, h, pos, seg_end, g + b, l, &stage[w][0][0][0], p_lds[w], al_lds[w],
+                                   cz_lds[w], false);
     pos = seg_end;
     if (pos >= e) break;
     ++b;
