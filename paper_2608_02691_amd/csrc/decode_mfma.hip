@@ -89,33 +89,43 @@ __device__ __forceinline__ int seq_len_m(const DecodeArgs& a, int b) {
 
 // ---------------------------------------------------------------------------------------------
 // Query operands of one (sequence, KV head): q' = q R_K (fp32) scaled by log2(e)/sqrt(d) and a
-// per-head power of two sigma (max |q' sigma| in [256, 512)), laid out as the MFMA A operand of the
-// score contraction: a row holds q'_j on the channels of one group, times 2^e of the channel's
-// code position, as fp16 (row layouts: see the scan below). Constants: -sum_k A_k per row
-// (accumulator start), sum_{k in g} q'_jk (for the zero term) and 1/sigma.
-// One block serves KV head h of kQpSeqs sequences: R_K[h] goes once into LDS as the B operand of a
-// bf16 matrix-core product (split into two bf16 terms, as in the cache write: error below
-// 2^-17 |R|); the query rows are exact in bf16. Rows s * 8 + jj = query head jj of sequence
-// b0 + s (16-row tiles, wave w owns tile w).
+// per-head power of two sigma, laid out as the MFMA A operand of the score contraction: a row holds
+// q'_j on the channels of one group, times 2^e of the channel's code position, as fp16 (row layouts:
+// see the scan below). Constants: -sum_k A_k per row (accumulator start), sum_{k in g} q'_jk (for the
+// zero term) and 1/sigma. sigma comes from the row's norm, which bounds every |q'_c| (R_K orthogonal):
+// sigma |q'|_2 < 512, so every A value stays below 2^15 at the largest code factor 2^6.
+// One block serves KV head h of kQpSeqs sequences and 128 / SPLIT channels of q' (whole groups:
+// the operand block of group g and the group's constants only need its channels): those columns of
+// R_K[h] go into LDS as the B operand of a bf16 matrix-core product (split into two bf16 terms, as in
+// the cache write: error below 2^-17 |R|); the query rows are exact in bf16. Rows s * 8 + jj = query
+// head jj of sequence b0 + s (16-row tiles, wave w owns tile w).
 constexpr int kQpSeqs = 8;
-constexpr int kQpRow = 136;  // bf16 per LDS row of R^T (128 + 8 pad: conflict-free 16-byte reads)
+constexpr int kQpRow = 136;   // bf16 per LDS row of R^T (128 + 8 pad: conflict-free 16-byte reads)
 typedef __bf16 qp_bf16x8_t __attribute__((ext_vector_type(8)));
 
-// LDS of the query-operand role: R^T as bf16 hi / lo, the q' rows, per-row max and scale.
-constexpr int kQpLdsBytes = 2 * kHeadDim * kQpRow * 2 + 8 * kQpSeqs * (kHeadDim + 4) * 4 + 2 * 8 * kQpSeqs * 4;
+// LDS of the query-operand role with SPLIT blocks per (KV head, sequences): the block's columns of
+// R^T as bf16 hi / lo, its q' columns, the per-row scale (the largest size, SPLIT = 1).
+constexpr int qp_lds_bytes(int split) {
+  return 2 * (kHeadDim / split) * kQpRow * 2 + 8 * kQpSeqs * (kHeadDim / split + 4) * 4 + 8 * kQpSeqs * 4;
+}
+constexpr int kQpLdsBytes = qp_lds_bytes(1);
+static_assert(qp_lds_bytes(4) >= 512 * 4, "the page-prefix block's two 256-entry scans fit the query role's LDS");
 
+template <int SPLIT>
 __device__ void qprep_block(const DecodeArgs& a, int blk, bool wide, uint8_t* lds) {
-  uint16_t(*Rt)[kHeadDim][kQpRow] = reinterpret_cast<uint16_t(*)[kHeadDim][kQpRow]>(lds);  // [hi, lo][c][k] = R[k][c]
-  float(*qb)[kHeadDim + 4] = reinterpret_cast<float(*)[kHeadDim + 4]>(lds + 2 * kHeadDim * kQpRow * 2);  // q' rows
-  int* smax = reinterpret_cast<int*>(lds + 2 * kHeadDim * kQpRow * 2 + 8 * kQpSeqs * (kHeadDim + 4) * 4);
-  float* sig = reinterpret_cast<float*>(smax + 8 * kQpSeqs);
+  constexpr int kQpSplit = SPLIT, kQpCols = kHeadDim / SPLIT;
+  uint16_t(*Rt)[kQpCols][kQpRow] = reinterpret_cast<uint16_t(*)[kQpCols][kQpRow]>(lds);  // [hi, lo][c][k] = R[k][32 g + c]
+  float(*qb)[kQpCols + 4] = reinterpret_cast<float(*)[kQpCols + 4]>(lds + 2 * kQpCols * kQpRow * 2);  // q' rows
+  float* sig = reinterpret_cast<float*>(lds + 2 * kQpCols * kQpRow * 2 + 8 * kQpSeqs * (kQpCols + 4) * 4);
   const int H = a.H, gq = a.gq, tid = threadIdx.x;
-  const int h = blk % H, b0 = kQpSeqs * (blk / H), nseq = min(kQpSeqs, a.B - b0);
+  constexpr int kGpb = kQpCols / 32;  // groups per block
+  const int g0 = (blk % kQpSplit) * kGpb, hb = blk / kQpSplit;
+  const int h = hb % H, b0 = kQpSeqs * (hb / H), nseq = min(kQpSeqs, a.B - b0);
   const int w = tid >> 6, l = tid & 63, lo = l & 15, hi = l >> 4;
-  if (tid < 8 * kQpSeqs) smax[tid] = 0;
   // A operand (query rows 16 w + lo, 8 consecutive channels per lane), fetched before R so the
   // two latencies overlap; absent rows are zero
   qp_bf16x8_t A[4];
+  float ss = 0.0f;  // sum of squares of the lane's 32 channels
   {
     const int row = 16 * w + lo, sq = row >> 3, jj = row & 7;
     const bool ok = sq < nseq && jj < gq;
@@ -124,23 +134,29 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, bool wide, uint8_t* ld
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const uint4 v = *reinterpret_cast<const uint4*>(qr + 32 * ks);
-      A[ks] = __builtin_bit_cast(qp_bf16x8_t, make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep));
+      const uint32_t u[4] = {v.x & keep, v.y & keep, v.z & keep, v.w & keep};
+      A[ks] = __builtin_bit_cast(qp_bf16x8_t, make_uint4(u[0], u[1], u[2], u[3]));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x0 = __uint_as_float(u[e] << 16), x1 = __uint_as_float(u[e] & 0xFFFF0000u);
+        ss = fmaf(x0, x0, fmaf(x1, x1, ss));
+      }
     }
   }
   {
-    // R^T as bf16 hi/lo: thread (c, k0) reads R[k0 .. k0 + 7][c] (coalesced over c) and writes one
-    // 16-byte row piece per term
-    // (all 64 loads of a thread are issued before the first conversion: one round trip)
-    const float* R = a.R_k + (size_t)h * kHeadDim * kHeadDim;
-    const int c = tid & 127, kb = tid >> 7;
-    float rall[8][8];
+    // the block's columns of R as bf16 hi/lo rows of R^T: thread (c, kb) reads R[k0 .. k0 + 7][32 g0 + c]
+    // for k0 = 8 (kb + kKb u) (coalesced over c) and writes one 16-byte row piece per term
+    constexpr int kKb = 256 / kQpCols, kNu = 16 / kKb;
+    const float* R = a.R_k + (size_t)h * kHeadDim * kHeadDim + 32 * g0;
+    const int c = tid & (kQpCols - 1), kb = tid / kQpCols;
+    float rall[kNu][8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+    for (int u = 0; u < kNu; ++u)
 #pragma unroll
-      for (int q = 0; q < 8; ++q) rall[u][q] = R[(8 * (kb + 2 * u) + q) * kHeadDim + c];
+      for (int q = 0; q < 8; ++q) rall[u][q] = R[(8 * (kb + kKb * u) + q) * kHeadDim + c];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int k0 = 8 * (kb + 2 * u);
+    for (int u = 0; u < kNu; ++u) {
+      const int k0 = 8 * (kb + kKb * u);
       const float* r8 = rall[u];
       uint32_t hw[4], lw[4];
 #pragma unroll
@@ -154,10 +170,21 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, bool wide, uint8_t* ld
       *reinterpret_cast<uint4*>(&Rt[1][c][k0]) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
     }
   }
+  // sigma of row 16 w + lo from |q|_2 (the four lanes hi of the row hold its 128 channels):
+  // max_c |q'_c| <= log2(e)/sqrt(d) |q|_2 (with a 2^-10 margin for the rounding of the sum and of
+  // the product's terms), sigma = 2^(9 - ex) for that bound below 2^ex
+  ss += __shfl_xor(ss, 16);
+  ss += __shfl_xor(ss, 32);
+  if (hi == 0) {
+    const float m = sqrtf(ss) * (kLogit2 * (1.0f + 0x1p-10f));
+    int ex = 0;
+    frexpf(m, &ex);
+    sig[16 * w + lo] = m > 0.0f ? ldexpf(1.0f, max(-100, min(100, 9 - ex))) : 1.0f;
+  }
   __syncthreads();
   // D[row][c] of n-tile p sits in lane (c % 16) + 16 (row / 4), register row % 4
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
+  for (int p = 0; p < kQpCols / 16; ++p) {
     float4_t d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
@@ -170,38 +197,22 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, bool wide, uint8_t* ld
     for (int r = 0; r < 4; ++r) qb[16 * w + 4 * hi + r][16 * p + lo] = d[r] * kLogit2;
   }
   __syncthreads();
-  {
-    // per-row max |q'|: thread -> (row, 32-channel quarter), then a 4-way LDS max
-    const int row = tid >> 2, qt = tid & 3;
-    float m = 0.0f;
-#pragma unroll 8
-    for (int c = 0; c < 32; ++c) m = fmaxf(m, fabsf(qb[row][32 * qt + c]));
-    atomicMax(&smax[row], __float_as_int(m));  // non-negative floats order like their bits
-  }
-  __syncthreads();
-  if (tid < 8 * kQpSeqs) {
-    const float m = __int_as_float(smax[tid]);
-    int ex = 0;
-    frexpf(m, &ex);
-    sig[tid] = m > 0.0f ? ldexpf(1.0f, max(-100, min(100, 9 - ex))) : 1.0f;
-  }
-  __syncthreads();
-  // A operand chunks: (sequence, k block i, lane l) -> 8 fp16 values. Lane l = m + 16 q holds row
-  // m, which belongs to query head jj and is nonzero only in the blocks of its group slot: narrow
-  // rows (j, g) = 4 j + g in block g; wide rows (j, gg) = 2 j + gg in the blocks i with i % 2 = gg.
-  // Its eight values are channels 32 i + 4 q + 0..3 (code position x = 2 i) and
-  // 32 i + 16 + 4 q + 0..3 (x = 2 i + 1), scaled by sigma and 2^e(x).
-  for (int cidx = tid; cidx < nseq * 256; cidx += 256) {
-    const int sq = cidx >> 8, i = (cidx >> 6) & 3, l = cidx & 63;
+  // A operand chunks of the block's groups g: (sequence, g, lane l) -> 8 fp16 values. Lane l = m + 16 q
+  // holds row m, which belongs to query head jj and is nonzero only in the blocks of its group slot:
+  // narrow rows (j, g) = 4 j + g in block g; wide rows (j, gg) = 2 j + gg in the blocks i with
+  // i % 2 = gg. Its eight values are channels 32 g + 4 q + 0..3 (code position x = 2 g) and
+  // 32 g + 16 + 4 q + 0..3 (x = 2 g + 1), scaled by sigma and 2^e(x).
+  for (int cidx = tid; cidx < nseq * kGpb * 64; cidx += 256) {
+    const int sq = cidx / (kGpb * 64), gi = (cidx / 64) % kGpb, l = cidx & 63, g = g0 + gi;
     const int m = l & 15, q = l >> 4;
     const int jj = wide ? m >> 1 : m >> 2;
-    const bool on = wide ? (m & 1) == (i & 1) : (m & 3) == i;
+    const bool on = wide ? (m & 1) == (g & 1) : (m & 3) == g;
     const int row = 8 * sq + jj;
     uint32_t packed[4] = {0u, 0u, 0u, 0u};
     if (on && jj < gq) {
-      const float4 lo4 = *reinterpret_cast<const float4*>(&qb[row][32 * i + 4 * q]);
-      const float4 hi4 = *reinterpret_cast<const float4*>(&qb[row][32 * i + 16 + 4 * q]);
-      const float s0 = sig[row] * (float)(1 << land_e(2 * i)), s1 = sig[row] * (float)(1 << land_e(2 * i + 1));
+      const float4 lo4 = *reinterpret_cast<const float4*>(&qb[row][32 * gi + 4 * q]);
+      const float4 hi4 = *reinterpret_cast<const float4*>(&qb[row][32 * gi + 16 + 4 * q]);
+      const float s0 = sig[row] * (float)(1 << land_e(2 * g)), s1 = sig[row] * (float)(1 << land_e(2 * g + 1));
       const float v[8] = {lo4.x * s0, lo4.y * s0, lo4.z * s0, lo4.w * s0, hi4.x * s1, hi4.y * s1, hi4.z * s1, hi4.w * s1};
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -210,22 +221,22 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, bool wide, uint8_t* ld
       }
     }
     uint8_t* out = a.qop + ((size_t)(b0 + sq) * H + h) * kQopTile;
-    *reinterpret_cast<uint4*>(out + (i * 64 + l) * 16) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+    *reinterpret_cast<uint4*>(out + (g * 64 + l) * 16) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
   }
   // Per (query head jj, group g): -sum of the row's 32 fp16 A values in block g (the accumulator
-  // start of that row's tile), sum of q' over group g, and 1/sigma; thread -> (row, g), a
+  // start of that row's tile), sum of q' over group g, and 1/sigma (group 0); thread -> (row, g), a
   // sequential sum over the group's channels. Narrow layout after the 4096 bytes of A operands:
   // start[4 jj + g], qsum[16 + 4 jj + g], 1/sigma[32 + jj]; wide: start of D01 [2 jj + g] (g < 2)
   // and of D23 [16 + 2 jj + g - 2] (g >= 2), qsum[32 + 4 jj + g], 1/sigma[64 + jj] (floats).
-  {
-    const int row = tid >> 2, g = tid & 3, sq = row >> 3, jj = row & 7;
+  if (tid < 8 * kQpSeqs * kGpb) {
+    const int row = tid % (8 * kQpSeqs), gi = tid / (8 * kQpSeqs), g = g0 + gi, sq = row >> 3, jj = row & 7;
     if (sq < nseq && jj < (wide ? 8 : 4)) {
       float csum = 0.0f, qsum = 0.0f;
       if (jj < gq) {
         const float s0 = sig[row] * (float)(1 << land_e(2 * g)), s1 = sig[row] * (float)(1 << land_e(2 * g + 1));
 #pragma unroll
         for (int c4 = 0; c4 < 8; ++c4) {
-          const float4 v = *reinterpret_cast<const float4*>(&qb[row][32 * g + 4 * c4]);
+          const float4 v = *reinterpret_cast<const float4*>(&qb[row][32 * gi + 4 * c4]);
           const float sc = c4 < 4 ? s0 : s1;  // channels 32 g + 0..15 sit at code position 2 g
           csum += (float)(_Float16)(v.x * sc) + (float)(_Float16)(v.y * sc) + (float)(_Float16)(v.z * sc) +
                   (float)(_Float16)(v.w * sc);
@@ -751,6 +762,7 @@ __device__ void page_prefix_block(const DecodeArgs& a, uint8_t* lds) {
 // computes). Entry: address of the record of KV head 0, cached tokens of the page (0, with the
 // address of block 0, for a block id outside the pool).
 constexpr int kPlPages = 1024;
+static_assert(kPlPages == 4 * 256, "page_list_block writes four entries per thread of its 256");
 
 __device__ void page_list_block(const DecodeArgs& a, int b, int p0, uint8_t* lds) {
   int* red = reinterpret_cast<int*>(lds);
@@ -793,10 +805,17 @@ __device__ void page_list_block(const DecodeArgs& a, int b, int p0, uint8_t* lds
 // per sequence). Lower block ids are dispatched first. The roles share one LDS buffer.
 constexpr int kPrepLdsBytes = kAppendLdsBytes > kQpLdsBytes ? kAppendLdsBytes : kQpLdsBytes;
 
+// AP: the launch carries append blocks (their LDS sets the block's size; without them the roles
+// below fit several blocks per CU).
+// The query role runs as one block per (KV head, 8 sequences) beside append blocks (whose LDS allows
+// one block per CU: fewer blocks keep the launch in one round) and as four (one per 32-channel group
+// of q', shorter chains) otherwise.
+constexpr int qp_split(bool ap) { return ap ? 1 : 4; }
+template <bool AP>
 __global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int wide, int nq, int nseg, AppendArgs ap, int nap) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kPrepLdsBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[AP ? kPrepLdsBytes : qp_lds_bytes(qp_split(false))];
   int blk = blockIdx.x;
-  if (blk < nap) {
+  if (AP && blk < nap) {
     const int bx = blk % ap.nbx, r = blk / ap.nbx;
     if (ap.cv.groups == 1)
       append_block<1, 4, 1>(ap.cv, ap.k, ap.v, ap.slots, ap.n, ap.R_k, ap.R_v, ap.mu_rk, ap.clip_k, ap.clip_v, bx,
@@ -810,7 +829,7 @@ __global__ __launch_bounds__(256) void qprep_kernel(DecodeArgs a, int wide, int 
   if (blk == 0)
     page_prefix_block(a, lds);
   else if (blk <= nq)
-    qprep_block(a, blk - 1, wide != 0, lds);
+    qprep_block<qp_split(AP)>(a, blk - 1, wide != 0, lds);
   else
     page_list_block(a, (blk - 1 - nq) / nseg, ((blk - 1 - nq) % nseg) * kPlPages, lds);
 }
@@ -1403,12 +1422,16 @@ hipError_t launch_qprep(const DecodeArgs& a, const AppendArgs* ap, hipStream_t s
     none.nbx = (ap->n + 16 * 4 - 1) / (16 * 4);  // one 16-token tile per wave and step
     nap = none.nbx * ap->cv.num_kv_heads * 2;
   }
-  const int nq = a.H * ((a.B + kQpSeqs - 1) / kQpSeqs);
+  const int nq = a.H * ((a.B + kQpSeqs - 1) / kQpSeqs) * qp_split(nap > 0);
   const long long maxlen = min((long long)a.max_ctx, (long long)a.max_blocks * kBlock);
   const int maxp = (int)((maxlen + kBlock - 1) / kBlock);
   const int nseg = max(1, (maxp + kPlPages - 1) / kPlPages);
-  hipLaunchKernelGGL(qprep_kernel, dim3(nap + 1 + nq + a.B * nseg), dim3(256), 0, s, a, a.gq > 4 ? 1 : 0, nq, nseg,
-                     none, nap);
+  if (nap > 0)
+    hipLaunchKernelGGL(qprep_kernel<true>, dim3(nap + 1 + nq + a.B * nseg), dim3(256), 0, s, a, a.gq > 4 ? 1 : 0, nq,
+                       nseg, none, nap);
+  else
+    hipLaunchKernelGGL(qprep_kernel<false>, dim3(1 + nq + a.B * nseg), dim3(256), 0, s, a, a.gq > 4 ? 1 : 0, nq, nseg,
+                       none, 0);
   return hipGetLastError();
 }
 
