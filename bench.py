@@ -36,10 +36,27 @@ def log(msg):
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_source_hash():
+# the sources each measured kernel is built from (its file, the headers it includes, and the host
+# code that sizes its launch); counters stay valid while these files are unchanged
+_COMMON = ("common.h", "kernels.h", "api.hip")
+KERNEL_SOURCES = {
+    "decode_scan": ("decode_mfma.hip", "append_core.h") + _COMMON,
+    "qprep": ("decode_mfma.hip", "append_core.h") + _COMMON,
+    "merge": ("decode_mfma.hip", "append_core.h") + _COMMON,
+    "append": ("append.hip", "append_core.h") + _COMMON,
+    "wo": ("wo_gemm.hip",) + _COMMON,
+    "wo_reduce": ("wo_gemm.hip",) + _COMMON,
+    "outerr_scan": ("outerr.hip",) + _COMMON,
+}
+
+
+def kernel_source_hash(kernel_key=None):
+    """Hash of the kernel sources a counter entry was taken on (kernel_key such as "decode_scan_cfg4";
+    None: every source)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_02691_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    files = KERNEL_SOURCES.get(kernel_key.rsplit("_cfg", 1)[0]) if kernel_key else None
+    for name in sorted(files or os.listdir(csrc)):
         if name.endswith((".hip", ".h")):
             with open(os.path.join(csrc, name), "rb") as f:
                 h.update(name.encode() + f.read())
@@ -57,7 +74,7 @@ def committed_counters(kernel_key):
     with open(path) as f:
         data = json.load(f)
     entry = data.get(kernel_key)
-    if not entry or entry.get("source_hash") != kernel_source_hash():
+    if not entry or entry.get("source_hash") != kernel_source_hash(kernel_key):
         return None
     return entry
 
