@@ -71,7 +71,7 @@ __device__ __forceinline__ void oe_wave_sync() {
 // Block (chunk, KV head h, sequence b). Lane roles as in the vector-ALU decode scan: for the scores,
 // token tq = l / 4 of the page and 32-channel quarter gk = l % 4; for the values, channels 2l, 2l+1.
 template <int MAXG, int NG>
-__global__ __launch_bounds__(256) void outerr_scan_kernel(OutErrArgs e) {
+__global__ __launch_bounds__(256, MAXG <= 4 ? 4 : 1) void outerr_scan_kernel(OutErrArgs e) {
   using Lay = Rec<NG>;
   const DecodeArgs& a = e.a;
   __shared__ float qf[MAXG][kHeadDim];       // q (model basis), base-2 logit units
@@ -134,32 +134,55 @@ __global__ __launch_bounds__(256) void outerr_scan_kernel(OutErrArgs e) {
     const bool valid = pos >= t0 && pos < t1;
     const int posc = min(max(pos, t0), t1 - 1);  // a row inside the caller's store
 
-    // ---- INT2 scores: token tq, quarter gk (codes, then the affine metadata factored out)
+    // ---- INT2 and full-precision scores of token tq over the lane's channel quarter gk: half mm of the
+    // token's code words holds channels 32 gk + mm (bits 4 gk) and 32 gk + 16 + mm (bits 4 gk + 2); the
+    // codes and the raw key values are unpacked four halves at a time, each chunk feeding every head
     const uint4* kc = reinterpret_cast<const uint4*>(rec + kOffKCodes + 32 * tq);
     const uint4 k0 = kc[0], k1 = kc[1];
     const uint32_t kw[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
     const uint32_t meta =
         *reinterpret_cast<const uint32_t*>(rec + Lay::kOffKMeta + 4 * NG * tq + 4 * (NG == 4 ? gk : 0));
     const float ks = f16_bits_to_f32(meta & 0xFFFF), kz = f16_bits_to_f32(meta >> 16);
-    float codes[kGroup];
-#pragma unroll
-    for (int mm = 0; mm < 16; ++mm) {
-      const uint32_t half = (kw[mm >> 1] >> (16 * (mm & 1))) & 0xFFFF;
-      codes[mm] = static_cast<float>((half >> (4 * gk)) & 3);           // channel 16 (2 gk) + mm
-      codes[16 + mm] = static_cast<float>((half >> (4 * gk + 2)) & 3);  // channel 16 (2 gk + 1) + mm
-    }
-    // ---- full-precision scores: the token's raw key row, channels 32 gk .. 32 gk + 31
-    float kf[32];
+    uint32_t kraw[16];  // the token's raw key row, channels 32 gk .. 32 gk + 31 (two per word)
     {
       const uint4* kp = reinterpret_cast<const uint4*>(krow0 + (size_t)posc * row_stride + 32 * gk);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const uint4 x = kp[u];
-        const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
+        kraw[4 * u] = x.x;
+        kraw[4 * u + 1] = x.y;
+        kraw[4 * u + 2] = x.z;
+        kraw[4 * u + 3] = x.w;
+      }
+    }
+    auto kf = [&](int c) {  // raw key value of channel 32 gk + c
+      return __uint_as_float((c & 1) ? (kraw[c >> 1] & 0xFFFF0000u) : (kraw[c >> 1] << 16));
+    };
+    float d1[MAXG], d2[MAXG];
+#pragma unroll
+    for (int j = 0; j < MAXG; ++j) d1[j] = d2[j] = 0.0f;
+#pragma unroll
+    for (int mc = 0; mc < 16; mc += 4) {
+      float cl[4], chi[4], fl[4], fh[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int mm = mc + i;
+        const uint32_t half = (kw[mm >> 1] >> (16 * (mm & 1))) & 0xFFFF;
+        cl[i] = static_cast<float>((half >> (4 * gk)) & 3);       // channel 32 gk + mm
+        chi[i] = static_cast<float>((half >> (4 * gk + 2)) & 3);  // channel 32 gk + 16 + mm
+        fl[i] = kf(mm);
+        fh[i] = kf(16 + mm);
+      }
+#pragma unroll
+      for (int j = 0; j < MAXG; ++j) {
+        if (j >= gq) continue;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          kf[8 * u + 2 * i] = __uint_as_float(xs[i] << 16);
-          kf[8 * u + 2 * i + 1] = __uint_as_float(xs[i] & 0xFFFF0000u);
+          const int mm = mc + i;
+          d2[j] = fmaf(qr[j][32 * gk + mm], cl[i], d2[j]);
+          d2[j] = fmaf(qr[j][32 * gk + 16 + mm], chi[i], d2[j]);
+          d1[j] = fmaf(qf[j][32 * gk + mm], fl[i], d1[j]);
+          d1[j] = fmaf(qf[j][32 * gk + 16 + mm], fh[i], d1[j]);
         }
       }
     }
@@ -168,17 +191,9 @@ __global__ __launch_bounds__(256) void outerr_scan_kernel(OutErrArgs e) {
     for (int j = 0; j < MAXG; ++j) {
       al1[j] = al2[j] = 1.0f;
       if (j >= gq) continue;
-      float d2 = 0.0f, d1 = 0.0f;
-#pragma unroll
-      for (int mm = 0; mm < 16; ++mm) {
-        d2 = fmaf(qr[j][32 * gk + mm], codes[mm], d2);
-        d2 = fmaf(qr[j][32 * gk + 16 + mm], codes[16 + mm], d2);
-      }
-#pragma unroll
-      for (int c = 0; c < 32; ++c) d1 = fmaf(qf[j][32 * gk + c], kf[c], d1);
       // the token's scores: sums over its four quarter lanes (a DPP quad)
-      float s2 = quad_sum4(ks * d2 + kz * qsum[j][gk]);
-      float s1 = quad_sum4(d1);
+      float s2 = quad_sum4(ks * d2[j] + kz * qsum[j][gk]);
+      float s1 = quad_sum4(d1[j]);
       s1 = valid ? s1 : -INFINITY;
       s2 = valid ? s2 : -INFINITY;
       // page maxima: over the four tokens of each DPP row, then the rows
@@ -201,22 +216,11 @@ __global__ __launch_bounds__(256) void outerr_scan_kernel(OutErrArgs e) {
     }
     oe_wave_sync();
 
-    // ---- values of channels c0, c0 + 1: INT2 (R_V basis) and full precision (model basis)
-    const uint4* vc = reinterpret_cast<const uint4*>(rec + kOffVCodes + 32 * m0);
-    const uint4 va = vc[0], vb = vc[1], vc2 = vc[2], vd = vc[3];  // halves m0 (tokens 0..15), m0 + 1
-    const uint32_t hv0[8] = {va.x, va.y, va.z, va.w, vb.x, vb.y, vb.z, vb.w};
-    const uint32_t hv1[8] = {vc2.x, vc2.y, vc2.z, vc2.w, vd.x, vd.y, vd.z, vd.w};
+    // ---- values of channels c0, c0 + 1: INT2 (R_V basis) and full precision (model basis), in two
+    // halves of eight tokens (the loads of a half, then its arithmetic)
+    const uint4* vc = reinterpret_cast<const uint4*>(rec + kOffVCodes + 32 * m0);  // halves m0, m0 + 1
     const uint4* vsp = reinterpret_cast<const uint4*>(rec + Lay::kOffVScale + 32 * (NG == 4 ? gv : 0));
     const uint4* vzp = reinterpret_cast<const uint4*>(rec + Lay::kOffVZero + 32 * (NG == 4 ? gv : 0));
-    const uint4 s0 = vsp[0], s1 = vsp[1], z0 = vzp[0], z1 = vzp[1];
-    const uint32_t sw[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-    const uint32_t zw[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
-    uint32_t vf[kBlock];
-#pragma unroll
-    for (int t = 0; t < kBlock; ++t) {
-      const int pt = min(max(pg * kBlock + t, t0), t1 - 1);
-      vf[t] = *reinterpret_cast<const uint32_t*>(vrow0 + (size_t)pt * row_stride + c0);
-    }
 #pragma unroll
     for (int j = 0; j < MAXG; ++j) {
 #pragma unroll
@@ -227,23 +231,35 @@ __global__ __launch_bounds__(256) void outerr_scan_kernel(OutErrArgs e) {
       }
     }
 #pragma unroll
-    for (int t = 0; t < kBlock; ++t) {
-      const int sh = 16 * (t & 1);
-      const float vs = f16_bits_to_f32((sw[t >> 1] >> sh) & 0xFFFF);
-      const float vz = f16_bits_to_f32((zw[t >> 1] >> sh) & 0xFFFF);
-      const float x0 = fmaf(static_cast<float>((hv0[t >> 1] >> (sh + 2 * pv)) & 3), vs, vz);
-      const float x1 = fmaf(static_cast<float>((hv1[t >> 1] >> (sh + 2 * pv)) & 3), vs, vz);
-      const float r0 = __uint_as_float(vf[t] << 16), r1 = __uint_as_float(vf[t] & 0xFFFF0000u);
+    for (int H = 0; H < 2; ++H) {
+      const uint4 ca = vc[H], cb = vc[2 + H], s4 = vsp[H], z4 = vzp[H];  // tokens 8 H .. 8 H + 7
+      const uint32_t hv0[4] = {ca.x, ca.y, ca.z, ca.w}, hv1[4] = {cb.x, cb.y, cb.z, cb.w};
+      const uint32_t sw[4] = {s4.x, s4.y, s4.z, s4.w}, zw[4] = {z4.x, z4.y, z4.z, z4.w};
+      uint32_t vf[8];
 #pragma unroll
-      for (int j = 0; j < MAXG; ++j) {
-        if (j < gq) {
-          const float p1 = pb[w][0][t][j], p2 = pb[w][1][t][j];
-          o[0][j][0] = fmaf(p1, r0, o[0][j][0]);
-          o[0][j][1] = fmaf(p1, r1, o[0][j][1]);
-          o[1][j][0] = fmaf(p2, r0, o[1][j][0]);
-          o[1][j][1] = fmaf(p2, r1, o[1][j][1]);
-          o[2][j][0] = fmaf(p2, x0, o[2][j][0]);
-          o[2][j][1] = fmaf(p2, x1, o[2][j][1]);
+      for (int i = 0; i < 8; ++i) {
+        const int pt = min(max(pg * kBlock + 8 * H + i, t0), t1 - 1);
+        vf[i] = *reinterpret_cast<const uint32_t*>(vrow0 + (size_t)pt * row_stride + c0);
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int t = 8 * H + i, sh = 16 * (i & 1);
+        const float vs = f16_bits_to_f32((sw[i >> 1] >> sh) & 0xFFFF);
+        const float vz = f16_bits_to_f32((zw[i >> 1] >> sh) & 0xFFFF);
+        const float x0 = fmaf(static_cast<float>((hv0[i >> 1] >> (sh + 2 * pv)) & 3), vs, vz);
+        const float x1 = fmaf(static_cast<float>((hv1[i >> 1] >> (sh + 2 * pv)) & 3), vs, vz);
+        const float r0 = __uint_as_float(vf[i] << 16), r1 = __uint_as_float(vf[i] & 0xFFFF0000u);
+#pragma unroll
+        for (int j = 0; j < MAXG; ++j) {
+          if (j < gq) {
+            const float p1 = pb[w][0][t][j], p2 = pb[w][1][t][j];
+            o[0][j][0] = fmaf(p1, r0, o[0][j][0]);
+            o[0][j][1] = fmaf(p1, r1, o[0][j][1]);
+            o[1][j][0] = fmaf(p2, r0, o[1][j][0]);
+            o[1][j][1] = fmaf(p2, r1, o[1][j][1]);
+            o[2][j][0] = fmaf(p2, x0, o[2][j][0]);
+            o[2][j][1] = fmaf(p2, x1, o[2][j][1]);
+          }
         }
       }
     }
