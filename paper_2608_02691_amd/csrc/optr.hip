@@ -1247,17 +1247,38 @@ __global__ __launch_bounds__(256) void cal_to_f32_kernel(const double* __restric
   if (i < n) dst[i] = (float)src[i];
 }
 
-// W_{O,j}^T W_{O,j}: block (query head j, row a), thread = column b.
-__global__ __launch_bounds__(128) void cal_gram_kernel(const uint16_t* __restrict__ W, int dm, int Hq,
+// W_{O,j}^T W_{O,j} on the fp64 matrix cores: block = query head j, eight waves; wave w owns output rows
+// 16 w .. 16 w + 15 (all eight 16-column tiles). The head's d_model x 128 slice of W_O goes through LDS
+// 16 rows at a time (bf16 -> fp64, exact); K = those rows, 4 per step.
+constexpr int kGramRows = 16;
+__global__ __launch_bounds__(512) void cal_gram_kernel(const uint16_t* __restrict__ W, int dm, int Hq,
                                                        double* __restrict__ gram) {
-  const int j = blockIdx.x, a = blockIdx.y, b = threadIdx.x;
+  __shared__ double xs[kGramRows][kD + 2];
+  const int j = blockIdx.x, tid = threadIdx.x, w = tid >> 6, l = tid & 63, lo = l & 15, lk = l >> 4;
   const size_t ld = (size_t)Hq * kD;
-  double acc = 0.0;
-  for (int r = 0; r < dm; ++r) {
-    const uint16_t* wr = W + (size_t)r * ld + (size_t)j * kD;
-    acc = fma(bf16d(wr[a]), bf16d(wr[b]), acc);
+  f64x4 acc[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = f64x4{0.0, 0.0, 0.0, 0.0};
+  for (int r0 = 0; r0 < dm; r0 += kGramRows) {
+    for (int e = tid; e < kGramRows * kD; e += 512) {
+      const int rr = e / kD, c = e % kD;
+      xs[rr][c] = r0 + rr < dm ? bf16d(W[(size_t)(r0 + rr) * ld + (size_t)j * kD + c]) : 0.0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k4 = 0; k4 < kGramRows; k4 += 4) {
+      // A[m][k] = X[k][16 w + m], B[k][n] = X[k][16 t + n]: lane l holds A[lo][lk] and B[lk][lo]
+      const double av = xs[k4 + lk][16 * w + lo];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) acc[t] = mfma64(av, xs[k4 + lk][16 * t + lo], acc[t]);
+    }
+    __syncthreads();
   }
-  gram[((size_t)j * kD + a) * kD + b] = acc;
+  // element v of tile t: row 16 w + lk + 4 v, column 16 t + lo
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) gram[((size_t)j * kD + 16 * w + lk + 4 * v) * kD + 16 * t + lo] = acc[t][v];
 }
 
 // Per-channel mean of the keys: block = KV head, thread = channel (sequential fp64 sum).
@@ -1384,7 +1405,7 @@ void cal_bind_shared(CalCfg& c, uint8_t* base) {
 }
 
 hipError_t cal_gram(const CalCfg& c, const uint16_t* W_o, hipStream_t s) {
-  hipLaunchKernelGGL(cal_gram_kernel, dim3(c.Hq, kD), dim3(kD), 0, s, W_o, c.dm, c.Hq, c.gram);
+  hipLaunchKernelGGL(cal_gram_kernel, dim3(c.Hq), dim3(512), 0, s, W_o, c.dm, c.Hq, c.gram);
   return hipGetLastError();
 }
 
