@@ -206,7 +206,9 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, bool wide, uint8_t* ld
     const int sq = cidx / (kGpb * 64), gi = (cidx / 64) % kGpb, l = cidx & 63, g = g0 + gi;
     const int m = l & 15, q = l >> 4;
     const int jj = wide ? m >> 1 : m >> 2;
-    const bool on = wide ? (m & 1) == (g & 1) : (m & 3) == g;
+    // with one group per token every block sits in row (j, 0) (the scan then reads one dense dot)
+    const int gs = a.groups == 1 ? 0 : g;
+    const bool on = wide ? (m & 1) == (gs & 1) : (m & 3) == gs;
     const int row = 8 * sq + jj;
     uint32_t packed[4] = {0u, 0u, 0u, 0u};
     if (on && jj < gq) {
@@ -259,9 +261,9 @@ __device__ void qprep_block(const DecodeArgs& a, int blk, bool wide, uint8_t* ld
 }
 
 // ---------------------------------------------------------------------------------------------
-// Row layouts (groups of 32 channels; with one 128-channel group per token the four 32-channel
-// blocks read that group's scale and zero, and the zero term is z * sum_k q'_jk with no product).
-// The matrix cores contract over 32 channels, one quant group, while a group's scale
+// Row layouts (groups of 32 channels; with one 128-channel group per token every k block of the
+// query sits in row (j, 0), all four accumulate into tile 0, and the score is s D + z sum_k q'_jk with
+// no zero-term product). The matrix cores contract over 32 channels, one quant group, while a group's scale
 // multiplies only that group's partial dot product, so a score row serves one group: it is
 // nonzero only in that group's k block.
 //  * narrow (up to 4 query heads per KV head): row (j, g) = 4 j + g; the four k blocks accumulate
@@ -464,7 +466,7 @@ __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoa
   for (int P = 0; P < 2; ++P)
 #pragma unroll
     for (int t = 0; t < NT; ++t) d[P][t] = st.cinit[t];
-  if constexpr (WIDE) {
+  if constexpr (WIDE && NG != 1) {
     // blocks 0, 2 then 1, 3: four independent chains (page x tile) of two
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -473,22 +475,20 @@ __device__ __forceinline__ void qk_pair(const ScanState<WIDE>& st, const PairLoa
 #pragma unroll
         for (int t = 0; t < 2; ++t) d[P][t] = mfma16(st.A[2 * t + i], B[P][2 * t + i], d[P][t]);
   } else {
+    // every block into tile 0 (with one group per token the query rows are dense: see qprep_block)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int P = 0; P < 2; ++P) d[P][0] = mfma16(st.A[i], B[P][i], d[P][0]);
   }
   if constexpr (NG == 1) {
-    // one (s, z) per token: score = s sum_g D_g + z Q_j (no matrix-core zero term)
+    // one (s, z) per token: score = s D + z Q_j, D (all 128 channels) in row (j, 0) of tile 0
 #pragma unroll
     for (int P = 0; P < 2; ++P) {
       const half2_t m = as_h2(cur.km[P].x);
 #pragma unroll
       for (int u = 0; u < NJ; ++u) {
-        float Dg[4];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) Dg[g] = WIDE ? d[P][g >> 1][2 * u + (g & 1)] : d[P][0][g];
-        const float Ds = ((Dg[0] + Dg[1]) + Dg[2]) + Dg[3];
+        const float Ds = d[P][0][WIDE ? 2 * u : 0];
         a2[P][u] = fmaf((float)m.x, Ds, (float)m.y * st.Qz[u]);
       }
     }
@@ -858,13 +858,23 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
   ScanState<WIDE> st;
 #pragma unroll
   for (int i = 0; i < 4; ++i) st.A[i] = *reinterpret_cast<const half8_t*>(qop + (i * 64 + l) * 16);
-  if constexpr (WIDE) {
+  if constexpr (WIDE && NG == 1) {
+    // dense rows (j, 0): the accumulator start of row 2 j is the sum of its four group entries
+    const float4_t c01 = *reinterpret_cast<const float4_t*>(cst + 4 * hi);
+    const float4_t c23 = *reinterpret_cast<const float4_t*>(cst + 16 + 4 * hi);
+    st.cinit[0] = float4_t{(c01[0] + c01[1]) + (c23[0] + c23[1]), 0.0f, (c01[2] + c01[3]) + (c23[2] + c23[3]), 0.0f};
+    st.cinit[1] = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < 2; ++u) st.invsig[u] = cst[64 + 2 * hi + u] > 0.0f ? cst[64 + 2 * hi + u] : 1.0f;
+  } else if constexpr (WIDE) {
     st.cinit[0] = *reinterpret_cast<const float4_t*>(cst + 4 * hi);       // D01 rows 4hi..4hi+3
     st.cinit[1] = *reinterpret_cast<const float4_t*>(cst + 16 + 4 * hi);  // D23 rows 4hi..4hi+3
 #pragma unroll
     for (int u = 0; u < 2; ++u) st.invsig[u] = cst[64 + 2 * hi + u] > 0.0f ? cst[64 + 2 * hi + u] : 1.0f;
   } else {
     st.cinit[0] = *reinterpret_cast<const float4_t*>(cst + 4 * hi);
+    if constexpr (NG == 1)  // dense row (j, 0): the sum of its four group entries
+      st.cinit[0] = float4_t{((st.cinit[0][0] + st.cinit[0][1]) + st.cinit[0][2]) + st.cinit[0][3], 0.f, 0.f, 0.f};
     st.invsig[0] = cst[32 + hi] > 0.0f ? cst[32 + hi] : 1.0f;
   }
   {
