@@ -355,31 +355,36 @@ __device__ __forceinline__ void dma_pair(uint32_t a_lo, uint32_t a_hi, uint32_t 
 // An empty asm that uses every register read_pair filled: the compiler places its wait for those
 // LDS reads here, ahead of the scalar block-id loads that follow (a later wait would have to
 // wait for those loads too, since scalar loads return out of order).
-template <bool WIDE>
+// With one group per token only the first metadata word and the first scale pair are used (and
+// pinned); the other slots hold copies the compiler drops.
+template <bool WIDE, int NG>
 __device__ __forceinline__ void pin_pair(PairLoads<WIDE>& p) {
   typedef uint32_t u2v __attribute__((ext_vector_type(2)));
   typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 #pragma unroll
   for (int P = 0; P < 2; ++P) {
     u2v kc = __builtin_bit_cast(u2v, p.kc[P]), vc = __builtin_bit_cast(u2v, p.vc[P]);
-    u4v km = __builtin_bit_cast(u4v, p.km[P]);
     u2v vs0 = __builtin_bit_cast(u2v, p.vs[P][0]), vz = __builtin_bit_cast(u2v, p.vz[P]);
-    asm volatile("" : "+v"(kc), "+v"(vc), "+v"(km), "+v"(vs0), "+v"(vz));
+    if constexpr (NG == 1) {
+      asm volatile("" : "+v"(kc), "+v"(vc), "+v"(p.km[P].x), "+v"(vs0), "+v"(vz));
+    } else {
+      u4v km = __builtin_bit_cast(u4v, p.km[P]);
+      asm volatile("" : "+v"(kc), "+v"(vc), "+v"(km), "+v"(vs0), "+v"(vz));
+      p.km[P] = __builtin_bit_cast(uint4, km);
+    }
     p.kc[P] = __builtin_bit_cast(uint2, kc);
     p.vc[P] = __builtin_bit_cast(uint2, vc);
-    p.km[P] = __builtin_bit_cast(uint4, km);
     p.vs[P][0] = __builtin_bit_cast(uint2, vs0);
     p.vz[P] = __builtin_bit_cast(uint2, vz);
-    if constexpr (WIDE) {
+    if constexpr (WIDE && NG != 1) {
       u2v vs1 = __builtin_bit_cast(u2v, p.vs[P][1]);
       asm volatile("" : "+v"(vs1));
       p.vs[P][1] = __builtin_bit_cast(uint2, vs1);
     }
   }
 }
-// With one group per token (NG = 1) the token's single (s, z) is read into all four group slots:
-// the score sum_g s_g D_g + sum_g z_g Q_g then equals s D + z Q over the 128 channels, and the
-// value weights of every group column use the token's one scale and zero.
+// With one group per token (NG = 1) the token's single (s, z) is read into the group slots: the score
+// is s D + z Q over the 128 channels, and the one value-weight operand uses the token's scale and zero.
 template <bool WIDE, int NG>
 __device__ __forceinline__ void read_pair(const uint8_t* slot, uint32_t nv0, uint32_t nv1, int lo, int hi,
                                           const uint8_t* czb, PairLoads<WIDE>& p) {
@@ -972,7 +977,7 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
     else
       wait_vm_all();
     read_pair<WIDE, NG>(stage_w, nv[0][0], nv[0][1], lo, hi, czb, X);
-    pin_pair(X);
+    pin_pair<WIDE, NG>(X);
     if (kStages < npairs) {
       PageEnt e0, e1;
       entries(kStages, e0, e1);
@@ -998,7 +1003,7 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
       else
         wait_vm_all();
       read_pair<WIDE, NG>(stage_w + SL * 2 * kRecord, nv[SL][0], nv[SL][1], lo, hi, czb, nxt);
-      pin_pair(nxt);
+      pin_pair<WIDE, NG>(nxt);
       if (STEADY) {
         // The entries read one step ago are pinned (their wait placed) before the next loads issue:
         // scalar loads return out of order, so a wait placed after those would wait for them too.
