@@ -555,7 +555,7 @@ OePlan make_oe_plan(int B, int Hq, int H, int max_ctx, int d_model) {
   p.off_part = off;
   off = up(off + (size_t)B * p.n_chunks * Hq * kOePartStride * sizeof(float));
   p.off_dov = off;
-  off = up(off + (size_t)B * Hq * 2 * kHeadDim * sizeof(float));
+  off = up(off + 3 * (size_t)B * Hq * 2 * kHeadDim * sizeof(uint16_t));
   p.off_spart = off;
   off = up(off + (size_t)B * Hq * p.ntiles * 4 * sizeof(float));
   p.total = off;
@@ -619,7 +619,7 @@ int int2kv_output_error(const int2kv_cache* cache, const uint16_t* q, int batch,
   e.v_rows = v_rows;
   e.row_cap = row_cap;
   e.part = reinterpret_cast<float*>(ws + plan.off_part);
-  e.dov = reinterpret_cast<float*>(ws + plan.off_dov);
+  e.dov = reinterpret_cast<uint16_t*>(ws + plan.off_dov);
   e.spart = reinterpret_cast<float*>(ws + plan.off_spart);
   return hip_status(launch_output_error(e, W_o, d_model, stats, dy, stream, g_ev_before, g_ev_after), "output_error");
 }

@@ -136,7 +136,8 @@ struct OutErrArgs {
   const uint16_t *k_rows, *v_rows;  // full-precision keys and values, row b * row_cap + t, [H, 128]
   int row_cap;
   float* part;                  // [B, n_chunks, Hq, kOePartStride]
-  float* dov;                   // [B, Hq, 2, 128]: o2 - o1, o3 - o2 (model basis)
+  uint16_t* dov;                // [3][B, Hq, 2, 128]: o2 - o1, o3 - o2 (model basis) as three bf16 terms
+                                // whose sum is the fp32 value exactly
   float* spart;                 // [B, Hq, row tiles of kOeRowTile rows, 4]
 };
 // stats: [B, Hq, 4]; dy (may be null): [B, Hq, 2, d_model]; ev0 / ev1 track the scan kernel

@@ -356,21 +356,35 @@ __global__ __launch_bounds__(128) void outerr_merge_kernel(OutErrArgs e) {
     o3 = fmaf(os[4 * i + 2], r.z, o3);
     o3 = fmaf(os[4 * i + 3], r.w, o3);
   }
-  float* d = e.dov + ((size_t)b * a.Hq + j) * 2 * kHeadDim;
-  d[c] = o2 - o1;
-  d[kHeadDim + c] = o3 - o2;
+  // do as three bf16 terms (the projection's matrix-core operands): truncation leaves each remainder
+  // exact, and the third takes the last 8 significant bits, so t0 + t1 + t2 = do exactly
+  const size_t plane = (size_t)a.B * a.Hq * 2 * kHeadDim;
+  uint16_t* d = e.dov + ((size_t)b * a.Hq + j) * 2 * kHeadDim;
+  const float dv[2] = {o2 - o1, o3 - o2};
+#pragma unroll
+  for (int kv = 0; kv < 2; ++kv) {
+    const uint32_t b0 = __float_as_uint(dv[kv]) & 0xFFFF0000u;
+    const float r1 = dv[kv] - __uint_as_float(b0);
+    const uint32_t b1 = __float_as_uint(r1) & 0xFFFF0000u;
+    const float r2 = r1 - __uint_as_float(b1);
+    d[kv * kHeadDim + c] = (uint16_t)(b0 >> 16);
+    d[plane + kv * kHeadDim + c] = (uint16_t)(b1 >> 16);
+    d[2 * plane + kv * kHeadDim + c] = (uint16_t)(__float_as_uint(r2) >> 16);
+  }
 }
 
 typedef float oe_f4_t __attribute__((ext_vector_type(4)));
 
 // Block (query head j, tile of kOeRowTile rows of W_O), four waves: dy[b][j][{K, V}][row] =
 // do[b][j][{K, V}] . W_O[row][j * 128 ..] for every sequence, and the tile's partial statistics, on
-// the fp32 matrix cores (16 x 16 x 4 steps: lane l holds A[l % 16][l / 16] and B[l / 16][l % 16],
-// D[4 (l / 16) + v][l % 16] is element v of its accumulator). M: the 2B rows m = 2 b + {0: K, 1: V}
-// of do, 16 at a time; N: wave w's two 16-row tiles of the block's rows; K: the head's 128
-// channels, step s taking channels 32 (l / 16) + s, so that each lane reads 32 contiguous channels
-// of its do and W_O rows.
+// the bf16 matrix cores with do as three exact bf16 terms (fp32 products and accumulation, as an
+// fp32 product would give): 16 x 16 x 32 steps, lane l holds A[l % 16][8 (l / 16) ..] and
+// B[8 (l / 16) ..][l % 16], D[4 (l / 16) + v][l % 16] is element v of its accumulator. M: the 2B rows
+// m = 2 b + {0: K, 1: V} of do, 16 at a time; N: wave w's two 16-row tiles of the block's rows; K:
+// the head's 128 channels in four blocks of 32 (lane: channels 32 i + 8 (l / 16) .. + 7 of its do
+// and W_O rows).
 constexpr int kOeNT = kOeRowTile / 64;  // 16-row N tiles per wave
+typedef __bf16 oe_bf16x8_t __attribute__((ext_vector_type(8)));
 __global__ __launch_bounds__(256) void outerr_proj_kernel(OutErrArgs e, const uint16_t* __restrict__ W_o,
                                                           int d_model, float* __restrict__ dy,
                                                           float* __restrict__ spart, int ntiles) {
@@ -380,47 +394,42 @@ __global__ __launch_bounds__(256) void outerr_proj_kernel(OutErrArgs e, const ui
   const int w = tid >> 6, l = tid & 63, li = l & 15, lk = l >> 4;
   int n[kOeNT];
   bool have[kOeNT];
-  float wb[kOeNT][32];
+  oe_bf16x8_t wb[kOeNT][4];
 #pragma unroll
   for (int nt = 0; nt < kOeNT; ++nt) {
     n[nt] = tile * kOeRowTile + 16 * (kOeNT * w + nt) + li;  // this lane's W_O row of N tile nt
     have[nt] = n[nt] < d_model;
     const uint4* wp = reinterpret_cast<const uint4*>(W_o + (size_t)(have[nt] ? n[nt] : 0) * a.Hq * kHeadDim +
-                                                     (size_t)j * kHeadDim + 32 * lk);
+                                                     (size_t)j * kHeadDim + 8 * lk);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const uint4 x = have[nt] ? wp[u] : make_uint4(0, 0, 0, 0);
-      const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        wb[nt][8 * u + 2 * i] = __uint_as_float(xs[i] << 16);
-        wb[nt][8 * u + 2 * i + 1] = __uint_as_float(xs[i] & 0xFFFF0000u);
-      }
-    }
+    for (int i = 0; i < 4; ++i)
+      wb[nt][i] = __builtin_bit_cast(oe_bf16x8_t, have[nt] ? wp[4 * i] : make_uint4(0, 0, 0, 0));
   }
   const int M = 2 * a.B;
+  const size_t plane = (size_t)a.B * a.Hq * 2 * kHeadDim;
   for (int m0 = 0; m0 < M; m0 += 16) {
     const int m = m0 + li, mc = m < M ? m : 0;
-    float da[32];
+    oe_bf16x8_t da[3][4];
     {
-      const float4* dp = reinterpret_cast<const float4*>(
-          e.dov + (((size_t)(mc >> 1) * a.Hq + j) * 2 + (mc & 1)) * kHeadDim + 32 * lk);
+      const uint16_t* dp = e.dov + (((size_t)(mc >> 1) * a.Hq + j) * 2 + (mc & 1)) * kHeadDim + 8 * lk;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float4 x = m < M ? dp[u] : make_float4(0.f, 0.f, 0.f, 0.f);
-        da[4 * u] = x.x;
-        da[4 * u + 1] = x.y;
-        da[4 * u + 2] = x.z;
-        da[4 * u + 3] = x.w;
-      }
+      for (int t = 0; t < 3; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          da[t][i] = __builtin_bit_cast(
+              oe_bf16x8_t, m < M ? *reinterpret_cast<const uint4*>(dp + t * plane + 32 * i) : make_uint4(0, 0, 0, 0));
     }
     oe_f4_t acc[kOeNT];
 #pragma unroll
     for (int nt = 0; nt < kOeNT; ++nt) acc[nt] = oe_f4_t{0.f, 0.f, 0.f, 0.f};
+    // smallest term first
 #pragma unroll
-    for (int s = 0; s < 32; ++s)
+    for (int t = 2; t >= 0; --t)
 #pragma unroll
-      for (int nt = 0; nt < kOeNT; ++nt) acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(da[s], wb[nt][s], acc[nt], 0, 0, 0);
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int nt = 0; nt < kOeNT; ++nt)
+          acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(da[t][i], wb[nt][i], acc[nt], 0, 0, 0);
     // acc[nt][v]: do row m0 + 4 lk + v, i.e. sequence m0 / 2 + 2 lk + v / 2, K (v even) or V (v odd)
 #pragma unroll
     for (int hb = 0; hb < 2; ++hb) {
