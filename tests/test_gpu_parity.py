@@ -351,3 +351,30 @@ def test_decode_large_value_and_key_ranges(G, variant):
                           dev(w.R_k), dev(w.R_v))
     worst = assert_rows_close(out.cpu().numpy(), ref, what="decode, large ranges")
     print(f"largest V scale {max(big_scales):.0f}; worst row error {worst:.2e}", flush=True)
+
+
+@pytest.mark.parametrize("G", [32, 128])
+@pytest.mark.parametrize("variant", [1, 2])
+def test_decode_queries_on_one_rotated_channel_and_extreme_norms(G, variant):
+    """Queries whose rotated form q R_K lies on a single channel (there the largest |q'_c| equals
+    |q|_2, the bound from which the matrix-core scan takes its fp16 operand scale), and queries of
+    tiny and of four times the usual norm, against the oracle."""
+    print(f"\n[decode extreme queries] G={G} variant={variant}", flush=True)
+    K.int2kv_set_decode_tuning(0, variant)
+    w = W.make_workload(4, batch=3, ctx_lens=np.array([300, 47, 129]), num_q_heads=10, num_kv_heads=2)
+    gq = w.num_q_heads // w.num_kv_heads
+    qf = W.bf16_bits_to_f32(w.q).astype(np.float64)
+    for j in range(w.num_q_heads):
+        h = j // gq
+        qf[0, j] = 8.0 * w.R_k[h][:, (37 * j + 5) % 128]  # q R_K = 8 e_c (up to the rotation's rounding)
+    qf[1] *= 1e-3  # near-uniform softmax
+    qf[2] *= 4.0   # logits of several units (the fp16 query operand's score error is about 2^-12 of them)
+    q = W.f32_to_bf16_bits(qf.astype(np.float32))
+    pool = oracle_pool(w, group=G)
+    ref = O.decode(pool, q, w.block_table, w.ctx_lens, w.R_k, w.R_v)
+    out = K.int2kv_decode(gpu_cache(pool), dev(q), dev(w.block_table), dev(w.ctx_lens), int(w.ctx_lens.max()),
+                          dev(w.R_k), dev(w.R_v))
+    got = out.cpu().numpy()
+    assert np.isfinite(got).all()
+    worst = assert_rows_close(got, ref, what="decode, extreme queries")
+    print(f"worst row error {worst:.2e}", flush=True)
