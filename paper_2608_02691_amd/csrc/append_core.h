@@ -87,13 +87,13 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
     for (int p = 0; p < 8; ++p)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        mn = __builtin_fminf(mn, acc[p][j]);
-        mx = __builtin_fmaxf(mx, acc[p][j]);
+        mn = __builtin_elementwise_minimum(mn, acc[p][j]);
+        mx = __builtin_elementwise_maximum(mx, acc[p][j]);
       }
-    mn = __builtin_fminf(mn, __shfl_xor(mn, 16));
-    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 16));
-    mn = __builtin_fminf(mn, __shfl_xor(mn, 32));
-    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 32));
+    mn = __builtin_elementwise_minimum(mn, __shfl_xor(mn, 16));
+    mx = __builtin_elementwise_maximum(mx, __shfl_xor(mx, 16));
+    mn = __builtin_elementwise_minimum(mn, __shfl_xor(mn, 32));
+    mx = __builtin_elementwise_maximum(mx, __shfl_xor(mx, 32));
     uint32_t s_bits, z_bits;
     float zf, inv;
     int2_group_params_fast(mn, mx, clip, recip_tab, s_bits, z_bits, zf, inv);
@@ -126,13 +126,13 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
   float pmn[4], pmx[4];
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    float a = __builtin_fminf(acc[2 * g][0], acc[2 * g][1]), b = __builtin_fmaxf(acc[2 * g][0], acc[2 * g][1]);
-    a = __builtin_fminf(a, __builtin_fminf(acc[2 * g][2], acc[2 * g][3]));
-    b = __builtin_fmaxf(b, __builtin_fmaxf(acc[2 * g][2], acc[2 * g][3]));
-    a = __builtin_fminf(a, __builtin_fminf(acc[2 * g + 1][0], acc[2 * g + 1][1]));
-    b = __builtin_fmaxf(b, __builtin_fmaxf(acc[2 * g + 1][0], acc[2 * g + 1][1]));
-    pmn[g] = __builtin_fminf(a, __builtin_fminf(acc[2 * g + 1][2], acc[2 * g + 1][3]));
-    pmx[g] = __builtin_fmaxf(b, __builtin_fmaxf(acc[2 * g + 1][2], acc[2 * g + 1][3]));
+    float a = __builtin_elementwise_minimum(acc[2 * g][0], acc[2 * g][1]), b = __builtin_elementwise_maximum(acc[2 * g][0], acc[2 * g][1]);
+    a = __builtin_elementwise_minimum(a, __builtin_elementwise_minimum(acc[2 * g][2], acc[2 * g][3]));
+    b = __builtin_elementwise_maximum(b, __builtin_elementwise_maximum(acc[2 * g][2], acc[2 * g][3]));
+    a = __builtin_elementwise_minimum(a, __builtin_elementwise_minimum(acc[2 * g + 1][0], acc[2 * g + 1][1]));
+    b = __builtin_elementwise_maximum(b, __builtin_elementwise_maximum(acc[2 * g + 1][0], acc[2 * g + 1][1]));
+    pmn[g] = __builtin_elementwise_minimum(a, __builtin_elementwise_minimum(acc[2 * g + 1][2], acc[2 * g + 1][3]));
+    pmx[g] = __builtin_elementwise_maximum(b, __builtin_elementwise_maximum(acc[2 * g + 1][2], acc[2 * g + 1][3]));
   }
   float mn, mx;
   {
@@ -141,13 +141,13 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
     const float sx0 = h1 ? pmx[0] : pmx[2], sx1 = h1 ? pmx[1] : pmx[3];
     float kn0 = h1 ? pmn[2] : pmn[0], kn1 = h1 ? pmn[3] : pmn[1];
     float kx0 = h1 ? pmx[2] : pmx[0], kx1 = h1 ? pmx[3] : pmx[1];
-    kn0 = __builtin_fminf(kn0, __shfl_xor(sn0, 32));
-    kn1 = __builtin_fminf(kn1, __shfl_xor(sn1, 32));
-    kx0 = __builtin_fmaxf(kx0, __shfl_xor(sx0, 32));
-    kx1 = __builtin_fmaxf(kx1, __shfl_xor(sx1, 32));
+    kn0 = __builtin_elementwise_minimum(kn0, __shfl_xor(sn0, 32));
+    kn1 = __builtin_elementwise_minimum(kn1, __shfl_xor(sn1, 32));
+    kx0 = __builtin_elementwise_maximum(kx0, __shfl_xor(sx0, 32));
+    kx1 = __builtin_elementwise_maximum(kx1, __shfl_xor(sx1, 32));
     // keep group 2 h1 + h0, send the other to the lane 16 away
-    mn = __builtin_fminf(h0 ? kn1 : kn0, __shfl_xor(h0 ? kn0 : kn1, 16));
-    mx = __builtin_fmaxf(h0 ? kx1 : kx0, __shfl_xor(h0 ? kx0 : kx1, 16));
+    mn = __builtin_elementwise_minimum(h0 ? kn1 : kn0, __shfl_xor(h0 ? kn0 : kn1, 16));
+    mx = __builtin_elementwise_maximum(h0 ? kx1 : kx0, __shfl_xor(h0 ? kx0 : kx1, 16));
   }
   uint32_t s_bits, z_bits;
   float zf, inv;
