@@ -67,6 +67,23 @@ __device__ __forceinline__ void int2_group_params_fast(float mn, float mx, float
   }
 }
 
+// Cross-lane exchanges of the group reductions on the vector ALU (no LDS round trip).
+// lane_swap32(a, b): lanes 32-63 of a trade places with lanes 0-31 of b, so afterwards lane l < 32
+// holds (a[l], a[l + 32]) and lane l >= 32 holds (b[l - 32], b[l]). lane_swap16: the same between
+// the odd 16-lane rows of a and the even rows of b, so a lane of an even row holds (a[l], a[l + 16])
+// and a lane of an odd row (b[l - 16], b[l]).
+struct LanePair {
+  float a, b;
+};
+__device__ __forceinline__ LanePair lane_swap32(float a, float b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  return LanePair{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+__device__ __forceinline__ LanePair lane_swap16(float a, float b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  return LanePair{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+
 // Packed output of one lane for one 16-token tile: halves 4 hi .. 4 hi + 3 of its token (two per
 // word) and the scale / zero of group hi.
 struct ApOut {
@@ -90,10 +107,14 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
         mn = __builtin_elementwise_minimum(mn, acc[p][j]);
         mx = __builtin_elementwise_maximum(mx, acc[p][j]);
       }
-    mn = __builtin_elementwise_minimum(mn, __shfl_xor(mn, 16));
-    mx = __builtin_elementwise_maximum(mx, __shfl_xor(mx, 16));
-    mn = __builtin_elementwise_minimum(mn, __shfl_xor(mn, 32));
-    mx = __builtin_elementwise_maximum(mx, __shfl_xor(mx, 32));
+    {
+      const auto n16 = lane_swap16(mn, mn), x16 = lane_swap16(mx, mx);
+      mn = __builtin_elementwise_minimum(n16.a, n16.b);
+      mx = __builtin_elementwise_maximum(x16.a, x16.b);
+      const auto n32 = lane_swap32(mn, mn), x32 = lane_swap32(mx, mx);
+      mn = __builtin_elementwise_minimum(n32.a, n32.b);
+      mx = __builtin_elementwise_maximum(x32.a, x32.b);
+    }
     uint32_t s_bits, z_bits;
     float zf, inv;
     int2_group_params_fast(mn, mx, clip, recip_tab, s_bits, z_bits, zf, inv);
@@ -122,7 +143,6 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
   }
   // group g = tiles 2g, 2g + 1: lane-local min/max of its eight values, then a reduce-scatter
   // over the four lanes of the token (xor 32, then xor 16) leaves group hi's extremes in lane hi
-  const bool h1 = (hi & 2) != 0, h0 = (hi & 1) != 0;
   float pmn[4], pmx[4];
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
@@ -136,18 +156,16 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
   }
   float mn, mx;
   {
-    // keep groups 2 h1, 2 h1 + 1, send the other two to the lane 32 away
-    const float sn0 = h1 ? pmn[0] : pmn[2], sn1 = h1 ? pmn[1] : pmn[3];
-    const float sx0 = h1 ? pmx[0] : pmx[2], sx1 = h1 ? pmx[1] : pmx[3];
-    float kn0 = h1 ? pmn[2] : pmn[0], kn1 = h1 ? pmn[3] : pmn[1];
-    float kx0 = h1 ? pmx[2] : pmx[0], kx1 = h1 ? pmx[3] : pmx[1];
-    kn0 = __builtin_elementwise_minimum(kn0, __shfl_xor(sn0, 32));
-    kn1 = __builtin_elementwise_minimum(kn1, __shfl_xor(sn1, 32));
-    kx0 = __builtin_elementwise_maximum(kx0, __shfl_xor(sx0, 32));
-    kx1 = __builtin_elementwise_maximum(kx1, __shfl_xor(sx1, 32));
-    // keep group 2 h1 + h0, send the other to the lane 16 away
-    mn = __builtin_elementwise_minimum(h0 ? kn1 : kn0, __shfl_xor(h0 ? kn0 : kn1, 16));
-    mx = __builtin_elementwise_maximum(h0 ? kx1 : kx0, __shfl_xor(h0 ? kx0 : kx1, 16));
+    // lanes 0-31 keep groups 0 and 1, lanes 32-63 groups 2 and 3: one swap of (group g, group
+    // g + 2) leaves both lanes' halves of the kept group in the swap's two results
+    const auto n0 = lane_swap32(pmn[0], pmn[2]), n1 = lane_swap32(pmn[1], pmn[3]);
+    const auto x0 = lane_swap32(pmx[0], pmx[2]), x1 = lane_swap32(pmx[1], pmx[3]);
+    const float kn0 = __builtin_elementwise_minimum(n0.a, n0.b), kn1 = __builtin_elementwise_minimum(n1.a, n1.b);
+    const float kx0 = __builtin_elementwise_maximum(x0.a, x0.b), kx1 = __builtin_elementwise_maximum(x1.a, x1.b);
+    // even rows (hi 0, 2) keep the first of the two, odd rows the second: the same with rows of 16
+    const auto n = lane_swap16(kn0, kn1), x = lane_swap16(kx0, kx1);
+    mn = __builtin_elementwise_minimum(n.a, n.b);
+    mx = __builtin_elementwise_maximum(x.a, x.b);
   }
   uint32_t s_bits, z_bits;
   float zf, inv;
