@@ -170,15 +170,22 @@ __device__ __forceinline__ ApOut quantize_tile(const ap_f4_t (&acc)[8], float cl
   uint32_t s_bits, z_bits;
   float zf, inv;
   int2_group_params_fast(mn, mx, clip, recip_tab, s_bits, z_bits, zf, inv);
-  // every lane of the token gathers the four groups' zero and reciprocal scale
+  // every lane of the token gathers the four groups' zero and reciprocal scale: a swap of rows of
+  // 16 gives each lane (group 2 h1, group 2 h1 + 1), swaps of halves of 32 then give (group 0,
+  // group 2) and (group 1, group 3) in every lane
   float zg[4], ig[4], sg[4];
   const float sfo = __half2float(__ushort_as_half((unsigned short)s_bits));
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    zg[g] = __shfl(zf, lo + 16 * g);
-    ig[g] = __shfl(inv, lo + 16 * g);
-    if constexpr (ERR) sg[g] = __shfl(sfo, lo + 16 * g);
-  }
+  auto gather4 = [](float v, float(&out)[4]) {
+    const LanePair r = lane_swap16(v, v);
+    const LanePair e = lane_swap32(r.a, r.a), o = lane_swap32(r.b, r.b);
+    out[0] = e.a;
+    out[1] = o.a;
+    out[2] = e.b;
+    out[3] = o.b;
+  };
+  gather4(zf, zg);
+  gather4(inv, ig);
+  if constexpr (ERR) gather4(sfo, sg);
   // codes: half 4 hi + j of the token collects tiles p = 0..7 of register j at bits 2p, summed as
   // exact small integers in fp32
   float hf[4] = {0.f, 0.f, 0.f, 0.f};
