@@ -354,8 +354,8 @@ def main():
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (see DESIGN.md for "
-              "how the decode would shard); run it with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path (the decode would shard "
+              "by KV head and sequence, one process per GPU); run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -60,7 +60,7 @@ extern "C" {
 typedef enum {
   INT2KV_OK = 0,
   INT2KV_EINVAL = -1,       /* bad pointer, shape or alignment                         */
-  INT2KV_EUNSUPPORTED = -2, /* a shape this build does not implement                   */
+  INT2KV_EUNSUPPORTED = -2, /* a shape the library does not implement                 */
   INT2KV_EWORKSPACE = -3,   /* workspace missing or smaller than required              */
   INT2KV_EHIP = -4          /* a HIP launch reported an error                          */
 } int2kv_status;
