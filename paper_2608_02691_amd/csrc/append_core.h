@@ -473,6 +473,9 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
         if (f + kApDepth < 96) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
     };
+    // a wave in its matrix-core phase is issued first: the other wave of the SIMD fills the gaps
+    // between its products with quantizer instructions
+    __builtin_amdgcn_s_setprio(1);
     if (had) {
       mfma_pass(std::integral_constant<int, 64>{});
 #pragma unroll
@@ -484,6 +487,7 @@ __device__ __forceinline__ void append_block(const CacheView& cv, const uint16_t
     } else {
       mfma_pass(std::integral_constant<int, 0>{});
     }
+    __builtin_amdgcn_s_setprio(0);
     ApOut out[kApTiles];
 #pragma unroll
     for (int u = 0; u < kApTiles; ++u) out[u] = quantize_tile<NG, ERR>(acc[u], clip, recip_tab, lo, hi);
