@@ -998,6 +998,9 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
     const int kk = k + J;
     const bool more = STEADY || kk + 1 < npairs;
     if (more) {
+      // the pair's LDS reads and the next DMA go first on the SIMD (the other wave's landing and
+      // softmax fill in behind them)
+      __builtin_amdgcn_s_setprio(1);
       if (STEADY || kk + kStages < npairs)
         asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kDmaPerPair * (kStages - 1)) : "memory");
       else
@@ -1019,6 +1022,7 @@ __device__ __forceinline__ bool scan_segment(const DecodeArgs& a, int b, int h, 
         entries(kk + 1 + kStages, e0, e1);
         stage(std::integral_constant<int, SL>{}, e0, e1);
       }
+      __builtin_amdgcn_s_setprio(0);
     }
     float a2[2][NJ];
     if (more) qk_pair<WIDE, NG>(st, nxt, lo, a2);
