@@ -665,13 +665,17 @@ constexpr int kWavesPerWG = 8;   // one wave per KV head of a head group
 typedef __attribute__((address_space(4))) const int32_t* cint_ptr;  // read through the scalar cache
 
 // Work split of the scan. Every sequence a work-group starts costs a prologue and a pipeline
-// refill (measured: about 4 us per extra segment, the time of ~6 pages), so the pages are split
+// refill (measured: about 4 us per extra segment, the time of ~6 pages; 8 units measured best in a
+// sweep of 3 to 10 on the ragged 64-sequence batch), so the pages are split
 // evenly along a cost axis on which each non-empty sequence b occupies [c0(b), c1(b)): kSegCost
 // units of lead-in, then one unit per page (c1 - c0 = kSegCost + pages; empty sequences take no
 // room). Group g of G starts at cost x(g) = floor(g W / G), W = P + kSegCost * (non-empty
 // sequences); a start inside a lead-in maps to the sequence's first page. Ranges that take on
 // extra sequence starts thus get fewer pages.
-constexpr int kSegCost = 6;
+#ifndef INT2KV_SCAN_SEG_COST
+#define INT2KV_SCAN_SEG_COST 8
+#endif
+constexpr int kSegCost = INT2KV_SCAN_SEG_COST;
 
 // Pages of every sequence and their exclusive prefix sums (prefix[B] = total pages), and for each
 // scan work-group g the sequence b holding the first page of its range with that sequence's page
